@@ -1,0 +1,18 @@
+"""CPU fp64 oracle for Higher-order Linear Attention (HLA).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the CPU
+baseline leg of the benchmark may import, call, link or run anything in this
+package.  The GPU product path never routes through it and shares no code with
+it: the two meet only on seeded inputs produced by a generator module that
+holds none of the method's arithmetic.
+
+Modules
+  hla2      second-order HLA (Sec. 3 and Sec. 4 of the paper): the plain
+            definition, the serial online recurrence, the chunked associative
+            scan and the masked semidirect product.
+  hla3      third-order HLA (Sec. 7): the streaming kernel and the
+            chunk-parallel concatenation operator.
+  hla2_ref.c  the serial second-order recurrence in plain C (fp64), used to
+            time the oracle on host cores and to check large cases quickly.
+  native    ctypes loader for the compiled C oracle.
+"""
