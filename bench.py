@@ -1,0 +1,206 @@
+#!/usr/bin/env python3
+"""Throughput of the masked second-order HLA hot path on one MI355X.
+
+One step = one hla2_forward over the whole batch of the workload (per-chunk
+summaries, the semidirect-product scan and the readout), inputs resident in
+HBM.  Prints ONE JSON line with tokens/s, a roofline entry for the kernel that
+takes the most time, and the CPU oracle timed on the host cores.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--algo auto|chunked|fused]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
+FP32_VALU_PEAK_TFLOPS = 157.3   # fp32 vector
+
+DEFAULT_WORKLOAD = "hla2-masked-bf16-B4H16-n4096-d64-C64"
+
+
+def kernel_costs(w, algo):
+    """Algorithmic cost of one launch of each kernel of the forward path:
+    {name: (bound, bytes, flops)}.  bytes = HBM bytes the kernel must move
+    (inputs read once, outputs written once); flops = useful arithmetic
+    (a dense C x C product counts C^2 per output element, triangles are not
+    halved)."""
+    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
+    BH = B * H
+    M = -(-n // C)
+    es = 2 if w["dist"] == "unit" else 4
+    F = d * d + 2 * d * dv + 2 * d
+    qkv = BH * n * (2 * d + dv) * es
+    outb = BH * n * dv * 4
+    states = BH * M * F * 4
+    if algo == "fused":
+        from paper_2510_27258_amd.fused_info import fused_costs
+        return fused_costs(w)
+    tok = BH * n
+    return {
+        "chunk_summary": ("alu", qkv + states, tok * 2 * (C * d / 2 + C * dv / 2 + d * d + 2 * d * dv)),
+        "scan": ("hbm", 2 * states, BH * M * 2 * (d * d * dv + d * d)),
+        "readout": ("alu", qkv + states + outb, tok * 2 * (d * d + 1.5 * C * d + 2 * d * dv + C * dv / 2)),
+    }
+
+
+def peak_for(bound):
+    if bound == "hbm":
+        return HBM_PEAK_GBS, "GB/s"
+    if bound == "mfma":
+        return BF16_MFMA_PEAK_TFLOPS, "TFLOP/s"
+    return FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
+
+
+def traffic_for(kernel, workload):
+    """HBM traffic per launch from the committed counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except Exception:
+        return None
+    e = rec.get(workload, {}).get(kernel)
+    if not e:
+        return None
+    if e.get("source_sha") != source_sha():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def source_sha():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2510_27258_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".cpp", ".h")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(w, q, k, v, budget_s=20.0):
+    """The C oracle (serial fp64 recurrence, heads over OpenMP threads) on the
+    host cores, on as many whole heads of the workload as fit the budget."""
+    import numpy as np
+    from oracle import native
+    B, H, n = w["B"], w["H"], w["n"]
+    threads = os.cpu_count() or 1
+    # probe one head to size the sample
+    t0 = time.perf_counter()
+    native.hla2_serial_c(q[0, :1], k[0, :1], v[0, :1], masked=bool(w["masked"]), threads=1, return_state=False)
+    per_head = max(time.perf_counter() - t0, 1e-6)
+    heads = int(min(B * H, max(1, budget_s * threads / per_head)))
+    heads = max(min(heads, B * H), min(threads, B * H))
+    qs = q.reshape(B * H, n, -1)[:heads]
+    ks = k.reshape(B * H, n, -1)[:heads]
+    vs = v.reshape(B * H, n, -1)[:heads]
+    t0 = time.perf_counter()
+    _, _, _, used = native.hla2_serial_c(qs, ks, vs, masked=bool(w["masked"]), threads=threads,
+                                         return_state=False)
+    dt = time.perf_counter() - t0
+    return {"value": heads * n / dt, "unit": "tokens/s", "cores": int(used), "kind": "oracle",
+            "sample": f"{heads} of {B * H} heads x {n} tokens, C fp64 serial recurrence, {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--algo", default="auto", choices=["auto", "chunked", "fused"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (heads or sequence segments would "
+              "shard across GPUs; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
+    from paper_2510_27258_amd import inputs as I
+
+    w = dict(I.WORKLOADS[args.workload])
+    if w["kind"] != "forward":
+        raise SystemExit("bench.py times the forward workloads")
+    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
+    q, k, v, code = I.draw_qkv(B, H, n, d, dv, w["dist"], w["seed"])
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    algo = {"auto": capi.HLA_ALGO_AUTO, "chunked": capi.HLA_ALGO_CHUNKED, "fused": capi.HLA_ALGO_FUSED}[args.algo]
+    wsb = hla.workspace_bytes(B, H, n, d, dv, C, code, algo)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    out = torch.empty(B, H, n, dv, dtype=torch.float32, device=dev)
+
+    def step():
+        hla.forward(qd, kd, vd, C, masked=bool(w["masked"]), normalized=bool(w["normalized"]), eps=w["eps"],
+                    algo=algo, out=out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # per-kernel durations: a second pass with the library's event bracketing
+    capi.hla_profile_begin(8 * args.steps + 8)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    prof = capi.hla_profile_summary()
+    capi.hla_profile_end()
+    used_algo = "fused" if ("walk" in " ".join(prof)) else "chunked"
+    costs = kernel_costs(w, used_algo)
+    dom = max(prof, key=lambda kname: prof[kname][1])
+    cnt, tot_ms = prof[dom]
+    avg_s = tot_ms / cnt / 1e3
+    bound, nbytes, nflops = costs[dom]
+    peak, unit = peak_for(bound)
+    achieved = (nbytes / avg_s / 1e9) if bound == "hbm" else (nflops / avg_s / 1e12)
+    tr = traffic_for(dom, args.workload)
+
+    tokens = B * H * n
+    rec = {
+        "metric": "masked HLA-2 forward tokens/s (B*H*n) + % bf16 MFMA peak; decode step GB/s",
+        "value": tokens / (ms / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if used_algo == "fused" else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "H": H, "n": n, "d": d, "dv": dv, "chunk": C,
+                   "masked": w["masked"], "normalized": w["normalized"], "input_dtype": "bf16" if code else "fp32",
+                   "algo": used_algo, "global_batch": B * H, "seq_len": n, "parallelism": "none"},
+        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+                     "traffic": tr, "kernel": dom, "avg_launch_ms": avg_s * 1e3,
+                     "algorithmic_bytes": nbytes, "algorithmic_flops": nflops},
+        "kernels_ms": {kname: v_[1] / v_[0] for kname, v_ in prof.items()},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,156 @@
+/*
+ * hla.h — C ABI of the MI355X (gfx950) Higher-order Linear Attention library.
+ *
+ * The library computes the strictly causal (masked) second-order HLA of
+ * "Higher-order Linear Attention" (arXiv 2510.27258):
+ *
+ *     o_t = q_t^T (S_t C_t - G_t)                               (Thm. 1)
+ *         = sum_{j<=t} sum_{i<=j} (q_t.k_i)(q_j.k_i) v_j        (Sec. 3.1)
+ *
+ * with S_t = sum k k^T, C_t = sum q v^T, m_t = sum q and the masking summaries
+ * G_t = sum_i k_i k_i^T C_{i-1}, h_t = sum_i k_i k_i^T m_{i-1} (Sec. 3 and
+ * 3.1), its ratio-normalised form num/(den + eps) with den_t = q_t^T(S_t m_t -
+ * h_t) (Thm. 1), and the unmasked operator q_t^T S_t C_t (Eq. hla-unnorm,
+ * Eq. hla-row).  Sequences are processed by the chunk-parallel associative
+ * scan of Sec. 4 (Eq. semidirect, Thm. 2, Rem. scan-modes); the decode step
+ * applies the online updates of Sec. 3.1.
+ *
+ * Conventions for every call
+ *   - Pointers to tensors are DEVICE pointers.  The caller owns all memory,
+ *     including workspaces sized by the *_workspace_bytes queries.  The library
+ *     never allocates device memory, never synchronises, and enqueues work
+ *     only on `stream` (a hipStream_t; NULL = the default stream).  Results
+ *     are available once that stream reaches the enqueued work.
+ *   - Tensors are row-major and contiguous:
+ *       q, k [B, H, n, d]   v [B, H, n, dv]   out [B, H, n, dv]
+ *     q/k/v are `dtype` (HLA_FP32 or HLA_BF16: raw bfloat16 bit patterns);
+ *     outputs and states are always fp32.  Base pointers must be 16-byte
+ *     aligned.  Inputs are read-only; inputs and outputs must not alias.
+ *   - A head's second-order state is one fp32 record of
+ *     F = d*d + 2*d*dv + 2*d floats (hla2_state_floats), in the order
+ *       S [d][d] | C [d][dv] | m [d] | G [d][dv] | h [d]
+ *     i.e. (S^K, C^QV, m^Q, G, h) of Sec. 3.1.  A state array [B, H, F]
+ *     stores the records of all heads back to back.  The all-zero record is
+ *     the identity segment (Thm. 2).
+ *   - Supported sizes: d, dv in {16, 32, 64, 128}; chunk in {16, 32, 64,
+ *     128}; any n >= 1 (a short last chunk is exact); B*H <= 65535.
+ *     masked, normalized in {0, 1}; eps finite and >= 0 (added to the
+ *     denominator as is, den + eps).  Decay is 1 and the ridge 0.
+ *   - Every call returns an hla_status.  On failure nothing is enqueued and
+ *     hla_last_error() describes the reason (a thread-local string).
+ *     Results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef HLA_H
+#define HLA_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HLA_OK = 0,
+  HLA_ERR_INVALID = 1,      /* null pointer, bad size, flag or alignment */
+  HLA_ERR_UNSUPPORTED = 2,  /* valid but not implemented (e.g. d = 96)  */
+  HLA_ERR_WORKSPACE = 3,    /* workspace missing or too small           */
+  HLA_ERR_HIP = 4           /* a HIP launch or runtime call failed      */
+} hla_status;
+
+typedef enum { HLA_FP32 = 0, HLA_BF16 = 1 } hla_dtype;
+
+/* Forward algorithms selectable through hla2_forward_ex. */
+typedef enum {
+  HLA_ALGO_AUTO = 0,     /* library choice (fused when supported)             */
+  HLA_ALGO_CHUNKED = 1,  /* per-chunk summaries, (+)-scan, per-chunk readout  */
+  HLA_ALGO_FUSED = 2     /* segment walk with the carry state kept on chip    */
+} hla_algo;
+
+/* Reason for the last failed call on this thread ("" if none). */
+const char *hla_last_error(void);
+
+/* Floats in one second-order state record: d*d + 2*d*dv + 2*d. */
+size_t hla2_state_floats(int d, int dv);
+
+/* ---------------------------------------------------------------------------
+ * hla2_forward — masked (or unmasked) second-order HLA over whole sequences.
+ * Thm. 1 (output), Sec. 4 (chunk-parallel scan).  out[b,h,t,:] = o_t of head
+ * (b,h); with normalized = 1, num_t / (den_t + eps).  `chunk` is the scan's
+ * chunk size; results do not depend on it beyond rounding (Thm. 2).
+ * workspace: at least hla2_workspace_bytes(...) bytes of device memory (its
+ * contents on entry are ignored).  Returns HLA_ERR_WORKSPACE if smaller.
+ * ------------------------------------------------------------------------- */
+size_t hla2_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
+int hla2_forward(const void *q, const void *k, const void *v, float *out,
+                 int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
+                 float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
+
+/* As hla2_forward with an explicit algorithm (hla_algo).  HLA_ALGO_FUSED
+ * returns HLA_ERR_UNSUPPORTED for shapes it does not cover. */
+size_t hla2_workspace_bytes_ex(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo);
+int hla2_forward_ex(const void *q, const void *k, const void *v, float *out,
+                    int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
+                    float eps, int dtype, void *workspace, size_t workspace_bytes, int algo,
+                    void *stream);
+
+/* ---------------------------------------------------------------------------
+ * hla2_chunk_summaries — the summary of every chunk of `chunk` tokens with a
+ * zero carry-in: the (+)-product of its token segments (Sec. 4.2, Rem.
+ * scan-modes: chunk summary).  states: [B, H, M, F], M = ceil(n / chunk);
+ * chunk c covers tokens [c*chunk, min(n, (c+1)*chunk)).
+ * ------------------------------------------------------------------------- */
+int hla2_chunk_summaries(const void *q, const void *k, const void *v, float *states,
+                         int B, int H, int n, int d, int dv, int chunk, int dtype, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * hla2_scan — exclusive scan under the masked semidirect product, Eq.
+ * (semidirect): prefix[b,h,c] = init (+) states[b,h,0] (+) ... (+)
+ * states[b,h,c-1] (Rem. scan-modes).  states, prefix: [B, H, M, F];
+ * init: [B, H, F] or NULL (identity); total: [B, H, F] receives the inclusive
+ * product of all M segments, or NULL.  prefix and total must not alias
+ * states or init.
+ * ------------------------------------------------------------------------- */
+int hla2_scan(const float *states, const float *init, float *prefix, float *total,
+              int B, int H, int M, int d, int dv, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * hla2_prefill — continue every head's state over n new tokens:
+ *   state <- state (+) summary(tokens)          (Thm. 2)
+ * and, if out != NULL, write the outputs of those tokens ([B, H, n, dv]) as
+ * the serial recurrence started from the given state would (Sec. 3.1,
+ * Thm. 1).  state: [B, H, F], updated in place.  workspace: at least
+ * hla2_prefill_workspace_bytes(...) bytes.
+ * ------------------------------------------------------------------------- */
+size_t hla2_prefill_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
+int hla2_prefill(float *state, const void *q, const void *k, const void *v, float *out,
+                 int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
+                 float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * hla2_step — one decode step per head: the online updates of Sec. 3.1 and
+ * the readout of Thm. 1 (Sec. 5 order).  q_t, k_t: [B, H, d]; v_t: [B, H, dv];
+ * out_t: [B, H, dv] fp32; state: [B, H, F], updated in place.
+ * ------------------------------------------------------------------------- */
+int hla2_step(float *state, const void *q_t, const void *k_t, const void *v_t, float *out_t,
+              int B, int H, int d, int dv, int masked, int normalized, float eps, int dtype,
+              void *stream);
+
+
+/* ---------------------------------------------------------------------------
+ * Benchmark timing.  hla_profile_begin(max_records) creates 2*max_records HIP
+ * events (host objects, no device memory) and starts bracketing every kernel
+ * the library launches with events recorded on that kernel's stream;
+ * hla_profile_end() stops.  After synchronising the stream,
+ * hla_profile_summary(buf, len) writes one line per kernel name,
+ * "name launches total_ms", and forgets the records.  Records beyond
+ * max_records are not timed.  Not thread-safe; for benchmarks only.
+ * ------------------------------------------------------------------------- */
+int hla_profile_begin(int max_records);
+int hla_profile_end(void);
+int hla_profile_summary(char *buf, size_t len);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HLA_H */

@@ -310,3 +310,31 @@ def exclusive_scan_states(states):
     pre = blelloch_exclusive(items, combine, E)
     total = combine(pre[-1], items[-1])
     return tuple(np.stack([p[i] for p in pre], axis=nb) for i in range(5)), total
+
+
+def hla2_den_scale(q, k, masked=True):
+    """Sum of the absolute values of the terms of den_t, in fp64, [..., n].
+
+    masked:   D_t = sum_{j<=t} |q_t^T S_j q_j|   (Thm. 1 proof, v_j -> 1)
+    unmasked: D_t = sum_{j<=t} |q_t^T S_t q_j|   (Eq. hla-row)
+    It bounds |den_t| and is the scale against which a computed den_t is
+    judged where den_t itself is near zero."""
+    q, k = _f64(q), _f64(k)
+    batch = q.shape[:-2]
+    n, d = q.shape[-2:]
+    S = np.zeros(batch + (d, d))
+    R = np.empty(q.shape)
+    for t in range(n):
+        S = S + k[..., t, :, None] * k[..., t, None, :]
+        R[..., t, :] = np.einsum('...ab,...b->...a', S, q[..., t, :])       # r_t = S_t q_t
+    D = np.empty(batch + (n,))
+    blk = 1024
+    for s in range(0, n, blk):
+        e = min(n, s + blk)
+        if masked:
+            A = np.abs(q[..., s:e, :] @ np.swapaxes(R[..., :e, :], -1, -2))  # |q_t . r_j|
+        else:
+            A = np.abs(R[..., s:e, :] @ np.swapaxes(q[..., :e, :], -1, -2))  # |r_t . q_j|
+        A = A * (np.arange(e)[None, :] <= np.arange(s, e)[:, None])
+        D[..., s:e] = A.sum(-1)
+    return D

@@ -1,0 +1,9 @@
+"""MI355X-native Higher-order Linear Attention (arXiv 2510.27258).
+
+The computation lives in libhla.so (HIP for gfx950, C ABI in include/hla.h).
+`capi` mirrors the C entry points one to one; `hla` wraps them for torch
+tensors (torch provides device memory and the current stream only).
+"""
+from . import capi  # noqa: F401
+from .hla import (chunk_summaries, forward, hla3_forward, new_state, prefill, scan,  # noqa: F401
+                  split_state, state_floats, step, workspace_bytes)

@@ -1,0 +1,153 @@
+"""ctypes binding of libhla.so: one Python function per C entry point, same
+names and argument order as include/hla.h.  Pointers are passed as integers
+(device addresses), streams as integers (hipStream_t, 0 = default stream).
+
+The library must have been built (paper_2510_27258_amd/build.py); there is no
+fallback: a missing library raises at first use.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhla.so")
+
+HLA_OK, HLA_ERR_INVALID, HLA_ERR_UNSUPPORTED, HLA_ERR_WORKSPACE, HLA_ERR_HIP = range(5)
+HLA_FP32, HLA_BF16 = 0, 1
+HLA_ALGO_AUTO, HLA_ALGO_CHUNKED, HLA_ALGO_FUSED = 0, 1, 2
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_F = ctypes.c_float
+_Z = ctypes.c_size_t
+
+_SIGS = {
+    "hla_last_error": (ctypes.c_char_p, []),
+    "hla2_state_floats": (_Z, [_I, _I]),
+    "hla2_workspace_bytes": (_Z, [_I] * 7),
+    "hla2_workspace_bytes_ex": (_Z, [_I] * 8),
+    "hla2_forward": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
+    "hla2_forward_ex": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _I, _P]),
+    "hla2_chunk_summaries": (_I, [_P, _P, _P, _P] + [_I] * 7 + [_P]),
+    "hla2_scan": (_I, [_P, _P, _P, _P] + [_I] * 5 + [_P]),
+    "hla2_prefill_workspace_bytes": (_Z, [_I] * 7),
+    "hla2_prefill": (_I, [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
+    "hla2_step": (_I, [_P, _P, _P, _P, _P] + [_I] * 6 + [_F, _I, _P]),
+    "hla_profile_begin": (_I, [_I]),
+    "hla_profile_end": (_I, []),
+    "hla_profile_summary": (_I, [ctypes.c_char_p, _Z]),
+    "hla3_workspace_bytes": (_Z, [_I] * 7),
+    "hla3_forward": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
+}
+
+
+class HLAError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"HLA error {code}: {msg}")
+        self.code = code
+
+
+def lib():
+    """The loaded library (ctypes.CDLL).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2510_27258_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name, None)
+            if fn is None:
+                continue
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_symbols():
+    return [n for n in _SIGS if hasattr(lib(), n)]
+
+
+def _call(name, *args):
+    rc = getattr(lib(), name)(*args)
+    if rc != HLA_OK:
+        raise HLAError(rc, lib().hla_last_error().decode())
+    return rc
+
+
+def hla_last_error():
+    return lib().hla_last_error().decode()
+
+
+def hla2_state_floats(d, dv):
+    return lib().hla2_state_floats(d, dv)
+
+
+def hla2_workspace_bytes(B, H, n, d, dv, chunk, dtype):
+    return lib().hla2_workspace_bytes(B, H, n, d, dv, chunk, dtype)
+
+
+def hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, algo):
+    return lib().hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, algo)
+
+
+def hla2_forward(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes, stream):
+    return _call("hla2_forward", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
+                 ws_bytes, stream)
+
+
+def hla2_forward_ex(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes, algo,
+                    stream):
+    return _call("hla2_forward_ex", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
+                 ws_bytes, algo, stream)
+
+
+def hla2_chunk_summaries(q, k, v, states, B, H, n, d, dv, chunk, dtype, stream):
+    return _call("hla2_chunk_summaries", q, k, v, states, B, H, n, d, dv, chunk, dtype, stream)
+
+
+def hla2_scan(states, init, prefix, total, B, H, M, d, dv, stream):
+    return _call("hla2_scan", states, init, prefix, total, B, H, M, d, dv, stream)
+
+
+def hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype):
+    return lib().hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype)
+
+
+def hla2_prefill(state, q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes,
+                 stream):
+    return _call("hla2_prefill", state, q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
+                 ws_bytes, stream)
+
+
+def hla2_step(state, q_t, k_t, v_t, out_t, B, H, d, dv, masked, normalized, eps, dtype, stream):
+    return _call("hla2_step", state, q_t, k_t, v_t, out_t, B, H, d, dv, masked, normalized, eps, dtype, stream)
+
+
+def hla3_workspace_bytes(B, H, n, d, dv, chunk, dtype):
+    return lib().hla3_workspace_bytes(B, H, n, d, dv, chunk, dtype)
+
+
+def hla3_forward(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes, stream):
+    return _call("hla3_forward", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
+                 ws_bytes, stream)
+
+
+def hla_profile_begin(max_records):
+    return _call("hla_profile_begin", max_records)
+
+
+def hla_profile_end():
+    return _call("hla_profile_end")
+
+
+def hla_profile_summary():
+    """{kernel name: (launches, total_ms)} of the records since the last call."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    _call("hla_profile_summary", buf, len(buf))
+    res = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.split()
+        res[name] = (int(cnt), float(ms))
+    return res

@@ -1,0 +1,44 @@
+// Shared device/host definitions for the HLA HIP library (gfx950).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace hla {
+
+// Record layout of one second-order state (one head or one chunk), fp32:
+//   S [d][d] | C [d][dv] | m [d] | G [d][dv] | h [d]
+__host__ __device__ inline size_t state_floats(int d, int dv) {
+  return (size_t)d * d + 2 * (size_t)d * dv + 2 * (size_t)d;
+}
+__host__ __device__ inline size_t off_C(int d, int dv) { return (size_t)d * d; }
+__host__ __device__ inline size_t off_m(int d, int dv) { return (size_t)d * d + (size_t)d * dv; }
+__host__ __device__ inline size_t off_G(int d, int dv) { return (size_t)d * d + (size_t)d * dv + d; }
+__host__ __device__ inline size_t off_h(int d, int dv) { return (size_t)d * d + 2 * (size_t)d * dv + d; }
+
+// Element loads converting the storage type to fp32.  bf16 is held as its
+// 16-bit pattern; widening is exact.
+__device__ __forceinline__ float ldf(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ float ldf(const uint16_t* p, size_t i) {
+  return __uint_as_float(((uint32_t)p[i]) << 16);
+}
+
+}  // namespace hla
+
+// Launchers implemented in the .hip files (host code, called by the C ABI).
+namespace hla {
+struct Fwd {
+  const void* q; const void* k; const void* v; float* out;
+  int BH, n, d, dv, chunk, masked, normalized, dtype;
+  float eps;
+};
+hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, float* states,
+                                  int BH, int n, int d, int dv, int chunk, int dtype,
+                                  hipStream_t s);
+hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
+                       int BH, int M, int d, int dv, hipStream_t s);
+hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s);
+hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out,
+                       int BH, int d, int dv, int masked, int normalized, float eps, int dtype,
+                       hipStream_t s);
+}  // namespace hla

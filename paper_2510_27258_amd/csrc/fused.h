@@ -1,0 +1,10 @@
+// Fused segment-walk forward for bf16 inputs (MFMA).  See fused.hip.
+#pragma once
+#include "common.h"
+
+namespace hla {
+bool fused_supported(int n, int d, int dv, int chunk, int dtype, int masked);
+size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk);
+// init/final: optional [BH][F] states (carry-in of token 0 / state after the last token).
+hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, void* workspace, hipStream_t s);
+}  // namespace hla

@@ -1,0 +1,227 @@
+// C ABI of the HLA library: argument validation, workspace carving and kernel
+// dispatch.  No call allocates, synchronises or throws across the boundary.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/hla.h"
+#include "common.h"
+#include "fused.h"
+#include "profile.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return HLA_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(HLA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool pow2_in(int x, int lo, int hi) { return x >= lo && x <= hi && (x & (x - 1)) == 0; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int check_dims(int B, int H, int n, int d, int dv, int chunk, int dtype, bool need_n) {
+  if (B < 1 || H < 1) return fail(HLA_ERR_INVALID, "B and H must be >= 1 (got B=%d H=%d)", B, H);
+  if ((long long)B * H > 65535) return fail(HLA_ERR_UNSUPPORTED, "B*H=%lld exceeds 65535", (long long)B * H);
+  if (need_n && n < 1) return fail(HLA_ERR_INVALID, "n must be >= 1 (got %d)", n);
+  if (!pow2_in(d, 16, 128) || !pow2_in(dv, 16, 128))
+    return fail(HLA_ERR_UNSUPPORTED, "d and dv must be one of 16, 32, 64, 128 (got d=%d dv=%d)", d, dv);
+  if (chunk != 0 && !pow2_in(chunk, 16, 128))
+    return fail(HLA_ERR_UNSUPPORTED, "chunk must be one of 16, 32, 64, 128 (got %d)", chunk);
+  if (dtype != HLA_FP32 && dtype != HLA_BF16) return fail(HLA_ERR_INVALID, "dtype must be HLA_FP32 or HLA_BF16");
+  return HLA_OK;
+}
+
+int check_flags(int masked, int normalized, float eps) {
+  if ((masked != 0 && masked != 1) || (normalized != 0 && normalized != 1))
+    return fail(HLA_ERR_INVALID, "masked and normalized must be 0 or 1");
+  if (!std::isfinite(eps) || eps < 0.f) return fail(HLA_ERR_INVALID, "eps must be finite and >= 0");
+  return HLA_OK;
+}
+
+int check_ptr(const void* p, const char* name) {
+  if (!p) return fail(HLA_ERR_INVALID, "%s is NULL", name);
+  if (!aligned16(p)) return fail(HLA_ERR_INVALID, "%s is not 16-byte aligned", name);
+  return HLA_OK;
+}
+
+size_t chunked_ws(int BH, int n, int d, int dv, int chunk) {
+  const size_t M = (size_t)(n + chunk - 1) / chunk;
+  return 2 * align256(sizeof(float) * (size_t)BH * M * hla::state_floats(d, dv));
+}
+
+int select_algo(int algo, int n, int d, int dv, int chunk, int dtype, int masked) {
+  if (algo == HLA_ALGO_AUTO) return hla::fused_supported(n, d, dv, chunk, dtype, masked) ? HLA_ALGO_FUSED : HLA_ALGO_CHUNKED;
+  return algo;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hla_last_error(void) { return g_err; }
+
+size_t hla2_state_floats(int d, int dv) { return hla::state_floats(d, dv); }
+
+size_t hla2_workspace_bytes_ex(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo) {
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  const int a = select_algo(algo, n, d, dv, chunk, dtype, 1);
+  if (a == HLA_ALGO_FUSED) return hla::fused_workspace_bytes(B * H, n, d, dv, chunk);
+  return chunked_ws(B * H, n, d, dv, chunk);
+}
+
+size_t hla2_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
+  // large enough for whichever algorithm AUTO selects for either flag value
+  size_t a = hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, HLA_ALGO_AUTO);
+  size_t b = hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, HLA_ALGO_CHUNKED);
+  return a > b ? a : b;
+}
+
+int hla2_forward_ex(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
+                    int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
+                    size_t workspace_bytes, int algo, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
+      (rc = check_ptr(out, "out")))
+    return rc;
+  if (algo < HLA_ALGO_AUTO || algo > HLA_ALGO_FUSED) return fail(HLA_ERR_INVALID, "unknown algo %d", algo);
+  const int a = select_algo(algo, n, d, dv, chunk, dtype, masked);
+  const int BH = B * H;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
+  if (a == HLA_ALGO_FUSED) {
+    if (!hla::fused_supported(n, d, dv, chunk, dtype, masked))
+      return fail(HLA_ERR_UNSUPPORTED, "fused path needs bf16 inputs, masked=1 and (d, dv, chunk) in its "
+                                       "instantiated set (got d=%d dv=%d chunk=%d dtype=%d)", d, dv, chunk, dtype);
+    const size_t need = hla::fused_workspace_bytes(BH, n, d, dv, chunk);
+    if (!workspace || workspace_bytes < need)
+      return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+    hipError_t e = hla::launch_fused(f, nullptr, nullptr, workspace, s);
+    if (e != hipSuccess) return hip_fail(e, "fused forward");
+    return ok();
+  }
+  const size_t need = chunked_ws(BH, n, d, dv, chunk);
+  if (!workspace || workspace_bytes < need)
+    return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  const int M = (n + chunk - 1) / chunk;
+  float* states = static_cast<float*>(workspace);
+  float* prefix = reinterpret_cast<float*>(static_cast<char*>(workspace) + need / 2);
+  hipError_t e = HLA_PROF("chunk_summary", s, hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, chunk, dtype, s));
+  if (e != hipSuccess) return hip_fail(e, "chunk summaries");
+  e = HLA_PROF("scan", s, hla::launch_scan(states, nullptr, prefix, nullptr, BH, M, d, dv, s));
+  if (e != hipSuccess) return hip_fail(e, "scan");
+  e = HLA_PROF("readout", s, hla::launch_readout(f, prefix, s));
+  if (e != hipSuccess) return hip_fail(e, "readout");
+  return ok();
+}
+
+int hla2_forward(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
+                 int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  return hla2_forward_ex(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, workspace,
+                         workspace_bytes, HLA_ALGO_AUTO, stream);
+}
+
+int hla2_chunk_summaries(const void* q, const void* k, const void* v, float* states, int B, int H, int n, int d,
+                         int dv, int chunk, int dtype, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
+      (rc = check_ptr(states, "states")))
+    return rc;
+  hipError_t e = hla::launch_chunk_summaries(q, k, v, states, B * H, n, d, dv, chunk, dtype,
+                                             reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "chunk summaries");
+  return ok();
+}
+
+int hla2_scan(const float* states, const float* init, float* prefix, float* total, int B, int H, int M, int d,
+              int dv, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, 1, d, dv, 0, HLA_FP32, false)) != HLA_OK) return rc;
+  if (M < 1) return fail(HLA_ERR_INVALID, "M must be >= 1 (got %d)", M);
+  if ((rc = check_ptr(states, "states")) || (rc = check_ptr(prefix, "prefix"))) return rc;
+  if (init && !aligned16(init)) return fail(HLA_ERR_INVALID, "init is not 16-byte aligned");
+  if (total && !aligned16(total)) return fail(HLA_ERR_INVALID, "total is not 16-byte aligned");
+  hipError_t e = hla::launch_scan(states, init, prefix, total, B * H, M, d, dv, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "scan");
+  return ok();
+}
+
+size_t hla2_prefill_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  return chunked_ws(B * H, n, d, dv, chunk) + align256(sizeof(float) * (size_t)B * H * hla::state_floats(d, dv));
+}
+
+int hla2_prefill(float* state, const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d,
+                 int dv, int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
+  if ((rc = check_ptr(state, "state")) || (rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) ||
+      (rc = check_ptr(v, "v")))
+    return rc;
+  if (out && !aligned16(out)) return fail(HLA_ERR_INVALID, "out is not 16-byte aligned");
+  const int BH = B * H;
+  const size_t cws = chunked_ws(BH, n, d, dv, chunk);
+  const size_t need = hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype);
+  if (!workspace || workspace_bytes < need)
+    return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int M = (n + chunk - 1) / chunk;
+  char* base = static_cast<char*>(workspace);
+  float* states = reinterpret_cast<float*>(base);
+  float* prefix = reinterpret_cast<float*>(base + cws / 2);
+  float* total = reinterpret_cast<float*>(base + cws);
+  hipError_t e = hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, chunk, dtype, s);
+  if (e != hipSuccess) return hip_fail(e, "chunk summaries");
+  e = hla::launch_scan(states, state, prefix, total, BH, M, d, dv, s);
+  if (e != hipSuccess) return hip_fail(e, "scan");
+  if (out) {
+    hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
+    e = hla::launch_readout(f, prefix, s);
+    if (e != hipSuccess) return hip_fail(e, "readout");
+  }
+  e = hipMemcpyAsync(state, total, sizeof(float) * (size_t)BH * hla::state_floats(d, dv), hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "state copy");
+  return ok();
+}
+
+int hla2_step(float* state, const void* q_t, const void* k_t, const void* v_t, float* out_t, int B, int H, int d,
+              int dv, int masked, int normalized, float eps, int dtype, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, 1, d, dv, 0, dtype, false)) != HLA_OK) return rc;
+  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
+  if ((rc = check_ptr(state, "state")) || (rc = check_ptr(q_t, "q_t")) || (rc = check_ptr(k_t, "k_t")) ||
+      (rc = check_ptr(v_t, "v_t")) || (rc = check_ptr(out_t, "out_t")))
+    return rc;
+  hipError_t e = hla::launch_step(state, q_t, k_t, v_t, out_t, B * H, d, dv, masked, normalized, eps, dtype,
+                                  reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "step");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,274 @@
+"""GPU parity of the second-order HLA library against the fp64 oracle.
+
+Every call goes through the C ABI (paper_2510_27258_amd.capi via the torch
+helpers).  Inputs come from the seeded generator; expected values come from
+the oracle only.  Bars: 1e-5 (fp32 inputs) and 2e-3 (bf16 inputs) on the
+row-wise relative error max_t ||o_t - ref_t||_inf / ||ref_t||_inf.  The ratio
+normalised output is judged on rows whose denominator is well away from zero
+(|den_t + eps| >= 0.05 D_t, D_t the sum of |terms| of den_t); its numerator
+and denominator are judged separately everywhere.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2510_27258_amd as hla
+from paper_2510_27258_amd import capi
+from paper_2510_27258_amd import inputs as I
+from oracle import hla2 as O
+from oracle import native
+from tests.helpers import dev, gen, rowwise_err, tol_for
+
+pytestmark = pytest.mark.gpu
+
+ALGOS = [capi.HLA_ALGO_CHUNKED]
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _oracle(q, k, v, masked, state=None):
+    num, den, fin, _ = native.hla2_serial_c(q, k, v, masked=masked, state=state, threads=16)
+    return num, den, fin
+
+
+def _check_forward(B, H, n, d, dv, chunk, dist, masked, normalized, algo, seed=0, eps=1e-6):
+    q, k, v, code = gen(B, H, n, d, dv, dist, seed)
+    _say(f"case B={B} H={H} n={n} d={d} dv={dv} chunk={chunk} dist={dist} masked={masked} "
+         f"normalized={normalized} algo={algo}")
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    num_ref, den_ref, _ = _oracle(q, k, v, masked)
+    tol = tol_for(code)
+    num = hla.forward(qd, kd, vd, chunk, masked=masked, normalized=False, algo=algo).cpu().numpy()
+    err = rowwise_err(num, num_ref)
+    assert err <= tol, f"num row-wise error {err:.3e} > {tol}"
+    if normalized:
+        out = hla.forward(qd, kd, vd, chunk, masked=masked, normalized=True, eps=eps, algo=algo).cpu().numpy()
+        ones = torch.ones(B, H, n, 16, dtype=vd.dtype, device="cuda")
+        den = hla.forward(qd, kd, ones, chunk, masked=masked, normalized=False, algo=algo)[..., 0].cpu().numpy()
+        D = O.hla2_den_scale(q, k, masked=bool(masked))
+        e_den = float((np.abs(den - den_ref) / D).max())
+        assert e_den <= tol, f"den error {e_den:.3e} > {tol}"
+        good = np.abs(den_ref + eps) >= 0.05 * D
+        assert good.mean() > 0.3
+        ref = num_ref / (den_ref + eps)[..., None]
+        e_out = rowwise_err(out[good], ref[good])
+        assert e_out <= tol, f"normalised output error {e_out:.3e} > {tol}"
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("shape", [
+    (1, 2, 256, 32, 32, 64),      # the small fp32 workload (B1 H2 n256 d32, chunk 64)
+    (2, 3, 200, 32, 64, 64),      # d != dv, ragged tail
+    (1, 2, 77, 16, 16, 16),
+    (1, 1, 1, 16, 16, 16),        # a single token
+    (1, 2, 300, 128, 128, 128),
+    (1, 2, 130, 64, 128, 32),
+    (2, 2, 257, 128, 16, 64),
+    (1, 1, 50, 64, 64, 128),      # n < chunk
+])
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_forward_small(shape, dist, algo):
+    B, H, n, d, dv, chunk = shape
+    for masked in (1, 0):
+        _check_forward(B, H, n, d, dv, chunk, dist, masked, normalized=False, algo=algo)
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_forward_normalized_small(dist, algo):
+    for masked in (1, 0):
+        _check_forward(2, 2, 190, 32, 32, 64, dist, masked, normalized=True, algo=algo)
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+def test_forward_every_chunk(algo):
+    for chunk in (16, 32, 64, 128):
+        _check_forward(1, 2, 203, 64, 64, chunk, "unit", 1, normalized=False, algo=algo)
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+def test_bf16_d64_workload_sampled_heads(algo):
+    """B4 H16 n4096 d=dv=64 bf16, chunk 64: full GPU run, 4 sampled heads vs the oracle."""
+    w = I.WORKLOADS["hla2-masked-bf16-B4H16-n4096-d64-C64"]
+    q, k, v, code = gen(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
+    _say("case bf16 B4H16 n4096 d64 full size")
+    out = hla.forward(dev(q, code), dev(k, code), dev(v, code), w["chunk"], masked=True, algo=algo).cpu().numpy()
+    heads = [(0, 0), (1, 5), (2, 11), (3, 15)]
+    qs = np.stack([q[b, h] for b, h in heads])
+    ks = np.stack([k[b, h] for b, h in heads])
+    vs = np.stack([v[b, h] for b, h in heads])
+    num_ref, _, _ = _oracle(qs, ks, vs, True)
+    got = np.stack([out[b, h] for b, h in heads])
+    err = rowwise_err(got, num_ref)
+    _say(f"row-wise error {err:.3e}")
+    assert err <= 2e-3
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+def test_bf16_d128_normalized_workload_sampled_heads(algo):
+    """B2 H32 n16384 d=dv=128 bf16, chunk 128, ratio-normalised: full GPU run,
+    2 sampled heads vs the oracle (num, den and the normalised output)."""
+    w = I.WORKLOADS["hla2-masked-normalized-bf16-B2H32-n16384-d128-C128"]
+    q, k, v, code = gen(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
+    _say("case bf16 B2H32 n16384 d128 normalized full size")
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    eps = w["eps"]
+    out = hla.forward(qd, kd, vd, w["chunk"], masked=True, normalized=True, eps=eps, algo=algo).cpu().numpy()
+    num = hla.forward(qd, kd, vd, w["chunk"], masked=True, normalized=False, algo=algo).cpu().numpy()
+    heads = [(0, 3), (1, 30)]
+    qs = np.stack([q[b, h] for b, h in heads])
+    ks = np.stack([k[b, h] for b, h in heads])
+    vs = np.stack([v[b, h] for b, h in heads])
+    ones = torch.ones(2, 1, w["n"], 16, dtype=torch.bfloat16, device="cuda")
+    den = hla.forward(dev(qs[:, None], code), dev(ks[:, None], code), ones, w["chunk"], masked=True,
+                      algo=algo)[:, 0, :, 0].cpu().numpy()
+    num_ref, den_ref, _ = _oracle(qs, ks, vs, True)
+    D = O.hla2_den_scale(qs, ks)
+    got_num = np.stack([num[b, h] for b, h in heads])
+    got_out = np.stack([out[b, h] for b, h in heads])
+    e_num = rowwise_err(got_num, num_ref)
+    e_den = float((np.abs(den - den_ref) / D).max())
+    good = np.abs(den_ref + eps) >= 0.05 * D
+    ref = num_ref / (den_ref + eps)[..., None]
+    e_out = rowwise_err(got_out[good], ref[good])
+    _say(f"num {e_num:.3e} den {e_den:.3e} out {e_out:.3e} rows kept {good.mean():.3f} "
+         f"negative den {float((den_ref < 0).mean()):.3f}")
+    assert e_num <= 2e-3 and e_den <= 2e-3 and e_out <= 2e-3
+
+
+# ----------------------------------------------------------------- summaries and scan
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_chunk_summaries_and_scan(dist):
+    B, H, n, d, dv, chunk = 2, 2, 150, 32, 16, 32
+    q, k, v, code = gen(B, H, n, d, dv, dist, 3)
+    _say(f"case summaries+scan {dist}")
+    st = hla.chunk_summaries(dev(q, code), dev(k, code), dev(v, code), chunk)
+    ref = O.chunk_summaries(q, k, v, chunk)
+    S, C, m, G, h = (x.cpu().numpy() for x in hla.split_state(st, d, dv))
+    for got, exp in zip((S, C, m, G, h), ref):
+        scale = np.abs(exp).max()
+        assert np.abs(got - exp).max() <= 1e-5 * scale
+    # scan with an initial state
+    init_q, init_k, init_v, _ = gen(B, H, 40, d, dv, dist, 4)
+    _, init = O.hla2_serial(init_q, init_k, init_v)
+    init_dev = torch.cat([torch.from_numpy(np.ascontiguousarray(x, np.float32)).reshape(B, H, -1) for x in init],
+                         dim=-1).cuda()
+    prefix, total = hla.scan(st, d, dv, init=init_dev)
+    pre_ref, tot_ref = O.exclusive_scan_states(ref)
+    pre_ref = tuple(np.stack([O.combine(tuple(x[:, :] for x in init),
+                                        tuple(y[:, :, c] for y in pre_ref))[i] for c in range(st.shape[2])],
+                             axis=2) for i in range(5))
+    tot_ref = O.combine(init, tot_ref)
+    for got, exp in zip(hla.split_state(prefix, d, dv), pre_ref):
+        got = got.cpu().numpy()
+        assert np.abs(got - exp).max() <= 1e-5 * max(np.abs(exp).max(), 1.0)
+    for got, exp in zip(hla.split_state(total, d, dv), tot_ref):
+        got = got.cpu().numpy()
+        assert np.abs(got - exp).max() <= 1e-5 * max(np.abs(exp).max(), 1.0)
+
+
+# ----------------------------------------------------------------- prefill and decode
+def _state_to_np(state, d, dv):
+    return tuple(x.cpu().numpy().astype(np.float64) for x in hla.split_state(state, d, dv))
+
+
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+@pytest.mark.parametrize("masked,normalized", [(1, 0), (0, 0), (1, 1)])
+def test_prefill_then_steps(dist, masked, normalized):
+    B, H, d, dv, n1, steps, chunk = 2, 3, 32, 64, 100, 20, 32
+    q, k, v, code = gen(B, H, n1 + steps, d, dv, dist, 5)
+    _say(f"case prefill+steps {dist} masked={masked} normalized={normalized}")
+    eps = 0.5 if normalized else 1e-6
+    num_ref, den_ref, fin_ref = _oracle(q, k, v, masked)
+    ref = num_ref / (den_ref + eps)[..., None] if normalized else num_ref
+    state = hla.new_state(B, H, d, dv)
+    out1 = hla.prefill(state, dev(q[:, :, :n1], code), dev(k[:, :, :n1], code), dev(v[:, :, :n1], code), chunk,
+                       masked=masked, normalized=normalized, eps=eps).cpu().numpy()
+    outs = [out1]
+    for t in range(n1, n1 + steps):
+        o = hla.step(state, dev(q[:, :, t], code), dev(k[:, :, t], code), dev(v[:, :, t], code), masked=masked,
+                     normalized=normalized, eps=eps)
+        outs.append(o.cpu().numpy()[:, :, None])
+    got = np.concatenate(outs, axis=2)
+    if normalized:
+        good = np.abs(den_ref + eps) >= 0.05 * O.hla2_den_scale(q, k, masked=bool(masked))
+        assert rowwise_err(got[good], ref[good]) <= 1e-4
+    else:
+        assert rowwise_err(got, ref) <= 1e-5
+    for g, e in zip(_state_to_np(state, d, dv), fin_ref):
+        assert np.abs(g - e).max() <= 1e-5 * np.abs(e).max()
+
+
+def test_decode_workload_sampled_heads():
+    """B64 H32 d=dv=128: prefill 2048 bf16 tokens, then 1024 steps; 16 sampled
+    heads vs the oracle over all 3072 tokens, including the final states."""
+    w = I.WORKLOADS["hla2-decode-bf16-B64H32-d128-prefix2048-steps1024"]
+    B, H, d, dv = w["B"], w["H"], w["d"], w["dv"]
+    q, k, v, code = gen(B, H, w["n"], d, dv, w["dist"], w["seed"])
+    qs, ks, vs, _ = gen(B, H, w["steps"], d, dv, w["dist"], w["step_seed"])
+    _say("case decode B64 H32 d128 prefix 2048 + 1024 steps")
+    rng = np.random.default_rng(123)
+    sel = sorted(rng.choice(B * H, size=16, replace=False).tolist())
+    bsel, hsel = np.array(sel) // H, np.array(sel) % H
+    bsel_d, hsel_d = torch.as_tensor(bsel, device="cuda"), torch.as_tensor(hsel, device="cuda")
+    state = hla.new_state(B, H, d, dv)
+    hla.prefill(state, dev(q, code), dev(k, code), dev(v, code), w["chunk"], want_out=False)
+    qsd, ksd, vsd = dev(qs, code), dev(ks, code), dev(vs, code)
+    got = []
+    for t in range(w["steps"]):
+        o = hla.step(state, qsd[:, :, t].contiguous(), ksd[:, :, t].contiguous(), vsd[:, :, t].contiguous())
+        got.append(o[bsel_d, hsel_d])
+    got = torch.stack(got, dim=1).cpu().numpy()
+    qa = np.concatenate([q[bsel, hsel], qs[bsel, hsel]], axis=1)
+    ka = np.concatenate([k[bsel, hsel], ks[bsel, hsel]], axis=1)
+    va = np.concatenate([v[bsel, hsel], vs[bsel, hsel]], axis=1)
+    num_ref, _, fin_ref = _oracle(qa, ka, va, True)
+    err = rowwise_err(got, num_ref[:, w["n"]:])
+    _say(f"decode row-wise error {err:.3e}")
+    assert err <= 2e-3
+    for g, e in zip(_state_to_np(state, d, dv), fin_ref):
+        g = g[bsel, hsel]
+        assert np.abs(g - e).max() <= 2e-3 * np.abs(e).max()
+
+
+# ----------------------------------------------------------------- ABI behaviour
+def test_abi_errors_leave_outputs_untouched():
+    q = torch.zeros(1, 1, 8, 16, device="cuda")
+    out = torch.full((1, 1, 8, 16), 7.0, device="cuda")
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    L = capi.lib()
+    rc = L.hla2_forward(q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 8, 24, 16, 16, 1, 0,
+                        1e-6, 0, ws.data_ptr(), ws.numel(), s)
+    assert rc == capi.HLA_ERR_UNSUPPORTED and "d and dv" in capi.hla_last_error()
+    rc = L.hla2_forward(None, q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 8, 16, 16, 16, 1, 0, 1e-6, 0,
+                        ws.data_ptr(), ws.numel(), s)
+    assert rc == capi.HLA_ERR_INVALID
+    rc = L.hla2_forward(q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 8, 16, 16, 16, 1, 0, 1e-6,
+                        0, ws.data_ptr(), 16, s)
+    assert rc == capi.HLA_ERR_WORKSPACE
+    rc = L.hla2_forward(q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 8, 16, 16, 16, 2, 0, 1e-6,
+                        0, ws.data_ptr(), ws.numel(), s)
+    assert rc == capi.HLA_ERR_INVALID
+    rc = L.hla2_forward(q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 8, 16, 16, 16, 1, 0,
+                        float("nan"), 0, ws.data_ptr(), ws.numel(), s)
+    assert rc == capi.HLA_ERR_INVALID
+    rc = L.hla2_forward(q.data_ptr() + 4, q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 8, 16, 16, 16, 1, 0,
+                        1e-6, 0, ws.data_ptr(), ws.numel(), s)
+    assert rc == capi.HLA_ERR_INVALID
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
+
+
+def test_deterministic():
+    q, k, v, code = gen(1, 4, 500, 64, 64, "unit", 9)
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    for algo in ALGOS:
+        a = hla.forward(qd, kd, vd, 64, algo=algo)
+        b = hla.forward(qd, kd, vd, 64, algo=algo)
+        assert torch.equal(a, b)

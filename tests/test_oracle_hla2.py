@@ -339,3 +339,13 @@ def test_pins_catch_mask_without_diagonal():
     bad = ((W @ W.T) * L) @ v
     t = np.arange(1, n + 1)
     assert np.abs(bad[:, 0] - t * (t + 1) / 2).max() >= 1
+
+
+def test_den_scale_bounds_den():
+    q, k, v = _rand((2, 30, 4), 3, seed=19)
+    for masked in (True, False):
+        (_, den), _ = H.hla2_serial(q, k, v, masked=masked, return_num_den=True)
+        D = H.hla2_den_scale(q, k, masked=masked)
+        assert np.all(np.abs(den) <= D * (1 + 1e-12))
+        # with q = k the diagonal term q_t^T S_t q_t >= 0 and all terms of t=1 coincide
+        np.testing.assert_allclose(D[..., 0], np.abs(den[..., 0]), rtol=1e-12)
