@@ -25,29 +25,48 @@ FP32_VALU_PEAK_TFLOPS = 157.3   # fp32 vector
 DEFAULT_WORKLOAD = "hla2-masked-bf16-B4H16-n4096-d64-C64"
 
 
-def kernel_costs(w, algo):
+def kernel_costs(w, P=None):
     """Algorithmic cost of one launch of each kernel of the forward path:
     {name: (bound, bytes, flops)}.  bytes = HBM bytes the kernel must move
-    (inputs read once, outputs written once); flops = useful arithmetic
-    (a dense C x C product counts C^2 per output element, triangles are not
-    halved)."""
+    (inputs read once, outputs written once); flops = useful arithmetic of
+    the kernel's formulation (a dense C x C product counts C^2 per output
+    element; triangles are not halved).  P = segments per head (fused path)."""
     B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
     BH = B * H
     M = -(-n // C)
     es = 2 if w["dist"] == "unit" else 4
     F = d * d + 2 * d * dv + 2 * d
-    qkv = BH * n * (2 * d + dv) * es
-    outb = BH * n * dv * 4
-    states = BH * M * F * 4
-    if algo == "fused":
-        from paper_2510_27258_amd.fused_info import fused_costs
-        return fused_costs(w)
     tok = BH * n
-    return {
-        "chunk_summary": ("alu", qkv + states, tok * 2 * (C * d / 2 + C * dv / 2 + d * d + 2 * d * dv)),
-        "scan": ("hbm", 2 * states, BH * M * 2 * (d * d * dv + d * d)),
-        "readout": ("alu", qkv + states + outb, tok * 2 * (d * d + 1.5 * C * d + 2 * d * dv + C * dv / 2)),
+    qkv_tok = (2 * d + dv) * es
+    costs = {
+        # general path
+        "chunk_summary": ("alu", tok * qkv_tok + BH * M * F * 4, tok * 2 * (C * d / 2 + C * dv / 2 + d * d + 2 * d * dv)),
+        "readout": ("alu", tok * (qkv_tok + 4 * dv) + BH * M * F * 4,
+                    tok * 2 * (d * d + 1.5 * C * d + 2 * d * dv + C * dv / 2)),
+        "scan": ("hbm", 2 * BH * M * F * 4, BH * M * 2 * (d * d * dv + d * d)),
     }
+    if P:
+        cps = -(-M // P)
+        sum_tok = BH * min(n, (P - 1) * cps * C)
+        costs.update({
+            # fused path: the output walk reads q/k/v once and writes out once
+            "walk": ("hbm", tok * (qkv_tok + 4 * dv) + BH * P * F * 4,
+                     tok * 2 * (3 * C * d + C * dv + 2 * d * d + 2 * d * dv)),
+            "walk_summary": ("hbm", sum_tok * qkv_tok + BH * (P - 1) * F * 4,
+                             sum_tok * 2 * (2 * C * d + 2 * d * d + 2 * d * dv)),
+            "flip": ("hbm", 2 * BH * P * F * 4, BH * P * 2 * (d * d * dv + d * d)),
+            "scan": ("hbm", 2 * BH * max(P - 1, 1) * F * 4, BH * max(P - 1, 1) * 2 * (d * d * dv + d * d)),
+        })
+    return costs
+
+
+def fused_segments(BH, n, C):
+    """Segments per head chosen by the library for the fused path (same rule as fused_plan)."""
+    M = -(-n // C)
+    p = int(os.environ.get("HLA_FUSED_SEGMENTS", 256 // BH))
+    p = max(1, min(p, M))
+    cps = -(-M // p)
+    return -(-M // cps)
 
 
 def peak_for(bound):
@@ -165,8 +184,11 @@ def main():
     torch.cuda.synchronize()
     prof = capi.hla_profile_summary()
     capi.hla_profile_end()
-    used_algo = "fused" if ("walk" in " ".join(prof)) else "chunked"
-    costs = kernel_costs(w, used_algo)
+    used_algo = "fused" if "walk" in prof else "chunked"
+    P = None
+    if used_algo == "fused":
+        P = fused_segments(B * H, n, C)
+    costs = kernel_costs(w, P)
     dom = max(prof, key=lambda kname: prof[kname][1])
     cnt, tot_ms = prof[dom]
     avg_s = tot_ms / cnt / 1e3

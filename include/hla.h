@@ -93,6 +93,11 @@ int hla2_forward_ex(const void *q, const void *k, const void *v, float *out,
                     float eps, int dtype, void *workspace, size_t workspace_bytes, int algo,
                     void *stream);
 
+/* 1 if hla2_forward_ex would accept `algo` for these arguments, else 0.
+ * HLA_ALGO_FUSED covers bf16 inputs, masked = 1 and (chunk, d, dv) in
+ * {(64,64,64), (32,32,32), (64,32,32), (32,64,64), (64,64,32), (64,32,64)}. */
+int hla2_algo_supported(int algo, int n, int d, int dv, int chunk, int dtype, int masked);
+
 /* ---------------------------------------------------------------------------
  * hla2_chunk_summaries — the summary of every chunk of `chunk` tokens with a
  * zero carry-in: the (+)-product of its token segments (Sec. 4.2, Rem.

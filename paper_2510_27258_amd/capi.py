@@ -27,6 +27,7 @@ _SIGS = {
     "hla2_state_floats": (_Z, [_I, _I]),
     "hla2_workspace_bytes": (_Z, [_I] * 7),
     "hla2_workspace_bytes_ex": (_Z, [_I] * 8),
+    "hla2_algo_supported": (_I, [_I] * 7),
     "hla2_forward": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
     "hla2_forward_ex": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _I, _P]),
     "hla2_chunk_summaries": (_I, [_P, _P, _P, _P] + [_I] * 7 + [_P]),
@@ -90,6 +91,10 @@ def hla2_workspace_bytes(B, H, n, d, dv, chunk, dtype):
 
 def hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, algo):
     return lib().hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, algo)
+
+
+def hla2_algo_supported(algo, n, d, dv, chunk, dtype, masked):
+    return lib().hla2_algo_supported(algo, n, d, dv, chunk, dtype, masked)
 
 
 def hla2_forward(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes, stream):

@@ -37,6 +37,11 @@ hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, f
                                   hipStream_t s);
 hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
                        int BH, int M, int d, int dv, hipStream_t s);
+// Strided form: head h's segment c is states[h*in_stride + c*F]; its prefix
+// goes to prefix[h*pre_stride + c*F] and its total to total[h*tot_stride].
+hipError_t launch_scan_strided(const float* states, const float* init, float* prefix, float* total, int BH, int M,
+                               int d, int dv, size_t in_stride, size_t pre_stride, size_t tot_stride,
+                               hipStream_t s);
 hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s);
 hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out,
                        int BH, int d, int dv, int masked, int normalized, float eps, int dtype,

@@ -24,7 +24,8 @@ static inline int scan_cols(int d, int dv) {
 
 __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, const float* __restrict__ init,
                                               float* __restrict__ prefix, float* __restrict__ total,
-                                              int BH, int M, int d, int dv, int CB, int nblk) {
+                                              int BH, int M, int d, int dv, int CB, int nblk, size_t in_stride,
+                                              size_t pre_stride, size_t tot_stride) {
   extern __shared__ float smem[];
   const int ldS = d + 4;
   float* ScT = smem;                       // [d][d+4]: ScT[a'][a] = S_c[a][a']
@@ -40,8 +41,8 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
   const int ncol = min(CB, dv - c0);
   const size_t F = state_floats(d, dv);
   const size_t oC = off_C(d, dv), om = off_m(d, dv), oG = off_G(d, dv), oh = off_h(d, dv);
-  const float* in = states + (size_t)bh * M * F;
-  float* pre = prefix + (size_t)bh * M * F;
+  const float* in = states + (size_t)bh * in_stride;
+  float* pre = prefix + (size_t)bh * pre_stride;
   const float* ini = init ? init + (size_t)bh * F : nullptr;
 
   // cross-term tile: thread -> (a-quad, j-quad)
@@ -76,7 +77,7 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
   __syncthreads();
 
   for (int c = 0; c <= M; ++c) {
-    float* dst = (c < M) ? pre + (size_t)c * F : (total ? total + (size_t)bh * F : nullptr);
+    float* dst = (c < M) ? pre + (size_t)c * F : (total ? total + (size_t)bh * tot_stride : nullptr);
     // write the exclusive prefix of segment c (or the total after the last)
     if (dst) {
       if (blk == 0) {
@@ -144,6 +145,13 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
 
 hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
                        int BH, int M, int d, int dv, hipStream_t s) {
+  const size_t F = state_floats(d, dv);
+  return launch_scan_strided(states, init, prefix, total, BH, M, d, dv, (size_t)M * F, (size_t)M * F, F, s);
+}
+
+hipError_t launch_scan_strided(const float* states, const float* init, float* prefix, float* total, int BH, int M,
+                               int d, int dv, size_t in_stride, size_t pre_stride, size_t tot_stride,
+                               hipStream_t s) {
   const int CB = scan_cols(d, dv);
   const int nblk = (dv + CB - 1) / CB;
   const int groups = (BH + 7) / 8;
@@ -151,7 +159,7 @@ hipError_t launch_scan(const float* states, const float* init, float* prefix, fl
   hipError_t e = hipFuncSetAttribute((const void*)k_scan, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_scan, dim3(groups * 8 * nblk), dim3(256), lds, s, states, init, prefix, total, BH, M, d,
-                     dv, CB, nblk);
+                     dv, CB, nblk, in_stride, pre_stride, tot_stride);
   return hipGetLastError();
 }
 

@@ -80,6 +80,13 @@ const char* hla_last_error(void) { return g_err; }
 
 size_t hla2_state_floats(int d, int dv) { return hla::state_floats(d, dv); }
 
+int hla2_algo_supported(int algo, int n, int d, int dv, int chunk, int dtype, int masked) {
+  if (check_dims(1, 1, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  if (algo == HLA_ALGO_AUTO || algo == HLA_ALGO_CHUNKED) return 1;
+  if (algo == HLA_ALGO_FUSED) return hla::fused_supported(n, d, dv, chunk, dtype, masked) ? 1 : 0;
+  return 0;
+}
+
 size_t hla2_workspace_bytes_ex(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo) {
   if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
   const int a = select_algo(algo, n, d, dv, chunk, dtype, 1);

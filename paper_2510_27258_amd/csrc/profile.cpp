@@ -27,12 +27,12 @@ void prof_start(const char* name, hipStream_t s) {
   if (!g_on || (int)g_rec.size() >= g_cap) { g_open = -1; return; }
   const int slot = (int)g_rec.size();
   g_rec.push_back({name, slot});
-  hipEventRecord(g_ev[2 * slot], s);
+  (void)hipEventRecord(g_ev[2 * slot], s);
   g_open = slot;
 }
 void prof_stop(hipStream_t s) {
   if (!g_on || g_open < 0) return;
-  hipEventRecord(g_ev[2 * g_open + 1], s);
+  (void)hipEventRecord(g_ev[2 * g_open + 1], s);
   g_open = -1;
 }
 }  // namespace hla
@@ -41,7 +41,7 @@ extern "C" {
 
 int hla_profile_begin(int max_records) {
   if (max_records < 1) return HLA_ERR_INVALID;
-  for (hipEvent_t e : g_ev) hipEventDestroy(e);
+  for (hipEvent_t e : g_ev) (void)hipEventDestroy(e);
   g_ev.assign(2 * (size_t)max_records, nullptr);
   for (auto& e : g_ev)
     if (hipEventCreate(&e) != hipSuccess) return HLA_ERR_HIP;

@@ -23,7 +23,8 @@ from tests.helpers import dev, gen, rowwise_err, tol_for
 
 pytestmark = pytest.mark.gpu
 
-ALGOS = [capi.HLA_ALGO_CHUNKED]
+ALGOS = [capi.HLA_ALGO_CHUNKED, capi.HLA_ALGO_FUSED]
+FUSED_SHAPES = [(64, 64, 64), (32, 32, 32), (64, 32, 32), (32, 64, 64), (64, 64, 32), (64, 32, 64)]
 
 
 def _say(*a):
@@ -36,7 +37,14 @@ def _oracle(q, k, v, masked, state=None):
     return num, den, fin
 
 
+def _supported(algo, n, d, dv, chunk, code, masked):
+    return bool(capi.hla2_algo_supported(algo, n, d, dv, chunk, code, masked))
+
+
 def _check_forward(B, H, n, d, dv, chunk, dist, masked, normalized, algo, seed=0, eps=1e-6):
+    code = I.HLA_BF16 if dist == "unit" else I.HLA_FP32
+    if not _supported(algo, n, d, dv, chunk, code, masked):
+        return False
     q, k, v, code = gen(B, H, n, d, dv, dist, seed)
     _say(f"case B={B} H={H} n={n} d={d} dv={dv} chunk={chunk} dist={dist} masked={masked} "
          f"normalized={normalized} algo={algo}")
@@ -48,7 +56,7 @@ def _check_forward(B, H, n, d, dv, chunk, dist, masked, normalized, algo, seed=0
     assert err <= tol, f"num row-wise error {err:.3e} > {tol}"
     if normalized:
         out = hla.forward(qd, kd, vd, chunk, masked=masked, normalized=True, eps=eps, algo=algo).cpu().numpy()
-        ones = torch.ones(B, H, n, 16, dtype=vd.dtype, device="cuda")
+        ones = torch.ones(B, H, n, dv, dtype=vd.dtype, device="cuda")
         den = hla.forward(qd, kd, ones, chunk, masked=masked, normalized=False, algo=algo)[..., 0].cpu().numpy()
         D = O.hla2_den_scale(q, k, masked=bool(masked))
         e_den = float((np.abs(den - den_ref) / D).max())
@@ -58,6 +66,7 @@ def _check_forward(B, H, n, d, dv, chunk, dist, masked, normalized, algo, seed=0
         ref = num_ref / (den_ref + eps)[..., None]
         e_out = rowwise_err(out[good], ref[good])
         assert e_out <= tol, f"normalised output error {e_out:.3e} > {tol}"
+    return True
 
 
 @pytest.mark.parametrize("algo", ALGOS)
@@ -87,6 +96,8 @@ def test_forward_normalized_small(dist, algo):
 
 @pytest.mark.parametrize("algo", ALGOS)
 def test_forward_every_chunk(algo):
+    if algo == capi.HLA_ALGO_FUSED:
+        pytest.skip("the fused path has its own shape tests")
     for chunk in (16, 32, 64, 128):
         _check_forward(1, 2, 203, 64, 64, chunk, "unit", 1, normalized=False, algo=algo)
 
@@ -95,10 +106,12 @@ def test_forward_every_chunk(algo):
 def test_bf16_d64_workload_sampled_heads(algo):
     """B4 H16 n4096 d=dv=64 bf16, chunk 64: full GPU run, 4 sampled heads vs the oracle."""
     w = I.WORKLOADS["hla2-masked-bf16-B4H16-n4096-d64-C64"]
+    if not _supported(algo, w["n"], w["d"], w["dv"], w["chunk"], I.HLA_BF16, 1):
+        pytest.skip("algorithm does not cover this shape")
     q, k, v, code = gen(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
     _say("case bf16 B4H16 n4096 d64 full size")
     out = hla.forward(dev(q, code), dev(k, code), dev(v, code), w["chunk"], masked=True, algo=algo).cpu().numpy()
-    heads = [(0, 0), (1, 5), (2, 11), (3, 15)]
+    heads = [(0, 0), (1, 5), (2, 11), (3, 15), (3, 0)]
     qs = np.stack([q[b, h] for b, h in heads])
     ks = np.stack([k[b, h] for b, h in heads])
     vs = np.stack([v[b, h] for b, h in heads])
@@ -114,6 +127,8 @@ def test_bf16_d128_normalized_workload_sampled_heads(algo):
     """B2 H32 n16384 d=dv=128 bf16, chunk 128, ratio-normalised: full GPU run,
     2 sampled heads vs the oracle (num, den and the normalised output)."""
     w = I.WORKLOADS["hla2-masked-normalized-bf16-B2H32-n16384-d128-C128"]
+    if not _supported(algo, w["n"], w["d"], w["dv"], w["chunk"], I.HLA_BF16, 1):
+        pytest.skip("algorithm does not cover this shape")
     q, k, v, code = gen(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
     _say("case bf16 B2H32 n16384 d128 normalized full size")
     qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
@@ -124,7 +139,7 @@ def test_bf16_d128_normalized_workload_sampled_heads(algo):
     qs = np.stack([q[b, h] for b, h in heads])
     ks = np.stack([k[b, h] for b, h in heads])
     vs = np.stack([v[b, h] for b, h in heads])
-    ones = torch.ones(2, 1, w["n"], 16, dtype=torch.bfloat16, device="cuda")
+    ones = torch.ones(2, 1, w["n"], w["dv"], dtype=torch.bfloat16, device="cuda")
     den = hla.forward(dev(qs[:, None], code), dev(ks[:, None], code), ones, w["chunk"], masked=True,
                       algo=algo)[:, 0, :, 0].cpu().numpy()
     num_ref, den_ref, _ = _oracle(qs, ks, vs, True)
@@ -139,6 +154,40 @@ def test_bf16_d128_normalized_workload_sampled_heads(algo):
     _say(f"num {e_num:.3e} den {e_den:.3e} out {e_out:.3e} rows kept {good.mean():.3f} "
          f"negative den {float((den_ref < 0).mean()):.3f}")
     assert e_num <= 2e-3 and e_den <= 2e-3 and e_out <= 2e-3
+
+
+# ----------------------------------------------------------------- fused path specifics
+@pytest.mark.parametrize("shape", FUSED_SHAPES)
+def test_fused_shapes(shape):
+    C, d, dv = shape
+    for (B, H, n) in ((1, 2, 5 * C + 7), (2, 3, 3 * C), (1, 1, C - 3)):
+        for normalized in (False, True):
+            assert _check_forward(B, H, n, d, dv, C, "unit", 1, normalized, capi.HLA_ALGO_FUSED, seed=n)
+
+
+@pytest.mark.parametrize("segments", [1, 2, 3, 7, 100])
+def test_fused_segment_counts(segments, monkeypatch):
+    """The result must not depend on how chunks are grouped into segments."""
+    monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
+    assert _check_forward(1, 2, 64 * 9 + 20, 64, 64, 64, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=11)
+
+
+def test_fused_matches_chunked_closely():
+    q, k, v, code = gen(2, 4, 1000, 64, 64, "unit", 21)
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    a = hla.forward(qd, kd, vd, 64, algo=capi.HLA_ALGO_FUSED).cpu().numpy()
+    b = hla.forward(qd, kd, vd, 64, algo=capi.HLA_ALGO_CHUNKED).cpu().numpy()
+    assert rowwise_err(a, b) <= 2e-3
+
+
+def test_fused_rejects_unsupported():
+    q = torch.zeros(1, 1, 64, 128, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(capi.HLAError) as ei:
+        hla.forward(q, q, q, 64, algo=capi.HLA_ALGO_FUSED)
+    assert ei.value.code == capi.HLA_ERR_UNSUPPORTED
+    qf = torch.zeros(1, 1, 64, 64, device="cuda")
+    with pytest.raises(capi.HLAError):
+        hla.forward(qf, qf, qf, 64, algo=capi.HLA_ALGO_FUSED)
 
 
 # ----------------------------------------------------------------- summaries and scan
