@@ -54,7 +54,7 @@ def kernel_costs(w, P=None):
                      tok * 2 * (3 * C * d + C * dv + 2 * d * d + 2 * d * dv)),
             "walk_summary": ("hbm", sum_tok * qkv_tok + BH * (P - 1) * F * 4,
                              sum_tok * 2 * (2 * C * d + 2 * d * d + 2 * d * dv)),
-            "flip": ("hbm", 2 * BH * P * F * 4, BH * P * 2 * (d * d * dv + d * d)),
+            "carry": ("hbm", 2 * BH * P * F * 4, BH * P * 4 * (d * d * dv + d * d)),
             "scan": ("hbm", 2 * BH * max(P - 1, 1) * F * 4, BH * max(P - 1, 1) * 2 * (d * d * dv + d * d)),
         })
     return costs
@@ -136,6 +136,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--algo", default="auto", choices=["auto", "chunked", "fused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run --steps device-to-device copies of this many bytes (counter calibration)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -145,6 +147,15 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_bytes:
+        src = torch.ones(args.copy_bytes // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": args.copy_bytes, "steps": args.steps}))
+        return
 
     import paper_2510_27258_amd as hla
     from paper_2510_27258_amd import capi

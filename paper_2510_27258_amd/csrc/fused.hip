@@ -5,10 +5,10 @@
 //   1. k_walk<SUMMARY>: each workgroup walks one segment from a zero carry and
 //      produces its summary (S, C, m, Phi, eta) with Phi = S C - G and
 //      eta = S m - h (an exact change of variables of the 5-tuple).
-//   2. k_flip turns summaries into the paper's 5-tuples (G = S C - Phi,
-//      h = S m - eta); k_scan (hla2_scan.hip) takes the exclusive
-//      semidirect-product scan over segments, Eq. (semidirect); k_flip turns
-//      the carries back (Phi0 = S0 C0 - G0, eta0 = S0 m0 - h0).
+//   2. k_carry takes the exclusive semidirect-product scan over the segments
+//      of each head on the paper's 5-tuples, Eq. (semidirect), reading the
+//      summaries through G = S C - Phi, h = S m - eta and writing each carry
+//      back as (S0, Phi0 = S0 C0 - G0, eta0 = S0 m0 - h0).
 //   3. k_walk<OUTPUT>: each workgroup walks one segment again from its carry
 //      and writes the outputs.
 //
@@ -28,10 +28,10 @@
 // lo = bf16(x - hi); the product with an exact bf16 partner is taken as two
 // MFMAs, so the operand keeps ~16 significant bits.  Accumulation is fp32.
 //
-// Layout: 256 threads = 4 waves.  Wave w owns the 16-column tiles
-// {w, w+4, ...} of S0, R (over d) and of Phi0, O (over dv); S0 and Phi0 stay
-// in MFMA accumulators for the whole walk and are fed back as MFMA B
-// operands straight from registers.  Q, K, K^T, V^T, W/T, R and R^T are
+// Layout: 512 threads = 8 waves.  Wave w owns the 16-column tiles
+// {w%4, w%4+4, ...} of S0, R (over d) and of Phi0, O (over dv), and half of
+// the token tiles of R and O; S0 and Phi0 stay in MFMA accumulators for the
+// whole walk and are fed back as MFMA B operands straight from registers.  Q, K, K^T, V^T, W/T, R and R^T are
 // staged in LDS as bf16.
 #include "fused.h"
 #include "profile.h"
@@ -43,7 +43,8 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint16_t u16x4;
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
+constexpr int kColWaves = 4;              // waves that split the state columns
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPad = 8;   // bf16 elements of padding per LDS row
 
@@ -140,13 +141,16 @@ struct Cfg {
   static constexpr int oRth = oRl + (SUMMARY ? 0 : C * ldR);
   static constexpr int oRtl = oRth + D * ldRt;
   static constexpr int oQt = oRtl + D * ldRt;
-  static constexpr int n16 = oQt + (SUMMARY ? D * ldQt : 0);          // bf16 elements
-  static constexpr int f_eta = 0, f_cs = D, f_den = 2 * D, f_denp = 2 * D + C;   // fp32 region
-  static constexpr int nf32 = 2 * D + C + (C / 16) * C;
-  static constexpr size_t bytes = (size_t)n16 * 2 + (size_t)nf32 * 4 + 16;
+  static constexpr int n16 = oQt + (SUMMARY ? D * ldQt : 0);          // bf16 elements of tiles
+  // the output walk folds its carry in fp32 scratch that reuses the tile region
+  static constexpr int fold_f = SUMMARY ? 0 : 2 * D * (D + 2) + 2 * D * DV + 2 * D;
+  static constexpr int n16t = (n16 > 2 * fold_f ? n16 : 2 * fold_f);
+  static constexpr int f_eta = 0, f_cs = D, f_den = 3 * D, f_denp = 3 * D + C;   // fp32 region
+  static constexpr int nf32 = 3 * D + C + (C / 16) * C;
+  static constexpr size_t bytes = (size_t)((n16t + 7) & ~7) * 2 + (size_t)nf32 * 4;
   static constexpr int RT = C / 16;                  // token tiles
-  static constexpr int SA = (D / 16 + kWaves - 1) / kWaves;   // column tiles of S0/R per wave
-  static constexpr int SB = (DV / 16 + kWaves - 1) / kWaves;  // column tiles of Phi0/O per wave
+  static constexpr int SA = (D / 16 + kColWaves - 1) / kColWaves;   // column tiles of S0/R per wave
+  static constexpr int SB = (DV / 16 + kColWaves - 1) / kColWaves;  // column tiles of Phi0/O per wave
   static constexpr int DT = D / 16;
   static constexpr int KC = C / 32, KD = D / 32;
   // global->LDS staging: 16-byte segments per operand
@@ -156,57 +160,338 @@ struct Cfg {
   static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
-// k_flip: for each record, X <- S C - X and y <- S m - y (both directions of
-// Phi = S C - G, eta = S m - h).  One workgroup per (record, 32 columns).
-// Records: head h, record i < per_head at src[(h*src_hs + i)*F] and
-// dst[(h*dst_hs + i)*F].  In place (src == dst) is allowed.
-__global__ __launch_bounds__(256) void k_flip(const float* src, float* dst, int per_head, int src_hs, int dst_hs,
-                                              int d, int dv) {
+// k_carry: the carries of all segments of a head, by the exclusive
+// semidirect-product scan of Eq. (semidirect) over the paper's 5-tuples,
+// with the conversions to and from the walk's (S, Phi, eta) form folded in.
+//   acc = init (or E); for s < nsum:
+//     car[s]  = (S_acc, C_acc, m_acc, S_acc C_acc - G_acc, S_acc m_acc - h_acc)
+//     seg s arrives as (S_s, C_s, m_s, Phi_s, eta_s); its G_s = S_s C_s - Phi_s,
+//     acc (+)= seg:  G_acc += G_s + S_s C_acc = S_s (C_s + C_acc) - Phi_s + G_acc
+//                    h_acc += S_s (m_s + m_acc) - eta_s + ...,  S, C, m add.
+//   after the loop: car[nsum] (when nsum < P) in walk form, or the total in
+//   5-tuple form to `fin`.
+// One workgroup per (head, block of CB value columns); a head's blocks share
+// an XCD.  Every workgroup keeps its own S_acc (registers, 64 per thread at
+// d = 128) because every column block needs all of it.
+template <int d, int dv, int CB>
+__global__ __launch_bounds__(256) void k_carry(const float* __restrict__ segs, const float* __restrict__ init,
+                                               float* __restrict__ car, float* __restrict__ fin, int BH, int nsum,
+                                               int P) {
+  constexpr int nblk = (dv + CB - 1) / CB;
   extern __shared__ float sm[];
-  const int rec = blockIdx.x, blk = blockIdx.y, tid = threadIdx.x;
+  const int ldS = d + 4;
+  float* XT = sm;                 // [d][d+4]  transposed S_acc or S_s
+  float* Cacc = XT + d * ldS;     // [d][CB]
+  float* Ybuf = Cacc + d * CB;    // [d][CB]
+  float* macc = Ybuf + d * CB;    // [d]
+  float* mbuf = macc + d;         // [d]
+  const int tid = threadIdx.x;
+  const int L = blockIdx.x;
+  const int group = L / (8 * nblk), within = L % (8 * nblk);
+  const int bh = group * 8 + within % 8, blk = within / 8;
+  if (bh >= BH) return;
+  const int c0 = blk * CB, ncol = min(CB, dv - c0);
   const size_t F = state_floats(d, dv);
-  const int hh = rec / per_head, ii = rec % per_head;
-  const float* s = src + ((size_t)hh * src_hs + ii) * F;
-  float* o = dst + ((size_t)hh * dst_hs + ii) * F;
-  const int c0 = blk * 32, nc = min(32, dv - c0);
-  float* Cs = sm;                       // [d][32]
-  for (int idx = tid; idx < d * 32; idx += 256) {
-    const int a = idx / 32, j = idx % 32;
-    Cs[idx] = j < nc ? s[off_C(d, dv) + (size_t)a * dv + c0 + j] : 0.f;
+  const size_t oC = off_C(d, dv), om = off_m(d, dv), oG = off_G(d, dv), oh = off_h(d, dv);
+  const float* ini = init ? init + (size_t)bh * F : nullptr;
+  const int nj4 = CB / 4, jq = tid % nj4, aq = tid / nj4;
+  const bool active = (aq * 4 < d) && (jq * 4 < ncol);
+  constexpr int nS = (d * d + 255) / 256;
+  float sacc[nS];
+  float gacc[4][4];
+  float hacc = 0.f;
+#pragma unroll
+  for (int r = 0; r < nS; ++r) {
+    const int idx = tid + 256 * r;
+    sacc[r] = (ini && idx < d * d) ? ini[idx] : 0.f;
   }
-  __syncthreads();
-  for (int idx = tid; idx < d * nc; idx += 256) {
-    const int a = idx / nc, j = idx % nc;
-    float acc = 0.f;
-    for (int b = 0; b < d; ++b) acc += s[(size_t)a * d + b] * Cs[b * 32 + j];
-    o[off_G(d, dv) + (size_t)a * dv + c0 + j] = acc - s[off_G(d, dv) + (size_t)a * dv + c0 + j];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      gacc[i][j] = (ini && active) ? ini[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j] : 0.f;
+#pragma unroll
+  for (int idx = tid; idx < d * CB; idx += 256) {
+    const int a = idx / CB, j = idx % CB;
+    Cacc[idx] = (ini && j < ncol) ? ini[oC + (size_t)a * dv + c0 + j] : 0.f;
   }
-  if (blk == 0) {
-    for (int a = tid; a < d; a += 256) {
-      float acc = 0.f;
-      for (int b = 0; b < d; ++b) acc += s[(size_t)a * d + b] * s[off_m(d, dv) + b];
-      o[off_h(d, dv) + a] = acc - s[off_h(d, dv) + a];
+  for (int a = tid; a < d; a += 256) macc[a] = ini ? ini[om + a] : 0.f;
+  if (tid < d && ini) hacc = ini[oh + tid];
+
+  // out[i][j] = sum_a' X[a0+i][a'] Y[a'][j0+j] with X staged transposed in XT
+  auto product = [&](const float* Y, float acc[4][4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+#pragma unroll 8
+    for (int ap = 0; ap < d; ++ap) {
+      const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldS + aq * 4]);
+      const float4 y4 = *reinterpret_cast<const float4*>(&Y[ap * CB + jq * 4]);
+      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, yv[4] = {y4.x, y4.y, y4.z, y4.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += xv[i] * yv[j];
     }
-    if (src != dst) {
-      for (size_t idx = tid; idx < (size_t)d * d; idx += 256) o[idx] = s[idx];
-      for (int idx = tid; idx < d; idx += 256) o[off_m(d, dv) + idx] = s[off_m(d, dv) + idx];
+  };
+  auto stage_sacc = [&]() {
+#pragma unroll
+    for (int r = 0; r < nS; ++r) {
+      const int idx = tid + 256 * r;
+      if (idx < d * d) XT[(idx % d) * ldS + idx / d] = sacc[r];
+    }
+  };
+  // write the acc state in walk form to dst (S, C, m copied; Phi, eta converted)
+  auto write_walk_form = [&](float* dst) {
+    __syncthreads();
+    stage_sacc();
+    __syncthreads();
+    if (active) {
+      float pr[4][4];
+      product(Cacc, pr);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          dst[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j] = pr[i][j] - gacc[i][j];
+    }
+#pragma unroll
+    for (int idx = tid; idx < d * CB; idx += 256) {
+      const int a = idx / CB, j = idx % CB;
+      if (j < ncol) dst[oC + (size_t)a * dv + c0 + j] = Cacc[idx];
+    }
+    if (blk == 0) {
+#pragma unroll
+      for (int r = 0; r < nS; ++r) {
+        const int idx = tid + 256 * r;
+        if (idx < d * d) dst[idx] = sacc[r];
+      }
+      if (tid < d) {
+        float e = 0.f;
+#pragma unroll 8
+        for (int ap = 0; ap < d; ++ap) e += XT[ap * ldS + tid] * macc[ap];
+        dst[om + tid] = macc[tid];
+        dst[oh + tid] = e - hacc;
+      }
+    }
+  };
+
+  for (int sg = 0; sg < nsum; ++sg) {
+    if (car) write_walk_form(car + ((size_t)bh * P + sg) * F);
+    const float* x = segs + ((size_t)bh * P + sg) * F;
+    __syncthreads();
+    {
+      // issue every global load of the segment before its first use
+      constexpr int nSS = (d * d + 255) / 256, nCC = (d * CB + 255) / 256;
+      float sv[nSS], cv[nCC];
+#pragma unroll
+      for (int r = 0; r < nSS; ++r) {
+        const int idx = tid + 256 * r;
+        sv[r] = idx < d * d ? x[idx] : 0.f;
+      }
+#pragma unroll
+      for (int r = 0; r < nCC; ++r) {
+        const int idx = tid + 256 * r, a = idx / CB, j = idx % CB;
+        cv[r] = (idx < d * CB && j < ncol) ? x[oC + (size_t)a * dv + c0 + j] : 0.f;
+      }
+      const float mv = tid < d ? x[om + tid] : 0.f;
+#pragma unroll
+      for (int r = 0; r < nSS; ++r) {
+        const int idx = tid + 256 * r;
+        if (idx < d * d) XT[(idx % d) * ldS + idx / d] = sv[r];
+      }
+#pragma unroll
+      for (int r = 0; r < nCC; ++r) {
+        const int idx = tid + 256 * r;
+        if (idx < d * CB) Ybuf[idx] = Cacc[idx] + cv[r];
+      }
+      if (tid < d) mbuf[tid] = macc[tid] + mv;
+    }
+    __syncthreads();
+    if (active) {
+      float phi[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) phi[i][j] = x[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j];
+      float pr[4][4];
+      product(Ybuf, pr);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) gacc[i][j] += pr[i][j] - phi[i][j];
+    }
+    if (tid < d) {
+      const float eta_s = x[oh + tid];
+      float e = 0.f;
+#pragma unroll 8
+      for (int ap = 0; ap < d; ++ap) e += XT[ap * ldS + tid] * mbuf[ap];
+      hacc += e - eta_s;
+    }
+#pragma unroll
+    for (int r = 0; r < nS; ++r) {
+      const int idx = tid + 256 * r;
+      if (idx < d * d) sacc[r] += XT[(idx % d) * ldS + idx / d];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int idx = tid; idx < d * CB; idx += 256) Cacc[idx] = Ybuf[idx];
+    if (tid < d) macc[tid] = mbuf[tid];
+  }
+  if (car && nsum < P) write_walk_form(car + ((size_t)bh * P + nsum) * F);
+  if (fin) {
+    float* dst = fin + (size_t)bh * F;
+    __syncthreads();
+    if (active)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dst[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j] = gacc[i][j];
+#pragma unroll
+    for (int idx = tid; idx < d * CB; idx += 256) {
+      const int a = idx / CB, j = idx % CB;
+      if (j < ncol) dst[oC + (size_t)a * dv + c0 + j] = Cacc[idx];
+    }
+    if (blk == 0) {
+#pragma unroll
+      for (int r = 0; r < nS; ++r) {
+        const int idx = tid + 256 * r;
+        if (idx < d * d) dst[idx] = sacc[r];
+      }
+      if (tid < d) {
+        dst[om + tid] = macc[tid];
+        dst[oh + tid] = hacc;
+      }
     }
   }
-  if (src != dst)
-    for (int idx = tid; idx < d * nc; idx += 256) {
-      const int a = idx / nc, j = idx % nc;
-      o[off_C(d, dv) + (size_t)a * dv + c0 + j] = s[off_C(d, dv) + (size_t)a * dv + c0 + j];
-    }
 }
 
-// One segment walk.  grid = (segments, BH).  SUMMARY: zero carry, writes the
-// segment summary (S, C, m, Phi, eta) to `rec`.  !SUMMARY: reads the carry
-// (S0, ., ., Phi0, eta0) from `rec` (NULL = zero) and writes outputs.
+// Carry of segment `seg` of head bh, folded by the workgroup itself:
+//   acc = init (+) seg_0 (+) ... (+) seg_{seg-1}     (Eq. (semidirect) on 5-tuples)
+// where segment summaries arrive as (S, C, m, Phi, eta) and G_s = S_s C_s -
+// Phi_s, h_s = S_s m_s - eta_s, so the cross term S_s C_acc and G_s combine
+// into one product: G_acc += S_s (C_s + C_acc) - Phi_s.  The carry is then
+// converted once: Phi0 = S_acc C_acc - G_acc, eta0 = S_acc m_acc - h_acc.
+// S matrices are kept transposed in LDS ([a'][a], row length D+2) so a thread
+// reads the two rows of its 2 x 4 output block as one 8-byte load.
+// Results: S_acc^T in `Sout`, Phi0 in `Pout` [D][DV], eta0 in `eout`.
+template <int D, int DV>
+__device__ void fold_carry(const float* __restrict__ segs, const float* __restrict__ init, int bh, int seg,
+                           int nseg, float* sc, float*& Sout, float*& Pout, float* eout) {
+  constexpr int ldT = D + 2;
+  constexpr int NB4 = DV / 4;                   // column quads
+  constexpr int NT = (D / 2) * NB4;             // threads with a 2 x 4 output block
+  static_assert(NT <= kThreads, "product split");
+  const size_t F = state_floats(D, DV);
+  float* SaccT = sc;                  // [D][D+2]
+  float* SsT = SaccT + D * ldT;       // [D][D+2]
+  float* Cacc = SsT + D * ldT;        // [D][DV]
+  float* Y = Cacc + D * DV;           // [D][DV]
+  float* macc = Y + D * DV;           // [D]
+  float* y = macc + D;                // [D]
+  const int tid = threadIdx.x;
+  const bool act = tid < NT;
+  const int a0 = act ? 2 * (tid / NB4) : 0, b0 = 4 * (tid % NB4);
+  const float* ini = init ? init + (size_t)bh * F : nullptr;
+  float g[2][4];
+  float h = 0.f;
+  for (int idx = tid; idx < D * D; idx += kThreads) SaccT[(idx % D) * ldT + idx / D] = ini ? ini[idx] : 0.f;
+  for (int idx = tid; idx < D * DV; idx += kThreads) Cacc[idx] = ini ? ini[off_C(D, DV) + idx] : 0.f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) g[i][j] = (ini && act) ? ini[off_G(D, DV) + (size_t)(a0 + i) * DV + b0 + j] : 0.f;
+  if (tid < D) {
+    macc[tid] = ini ? ini[off_m(D, DV) + tid] : 0.f;
+    h = ini ? ini[off_h(D, DV) + tid] : 0.f;
+  }
+  // out[i][j] = sum_a' X[a0+i][a'] Z[a'][b0+j] with X^T in XT
+  auto prod = [&](const float* XT, const float* Z, float o[2][4]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[i][j] = 0.f;
+#pragma unroll 8
+    for (int ap = 0; ap < D; ++ap) {
+      const float2 x2 = *reinterpret_cast<const float2*>(&XT[ap * ldT + a0]);
+      const float4 z4 = *reinterpret_cast<const float4*>(&Z[ap * DV + b0]);
+      const float xv[2] = {x2.x, x2.y}, zv[4] = {z4.x, z4.y, z4.z, z4.w};
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[i][j] += xv[i] * zv[j];
+    }
+  };
+  for (int sp = 0; sp < seg; ++sp) {
+    const float* x = segs + ((size_t)bh * nseg + sp) * F;
+    float phi[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) phi[i][j] = act ? x[off_G(D, DV) + (size_t)(a0 + i) * DV + b0 + j] : 0.f;
+    const float eta_s = tid < D ? x[off_h(D, DV) + tid] : 0.f;
+    __syncthreads();
+    for (int idx = tid; idx < D * D; idx += kThreads) SsT[(idx % D) * ldT + idx / D] = x[idx];
+    for (int idx = tid; idx < D * DV; idx += kThreads) Y[idx] = Cacc[idx] + x[off_C(D, DV) + idx];
+    if (tid < D) y[tid] = macc[tid] + x[off_m(D, DV) + tid];
+    __syncthreads();
+    if (act) {
+      float o[2][4];
+      prod(SsT, Y, o);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) g[i][j] += o[i][j] - phi[i][j];
+    }
+    if (tid < D) {
+      float acc = 0.f;
+#pragma unroll 8
+      for (int ap = 0; ap < D; ++ap) acc += SsT[ap * ldT + tid] * y[ap];
+      h += acc - eta_s;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < D * D; idx += kThreads) {
+      const int o = (idx / D) * ldT + idx % D;
+      SaccT[o] += SsT[o];
+    }
+    for (int idx = tid; idx < D * DV; idx += kThreads) Cacc[idx] = Y[idx];
+    if (tid < D) macc[tid] = y[tid];
+  }
+  __syncthreads();
+  // Phi0 = S_acc C_acc - G_acc (into Y), eta0 = S_acc m_acc - h_acc
+  if (act) {
+    float o[2][4];
+    prod(SaccT, Cacc, o);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Y[(a0 + i) * DV + b0 + j] = o[i][j] - g[i][j];
+  }
+  if (tid < D) {
+    float acc = 0.f;
+#pragma unroll 8
+    for (int ap = 0; ap < D; ++ap) acc += SaccT[ap * ldT + tid] * macc[ap];
+    eout[tid] = acc - h;
+  }
+  __syncthreads();
+  Sout = SaccT;
+  Pout = Y;
+}
+
+// One segment walk.  grid = (segments, BH), 8 waves.  Wave w owns column
+// tile ct = w % 4 (+4, +8, ... when d or dv > 64) of S0/R and of Phi0/O, and
+// the row half rh = w / 4 of the token tiles of R and O.  Both row halves keep
+// a full copy of the S0/Phi0 columns they own (the carry updates are done by
+// both), so every B operand taken from the carry stays in registers.
+// SUMMARY: zero carry, writes the segment summary (S, C, m, Phi, eta) to
+// `rec`.  !SUMMARY: reads the carry (S0, ., ., Phi0, eta0) from `rec` (NULL =
+// zero) and writes outputs.
 template <int C, int D, int DV, bool SUMMARY>
 __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v, float* __restrict__ out,
-                                                      float* __restrict__ rec, int n, int cps, int nseg,
-                                                      int normalized, float eps) {
+                                                      float* __restrict__ rec, const float* __restrict__ init, int n,
+                                                      int cps, int nseg, int normalized, float eps) {
   using G = Cfg<C, D, DV, SUMMARY>;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
@@ -220,18 +505,20 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
   uint16_t* Rth = lds + G::oRth;
   uint16_t* Rtl = lds + G::oRtl;
   uint16_t* Qt = lds + G::oQt;
-  float* fl = reinterpret_cast<float*>(lds + ((G::n16 + 7) & ~7));
+  float* fl = reinterpret_cast<float*>(lds + ((G::n16t + 7) & ~7));
   float* eta = fl + G::f_eta;
-  float* colsum = fl + G::f_cs;
+  float* colsum = fl + G::f_cs;       // [2][D]: per row half
   float* den = fl + G::f_den;
   float* denp = fl + G::f_denp;
 
   const int seg = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const int ct = w % kColWaves, rh = w / kColWaves;
+  constexpr int RH = G::RT / 2;                // token tiles per row half
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t F = state_floats(D, DV);
-  float* rc = rec ? rec + ((size_t)bh * nseg + seg) * F : nullptr;
+  float* rc = SUMMARY ? rec + ((size_t)bh * nseg + seg) * F : nullptr;
 
   // ---- carry in (fp32 accumulators) ----
   f32x4 S0[G::SA][G::DT];
@@ -240,25 +527,40 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
 #pragma unroll
   for (int sa = 0; sa < G::SA; ++sa)
 #pragma unroll
-    for (int rt = 0; rt < G::DT; ++rt) {
-      const int at = w + kWaves * sa;
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
-      if (!SUMMARY && rc && at < G::DT)
-        for (int j = 0; j < 4; ++j) x[j] = rc[(size_t)(rt * 16 + 4 * lg + j) * D + at * 16 + lr];
-      S0[sa][rt] = x;
-    }
+    for (int rt = 0; rt < G::DT; ++rt) S0[sa][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int sb = 0; sb < G::SB; ++sb)
 #pragma unroll
     for (int rt = 0; rt < G::DT; ++rt) {
-      const int bt = w + kWaves * sb;
-      f32x4 x = {0.f, 0.f, 0.f, 0.f};
-      if (!SUMMARY && rc && bt * 16 < DV)
-        for (int j = 0; j < 4; ++j) x[j] = rc[off_G(D, DV) + (size_t)(rt * 16 + 4 * lg + j) * DV + bt * 16 + lr];
-      P0[sb][rt] = x;
+      P0[sb][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
       if (SUMMARY) Cs[SUMMARY ? sb : 0][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-  for (int a = tid; a < D; a += kThreads) eta[a] = (!SUMMARY && rc) ? rc[off_h(D, DV) + a] : 0.f;
+  for (int a = tid; a < D; a += kThreads) eta[a] = 0.f;
+  if (!SUMMARY && (seg > 0 || init)) {
+    // the tile region of LDS is free until the first chunk is staged
+    float* Sc;
+    float* Pc;
+    fold_carry<D, DV>(rec, init, bh, seg, nseg, reinterpret_cast<float*>(lds), Sc, Pc, eta);
+#pragma unroll
+    for (int sa = 0; sa < G::SA; ++sa) {
+      const int at = ct + kColWaves * sa;
+      if (at >= G::DT) break;
+#pragma unroll
+      for (int rt = 0; rt < G::DT; ++rt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) S0[sa][rt][j] = Sc[(at * 16 + lr) * (D + 2) + rt * 16 + 4 * lg + j];
+    }
+#pragma unroll
+    for (int sb = 0; sb < G::SB; ++sb) {
+      const int bt = ct + kColWaves * sb;
+      if (bt * 16 >= DV) break;
+#pragma unroll
+      for (int rt = 0; rt < G::DT; ++rt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) P0[sb][rt][j] = Pc[(rt * 16 + 4 * lg + j) * DV + bt * 16 + lr];
+    }
+    __syncthreads();
+  }
   float m_acc = 0.f;   // SUMMARY: column sum of Q for column tid (< D)
 
   // ---- prefetch registers for the next chunk ----
@@ -268,7 +570,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + kThreads * i;
-      const int t = e / (D / 8), a8 = (e % (D / 8)) * 8;
+      const int t = e % C, a8 = (e / C) * 8;     // consecutive lanes take consecutive tokens
       uint4 zq = make_uint4(0, 0, 0, 0), zk = zq;
       if (e < G::segQ && t0 + t < n) {
         const size_t off = ((size_t)bh * n + t0 + t) * D + a8;
@@ -281,7 +583,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + kThreads * i;
-      const int t = e / (DV / 8), b8 = (e % (DV / 8)) * 8;
+      const int t = e % C, b8 = (e / C) * 8;
       uint4 zv = make_uint4(0, 0, 0, 0);
       if (e < G::segV && t0 + t < n) zv = *reinterpret_cast<const uint4*>(v + ((size_t)bh * n + t0 + t) * DV + b8);
       pv[i] = zv;
@@ -296,7 +598,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + kThreads * i;
       if (e < G::segQ) {
-        const int t = e / (D / 8), a8 = (e % (D / 8)) * 8;
+        const int t = e % C, a8 = (e / C) * 8;
         *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
         *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
         const uint16_t* kk = reinterpret_cast<const uint16_t*>(&pk[i]);
@@ -313,7 +615,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + kThreads * i;
       if (e < G::segV) {
-        const int t = e / (DV / 8), b8 = (e % (DV / 8)) * 8;
+        const int t = e % C, b8 = (e / C) * 8;
         const uint16_t* vv = reinterpret_cast<const uint16_t*>(&pv[i]);
 #pragma unroll
         for (int j = 0; j < 8; ++j) Vt[(b8 + j) * G::ldVt + t] = vv[j];
@@ -325,41 +627,39 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
       for (int t = 0; t < C; ++t) m_acc += bf16_to_f(Qs[t * G::ldQ + tid]);
 
     // ---- stage 1: W = L (.) Q K^T, computed as W^T = K Q^T and stored transposed ----
-    for (int it = w; it < G::RT; it += kWaves) {
-      f32x4 acc[G::RT];
-#pragma unroll
-      for (int jt = 0; jt < G::RT; ++jt) acc[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < G::KD; ++s) {
-        const bf16x8 a = frag(Ks, G::ldK, it * 16, s * 32);
-#pragma unroll
-        for (int jt = 0; jt < G::RT; ++jt) acc[jt] = mfma(a, frag(Qs, G::ldQ, jt * 16, s * 32), acc[jt]);
+    for (int tile = w; tile < G::RT * G::RT; tile += kWaves) {
+      const int it = tile % G::RT, jt = tile / G::RT;
+      if (it > jt) {          // tile entirely above the diagonal of W^T (key after query): zero
+        store_T(f32x4{0.f, 0.f, 0.f, 0.f}, Wh, Wl, G::ldW, it * 16, jt * 16);
+        continue;
       }
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int jt = 0; jt < G::RT; ++jt) {
+      for (int s = 0; s < G::KD; ++s) acc = mfma(frag(Ks, G::ldK, it * 16, s * 32), frag(Qs, G::ldQ, jt * 16, s * 32), acc);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)   // keep key i <= query t
-          if (it * 16 + 4 * lg + j > jt * 16 + lr) acc[jt][j] = 0.f;
-        store_T(acc[jt], Wh, Wl, G::ldW, it * 16, jt * 16);
-      }
+      for (int j = 0; j < 4; ++j)   // keep key i <= query t
+        if (it * 16 + 4 * lg + j > jt * 16 + lr) acc[j] = 0.f;
+      store_T(acc, Wh, Wl, G::ldW, it * 16, jt * 16);
     }
     __syncthreads();
 
-    // ---- stage 2: R = W K + Q S0 (old S0), then S0 += K^T K ----
+    // ---- stage 2: R = W K + Q S0 (old S0) on this wave's row half; S0 += K^T K ----
 #pragma unroll
     for (int sa = 0; sa < G::SA; ++sa) {
-      const int at = w + kWaves * sa;
+      const int at = ct + kColWaves * sa;
       if (at >= G::DT) break;
-      f32x4 racc[G::RT];
+      f32x4 racc[RH];
 #pragma unroll
-      for (int rt = 0; rt < G::RT; ++rt) racc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int r = 0; r < RH; ++r) racc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
         const bf16x8 bK = frag(Kt, G::ldKt, at * 16, s * 32);
 #pragma unroll
-        for (int rt = 0; rt < G::RT; ++rt) {
-          racc[rt] = mfma(frag(Wh, G::ldW, rt * 16, s * 32), bK, racc[rt]);
-          racc[rt] = mfma(frag(Wl, G::ldW, rt * 16, s * 32), bK, racc[rt]);
+        for (int r = 0; r < RH; ++r) {
+          const int rt = rh * RH + r;
+          if (s * 32 > rt * 16 + 15) continue;   // W row tile rt has no keys at or beyond s*32
+          racc[r] = mfma(frag(Wh, G::ldW, rt * 16, s * 32), bK, racc[r]);
+          racc[r] = mfma(frag(Wl, G::ldW, rt * 16, s * 32), bK, racc[r]);
         }
       }
 #pragma unroll
@@ -367,10 +667,10 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
         bf16x8 bh, bl;
         frag_from_acc(S0[sa][2 * s], S0[sa][2 * s + 1], bh, bl);
 #pragma unroll
-        for (int rt = 0; rt < G::RT; ++rt) {
-          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 16, s * 32);
-          racc[rt] = mfma(aQ, bh, racc[rt]);
-          racc[rt] = mfma(aQ, bl, racc[rt]);
+        for (int r = 0; r < RH; ++r) {
+          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, (rh * RH + r) * 16, s * 32);
+          racc[r] = mfma(aQ, bh, racc[r]);
+          racc[r] = mfma(aQ, bl, racc[r]);
         }
       }
 #pragma unroll
@@ -379,52 +679,49 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
 #pragma unroll
         for (int rt = 0; rt < G::DT; ++rt) S0[sa][rt] = mfma(frag(Kt, G::ldKt, rt * 16, s * 32), bK, S0[sa][rt]);
       }
-      // eta advance: column sums of R (applied after the readout has used the old eta)
+      // eta advance: column sums of R over this row half
       float cs = 0.f;
 #pragma unroll
-      for (int rt = 0; rt < G::RT; ++rt) cs += racc[rt][0] + racc[rt][1] + racc[rt][2] + racc[rt][3];
+      for (int r = 0; r < RH; ++r) cs += racc[r][0] + racc[r][1] + racc[r][2] + racc[r][3];
       cs += __shfl_xor(cs, 16);
       cs += __shfl_xor(cs, 32);
-      if (lg == 0) colsum[at * 16 + lr] = cs;
+      if (lg == 0) colsum[rh * D + at * 16 + lr] = cs;
 #pragma unroll
-      for (int rt = 0; rt < G::RT; ++rt) {
-        store_T(racc[rt], Rth, Rtl, G::ldRt, rt * 16, at * 16);
-        if (!SUMMARY) store_N(racc[rt], Rh, Rl, G::ldR, rt * 16, at * 16);
+      for (int r = 0; r < RH; ++r) {
+        const int rt = rh * RH + r;
+        store_T(racc[r], Rth, Rtl, G::ldRt, rt * 16, at * 16);
+        if (!SUMMARY) store_N(racc[r], Rh, Rl, G::ldR, rt * 16, at * 16);
       }
     }
     __syncthreads();
-    float eta_add = (tid < D) ? colsum[tid] : 0.f;
+    const float eta_add = (tid < D) ? colsum[tid] + colsum[D + tid] : 0.f;
 
     if (!SUMMARY) {
       // ---- stage 3: T = L (.) Q R^T, computed as T^T = R Q^T, stored transposed into the W buffers ----
-      for (int it = w; it < G::RT; it += kWaves) {
-        f32x4 acc[G::RT];
-#pragma unroll
-        for (int jt = 0; jt < G::RT; ++jt) acc[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int tile = w; tile < G::RT * G::RT; tile += kWaves) {
+        const int it = tile % G::RT, jt = tile / G::RT;
+        if (it > jt) {
+          store_T(f32x4{0.f, 0.f, 0.f, 0.f}, Wh, Wl, G::ldW, it * 16, jt * 16);
+          if (lg == 0) denp[it * C + jt * 16 + lr] = 0.f;
+          continue;
+        }
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < G::KD; ++s) {
-          const bf16x8 ah = frag(Rh, G::ldR, it * 16, s * 32);
-          const bf16x8 al = frag(Rl, G::ldR, it * 16, s * 32);
-#pragma unroll
-          for (int jt = 0; jt < G::RT; ++jt) {
-            const bf16x8 b = frag(Qs, G::ldQ, jt * 16, s * 32);
-            acc[jt] = mfma(ah, b, acc[jt]);
-            acc[jt] = mfma(al, b, acc[jt]);
-          }
+          const bf16x8 b = frag(Qs, G::ldQ, jt * 16, s * 32);
+          acc = mfma(frag(Rh, G::ldR, it * 16, s * 32), b, acc);
+          acc = mfma(frag(Rl, G::ldR, it * 16, s * 32), b, acc);
         }
+        float ps = 0.f;
 #pragma unroll
-        for (int jt = 0; jt < G::RT; ++jt) {
-          float ps = 0.f;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {     // keep j <= t
-            if (it * 16 + 4 * lg + j > jt * 16 + lr) acc[jt][j] = 0.f;
-            ps += acc[jt][j];
-          }
-          ps += __shfl_xor(ps, 16);
-          ps += __shfl_xor(ps, 32);
-          if (lg == 0) denp[it * C + jt * 16 + lr] = ps;
-          store_T(acc[jt], Wh, Wl, G::ldW, it * 16, jt * 16);
+        for (int j = 0; j < 4; ++j) {     // keep j <= t
+          if (it * 16 + 4 * lg + j > jt * 16 + lr) acc[j] = 0.f;
+          ps += acc[j];
         }
+        ps += __shfl_xor(ps, 16);
+        ps += __shfl_xor(ps, 32);
+        if (lg == 0) denp[it * C + jt * 16 + lr] = ps;
+        store_T(acc, Wh, Wl, G::ldW, it * 16, jt * 16);
       }
       __syncthreads();
       // den_t = sum_j T[t][j] + q_t . eta0
@@ -432,24 +729,26 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
         float s = 0.f;
         for (int it = 0; it < G::RT; ++it) s += denp[it * C + tid];
         for (int a = 0; a < D; ++a) s += bf16_to_f(Qs[tid * G::ldQ + a]) * eta[a];
-        den[tid] = s;
+        den[tid] = 1.f / (s + eps);
       }
       __syncthreads();
       // ---- stage 4: O = T V + Q Phi0 (old Phi0); stage 5: Phi0 += R^T V ----
 #pragma unroll
       for (int sb = 0; sb < G::SB; ++sb) {
-        const int bt = w + kWaves * sb;
+        const int bt = ct + kColWaves * sb;
         if (bt * 16 >= DV) break;
-        f32x4 oacc[G::RT];
+        f32x4 oacc[RH];
 #pragma unroll
-        for (int rt = 0; rt < G::RT; ++rt) oacc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int r = 0; r < RH; ++r) oacc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < G::KC; ++s) {
           const bf16x8 bV = frag(Vt, G::ldVt, bt * 16, s * 32);
 #pragma unroll
-          for (int rt = 0; rt < G::RT; ++rt) {
-            oacc[rt] = mfma(frag(Wh, G::ldW, rt * 16, s * 32), bV, oacc[rt]);
-            oacc[rt] = mfma(frag(Wl, G::ldW, rt * 16, s * 32), bV, oacc[rt]);
+          for (int r = 0; r < RH; ++r) {
+            const int rt = rh * RH + r;
+            if (s * 32 > rt * 16 + 15) continue;   // T row tile rt has no j at or beyond s*32
+            oacc[r] = mfma(frag(Wh, G::ldW, rt * 16, s * 32), bV, oacc[r]);
+            oacc[r] = mfma(frag(Wl, G::ldW, rt * 16, s * 32), bV, oacc[r]);
           }
         }
 #pragma unroll
@@ -457,20 +756,20 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
           bf16x8 bh, bl;
           frag_from_acc(P0[sb][2 * s], P0[sb][2 * s + 1], bh, bl);
 #pragma unroll
-          for (int rt = 0; rt < G::RT; ++rt) {
-            const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 16, s * 32);
-            oacc[rt] = mfma(aQ, bh, oacc[rt]);
-            oacc[rt] = mfma(aQ, bl, oacc[rt]);
+          for (int r = 0; r < RH; ++r) {
+            const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, (rh * RH + r) * 16, s * 32);
+            oacc[r] = mfma(aQ, bh, oacc[r]);
+            oacc[r] = mfma(aQ, bl, oacc[r]);
           }
         }
 #pragma unroll
-        for (int rt = 0; rt < G::RT; ++rt)
+        for (int r = 0; r < RH; ++r)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int t = rt * 16 + 4 * lg + j;
+            const int t = (rh * RH + r) * 16 + 4 * lg + j;
             if (t0 + t < n) {
-              float o = oacc[rt][j];
-              if (normalized) o = o / (den[t] + eps);
+              float o = oacc[r][j];
+              if (normalized) o *= den[t];
               out[((size_t)bh * n + t0 + t) * DV + bt * 16 + lr] = o;
             }
           }
@@ -488,7 +787,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
       // summaries: Phi += R^T V and C += Q^T V
 #pragma unroll
       for (int sb = 0; sb < G::SB; ++sb) {
-        const int bt = w + kWaves * sb;
+        const int bt = ct + kColWaves * sb;
         if (bt * 16 >= DV) break;
 #pragma unroll
         for (int s = 0; s < G::KC; ++s) {
@@ -506,12 +805,11 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
     if (tid < D) eta[tid] += eta_add;
   }
 
-  if (SUMMARY) {
+  if (SUMMARY && rh == 0) {
     // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
-    __syncthreads();
 #pragma unroll
     for (int sa = 0; sa < G::SA; ++sa) {
-      const int at = w + kWaves * sa;
+      const int at = ct + kColWaves * sa;
       if (at >= G::DT) break;
 #pragma unroll
       for (int rt = 0; rt < G::DT; ++rt)
@@ -519,7 +817,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
     }
 #pragma unroll
     for (int sb = 0; sb < G::SB; ++sb) {
-      const int bt = w + kWaves * sb;
+      const int bt = ct + kColWaves * sb;
       if (bt * 16 >= DV) break;
 #pragma unroll
       for (int rt = 0; rt < G::DT; ++rt)
@@ -529,6 +827,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
           rc[off_C(D, DV) + e] = Cs[SUMMARY ? sb : 0][rt][j];
         }
     }
+  }
+  if (SUMMARY) {
+    __syncthreads();
     if (tid < D) {
       rc[off_m(D, DV) + tid] = m_acc;
       rc[off_h(D, DV) + tid] = eta[tid];
@@ -547,13 +848,10 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   const size_t F = state_floats(D, DV);
   const int BH = f.BH;
   float* segs = reinterpret_cast<float*>(ws);                    // [BH][P][F] segment summaries
-  float* car = segs + (size_t)BH * P * F;                        // [BH][P][F] carries
   const uint16_t* q = static_cast<const uint16_t*>(f.q);
   const uint16_t* k = static_cast<const uint16_t*>(f.k);
   const uint16_t* v = static_cast<const uint16_t*>(f.v);
   const int nsum = final_state ? P : P - 1;                      // segments whose summary is needed
-  const dim3 fblk((DV + 31) / 32);
-  const size_t flds = sizeof(float) * D * 32;
   hipError_t e;
   if (nsum > 0) {
     auto ks = k_walk<C, D, DV, true>;
@@ -561,43 +859,35 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     if ((e = hipFuncSetAttribute((const void*)ks, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lb)) != hipSuccess)
       return e;
     prof_start("walk_summary", s);
-    hipLaunchKernelGGL(ks, dim3(nsum, BH), dim3(kThreads), lb, s, q, k, v, (float*)nullptr, segs, f.n, cps, P, 0,
-                       0.f);
+    hipLaunchKernelGGL(ks, dim3(nsum, BH), dim3(kThreads), lb, s, q, k, v, (float*)nullptr, segs,
+                       (const float*)nullptr, f.n, cps, P, 0, 0.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    prof_start("flip", s);
-    hipLaunchKernelGGL(k_flip, dim3(BH * nsum, fblk.x), dim3(256), flds, s, segs, segs, nsum, P, P, D, DV);
+  }
+  const bool want_out = f.out != nullptr;
+  if (final_state) {
+    // total state after all P segments: the semidirect-product fold in k_carry
+    constexpr int CB = (4096 / D < DV) ? 4096 / D : DV;
+    constexpr int nblk = (DV + CB - 1) / CB;
+    const size_t lds = sizeof(float) * ((size_t)D * (D + 4) + 2 * (size_t)D * CB + 2 * D);
+    auto kc = k_carry<D, DV, CB>;
+    if ((e = hipFuncSetAttribute((const void*)kc, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
+        hipSuccess)
+      return e;
+    prof_start("carry", s);
+    hipLaunchKernelGGL(kc, dim3(((BH + 7) / 8) * 8 * nblk), dim3(256), lds, s, segs, init, (float*)nullptr,
+                       final_state, BH, nsum, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // carries: prefix of segment c at car[c]; the total goes to the final
-    // state, or (when only P-1 summaries exist) is the carry of segment P-1
-    prof_start("scan", s);
-    if (final_state)
-      e = launch_scan_strided(segs, init, car, final_state, BH, nsum, D, DV, (size_t)P * F, (size_t)P * F, F, s);
-    else
-      e = launch_scan_strided(segs, init, car, car + (size_t)(P - 1) * F, BH, nsum, D, DV, (size_t)P * F,
-                              (size_t)P * F, (size_t)P * F, s);
-    prof_stop(s);
-    if (e != hipSuccess) return e;
   }
-  if (!f.out) return hipSuccess;
-  if (nsum > 0) {
-    prof_start("flip", s);
-    hipLaunchKernelGGL(k_flip, dim3(BH * P, fblk.x), dim3(256), flds, s, car, car, P, P, P, D, DV);
-    prof_stop(s);
-  } else if (init) {
-    prof_start("flip", s);
-    hipLaunchKernelGGL(k_flip, dim3(BH, fblk.x), dim3(256), flds, s, init, car, 1, 1, P, D, DV);
-    prof_stop(s);
-  }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (!want_out) return hipSuccess;
   auto kw = k_walk<C, D, DV, false>;
   const size_t lb = Cfg<C, D, DV, false>::bytes;
   if ((e = hipFuncSetAttribute((const void*)kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lb)) != hipSuccess)
     return e;
   prof_start("walk", s);
-  hipLaunchKernelGGL(kw, dim3(P, BH), dim3(kThreads), lb, s, q, k, v, f.out,
-                     (nsum > 0 || init) ? car : (float*)nullptr, f.n, cps, P, f.normalized, f.eps);
+  hipLaunchKernelGGL(kw, dim3(P, BH), dim3(kThreads), lb, s, q, k, v, f.out, segs, init, f.n, cps, P,
+                     f.normalized, f.eps);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -624,7 +914,7 @@ bool fused_supported(int n, int d, int dv, int chunk, int dtype, int masked) {
 size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
   int P, cps;
   fused_plan(BH, n, chunk, &P, &cps);
-  return 2 * sizeof(float) * (size_t)BH * P * state_floats(d, dv) + 256;
+  return sizeof(float) * (size_t)BH * P * state_floats(d, dv) + 256;
 }
 
 hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, void* workspace, hipStream_t s) {
