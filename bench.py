@@ -63,7 +63,7 @@ def kernel_costs(w, P=None):
 def fused_segments(BH, n, C):
     """Segments per head chosen by the library for the fused path (same rule as fused_plan)."""
     M = -(-n // C)
-    p = int(os.environ.get("HLA_FUSED_SEGMENTS", 256 // BH))
+    p = int(os.environ.get("HLA_FUSED_SEGMENTS", 512 // BH))
     p = max(1, min(p, M))
     cps = -(-M // p)
     return -(-M // cps)

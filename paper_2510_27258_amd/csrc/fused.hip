@@ -5,12 +5,13 @@
 //   1. k_walk<SUMMARY>: each workgroup walks one segment from a zero carry and
 //      produces its summary (S, C, m, Phi, eta) with Phi = S C - G and
 //      eta = S m - h (an exact change of variables of the 5-tuple).
-//   2. k_carry takes the exclusive semidirect-product scan over the segments
-//      of each head on the paper's 5-tuples, Eq. (semidirect), reading the
-//      summaries through G = S C - Phi, h = S m - eta and writing each carry
-//      back as (S0, Phi0 = S0 C0 - G0, eta0 = S0 m0 - h0).
-//   3. k_walk<OUTPUT>: each workgroup walks one segment again from its carry
-//      and writes the outputs.
+//   2. k_seg_cross: the semidirect product of Eq. (semidirect) across
+//      segments in reduce-then-scan form: each segment's contribution
+//      G_s + S_s C_{<s} (and h_s + S_s m_{<s}) is computed in parallel.
+//   3. k_walk<OUTPUT>: each workgroup sums the contributions before its
+//      segment into its carry (fold_sum), converts it once to (S0, Phi0, eta0),
+//      walks its chunks from that carry and writes the outputs.
+//   k_total sums all contributions into the total state when a caller needs it.
 //
 // Per chunk (tokens of the chunk as the rows of Q, K, V; S0, Phi0, eta0 the
 // carry of the chunk), with r_j = S_j q_j (the proof of Thm. 1 sums
@@ -28,11 +29,13 @@
 // lo = bf16(x - hi); the product with an exact bf16 partner is taken as two
 // MFMAs, so the operand keeps ~16 significant bits.  Accumulation is fp32.
 //
-// Layout: 512 threads = 8 waves.  Wave w owns the 16-column tiles
-// {w%4, w%4+4, ...} of S0, R (over d) and of Phi0, O (over dv), and half of
-// the token tiles of R and O; S0 and Phi0 stay in MFMA accumulators for the
-// whole walk and are fed back as MFMA B operands straight from registers.  Q, K, K^T, V^T, W/T, R and R^T are
-// staged in LDS as bf16.
+// Layout: 256 threads = 4 waves on v_mfma_f32_32x32x16_bf16.  Every product
+// of a chunk is at most 2 x 2 tiles of 32 x 32; wave w owns output tile
+// (row w/2, column w%2).  The wave owning column c of R (or O) keeps the whole
+// column c of S0 (or Phi0) in MFMA accumulators for the whole walk and feeds
+// it back as the B operand straight from registers (both row waves of a
+// column keep a copy).  Q, K, K^T, V^T, W/T, R and R^T are staged in LDS as
+// bf16.
 #include "fused.h"
 #include "profile.h"
 
@@ -40,11 +43,9 @@ namespace hla {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((ext_vector_type(4))) uint16_t u16x4;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
 
-constexpr int kWaves = 8;
-constexpr int kColWaves = 4;              // waves that split the state columns
+constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPad = 8;   // bf16 elements of padding per LDS row
 
@@ -57,70 +58,74 @@ __device__ __forceinline__ void split(float x, uint16_t& hi, uint16_t& lo) {
   hi = bf16_bits(h);
   lo = bf16_bits((__bf16)(x - (float)h));
 }
+__device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) { return a | (uint32_t)b << 16; }
 
-__device__ __forceinline__ f32x4 mfma(const bf16x8& a, const bf16x8& b, const f32x4& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+// Lane layout of v_mfma_f32_32x32x16_bf16 (l = lane, r = l % 32, g = l / 32):
+//   A: row r, k = 8g .. 8g+7;  B: column r, the same k (any k order shared by
+//   A and B gives the same product);  D: element e is D[8(e/4) + 4g + e%4][r].
+__device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) z[e] = 0.f;
+  return z;
+}
+__device__ __forceinline__ int acc_row(int e, int g) { return 8 * (e >> 2) + 4 * g + (e & 3); }
 
-// Operand fragment from a row-major bf16 LDS tile X[row][k]: lane (r = l%16,
-// g = l/16) takes X[row0 + r][k0 + 8g .. 8g+7].  It is the A operand of X Y
-// (rows of X = rows of the result) and the B operand of Z X^T (rows of X =
-// columns of the result); both operands of a product use the same k order.
+// Operand fragment from a row-major bf16 LDS tile X[row][k]: lane takes
+// X[row0 + r][k0 + 8g .. 8g+7].  A operand of X Y, or B operand of Z X^T.
 __device__ __forceinline__ bf16x8 frag(const uint16_t* X, int ld, int row0, int k0) {
   const int l = threadIdx.x & 63;
-  const uint16_t* p = X + (row0 + (l & 15)) * ld + k0 + 8 * (l >> 4);
+  const uint16_t* p = X + (row0 + (l & 31)) * ld + k0 + 8 * (l >> 5);
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 }
 
-// Same, with the k order of accumulator-fed operands: lane takes
-// X[row0 + r][k0 + 4g .. 4g+3] and X[row0 + r][k0 + 16 + 4g .. +3].
+// Same, in the k order of an accumulator-fed partner: lane takes
+// X[row0 + r][k0 + 4g .. 4g+3] and X[row0 + r][k0 + 8 + 4g .. 8+4g+3].
 __device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int row0, int k0) {
   const int l = threadIdx.x & 63;
-  const uint16_t* p = X + (row0 + (l & 15)) * ld + k0 + 4 * (l >> 4);
+  const uint16_t* p = X + (row0 + (l & 31)) * ld + k0 + 4 * (l >> 5);
   const uint2 a = *reinterpret_cast<const uint2*>(p);
-  const uint2 b = *reinterpret_cast<const uint2*>(p + 16);
+  const uint2 b = *reinterpret_cast<const uint2*>(p + 8);
   return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
 }
 
-// B operand from two fp32 accumulator tiles holding Y[k0 .. k0+15][n0..] and
-// Y[k0+16 .. k0+31][n0..] (lane holds rows 4g..4g+3 of column r of each),
-// split into hi and lo parts.  Pairs with frag_acc_order.
-__device__ __forceinline__ void frag_from_acc(const f32x4& t0, const f32x4& t1, bf16x8& hi, bf16x8& lo) {
-  uint16_t h[8], o[8];
+// B operand for k rows 16h .. 16h+15 of an accumulator tile Y (32 rows): the
+// lane's elements 8h .. 8h+7 are rows 16h + {4g..4g+3, 8+4g..8+4g+3} of its
+// column, matching frag_acc_order.  Split into hi and lo parts.
+__device__ __forceinline__ void frag_from_acc(const f32x16& t, int h, bf16x8& hi, bf16x8& lo) {
+  uint16_t a[8], b[8];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    split(t0[j], h[j], o[j]);
-    split(t1[j], h[4 + j], o[4 + j]);
+  for (int i = 0; i < 8; ++i) split(t[8 * h + i], a[i], b[i]);
+  hi = __builtin_bit_cast(bf16x8, make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(a[4], a[5]), pack2(a[6], a[7])));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(pack2(b[0], b[1]), pack2(b[2], b[3]), pack2(b[4], b[5]), pack2(b[6], b[7])));
+}
+
+// Store an accumulator tile D[row0 + i][col0 + r] transposed as X[col0 + r][row0 + i],
+// split into hi/lo tiles (four 8-byte stores each).
+__device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
+  const int l = threadIdx.x & 63, g = l >> 5;
+  const int base = (col0 + (l & 31)) * ld + row0 + 4 * g;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint16_t h[4], o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) split(acc[4 * q + j], h[j], o[j]);
+    *reinterpret_cast<uint2*>(Xh + base + 8 * q) = make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
+    *reinterpret_cast<uint2*>(Xl + base + 8 * q) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
   }
-  uint4 hv, ov;
-  hv.x = h[0] | (uint32_t)h[1] << 16; hv.y = h[2] | (uint32_t)h[3] << 16;
-  hv.z = h[4] | (uint32_t)h[5] << 16; hv.w = h[6] | (uint32_t)h[7] << 16;
-  ov.x = o[0] | (uint32_t)o[1] << 16; ov.y = o[2] | (uint32_t)o[3] << 16;
-  ov.z = o[4] | (uint32_t)o[5] << 16; ov.w = o[6] | (uint32_t)o[7] << 16;
-  hi = __builtin_bit_cast(bf16x8, hv);
-  lo = __builtin_bit_cast(bf16x8, ov);
 }
 
-// Store an accumulator tile D[row0 + 4g + j][col0 + r] transposed, as
-// X[col0 + r][row0 + 4g + j], split into hi/lo tiles (8-byte stores).
-__device__ __forceinline__ void store_T(const f32x4& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
-  const int l = threadIdx.x & 63;
-  uint16_t h[4], o[4];
+// Store an accumulator tile row-major as X[row0 + i][col0 + r], hi/lo.
+__device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
+  const int l = threadIdx.x & 63, g = l >> 5;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) split(acc[j], h[j], o[j]);
-  const int off = (col0 + (l & 15)) * ld + row0 + 4 * (l >> 4);
-  *reinterpret_cast<uint2*>(Xh + off) = make_uint2(h[0] | (uint32_t)h[1] << 16, h[2] | (uint32_t)h[3] << 16);
-  *reinterpret_cast<uint2*>(Xl + off) = make_uint2(o[0] | (uint32_t)o[1] << 16, o[2] | (uint32_t)o[3] << 16);
-}
-
-// Store an accumulator tile row-major as X[row0 + 4g + j][col0 + r], hi/lo.
-__device__ __forceinline__ void store_N(const f32x4& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
-  const int l = threadIdx.x & 63;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int e = 0; e < 16; ++e) {
     uint16_t h, o;
-    split(acc[j], h, o);
-    const int off = (row0 + 4 * (l >> 4) + j) * ld + col0 + (l & 15);
+    split(acc[e], h, o);
+    const int off = (row0 + acc_row(e, g)) * ld + col0 + (l & 31);
     Xh[off] = h;
     Xl[off] = o;
   }
@@ -128,367 +133,237 @@ __device__ __forceinline__ void store_N(const f32x4& acc, uint16_t* Xh, uint16_t
 
 template <int C, int D, int DV, bool SUMMARY>
 struct Cfg {
+  // Two reused buffers: B1 holds W, then R^T (after a barrier); B2 holds R,
+  // then T (after a barrier).  Summaries use only B1 and add Q^T.
+  static constexpr int CD = C > D ? C : D;
   static constexpr int ldQ = D + kPad, ldK = D + kPad, ldKt = C + kPad, ldVt = C + kPad;
-  static constexpr int ldW = C + kPad, ldR = D + kPad, ldRt = C + kPad, ldQt = C + kPad;
+  static constexpr int ld1 = C + kPad, ld2 = CD + kPad, ldQt = C + kPad;
+  static constexpr int ldW = ld1, ldRt = ld1, ldR = ld2, ldT = ld2;
   static constexpr int oQ = 0;
   static constexpr int oK = oQ + C * ldQ;
   static constexpr int oKt = oK + C * ldK;
   static constexpr int oVt = oKt + D * ldKt;
-  static constexpr int oWh = oVt + DV * ldVt;
-  static constexpr int oWl = oWh + C * ldW;
-  static constexpr int oRh = oWl + C * ldW;
-  static constexpr int oRl = oRh + (SUMMARY ? 0 : C * ldR);
-  static constexpr int oRth = oRl + (SUMMARY ? 0 : C * ldR);
-  static constexpr int oRtl = oRth + D * ldRt;
-  static constexpr int oQt = oRtl + D * ldRt;
+  static constexpr int oB1h = oVt + DV * ldVt;
+  static constexpr int oB1l = oB1h + CD * ld1;
+  static constexpr int oB2h = oB1l + CD * ld1;
+  static constexpr int oB2l = oB2h + (SUMMARY ? 0 : C * ld2);
+  static constexpr int oQt = oB2l + (SUMMARY ? 0 : C * ld2);
   static constexpr int n16 = oQt + (SUMMARY ? D * ldQt : 0);          // bf16 elements of tiles
   // the output walk folds its carry in fp32 scratch that reuses the tile region
-  static constexpr int fold_f = SUMMARY ? 0 : 2 * D * (D + 2) + 2 * D * DV + 2 * D;
+  static constexpr int fold_f = SUMMARY ? 0 : D * (D + 4) + 2 * D * DV + D;   // fold_sum scratch
   static constexpr int n16t = (n16 > 2 * fold_f ? n16 : 2 * fold_f);
-  static constexpr int f_eta = 0, f_cs = D, f_den = 3 * D, f_denp = 3 * D + C;   // fp32 region
-  static constexpr int nf32 = 3 * D + C + (C / 16) * C;
+  static constexpr int RT = C / 32, DT = D / 32, VT = DV / 32;       // 32-wide tiles
+  static constexpr int KC = C / 16, KD = D / 16;                     // 16-deep k steps
+  static constexpr int f_eta = 0, f_cs = D, f_den = D + RT * D, f_denp = f_den + C;   // fp32 region
+  static constexpr int nf32 = f_denp + RT * C;
   static constexpr size_t bytes = (size_t)((n16t + 7) & ~7) * 2 + (size_t)nf32 * 4;
-  static constexpr int RT = C / 16;                  // token tiles
-  static constexpr int SA = (D / 16 + kColWaves - 1) / kColWaves;   // column tiles of S0/R per wave
-  static constexpr int SB = (DV / 16 + kColWaves - 1) / kColWaves;  // column tiles of Phi0/O per wave
-  static constexpr int DT = D / 16;
-  static constexpr int KC = C / 32, KD = D / 32;
   // global->LDS staging: 16-byte segments per operand
   static constexpr int segQ = C * D / 8, segV = C * DV / 8;
   static constexpr int pfQ = (segQ + kThreads - 1) / kThreads, pfV = (segV + kThreads - 1) / kThreads;
-  static_assert(C % 32 == 0 && D % 32 == 0 && DV % 16 == 0, "tile shape");
+  static_assert(C % 32 == 0 && D % 32 == 0 && DV % 32 == 0 && C <= 64 && D <= 64 && DV <= 64, "tile shape");
   static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
-// k_carry: the carries of all segments of a head, by the exclusive
-// semidirect-product scan of Eq. (semidirect) over the paper's 5-tuples,
-// with the conversions to and from the walk's (S, Phi, eta) form folded in.
-//   acc = init (or E); for s < nsum:
-//     car[s]  = (S_acc, C_acc, m_acc, S_acc C_acc - G_acc, S_acc m_acc - h_acc)
-//     seg s arrives as (S_s, C_s, m_s, Phi_s, eta_s); its G_s = S_s C_s - Phi_s,
-//     acc (+)= seg:  G_acc += G_s + S_s C_acc = S_s (C_s + C_acc) - Phi_s + G_acc
-//                    h_acc += S_s (m_s + m_acc) - eta_s + ...,  S, C, m add.
-//   after the loop: car[nsum] (when nsum < P) in walk form, or the total in
-//   5-tuple form to `fin`.
-// One workgroup per (head, block of CB value columns); a head's blocks share
-// an XCD.  Every workgroup keeps its own S_acc (registers, 64 per thread at
-// d = 128) because every column block needs all of it.
-template <int d, int dv, int CB>
-__global__ __launch_bounds__(256) void k_carry(const float* __restrict__ segs, const float* __restrict__ init,
-                                               float* __restrict__ car, float* __restrict__ fin, int BH, int nsum,
-                                               int P) {
-  constexpr int nblk = (dv + CB - 1) / CB;
+// The semidirect-product scan over segments, Eq. (semidirect), organised as
+// reduce-then-scan.  For segments A (everything before s, including the
+// initial state) and B = segment s:
+//   G_{A(+)B} = G_A + [G_B + S_B C_A],   h_{A(+)B} = h_A + [h_B + S_B m_A]
+// and S, C, m add.  The bracket depends on A only through the additive
+// prefixes C_A and m_A, so every segment's bracket is computed in parallel
+// (k_seg_cross); the carry of segment s is then a plain sum of the brackets
+// and summaries before it (fold_sum, in the output walk's prologue), and the
+// total state a plain sum of all of them (k_total).
+//
+// k_seg_cross: one workgroup per (segment s < nsum, head).  The summary of s
+// arrives as (S, C, m, Phi, eta) with Phi = S C - G, eta = S m - h, so
+//   G_s + S_s C_A = S_s (C_A + C_s) - Phi_s,  h_s + S_s m_A = S_s (m_A + m_s) - eta_s,
+// with C_A = C_init + sum_{s'<s} C_s'.  The brackets replace Phi_s and eta_s
+// in the record (in place; other workgroups read only S, C and m).
+template <int D, int DV>
+__global__ __launch_bounds__(256) void k_seg_cross(float* __restrict__ segs, const float* __restrict__ init,
+                                                   int nseg) {
+  constexpr int T = 256, ldT = D + 4, NB4 = DV / 4, NT = (D / 4) * NB4;
+  constexpr int nS4 = D * D / 4 / T, nC4 = D * DV / 4 / T;
+  static_assert(NT <= T && D * D % (4 * T) == 0 && D * DV % (4 * T) == 0, "thread split");
   extern __shared__ float sm[];
-  const int ldS = d + 4;
-  float* XT = sm;                 // [d][d+4]  transposed S_acc or S_s
-  float* Cacc = XT + d * ldS;     // [d][CB]
-  float* Ybuf = Cacc + d * CB;    // [d][CB]
-  float* macc = Ybuf + d * CB;    // [d]
-  float* mbuf = macc + d;         // [d]
-  const int tid = threadIdx.x;
-  const int L = blockIdx.x;
-  const int group = L / (8 * nblk), within = L % (8 * nblk);
-  const int bh = group * 8 + within % 8, blk = within / 8;
-  if (bh >= BH) return;
-  const int c0 = blk * CB, ncol = min(CB, dv - c0);
-  const size_t F = state_floats(d, dv);
-  const size_t oC = off_C(d, dv), om = off_m(d, dv), oG = off_G(d, dv), oh = off_h(d, dv);
+  float* XT = sm;                 // [D][D+4]  S_s^T
+  float* Y = XT + D * ldT;        // [D][DV]   C_A + C_s
+  float* y = Y + D * DV;          // [D]       m_A + m_s
+  const int s = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const size_t F = state_floats(D, DV);
+  float* x = segs + ((size_t)bh * nseg + s) * F;
   const float* ini = init ? init + (size_t)bh * F : nullptr;
-  const int nj4 = CB / 4, jq = tid % nj4, aq = tid / nj4;
-  const bool active = (aq * 4 < d) && (jq * 4 < ncol);
-  constexpr int nS = (d * d + 255) / 256;
-  float sacc[nS];
-  float gacc[4][4];
-  float hacc = 0.f;
+  const bool act = tid < NT;
+  const int a0 = act ? 4 * (tid / NB4) : 0, b0 = 4 * (tid % NB4);
+  // issue every load first: S_s, Phi_s block, eta_s, then C and m of segments <= s
+  float4 sv[nS4], pv[4], cs[nC4];
+  float ev = 0.f, ms = 0.f;
 #pragma unroll
-  for (int r = 0; r < nS; ++r) {
-    const int idx = tid + 256 * r;
-    sacc[r] = (ini && idx < d * d) ? ini[idx] : 0.f;
-  }
+  for (int r = 0; r < nS4; ++r) sv[r] = reinterpret_cast<const float4*>(x)[tid + T * r];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
+    pv[i] = act ? *reinterpret_cast<const float4*>(x + off_G(D, DV) + (size_t)(a0 + i) * DV + b0)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+  if (tid < D) ev = x[off_h(D, DV) + tid];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      gacc[i][j] = (ini && active) ? ini[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j] : 0.f;
+  for (int r = 0; r < nC4; ++r)
+    cs[r] = ini ? reinterpret_cast<const float4*>(ini + off_C(D, DV))[tid + T * r] : make_float4(0.f, 0.f, 0.f, 0.f);
+  if (tid < D && ini) ms = ini[off_m(D, DV) + tid];
+  for (int sp = 0; sp <= s; ++sp) {
+    const float* xp = segs + ((size_t)bh * nseg + sp) * F;
 #pragma unroll
-  for (int idx = tid; idx < d * CB; idx += 256) {
-    const int a = idx / CB, j = idx % CB;
-    Cacc[idx] = (ini && j < ncol) ? ini[oC + (size_t)a * dv + c0 + j] : 0.f;
+    for (int r = 0; r < nC4; ++r) {
+      const float4 c4 = reinterpret_cast<const float4*>(xp + off_C(D, DV))[tid + T * r];
+      cs[r].x += c4.x; cs[r].y += c4.y; cs[r].z += c4.z; cs[r].w += c4.w;
+    }
+    if (tid < D) ms += xp[off_m(D, DV) + tid];
   }
-  for (int a = tid; a < d; a += 256) macc[a] = ini ? ini[om + a] : 0.f;
-  if (tid < d && ini) hacc = ini[oh + tid];
-
-  // out[i][j] = sum_a' X[a0+i][a'] Y[a'][j0+j] with X staged transposed in XT
-  auto product = [&](const float* Y, float acc[4][4]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-#pragma unroll 8
-    for (int ap = 0; ap < d; ++ap) {
-      const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldS + aq * 4]);
-      const float4 y4 = *reinterpret_cast<const float4*>(&Y[ap * CB + jq * 4]);
-      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, yv[4] = {y4.x, y4.y, y4.z, y4.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += xv[i] * yv[j];
-    }
-  };
-  auto stage_sacc = [&]() {
-#pragma unroll
-    for (int r = 0; r < nS; ++r) {
-      const int idx = tid + 256 * r;
-      if (idx < d * d) XT[(idx % d) * ldS + idx / d] = sacc[r];
-    }
-  };
-  // write the acc state in walk form to dst (S, C, m copied; Phi, eta converted)
-  auto write_walk_form = [&](float* dst) {
-    __syncthreads();
-    stage_sacc();
-    __syncthreads();
-    if (active) {
-      float pr[4][4];
-      product(Cacc, pr);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          dst[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j] = pr[i][j] - gacc[i][j];
-    }
-#pragma unroll
-    for (int idx = tid; idx < d * CB; idx += 256) {
-      const int a = idx / CB, j = idx % CB;
-      if (j < ncol) dst[oC + (size_t)a * dv + c0 + j] = Cacc[idx];
-    }
-    if (blk == 0) {
-#pragma unroll
-      for (int r = 0; r < nS; ++r) {
-        const int idx = tid + 256 * r;
-        if (idx < d * d) dst[idx] = sacc[r];
-      }
-      if (tid < d) {
-        float e = 0.f;
-#pragma unroll 8
-        for (int ap = 0; ap < d; ++ap) e += XT[ap * ldS + tid] * macc[ap];
-        dst[om + tid] = macc[tid];
-        dst[oh + tid] = e - hacc;
-      }
-    }
-  };
-
-  for (int sg = 0; sg < nsum; ++sg) {
-    if (car) write_walk_form(car + ((size_t)bh * P + sg) * F);
-    const float* x = segs + ((size_t)bh * P + sg) * F;
-    __syncthreads();
-    {
-      // issue every global load of the segment before its first use
-      constexpr int nSS = (d * d + 255) / 256, nCC = (d * CB + 255) / 256;
-      float sv[nSS], cv[nCC];
-#pragma unroll
-      for (int r = 0; r < nSS; ++r) {
-        const int idx = tid + 256 * r;
-        sv[r] = idx < d * d ? x[idx] : 0.f;
-      }
-#pragma unroll
-      for (int r = 0; r < nCC; ++r) {
-        const int idx = tid + 256 * r, a = idx / CB, j = idx % CB;
-        cv[r] = (idx < d * CB && j < ncol) ? x[oC + (size_t)a * dv + c0 + j] : 0.f;
-      }
-      const float mv = tid < d ? x[om + tid] : 0.f;
-#pragma unroll
-      for (int r = 0; r < nSS; ++r) {
-        const int idx = tid + 256 * r;
-        if (idx < d * d) XT[(idx % d) * ldS + idx / d] = sv[r];
-      }
-#pragma unroll
-      for (int r = 0; r < nCC; ++r) {
-        const int idx = tid + 256 * r;
-        if (idx < d * CB) Ybuf[idx] = Cacc[idx] + cv[r];
-      }
-      if (tid < d) mbuf[tid] = macc[tid] + mv;
-    }
-    __syncthreads();
-    if (active) {
-      float phi[4][4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) phi[i][j] = x[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j];
-      float pr[4][4];
-      product(Ybuf, pr);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) gacc[i][j] += pr[i][j] - phi[i][j];
-    }
-    if (tid < d) {
-      const float eta_s = x[oh + tid];
-      float e = 0.f;
-#pragma unroll 8
-      for (int ap = 0; ap < d; ++ap) e += XT[ap * ldS + tid] * mbuf[ap];
-      hacc += e - eta_s;
-    }
-#pragma unroll
-    for (int r = 0; r < nS; ++r) {
-      const int idx = tid + 256 * r;
-      if (idx < d * d) sacc[r] += XT[(idx % d) * ldS + idx / d];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int idx = tid; idx < d * CB; idx += 256) Cacc[idx] = Ybuf[idx];
-    if (tid < d) macc[tid] = mbuf[tid];
+  for (int r = 0; r < nS4; ++r) {
+    const int e4 = tid + T * r, a = (4 * e4) / D, ap = (4 * e4) % D;
+    XT[(ap + 0) * ldT + a] = sv[r].x;
+    XT[(ap + 1) * ldT + a] = sv[r].y;
+    XT[(ap + 2) * ldT + a] = sv[r].z;
+    XT[(ap + 3) * ldT + a] = sv[r].w;
   }
-  if (car && nsum < P) write_walk_form(car + ((size_t)bh * P + nsum) * F);
-  if (fin) {
-    float* dst = fin + (size_t)bh * F;
-    __syncthreads();
-    if (active)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dst[oG + (size_t)(aq * 4 + i) * dv + c0 + jq * 4 + j] = gacc[i][j];
-#pragma unroll
-    for (int idx = tid; idx < d * CB; idx += 256) {
-      const int a = idx / CB, j = idx % CB;
-      if (j < ncol) dst[oC + (size_t)a * dv + c0 + j] = Cacc[idx];
-    }
-    if (blk == 0) {
-#pragma unroll
-      for (int r = 0; r < nS; ++r) {
-        const int idx = tid + 256 * r;
-        if (idx < d * d) dst[idx] = sacc[r];
-      }
-      if (tid < d) {
-        dst[om + tid] = macc[tid];
-        dst[oh + tid] = hacc;
-      }
-    }
-  }
-}
-
-// Carry of segment `seg` of head bh, folded by the workgroup itself:
-//   acc = init (+) seg_0 (+) ... (+) seg_{seg-1}     (Eq. (semidirect) on 5-tuples)
-// where segment summaries arrive as (S, C, m, Phi, eta) and G_s = S_s C_s -
-// Phi_s, h_s = S_s m_s - eta_s, so the cross term S_s C_acc and G_s combine
-// into one product: G_acc += S_s (C_s + C_acc) - Phi_s.  The carry is then
-// converted once: Phi0 = S_acc C_acc - G_acc, eta0 = S_acc m_acc - h_acc.
-// S matrices are kept transposed in LDS ([a'][a], row length D+2) so a thread
-// reads the two rows of its 2 x 4 output block as one 8-byte load.
-// Results: S_acc^T in `Sout`, Phi0 in `Pout` [D][DV], eta0 in `eout`.
-template <int D, int DV>
-__device__ void fold_carry(const float* __restrict__ segs, const float* __restrict__ init, int bh, int seg,
-                           int nseg, float* sc, float*& Sout, float*& Pout, float* eout) {
-  constexpr int ldT = D + 2;
-  constexpr int NB4 = DV / 4;                   // column quads
-  constexpr int NT = (D / 2) * NB4;             // threads with a 2 x 4 output block
-  static_assert(NT <= kThreads, "product split");
-  const size_t F = state_floats(D, DV);
-  float* SaccT = sc;                  // [D][D+2]
-  float* SsT = SaccT + D * ldT;       // [D][D+2]
-  float* Cacc = SsT + D * ldT;        // [D][DV]
-  float* Y = Cacc + D * DV;           // [D][DV]
-  float* macc = Y + D * DV;           // [D]
-  float* y = macc + D;                // [D]
-  const int tid = threadIdx.x;
-  const bool act = tid < NT;
-  const int a0 = act ? 2 * (tid / NB4) : 0, b0 = 4 * (tid % NB4);
-  const float* ini = init ? init + (size_t)bh * F : nullptr;
-  float g[2][4];
-  float h = 0.f;
-  for (int idx = tid; idx < D * D; idx += kThreads) SaccT[(idx % D) * ldT + idx / D] = ini ? ini[idx] : 0.f;
-  for (int idx = tid; idx < D * DV; idx += kThreads) Cacc[idx] = ini ? ini[off_C(D, DV) + idx] : 0.f;
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) g[i][j] = (ini && act) ? ini[off_G(D, DV) + (size_t)(a0 + i) * DV + b0 + j] : 0.f;
-  if (tid < D) {
-    macc[tid] = ini ? ini[off_m(D, DV) + tid] : 0.f;
-    h = ini ? ini[off_h(D, DV) + tid] : 0.f;
-  }
-  // out[i][j] = sum_a' X[a0+i][a'] Z[a'][b0+j] with X^T in XT
-  auto prod = [&](const float* XT, const float* Z, float o[2][4]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) o[i][j] = 0.f;
+  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(Y)[tid + T * r] = cs[r];
+  if (tid < D) y[tid] = ms;
+  __syncthreads();
+  if (act) {
+    float o[4][4] = {};
 #pragma unroll 8
     for (int ap = 0; ap < D; ++ap) {
-      const float2 x2 = *reinterpret_cast<const float2*>(&XT[ap * ldT + a0]);
-      const float4 z4 = *reinterpret_cast<const float4*>(&Z[ap * DV + b0]);
-      const float xv[2] = {x2.x, x2.y}, zv[4] = {z4.x, z4.y, z4.z, z4.w};
+      const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldT + a0]);
+      const float4 z4 = *reinterpret_cast<const float4*>(&Y[ap * DV + b0]);
+      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, zv[4] = {z4.x, z4.y, z4.z, z4.w};
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) o[i][j] += xv[i] * zv[j];
     }
-  };
-  for (int sp = 0; sp < seg; ++sp) {
-    const float* x = segs + ((size_t)bh * nseg + sp) * F;
-    float phi[2][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) phi[i][j] = act ? x[off_G(D, DV) + (size_t)(a0 + i) * DV + b0 + j] : 0.f;
-    const float eta_s = tid < D ? x[off_h(D, DV) + tid] : 0.f;
-    __syncthreads();
-    for (int idx = tid; idx < D * D; idx += kThreads) SsT[(idx % D) * ldT + idx / D] = x[idx];
-    for (int idx = tid; idx < D * DV; idx += kThreads) Y[idx] = Cacc[idx] + x[off_C(D, DV) + idx];
-    if (tid < D) y[tid] = macc[tid] + x[off_m(D, DV) + tid];
-    __syncthreads();
-    if (act) {
-      float o[2][4];
-      prod(SsT, Y, o);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) g[i][j] += o[i][j] - phi[i][j];
-    }
-    if (tid < D) {
-      float acc = 0.f;
-#pragma unroll 8
-      for (int ap = 0; ap < D; ++ap) acc += SsT[ap * ldT + tid] * y[ap];
-      h += acc - eta_s;
-    }
-    __syncthreads();
-    for (int idx = tid; idx < D * D; idx += kThreads) {
-      const int o = (idx / D) * ldT + idx % D;
-      SaccT[o] += SsT[o];
-    }
-    for (int idx = tid; idx < D * DV; idx += kThreads) Cacc[idx] = Y[idx];
-    if (tid < D) macc[tid] = y[tid];
-  }
-  __syncthreads();
-  // Phi0 = S_acc C_acc - G_acc (into Y), eta0 = S_acc m_acc - h_acc
-  if (act) {
-    float o[2][4];
-    prod(SaccT, Cacc, o);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) Y[(a0 + i) * DV + b0 + j] = o[i][j] - g[i][j];
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<float4*>(x + off_G(D, DV) + (size_t)(a0 + i) * DV + b0) =
+          make_float4(o[i][0] - pv[i].x, o[i][1] - pv[i].y, o[i][2] - pv[i].z, o[i][3] - pv[i].w);
   }
   if (tid < D) {
     float acc = 0.f;
 #pragma unroll 8
-    for (int ap = 0; ap < D; ++ap) acc += SaccT[ap * ldT + tid] * macc[ap];
-    eout[tid] = acc - h;
+    for (int ap = 0; ap < D; ++ap) acc += XT[ap * ldT + tid] * y[ap];
+    x[off_h(D, DV) + tid] = acc - ev;
+  }
+}
+
+// k_total: the state after all nsum segments, init (+) seg_0 (+) ... : S, C,
+// m add; G and h add the brackets written by k_seg_cross.  Elementwise.
+__global__ __launch_bounds__(256) void k_total(const float* __restrict__ segs, const float* __restrict__ init,
+                                               float* __restrict__ fin, int nseg, int nsum, int F4) {
+  const int bh = blockIdx.y;
+  const size_t F = (size_t)F4 * 4;
+  for (int e4 = blockIdx.x * 256 + threadIdx.x; e4 < F4; e4 += gridDim.x * 256) {
+    float4 acc = init ? reinterpret_cast<const float4*>(init + bh * F)[e4] : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sp = 0; sp < nsum; ++sp) {
+      const float4 v = reinterpret_cast<const float4*>(segs + ((size_t)bh * nseg + sp) * F)[e4];
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    reinterpret_cast<float4*>(fin + bh * F)[e4] = acc;
+  }
+}
+
+// Carry of segment `seg` of head bh in the output walk's prologue: sum of the
+// initial state and the records of segments < seg (after k_seg_cross), then
+// Phi0 = S_acc C_acc - G_acc and eta0 = S_acc m_acc - h_acc.
+// Results: S_acc^T in `Sout` ([D][D+4]), Phi0 in `Pout` ([D][DV]), eta0 in `eout`.
+template <int D, int DV>
+__device__ void fold_sum(const float* __restrict__ segs, const float* __restrict__ init, int bh, int seg,
+                         int nseg, float* sc, float*& Sout, float*& Pout, float* eout) {
+  constexpr int ldT = D + 4, NB4 = DV / 4, NT = (D / 4) * NB4;
+  constexpr int nS4 = D * D / 4 / kThreads, nC4 = D * DV / 4 / kThreads;
+  static_assert(NT <= kThreads && D * D % (4 * kThreads) == 0 && D * DV % (4 * kThreads) == 0, "thread split");
+  const size_t F = state_floats(D, DV);
+  float* XT = sc;                     // [D][D+4]  S_acc^T
+  float* Y = XT + D * ldT;            // [D][DV]   Phi0
+  float* Cs = Y + D * DV;             // [D][DV]   C_acc
+  float* y = Cs + D * DV;             // [D]       m_acc
+  const int tid = threadIdx.x;
+  const bool act = tid < NT;
+  const int a0 = act ? 4 * (tid / NB4) : 0, b0 = 4 * (tid % NB4);
+  float4 sacc[nS4], cacc[nC4], gacc[4];
+  float macc = 0.f, hacc = 0.f;
+  auto add = [](float4& a, const float4& b) { a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w; };
+  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int r = 0; r < nS4; ++r) sacc[r] = z4;
+#pragma unroll
+  for (int r = 0; r < nC4; ++r) cacc[r] = z4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) gacc[i] = z4;
+  for (int sp = -1; sp < seg; ++sp) {
+    const float* x = sp < 0 ? (init ? init + (size_t)bh * F : nullptr) : segs + ((size_t)bh * nseg + sp) * F;
+    if (!x) continue;
+#pragma unroll
+    for (int r = 0; r < nS4; ++r) add(sacc[r], reinterpret_cast<const float4*>(x)[tid + kThreads * r]);
+#pragma unroll
+    for (int r = 0; r < nC4; ++r) add(cacc[r], reinterpret_cast<const float4*>(x + off_C(D, DV))[tid + kThreads * r]);
+    if (act)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) add(gacc[i], *reinterpret_cast<const float4*>(x + off_G(D, DV) + (size_t)(a0 + i) * DV + b0));
+    if (tid < D) {
+      macc += x[off_m(D, DV) + tid];
+      hacc += x[off_h(D, DV) + tid];
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < nS4; ++r) {
+    const int e4 = tid + kThreads * r, a = (4 * e4) / D, ap = (4 * e4) % D;
+    XT[(ap + 0) * ldT + a] = sacc[r].x;
+    XT[(ap + 1) * ldT + a] = sacc[r].y;
+    XT[(ap + 2) * ldT + a] = sacc[r].z;
+    XT[(ap + 3) * ldT + a] = sacc[r].w;
+  }
+#pragma unroll
+  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(Cs)[tid + kThreads * r] = cacc[r];
+  if (tid < D) y[tid] = macc;
+  __syncthreads();
+  if (act) {
+    float o[4][4] = {};
+#pragma unroll 8
+    for (int ap = 0; ap < D; ++ap) {
+      const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldT + a0]);
+      const float4 c4 = *reinterpret_cast<const float4*>(&Cs[ap * DV + b0]);
+      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, cv[4] = {c4.x, c4.y, c4.z, c4.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[i][j] += xv[i] * cv[j];
+    }
+    const float gv[4][4] = {{gacc[0].x, gacc[0].y, gacc[0].z, gacc[0].w}, {gacc[1].x, gacc[1].y, gacc[1].z, gacc[1].w},
+                            {gacc[2].x, gacc[2].y, gacc[2].z, gacc[2].w}, {gacc[3].x, gacc[3].y, gacc[3].z, gacc[3].w}};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Y[(a0 + i) * DV + b0 + j] = o[i][j] - gv[i][j];
+  }
+  if (tid < D) {
+    float acc = 0.f;
+#pragma unroll 8
+    for (int ap = 0; ap < D; ++ap) acc += XT[ap * ldT + tid] * y[ap];
+    eout[tid] = acc - hacc;
   }
   __syncthreads();
-  Sout = SaccT;
+  Sout = XT;
   Pout = Y;
 }
 
-// One segment walk.  grid = (segments, BH), 8 waves.  Wave w owns column
-// tile ct = w % 4 (+4, +8, ... when d or dv > 64) of S0/R and of Phi0/O, and
-// the row half rh = w / 4 of the token tiles of R and O.  Both row halves keep
-// a full copy of the S0/Phi0 columns they own (the carry updates are done by
-// both), so every B operand taken from the carry stays in registers.
+// One segment walk.  grid = (segments, BH), 4 waves.  Wave w works on output
+// tile (rt = w/2, ct = w%2) of R and of O; it keeps columns ct of S0 and of
+// Phi0 (all their rows) in accumulators.
 // SUMMARY: zero carry, writes the segment summary (S, C, m, Phi, eta) to
-// `rec`.  !SUMMARY: reads the carry (S0, ., ., Phi0, eta0) from `rec` (NULL =
-// zero) and writes outputs.
+// rec[bh][seg].  !SUMMARY: folds the carry from rec[bh][0..seg) and init,
+// then writes outputs.
 template <int C, int D, int DV, bool SUMMARY>
-__global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+__global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v, float* __restrict__ out,
                                                       float* __restrict__ rec, const float* __restrict__ init, int n,
                                                       int cps, int nseg, int normalized, float eps) {
@@ -498,67 +373,54 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
   uint16_t* Ks = lds + G::oK;
   uint16_t* Kt = lds + G::oKt;
   uint16_t* Vt = lds + G::oVt;
-  uint16_t* Wh = lds + G::oWh;   // W, later T
-  uint16_t* Wl = lds + G::oWl;
-  uint16_t* Rh = lds + G::oRh;
-  uint16_t* Rl = lds + G::oRl;
-  uint16_t* Rth = lds + G::oRth;
-  uint16_t* Rtl = lds + G::oRtl;
+  uint16_t* Wh = lds + G::oB1h;   // W, then R^T
+  uint16_t* Wl = lds + G::oB1l;
+  uint16_t* Rth = Wh;
+  uint16_t* Rtl = Wl;
+  uint16_t* Rh = lds + G::oB2h;   // R, then T
+  uint16_t* Rl = lds + G::oB2l;
+  uint16_t* Th = Rh;
+  uint16_t* Tl = Rl;
   uint16_t* Qt = lds + G::oQt;
   float* fl = reinterpret_cast<float*>(lds + ((G::n16t + 7) & ~7));
   float* eta = fl + G::f_eta;
-  float* colsum = fl + G::f_cs;       // [2][D]: per row half
-  float* den = fl + G::f_den;
-  float* denp = fl + G::f_denp;
+  float* colsum = fl + G::f_cs;       // [RT][D]
+  float* den = fl + G::f_den;         // [C]
+  float* denp = fl + G::f_denp;       // [RT][C]
 
   const int seg = blockIdx.x, bh = blockIdx.y;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
-  const int ct = w % kColWaves, rh = w / kColWaves;
-  constexpr int RH = G::RT / 2;                // token tiles per row half
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int rt = w >> 1, ct = w & 1;
+  const bool has_r = rt < G::RT && ct < G::DT;        // owns R tile (rt, ct) and S0 column ct
+  const bool has_o = rt < G::RT && ct < G::VT;        // owns O tile (rt, ct) and Phi0 column ct
+  const bool upd_p = SUMMARY ? (has_o && rt == 0) : has_o;
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t F = state_floats(D, DV);
   float* rc = SUMMARY ? rec + ((size_t)bh * nseg + seg) * F : nullptr;
 
-  // ---- carry in (fp32 accumulators) ----
-  f32x4 S0[G::SA][G::DT];
-  f32x4 P0[G::SB][G::DT];
-  f32x4 Cs[SUMMARY ? G::SB : 1][G::DT];
+  // ---- carry in (fp32 accumulators, column ct, all rows) ----
+  f32x16 S0[G::DT], P0[G::DT], Cs[SUMMARY ? G::DT : 1];
 #pragma unroll
-  for (int sa = 0; sa < G::SA; ++sa)
-#pragma unroll
-    for (int rt = 0; rt < G::DT; ++rt) S0[sa][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int sb = 0; sb < G::SB; ++sb)
-#pragma unroll
-    for (int rt = 0; rt < G::DT; ++rt) {
-      P0[sb][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (SUMMARY) Cs[SUMMARY ? sb : 0][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+  for (int i = 0; i < G::DT; ++i) {
+    S0[i] = zero16();
+    P0[i] = zero16();
+    if (SUMMARY) Cs[SUMMARY ? i : 0] = zero16();
+  }
   for (int a = tid; a < D; a += kThreads) eta[a] = 0.f;
   if (!SUMMARY && (seg > 0 || init)) {
     // the tile region of LDS is free until the first chunk is staged
     float* Sc;
     float* Pc;
-    fold_carry<D, DV>(rec, init, bh, seg, nseg, reinterpret_cast<float*>(lds), Sc, Pc, eta);
+    fold_sum<D, DV>(rec, init, bh, seg, nseg, reinterpret_cast<float*>(lds), Sc, Pc, eta);
 #pragma unroll
-    for (int sa = 0; sa < G::SA; ++sa) {
-      const int at = ct + kColWaves * sa;
-      if (at >= G::DT) break;
+    for (int i = 0; i < G::DT; ++i)
 #pragma unroll
-      for (int rt = 0; rt < G::DT; ++rt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) S0[sa][rt][j] = Sc[(at * 16 + lr) * (D + 2) + rt * 16 + 4 * lg + j];
-    }
-#pragma unroll
-    for (int sb = 0; sb < G::SB; ++sb) {
-      const int bt = ct + kColWaves * sb;
-      if (bt * 16 >= DV) break;
-#pragma unroll
-      for (int rt = 0; rt < G::DT; ++rt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) P0[sb][rt][j] = Pc[(rt * 16 + 4 * lg + j) * DV + bt * 16 + lr];
-    }
+      for (int e = 0; e < 16; ++e) {
+        const int row = i * 32 + acc_row(e, lg);
+        if (has_r) S0[i][e] = Sc[(ct * 32 + lr) * (D + 4) + row];
+        if (has_o) P0[i][e] = Pc[row * DV + ct * 32 + lr];
+      }
     __syncthreads();
   }
   float m_acc = 0.f;   // SUMMARY: column sum of Q for column tid (< D)
@@ -623,181 +485,160 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
     }
     __syncthreads();
     if (c + 1 < c_end) fetch(c + 1);
-    if (SUMMARY && tid < D)
-      for (int t = 0; t < C; ++t) m_acc += bf16_to_f(Qs[t * G::ldQ + tid]);
+    if (SUMMARY && tid < D) {
+      const uint16_t* row = Qt + tid * G::ldQt;
+#pragma unroll
+      for (int t8 = 0; t8 < C; t8 += 8) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row + t8);
+        const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m_acc += bf16_to_f(e8[j]);
+      }
+    }
 
     // ---- stage 1: W = L (.) Q K^T, computed as W^T = K Q^T and stored transposed ----
-    for (int tile = w; tile < G::RT * G::RT; tile += kWaves) {
-      const int it = tile % G::RT, jt = tile / G::RT;
-      if (it > jt) {          // tile entirely above the diagonal of W^T (key after query): zero
-        store_T(f32x4{0.f, 0.f, 0.f, 0.f}, Wh, Wl, G::ldW, it * 16, jt * 16);
-        continue;
+    {
+      const int it = w >> 1, jt = w & 1;       // key tile, query tile
+      if (it < G::RT && jt < G::RT) {
+        f32x16 acc = zero16();
+        if (it <= jt) {
+#pragma unroll
+          for (int s = 0; s < G::KD; ++s)
+            acc = mfma(frag(Ks, G::ldK, it * 32, s * 16), frag(Qs, G::ldQ, jt * 32, s * 16), acc);
+#pragma unroll
+          for (int e = 0; e < 16; ++e)   // keep key i <= query t
+            if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
+        }
+        store_T(acc, Wh, Wl, G::ldW, it * 32, jt * 32);
       }
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < G::KD; ++s) acc = mfma(frag(Ks, G::ldK, it * 16, s * 32), frag(Qs, G::ldQ, jt * 16, s * 32), acc);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)   // keep key i <= query t
-        if (it * 16 + 4 * lg + j > jt * 16 + lr) acc[j] = 0.f;
-      store_T(acc, Wh, Wl, G::ldW, it * 16, jt * 16);
     }
     __syncthreads();
 
-    // ---- stage 2: R = W K + Q S0 (old S0) on this wave's row half; S0 += K^T K ----
-#pragma unroll
-    for (int sa = 0; sa < G::SA; ++sa) {
-      const int at = ct + kColWaves * sa;
-      if (at >= G::DT) break;
-      f32x4 racc[RH];
-#pragma unroll
-      for (int r = 0; r < RH; ++r) racc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // ---- stage 2: R = W K + Q S0 (old S0) on tile (rt, ct); S0 += K^T K on column ct ----
+    f32x16 racc = zero16();
+    if (has_r) {
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
-        const bf16x8 bK = frag(Kt, G::ldKt, at * 16, s * 32);
-#pragma unroll
-        for (int r = 0; r < RH; ++r) {
-          const int rt = rh * RH + r;
-          if (s * 32 > rt * 16 + 15) continue;   // W row tile rt has no keys at or beyond s*32
-          racc[r] = mfma(frag(Wh, G::ldW, rt * 16, s * 32), bK, racc[r]);
-          racc[r] = mfma(frag(Wl, G::ldW, rt * 16, s * 32), bK, racc[r]);
-        }
+        if (s * 16 > rt * 32 + 31) break;         // keys past this row tile: W is zero
+        const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
+        racc = mfma(frag(Wh, G::ldW, rt * 32, s * 16), bK, racc);
+        racc = mfma(frag(Wl, G::ldW, rt * 32, s * 16), bK, racc);
       }
 #pragma unroll
       for (int s = 0; s < G::KD; ++s) {
         bf16x8 bh, bl;
-        frag_from_acc(S0[sa][2 * s], S0[sa][2 * s + 1], bh, bl);
-#pragma unroll
-        for (int r = 0; r < RH; ++r) {
-          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, (rh * RH + r) * 16, s * 32);
-          racc[r] = mfma(aQ, bh, racc[r]);
-          racc[r] = mfma(aQ, bl, racc[r]);
-        }
+        frag_from_acc(S0[s >> 1], s & 1, bh, bl);
+        const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, s * 16);
+        racc = mfma(aQ, bh, racc);
+        racc = mfma(aQ, bl, racc);
       }
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
-        const bf16x8 bK = frag(Kt, G::ldKt, at * 16, s * 32);
+        const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
 #pragma unroll
-        for (int rt = 0; rt < G::DT; ++rt) S0[sa][rt] = mfma(frag(Kt, G::ldKt, rt * 16, s * 32), bK, S0[sa][rt]);
+        for (int i = 0; i < G::DT; ++i) S0[i] = mfma(frag(Kt, G::ldKt, i * 32, s * 16), bK, S0[i]);
       }
-      // eta advance: column sums of R over this row half
+      // eta advance: column sums of R over this row tile
       float cs = 0.f;
 #pragma unroll
-      for (int r = 0; r < RH; ++r) cs += racc[r][0] + racc[r][1] + racc[r][2] + racc[r][3];
-      cs += __shfl_xor(cs, 16);
+      for (int e = 0; e < 16; ++e) cs += racc[e];
       cs += __shfl_xor(cs, 32);
-      if (lg == 0) colsum[rh * D + at * 16 + lr] = cs;
-#pragma unroll
-      for (int r = 0; r < RH; ++r) {
-        const int rt = rh * RH + r;
-        store_T(racc[r], Rth, Rtl, G::ldRt, rt * 16, at * 16);
-        if (!SUMMARY) store_N(racc[r], Rh, Rl, G::ldR, rt * 16, at * 16);
-      }
+      if (lg == 0) colsum[rt * D + ct * 32 + lr] = cs;
+    }
+    __syncthreads();     // every wave is done reading W: B1 takes R^T
+    if (has_r) {
+      store_T(racc, Rth, Rtl, G::ldRt, rt * 32, ct * 32);
+      if (!SUMMARY) store_N(racc, Rh, Rl, G::ldR, rt * 32, ct * 32);
     }
     __syncthreads();
-    const float eta_add = (tid < D) ? colsum[tid] + colsum[D + tid] : 0.f;
+    float eta_add = 0.f;
+    if (tid < D)
+#pragma unroll
+      for (int i = 0; i < G::RT; ++i) eta_add += colsum[i * D + tid];
 
     if (!SUMMARY) {
       // ---- stage 3: T = L (.) Q R^T, computed as T^T = R Q^T, stored transposed into the W buffers ----
-      for (int tile = w; tile < G::RT * G::RT; tile += kWaves) {
-        const int it = tile % G::RT, jt = tile / G::RT;
-        if (it > jt) {
-          store_T(f32x4{0.f, 0.f, 0.f, 0.f}, Wh, Wl, G::ldW, it * 16, jt * 16);
-          if (lg == 0) denp[it * C + jt * 16 + lr] = 0.f;
-          continue;
-        }
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      {
+        const int it = w >> 1, jt = w & 1;     // j tile, t tile
+        const bool tile = it < G::RT && jt < G::RT;
+        f32x16 acc = zero16();
+        if (tile && it <= jt) {
 #pragma unroll
-        for (int s = 0; s < G::KD; ++s) {
-          const bf16x8 b = frag(Qs, G::ldQ, jt * 16, s * 32);
-          acc = mfma(frag(Rh, G::ldR, it * 16, s * 32), b, acc);
-          acc = mfma(frag(Rl, G::ldR, it * 16, s * 32), b, acc);
-        }
-        float ps = 0.f;
+          for (int s = 0; s < G::KD; ++s) {
+            const bf16x8 b = frag(Qs, G::ldQ, jt * 32, s * 16);
+            acc = mfma(frag(Rh, G::ldR, it * 32, s * 16), b, acc);
+            acc = mfma(frag(Rl, G::ldR, it * 32, s * 16), b, acc);
+          }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {     // keep j <= t
-          if (it * 16 + 4 * lg + j > jt * 16 + lr) acc[j] = 0.f;
-          ps += acc[j];
+          for (int e = 0; e < 16; ++e)     // keep j <= t
+            if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
         }
-        ps += __shfl_xor(ps, 16);
-        ps += __shfl_xor(ps, 32);
-        if (lg == 0) denp[it * C + jt * 16 + lr] = ps;
-        store_T(acc, Wh, Wl, G::ldW, it * 16, jt * 16);
+        if (tile) {
+          float ps = 0.f;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) ps += acc[e];
+          ps += __shfl_xor(ps, 32);
+          if (lg == 0) denp[it * C + jt * 32 + lr] = ps;
+        }
+        __syncthreads();     // every wave is done reading R: B2 takes T
+        if (tile) store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);
       }
       __syncthreads();
-      // den_t = sum_j T[t][j] + q_t . eta0
+      // den_t = sum_j T[t][j] + q_t . eta0, stored as 1 / (den_t + eps)
       if (normalized && tid < C) {
         float s = 0.f;
-        for (int it = 0; it < G::RT; ++it) s += denp[it * C + tid];
-        for (int a = 0; a < D; ++a) s += bf16_to_f(Qs[tid * G::ldQ + a]) * eta[a];
+#pragma unroll
+        for (int i = 0; i < G::RT; ++i) s += denp[i * C + tid];
+        const uint16_t* row = Qs + tid * G::ldQ;
+#pragma unroll
+        for (int a8 = 0; a8 < D; a8 += 8) {
+          const uint4 u = *reinterpret_cast<const uint4*>(row + a8);
+          const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) s += bf16_to_f(e8[j]) * eta[a8 + j];
+        }
         den[tid] = 1.f / (s + eps);
       }
       __syncthreads();
-      // ---- stage 4: O = T V + Q Phi0 (old Phi0); stage 5: Phi0 += R^T V ----
-#pragma unroll
-      for (int sb = 0; sb < G::SB; ++sb) {
-        const int bt = ct + kColWaves * sb;
-        if (bt * 16 >= DV) break;
-        f32x4 oacc[RH];
-#pragma unroll
-        for (int r = 0; r < RH; ++r) oacc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // ---- stage 4: O = T V + Q Phi0 (old Phi0) on tile (rt, ct); stage 5: Phi0 += R^T V ----
+      if (has_o) {
+        f32x16 oacc = zero16();
 #pragma unroll
         for (int s = 0; s < G::KC; ++s) {
-          const bf16x8 bV = frag(Vt, G::ldVt, bt * 16, s * 32);
-#pragma unroll
-          for (int r = 0; r < RH; ++r) {
-            const int rt = rh * RH + r;
-            if (s * 32 > rt * 16 + 15) continue;   // T row tile rt has no j at or beyond s*32
-            oacc[r] = mfma(frag(Wh, G::ldW, rt * 16, s * 32), bV, oacc[r]);
-            oacc[r] = mfma(frag(Wl, G::ldW, rt * 16, s * 32), bV, oacc[r]);
-          }
+          if (s * 16 > rt * 32 + 31) break;       // j past this row tile: T is zero
+          const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
+          oacc = mfma(frag(Th, G::ldT, rt * 32, s * 16), bV, oacc);
+          oacc = mfma(frag(Tl, G::ldT, rt * 32, s * 16), bV, oacc);
         }
 #pragma unroll
         for (int s = 0; s < G::KD; ++s) {
           bf16x8 bh, bl;
-          frag_from_acc(P0[sb][2 * s], P0[sb][2 * s + 1], bh, bl);
-#pragma unroll
-          for (int r = 0; r < RH; ++r) {
-            const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, (rh * RH + r) * 16, s * 32);
-            oacc[r] = mfma(aQ, bh, oacc[r]);
-            oacc[r] = mfma(aQ, bl, oacc[r]);
-          }
+          frag_from_acc(P0[s >> 1], s & 1, bh, bl);
+          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, s * 16);
+          oacc = mfma(aQ, bh, oacc);
+          oacc = mfma(aQ, bl, oacc);
         }
 #pragma unroll
-        for (int r = 0; r < RH; ++r)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int t = (rh * RH + r) * 16 + 4 * lg + j;
-            if (t0 + t < n) {
-              float o = oacc[r][j];
-              if (normalized) o *= den[t];
-              out[((size_t)bh * n + t0 + t) * DV + bt * 16 + lr] = o;
-            }
-          }
-#pragma unroll
-        for (int s = 0; s < G::KC; ++s) {
-          const bf16x8 bV = frag(Vt, G::ldVt, bt * 16, s * 32);
-#pragma unroll
-          for (int rt = 0; rt < G::DT; ++rt) {
-            P0[sb][rt] = mfma(frag(Rth, G::ldRt, rt * 16, s * 32), bV, P0[sb][rt]);
-            P0[sb][rt] = mfma(frag(Rtl, G::ldRt, rt * 16, s * 32), bV, P0[sb][rt]);
+        for (int e = 0; e < 16; ++e) {
+          const int t = rt * 32 + acc_row(e, lg);
+          if (t0 + t < n) {
+            float o = oacc[e];
+            if (normalized) o *= den[t];
+            out[((size_t)bh * n + t0 + t) * DV + ct * 32 + lr] = o;
           }
         }
       }
-    } else {
-      // summaries: Phi += R^T V and C += Q^T V
+    }
+    if (upd_p) {
+      // Phi0 += R^T V (and, for summaries, C += Q^T V) on column ct
 #pragma unroll
-      for (int sb = 0; sb < G::SB; ++sb) {
-        const int bt = ct + kColWaves * sb;
-        if (bt * 16 >= DV) break;
+      for (int s = 0; s < G::KC; ++s) {
+        const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
 #pragma unroll
-        for (int s = 0; s < G::KC; ++s) {
-          const bf16x8 bV = frag(Vt, G::ldVt, bt * 16, s * 32);
-#pragma unroll
-          for (int rt = 0; rt < G::DT; ++rt) {
-            P0[sb][rt] = mfma(frag(Rth, G::ldRt, rt * 16, s * 32), bV, P0[sb][rt]);
-            P0[sb][rt] = mfma(frag(Rtl, G::ldRt, rt * 16, s * 32), bV, P0[sb][rt]);
-            Cs[SUMMARY ? sb : 0][rt] = mfma(frag(Qt, G::ldQt, rt * 16, s * 32), bV, Cs[SUMMARY ? sb : 0][rt]);
-          }
+        for (int i = 0; i < G::DT; ++i) {
+          P0[i] = mfma(frag(Rth, G::ldRt, i * 32, s * 16), bV, P0[i]);
+          P0[i] = mfma(frag(Rtl, G::ldRt, i * 32, s * 16), bV, P0[i]);
+          if (SUMMARY) Cs[SUMMARY ? i : 0] = mfma(frag(Qt, G::ldQt, i * 32, s * 16), bV, Cs[SUMMARY ? i : 0]);
         }
       }
     }
@@ -805,30 +646,22 @@ __global__ __launch_bounds__(kThreads, 1) void k_walk(const uint16_t* __restrict
     if (tid < D) eta[tid] += eta_add;
   }
 
-  if (SUMMARY && rh == 0) {
-    // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
-#pragma unroll
-    for (int sa = 0; sa < G::SA; ++sa) {
-      const int at = ct + kColWaves * sa;
-      if (at >= G::DT) break;
-#pragma unroll
-      for (int rt = 0; rt < G::DT; ++rt)
-        for (int j = 0; j < 4; ++j) rc[(size_t)(rt * 16 + 4 * lg + j) * D + at * 16 + lr] = S0[sa][rt][j];
-    }
-#pragma unroll
-    for (int sb = 0; sb < G::SB; ++sb) {
-      const int bt = ct + kColWaves * sb;
-      if (bt * 16 >= DV) break;
-#pragma unroll
-      for (int rt = 0; rt < G::DT; ++rt)
-        for (int j = 0; j < 4; ++j) {
-          const size_t e = (size_t)(rt * 16 + 4 * lg + j) * DV + bt * 16 + lr;
-          rc[off_G(D, DV) + e] = P0[sb][rt][j];
-          rc[off_C(D, DV) + e] = Cs[SUMMARY ? sb : 0][rt][j];
-        }
-    }
-  }
   if (SUMMARY) {
+    // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
+    if (has_r && rt == 0)
+#pragma unroll
+      for (int i = 0; i < G::DT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) rc[(size_t)(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr] = S0[i][e];
+    if (upd_p)
+#pragma unroll
+      for (int i = 0; i < G::DT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const size_t o = (size_t)(i * 32 + acc_row(e, lg)) * DV + ct * 32 + lr;
+          rc[off_G(D, DV) + o] = P0[i][e];
+          rc[off_C(D, DV) + o] = Cs[SUMMARY ? i : 0][e];
+        }
     __syncthreads();
     if (tid < D) {
       rc[off_m(D, DV) + tid] = m_acc;
@@ -865,18 +698,20 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const bool want_out = f.out != nullptr;
-  if (final_state) {
-    // total state after all P segments: the semidirect-product fold in k_carry
-    constexpr int CB = (4096 / D < DV) ? 4096 / D : DV;
-    constexpr int nblk = (DV + CB - 1) / CB;
-    const size_t lds = sizeof(float) * ((size_t)D * (D + 4) + 2 * (size_t)D * CB + 2 * D);
-    auto kc = k_carry<D, DV, CB>;
-    if ((e = hipFuncSetAttribute((const void*)kc, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
-        hipSuccess)
+  if (nsum > 0) {
+    const size_t lds = sizeof(float) * ((size_t)D * (D + 4) + (size_t)D * DV + D);
+    auto kx = k_seg_cross<D, DV>;
+    if ((e = hipFuncSetAttribute((const void*)kx, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
       return e;
-    prof_start("carry", s);
-    hipLaunchKernelGGL(kc, dim3(((BH + 7) / 8) * 8 * nblk), dim3(256), lds, s, segs, init, (float*)nullptr,
-                       final_state, BH, nsum, P);
+    prof_start("seg_cross", s);
+    hipLaunchKernelGGL(kx, dim3(nsum, BH), dim3(256), lds, s, segs, init, P);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (final_state) {
+    const int F4 = (int)(F / 4);
+    prof_start("total", s);
+    hipLaunchKernelGGL(k_total, dim3((F4 + 255) / 256, BH), dim3(256), 0, s, segs, init, final_state, P, nsum, F4);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -896,7 +731,7 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
 
 void fused_plan(int BH, int n, int chunk, int* P, int* cps) {
   const int M = (n + chunk - 1) / chunk;
-  int p = 256 / BH;                       // about one workgroup per CU
+  int p = 512 / BH;                       // about two workgroups per CU
   if (const char* e = getenv("HLA_FUSED_SEGMENTS")) p = atoi(e);
   if (p < 1) p = 1;
   if (p > M) p = M;

@@ -178,7 +178,9 @@ int hla2_scan(const float* states, const float* init, float* prefix, float* tota
 
 size_t hla2_prefill_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
   if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
-  return chunked_ws(B * H, n, d, dv, chunk) + align256(sizeof(float) * (size_t)B * H * hla::state_floats(d, dv));
+  const size_t a = chunked_ws(B * H, n, d, dv, chunk);
+  const size_t b = align256(hla::fused_workspace_bytes(B * H, n, d, dv, chunk));
+  return (a > b ? a : b) + align256(sizeof(float) * (size_t)B * H * hla::state_floats(d, dv));
 }
 
 int hla2_prefill(float* state, const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d,
@@ -194,6 +196,7 @@ int hla2_prefill(float* state, const void* q, const void* k, const void* v, floa
   if (out && !aligned16(out)) return fail(HLA_ERR_INVALID, "out is not 16-byte aligned");
   const int BH = B * H;
   const size_t cws = chunked_ws(BH, n, d, dv, chunk);
+  const size_t fws = align256(hla::fused_workspace_bytes(BH, n, d, dv, chunk));
   const size_t need = hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype);
   if (!workspace || workspace_bytes < need)
     return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
@@ -202,7 +205,15 @@ int hla2_prefill(float* state, const void* q, const void* k, const void* v, floa
   char* base = static_cast<char*>(workspace);
   float* states = reinterpret_cast<float*>(base);
   float* prefix = reinterpret_cast<float*>(base + cws / 2);
-  float* total = reinterpret_cast<float*>(base + cws);
+  float* total = reinterpret_cast<float*>(base + (cws > fws ? cws : fws));
+  if (hla::fused_supported(n, d, dv, chunk, dtype, out ? masked : 1)) {
+    hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
+    hipError_t e = hla::launch_fused(f, state, total, workspace, s);
+    if (e != hipSuccess) return hip_fail(e, "fused prefill");
+    e = hipMemcpyAsync(state, total, sizeof(float) * (size_t)BH * hla::state_floats(d, dv), hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "state copy");
+    return ok();
+  }
   hipError_t e = hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, chunk, dtype, s);
   if (e != hipSuccess) return hip_fail(e, "chunk summaries");
   e = hla::launch_scan(states, state, prefix, total, BH, M, d, dv, s);

@@ -253,6 +253,35 @@ def test_prefill_then_steps(dist, masked, normalized):
         assert np.abs(g - e).max() <= 1e-5 * np.abs(e).max()
 
 
+@pytest.mark.parametrize("normalized", [0, 1])
+def test_prefill_chain_fused_shape(normalized):
+    """Two chained prefills on a shape the fused path covers (init state in,
+    total state out), then decode steps; all against one serial oracle run."""
+    B, H, d, dv, chunk = 2, 3, 64, 64, 64
+    n1, n2, steps = 5 * 64 + 9, 7 * 64 + 40, 6
+    q, k, v, code = gen(B, H, n1 + n2 + steps, d, dv, "unit", 31)
+    _say(f"case fused-shape prefill chain normalized={normalized}")
+    eps = 0.5 if normalized else 1e-6
+    num_ref, den_ref, fin_ref = _oracle(q, k, v, True)
+    ref = num_ref / (den_ref + eps)[..., None] if normalized else num_ref
+    state = hla.new_state(B, H, d, dv)
+    outs = []
+    for a, b in ((0, n1), (n1, n1 + n2)):
+        outs.append(hla.prefill(state, dev(q[:, :, a:b], code), dev(k[:, :, a:b], code), dev(v[:, :, a:b], code),
+                                chunk, masked=True, normalized=normalized, eps=eps).cpu().numpy())
+    for t in range(n1 + n2, n1 + n2 + steps):
+        outs.append(hla.step(state, dev(q[:, :, t], code), dev(k[:, :, t], code), dev(v[:, :, t], code),
+                             normalized=normalized, eps=eps).cpu().numpy()[:, :, None])
+    got = np.concatenate(outs, axis=2)
+    if normalized:
+        good = np.abs(den_ref + eps) >= 0.05 * O.hla2_den_scale(q, k)
+        assert rowwise_err(got[good], ref[good]) <= 2e-3
+    else:
+        assert rowwise_err(got, ref) <= 2e-3
+    for g, e in zip(_state_to_np(state, d, dv), fin_ref):
+        assert np.abs(g - e).max() <= 1e-4 * np.abs(e).max()
+
+
 def test_decode_workload_sampled_heads():
     """B64 H32 d=dv=128: prefill 2048 bf16 tokens, then 1024 steps; 16 sampled
     heads vs the oracle over all 3072 tokens, including the final states."""
