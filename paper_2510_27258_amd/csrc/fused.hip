@@ -118,6 +118,26 @@ __device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_
   }
 }
 
+// Both layouts from one split: transposed into (Th, Tl) and row-major into (Nh, Nl).
+__device__ __forceinline__ void store_TN(const f32x16& acc, uint16_t* Th, uint16_t* Tl, int ldT, uint16_t* Nh,
+                                         uint16_t* Nl, int ldN, int row0, int col0) {
+  const int l = threadIdx.x & 63, g = l >> 5;
+  const int baseT = (col0 + (l & 31)) * ldT + row0 + 4 * g;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint16_t h[4], o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      split(acc[4 * q + j], h[j], o[j]);
+      const int offN = (row0 + 8 * q + 4 * g + j) * ldN + col0 + (l & 31);
+      Nh[offN] = h[j];
+      Nl[offN] = o[j];
+    }
+    *reinterpret_cast<uint2*>(Th + baseT + 8 * q) = make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
+    *reinterpret_cast<uint2*>(Tl + baseT + 8 * q) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+  }
+}
+
 // Store an accumulator tile row-major as X[row0 + i][col0 + r], hi/lo.
 __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
   const int l = threadIdx.x & 63, g = l >> 5;
@@ -429,6 +449,21 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
   uint4 pq[G::pfQ], pk[G::pfQ], pv[G::pfV];
   auto fetch = [&](int c) {
     const int t0 = c * C;
+    if (t0 + C <= n && G::segQ % kThreads == 0 && G::segV % kThreads == 0) {   // full chunk: no guards
+#pragma unroll
+      for (int i = 0; i < G::pfQ; ++i) {
+        const int e = tid + kThreads * i;
+        const size_t off = ((size_t)bh * n + t0 + e % C) * D + (e / C) * 8;
+        pq[i] = *reinterpret_cast<const uint4*>(q + off);
+        pk[i] = *reinterpret_cast<const uint4*>(k + off);
+      }
+#pragma unroll
+      for (int i = 0; i < G::pfV; ++i) {
+        const int e = tid + kThreads * i;
+        pv[i] = *reinterpret_cast<const uint4*>(v + ((size_t)bh * n + t0 + e % C) * DV + (e / C) * 8);
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + kThreads * i;
@@ -547,8 +582,10 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
     }
     __syncthreads();     // every wave is done reading W: B1 takes R^T
     if (has_r) {
-      store_T(racc, Rth, Rtl, G::ldRt, rt * 32, ct * 32);
-      if (!SUMMARY) store_N(racc, Rh, Rl, G::ldR, rt * 32, ct * 32);
+      if (SUMMARY)
+        store_T(racc, Rth, Rtl, G::ldRt, rt * 32, ct * 32);
+      else
+        store_TN(racc, Rth, Rtl, G::ldRt, Rh, Rl, G::ldR, rt * 32, ct * 32);
     }
     __syncthreads();
     float eta_add = 0.f;
