@@ -46,24 +46,45 @@ def kernel_costs(w, P=None):
         "scan": ("hbm", 2 * BH * M * F * 4, BH * M * 2 * (d * d * dv + d * d)),
     }
     if P:
-        cps = -(-M // P)
-        sum_tok = BH * min(n, (P - 1) * cps * C)
+        Ct = fused_tile(C)
+        cps = -(-(-(-n // Ct)) // P)
+        sum_tok = BH * min(n, (P - 1) * cps * Ct)
+        ncross = P - 1
         costs.update({
             # fused path: the output walk reads q/k/v once and writes out once
-            "walk": ("hbm", tok * (qkv_tok + 4 * dv) + BH * P * F * 4,
-                     tok * 2 * (3 * C * d + C * dv + 2 * d * d + 2 * d * dv)),
+            # (the carry records it also reads are this design's own traffic).
+            # flops: the dense reference count of the chunk form at the
+            # workload's chunk
+            "walk": ("hbm", tok * (qkv_tok + 4 * dv),
+                     tok * reference_flops_per_token(C, d, dv)),
             "walk_summary": ("hbm", sum_tok * qkv_tok + BH * (P - 1) * F * 4,
-                             sum_tok * 2 * (2 * C * d + 2 * d * d + 2 * d * dv)),
-            "carry": ("hbm", 2 * BH * P * F * 4, BH * P * 4 * (d * d * dv + d * d)),
-            "scan": ("hbm", 2 * BH * max(P - 1, 1) * F * 4, BH * max(P - 1, 1) * 2 * (d * d * dv + d * d)),
+                             sum_tok * 2 * (2 * Ct * d + 2 * d * d + 2 * d * dv + d * dv)),
+            # per segment: S of the segments before it, its own record, Phi/eta written back
+            "seg_cross": ("hbm", BH * (ncross * (F + d * dv + d) + ncross * (ncross - 1) // 2 * d * d) * 4,
+                          BH * ncross * 2 * (d * d * dv + d * d)),
+            "total": ("hbm", BH * (P + 2) * F * 4, BH * 2 * (d * d * dv + d * d)),
         })
     return costs
 
 
-def fused_segments(BH, n, C):
-    """Segments per head chosen by the library for the fused path (same rule as fused_plan)."""
-    M = -(-n // C)
-    p = int(os.environ.get("HLA_FUSED_SEGMENTS", 512 // BH))
+def reference_flops_per_token(C, d, dv):
+    """Dense flop count per token of the chunk form with chunk C (no triangle
+    discount): 2 (C^2 + 2 C d + 2 C dv + 2 d^2 + 4 d dv)."""
+    return 2 * (C * C + 2 * C * d + 2 * C * dv + 2 * d * d + 4 * d * dv)
+
+
+def fused_tile(C):
+    """Token tile of the fused walk: chunk 32 and 64 as given, chunk 128 in 64-token tiles."""
+    return 32 if C == 32 else 64
+
+
+def fused_segments(BH, n, C, d, dv):
+    """Segments per head chosen by the library for the fused path (same rule as
+    fused_plan): 256 CUs x output-walk workgroups per CU (two for d, dv <= 64,
+    one when either is 128), capped by the number of tiles."""
+    M = -(-n // fused_tile(C))
+    blocks = 1 if max(d, dv) > 64 else 2
+    p = int(os.environ.get("HLA_FUSED_SEGMENTS", 256 * blocks // BH))
     p = max(1, min(p, M))
     cps = -(-M // p)
     return -(-M // cps)
@@ -128,6 +149,67 @@ def cpu_baseline(w, q, k, v, budget_s=20.0):
             "sample": f"{heads} of {B * H} heads x {n} tokens, C fp64 serial recurrence, {dt:.2f} s"}
 
 
+def measure_scan(w, qd, kd, vd, reps=10):
+    """The semidirect-product scan kernel alone over the per-chunk summaries of
+    the workload: reads every chunk state and writes its exclusive prefix."""
+    import torch
+    import paper_2510_27258_amd as hla
+    d, dv = w["d"], w["dv"]
+    states = hla.chunk_summaries(qd, kd, vd, w["chunk"])
+    hla.scan(states, d, dv)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        hla.scan(states, d, dv)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = 2 * states.numel() * 4 + states.shape[0] * states.shape[1] * states.shape[3] * 4
+    B, H, M, F = states.shape
+    del states
+    return {"kernel": "scan", "states": B * H * M, "ms": ms, "achieved": nbytes / ms / 1e6, "unit": "GB/s",
+            "peak": HBM_PEAK_GBS, "frac": nbytes / ms / 1e6 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes}
+
+
+def measure_decode(steps=None):
+    """hla2_step on the decode workload: state from a prefill of the seeded
+    2048-token prefix, then the seeded step tokens, one launch per step."""
+    import numpy as np
+    import torch
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import inputs as I
+    w = I.WORKLOADS["hla2-decode-bf16-B64H32-d128-prefix2048-steps1024"]
+    B, H, d, dv, n = w["B"], w["H"], w["d"], w["dv"], w["n"]
+    steps = steps or w["steps"]
+    dev = torch.device("cuda:0")
+    state = hla.new_state(B, H, d, dv, device=dev)
+    # prefix in batch slices to bound host memory; draws follow the seeded recipe per slice
+    q, k, v, code = I.draw_qkv(B, H, n, d, dv, w["dist"], w["seed"])
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    del q, k, v
+    hla.prefill(state, qd, kd, vd, w["chunk"], want_out=False)
+    del qd, kd, vd
+    qs, ks, vs, _ = I.draw_qkv(B, H, steps, d, dv, w["dist"], w["step_seed"])
+    qsd, ksd, vsd = (I.to_torch(x, code, dev).permute(2, 0, 1, 3).contiguous() for x in (qs, ks, vs))
+    del qs, ks, vs
+    outs = torch.empty(steps, B, H, dv, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for t in range(steps):
+        hla.step(state, qsd[t], ksd[t], vsd[t], out=outs[t])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    F = d * d + 2 * d * dv + 2 * d
+    per_head = 2 * F * 4 + (2 * d + dv) * 2 + dv * 4
+    nbytes = B * H * per_head
+    return {"workload": "hla2-decode-bf16-B64H32-d128-prefix2048-steps1024", "steps": steps, "ms_per_step": ms,
+            "achieved": nbytes / ms / 1e6, "unit": "GB/s", "peak": HBM_PEAK_GBS,
+            "frac": nbytes / ms / 1e6 / HBM_PEAK_GBS, "bytes_per_step": nbytes}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,6 +218,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--algo", default="auto", choices=["auto", "chunked", "fused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
+    ap.add_argument("--no-scan", action="store_true", help="skip the standalone scan measurement")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -198,7 +282,7 @@ def main():
     used_algo = "fused" if "walk" in prof else "chunked"
     P = None
     if used_algo == "fused":
-        P = fused_segments(B * H, n, C)
+        P = fused_segments(B * H, n, C, d, dv)
     costs = kernel_costs(w, P)
     dom = max(prof, key=lambda kname: prof[kname][1])
     cnt, tot_ms = prof[dom]
@@ -227,11 +311,19 @@ def main():
                    "algo": used_algo, "global_batch": B * H, "seq_len": n, "parallelism": "none"},
         "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
                      "traffic": tr, "kernel": dom, "avg_launch_ms": avg_s * 1e3,
-                     "algorithmic_bytes": nbytes, "algorithmic_flops": nflops},
+                     "algorithmic_bytes": nbytes, "algorithmic_flops": nflops,
+                     "mfma_tflops": nflops / avg_s / 1e12,
+                     "mfma_frac": nflops / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS},
         "kernels_ms": {kname: v_[1] / v_[0] for kname, v_ in prof.items()},
     }
+    if not args.no_scan:
+        rec["scan"] = measure_scan(w, qd, kd, vd)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
+    if not args.no_decode:
+        del q, k, v, qd, kd, vd, ws, out
+        torch.cuda.empty_cache()
+        rec["decode"] = measure_decode()
     print(json.dumps(rec), flush=True)
 
 

@@ -6,12 +6,13 @@
 //      produces its summary (S, C, m, Phi, eta) with Phi = S C - G and
 //      eta = S m - h (an exact change of variables of the 5-tuple).
 //   2. k_seg_cross: the semidirect product of Eq. (semidirect) across
-//      segments in reduce-then-scan form: each segment's contribution
-//      G_s + S_s C_{<s} (and h_s + S_s m_{<s}) is computed in parallel.
-//   3. k_walk<OUTPUT>: each workgroup sums the contributions before its
-//      segment into its carry (fold_sum), converts it once to (S0, Phi0, eta0),
-//      walks its chunks from that carry and writes the outputs.
-//   k_total sums all contributions into the total state when a caller needs it.
+//      segments in reduce-then-scan form, in the Phi variables: each
+//      segment's bracket Phi_s + S_{<s} C_s (and eta_s + S_{<s} m_s) is
+//      computed in parallel.
+//   3. k_walk<OUTPUT>: each workgroup sums the brackets before its segment
+//      into its carry (S0, Phi0, eta0), walks its chunks from that carry and
+//      writes the outputs.
+//   k_total sums all brackets into the total state when a caller needs it.
 //
 // Per chunk (tokens of the chunk as the rows of Q, K, V; S0, Phi0, eta0 the
 // carry of the chunk), with r_j = S_j q_j (the proof of Thm. 1 sums
@@ -29,12 +30,13 @@
 // lo = bf16(x - hi); the product with an exact bf16 partner is taken as two
 // MFMAs, so the operand keeps ~16 significant bits.  Accumulation is fp32.
 //
-// Layout: 256 threads = 4 waves on v_mfma_f32_32x32x16_bf16.  Every product
-// of a chunk is at most 2 x 2 tiles of 32 x 32; wave w owns output tile
-// (row w/2, column w%2).  The wave owning column c of R (or O) keeps the whole
-// column c of S0 (or Phi0) in MFMA accumulators for the whole walk and feeds
-// it back as the B operand straight from registers (both row waves of a
-// column keep a copy).  Q, K, K^T, V^T, W/T, R and R^T are staged in LDS as
+// Layout: 256 threads = 4 waves on v_mfma_f32_32x32x16_bf16; a chunk has at
+// most 2 row tiles of 32 tokens.  With d, dv <= 64 wave w owns output tile
+// (row w/2, column w%2); with d or dv = 128 wave w owns column tile w over
+// all row tiles.  The wave owning column c of R (or O) keeps the whole column
+// c of S0 (or Phi0) in MFMA accumulators for the whole walk and feeds it back
+// as the B operand straight from registers (with two row waves per column
+// both keep a copy).  Q, K, K^T, V^T, W/T, R and R^T are staged in LDS as
 // bf16.
 #include "fused.h"
 #include "profile.h"
@@ -59,6 +61,21 @@ __device__ __forceinline__ void split(float x, uint16_t& hi, uint16_t& lo) {
   lo = bf16_bits((__bf16)(x - (float)h));
 }
 __device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) { return a | (uint32_t)b << 16; }
+
+// Buffer resource over [p, p + bytes): loads past the end return zero and
+// stores past the end are dropped, which zero-fills the ragged last chunk and
+// clips its outputs.  Offsets are 32-bit bytes from p.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_load16(rsrc_t r, uint32_t off) {
+  const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+  return make_uint4(x[0], x[1], x[2], x[3]);
+}
+__device__ __forceinline__ void buf_store4(rsrc_t r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
+}
 
 // Lane layout of v_mfma_f32_32x32x16_bf16 (l = lane, r = l % 32, g = l / 32):
 //   A: row r, k = 8g .. 8g+7;  B: column r, the same k (any k order shared by
@@ -169,224 +186,227 @@ struct Cfg {
   static constexpr int oB2l = oB2h + (SUMMARY ? 0 : C * ld2);
   static constexpr int oQt = oB2l + (SUMMARY ? 0 : C * ld2);
   static constexpr int n16 = oQt + (SUMMARY ? D * ldQt : 0);          // bf16 elements of tiles
-  // the output walk folds its carry in fp32 scratch that reuses the tile region
-  static constexpr int fold_f = SUMMARY ? 0 : D * (D + 4) + 2 * D * DV + D;   // fold_sum scratch
-  static constexpr int n16t = (n16 > 2 * fold_f ? n16 : 2 * fold_f);
   static constexpr int RT = C / 32, DT = D / 32, VT = DV / 32;       // 32-wide tiles
   static constexpr int KC = C / 16, KD = D / 16;                     // 16-deep k steps
+  // Wave w owns column tile ct = w % NCT of R, O, S0 and Phi0 and the row
+  // tiles rg, rg + NRG, ... (rg = w / NCT).  With four column tiles (d = 128)
+  // every wave covers all row tiles and no state column is held twice.
+  static constexpr int NCT = (DT > 2 || VT > 2) ? 4 : 2;
+  static constexpr int NRG = kWaves / NCT;
+  static constexpr int RPW = (RT + NRG - 1) / NRG;                   // row tiles per wave
   static constexpr int f_eta = 0, f_cs = D, f_den = D + RT * D, f_denp = f_den + C;   // fp32 region
   static constexpr int nf32 = f_denp + RT * C;
-  static constexpr size_t bytes = (size_t)((n16t + 7) & ~7) * 2 + (size_t)nf32 * 4;
+  static constexpr size_t bytes = (size_t)((n16 + 7) & ~7) * 2 + (size_t)nf32 * 4;
+  // workgroups per CU: two when LDS allows and the state columns (d, dv <= 64) leave
+  // registers for a second workgroup
+  static constexpr int kBlocks = (2 * bytes <= 160 * 1024 && NCT == 2) ? 2 : 1;
   // global->LDS staging: 16-byte segments per operand
   static constexpr int segQ = C * D / 8, segV = C * DV / 8;
   static constexpr int pfQ = (segQ + kThreads - 1) / kThreads, pfV = (segV + kThreads - 1) / kThreads;
-  static_assert(C % 32 == 0 && D % 32 == 0 && DV % 32 == 0 && C <= 64 && D <= 64 && DV <= 64, "tile shape");
+  static_assert(C % 32 == 0 && D % 32 == 0 && DV % 32 == 0 && C <= 64 && D <= 128 && DV <= 128, "tile shape");
+  static_assert(DT <= NCT && VT <= NCT && RT <= 2, "wave layout");
   static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
 // The semidirect-product scan over segments, Eq. (semidirect), organised as
-// reduce-then-scan.  For segments A (everything before s, including the
-// initial state) and B = segment s:
-//   G_{A(+)B} = G_A + [G_B + S_B C_A],   h_{A(+)B} = h_A + [h_B + S_B m_A]
-// and S, C, m add.  The bracket depends on A only through the additive
-// prefixes C_A and m_A, so every segment's bracket is computed in parallel
-// (k_seg_cross); the carry of segment s is then a plain sum of the brackets
-// and summaries before it (fold_sum, in the output walk's prologue), and the
-// total state a plain sum of all of them (k_total).
+// reduce-then-scan in the (S, C, m, Phi, eta) variables, Phi = S C - G and
+// eta = S m - h.  Substituting Eq. (semidirect) gives
+//   Phi_{A(+)B} = Phi_A + Phi_B + S_A C_B,   eta_{A(+)B} = eta_A + eta_B + S_A m_B,
+// and S, C, m add.  With A = everything before segment s (the initial state
+// included) the bracket Phi_s + S_{<s} C_s depends on A only through the
+// additive prefix S_{<s}, so every segment's bracket is formed in parallel
+// (k_seg_cross) and the carry of a segment is a plain sum of the brackets
+// before it (the output walk's prologue); the total state is the plain sum
+// of all of them, converted back to G, h once (k_total).
 //
-// k_seg_cross: one workgroup per (segment s < nsum, head).  The summary of s
-// arrives as (S, C, m, Phi, eta) with Phi = S C - G, eta = S m - h, so
-//   G_s + S_s C_A = S_s (C_A + C_s) - Phi_s,  h_s + S_s m_A = S_s (m_A + m_s) - eta_s,
-// with C_A = C_init + sum_{s'<s} C_s'.  The brackets replace Phi_s and eta_s
-// in the record (in place; other workgroups read only S, C and m).
+// Records: [BH][nseg + 1][F] in the S|C|m|G|h layout with Phi in the G slot
+// and eta in the h slot; slot nseg holds the initial state converted to this
+// form (written only when there is one).
+
+// out[a][b] = z * Z[a][b] + sum_a' X[a][a'] Y[a'][b] for the thread's TI x TI
+// register blocks; XT = X^T ([D][D+4]) and Y ([D][DV]) in LDS, Z and out in
+// global memory with row stride DV (out may alias Z).
+template <int D, int DV>
+__device__ __forceinline__ void xy_plus(const float* XT, const float* Y, const float* Z, float z, float* out) {
+  constexpr int TI = (D >= 128 || DV >= 128) ? 8 : 4, ldT = D + 4;
+  constexpr int NBJ = DV / TI, NB = (D / TI) * NBJ;
+  for (int blk = threadIdx.x; blk < NB; blk += blockDim.x) {
+    const int a0 = TI * (blk / NBJ), b0 = TI * (blk % NBJ);
+    float o[TI][TI] = {};
+#pragma unroll 4
+    for (int ap = 0; ap < D; ++ap) {
+      float xv[TI], yv[TI];
+#pragma unroll
+      for (int i = 0; i < TI; i += 4) {
+        const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldT + a0 + i]);
+        const float4 y4 = *reinterpret_cast<const float4*>(&Y[ap * DV + b0 + i]);
+        xv[i] = x4.x; xv[i + 1] = x4.y; xv[i + 2] = x4.z; xv[i + 3] = x4.w;
+        yv[i] = y4.x; yv[i + 1] = y4.y; yv[i + 2] = y4.z; yv[i + 3] = y4.w;
+      }
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TI; ++j) o[i][j] += xv[i] * yv[j];
+    }
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TI; j += 4) {
+        const size_t off = (size_t)(a0 + i) * DV + b0 + j;
+        const float4 z4 = *reinterpret_cast<const float4*>(Z + off);
+        *reinterpret_cast<float4*>(out + off) =
+            make_float4(o[i][j] + z * z4.x, o[i][j + 1] + z * z4.y, o[i][j + 2] + z * z4.z, o[i][j + 3] + z * z4.w);
+      }
+  }
+}
+
+// out[a] = z * zv[a] + sum_a' X[a][a'] y[a'] for a = threadIdx.x < D.
+template <int D>
+__device__ __forceinline__ void xv_plus(const float* XT, const float* y, const float* zv, float z, float* out) {
+  const int a = threadIdx.x;
+  if (a >= D) return;
+  float acc = 0.f;
+#pragma unroll 8
+  for (int ap = 0; ap < D; ++ap) acc += XT[ap * (D + 4) + a] * y[ap];
+  out[a] = acc + z * zv[a];
+}
+
+// Stage X^T (X from float4 registers, row-major [D][D] split as element
+// 4 * (tid + 256 r)), Y ([D][DV] float4 registers) and y into LDS.
+template <int D, int DV>
+__device__ __forceinline__ void stage_xy(float* XT, float* Y, float* y, const float4* xs, const float4* ys, float yv) {
+  constexpr int nS4 = D * D / 4 / 256, nC4 = D * DV / 4 / 256, ldT = D + 4;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int r = 0; r < nS4; ++r) {
+    const int e4 = tid + 256 * r, a = (4 * e4) / D, ap = (4 * e4) % D;
+    XT[(ap + 0) * ldT + a] = xs[r].x;
+    XT[(ap + 1) * ldT + a] = xs[r].y;
+    XT[(ap + 2) * ldT + a] = xs[r].z;
+    XT[(ap + 3) * ldT + a] = xs[r].w;
+  }
+#pragma unroll
+  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(Y)[tid + 256 * r] = ys[r];
+  if (tid < D) y[tid] = yv;
+}
+
+__device__ __forceinline__ void add4(float4& a, const float4& b) {
+  a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+}
+
+// k_seg_cross: grid (nsum + [init != 0], BH), 256 threads.  Block s < nsum
+// replaces (Phi_s, eta_s) of record s by its bracket (Phi_s + S_{<s} C_s,
+// eta_s + S_{<s} m_s), S_{<s} = S_init + sum_{s'<s} S_s'.  Block s = nsum
+// converts the initial state into slot nseg: (S, C, m, S C - G, S m - h).
+// Blocks read S of other records and write only their own G/h slots.
 template <int D, int DV>
 __global__ __launch_bounds__(256) void k_seg_cross(float* __restrict__ segs, const float* __restrict__ init,
-                                                   int nseg) {
-  constexpr int T = 256, ldT = D + 4, NB4 = DV / 4, NT = (D / 4) * NB4;
-  constexpr int nS4 = D * D / 4 / T, nC4 = D * DV / 4 / T;
-  static_assert(NT <= T && D * D % (4 * T) == 0 && D * DV % (4 * T) == 0, "thread split");
+                                                   int nseg, int nsum) {
+  constexpr int nS4 = D * D / 4 / 256, nC4 = D * DV / 4 / 256, ldT = D + 4;
+  static_assert(D * D % 1024 == 0 && D * DV % 1024 == 0, "thread split");
   extern __shared__ float sm[];
-  float* XT = sm;                 // [D][D+4]  S_s^T
-  float* Y = XT + D * ldT;        // [D][DV]   C_A + C_s
-  float* y = Y + D * DV;          // [D]       m_A + m_s
+  float* XT = sm;                 // [D][D+4]  X^T
+  float* Y = XT + D * ldT;        // [D][DV]
+  float* y = Y + D * DV;          // [D]
   const int s = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const size_t F = state_floats(D, DV);
-  float* x = segs + ((size_t)bh * nseg + s) * F;
+  const bool conv = s == nsum;
+  float* base = segs + (size_t)bh * (nseg + 1) * F;
   const float* ini = init ? init + (size_t)bh * F : nullptr;
-  const bool act = tid < NT;
-  const int a0 = act ? 4 * (tid / NB4) : 0, b0 = 4 * (tid % NB4);
-  // issue every load first: S_s, Phi_s block, eta_s, then C and m of segments <= s
-  float4 sv[nS4], pv[4], cs[nC4];
-  float ev = 0.f, ms = 0.f;
-#pragma unroll
-  for (int r = 0; r < nS4; ++r) sv[r] = reinterpret_cast<const float4*>(x)[tid + T * r];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    pv[i] = act ? *reinterpret_cast<const float4*>(x + off_G(D, DV) + (size_t)(a0 + i) * DV + b0)
-                : make_float4(0.f, 0.f, 0.f, 0.f);
-  if (tid < D) ev = x[off_h(D, DV) + tid];
-#pragma unroll
-  for (int r = 0; r < nC4; ++r)
-    cs[r] = ini ? reinterpret_cast<const float4*>(ini + off_C(D, DV))[tid + T * r] : make_float4(0.f, 0.f, 0.f, 0.f);
-  if (tid < D && ini) ms = ini[off_m(D, DV) + tid];
-  for (int sp = 0; sp <= s; ++sp) {
-    const float* xp = segs + ((size_t)bh * nseg + sp) * F;
-#pragma unroll
-    for (int r = 0; r < nC4; ++r) {
-      const float4 c4 = reinterpret_cast<const float4*>(xp + off_C(D, DV))[tid + T * r];
-      cs[r].x += c4.x; cs[r].y += c4.y; cs[r].z += c4.z; cs[r].w += c4.w;
-    }
-    if (tid < D) ms += xp[off_m(D, DV) + tid];
-  }
-#pragma unroll
-  for (int r = 0; r < nS4; ++r) {
-    const int e4 = tid + T * r, a = (4 * e4) / D, ap = (4 * e4) % D;
-    XT[(ap + 0) * ldT + a] = sv[r].x;
-    XT[(ap + 1) * ldT + a] = sv[r].y;
-    XT[(ap + 2) * ldT + a] = sv[r].z;
-    XT[(ap + 3) * ldT + a] = sv[r].w;
-  }
-#pragma unroll
-  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(Y)[tid + T * r] = cs[r];
-  if (tid < D) y[tid] = ms;
-  __syncthreads();
-  if (act) {
-    float o[4][4] = {};
-#pragma unroll 8
-    for (int ap = 0; ap < D; ++ap) {
-      const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldT + a0]);
-      const float4 z4 = *reinterpret_cast<const float4*>(&Y[ap * DV + b0]);
-      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, zv[4] = {z4.x, z4.y, z4.z, z4.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) o[i][j] += xv[i] * zv[j];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<float4*>(x + off_G(D, DV) + (size_t)(a0 + i) * DV + b0) =
-          make_float4(o[i][0] - pv[i].x, o[i][1] - pv[i].y, o[i][2] - pv[i].z, o[i][3] - pv[i].w);
-  }
-  if (tid < D) {
-    float acc = 0.f;
-#pragma unroll 8
-    for (int ap = 0; ap < D; ++ap) acc += XT[ap * ldT + tid] * y[ap];
-    x[off_h(D, DV) + tid] = acc - ev;
-  }
-}
-
-// k_total: the state after all nsum segments, init (+) seg_0 (+) ... : S, C,
-// m add; G and h add the brackets written by k_seg_cross.  Elementwise.
-__global__ __launch_bounds__(256) void k_total(const float* __restrict__ segs, const float* __restrict__ init,
-                                               float* __restrict__ fin, int nseg, int nsum, int F4) {
-  const int bh = blockIdx.y;
-  const size_t F = (size_t)F4 * 4;
-  for (int e4 = blockIdx.x * 256 + threadIdx.x; e4 < F4; e4 += gridDim.x * 256) {
-    float4 acc = init ? reinterpret_cast<const float4*>(init + bh * F)[e4] : make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sp = 0; sp < nsum; ++sp) {
-      const float4 v = reinterpret_cast<const float4*>(segs + ((size_t)bh * nseg + sp) * F)[e4];
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-    }
-    reinterpret_cast<float4*>(fin + bh * F)[e4] = acc;
-  }
-}
-
-// Carry of segment `seg` of head bh in the output walk's prologue: sum of the
-// initial state and the records of segments < seg (after k_seg_cross), then
-// Phi0 = S_acc C_acc - G_acc and eta0 = S_acc m_acc - h_acc.
-// Results: S_acc^T in `Sout` ([D][D+4]), Phi0 in `Pout` ([D][DV]), eta0 in `eout`.
-template <int D, int DV>
-__device__ void fold_sum(const float* __restrict__ segs, const float* __restrict__ init, int bh, int seg,
-                         int nseg, float* sc, float*& Sout, float*& Pout, float* eout) {
-  constexpr int ldT = D + 4, NB4 = DV / 4, NT = (D / 4) * NB4;
-  constexpr int nS4 = D * D / 4 / kThreads, nC4 = D * DV / 4 / kThreads;
-  static_assert(NT <= kThreads && D * D % (4 * kThreads) == 0 && D * DV % (4 * kThreads) == 0, "thread split");
-  const size_t F = state_floats(D, DV);
-  float* XT = sc;                     // [D][D+4]  S_acc^T
-  float* Y = XT + D * ldT;            // [D][DV]   Phi0
-  float* Cs = Y + D * DV;             // [D][DV]   C_acc
-  float* y = Cs + D * DV;             // [D]       m_acc
-  const int tid = threadIdx.x;
-  const bool act = tid < NT;
-  const int a0 = act ? 4 * (tid / NB4) : 0, b0 = 4 * (tid % NB4);
-  float4 sacc[nS4], cacc[nC4], gacc[4];
-  float macc = 0.f, hacc = 0.f;
-  auto add = [](float4& a, const float4& b) { a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w; };
+  float* dst = base + (size_t)(conv ? nseg : s) * F;
+  const float* src = conv ? ini : dst;
+  float4 xs[nS4], ys[nC4];
   const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int r = 0; r < nS4; ++r) sacc[r] = z4;
+  for (int r = 0; r < nS4; ++r) xs[r] = ini ? reinterpret_cast<const float4*>(ini)[tid + 256 * r] : z4;
+  if (!conv)
+    for (int sp = 0; sp < s; ++sp)
 #pragma unroll
-  for (int r = 0; r < nC4; ++r) cacc[r] = z4;
+      for (int r = 0; r < nS4; ++r) add4(xs[r], reinterpret_cast<const float4*>(base + (size_t)sp * F)[tid + 256 * r]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) gacc[i] = z4;
-  for (int sp = -1; sp < seg; ++sp) {
-    const float* x = sp < 0 ? (init ? init + (size_t)bh * F : nullptr) : segs + ((size_t)bh * nseg + sp) * F;
-    if (!x) continue;
+  for (int r = 0; r < nC4; ++r) ys[r] = reinterpret_cast<const float4*>(src + off_C(D, DV))[tid + 256 * r];
+  const float yv = tid < D ? src[off_m(D, DV) + tid] : 0.f;
+  stage_xy<D, DV>(XT, Y, y, xs, ys, yv);
+  if (conv) {
 #pragma unroll
-    for (int r = 0; r < nS4; ++r) add(sacc[r], reinterpret_cast<const float4*>(x)[tid + kThreads * r]);
+    for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(dst)[tid + 256 * r] = xs[r];
 #pragma unroll
-    for (int r = 0; r < nC4; ++r) add(cacc[r], reinterpret_cast<const float4*>(x + off_C(D, DV))[tid + kThreads * r]);
-    if (act)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) add(gacc[i], *reinterpret_cast<const float4*>(x + off_G(D, DV) + (size_t)(a0 + i) * DV + b0));
-    if (tid < D) {
-      macc += x[off_m(D, DV) + tid];
-      hacc += x[off_h(D, DV) + tid];
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < nS4; ++r) {
-    const int e4 = tid + kThreads * r, a = (4 * e4) / D, ap = (4 * e4) % D;
-    XT[(ap + 0) * ldT + a] = sacc[r].x;
-    XT[(ap + 1) * ldT + a] = sacc[r].y;
-    XT[(ap + 2) * ldT + a] = sacc[r].z;
-    XT[(ap + 3) * ldT + a] = sacc[r].w;
-  }
-#pragma unroll
-  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(Cs)[tid + kThreads * r] = cacc[r];
-  if (tid < D) y[tid] = macc;
-  __syncthreads();
-  if (act) {
-    float o[4][4] = {};
-#pragma unroll 8
-    for (int ap = 0; ap < D; ++ap) {
-      const float4 x4 = *reinterpret_cast<const float4*>(&XT[ap * ldT + a0]);
-      const float4 c4 = *reinterpret_cast<const float4*>(&Cs[ap * DV + b0]);
-      const float xv[4] = {x4.x, x4.y, x4.z, x4.w}, cv[4] = {c4.x, c4.y, c4.z, c4.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) o[i][j] += xv[i] * cv[j];
-    }
-    const float gv[4][4] = {{gacc[0].x, gacc[0].y, gacc[0].z, gacc[0].w}, {gacc[1].x, gacc[1].y, gacc[1].z, gacc[1].w},
-                            {gacc[2].x, gacc[2].y, gacc[2].z, gacc[2].w}, {gacc[3].x, gacc[3].y, gacc[3].z, gacc[3].w}};
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) Y[(a0 + i) * DV + b0 + j] = o[i][j] - gv[i][j];
-  }
-  if (tid < D) {
-    float acc = 0.f;
-#pragma unroll 8
-    for (int ap = 0; ap < D; ++ap) acc += XT[ap * ldT + tid] * y[ap];
-    eout[tid] = acc - hacc;
+    for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(dst + off_C(D, DV))[tid + 256 * r] = ys[r];
+    if (tid < D) dst[off_m(D, DV) + tid] = yv;
   }
   __syncthreads();
-  Sout = XT;
-  Pout = Y;
+  const float z = conv ? -1.f : 1.f;
+  xy_plus<D, DV>(XT, Y, src + off_G(D, DV), z, dst + off_G(D, DV));
+  xv_plus<D>(XT, y, src + off_h(D, DV), z, dst + off_h(D, DV));
 }
 
-// One segment walk.  grid = (segments, BH), 4 waves.  Wave w works on output
-// tile (rt = w/2, ct = w%2) of R and of O; it keeps columns ct of S0 and of
-// Phi0 (all their rows) in accumulators.
+// k_total: grid (BH), 256 threads.  The state after all nsum segments in the
+// S|C|m|G|h form: S, C, m, Phi, eta are sums over the converted initial state
+// and the brackets; then G = S C - Phi and h = S m - eta.
+template <int D, int DV>
+__global__ __launch_bounds__(256) void k_total(const float* __restrict__ segs, const float* __restrict__ init,
+                                               float* __restrict__ fin, int nseg, int nsum) {
+  constexpr int nS4 = D * D / 4 / 256, nC4 = D * DV / 4 / 256, ldT = D + 4;
+  extern __shared__ float sm[];
+  float* XT = sm;
+  float* Y = XT + D * ldT;
+  float* y = Y + D * DV;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const size_t F = state_floats(D, DV);
+  const float* base = segs + (size_t)bh * (nseg + 1) * F;
+  float* out = fin + (size_t)bh * F;
+  float4 xs[nS4], ys[nC4];
+  float yv = 0.f, ev = 0.f;
+  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int r = 0; r < nS4; ++r) xs[r] = z4;
+#pragma unroll
+  for (int r = 0; r < nC4; ++r) ys[r] = z4;
+  for (int sp = init ? -1 : 0; sp < nsum; ++sp) {
+    const float* x = base + (size_t)(sp < 0 ? nseg : sp) * F;
+#pragma unroll
+    for (int r = 0; r < nS4; ++r) add4(xs[r], reinterpret_cast<const float4*>(x)[tid + 256 * r]);
+#pragma unroll
+    for (int r = 0; r < nC4; ++r) add4(ys[r], reinterpret_cast<const float4*>(x + off_C(D, DV))[tid + 256 * r]);
+    if (tid < D) {
+      yv += x[off_m(D, DV) + tid];
+      ev += x[off_h(D, DV) + tid];
+    }
+  }
+  stage_xy<D, DV>(XT, Y, y, xs, ys, yv);
+#pragma unroll
+  for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(out)[tid + 256 * r] = xs[r];
+#pragma unroll
+  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(out + off_C(D, DV))[tid + 256 * r] = ys[r];
+  if (tid < D) {
+    out[off_m(D, DV) + tid] = yv;
+    out[off_h(D, DV) + tid] = ev;      // eta, replaced by h below
+  }
+  // Phi sum into the G slot of the output, then G = S C - Phi in place
+  float* Gout = out + off_G(D, DV);
+  for (int e4 = tid; e4 < D * DV / 4; e4 += 256) {
+    float4 acc = z4;
+    for (int sp = init ? -1 : 0; sp < nsum; ++sp)
+      add4(acc, reinterpret_cast<const float4*>(base + (size_t)(sp < 0 ? nseg : sp) * F + off_G(D, DV))[e4]);
+    reinterpret_cast<float4*>(Gout)[e4] = acc;
+  }
+  __syncthreads();
+  xy_plus<D, DV>(XT, Y, Gout, -1.f, Gout);
+  xv_plus<D>(XT, y, out + off_h(D, DV), -1.f, out + off_h(D, DV));
+}
+
+// One segment walk.  grid = (segments, BH), 4 waves.  Wave w owns column tile
+// ct = w % NCT of R and of O and keeps column ct of S0 and of Phi0 (all their
+// rows) in accumulators; it works on the row tiles rg, rg + NRG, ...
 // SUMMARY: zero carry, writes the segment summary (S, C, m, Phi, eta) to
-// rec[bh][seg].  !SUMMARY: folds the carry from rec[bh][0..seg) and init,
-// then writes outputs.
+// rec[bh][seg].  !SUMMARY: the carry is the sum of the converted initial
+// state and the brackets of the segments before this one (k_seg_cross); then
+// writes outputs.
 template <int C, int D, int DV, bool SUMMARY>
-__global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-                                                      const uint16_t* __restrict__ v, float* __restrict__ out,
-                                                      float* __restrict__ rec, const float* __restrict__ init, int n,
-                                                      int cps, int nseg, int normalized, float eps) {
+__global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k_walk(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    float* __restrict__ out, float* __restrict__ rec, const float* __restrict__ init, int n, int cps, int nseg,
+    int normalized, float eps) {
   using G = Cfg<C, D, DV, SUMMARY>;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
@@ -402,22 +422,25 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
   uint16_t* Th = Rh;
   uint16_t* Tl = Rl;
   uint16_t* Qt = lds + G::oQt;
-  float* fl = reinterpret_cast<float*>(lds + ((G::n16t + 7) & ~7));
+  float* fl = reinterpret_cast<float*>(lds + ((G::n16 + 7) & ~7));
   float* eta = fl + G::f_eta;
   float* colsum = fl + G::f_cs;       // [RT][D]
   float* den = fl + G::f_den;         // [C]
   float* denp = fl + G::f_denp;       // [RT][C]
 
   const int seg = blockIdx.x, bh = blockIdx.y;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 31, lg = l >> 5;
-  const int rt = w >> 1, ct = w & 1;
-  const bool has_r = rt < G::RT && ct < G::DT;        // owns R tile (rt, ct) and S0 column ct
-  const bool has_o = rt < G::RT && ct < G::VT;        // owns O tile (rt, ct) and Phi0 column ct
-  const bool upd_p = SUMMARY ? (has_o && rt == 0) : has_o;
+  const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: per-wave branches stay scalar
+  const int ct = w % G::NCT, rg = G::NRG == 1 ? 0 : w / G::NCT;
+  // owns R column tile ct and S0 column ct / O column tile ct and Phi0 column ct
+  const bool has_r = (G::DT == G::NCT || ct < G::DT) && (G::NRG == 1 || rg < G::RT);
+  const bool has_o = (G::VT == G::NCT || ct < G::VT) && (G::NRG == 1 || rg < G::RT);
+  const bool upd_p = SUMMARY ? (has_o && rg == 0) : has_o;
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t F = state_floats(D, DV);
-  float* rc = SUMMARY ? rec + ((size_t)bh * nseg + seg) * F : nullptr;
+  float* rc = SUMMARY ? rec + ((size_t)bh * (nseg + 1) + seg) * F : nullptr;
+  const rsrc_t ro = make_rsrc(SUMMARY ? nullptr : out + (size_t)bh * n * DV, SUMMARY ? 0u : (uint32_t)n * DV * 4);
 
   // ---- carry in (fp32 accumulators, column ct, all rows) ----
   f32x16 S0[G::DT], P0[G::DT], Cs[SUMMARY ? G::DT : 1];
@@ -428,62 +451,78 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
     if (SUMMARY) Cs[SUMMARY ? i : 0] = zero16();
   }
   for (int a = tid; a < D; a += kThreads) eta[a] = 0.f;
-  if (!SUMMARY && (seg > 0 || init)) {
-    // the tile region of LDS is free until the first chunk is staged
-    float* Sc;
-    float* Pc;
-    fold_sum<D, DV>(rec, init, bh, seg, nseg, reinterpret_cast<float*>(lds), Sc, Pc, eta);
+  if constexpr (!SUMMARY) {
+    if (seg > 0 || init) {
+      // sum the records in float4 registers; stage S0, then Phi0, in the
+      // (still free) tile region of LDS; every wave picks up its columns
+      constexpr int nS4 = D * D / 4 / kThreads, nP4 = D * DV / 4 / kThreads;
+      static_assert(D * D % (4 * kThreads) == 0 && D * DV % (4 * kThreads) == 0, "record split");
+      static_assert(D * D * 4 <= G::n16 * 2 && D * DV * 4 <= G::n16 * 2, "carry staging fits the tile region");
+      float4 sa[nS4], pa[nP4];
+      float ea = 0.f;
+      const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int i = 0; i < G::DT; ++i)
+      for (int r = 0; r < nS4; ++r) sa[r] = z4;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = i * 32 + acc_row(e, lg);
-        if (has_r) S0[i][e] = Sc[(ct * 32 + lr) * (D + 4) + row];
-        if (has_o) P0[i][e] = Pc[row * DV + ct * 32 + lr];
+      for (int r = 0; r < nP4; ++r) pa[r] = z4;
+      for (int sp = init ? -1 : 0; sp < seg; ++sp) {
+        const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
+#pragma unroll
+        for (int r = 0; r < nS4; ++r) {
+          const float4 u = reinterpret_cast<const float4*>(x)[tid + kThreads * r];
+          sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
+        }
+#pragma unroll
+        for (int r = 0; r < nP4; ++r) {
+          const float4 u = reinterpret_cast<const float4*>(x + off_G(D, DV))[tid + kThreads * r];
+          pa[r].x += u.x; pa[r].y += u.y; pa[r].z += u.z; pa[r].w += u.w;
+        }
+        if (tid < D) ea += x[off_h(D, DV) + tid];
       }
-    __syncthreads();
+      float* st = reinterpret_cast<float*>(lds);
+#pragma unroll
+      for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + kThreads * r] = sa[r];
+      if (tid < D) eta[tid] = ea;
+      __syncthreads();
+      if (has_r)
+#pragma unroll
+        for (int i = 0; i < G::DT; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) S0[i][e] = st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < nP4; ++r) reinterpret_cast<float4*>(st)[tid + kThreads * r] = pa[r];
+      __syncthreads();
+      if (has_o)
+#pragma unroll
+        for (int i = 0; i < G::DT; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) P0[i][e] = st[(i * 32 + acc_row(e, lg)) * DV + ct * 32 + lr];
+      __syncthreads();
+    }
   }
   float m_acc = 0.f;   // SUMMARY: column sum of Q for column tid (< D)
 
-  // ---- prefetch registers for the next chunk ----
+  // ---- prefetch registers for the next chunk (buffer loads: the tail past n reads zero) ----
+  const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t rk = make_rsrc(k + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t rv = make_rsrc(v + (size_t)bh * n * DV, (uint32_t)n * DV * 2);
   uint4 pq[G::pfQ], pk[G::pfQ], pv[G::pfV];
   auto fetch = [&](int c) {
-    const int t0 = c * C;
-    if (t0 + C <= n && G::segQ % kThreads == 0 && G::segV % kThreads == 0) {   // full chunk: no guards
-#pragma unroll
-      for (int i = 0; i < G::pfQ; ++i) {
-        const int e = tid + kThreads * i;
-        const size_t off = ((size_t)bh * n + t0 + e % C) * D + (e / C) * 8;
-        pq[i] = *reinterpret_cast<const uint4*>(q + off);
-        pk[i] = *reinterpret_cast<const uint4*>(k + off);
-      }
-#pragma unroll
-      for (int i = 0; i < G::pfV; ++i) {
-        const int e = tid + kThreads * i;
-        pv[i] = *reinterpret_cast<const uint4*>(v + ((size_t)bh * n + t0 + e % C) * DV + (e / C) * 8);
-      }
-      return;
-    }
+    const uint32_t t0 = (uint32_t)c * C;
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
-      const int e = tid + kThreads * i;
-      const int t = e % C, a8 = (e / C) * 8;     // consecutive lanes take consecutive tokens
-      uint4 zq = make_uint4(0, 0, 0, 0), zk = zq;
-      if (e < G::segQ && t0 + t < n) {
-        const size_t off = ((size_t)bh * n + t0 + t) * D + a8;
-        zq = *reinterpret_cast<const uint4*>(q + off);
-        zk = *reinterpret_cast<const uint4*>(k + off);
+      const int e = tid + kThreads * i;        // consecutive lanes take consecutive tokens
+      if (G::segQ % kThreads == 0 || e < G::segQ) {
+        const uint32_t off = ((t0 + e % C) * D + (e / C) * 8) * 2;
+        pq[i] = buf_load16(rq, off);
+        pk[i] = buf_load16(rk, off);
       }
-      pq[i] = zq;
-      pk[i] = zk;
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + kThreads * i;
-      const int t = e % C, b8 = (e / C) * 8;
-      uint4 zv = make_uint4(0, 0, 0, 0);
-      if (e < G::segV && t0 + t < n) zv = *reinterpret_cast<const uint4*>(v + ((size_t)bh * n + t0 + t) * DV + b8);
-      pv[i] = zv;
+      if (G::segV % kThreads == 0 || e < G::segV) pv[i] = buf_load16(rv, ((t0 + e % C) * DV + (e / C) * 8) * 2);
     }
   };
   if (c_begin < c_end) fetch(c_begin);
@@ -549,23 +588,36 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
     }
     __syncthreads();
 
-    // ---- stage 2: R = W K + Q S0 (old S0) on tile (rt, ct); S0 += K^T K on column ct ----
-    f32x16 racc = zero16();
+    // ---- stage 2: R = W K + Q S0 (old S0) on column tile ct; S0 += K^T K on column ct ----
+    f32x16 racc[G::RPW];
+#pragma unroll
+    for (int i = 0; i < G::RPW; ++i) racc[i] = zero16();
     if (has_r) {
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
-        if (s * 16 > rt * 32 + 31) break;         // keys past this row tile: W is zero
         const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
-        racc = mfma(frag(Wh, G::ldW, rt * 32, s * 16), bK, racc);
-        racc = mfma(frag(Wl, G::ldW, rt * 32, s * 16), bK, racc);
+#pragma unroll
+        for (int i = 0; i < G::RPW; ++i) {
+          const int rt = rg + G::NRG * i;
+          if (rt < G::RT && s * 16 <= rt * 32 + 31) {     // keys past the row tile: W is zero
+            racc[i] = mfma(frag(Wh, G::ldW, rt * 32, s * 16), bK, racc[i]);
+            racc[i] = mfma(frag(Wl, G::ldW, rt * 32, s * 16), bK, racc[i]);
+          }
+        }
       }
 #pragma unroll
       for (int s = 0; s < G::KD; ++s) {
         bf16x8 bh, bl;
         frag_from_acc(S0[s >> 1], s & 1, bh, bl);
-        const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, s * 16);
-        racc = mfma(aQ, bh, racc);
-        racc = mfma(aQ, bl, racc);
+#pragma unroll
+        for (int i = 0; i < G::RPW; ++i) {
+          const int rt = rg + G::NRG * i;
+          if (rt < G::RT) {
+            const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, s * 16);
+            racc[i] = mfma(aQ, bh, racc[i]);
+            racc[i] = mfma(aQ, bl, racc[i]);
+          }
+        }
       }
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
@@ -573,20 +625,31 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
 #pragma unroll
         for (int i = 0; i < G::DT; ++i) S0[i] = mfma(frag(Kt, G::ldKt, i * 32, s * 16), bK, S0[i]);
       }
-      // eta advance: column sums of R over this row tile
-      float cs = 0.f;
+      // eta advance: column sums of R over each row tile
 #pragma unroll
-      for (int e = 0; e < 16; ++e) cs += racc[e];
-      cs += __shfl_xor(cs, 32);
-      if (lg == 0) colsum[rt * D + ct * 32 + lr] = cs;
+      for (int i = 0; i < G::RPW; ++i) {
+        const int rt = rg + G::NRG * i;
+        if (rt < G::RT) {
+          float cs = 0.f;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) cs += racc[i][e];
+          cs += __shfl_xor(cs, 32);
+          if (lg == 0) colsum[rt * D + ct * 32 + lr] = cs;
+        }
+      }
     }
     __syncthreads();     // every wave is done reading W: B1 takes R^T
-    if (has_r) {
-      if (SUMMARY)
-        store_T(racc, Rth, Rtl, G::ldRt, rt * 32, ct * 32);
-      else
-        store_TN(racc, Rth, Rtl, G::ldRt, Rh, Rl, G::ldR, rt * 32, ct * 32);
-    }
+    if (has_r)
+#pragma unroll
+      for (int i = 0; i < G::RPW; ++i) {
+        const int rt = rg + G::NRG * i;
+        if (rt < G::RT) {
+          if (SUMMARY)
+            store_T(racc[i], Rth, Rtl, G::ldRt, rt * 32, ct * 32);
+          else
+            store_TN(racc[i], Rth, Rtl, G::ldRt, Rh, Rl, G::ldR, rt * 32, ct * 32);
+        }
+      }
     __syncthreads();
     float eta_add = 0.f;
     if (tid < D)
@@ -637,32 +700,48 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
         den[tid] = 1.f / (s + eps);
       }
       __syncthreads();
-      // ---- stage 4: O = T V + Q Phi0 (old Phi0) on tile (rt, ct); stage 5: Phi0 += R^T V ----
+      // ---- stage 4: O = T V + Q Phi0 (old Phi0) on column tile ct; stage 5: Phi0 += R^T V ----
       if (has_o) {
-        f32x16 oacc = zero16();
+        f32x16 oacc[G::RPW];
+#pragma unroll
+        for (int i = 0; i < G::RPW; ++i) oacc[i] = zero16();
 #pragma unroll
         for (int s = 0; s < G::KC; ++s) {
-          if (s * 16 > rt * 32 + 31) break;       // j past this row tile: T is zero
           const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
-          oacc = mfma(frag(Th, G::ldT, rt * 32, s * 16), bV, oacc);
-          oacc = mfma(frag(Tl, G::ldT, rt * 32, s * 16), bV, oacc);
+#pragma unroll
+          for (int i = 0; i < G::RPW; ++i) {
+            const int rt = rg + G::NRG * i;
+            if (rt < G::RT && s * 16 <= rt * 32 + 31) {   // j past the row tile: T is zero
+              oacc[i] = mfma(frag(Th, G::ldT, rt * 32, s * 16), bV, oacc[i]);
+              oacc[i] = mfma(frag(Tl, G::ldT, rt * 32, s * 16), bV, oacc[i]);
+            }
+          }
         }
 #pragma unroll
         for (int s = 0; s < G::KD; ++s) {
           bf16x8 bh, bl;
           frag_from_acc(P0[s >> 1], s & 1, bh, bl);
-          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, s * 16);
-          oacc = mfma(aQ, bh, oacc);
-          oacc = mfma(aQ, bl, oacc);
+#pragma unroll
+          for (int i = 0; i < G::RPW; ++i) {
+            const int rt = rg + G::NRG * i;
+            if (rt < G::RT) {
+              const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, s * 16);
+              oacc[i] = mfma(aQ, bh, oacc[i]);
+              oacc[i] = mfma(aQ, bl, oacc[i]);
+            }
+          }
         }
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int t = rt * 32 + acc_row(e, lg);
-          if (t0 + t < n) {
-            float o = oacc[e];
-            if (normalized) o *= den[t];
-            out[((size_t)bh * n + t0 + t) * DV + ct * 32 + lr] = o;
-          }
+        for (int i = 0; i < G::RPW; ++i) {
+          const int rt = rg + G::NRG * i;
+          if (rt < G::RT)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer and are dropped
+              const int t = rt * 32 + acc_row(e, lg);
+              float o = oacc[i][e];
+              if (normalized) o *= den[t];
+              buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, o);
+            }
         }
       }
     }
@@ -685,7 +764,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
 
   if (SUMMARY) {
     // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
-    if (has_r && rt == 0)
+    if (has_r && rg == 0)
 #pragma unroll
       for (int i = 0; i < G::DT; ++i)
 #pragma unroll
@@ -708,20 +787,42 @@ __global__ __launch_bounds__(kThreads, 2) void k_walk(const uint16_t* __restrict
 }
 
 struct Shape {
-  int C, D, DV;
+  int C, D, DV, blocks;   // blocks: output-walk workgroups per CU
 };
-constexpr Shape kShapes[] = {{64, 64, 64}, {32, 32, 32}, {64, 32, 32}, {32, 64, 64}, {64, 64, 32}, {64, 32, 64}};
+#define HLA_SHAPE_ROW(C_, D_, DV_) {C_, D_, DV_, Cfg<C_, D_, DV_, false>::kBlocks}
+constexpr Shape kShapes[] = {HLA_SHAPE_ROW(64, 64, 64),  HLA_SHAPE_ROW(32, 32, 32),   HLA_SHAPE_ROW(64, 32, 32),
+                             HLA_SHAPE_ROW(32, 64, 64),  HLA_SHAPE_ROW(64, 64, 32),   HLA_SHAPE_ROW(64, 32, 64),
+                             HLA_SHAPE_ROW(64, 128, 128), HLA_SHAPE_ROW(32, 128, 128)};
+#undef HLA_SHAPE_ROW
+
+// The walk's tile: chunk 32 and 64 are walked as given; chunk 128 is walked
+// in 64-token tiles.  The scan is exact for every chunking (Thm. 2), so the
+// tile changes only the rounding order.
+int fused_tile(int chunk) { return chunk == 32 ? 32 : (chunk == 64 || chunk == 128) ? 64 : 0; }
+
+const Shape* find_shape(int chunk, int d, int dv) {
+  const int C = fused_tile(chunk);
+  for (const Shape& sh : kShapes)
+    if (sh.C == C && sh.D == d && sh.DV == dv) return &sh;
+  return nullptr;
+}
+
+template <int D, int DV>
+hipError_t set_cross_lds(const void* kern, size_t* lds) {
+  *lds = sizeof(float) * ((size_t)D * (D + 4) + (size_t)D * DV + D);
+  return hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)*lds);
+}
 
 template <int C, int D, int DV>
 hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* ws, int P, int cps,
                      hipStream_t s) {
-  const size_t F = state_floats(D, DV);
   const int BH = f.BH;
-  float* segs = reinterpret_cast<float*>(ws);                    // [BH][P][F] segment summaries
+  float* segs = reinterpret_cast<float*>(ws);                    // [BH][P + 1][F] segment records
   const uint16_t* q = static_cast<const uint16_t*>(f.q);
   const uint16_t* k = static_cast<const uint16_t*>(f.k);
   const uint16_t* v = static_cast<const uint16_t*>(f.v);
   const int nsum = final_state ? P : P - 1;                      // segments whose summary is needed
+  const int ncross = nsum + (init ? 1 : 0);                      // + conversion of the initial state
   hipError_t e;
   if (nsum > 0) {
     auto ks = k_walk<C, D, DV, true>;
@@ -734,25 +835,23 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  const bool want_out = f.out != nullptr;
-  if (nsum > 0) {
-    const size_t lds = sizeof(float) * ((size_t)D * (D + 4) + (size_t)D * DV + D);
-    auto kx = k_seg_cross<D, DV>;
-    if ((e = hipFuncSetAttribute((const void*)kx, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess)
-      return e;
+  if (ncross > 0) {
+    size_t lds;
+    if ((e = set_cross_lds<D, DV>((const void*)k_seg_cross<D, DV>, &lds)) != hipSuccess) return e;
     prof_start("seg_cross", s);
-    hipLaunchKernelGGL(kx, dim3(nsum, BH), dim3(256), lds, s, segs, init, P);
+    hipLaunchKernelGGL((k_seg_cross<D, DV>), dim3(ncross, BH), dim3(256), lds, s, segs, init, P, nsum);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (final_state) {
-    const int F4 = (int)(F / 4);
+    size_t lds;
+    if ((e = set_cross_lds<D, DV>((const void*)k_total<D, DV>, &lds)) != hipSuccess) return e;
     prof_start("total", s);
-    hipLaunchKernelGGL(k_total, dim3((F4 + 255) / 256, BH), dim3(256), 0, s, segs, init, final_state, P, nsum, F4);
+    hipLaunchKernelGGL((k_total<D, DV>), dim3(BH), dim3(256), lds, s, segs, init, final_state, P, nsum);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (!want_out) return hipSuccess;
+  if (!f.out) return hipSuccess;
   auto kw = k_walk<C, D, DV, false>;
   const size_t lb = Cfg<C, D, DV, false>::bytes;
   if ((e = hipFuncSetAttribute((const void*)kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lb)) != hipSuccess)
@@ -764,11 +863,11 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   return hipGetLastError();
 }
 
-}  // namespace
-
-void fused_plan(int BH, int n, int chunk, int* P, int* cps) {
-  const int M = (n + chunk - 1) / chunk;
-  int p = 512 / BH;                       // about two workgroups per CU
+// Segments per head: enough output-walk workgroups to fill every CU
+// (HLA_FUSED_SEGMENTS overrides), each segment a whole number of tiles.
+void fused_plan(const Shape& sh, int BH, int n, int* P, int* cps) {
+  const int M = (n + sh.C - 1) / sh.C;
+  int p = 256 * sh.blocks / BH;
   if (const char* e = getenv("HLA_FUSED_SEGMENTS")) p = atoi(e);
   if (p < 1) p = 1;
   if (p > M) p = M;
@@ -776,31 +875,38 @@ void fused_plan(int BH, int n, int chunk, int* P, int* cps) {
   *P = (M + *cps - 1) / *cps;             // every segment non-empty
 }
 
+}  // namespace
+
 bool fused_supported(int n, int d, int dv, int chunk, int dtype, int masked) {
-  if (dtype != 1 || masked != 1 || n < 1) return false;
-  for (const Shape& sh : kShapes)
-    if (sh.C == chunk && sh.D == d && sh.DV == dv) return true;
-  return false;
+  // per-head byte offsets of q/k/v and of the output stay below 2^31
+  const long long span = (long long)n * (d > dv ? d : dv) * 4;
+  return dtype == 1 && masked == 1 && n >= 1 && span < (1LL << 31) && find_shape(chunk, d, dv) != nullptr;
 }
 
 size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
+  const Shape* sh = find_shape(chunk, d, dv);
+  if (!sh) return 0;
   int P, cps;
-  fused_plan(BH, n, chunk, &P, &cps);
-  return sizeof(float) * (size_t)BH * P * state_floats(d, dv) + 256;
+  fused_plan(*sh, BH, n, &P, &cps);
+  return sizeof(float) * (size_t)BH * (P + 1) * state_floats(d, dv) + 256;
 }
 
 hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, void* workspace, hipStream_t s) {
+  const Shape* sh = find_shape(f.chunk, f.d, f.dv);
+  if (!sh) return hipErrorNotSupported;
   int P, cps;
-  fused_plan(f.BH, f.n, f.chunk, &P, &cps);
+  fused_plan(*sh, f.BH, f.n, &P, &cps);
   char* ws = static_cast<char*>(workspace);
 #define HLA_SHAPE(C_, D_, DV_) \
-  if (f.chunk == C_ && f.d == D_ && f.dv == DV_) return run_shape<C_, D_, DV_>(f, init, final_state, ws, P, cps, s);
+  if (sh->C == C_ && sh->D == D_ && sh->DV == DV_) return run_shape<C_, D_, DV_>(f, init, final_state, ws, P, cps, s);
   HLA_SHAPE(64, 64, 64)
   HLA_SHAPE(32, 32, 32)
   HLA_SHAPE(64, 32, 32)
   HLA_SHAPE(32, 64, 64)
   HLA_SHAPE(64, 64, 32)
   HLA_SHAPE(64, 32, 64)
+  HLA_SHAPE(64, 128, 128)
+  HLA_SHAPE(32, 128, 128)
 #undef HLA_SHAPE
   return hipErrorNotSupported;
 }

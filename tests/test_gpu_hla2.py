@@ -24,7 +24,8 @@ from tests.helpers import dev, gen, rowwise_err, tol_for
 pytestmark = pytest.mark.gpu
 
 ALGOS = [capi.HLA_ALGO_CHUNKED, capi.HLA_ALGO_FUSED]
-FUSED_SHAPES = [(64, 64, 64), (32, 32, 32), (64, 32, 32), (32, 64, 64), (64, 64, 32), (64, 32, 64)]
+FUSED_SHAPES = [(64, 64, 64), (32, 32, 32), (64, 32, 32), (32, 64, 64), (64, 64, 32), (64, 32, 64), (64, 128, 128),
+                (32, 128, 128)]
 
 
 def _say(*a):
@@ -180,10 +181,19 @@ def test_fused_matches_chunked_closely():
     assert rowwise_err(a, b) <= 2e-3
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_fused_chunk128_walks_64_token_tiles(d):
+    """chunk=128 is walked in 64-token tiles; the result is the chunk=128 result
+    up to rounding (the scan is exact for any chunking)."""
+    for (B, H, n) in ((1, 2, 3 * 128 + 50), (2, 1, 128)):
+        for normalized in (False, True):
+            assert _check_forward(B, H, n, d, d, 128, "unit", 1, normalized, capi.HLA_ALGO_FUSED, seed=n + d)
+
+
 def test_fused_rejects_unsupported():
-    q = torch.zeros(1, 1, 64, 128, dtype=torch.bfloat16, device="cuda")
+    q = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(capi.HLAError) as ei:
-        hla.forward(q, q, q, 64, algo=capi.HLA_ALGO_FUSED)
+        hla.forward(q, q, q, 16, algo=capi.HLA_ALGO_FUSED)
     assert ei.value.code == capi.HLA_ERR_UNSUPPORTED
     qf = torch.zeros(1, 1, 64, 64, device="cuda")
     with pytest.raises(capi.HLAError):
@@ -253,14 +263,16 @@ def test_prefill_then_steps(dist, masked, normalized):
         assert np.abs(g - e).max() <= 1e-5 * np.abs(e).max()
 
 
+@pytest.mark.parametrize("d,chunk", [(64, 64), (128, 128)])
 @pytest.mark.parametrize("normalized", [0, 1])
-def test_prefill_chain_fused_shape(normalized):
+def test_prefill_chain_fused_shape(normalized, d, chunk):
     """Two chained prefills on a shape the fused path covers (init state in,
     total state out), then decode steps; all against one serial oracle run."""
-    B, H, d, dv, chunk = 2, 3, 64, 64, 64
+    B, H, dv = 2, 3, d
     n1, n2, steps = 5 * 64 + 9, 7 * 64 + 40, 6
     q, k, v, code = gen(B, H, n1 + n2 + steps, d, dv, "unit", 31)
-    _say(f"case fused-shape prefill chain normalized={normalized}")
+    assert _supported(capi.HLA_ALGO_FUSED, n1, d, dv, chunk, code, 1)
+    _say(f"case fused-shape prefill chain d={d} chunk={chunk} normalized={normalized}")
     eps = 0.5 if normalized else 1e-6
     num_ref, den_ref, fin_ref = _oracle(q, k, v, True)
     ref = num_ref / (den_ref + eps)[..., None] if normalized else num_ref
