@@ -786,8 +786,398 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
   }
 }
 
+// ---------------------------------------------------------------------------
+// Row-split walk (C = 64, D = DV): 2 x NCT waves.  Wave (h, ct) keeps rows
+// [h D/2, (h+1) D/2) of column tile ct of S0 and of Phi0, so every state
+// element is held, advanced and split by exactly one wave.  R = W K + Q S0
+// and O = T V + Q Phi0 contract over the state rows: each wave forms the
+// partial over its half for both row tiles, hands the partial of the other
+// row tile to its partner (h' = 1 - h, same ct) through LDS in fp32, and
+// finishes row tile rt = h with the partner's half and the W K (or T V)
+// term.  The exchange slots reuse K | K^T (for R; K is dead after the S0
+// advance) and the R buffer (for O; R is dead after T).
+template <int D, bool SUMMARY>
+struct CfgRS {
+  static constexpr int C = 64, DV = D;
+  static constexpr int NCT = D / 32, NW = 2 * NCT, NT = 64 * NW;
+  static constexpr int HT = NCT / 2, HALF = D / 2;             // 32-row state tiles per half
+  static constexpr int RT = 2, KC = C / 16, KH = D / 32;        // k-steps over tokens / over a half
+  static constexpr int ldQ = D + kPad, ldK = D + kPad, ldKt = C + kPad, ldVt = C + kPad;
+  static constexpr int ld1 = C + kPad, ld2 = D + kPad, ldT = C + kPad, ldQt = C + kPad;
+  static constexpr int oQ = 0;
+  static constexpr int oK = oQ + C * ldQ;
+  static constexpr int oKt = oK + C * ldK;
+  static constexpr int oVt = oKt + D * ldKt;
+  static constexpr int oB1h = oVt + DV * ldVt;                 // W, then R^T
+  static constexpr int oB1l = oB1h + D * ld1;
+  static constexpr int oB2h = oB1l + D * ld1;                  // R (then the O exchange) | Q^T (summary)
+  static constexpr int oB2l = oB2h + C * ld2;
+  static constexpr int n16 = SUMMARY ? oB2h + D * ldQt : oB2l + C * ld2;
+  static constexpr int oX = oK;                                // R exchange, then T (hi | lo)
+  static constexpr int oTh = oK, oTl = oK + C * ldT;
+  static constexpr int xfl = 2 * NCT * 1024;                   // exchange floats
+  static_assert(2 * xfl <= oVt - oK && 2 * C * ldT <= oVt - oK, "exchange and T fit K | K^T");
+  static_assert(SUMMARY || 2 * xfl <= 2 * C * ld2, "O exchange fits the R buffer");
+  static constexpr int f_eta = 0, f_cs = D, f_den = D + RT * D, f_denp = f_den + C;
+  static constexpr int nf32 = f_denp + RT * C;
+  static constexpr size_t bytes = (size_t)((n16 + 7) & ~7) * 2 + (size_t)nf32 * 4;
+  static constexpr int kBlocks = 2 * bytes <= 160 * 1024 && NW <= 4 ? 2 : 1;
+  static constexpr int segQ = C * D / 8, pfQ = segQ / NT, pfV = C * DV / 8 / NT;
+  static_assert(segQ % NT == 0 && pfQ >= 1 && (C * D / NT) == 16, "staging and den split");
+  static_assert(D == 64 || D == 128, "row-split shapes");
+  static_assert(bytes <= 160 * 1024, "LDS budget");
+};
+
+// Exchange slot of (column tile ct, row tile rt): 32 x 32 fp32 in MFMA
+// accumulator order, element 4q + j of lane l at [(slot * 4 + q) * 64 + l] * 4 + j.
+__device__ __forceinline__ void xch_put(float* X, int slot, const f32x16& a) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<float4*>(X + ((slot * 4 + q) * 64 + l) * 4) = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
+}
+__device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 u = *reinterpret_cast<const float4*>(X + ((slot * 4 + q) * 64 + l) * 4);
+    a[4 * q] += u.x; a[4 * q + 1] += u.y; a[4 * q + 2] += u.z; a[4 * q + 3] += u.w;
+  }
+}
+
+template <int D, bool SUMMARY>
+__global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlocks)) void k_walk_rs(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    float* __restrict__ out, float* __restrict__ rec, const float* __restrict__ init, int n, int cps, int nseg,
+    int normalized, float eps) {
+  using G = CfgRS<D, SUMMARY>;
+  constexpr int C = G::C, DV = G::DV, NT = G::NT;
+  extern __shared__ __align__(16) uint16_t lds[];
+  uint16_t* Qs = lds + G::oQ;
+  uint16_t* Ks = lds + G::oK;
+  uint16_t* Kt = lds + G::oKt;
+  uint16_t* Vt = lds + G::oVt;
+  uint16_t* Wh = lds + G::oB1h;   // W, then R^T
+  uint16_t* Wl = lds + G::oB1l;
+  uint16_t* Rh = lds + G::oB2h;   // R
+  uint16_t* Rl = lds + G::oB2l;
+  uint16_t* Qt = lds + G::oB2h;   // summaries
+  uint16_t* Th = lds + G::oTh;
+  uint16_t* Tl = lds + G::oTl;
+  float* XR = reinterpret_cast<float*>(lds + G::oX);     // R exchange
+  float* XO = reinterpret_cast<float*>(lds + G::oB2h);   // O exchange
+  float* fl = reinterpret_cast<float*>(lds + ((G::n16 + 7) & ~7));
+  float* eta = fl + G::f_eta;
+  float* colsum = fl + G::f_cs;       // [RT][D]
+  float* den = fl + G::f_den;         // [C]
+  float* denp = fl + G::f_denp;       // [RT][C]
+
+  const int seg = blockIdx.x, bh = blockIdx.y;
+  const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = w / G::NCT, ct = w % G::NCT;          // state row half, column tile
+  const int r0 = h * G::HALF;                         // first state row of this wave
+  const int M = (n + C - 1) / C;
+  const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
+  const size_t F = state_floats(D, DV);
+  float* rc = SUMMARY ? rec + ((size_t)bh * (nseg + 1) + seg) * F : nullptr;
+  const rsrc_t ro = make_rsrc(SUMMARY ? nullptr : out + (size_t)bh * n * DV, SUMMARY ? 0u : (uint32_t)n * DV * 4);
+
+  // ---- carry in: rows r0 .. r0 + D/2 of column tile ct ----
+  f32x16 S0[G::HT], P0[G::HT], Cs[SUMMARY ? G::HT : 1];
+#pragma unroll
+  for (int i = 0; i < G::HT; ++i) {
+    S0[i] = zero16();
+    P0[i] = zero16();
+    if (SUMMARY) Cs[SUMMARY ? i : 0] = zero16();
+  }
+  for (int a = tid; a < D; a += NT) eta[a] = 0.f;
+  if constexpr (!SUMMARY) {
+    if (seg > 0 || init) {
+      constexpr int nS4 = D * D / 4 / NT;
+      static_assert(D * D % (4 * NT) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
+      float4 sa[nS4], pa[nS4];
+      float ea = 0.f;
+      const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int r = 0; r < nS4; ++r) sa[r] = pa[r] = z4;
+      for (int sp = init ? -1 : 0; sp < seg; ++sp) {
+        const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
+#pragma unroll
+        for (int r = 0; r < nS4; ++r) {
+          const float4 u = reinterpret_cast<const float4*>(x)[tid + NT * r];
+          const float4 g = reinterpret_cast<const float4*>(x + off_G(D, DV))[tid + NT * r];
+          sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
+          pa[r].x += g.x; pa[r].y += g.y; pa[r].z += g.z; pa[r].w += g.w;
+        }
+        if (tid < D) ea += x[off_h(D, DV) + tid];
+      }
+      float* st = reinterpret_cast<float*>(lds);
+#pragma unroll
+      for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = sa[r];
+      if (tid < D) eta[tid] = ea;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < G::HT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S0[i][e] = st[(r0 + i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = pa[r];
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < G::HT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) P0[i][e] = st[(r0 + i * 32 + acc_row(e, lg)) * DV + ct * 32 + lr];
+      __syncthreads();
+    }
+  }
+  float m_acc = 0.f;   // SUMMARY: column sum of Q for column tid (< D)
+
+  // ---- prefetch registers for the next chunk (buffer loads: the tail past n reads zero) ----
+  const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t rk = make_rsrc(k + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t rv = make_rsrc(v + (size_t)bh * n * DV, (uint32_t)n * DV * 2);
+  uint4 pq[G::pfQ], pk[G::pfQ], pv[G::pfV];
+  auto fetch = [&](int c) {
+    const uint32_t t0 = (uint32_t)c * C;
+#pragma unroll
+    for (int i = 0; i < G::pfQ; ++i) {
+      const int e = tid + NT * i;        // consecutive lanes take consecutive tokens
+      const uint32_t off = ((t0 + e % C) * D + (e / C) * 8) * 2;
+      pq[i] = buf_load16(rq, off);
+      pk[i] = buf_load16(rk, off);
+    }
+#pragma unroll
+    for (int i = 0; i < G::pfV; ++i) {
+      const int e = tid + NT * i;
+      pv[i] = buf_load16(rv, ((t0 + e % C) * DV + (e / C) * 8) * 2);
+    }
+  };
+  if (c_begin < c_end) fetch(c_begin);
+
+  for (int c = c_begin; c < c_end; ++c) {
+    const int t0 = c * C;
+    // ---- stage 0: registers -> LDS (Q, K row-major; K^T, V^T; Q^T for summaries) ----
+#pragma unroll
+    for (int i = 0; i < G::pfQ; ++i) {
+      const int e = tid + NT * i;
+      const int t = e % C, a8 = (e / C) * 8;
+      *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
+      *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
+      const uint16_t* kk = reinterpret_cast<const uint16_t*>(&pk[i]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) Kt[(a8 + j) * G::ldKt + t] = kk[j];
+      if (SUMMARY) {
+        const uint16_t* qq = reinterpret_cast<const uint16_t*>(&pq[i]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) Qt[(a8 + j) * G::ldQt + t] = qq[j];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < G::pfV; ++i) {
+      const int e = tid + NT * i;
+      const int t = e % C, b8 = (e / C) * 8;
+      const uint16_t* vv = reinterpret_cast<const uint16_t*>(&pv[i]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) Vt[(b8 + j) * G::ldVt + t] = vv[j];
+    }
+    __syncthreads();
+    if (c + 1 < c_end) fetch(c + 1);
+    if (SUMMARY && tid < D) {
+      const uint16_t* row = Qt + tid * G::ldQt;
+#pragma unroll
+      for (int t8 = 0; t8 < C; t8 += 8) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row + t8);
+        const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m_acc += bf16_to_f(e8[j]);
+      }
+    }
+
+    // ---- stage 1: W = L (.) Q K^T on tiles (key it <= query jt), stored transposed ----
+    if (w < 4) {
+      const int it = w >> 1, jt = w & 1;
+      if (it <= jt) {
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s)
+          acc = mfma(frag(Ks, G::ldK, it * 32, s * 16), frag(Qs, G::ldQ, jt * 32, s * 16), acc);
+#pragma unroll
+        for (int e = 0; e < 16; ++e)   // keep key i <= query t
+          if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
+        store_T(acc, Wh, Wl, G::ld1, it * 32, jt * 32);
+      }
+    }
+    __syncthreads();
+
+    // ---- stage 2: R partials over this wave's state rows (both row tiles), then W K on row tile h ----
+    f32x16 part[2];
+    part[0] = zero16();
+    part[1] = zero16();
+#pragma unroll
+    for (int j = 0; j < G::KH; ++j) {
+      bf16x8 bh_, bl_;
+      frag_from_acc(S0[j >> 1], j & 1, bh_, bl_);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, r0 + j * 16);
+        part[rt] = mfma(aQ, bh_, part[rt]);
+        part[rt] = mfma(aQ, bl_, part[rt]);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < G::KC; ++s) {
+      const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
+      if (h == 0) {
+        if (s < 2) {
+          part[0] = mfma(frag(Wh, G::ld1, 0, s * 16), bK, part[0]);
+          part[0] = mfma(frag(Wl, G::ld1, 0, s * 16), bK, part[0]);
+        }
+      } else {
+        part[1] = mfma(frag(Wh, G::ld1, 32, s * 16), bK, part[1]);
+        part[1] = mfma(frag(Wl, G::ld1, 32, s * 16), bK, part[1]);
+      }
+      // S0 += K^T K on this wave's rows
+#pragma unroll
+      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag(Kt, G::ldKt, r0 + i * 32, s * 16), bK, S0[i]);
+    }
+    __syncthreads();                      // K, K^T and W are dead: K | K^T takes the exchange
+    xch_put(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0]);
+    __syncthreads();
+    f32x16 racc = h == 0 ? part[0] : part[1];
+    xch_add(XR, ct * 2 + h, racc);
+    {
+      float cs = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) cs += racc[e];
+      cs += __shfl_xor(cs, 32);
+      if (lg == 0) colsum[h * D + ct * 32 + lr] = cs;
+    }
+    if (SUMMARY)
+      store_T(racc, Wh, Wl, G::ld1, h * 32, ct * 32);
+    else
+      store_TN(racc, Wh, Wl, G::ld1, Rh, Rl, G::ld2, h * 32, ct * 32);
+    __syncthreads();
+    float eta_add = 0.f;
+    if (tid < D) eta_add = colsum[tid] + colsum[D + tid];
+
+    f32x16 oacc[2];
+    if (!SUMMARY) {
+      // ---- stage 3: T = L (.) Q R^T (as T^T = R Q^T) on tiles j it <= t jt; stored transposed in K | K^T ----
+      if (w < 4) {
+        const int it = w >> 1, jt = w & 1;
+        if (it <= jt) {
+          f32x16 acc = zero16();
+#pragma unroll
+          for (int s = 0; s < D / 16; ++s) {
+            const bf16x8 b = frag(Qs, G::ldQ, jt * 32, s * 16);
+            acc = mfma(frag(Rh, G::ld2, it * 32, s * 16), b, acc);
+            acc = mfma(frag(Rl, G::ld2, it * 32, s * 16), b, acc);
+          }
+#pragma unroll
+          for (int e = 0; e < 16; ++e)     // keep j <= t
+            if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
+          float ps = 0.f;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) ps += acc[e];
+          ps += __shfl_xor(ps, 32);
+          if (lg == 0) denp[it * C + jt * 32 + lr] = ps;
+          store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);
+        } else if (lg == 0) {
+          denp[it * C + jt * 32 + lr] = 0.f;
+        }
+      }
+      // ---- stage 4a: O partials Q Phi0 (old Phi0) over this wave's rows ----
+      oacc[0] = zero16();
+      oacc[1] = zero16();
+#pragma unroll
+      for (int j = 0; j < G::KH; ++j) {
+        bf16x8 bh_, bl_;
+        frag_from_acc(P0[j >> 1], j & 1, bh_, bl_);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, r0 + j * 16);
+          oacc[rt] = mfma(aQ, bh_, oacc[rt]);
+          oacc[rt] = mfma(aQ, bl_, oacc[rt]);
+        }
+      }
+    }
+    // ---- stage 5: Phi0 += R^T V (and, for summaries, C += Q^T V) on this wave's rows ----
+#pragma unroll
+    for (int s = 0; s < G::KC; ++s) {
+      const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
+#pragma unroll
+      for (int i = 0; i < G::HT; ++i) {
+        P0[i] = mfma(frag(Wh, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
+        P0[i] = mfma(frag(Wl, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
+        if (SUMMARY) Cs[SUMMARY ? i : 0] = mfma(frag(Qt, G::ldQt, r0 + i * 32, s * 16), bV, Cs[SUMMARY ? i : 0]);
+      }
+    }
+    if (!SUMMARY) {
+      __syncthreads();                    // T and denp visible; R and R^T are dead
+      xch_put(XO, ct * 2 + (1 - h), h == 0 ? oacc[1] : oacc[0]);
+      // den_t = sum_j T[t][j] + q_t . eta0 (8 or 4 threads per token, 16 dims each)
+      if (normalized) {
+        constexpr int TPR = NT / C;
+        const int t = tid / TPR, a0 = (tid % TPR) * 16;
+        const uint16_t* row = Qs + t * G::ldQ + a0;
+        float sd = 0.f;
+#pragma unroll
+        for (int a8 = 0; a8 < 16; a8 += 8) {
+          const uint4 u = *reinterpret_cast<const uint4*>(row + a8);
+          const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) sd += bf16_to_f(e8[j]) * eta[a0 + a8 + j];
+        }
+#pragma unroll
+        for (int o = 1; o < TPR; o <<= 1) sd += __shfl_xor(sd, o);
+        if (tid % TPR == 0) den[t] = 1.f / (sd + denp[t] + denp[C + t] + eps);
+      }
+      __syncthreads();
+      f32x16 o = h == 0 ? oacc[0] : oacc[1];
+      xch_add(XO, ct * 2 + h, o);
+      // ---- stage 4b: O (row tile h) += T V ----
+#pragma unroll
+      for (int s = 0; s < G::KC; ++s) {
+        if (h == 0 && s >= 2) break;      // j past row tile 0: T is zero
+        const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
+        o = mfma(frag(Th, G::ldT, h * 32, s * 16), bV, o);
+        o = mfma(frag(Tl, G::ldT, h * 32, s * 16), bV, o);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer and are dropped
+        const int t = h * 32 + acc_row(e, lg);
+        float y = o[e];
+        if (normalized) y *= den[t];
+        buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, y);
+      }
+    }
+    __syncthreads();   // LDS tiles and den/eta are rewritten by the next chunk
+    if (tid < D) eta[tid] += eta_add;
+  }
+
+  if (SUMMARY) {
+    // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
+#pragma unroll
+    for (int i = 0; i < G::HT; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = r0 + i * 32 + acc_row(e, lg);
+        rc[(size_t)row * D + ct * 32 + lr] = S0[i][e];
+        rc[off_G(D, DV) + (size_t)row * DV + ct * 32 + lr] = P0[i][e];
+        rc[off_C(D, DV) + (size_t)row * DV + ct * 32 + lr] = Cs[SUMMARY ? i : 0][e];
+      }
+    __syncthreads();
+    if (tid < D) {
+      rc[off_m(D, DV) + tid] = m_acc;
+      rc[off_h(D, DV) + tid] = eta[tid];
+    }
+  }
+}
+
 struct Shape {
-  int C, D, DV, blocks;   // blocks: output-walk workgroups per CU
+  int C, D, DV, blocks;   // blocks: output-walk workgroups per CU (column layout)
 };
 #define HLA_SHAPE_ROW(C_, D_, DV_) {C_, D_, DV_, Cfg<C_, D_, DV_, false>::kBlocks}
 constexpr Shape kShapes[] = {HLA_SHAPE_ROW(64, 64, 64),  HLA_SHAPE_ROW(32, 32, 32),   HLA_SHAPE_ROW(64, 32, 32),
@@ -813,7 +1203,32 @@ hipError_t set_cross_lds(const void* kern, size_t* lds) {
   return hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)*lds);
 }
 
-template <int C, int D, int DV>
+// Launch configuration of one walk kernel (function, threads, LDS bytes).
+struct WalkK {
+  const void* fn;
+  int threads;
+  size_t lds;
+};
+
+template <int C, int D, int DV, bool SUMMARY, bool RS>
+WalkK walk_kernel() {
+  if constexpr (RS) {
+    return {(const void*)k_walk_rs<D, SUMMARY>, CfgRS<D, SUMMARY>::NT, CfgRS<D, SUMMARY>::bytes};
+  } else {
+    return {(const void*)k_walk<C, D, DV, SUMMARY>, kThreads, Cfg<C, D, DV, SUMMARY>::bytes};
+  }
+}
+
+hipError_t launch_walk(const WalkK& kk, dim3 grid, hipStream_t s, const uint16_t* q, const uint16_t* k,
+                       const uint16_t* v, float* out, float* rec, const float* init, int n, int cps, int nseg,
+                       int normalized, float eps) {
+  hipError_t e = hipFuncSetAttribute(kk.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kk.lds);
+  if (e != hipSuccess) return e;
+  void* args[] = {&q, &k, &v, &out, &rec, &init, &n, &cps, &nseg, &normalized, &eps};
+  return hipLaunchKernel(kk.fn, grid, dim3(kk.threads), args, kk.lds, s);
+}
+
+template <int C, int D, int DV, bool RS>
 hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* ws, int P, int cps,
                      hipStream_t s) {
   const int BH = f.BH;
@@ -825,15 +1240,11 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   const int ncross = nsum + (init ? 1 : 0);                      // + conversion of the initial state
   hipError_t e;
   if (nsum > 0) {
-    auto ks = k_walk<C, D, DV, true>;
-    const size_t lb = Cfg<C, D, DV, true>::bytes;
-    if ((e = hipFuncSetAttribute((const void*)ks, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lb)) != hipSuccess)
-      return e;
     prof_start("walk_summary", s);
-    hipLaunchKernelGGL(ks, dim3(nsum, BH), dim3(kThreads), lb, s, q, k, v, (float*)nullptr, segs,
-                       (const float*)nullptr, f.n, cps, P, 0, 0.f);
+    e = launch_walk(walk_kernel<C, D, DV, true, RS>(), dim3(nsum, BH), s, q, k, v, nullptr, segs, nullptr, f.n,
+                    cps, P, 0, 0.f);
     prof_stop(s);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
   }
   if (ncross > 0) {
     size_t lds;
@@ -852,22 +1263,28 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (!f.out) return hipSuccess;
-  auto kw = k_walk<C, D, DV, false>;
-  const size_t lb = Cfg<C, D, DV, false>::bytes;
-  if ((e = hipFuncSetAttribute((const void*)kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lb)) != hipSuccess)
-    return e;
   prof_start("walk", s);
-  hipLaunchKernelGGL(kw, dim3(P, BH), dim3(kThreads), lb, s, q, k, v, f.out, segs, init, f.n, cps, P,
-                     f.normalized, f.eps);
+  e = launch_walk(walk_kernel<C, D, DV, false, RS>(), dim3(P, BH), s, q, k, v, f.out, segs, init, f.n, cps, P,
+                  f.normalized, f.eps);
   prof_stop(s);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 
 // Segments per head: enough output-walk workgroups to fill every CU
 // (HLA_FUSED_SEGMENTS overrides), each segment a whole number of tiles.
+// (64, 64, 64) and (64, 128, 128) walk in the row-split layout; the other
+// shapes in the column layout.
+bool row_split_shape(const Shape& sh) { return sh.C == 64 && sh.D == sh.DV && (sh.D == 64 || sh.D == 128); }
+
+int plan_blocks(const Shape& sh) {
+  if (row_split_shape(sh)) return sh.D == 64 ? CfgRS<64, false>::kBlocks : CfgRS<128, false>::kBlocks;
+  return sh.blocks;
+}
+
 void fused_plan(const Shape& sh, int BH, int n, int* P, int* cps) {
   const int M = (n + sh.C - 1) / sh.C;
-  int p = 256 * sh.blocks / BH;
+  int p = 256 * plan_blocks(sh) / BH;
   if (const char* e = getenv("HLA_FUSED_SEGMENTS")) p = atoi(e);
   if (p < 1) p = 1;
   if (p > M) p = M;
@@ -897,8 +1314,12 @@ hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, voi
   int P, cps;
   fused_plan(*sh, f.BH, f.n, &P, &cps);
   char* ws = static_cast<char*>(workspace);
+  if (row_split_shape(*sh)) {
+    if (sh->D == 64) return run_shape<64, 64, 64, true>(f, init, final_state, ws, P, cps, s);
+    return run_shape<64, 128, 128, true>(f, init, final_state, ws, P, cps, s);
+  }
 #define HLA_SHAPE(C_, D_, DV_) \
-  if (sh->C == C_ && sh->D == D_ && sh->DV == DV_) return run_shape<C_, D_, DV_>(f, init, final_state, ws, P, cps, s);
+  if (sh->C == C_ && sh->D == D_ && sh->DV == DV_) return run_shape<C_, D_, DV_, false>(f, init, final_state, ws, P, cps, s);
   HLA_SHAPE(64, 64, 64)
   HLA_SHAPE(32, 32, 32)
   HLA_SHAPE(64, 32, 32)
