@@ -116,6 +116,55 @@ def traffic_for(kernel, workload):
     return e.get("bytes_per_launch")
 
 
+def kernel_key(name):
+    """Bench name of a library kernel from its (demangled) dispatch name."""
+    if "k_walk" in name:
+        return "walk_summary" if ("true" in name or "Lb1E" in name) else "walk"
+    for key in ("k_seg_cross", "k_total", "k_scan", "k_chunk_summary", "k_readout", "k_step"):
+        if key in name:
+            return key[2:]
+    return None
+
+
+def ingest_counters(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes):
+    """Per-launch HBM bytes of each kernel from two rocprofv3 --pmc runs
+    (FETCH_SIZE, WRITE_SIZE; KiB per dispatch), each scaled by what the same
+    counter reads for a plain copy of copy_bytes bytes.  Updates
+    profiles/hbm_traffic.json under the workload, keyed by the source hash."""
+    import csv
+    import collections
+
+    def per_kernel(path):
+        acc = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return acc
+
+    def copy_kib(path):
+        vals = [v for name, vs in per_kernel(path).items() if kernel_key(name) is None for v in vs]
+        return max(vals)
+
+    f_scale = copy_bytes / (copy_kib(copy_fetch_csv) * 1024)
+    w_scale = copy_bytes / (copy_kib(copy_write_csv) * 1024)
+    fetch, write = per_kernel(fetch_csv), per_kernel(write_csv)
+    out = {}
+    for name, vals in fetch.items():
+        key = kernel_key(name)
+        if key is None or name not in write:
+            continue
+        fb = sum(vals) / len(vals) * 1024 * f_scale
+        wb = sum(write[name]) / len(write[name]) * 1024 * w_scale
+        out[key] = {"bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
+                    "dispatches": len(vals), "source_sha": source_sha(),
+                    "fetch_scale": f_scale, "write_scale": w_scale}
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    rec = json.load(open(path)) if os.path.exists(path) else {}
+    rec[workload] = out
+    with open(path, "w") as fh:
+        json.dump(rec, fh, indent=1, sort_keys=True)
+    print(json.dumps({workload: out}, indent=1))
+
+
 def source_sha():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2510_27258_amd", "csrc")
@@ -222,7 +271,12 @@ def main():
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone scan measurement")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
+    ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="write profiles/hbm_traffic.json for --workload from counter CSVs (with --copy-bytes)")
     args = ap.parse_args()
+    if args.ingest_counters:
+        ingest_counters(args.workload, *args.ingest_counters, args.copy_bytes)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (heads or sequence segments would "

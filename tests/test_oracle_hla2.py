@@ -144,6 +144,29 @@ def test_combine_associative_random():
         np.testing.assert_array_equal(x, y)
 
 
+def test_phi_form_composition():
+    """Eq. (semidirect) in the variables Phi = S C - G, eta = S m - h:
+    Phi_{A(+)B} = Phi_A + Phi_B + S_A C_B and eta_{A(+)B} = eta_A + eta_B + S_A m_B
+    (the form in which the fused path composes segments), on token segments."""
+    q, k, v = _rand((2, 13, 4), 3, seed=41)
+    A = H.segment_summary(q[:, :6], k[:, :6], v[:, :6])
+    B = H.segment_summary(q[:, 6:], k[:, 6:], v[:, 6:])
+    AB = H.combine(A, B)
+    phi = lambda X: X[0] @ X[1] - X[3]
+    eta = lambda X: np.einsum("...ij,...j->...i", X[0], X[2]) - X[4]
+    np.testing.assert_allclose(phi(AB), phi(A) + phi(B) + A[0] @ B[1], rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(eta(AB), eta(A) + eta(B) + np.einsum("...ij,...j->...i", A[0], B[2]),
+                               rtol=1e-11, atol=1e-11)
+    # Phi of a prefix state is sum_{j<=t} S_j q_j v_j^T (the proof of Thm. 1)
+    _, fin = H.hla2_serial(q, k, v)
+    direct = np.zeros_like(fin[1])
+    S = np.zeros_like(fin[0])
+    for t in range(q.shape[1]):
+        S = S + np.einsum("...i,...j->...ij", k[:, t], k[:, t])
+        direct += np.einsum("...i,...j->...ij", np.einsum("...ij,...j->...i", S, q[:, t]), v[:, t])
+    np.testing.assert_allclose(phi(fin), direct, rtol=1e-11, atol=1e-11)
+
+
 def test_segment_summary_equals_serial_state():
     q, k, v = _rand((3, 10, 5), 4, seed=6)
     summ = H.segment_summary(q, k, v)
