@@ -8,182 +8,225 @@
 //
 // The only cross-segment product is S_c C_acc, where C_acc is an additive
 // prefix, so the work splits over column blocks of C and G.  One workgroup
-// owns (head, column block) and streams the head's segments in order; block
-// 0 also carries S, m and h.  The column blocks of one head are placed on the
-// same XCD so the segment's S tile, read by each of them, is served from
-// that XCD's L2.
+// owns (head, column block) and streams the head's segments in order; the
+// blocks also share out the rows of S and h, and block 0 carries m.  The
+// column blocks of one head are placed on the same XCD so the segment's S
+// tile, read by each of them, is served from that XCD's L2.
+#include <type_traits>
+
 #include "common.h"
 
 namespace hla {
 
-constexpr int kScanCols = 16;   // value columns of C and G per workgroup
+// Columns of C and G per workgroup.  Narrow blocks give more workgroups per
+// head (more loads in flight) but every block re-reads S_c (from L2 after the
+// first) and moves C/G in short row pieces; measured best: 4 columns at
+// d = 64, 16 at d = 128.
+constexpr int scan_cols(int d) { return d == 16 ? 16 : d == 32 ? 8 : d == 64 ? 4 : 16; }
 
-// One workgroup per (head, 16 columns of C/G); block 0 also carries S, m, h.
-// The next segment's loads are issued before the current segment's
-// cross-term product, so memory latency overlaps the arithmetic.
+// Scan geometry for key dimension d: the product S_c C_acc of a workgroup
+// (d x d times d x CB) gives each of the 256 threads one row a and NB
+// adjacent columns; S_c and C_acc are double-buffered in LDS when both
+// copies fit, so a step needs one barrier.
 template <int d>
+struct ScanCfg {
+  static constexpr int CB = scan_cols(d), NB = d * CB / 256, TPR = CB / NB;
+  static constexpr int ldS = d + 4;
+  static constexpr int NBUF = 2 * d * ldS * 4 <= 80 * 1024 ? 2 : 1;
+  static constexpr int nS4 = d * d / 4 / 256 > 0 ? d * d / 4 / 256 : 1;   // float4 of S_c per thread
+  static constexpr int nC4 = (d * CB / 4 + 255) / 256;                    // float4 of a C or G block
+  static constexpr int PF = d <= 64 ? 2 : 1;                              // segments loaded ahead
+  static constexpr size_t lds_floats = (size_t)NBUF * (d * ldS + d * CB) + d;
+  static_assert(NB >= 1 && CB % NB == 0 && 256 / TPR == d && CB % 4 == 0 && PF <= 4, "one row per thread group");
+};
+
+// One workgroup per (head, CB columns of C/G); NBLK = dv / CB blocks per
+// head.  Block blk also owns rows [r0, r1) of S and h (S_acc and h_acc of
+// those rows), and block 0 owns m.
+template <int d, int NBLK>
 __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, const float* __restrict__ init,
                                               float* __restrict__ prefix, float* __restrict__ total,
                                               int BH, int M, int dv, int nblk, size_t in_stride,
                                               size_t pre_stride, size_t tot_stride) {
-  constexpr int CB = kScanCols;
-  constexpr int ldS = d + 4;
-  constexpr int nSS = (d * d + 255) / 256;      // S elements per thread
-  constexpr int nCC = (d * CB + 255) / 256;     // C-block elements per thread
+  using K = ScanCfg<d>;
+  constexpr int CB = K::CB, NB = K::NB, ldS = K::ldS, nC4 = K::nC4;
   extern __shared__ float smem[];
-  float* ScT = smem;                       // [d][d+4]: ScT[a'][a] = S_c[a][a']
-  float* Cacc = ScT + d * ldS;             // [d][CB]
-  float* Cnew = Cacc + d * CB;             // [d][CB]
-  float* macc = Cnew + d * CB;             // [d]
+  float* Sbuf = smem;                              // [NBUF][d][ldS]   S_c
+  float* Cbuf = Sbuf + K::NBUF * d * ldS;          // [NBUF][d][CB]    C_acc before segment c
+  float* macc = Cbuf + K::NBUF * d * CB;           // [d]
   const int tid = threadIdx.x;
   const int L = blockIdx.x;
-  const int group = L / (8 * nblk), within = L % (8 * nblk);
-  const int bh = group * 8 + within % 8;
+  const int group = L / (8 * NBLK), within = L % (8 * NBLK);
+  const int bh = group * 8 + within % 8;          // one head's blocks share an XCD (and its L2)
   const int blk = within / 8;
   if (bh >= BH) return;
   const int c0 = blk * CB;
+  constexpr int rows = (d + NBLK - 1) / NBLK;
+  const int r0 = min(d, blk * rows), r1 = min(d, r0 + rows);
   const size_t F = state_floats(d, dv);
   const size_t oC = off_C(d, dv), om = off_m(d, dv), oG = off_G(d, dv), oh = off_h(d, dv);
   const float* in = states + (size_t)bh * in_stride;
   float* pre = prefix + (size_t)bh * pre_stride;
   const float* ini = init ? init + (size_t)bh * F : nullptr;
-  // cross-term tile: thread -> rows 4*aq .. 4*aq+3, columns 4*jq .. 4*jq+3 of the block
-  const int jq = tid % (CB / 4), aq = tid / (CB / 4);
-  const bool active = aq * 4 < d;
-  const int gr = active ? aq * 4 : 0;
+  const int a = tid / K::TPR, j0 = (tid % K::TPR) * NB;     // product: row a, columns c0 + j0 ..
+  const int nown = (r1 - r0) * d;                            // S elements owned by this block
+  // float4 e of a C or G block: row e / (CB/4), columns c0 + 4 (e % (CB/4)) ..
+  auto blk_off = [&](int e) { return (size_t)(e / (CB / 4)) * dv + c0 + 4 * (e % (CB / 4)); };
+  auto ld4 = [](const float* p) { return *reinterpret_cast<const float4*>(p); };
+  auto st4 = [](float* p, const float4& v) { *reinterpret_cast<float4*>(p) = v; };
 
-  float sacc[nSS], gacc[4][4], hacc = 0.f;
+  // carried state: S_acc (own rows; element e = tid + 256 i), G_acc row a, h_acc (own rows)
+  constexpr int nSO = (rows * d + 255) / 256;
+  float sacc[nSO], gacc[NB], hacc = 0.f;
 #pragma unroll
-  for (int r = 0; r < nSS; ++r) {
-    const int idx = tid + 256 * r;
-    sacc[r] = (ini && blk == 0 && idx < d * d) ? ini[idx] : 0.f;
+  for (int i = 0; i < nSO; ++i) {
+    const int e = tid + 256 * i;
+    sacc[i] = (ini && e < nown) ? ini[(size_t)r0 * d + e] : 0.f;
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      gacc[i][j] = (ini && active) ? ini[oG + (size_t)(gr + i) * dv + c0 + jq * 4 + j] : 0.f;
-#pragma unroll
-  for (int r = 0; r < nCC; ++r) {
-    const int idx = tid + 256 * r;
-    if (idx < d * CB) Cacc[idx] = ini ? ini[oC + (size_t)(idx / CB) * dv + c0 + idx % CB] : 0.f;
-  }
-  if (tid < d) {
-    macc[tid] = ini ? ini[om + tid] : 0.f;
-    hacc = (ini && blk == 0) ? ini[oh + tid] : 0.f;
-  }
+  for (int j = 0; j < NB; ++j) gacc[j] = ini ? ini[oG + (size_t)a * dv + c0 + j0 + j] : 0.f;
+  if (tid < r1 - r0 && ini) hacc = ini[oh + r0 + tid];
+  for (int e = tid; e < d * CB; e += 256) Cbuf[e] = ini ? ini[oC + (size_t)(e / CB) * dv + c0 + e % CB] : 0.f;
+  if (tid < d) macc[tid] = ini ? ini[om + tid] : 0.f;
 
-  // registers holding segment c (loaded one step ahead)
-  float sv[nSS], cv[nCC], gv[4][4], mv = 0.f, hv = 0.f;
-  auto load = [&](int c) {
-    const float* x = in + (size_t)c * F;
+  // registers holding segments c .. c + PF - 1 (slot c % PF), loaded PF steps ahead
+  constexpr int PF = K::PF;
+  float4 sv[PF][K::nS4], cv[PF][nC4];
+  float gv[PF][NB], mv[PF], hv[PF];
+  auto load = [&](int c, auto slot_tag) {
+    constexpr int sl = decltype(slot_tag)::value;
+    const float* x = in + (size_t)min(c, M - 1) * F;
+    // every lane loads (indices clamped into the record) so no load sits under
+    // a branch and the wait counts stay exact across steps; out-of-range
+    // lanes are masked where the values are used
 #pragma unroll
-    for (int r = 0; r < nSS; ++r) {
-      const int idx = tid + 256 * r;
-      sv[r] = idx < d * d ? x[idx] : 0.f;
+    for (int r = 0; r < K::nS4; ++r) sv[sl][r] = ld4(x + 4 * min(tid + 256 * r, d * d / 4 - 1));
+#pragma unroll
+    for (int r = 0; r < nC4; ++r) cv[sl][r] = ld4(x + oC + blk_off(min(tid + 256 * r, d * CB / 4 - 1)));
+    if constexpr (NB % 4 == 0) {
+#pragma unroll
+      for (int j = 0; j < NB; j += 4) {
+        const float4 g = ld4(x + oG + (size_t)a * dv + c0 + j0 + j);
+        gv[sl][j] = g.x; gv[sl][j + 1] = g.y; gv[sl][j + 2] = g.z; gv[sl][j + 3] = g.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) gv[sl][j] = x[oG + (size_t)a * dv + c0 + j0 + j];
     }
-#pragma unroll
-    for (int r = 0; r < nCC; ++r) {
-      const int idx = tid + 256 * r;
-      cv[r] = idx < d * CB ? x[oC + (size_t)(idx / CB) * dv + c0 + idx % CB] : 0.f;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) gv[i][j] = active ? x[oG + (size_t)(gr + i) * dv + c0 + jq * 4 + j] : 0.f;
-    if (tid < d) {
-      mv = x[om + tid];
-      hv = x[oh + tid];
-    }
+    mv[sl] = x[om + min(tid, d - 1)];
+    hv[sl] = x[oh + r0 + min(tid, rows - 1)];
   };
-  if (M > 0) load(0);
+  if (M > 0) load(0, std::integral_constant<int, 0>());
+  if constexpr (PF > 1)
+    if (M > 1) load(1, std::integral_constant<int, 1>());
   __syncthreads();
 
-  for (int c = 0; c <= M; ++c) {
+  // one step: write the prefix of segment c, then consume slot sl and refill it with segment c + PF
+  auto step = [&](int c, auto slot_tag) -> bool {
+    constexpr int sl = decltype(slot_tag)::value;
+    const int p = K::NBUF == 2 ? (c & 1) : 0;   // LDS buffer (c parity)
+    float* Sc = Sbuf + p * d * ldS;
+    float* Cacc = Cbuf + p * d * CB;        // C before segment c
+    float* Cnext = Cbuf + (K::NBUF == 2 ? (1 - p) : 0) * d * CB;
     float* dst = (c < M) ? pre + (size_t)c * F : (total ? total + (size_t)bh * tot_stride : nullptr);
     // the exclusive prefix of segment c (or the total after the last)
     if (dst) {
-      if (blk == 0) {
 #pragma unroll
-        for (int r = 0; r < nSS; ++r) {
-          const int idx = tid + 256 * r;
-          if (idx < d * d) dst[idx] = sacc[r];
-        }
-        if (tid < d) {
-          dst[om + tid] = macc[tid];
-          dst[oh + tid] = hacc;
-        }
+      for (int i = 0; i < nSO; ++i) {
+        const int e = tid + 256 * i;
+        if (e < nown) dst[(size_t)r0 * d + e] = sacc[i];
       }
 #pragma unroll
-      for (int r = 0; r < nCC; ++r) {
-        const int idx = tid + 256 * r;
-        if (idx < d * CB) dst[oC + (size_t)(idx / CB) * dv + c0 + idx % CB] = Cacc[idx];
+      for (int r = 0; r < nC4; ++r) {
+        const int e = tid + 256 * r;
+        if (e < d * CB / 4) st4(dst + oC + blk_off(e), ld4(Cacc + 4 * e));
       }
-      if (active)
+      if constexpr (NB % 4 == 0) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < NB; j += 4)
+          st4(dst + oG + (size_t)a * dv + c0 + j0 + j, make_float4(gacc[j], gacc[j + 1], gacc[j + 2], gacc[j + 3]));
+      } else {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) dst[oG + (size_t)(gr + i) * dv + c0 + jq * 4 + j] = gacc[i][j];
+        for (int j = 0; j < NB; ++j) dst[oG + (size_t)a * dv + c0 + j0 + j] = gacc[j];
+      }
+      if (blk == 0 && tid < d) dst[om + tid] = macc[tid];
+      if (tid < r1 - r0) dst[oh + r0 + tid] = hacc;
     }
-    if (c == M) break;
-    // consume segment c's registers: stage S_c, C_new = C_acc + C_c, add G_c, h_c, S_c
+    if (c == M) return false;
+    // stage segment c: S_c, and C_acc + C_c for the next step
 #pragma unroll
-    for (int r = 0; r < nSS; ++r) {
-      const int idx = tid + 256 * r;
-      if (idx < d * d) ScT[(idx % d) * ldS + idx / d] = sv[r];
-      if (blk == 0) sacc[r] += sv[r];
+    for (int r = 0; r < K::nS4; ++r) {
+      const int e4 = tid + 256 * r;
+      if (e4 * 4 < d * d) {
+        const int row = (4 * e4) / d, col = (4 * e4) % d;
+        st4(&Sc[row * ldS + col], sv[sl][r]);
+      }
+    }
+    float4 cn[nC4];
+#pragma unroll
+    for (int r = 0; r < nC4; ++r) {
+      const int e = tid + 256 * r;
+      if (e < d * CB / 4) {
+        const float4 o = ld4(Cacc + 4 * e);
+        cn[r] = make_float4(o.x + cv[sl][r].x, o.y + cv[sl][r].y, o.z + cv[sl][r].z, o.w + cv[sl][r].w);
+        if (K::NBUF == 2) st4(Cnext + 4 * e, cn[r]);
+      }
     }
 #pragma unroll
-    for (int r = 0; r < nCC; ++r) {
-      const int idx = tid + 256 * r;
-      if (idx < d * CB) Cnew[idx] = Cacc[idx] + cv[r];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) gacc[i][j] += gv[i][j];
-    const float m_c = mv;
-    hacc += hv;
+    for (int j = 0; j < NB; ++j) gacc[j] += gv[sl][j];
+    const float m_c = mv[sl];
+    if (tid < r1 - r0) hacc += hv[sl];
     __syncthreads();
-    if (c + 1 < M) load(c + 1);
-    // G_acc += S_c C_acc   (segment A = accumulated prefix, B = segment c)
-    if (active) {
-      float acc[4][4];
+    if (c + PF < M) load(c + PF, slot_tag);
+    // G_acc += S_c C_acc (segment A = accumulated prefix, B = segment c)
+    {
+      float acc[NB];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < NB; ++j) acc[j] = 0.f;
+      const float* srow = Sc + a * ldS;
+#pragma unroll 4
+      for (int ap = 0; ap < d; ap += 4) {
+        const float4 s4 = ld4(srow + ap);
+        const float sv4[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-#pragma unroll 8
-      for (int ap = 0; ap < d; ++ap) {
-        const float4 s4 = *reinterpret_cast<const float4*>(&ScT[ap * ldS + gr]);
-        const float4 c4 = *reinterpret_cast<const float4*>(&Cacc[ap * CB + jq * 4]);
-        const float svv[4] = {s4.x, s4.y, s4.z, s4.w};
-        const float cvv[4] = {c4.x, c4.y, c4.z, c4.w};
+        for (int u = 0; u < 4; ++u) {
+          const float* crow = Cacc + (ap + u) * CB + j0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] += svv[i] * cvv[j];
+          for (int j = 0; j < NB; ++j) acc[j] += sv4[u] * crow[j];
+        }
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) gacc[i][j] += acc[i][j];
+      for (int j = 0; j < NB; ++j) gacc[j] += acc[j];
     }
-    // h_acc += S_c m_acc
-    if (blk == 0 && tid < d) {
+    // h_acc += S_c m_acc and S_acc += S_c on the owned rows
+    if (tid < r1 - r0) {
+      const float* srow = Sc + (r0 + tid) * ldS;
       float e = 0.f;
 #pragma unroll 8
-      for (int ap = 0; ap < d; ++ap) e += ScT[ap * ldS + tid] * macc[ap];
+      for (int ap = 0; ap < d; ++ap) e += srow[ap] * macc[ap];
       hacc += e;
     }
-    __syncthreads();
 #pragma unroll
-    for (int r = 0; r < nCC; ++r) {
-      const int idx = tid + 256 * r;
-      if (idx < d * CB) Cacc[idx] = Cnew[idx];
+    for (int i = 0; i < nSO; ++i) {
+      const int e = tid + 256 * i;
+      if (e < nown) sacc[i] += Sc[(r0 + e / d) * ldS + e % d];
     }
+    if (K::NBUF == 1) {
+      __syncthreads();   // everyone is done with Sc and Cacc
+#pragma unroll
+      for (int r = 0; r < nC4; ++r) {
+        const int e = tid + 256 * r;
+        if (e < d * CB / 4) st4(Cacc + 4 * e, cn[r]);
+      }
+    }
+    __syncthreads();   // macc readers are done; NBUF == 2: the other buffers are free
     if (tid < d) macc[tid] += m_c;
-    __syncthreads();
+    return true;
+  };
+  for (int c = 0;; c += PF) {
+    if (!step(c, std::integral_constant<int, 0>())) break;
+    if constexpr (PF > 1)
+      if (!step(c + 1, std::integral_constant<int, 1>())) break;
   }
 }
 
@@ -196,26 +239,27 @@ hipError_t launch_scan(const float* states, const float* init, float* prefix, fl
 hipError_t launch_scan_strided(const float* states, const float* init, float* prefix, float* total, int BH, int M,
                                int d, int dv, size_t in_stride, size_t pre_stride, size_t tot_stride,
                                hipStream_t s) {
-  const int nblk = (dv + kScanCols - 1) / kScanCols;
+  const int cb = scan_cols(d);
+  const int nblk = (dv + cb - 1) / cb;
   const int groups = (BH + 7) / 8;
-  const size_t lds = sizeof(float) * ((size_t)d * (d + 4) + 2 * (size_t)d * kScanCols + d);
   const void* kern = nullptr;
-  switch (d) {
-    case 16: kern = (const void*)k_scan<16>; break;
-    case 32: kern = (const void*)k_scan<32>; break;
-    case 64: kern = (const void*)k_scan<64>; break;
-    case 128: kern = (const void*)k_scan<128>; break;
-    default: return hipErrorInvalidValue;
+  size_t lds = 0;
+#define HLA_SCAN_CASE(D_, B_)                                 \
+  if (d == D_ && nblk == B_) {                                \
+    kern = (const void*)k_scan<D_, B_>;                       \
+    lds = ScanCfg<D_>::lds_floats * sizeof(float);            \
   }
+  HLA_SCAN_CASE(16, 1) HLA_SCAN_CASE(16, 2) HLA_SCAN_CASE(16, 4) HLA_SCAN_CASE(16, 8)
+  HLA_SCAN_CASE(32, 2) HLA_SCAN_CASE(32, 4) HLA_SCAN_CASE(32, 8) HLA_SCAN_CASE(32, 16)
+  HLA_SCAN_CASE(64, 4) HLA_SCAN_CASE(64, 8) HLA_SCAN_CASE(64, 16) HLA_SCAN_CASE(64, 32)
+  HLA_SCAN_CASE(128, 1) HLA_SCAN_CASE(128, 2) HLA_SCAN_CASE(128, 4) HLA_SCAN_CASE(128, 8)
+#undef HLA_SCAN_CASE
+  if (!kern) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  dim3 grid(groups * 8 * nblk), block(256);
-  switch (d) {
-    case 16: hipLaunchKernelGGL(k_scan<16>, grid, block, lds, s, states, init, prefix, total, BH, M, dv, nblk, in_stride, pre_stride, tot_stride); break;
-    case 32: hipLaunchKernelGGL(k_scan<32>, grid, block, lds, s, states, init, prefix, total, BH, M, dv, nblk, in_stride, pre_stride, tot_stride); break;
-    case 64: hipLaunchKernelGGL(k_scan<64>, grid, block, lds, s, states, init, prefix, total, BH, M, dv, nblk, in_stride, pre_stride, tot_stride); break;
-    default: hipLaunchKernelGGL(k_scan<128>, grid, block, lds, s, states, init, prefix, total, BH, M, dv, nblk, in_stride, pre_stride, tot_stride); break;
-  }
+  void* args[] = {&states, &init, &prefix, &total, &BH, &M, &dv, const_cast<int*>(&nblk), &in_stride, &pre_stride, &tot_stride};
+  e = hipLaunchKernel(kern, dim3(groups * 8 * nblk), dim3(256), args, lds, s);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 
