@@ -10,9 +10,10 @@ Modules
   hla2      second-order HLA (Sec. 3 and Sec. 4 of the paper): the plain
             definition, the serial online recurrence, the chunked associative
             scan and the masked semidirect product.
-  hla3      third-order HLA (Sec. 7): the streaming kernel and the
-            chunk-parallel concatenation operator.
-  hla2_ref.c  the serial second-order recurrence in plain C (fp64), used to
+  hla3      third-order HLA (Sec. 7): the triple sum over the index set of
+            Thm. 3, the streaming kernel (Alg. 3), the corrected-state
+            recurrence, the operator (x)_3 and the chunk-parallel scan (Alg. 4).
+  hla2_ref.c, hla3_ref.c  the serial recurrences in plain C (fp64), used to
             time the oracle on host cores and to check large cases quickly.
   native    ctypes loader for the compiled C oracle.
 """

@@ -79,3 +79,29 @@ def hla2_serial_c(q, k, v, masked=True, state=None, threads=0, return_state=True
                                int(bool(masked)), *[_ptr(x) for x in st], int(threads))
     final = tuple(st) if st[0] is not None else None
     return num, den, final, used
+
+
+def available():
+    try:
+        load()
+        return True
+    except Exception:
+        return False
+
+
+def hla3_serial_c(q, k, v, masked=True, threads=0):
+    """Serial third-order recurrence (Alg. 3) in C over heads [..., n, d].
+    Returns (num [..., n, dv], den [..., n], threads used)."""
+    lib = load()
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    batch = q.shape[:-2]
+    n, d = q.shape[-2:]
+    dv = v.shape[-1]
+    BH = int(np.prod(batch)) if batch else 1
+    num = np.empty(batch + (n, dv))
+    den = np.empty(batch + (n,))
+    used = lib.hla3_serial_f64(_ptr(q), _ptr(k), _ptr(v), _ptr(num), _ptr(den), BH, n, d, dv,
+                               int(bool(masked)), int(threads))
+    return num, den, used
