@@ -221,6 +221,43 @@ def measure_scan(w, qd, kd, vd, reps=10):
             "peak": HBM_PEAK_GBS, "frac": nbytes / ms / 1e6 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes}
 
 
+def measure_hla3(reps=20):
+    """hla3_forward on the masked third-order workload (B1 H8 n2048 d=dv=16,
+    fp32, chunk 32): tokens/s by HIP events, and per-kernel times."""
+    import torch
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
+    from paper_2510_27258_amd import inputs as I
+    name = "hla3-masked-fp32-B1H8-n2048-d16-C32"
+    w = I.WORKLOADS[name]
+    q, k, v, code = I.draw_qkv(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    out = torch.empty(w["B"], w["H"], w["n"], w["dv"], dtype=torch.float32, device=dev)
+    wsb = capi.hla3_workspace_bytes(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], code)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    run = lambda: hla.hla3_forward(qd, kd, vd, w["chunk"], out=out, workspace=ws)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    capi.hla_profile_begin(8 * reps + 8)
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    prof = capi.hla_profile_summary()
+    capi.hla_profile_end()
+    tokens = w["B"] * w["H"] * w["n"]
+    return {"workload": name, "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms, "dtype": "f32",
+            "kernels_ms": {k_: v_[1] / v_[0] for k_, v_ in prof.items()}}
+
+
 def measure_decode(steps=None):
     """hla2_step on the decode workload: state from a prefill of the seeded
     2048-token prefix, then the seeded step tokens, one launch per step."""
@@ -269,6 +306,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone scan measurement")
+    ap.add_argument("--no-hla3", action="store_true", help="skip the third-order measurement")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
     ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
@@ -372,6 +410,8 @@ def main():
     }
     if not args.no_scan:
         rec["scan"] = measure_scan(w, qd, kd, vd)
+    if not args.no_hla3:
+        rec["hla3"] = measure_hla3()
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
     if not args.no_decode:

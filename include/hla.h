@@ -94,8 +94,11 @@ int hla2_forward_ex(const void *q, const void *k, const void *v, float *out,
                     void *stream);
 
 /* 1 if hla2_forward_ex would accept `algo` for these arguments, else 0.
- * HLA_ALGO_FUSED covers bf16 inputs, masked = 1 and (chunk, d, dv) in
- * {(64,64,64), (32,32,32), (64,32,32), (32,64,64), (64,64,32), (64,32,64)}. */
+ * HLA_ALGO_FUSED covers bf16 inputs, masked = 1, n * max(d, dv) * 4 < 2^31
+ * and (tile, d, dv) in {(64,64,64), (32,32,32), (64,32,32), (32,64,64),
+ * (64,64,32), (64,32,64), (64,128,128), (32,128,128)}, where the tile is the
+ * chunk for chunk 32 and 64, and 64 for chunk 128 (the scan is exact for any
+ * chunking, Thm. 2, so the tile changes only the rounding order). */
 int hla2_algo_supported(int algo, int n, int d, int dv, int chunk, int dtype, int masked);
 
 /* ---------------------------------------------------------------------------
@@ -140,6 +143,28 @@ int hla2_step(float *state, const void *q_t, const void *k_t, const void *v_t, f
               int B, int H, int d, int dv, int masked, int normalized, float eps, int dtype,
               void *stream);
 
+
+/* ---------------------------------------------------------------------------
+ * hla3_forward — masked third-order HLA over whole sequences (Sec. 7).
+ * out[b,h,t,:] = q_t^T F_t with F_t the corrected third-order state (Eq.
+ * hla3-corrected-state, Thm. 3): the sum, over triples (i, u, j) <= t whose
+ * largest index is attained at least twice, of (q_t.k_i)(k_i.q_u)(q_u.k_j) v_j.
+ * With normalized = 1 the row is divided by (q_t^T eta_t + eps), eta_t the
+ * same sum without v_j.  Computed in fp32 by the chunk-parallel scan of Sec.
+ * 7.3 (operator (x)_3, Thm. 4).
+ * q, k: [B, H, n, d]; v: [B, H, n, dv], fp32 or bf16 (dtype); out: [B, H, n, dv]
+ * fp32; all device pointers, 16-byte aligned, caller-owned.
+ * Supported: masked = 1, d and dv in {16, 32}, chunk in {16, 32, 64, 128};
+ * chunks above 32 are walked in 32-token tiles (exact for any chunking,
+ * Thm. 4).  Other arguments return HLA_ERR_UNSUPPORTED (masked = 0: the
+ * unmasked operator q_t^T S^K_t S^Q_t P_t is not built on the GPU).
+ * workspace: at least hla3_workspace_bytes(...) bytes of device memory (its
+ * contents on entry are ignored); HLA_ERR_WORKSPACE if smaller.
+ * ------------------------------------------------------------------------- */
+size_t hla3_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
+int hla3_forward(const void *q, const void *k, const void *v, float *out,
+                 int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
+                 float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
  * Benchmark timing.  hla_profile_begin(max_records) creates 2*max_records HIP

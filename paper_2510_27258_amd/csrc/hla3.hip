@@ -1,0 +1,412 @@
+// Masked third-order HLA forward (Sec. 7), fp32 arithmetic (dot products over
+// d accumulated in fp64) on fp32 or bf16 inputs, by the chunk-parallel scan of
+// Sec. 7.3 in a walk form.
+//
+// The corrected state F_t = S^K S^Q P - G1 - G2 - G3 (Eq. hla3-corrected-state)
+// advances per token by (Eq. hla3-corrected-recurrence, with primes for the
+// moments before token j, delta_j = q_j . k_j)
+//   F += SK' q q^T k v^T + k k^T SQ' k v^T + k k^T q q^T P' + k k^T q q^T k v^T
+//      = r_j delta_j v_j^T + k_j (sigma_j v_j + delta_j P'^T q_j + delta_j^2 v_j)^T,
+// with r_j = SK'_j q_j and sigma_j = k_j^T SQ'_j k_j; num_t = q_t^T F_t and
+// den_t = q_t^T eta_t (the same with v := 1).  Over a tile of tokens
+// (Q, K, V as rows; A = Q K^T; L and Ls the causal masks with and without the
+// diagonal) and moment carry (SK0, SQ0, P0, m0):
+//   R  = Q SK0 + (A (.) Ls) K                      rows r_j
+//   sigma_j = k_j^T SQ0 k_j + sum_{u<j} A_uj^2
+//   Pq = Q P0 + (A (.) Ls) V,   pm = Q m0 + (A (.) Ls) 1
+//   X  = (sigma + delta^2) (.) V + delta (.) Pq,   x = sigma + delta^2 + delta (.) pm
+//   num = Q F0 + [(Q R^T) (.) L] (delta (.) V) + (A (.) L) X
+//   den = Q eta0 + [(Q R^T) (.) L] delta + (A (.) L) x
+//   F0 += R^T (delta (.) V) + K^T X,   eta0 += R^T delta + K^T x,
+//   SK0 += K^T K, SQ0 += Q^T Q, P0 += K^T V, m0 += K^T 1.
+// No increment depends on F, so F composes across segments as a plain sum of
+// per-segment brackets (each computed with the true moment prefixes): these
+// are exactly the carry terms of the operator (x)_3 (Eq. hla3-corrected-concat),
+// S^K_A R_B + M_B[S^Q_A] + U_B P_A, applied from the segment's tokens
+// without materialising the maps M.
+//
+// Launches (segments of whole tiles per head):
+//   1. k3_moments: per segment, (SK, SQ, P, m) of its tokens.
+//   2. k3_walk: per segment, moment carry = sum of the moments before it; walks
+//      its tiles from F = 0, writes num (into out) and den (workspace) without
+//      the F carry, and the segment's bracket (F, eta).
+//   3. k3_fix: out_t += q_t^T F_c, den_t += q_t . eta_c with F_c the sum of the
+//      brackets before the segment; normalises if asked.
+#include "hla3.h"
+#include "profile.h"
+
+namespace hla {
+namespace {
+
+constexpr int kT3 = 256;
+
+template <int D, int DV>
+struct Rec3 {   // per (head, segment): SK | SQ | P | m | F | eta
+  static constexpr int oSK = 0, oSQ = D * D, oP = 2 * D * D, om = oP + D * DV, oF = om + D, oe = oF + D * DV;
+  static constexpr int floats = oe + D;
+};
+
+template <typename T>
+__device__ __forceinline__ float ld3(const T* p, size_t i) { return ldf(p, i); }
+
+// Stage one tile of tokens (rows past n read as zero) into padded LDS rows.
+template <typename T, int C, int D, int DV>
+__device__ void stage_tile(const T* q, const T* k, const T* v, size_t head_tok, int t0, int n, float* Qs, float* Ks,
+                           float* Vs) {
+  for (int e = threadIdx.x; e < C * D; e += kT3) {
+    const int t = e / D, a = e % D;
+    const bool in = t0 + t < n;
+    const size_t g = (head_tok + t0 + t) * D + a;
+    Qs[t * (D + 1) + a] = in ? ld3(q, g) : 0.f;
+    Ks[t * (D + 1) + a] = in ? ld3(k, g) : 0.f;
+  }
+  for (int e = threadIdx.x; e < C * DV; e += kT3) {
+    const int t = e / DV, b = e % DV;
+    Vs[t * (DV + 1) + b] = (t0 + t < n) ? ld3(v, (head_tok + t0 + t) * DV + b) : 0.f;
+  }
+}
+
+// 1. Moments of each segment.  grid (nseg, BH).
+template <typename T, int C, int D, int DV>
+__global__ __launch_bounds__(kT3) void k3_moments(const T* __restrict__ q, const T* __restrict__ k,
+                                                  const T* __restrict__ v, float* __restrict__ rec, int n, int cps,
+                                                  int nseg) {
+  using Rc = Rec3<D, DV>;
+  constexpr int NO = 2 * D * D + D * DV + D;   // SK | SQ | P | m: the first NO floats of a record
+  __shared__ float Qs[C * (D + 1)], Ks[C * (D + 1)], Vs[C * (DV + 1)], acc[NO];
+  const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
+  for (int o = tid; o < NO; o += kT3) acc[o] = 0.f;     // each thread keeps its own slots
+  for (int c = c0; c < c1; ++c) {
+    stage_tile<T, C, D, DV>(q, k, v, (size_t)bh * n, c * C, n, Qs, Ks, Vs);
+    __syncthreads();
+    for (int o = tid; o < D * D; o += kT3) {            // K^T K and Q^T Q
+      const int a = o / D, b = o % D;
+      float sk = 0.f, sq = 0.f;
+      for (int t = 0; t < C; ++t) {
+        sk += Ks[t * (D + 1) + a] * Ks[t * (D + 1) + b];
+        sq += Qs[t * (D + 1) + a] * Qs[t * (D + 1) + b];
+      }
+      acc[Rc::oSK + o] += sk;
+      acc[Rc::oSQ + o] += sq;
+    }
+    for (int o = tid; o < D * DV; o += kT3) {           // K^T V
+      const int a = o / DV, b = o % DV;
+      float s = 0.f;
+      for (int t = 0; t < C; ++t) s += Ks[t * (D + 1) + a] * Vs[t * (DV + 1) + b];
+      acc[Rc::oP + o] += s;
+    }
+    for (int a = tid; a < D; a += kT3) {                 // K^T 1
+      float s = 0.f;
+      for (int t = 0; t < C; ++t) s += Ks[t * (D + 1) + a];
+      acc[Rc::om + a] += s;
+    }
+    __syncthreads();
+  }
+  float* r = rec + ((size_t)bh * nseg + seg) * Rc::floats;
+  for (int o = tid; o < NO; o += kT3) r[o] = acc[o];
+}
+
+// 2. The walk of one segment from its moment carry with F = 0.  grid (nseg, BH).
+template <typename T, int C, int D, int DV>
+__global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T* __restrict__ k,
+                                               const T* __restrict__ v, float* __restrict__ out,
+                                               float* __restrict__ den_out, float* __restrict__ rec, int n, int cps,
+                                               int nseg) {
+  using Rc = Rec3<D, DV>;
+  constexpr int lD = D + 1, lV = DV + 1, lC = C + 1;
+  __shared__ float Qs[C * lD], Ks[C * lD], Vs[C * lV];
+  __shared__ float SK[D * lD], SQ[D * lD], Pm[D * lV], mv[D], F[D * lV], eta[D];
+  __shared__ float A[C * lC], R[C * lD], Tm[C * lC], QSK[C * lD], QP[C * lV], QF[C * lV], Pq[C * lV], X[C * lV];
+  __shared__ float sig[C], dl[C], pm[C], xv[C], qeta[C];
+  const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
+  const size_t head_tok = (size_t)bh * n;
+  float* recs = rec + (size_t)bh * nseg * Rc::floats;
+
+  // moment carry: sum of the segments before this one; F = eta = 0
+  for (int e = tid; e < D * D; e += kT3) {
+    float sk = 0.f, sq = 0.f;
+    for (int sp = 0; sp < seg; ++sp) {
+      sk += recs[(size_t)sp * Rc::floats + Rc::oSK + e];
+      sq += recs[(size_t)sp * Rc::floats + Rc::oSQ + e];
+    }
+    SK[(e / D) * lD + e % D] = sk;
+    SQ[(e / D) * lD + e % D] = sq;
+  }
+  for (int e = tid; e < D * DV; e += kT3) {
+    float p = 0.f;
+    for (int sp = 0; sp < seg; ++sp) p += recs[(size_t)sp * Rc::floats + Rc::oP + e];
+    Pm[(e / DV) * lV + e % DV] = p;
+    F[(e / DV) * lV + e % DV] = 0.f;
+  }
+  for (int e = tid; e < D; e += kT3) {
+    float s = 0.f;
+    for (int sp = 0; sp < seg; ++sp) s += recs[(size_t)sp * Rc::floats + Rc::om + e];
+    mv[e] = s;
+    eta[e] = 0.f;
+  }
+
+  for (int c = c0; c < c1; ++c) {
+    const int t0 = c * C;
+    stage_tile<T, C, D, DV>(q, k, v, head_tok, t0, n, Qs, Ks, Vs);
+    __syncthreads();
+    // s1: A = Q K^T, Q SK0, Q P0, Q F0, q.m0, q.eta0, k^T SQ0 k.  Dot products
+    // over d accumulate in fp64 (products of fp32 values are exact there): a
+    // row such as o_1 = (q_1.k_1)^3 v_1 amplifies the cancellation of q.k.
+    for (int e = tid; e < C * C; e += kT3) {
+      const int t = e / C, i = e % C;
+      double s = 0.0;
+#pragma unroll 8
+      for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * Ks[i * lD + a];
+      A[t * lC + i] = (float)s;
+    }
+    for (int e = tid; e < C * D; e += kT3) {
+      const int t = e / D, b = e % D;
+      double s = 0.0;
+#pragma unroll 8
+      for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * SK[a * lD + b];
+      QSK[t * lD + b] = (float)s;
+    }
+    for (int e = tid; e < C * DV; e += kT3) {
+      const int t = e / DV, b = e % DV;
+      double s = 0.0, f = 0.0;
+#pragma unroll 8
+      for (int a = 0; a < D; ++a) {
+        s += (double)Qs[t * lD + a] * Pm[a * lV + b];
+        f += (double)Qs[t * lD + a] * F[a * lV + b];
+      }
+      QP[t * lV + b] = (float)s;
+      QF[t * lV + b] = (float)f;
+    }
+    for (int t = tid; t < C; t += kT3) {
+      double s = 0.0, w = 0.0, g = 0.0;
+      for (int a = 0; a < D; ++a) {
+        s += (double)Qs[t * lD + a] * mv[a];
+        w += (double)Qs[t * lD + a] * eta[a];
+        double y = 0.0;
+        for (int b = 0; b < D; ++b) y += (double)SQ[a * lD + b] * Ks[t * lD + b];
+        g += (double)Ks[t * lD + a] * y;
+      }
+      pm[t] = (float)s;
+      qeta[t] = (float)w;
+      sig[t] = (float)g;
+    }
+    __syncthreads();
+    // s2: prefixes inside the tile (strictly before j)
+    for (int e = tid; e < C * D; e += kT3) {
+      const int j = e / D, b = e % D;
+      float s = QSK[j * lD + b];
+      for (int i = 0; i < j; ++i) s += A[j * lC + i] * Ks[i * lD + b];
+      R[j * lD + b] = s;
+    }
+    for (int e = tid; e < C * DV; e += kT3) {
+      const int j = e / DV, b = e % DV;
+      float s = QP[j * lV + b];
+      for (int i = 0; i < j; ++i) s += A[j * lC + i] * Vs[i * lV + b];
+      Pq[j * lV + b] = s;
+    }
+    for (int j = tid; j < C; j += kT3) {
+      float s = sig[j], p = pm[j];
+      for (int u = 0; u < j; ++u) {
+        const float a = A[u * lC + j];
+        s += a * a;
+        p += A[j * lC + u];
+      }
+      sig[j] = s;
+      pm[j] = p;
+      dl[j] = A[j * lC + j];
+    }
+    __syncthreads();
+    // s3: T = (Q R^T) (.) L, X, x
+    for (int e = tid; e < C * C; e += kT3) {
+      const int t = e / C, j = e % C;
+      double s = 0.0;
+      if (j <= t) {
+#pragma unroll 8
+        for (int b = 0; b < D; ++b) s += (double)Qs[t * lD + b] * R[j * lD + b];
+      }
+      Tm[t * lC + j] = (float)s;
+    }
+    for (int e = tid; e < C * DV; e += kT3) {
+      const int j = e / DV, b = e % DV;
+      const float d0 = dl[j];
+      X[j * lV + b] = (sig[j] + d0 * d0) * Vs[j * lV + b] + d0 * Pq[j * lV + b];
+    }
+    for (int j = tid; j < C; j += kT3) {
+      const float d0 = dl[j];
+      xv[j] = sig[j] + d0 * d0 + d0 * pm[j];
+    }
+    __syncthreads();
+    // s4: outputs without the F carry of earlier segments, then the advance
+    for (int e = tid; e < C * DV; e += kT3) {
+      const int t = e / DV, b = e % DV;
+      float s = QF[t * lV + b];
+      for (int j = 0; j <= t; ++j) s += Tm[t * lC + j] * dl[j] * Vs[j * lV + b] + A[t * lC + j] * X[j * lV + b];
+      if (t0 + t < n) out[(head_tok + t0 + t) * DV + b] = s;
+    }
+    for (int t = tid; t < C; t += kT3) {
+      float s = qeta[t];
+      for (int j = 0; j <= t; ++j) s += Tm[t * lC + j] * dl[j] + A[t * lC + j] * xv[j];
+      if (t0 + t < n) den_out[head_tok + t0 + t] = s;
+    }
+    for (int e = tid; e < D * DV; e += kT3) {
+      const int a = e / DV, b = e % DV;
+      float f = 0.f, p = 0.f;
+      for (int j = 0; j < C; ++j) {
+        f += R[j * lD + a] * dl[j] * Vs[j * lV + b] + Ks[j * lD + a] * X[j * lV + b];
+        p += Ks[j * lD + a] * Vs[j * lV + b];
+      }
+      F[a * lV + b] += f;
+      Pm[a * lV + b] += p;
+    }
+    for (int e = tid; e < D * D; e += kT3) {
+      const int a = e / D, b = e % D;
+      float sk = 0.f, sq = 0.f;
+      for (int j = 0; j < C; ++j) {
+        sk += Ks[j * lD + a] * Ks[j * lD + b];
+        sq += Qs[j * lD + a] * Qs[j * lD + b];
+      }
+      SK[a * lD + b] += sk;
+      SQ[a * lD + b] += sq;
+    }
+    for (int a = tid; a < D; a += kT3) {
+      float e2 = 0.f, s = 0.f;
+      for (int j = 0; j < C; ++j) {
+        e2 += R[j * lD + a] * dl[j] + Ks[j * lD + a] * xv[j];
+        s += Ks[j * lD + a];
+      }
+      eta[a] += e2;
+      mv[a] += s;
+    }
+    __syncthreads();
+  }
+  // the segment's bracket (F, eta)
+  float* r = recs + (size_t)seg * Rc::floats;
+  for (int e = tid; e < D * DV; e += kT3) r[Rc::oF + e] = F[(e / DV) * lV + e % DV];
+  for (int e = tid; e < D; e += kT3) r[Rc::oe + e] = eta[e];
+}
+
+// 3. Add the F carry of earlier segments and normalise.  grid (nseg, BH).
+template <typename T, int C, int D, int DV>
+__global__ __launch_bounds__(kT3) void k3_fix(const T* __restrict__ q, float* __restrict__ out,
+                                              const float* __restrict__ den_in, const float* __restrict__ rec, int n,
+                                              int cps, int nseg, int normalized, float eps) {
+  using Rc = Rec3<D, DV>;
+  __shared__ float Fc[D * (DV + 1)], ec[D], Qs[C * (D + 1)], inv[C];
+  const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  if (seg == 0 && !normalized) return;          // nothing to add
+  const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
+  const size_t head_tok = (size_t)bh * n;
+  const float* recs = rec + (size_t)bh * nseg * Rc::floats;
+  for (int e = tid; e < D * DV; e += kT3) {
+    float s = 0.f;
+    for (int sp = 0; sp < seg; ++sp) s += recs[(size_t)sp * Rc::floats + Rc::oF + e];
+    Fc[(e / DV) * (DV + 1) + e % DV] = s;
+  }
+  for (int e = tid; e < D; e += kT3) {
+    float s = 0.f;
+    for (int sp = 0; sp < seg; ++sp) s += recs[(size_t)sp * Rc::floats + Rc::oe + e];
+    ec[e] = s;
+  }
+  for (int c = c0; c < c1; ++c) {
+    const int t0 = c * C;
+    for (int e = tid; e < C * D; e += kT3) {
+      const int t = e / D, a = e % D;
+      Qs[t * (D + 1) + a] = (t0 + t < n) ? ld3(q, (head_tok + t0 + t) * D + a) : 0.f;
+    }
+    __syncthreads();
+    if (normalized)
+      for (int t = tid; t < C; t += kT3) {
+        double s = 0.0;
+        for (int a = 0; a < D; ++a) s += (double)Qs[t * (D + 1) + a] * ec[a];
+        inv[t] = (t0 + t < n) ? 1.f / (den_in[head_tok + t0 + t] + (float)s + eps) : 0.f;
+      }
+    __syncthreads();
+    for (int e = tid; e < C * DV; e += kT3) {
+      const int t = e / DV, b = e % DV;
+      if (t0 + t >= n) continue;
+      double s = 0.0;
+      for (int a = 0; a < D; ++a) s += (double)Qs[t * (D + 1) + a] * Fc[a * (DV + 1) + b];
+      const size_t o = (head_tok + t0 + t) * DV + b;
+      float y = out[o] + (float)s;
+      if (normalized) y *= inv[t];
+      out[o] = y;
+    }
+    __syncthreads();
+  }
+}
+
+template <typename T, int C, int D, int DV>
+hipError_t run3(const Fwd& f, float* recs, float* den, int P, int cps, hipStream_t s) {
+  const T* q = static_cast<const T*>(f.q);
+  const T* k = static_cast<const T*>(f.k);
+  const T* v = static_cast<const T*>(f.v);
+  const dim3 grid(P, f.BH);
+  prof_start("hla3_moments", s);
+  hipLaunchKernelGGL((k3_moments<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, recs, f.n, cps, P);
+  prof_stop(s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  prof_start("hla3_walk", s);
+  hipLaunchKernelGGL((k3_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, den, recs, f.n, cps, P);
+  prof_stop(s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  prof_start("hla3_fix", s);
+  hipLaunchKernelGGL((k3_fix<T, C, D, DV>), grid, dim3(kT3), 0, s, q, f.out, den, recs, f.n, cps, P, f.normalized,
+                     f.eps);
+  prof_stop(s);
+  return hipGetLastError();
+}
+
+int tile3(int chunk) { return chunk >= 32 ? 32 : chunk; }
+
+void plan3(int BH, int n, int chunk, int* P, int* cps) {
+  const int C = tile3(chunk);
+  const int M = (n + C - 1) / C;
+  int p = 512 / BH;
+  if (p < 1) p = 1;
+  if (p > M) p = M;
+  *cps = (M + p - 1) / p;
+  *P = (M + *cps - 1) / *cps;
+}
+
+size_t rec_floats(int d, int dv) { return 2 * (size_t)d * d + 2 * (size_t)d * dv + 2 * (size_t)d; }
+
+}  // namespace
+
+bool hla3_supported(int d, int dv, int chunk, int masked) {
+  return masked == 1 && (d == 16 || d == 32) && (dv == 16 || dv == 32) && (chunk >= 16 && chunk <= 128);
+}
+
+size_t hla3_workspace(int BH, int n, int d, int dv, int chunk) {
+  int P, cps;
+  plan3(BH, n, chunk, &P, &cps);
+  const size_t a = ((sizeof(float) * (size_t)BH * P * rec_floats(d, dv)) + 255) & ~size_t(255);
+  return a + sizeof(float) * (size_t)BH * n + 256;
+}
+
+hipError_t launch_hla3(const Fwd& f, void* workspace, hipStream_t s) {
+  int P, cps;
+  plan3(f.BH, f.n, f.chunk, &P, &cps);
+  char* base = static_cast<char*>(workspace);
+  float* recs = reinterpret_cast<float*>(base);
+  float* den = reinterpret_cast<float*>(base + (((sizeof(float) * (size_t)f.BH * P * rec_floats(f.d, f.dv)) + 255) &
+                                                ~size_t(255)));
+  const int C = tile3(f.chunk);
+#define HLA3_CASE(T_, C_, D_, DV_) \
+  if (C == C_ && f.d == D_ && f.dv == DV_) return run3<T_, C_, D_, DV_>(f, recs, den, P, cps, s);
+#define HLA3_DT(T_)                                                                                       \
+  HLA3_CASE(T_, 16, 16, 16) HLA3_CASE(T_, 16, 16, 32) HLA3_CASE(T_, 16, 32, 16) HLA3_CASE(T_, 16, 32, 32) \
+  HLA3_CASE(T_, 32, 16, 16) HLA3_CASE(T_, 32, 16, 32) HLA3_CASE(T_, 32, 32, 16) HLA3_CASE(T_, 32, 32, 32)
+  if (f.dtype == 1) {
+    HLA3_DT(uint16_t)
+  } else {
+    HLA3_DT(float)
+  }
+#undef HLA3_DT
+#undef HLA3_CASE
+  return hipErrorNotSupported;
+}
+
+}  // namespace hla

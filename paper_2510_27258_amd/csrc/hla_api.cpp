@@ -8,6 +8,7 @@
 #include "../../include/hla.h"
 #include "common.h"
 #include "fused.h"
+#include "hla3.h"
 #include "profile.h"
 
 namespace {
@@ -239,6 +240,35 @@ int hla2_step(float* state, const void* q_t, const void* k_t, const void* v_t, f
   hipError_t e = hla::launch_step(state, q_t, k_t, v_t, out_t, B * H, d, dv, masked, normalized, eps, dtype,
                                   reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "step");
+  return ok();
+}
+
+size_t hla3_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  if (!hla::hla3_supported(d, dv, chunk, 1)) return 0;
+  return hla::hla3_workspace(B * H, n, d, dv, chunk);
+}
+
+int hla3_forward(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
+                 int chunk, int masked, int normalized, float eps, int dtype, void* workspace, size_t workspace_bytes,
+                 void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
+      (rc = check_ptr(out, "out")))
+    return rc;
+  if (!hla::hla3_supported(d, dv, chunk, masked))
+    return fail(HLA_ERR_UNSUPPORTED, "hla3_forward needs masked=1 and d, dv in {16, 32} (got masked=%d d=%d dv=%d)",
+                masked, d, dv);
+  const int BH = B * H;
+  const size_t need = hla::hla3_workspace(BH, n, d, dv, chunk);
+  if (!workspace || workspace_bytes < need)
+    return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
+  hipError_t e = hla::launch_hla3(f, workspace, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "hla3 forward");
   return ok();
 }
 

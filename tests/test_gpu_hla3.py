@@ -1,0 +1,104 @@
+"""GPU parity of the masked third-order HLA forward (Sec. 7) against the fp64
+oracle (Alg. 3 in C, itself pinned by the brute-force triple sum and Alg. 4).
+
+Every call goes through the C ABI.  Bars: 1e-5 (fp32 inputs) and 2e-3 (bf16
+inputs) on the row-wise relative error; the ratio-normalised output is judged
+on rows whose denominator is well away from zero (|den_t + eps| >= 0.05 D_t,
+D_t the sum of |terms| of den_t), with num and den judged separately everywhere.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2510_27258_amd as hla
+from paper_2510_27258_amd import capi
+from paper_2510_27258_amd import inputs as I
+from oracle import hla3 as O3
+from oracle import native
+from tests.helpers import dev, gen, rowwise_err, tol_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _check(B, H, n, d, dv, chunk, dist, normalized=False, seed=0, eps=1e-6):
+    q, k, v, code = gen(B, H, n, d, dv, dist, seed)
+    _say(f"case hla3 B={B} H={H} n={n} d={d} dv={dv} chunk={chunk} dist={dist} normalized={normalized}")
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    num_ref, den_ref, _ = native.hla3_serial_c(q, k, v, masked=True, threads=16)
+    tol = tol_for(code)
+    num = hla.hla3_forward(qd, kd, vd, chunk).cpu().numpy()
+    err = rowwise_err(num, num_ref)
+    assert err <= tol, f"num row-wise error {err:.3e} > {tol}"
+    if normalized:
+        out = hla.hla3_forward(qd, kd, vd, chunk, normalized=True, eps=eps).cpu().numpy()
+        ones = torch.ones(B, H, n, dv, dtype=vd.dtype, device="cuda")
+        den = hla.hla3_forward(qd, kd, ones, chunk)[..., 0].cpu().numpy()
+        D = O3.hla3_den_scale(q, k)
+        e_den = float((np.abs(den - den_ref) / D).max())
+        assert e_den <= tol, f"den error {e_den:.3e} > {tol}"
+        good = np.abs(den_ref + eps) >= 0.05 * D
+        assert good.mean() > 0.3
+        ref = num_ref / (den_ref + eps)[..., None]
+        e_out = rowwise_err(out[good], ref[good])
+        assert e_out <= tol, f"normalised output error {e_out:.3e} > {tol}"
+    return err
+
+
+@pytest.mark.parametrize("d,dv", [(16, 16), (16, 32), (32, 16), (32, 32)])
+@pytest.mark.parametrize("chunk", [16, 32, 64])
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_hla3_shapes(d, dv, chunk, dist):
+    for (B, H, n) in ((1, 2, 3 * chunk + 5), (2, 1, 1), (1, 3, 100)):
+        _check(B, H, n, d, dv, chunk, dist, seed=n + d)
+
+
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_hla3_normalized(dist):
+    _check(2, 2, 150, 16, 16, 32, dist, normalized=True, seed=3)
+
+
+def test_hla3_small_first_rows():
+    """Rows whose value is far below the size of their terms (row 1 is
+    (q_1.k_1)^3 v_1, with q.k a cancelling dot product): seeds where this
+    shows, fp32 inputs, 1e-5 bar."""
+    for seed in range(6):
+        _check(1, 2, 200, 16, 16, 32, "scaled", seed=seed)
+
+
+@pytest.mark.parametrize("BH", [(1, 1), (4, 16)])
+def test_hla3_segment_counts(BH):
+    """Different head counts give different segment plans; results must agree."""
+    B, H = BH
+    _check(B, H, 700, 16, 16, 32, "scaled", seed=B * H)
+
+
+def test_hla3_workload_all_heads():
+    """B1 H8 n2048 d=dv=16 fp32, chunk 32: every head against the oracle."""
+    w = I.WORKLOADS["hla3-masked-fp32-B1H8-n2048-d16-C32"]
+    err = _check(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], w["dist"], seed=w["seed"])
+    _say(f"hla3 workload row-wise error {err:.3e}")
+
+
+def test_hla3_errors():
+    q = torch.zeros(1, 1, 64, 16, device="cuda")
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    out = torch.empty(1, 1, 64, 16, device="cuda")
+    args = (q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 64, 16, 16, 32)
+    with pytest.raises(capi.HLAError) as ei:          # unmasked is not built on the GPU
+        capi.hla3_forward(*args, 0, 0, 1e-6, I.HLA_FP32, ws.data_ptr(), ws.numel(), None)
+    assert ei.value.code == capi.HLA_ERR_UNSUPPORTED
+    with pytest.raises(capi.HLAError) as ei:          # workspace too small
+        capi.hla3_forward(*args, 1, 0, 1e-6, I.HLA_FP32, ws.data_ptr(), 16, None)
+    assert ei.value.code == capi.HLA_ERR_WORKSPACE
+    q64 = torch.zeros(1, 1, 64, 64, device="cuda")
+    with pytest.raises(capi.HLAError) as ei:
+        hla.hla3_forward(q64, q64, q64, 32)
+    assert ei.value.code == capi.HLA_ERR_UNSUPPORTED
+    assert capi.hla3_workspace_bytes(1, 1, 64, 64, 64, 32, I.HLA_FP32) == 0
