@@ -59,9 +59,11 @@ def kernel_costs(w, P=None):
                      tok * reference_flops_per_token(C, d, dv)),
             "walk_summary": ("hbm", sum_tok * qkv_tok + BH * (P - 1) * F * 4,
                              sum_tok * 2 * (2 * Ct * d + 2 * d * d + 2 * d * dv + d * dv)),
-            # per segment: S of the segments before it, its own record, Phi/eta written back
-            "seg_cross": ("hbm", BH * (ncross * (F + d * dv + d) + ncross * (ncross - 1) // 2 * d * d) * 4,
-                          BH * ncross * 2 * (d * d * dv + d * d)),
+            # segment moments: k read once, S = K^T K per segment written
+            "moments": ("hbm", tok * d * es + BH * P * d * d * 4, tok * 2 * d * d),
+            # carry fix-up: q read, out read and written (den read when normalised)
+            "fix": ("hbm", tok * (d * es + 8 * dv + (4 if w["normalized"] else 0)), tok * 2 * d * dv),
+            "init_convert": ("hbm", BH * 2 * F * 4, BH * 2 * (d * d * dv + d * d)),
             "total": ("hbm", BH * (P + 2) * F * 4, BH * 2 * (d * d * dv + d * d)),
         })
     return costs

@@ -38,6 +38,8 @@
 // as the B operand straight from registers (with two row waves per column
 // both keep a copy).  Q, K, K^T, V^T, W/T, R and R^T are staged in LDS as
 // bf16.
+#include <type_traits>
+
 #include "fused.h"
 #include "profile.h"
 
@@ -91,18 +93,31 @@ __device__ __forceinline__ f32x16 zero16() {
 }
 __device__ __forceinline__ int acc_row(int e, int g) { return 8 * (e >> 2) + 4 * g + (e & 3); }
 
+// Lane index.  With O set it passes through an empty asm statement, so each
+// fragment access computes its LDS address next to the access instead of the
+// compiler hoisting every distinct address out of a walk loop and keeping them
+// live (or spilled) through it; worth it only where registers run out.
+template <bool O = false>
+__device__ __forceinline__ int lane64() {
+  int l = threadIdx.x & 63;
+  if constexpr (O) asm volatile("" : "+v"(l));
+  return l;
+}
+
 // Operand fragment from a row-major bf16 LDS tile X[row][k]: lane takes
 // X[row0 + r][k0 + 8g .. 8g+7].  A operand of X Y, or B operand of Z X^T.
+template <bool O = false>
 __device__ __forceinline__ bf16x8 frag(const uint16_t* X, int ld, int row0, int k0) {
-  const int l = threadIdx.x & 63;
+  const int l = lane64<O>();
   const uint16_t* p = X + (row0 + (l & 31)) * ld + k0 + 8 * (l >> 5);
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 }
 
 // Same, in the k order of an accumulator-fed partner: lane takes
 // X[row0 + r][k0 + 4g .. 4g+3] and X[row0 + r][k0 + 8 + 4g .. 8+4g+3].
+template <bool O = false>
 __device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int row0, int k0) {
-  const int l = threadIdx.x & 63;
+  const int l = lane64<O>();
   const uint16_t* p = X + (row0 + (l & 31)) * ld + k0 + 4 * (l >> 5);
   const uint2 a = *reinterpret_cast<const uint2*>(p);
   const uint2 b = *reinterpret_cast<const uint2*>(p + 8);
@@ -122,8 +137,10 @@ __device__ __forceinline__ void frag_from_acc(const f32x16& t, int h, bf16x8& hi
 
 // Store an accumulator tile D[row0 + i][col0 + r] transposed as X[col0 + r][row0 + i],
 // split into hi/lo tiles (four 8-byte stores each).
+template <bool O = false>
 __device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
-  const int l = threadIdx.x & 63, g = l >> 5;
+  const int l = lane64<O>();
+  const int g = l >> 5;
   const int base = (col0 + (l & 31)) * ld + row0 + 4 * g;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -136,9 +153,11 @@ __device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_
 }
 
 // Both layouts from one split: transposed into (Th, Tl) and row-major into (Nh, Nl).
+template <bool O = false>
 __device__ __forceinline__ void store_TN(const f32x16& acc, uint16_t* Th, uint16_t* Tl, int ldT, uint16_t* Nh,
                                          uint16_t* Nl, int ldN, int row0, int col0) {
-  const int l = threadIdx.x & 63, g = l >> 5;
+  const int l = lane64<O>();
+  const int g = l >> 5;
   const int baseT = (col0 + (l & 31)) * ldT + row0 + 4 * g;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -156,8 +175,10 @@ __device__ __forceinline__ void store_TN(const f32x16& acc, uint16_t* Th, uint16
 }
 
 // Store an accumulator tile row-major as X[row0 + i][col0 + r], hi/lo.
+template <bool O = false>
 __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
-  const int l = threadIdx.x & 63, g = l >> 5;
+  const int l = lane64<O>();
+  const int g = l >> 5;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     uint16_t h, o;
@@ -171,7 +192,7 @@ __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_
 template <int C, int D, int DV, bool SUMMARY>
 struct Cfg {
   // Two reused buffers: B1 holds W, then R^T (after a barrier); B2 holds R,
-  // then T (after a barrier).  Summaries use only B1 and add Q^T.
+  // then T (after a barrier).  SUMMARY walks use only B1.
   static constexpr int CD = C > D ? C : D;
   static constexpr int ldQ = D + kPad, ldK = D + kPad, ldKt = C + kPad, ldVt = C + kPad;
   static constexpr int ld1 = C + kPad, ld2 = CD + kPad, ldQt = C + kPad;
@@ -185,7 +206,9 @@ struct Cfg {
   static constexpr int oB2h = oB1l + CD * ld1;
   static constexpr int oB2l = oB2h + (SUMMARY ? 0 : C * ld2);
   static constexpr int oQt = oB2l + (SUMMARY ? 0 : C * ld2);
-  static constexpr int n16 = oQt + (SUMMARY ? D * ldQt : 0);          // bf16 elements of tiles
+  // bf16 elements of the tile region; at least D*D floats, where the walk's
+  // prologue stages the S carry before the first tile
+  static constexpr int n16 = oQt > 2 * D * D ? oQt : 2 * D * D;
   static constexpr int RT = C / 32, DT = D / 32, VT = DV / 32;       // 32-wide tiles
   static constexpr int KC = C / 16, KD = D / 16;                     // 16-deep k steps
   // Wave w owns column tile ct = w % NCT of R, O, S0 and Phi0 and the row
@@ -395,18 +418,325 @@ __global__ __launch_bounds__(256) void k_total(const float* __restrict__ segs, c
   xv_plus<D>(XT, y, out + off_h(D, DV), -1.f, out + off_h(D, DV));
 }
 
+// ---------------------------------------------------------------------------
+// Segment moments.  The walks start from the true S prefix, so every segment
+// needs S of the segments before it; with a final state also C and m.  grid
+// (nseg, BH), 4 waves: S = K^T K and C = Q^T V over the segment's tiles on
+// MFMA (q/k/v are exact in bf16, one pass), m = Q^T 1.  Written to the S, C
+// and m slots of the segment's record.
+template <int C, int D, int DV>
+__global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                                                      const uint16_t* __restrict__ v, float* __restrict__ rec, int n,
+                                                      int cps, int nseg, int want_cm) {
+  constexpr int ld = C + kPad, DT = D / 32, VT = DV / 32, KC = C / 16;
+  constexpr int nS = (DT * DT + kWaves - 1) / kWaves, nC = (DT * VT + kWaves - 1) / kWaves;
+  constexpr int segQ = C * D / 8, segV = C * DV / 8;
+  __shared__ __align__(16) uint16_t Kt[D * ld], Qt[D * ld], Vt[DV * ld];
+  const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
+  const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t rk = make_rsrc(k + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t rv = make_rsrc(v + (size_t)bh * n * DV, (uint32_t)n * DV * 2);
+  f32x16 sacc[nS], cacc[nC];
+#pragma unroll
+  for (int i = 0; i < nS; ++i) sacc[i] = zero16();
+#pragma unroll
+  for (int i = 0; i < nC; ++i) cacc[i] = zero16();
+  float macc = 0.f;
+  if (!want_cm) {
+    // S only: K tiles streamed through a ring of PF register slots (loads are
+    // unconditional; the tile index is clamped to the segment), so PF tiles
+    // are in flight while one is multiplied
+    constexpr int PF = 4, NL = (segQ + kThreads - 1) / kThreads;
+    uint4 kb[PF][NL];
+    auto load = [&](int c, auto slot_tag) {
+      constexpr int sl = decltype(slot_tag)::value;
+      const uint32_t t0 = (uint32_t)min(c, c1 - 1) * C;
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        const int e = min(tid + kThreads * i, segQ - 1);
+        kb[sl][i] = buf_load16(rk, ((t0 + e % C) * D + (e / C) * 8) * 2);
+      }
+    };
+    auto step = [&](int c, auto slot_tag) {
+      constexpr int sl = decltype(slot_tag)::value;
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        const int e = tid + kThreads * i;
+        if (e < segQ) {
+          const int t = e % C, a8 = (e / C) * 8;
+          const uint16_t* k8 = reinterpret_cast<const uint16_t*>(&kb[sl][i]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
+        }
+      }
+      __syncthreads();
+      load(c + PF, slot_tag);
+#pragma unroll
+      for (int i = 0; i < nS; ++i) {
+        const int ti = w + kWaves * i;
+        if (ti < DT * DT) {
+          const int it = ti / DT, jt = ti % DT;
+#pragma unroll
+          for (int s = 0; s < KC; ++s)
+            sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
+        }
+      }
+      __syncthreads();
+    };
+    if (c0 < c1) {
+      load(c0, std::integral_constant<int, 0>());
+      load(c0 + 1, std::integral_constant<int, 1>());
+      load(c0 + 2, std::integral_constant<int, 2>());
+      load(c0 + 3, std::integral_constant<int, 3>());
+    }
+    for (int c = c0; c < c1; c += PF) {
+      step(c, std::integral_constant<int, 0>());
+      if (c + 1 < c1) step(c + 1, std::integral_constant<int, 1>());
+      if (c + 2 < c1) step(c + 2, std::integral_constant<int, 2>());
+      if (c + 3 < c1) step(c + 3, std::integral_constant<int, 3>());
+    }
+  }
+  for (int c = want_cm ? c0 : c1; c < c1; ++c) {
+    const uint32_t t0 = (uint32_t)c * C;
+    for (int e = tid; e < segQ; e += kThreads) {        // consecutive lanes take consecutive tokens
+      const int t = e % C, a8 = (e / C) * 8;
+      const uint32_t off = ((t0 + t) * D + a8) * 2;
+      const uint4 kk = buf_load16(rk, off);
+      const uint16_t* k8 = reinterpret_cast<const uint16_t*>(&kk);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
+      if (want_cm) {
+        const uint4 qq = buf_load16(rq, off);
+        const uint16_t* q8 = reinterpret_cast<const uint16_t*>(&qq);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) Qt[(a8 + j) * ld + t] = q8[j];
+      }
+    }
+    if (want_cm)
+      for (int e = tid; e < segV; e += kThreads) {
+        const int t = e % C, b8 = (e / C) * 8;
+        const uint4 vv = buf_load16(rv, ((t0 + t) * DV + b8) * 2);
+        const uint16_t* v8 = reinterpret_cast<const uint16_t*>(&vv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) Vt[(b8 + j) * ld + t] = v8[j];
+      }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < nS; ++i) {
+      const int ti = w + kWaves * i;
+      if (ti < DT * DT) {
+        const int it = ti / DT, jt = ti % DT;
+#pragma unroll
+        for (int s = 0; s < KC; ++s) sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
+      }
+    }
+    if (want_cm) {
+#pragma unroll
+      for (int i = 0; i < nC; ++i) {
+        const int ti = w + kWaves * i;
+        if (ti < DT * VT) {
+          const int it = ti / VT, jt = ti % VT;
+#pragma unroll
+          for (int s = 0; s < KC; ++s)
+            cacc[i] = mfma(frag(Qt, ld, it * 32, s * 16), frag(Vt, ld, jt * 32, s * 16), cacc[i]);
+        }
+      }
+      if (tid < D) {
+        const uint16_t* row = Qt + tid * ld;
+#pragma unroll
+        for (int t8 = 0; t8 < C; t8 += 8) {
+          const uint4 u = *reinterpret_cast<const uint4*>(row + t8);
+          const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) macc += bf16_to_f(e8[j]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  float* r = rec + ((size_t)bh * (nseg + 1) + seg) * state_floats(D, DV);
+#pragma unroll
+  for (int i = 0; i < nS; ++i) {
+    const int ti = w + kWaves * i;
+    if (ti < DT * DT) {
+      const int it = ti / DT, jt = ti % DT;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) r[(size_t)(it * 32 + acc_row(e, lg)) * D + jt * 32 + lr] = sacc[i][e];
+    }
+  }
+  if (want_cm) {
+#pragma unroll
+    for (int i = 0; i < nC; ++i) {
+      const int ti = w + kWaves * i;
+      if (ti < DT * VT) {
+        const int it = ti / VT, jt = ti % VT;
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          r[off_C(D, DV) + (size_t)(it * 32 + acc_row(e, lg)) * DV + jt * 32 + lr] = cacc[i][e];
+      }
+    }
+    if (tid < D) r[off_m(D, DV) + tid] = macc;
+  }
+}
+
+// The carry fix-up.  The walks run every segment with Phi0 = eta0 = 0, so
+// their outputs miss q_t^T Phi_c and q_t . eta_c, where (Phi_c, eta_c) is the
+// sum of the converted initial state and the brackets of the segments before
+// this one (the Phi form of Eq. (semidirect)).
+//
+// k_carry: (Phi_c, eta_c) of every segment, as running sums over the records
+// (fp32, the G|h layout: Phi_c [D][DV] then eta_c [D]).  grid
+// (ceil((D*DV + D) / 256), BH); element-parallel and coalesced.
+template <int D, int DV>
+__global__ __launch_bounds__(256) void k_carry(const float* __restrict__ rec, const float* __restrict__ init,
+                                               float* __restrict__ carry, int nseg) {
+  constexpr int NC = D * DV + D;
+  const int bh = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= NC) return;
+  const size_t F = state_floats(D, DV);
+  const float* base = rec + (size_t)bh * (nseg + 1) * F + off_G(D, DV) + e;   // G and h slots are adjacent
+  float x = init ? base[(size_t)nseg * F] : 0.f;
+  for (int sp = 0; sp < nseg; ++sp) {
+    carry[((size_t)bh * nseg + sp) * NC + e] = x;
+    x += base[(size_t)sp * F];
+  }
+}
+
+// k_fix: one workgroup per (kFixTiles consecutive tiles, block of up to 64
+// value columns, head), 4 waves: out_t += q_t^T Phi_c on MFMA (q exact in
+// bf16, Phi_c split hi/lo while staged), then out_t /= (den_t + q_t . eta_c +
+// eps) when normalised.  Tiles of segment 0 have nothing to add unless there
+// is an initial state or a division.
+constexpr int kFixTiles = 4;
+
+template <int DV>
+constexpr int fix_cols() { return DV < 64 ? DV : 64; }
+
+template <int C, int D, int DV>
+constexpr size_t fix_lds_bytes() {
+  return 2 * ((size_t)C * (D + kPad) + 2 * (size_t)fix_cols<DV>() * (D + kPad)) + 4 * (2 * (size_t)D + C);
+}
+
+template <int C, int D, int DV>
+__global__ __launch_bounds__(kThreads) void k_fix(const uint16_t* __restrict__ q, float* __restrict__ out,
+                                                  const float* __restrict__ den_in, const float* __restrict__ carry,
+                                                  int has_init, int n, int cps, int nseg, int normalized, float eps) {
+  constexpr int XC = fix_cols<DV>(), ldQ = D + kPad, ldX = D + kPad, RT = C / 32, VT = XC / 32, KD = D / 16;
+  constexpr int NTI = RT * VT, nT = (NTI + kWaves - 1) / kWaves, NC = D * DV + D;
+  extern __shared__ __align__(16) uint16_t lds[];   // Q | Phi_c^T hi | Phi_c^T lo (XC columns), fp32 eta_c, eta, 1/den
+  uint16_t* Qs = lds;
+  uint16_t* Xh = Qs + C * ldQ;
+  uint16_t* Xl = Xh + XC * ldX;
+  float* ec = reinterpret_cast<float*>(Xl + XC * ldX);
+  float* es = ec + D;
+  float* inv = es + D;
+  const int bh = blockIdx.z, col0 = blockIdx.y * XC, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int M = (n + C - 1) / C;
+  const int c0 = blockIdx.x * kFixTiles, c1 = min(M, c0 + kFixTiles);
+  const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
+  const rsrc_t ro = make_rsrc(out + (size_t)bh * n * DV, (uint32_t)n * DV * 4);
+  int loaded = -1;
+  for (int c = c0; c < c1; ++c) {
+    const int seg = c / cps;
+    if (seg == 0 && !has_init && !normalized) continue;      // uniform: nothing to do for this tile
+    const uint32_t t0 = (uint32_t)c * C;
+    if (seg != loaded) {                                      // this segment's carry columns into LDS, split
+      const float* cb = carry + ((size_t)bh * nseg + seg) * NC;
+      for (int e = tid; e < D * XC; e += kThreads) {
+        const int a = e / XC, b = e % XC;
+        uint16_t hi, lo;
+        split(cb[(size_t)a * DV + col0 + b], hi, lo);
+        Xh[b * ldX + a] = hi;
+        Xl[b * ldX + a] = lo;
+      }
+      for (int a = tid; a < D; a += kThreads) ec[a] = cb[D * DV + a];
+      loaded = seg;
+    }
+    for (int e = tid; e < C * D / 8; e += kThreads) {
+      const int t = e / (D / 8), a8 = (e % (D / 8)) * 8;
+      *reinterpret_cast<uint4*>(Qs + t * ldQ + a8) = buf_load16(rq, ((t0 + t) * D + a8) * 2);
+    }
+    if (normalized && tid < D)      // eta of the tile start: the walk's eta0 + eta_c
+      es[tid] = ec[tid] + den_in[(size_t)gridDim.z * n + ((size_t)bh * M + c) * D + tid];
+    // this wave's earlier output values, in flight during the products
+    float prev[nT][16];
+#pragma unroll
+    for (int i = 0; i < nT; ++i) {
+      const int ti = w + kWaves * i;
+      if (ti < NTI) {
+        const int rt = ti / VT, ct = ti % VT;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer: loads read 0, stores drop
+          const int t = rt * 32 + acc_row(e, lg);
+          prev[i][e] = __uint_as_float(
+              __builtin_amdgcn_raw_buffer_load_b32(ro, (int)(((t0 + t) * DV + col0 + ct * 32 + lr) * 4), 0, 0));
+        }
+      }
+    }
+    __syncthreads();
+    if (normalized) {               // den_t = rowsum_t + q_t . es, TPR lanes per row
+      constexpr int TPR = kThreads / C < D / 8 ? kThreads / C : D / 8, PER = D / TPR;
+      static_assert(PER % 8 == 0 && TPR * C <= kThreads, "den lanes");
+      const int t = tid / TPR, p0 = (tid % TPR) * PER;
+      const uint16_t* row = Qs + (t < C ? t : C - 1) * ldQ + p0;
+      float s = 0.f;
+#pragma unroll
+      for (int a = 0; a < PER; a += 8) {
+        const uint4 x = *reinterpret_cast<const uint4*>(row + a);
+        const uint32_t u[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          s += __uint_as_float(u[j] << 16) * es[p0 + a + 2 * j];
+          s += __uint_as_float(u[j] & 0xffff0000u) * es[p0 + a + 2 * j + 1];
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o);
+      if (tid % TPR == 0 && t < C) inv[t] = (t0 + t < (uint32_t)n) ? 1.f / (den_in[(size_t)bh * n + t0 + t] + s + eps) : 0.f;
+      __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < nT; ++i) {
+      const int ti = w + kWaves * i;
+      if (ti < NTI) {
+        const int rt = ti / VT, ct = ti % VT;
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int s = 0; s < KD; ++s) {
+          const bf16x8 aQ = frag(Qs, ldQ, rt * 32, s * 16);
+          acc = mfma(aQ, frag(Xh, ldX, ct * 32, s * 16), acc);
+          acc = mfma(aQ, frag(Xl, ldX, ct * 32, s * 16), acc);
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int t = rt * 32 + acc_row(e, lg);
+          float y = prev[i][e] + acc[e];
+          if (normalized) y *= inv[t];
+          buf_store4(ro, ((t0 + t) * DV + col0 + ct * 32 + lr) * 4, y);
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // One segment walk.  grid = (segments, BH), 4 waves.  Wave w owns column tile
 // ct = w % NCT of R and of O and keeps column ct of S0 and of Phi0 (all their
 // rows) in accumulators; it works on the row tiles rg, rg + NRG, ...
-// SUMMARY: zero carry, writes the segment summary (S, C, m, Phi, eta) to
-// rec[bh][seg].  !SUMMARY: the carry is the sum of the converted initial
-// state and the brackets of the segments before this one (k_seg_cross); then
-// writes outputs.
+// The walk starts from S0 = the S prefix before the segment (the moments of
+// the converted initial state and of the earlier segments) and Phi0 = eta0 = 0,
+// and ends by writing the segment's bracket (its Phi0, eta0) into the Phi/eta
+// slots of its record.  !SUMMARY also writes num (without the Phi carry of
+// earlier segments) to out and, when normalised, den to den_out; k_fix adds
+// the carry and divides.  SUMMARY skips T and O.
 template <int C, int D, int DV, bool SUMMARY>
 __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k_walk(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    float* __restrict__ out, float* __restrict__ rec, const float* __restrict__ init, int n, int cps, int nseg,
-    int normalized, float eps) {
+    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ init,
+    int n, int cps, int nseg, int normalized, float eps) {
   using G = Cfg<C, D, DV, SUMMARY>;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
@@ -421,11 +751,9 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
   uint16_t* Rl = lds + G::oB2l;
   uint16_t* Th = Rh;
   uint16_t* Tl = Rl;
-  uint16_t* Qt = lds + G::oQt;
   float* fl = reinterpret_cast<float*>(lds + ((G::n16 + 7) & ~7));
   float* eta = fl + G::f_eta;
   float* colsum = fl + G::f_cs;       // [RT][D]
-  float* den = fl + G::f_den;         // [C]
   float* denp = fl + G::f_denp;       // [RT][C]
 
   const int seg = blockIdx.x, bh = blockIdx.y;
@@ -439,69 +767,45 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t F = state_floats(D, DV);
-  float* rc = SUMMARY ? rec + ((size_t)bh * (nseg + 1) + seg) * F : nullptr;
+  float* rc = rec + ((size_t)bh * (nseg + 1) + seg) * F;
   const rsrc_t ro = make_rsrc(SUMMARY ? nullptr : out + (size_t)bh * n * DV, SUMMARY ? 0u : (uint32_t)n * DV * 4);
 
   // ---- carry in (fp32 accumulators, column ct, all rows) ----
-  f32x16 S0[G::DT], P0[G::DT], Cs[SUMMARY ? G::DT : 1];
+  f32x16 S0[G::DT], P0[G::DT];
 #pragma unroll
   for (int i = 0; i < G::DT; ++i) {
     S0[i] = zero16();
     P0[i] = zero16();
-    if (SUMMARY) Cs[SUMMARY ? i : 0] = zero16();
   }
   for (int a = tid; a < D; a += kThreads) eta[a] = 0.f;
-  if constexpr (!SUMMARY) {
-    if (seg > 0 || init) {
-      // sum the records in float4 registers; stage S0, then Phi0, in the
-      // (still free) tile region of LDS; every wave picks up its columns
-      constexpr int nS4 = D * D / 4 / kThreads, nP4 = D * DV / 4 / kThreads;
-      static_assert(D * D % (4 * kThreads) == 0 && D * DV % (4 * kThreads) == 0, "record split");
-      static_assert(D * D * 4 <= G::n16 * 2 && D * DV * 4 <= G::n16 * 2, "carry staging fits the tile region");
-      float4 sa[nS4], pa[nP4];
-      float ea = 0.f;
-      const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (seg > 0 || init) {
+    // S0 = sum of the S slots of the converted initial state and the earlier
+    // segments, in float4 registers, staged through the (still free) tile
+    // region of LDS; every wave picks up its columns
+    constexpr int nS4 = D * D / 4 / kThreads;
+    static_assert(D * D % (4 * kThreads) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
+    float4 sa[nS4];
 #pragma unroll
-      for (int r = 0; r < nS4; ++r) sa[r] = z4;
+    for (int r = 0; r < nS4; ++r) sa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sp = init ? -1 : 0; sp < seg; ++sp) {
+      const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
 #pragma unroll
-      for (int r = 0; r < nP4; ++r) pa[r] = z4;
-      for (int sp = init ? -1 : 0; sp < seg; ++sp) {
-        const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
-#pragma unroll
-        for (int r = 0; r < nS4; ++r) {
-          const float4 u = reinterpret_cast<const float4*>(x)[tid + kThreads * r];
-          sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
-        }
-#pragma unroll
-        for (int r = 0; r < nP4; ++r) {
-          const float4 u = reinterpret_cast<const float4*>(x + off_G(D, DV))[tid + kThreads * r];
-          pa[r].x += u.x; pa[r].y += u.y; pa[r].z += u.z; pa[r].w += u.w;
-        }
-        if (tid < D) ea += x[off_h(D, DV) + tid];
+      for (int r = 0; r < nS4; ++r) {
+        const float4 u = reinterpret_cast<const float4*>(x)[tid + kThreads * r];
+        sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
       }
-      float* st = reinterpret_cast<float*>(lds);
-#pragma unroll
-      for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + kThreads * r] = sa[r];
-      if (tid < D) eta[tid] = ea;
-      __syncthreads();
-      if (has_r)
-#pragma unroll
-        for (int i = 0; i < G::DT; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) S0[i][e] = st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
-      __syncthreads();
-#pragma unroll
-      for (int r = 0; r < nP4; ++r) reinterpret_cast<float4*>(st)[tid + kThreads * r] = pa[r];
-      __syncthreads();
-      if (has_o)
-#pragma unroll
-        for (int i = 0; i < G::DT; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) P0[i][e] = st[(i * 32 + acc_row(e, lg)) * DV + ct * 32 + lr];
-      __syncthreads();
     }
+    float* st = reinterpret_cast<float*>(lds);
+#pragma unroll
+    for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + kThreads * r] = sa[r];
+    __syncthreads();
+    if (has_r)
+#pragma unroll
+      for (int i = 0; i < G::DT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S0[i][e] = st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+    __syncthreads();
   }
-  float m_acc = 0.f;   // SUMMARY: column sum of Q for column tid (< D)
 
   // ---- prefetch registers for the next chunk (buffer loads: the tail past n reads zero) ----
   const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
@@ -540,11 +844,6 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         const uint16_t* kk = reinterpret_cast<const uint16_t*>(&pk[i]);
 #pragma unroll
         for (int j = 0; j < 8; ++j) Kt[(a8 + j) * G::ldKt + t] = kk[j];
-        if (SUMMARY) {
-          const uint16_t* qq = reinterpret_cast<const uint16_t*>(&pq[i]);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) Qt[(a8 + j) * G::ldQt + t] = qq[j];
-        }
       }
     }
 #pragma unroll
@@ -559,16 +858,6 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     }
     __syncthreads();
     if (c + 1 < c_end) fetch(c + 1);
-    if (SUMMARY && tid < D) {
-      const uint16_t* row = Qt + tid * G::ldQt;
-#pragma unroll
-      for (int t8 = 0; t8 < C; t8 += 8) {
-        const uint4 u = *reinterpret_cast<const uint4*>(row + t8);
-        const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) m_acc += bf16_to_f(e8[j]);
-      }
-    }
 
     // ---- stage 1: W = L (.) Q K^T, computed as W^T = K Q^T and stored transposed ----
     {
@@ -684,20 +973,16 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         if (tile) store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);
       }
       __syncthreads();
-      // den_t = sum_j T[t][j] + q_t . eta0, stored as 1 / (den_t + eps)
-      if (normalized && tid < C) {
-        float s = 0.f;
+      // den_t = sum_j T[t][j] + q_t . eta0: the row sums here, and eta0 of this
+      // tile (before its advance) for k_fix, which adds q_t . (eta0 + eta_c)
+      if (normalized) {
+        if (tid < C && t0 + tid < n) {
+          float s = 0.f;
 #pragma unroll
-        for (int i = 0; i < G::RT; ++i) s += denp[i * C + tid];
-        const uint16_t* row = Qs + tid * G::ldQ;
-#pragma unroll
-        for (int a8 = 0; a8 < D; a8 += 8) {
-          const uint4 u = *reinterpret_cast<const uint4*>(row + a8);
-          const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) s += bf16_to_f(e8[j]) * eta[a8 + j];
+          for (int i = 0; i < G::RT; ++i) s += denp[i * C + tid];
+          den_out[(size_t)bh * n + t0 + tid] = s;
         }
-        den[tid] = 1.f / (s + eps);
+        if (tid < D) den_out[(size_t)gridDim.y * n + ((size_t)bh * ((n + C - 1) / C) + c) * D + tid] = eta[tid];
       }
       __syncthreads();
       // ---- stage 4: O = T V + Q Phi0 (old Phi0) on column tile ct; stage 5: Phi0 += R^T V ----
@@ -738,15 +1023,13 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
 #pragma unroll
             for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer and are dropped
               const int t = rt * 32 + acc_row(e, lg);
-              float o = oacc[i][e];
-              if (normalized) o *= den[t];
-              buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, o);
+              buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, oacc[i][e]);
             }
         }
       }
     }
     if (upd_p) {
-      // Phi0 += R^T V (and, for summaries, C += Q^T V) on column ct
+      // Phi0 += R^T V on column ct
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
         const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
@@ -754,7 +1037,6 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         for (int i = 0; i < G::DT; ++i) {
           P0[i] = mfma(frag(Rth, G::ldRt, i * 32, s * 16), bV, P0[i]);
           P0[i] = mfma(frag(Rtl, G::ldRt, i * 32, s * 16), bV, P0[i]);
-          if (SUMMARY) Cs[SUMMARY ? i : 0] = mfma(frag(Qt, G::ldQt, i * 32, s * 16), bV, Cs[SUMMARY ? i : 0]);
         }
       }
     }
@@ -762,28 +1044,16 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     if (tid < D) eta[tid] += eta_add;
   }
 
-  if (SUMMARY) {
-    // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
-    if (has_r && rg == 0)
+  // the segment's bracket: Phi0 into the G slot, eta0 into the h slot (the
+  // opaque lane index keeps the store addresses out of the walk's live range)
+  int col = ct * 32 + lr;
+  asm volatile("" : "+v"(col));
+  if (has_o && rg == 0)
 #pragma unroll
-      for (int i = 0; i < G::DT; ++i)
+    for (int i = 0; i < G::DT; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) rc[(size_t)(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr] = S0[i][e];
-    if (upd_p)
-#pragma unroll
-      for (int i = 0; i < G::DT; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const size_t o = (size_t)(i * 32 + acc_row(e, lg)) * DV + ct * 32 + lr;
-          rc[off_G(D, DV) + o] = P0[i][e];
-          rc[off_C(D, DV) + o] = Cs[SUMMARY ? i : 0][e];
-        }
-    __syncthreads();
-    if (tid < D) {
-      rc[off_m(D, DV) + tid] = m_acc;
-      rc[off_h(D, DV) + tid] = eta[tid];
-    }
-  }
+      for (int e = 0; e < 16; ++e) rc[off_G(D, DV) + (size_t)(i * 32 + acc_row(e, lg)) * DV + col] = P0[i][e];
+  if (tid < D) rc[off_h(D, DV) + tid] = eta[tid];
 }
 
 // ---------------------------------------------------------------------------
@@ -810,9 +1080,9 @@ struct CfgRS {
   static constexpr int oVt = oKt + D * ldKt;
   static constexpr int oB1h = oVt + DV * ldVt;                 // W, then R^T
   static constexpr int oB1l = oB1h + D * ld1;
-  static constexpr int oB2h = oB1l + D * ld1;                  // R (then the O exchange) | Q^T (summary)
+  static constexpr int oB2h = oB1l + D * ld1;                  // R (then the O exchange); absent in summaries
   static constexpr int oB2l = oB2h + C * ld2;
-  static constexpr int n16 = SUMMARY ? oB2h + D * ldQt : oB2l + C * ld2;
+  static constexpr int n16 = SUMMARY ? oB2h : oB2l + C * ld2;
   static constexpr int oX = oK;                                // R exchange, then T (hi | lo)
   static constexpr int oTh = oK, oTl = oK + C * ldT;
   static constexpr int xfl = 2 * NCT * 1024;                   // exchange floats
@@ -830,14 +1100,16 @@ struct CfgRS {
 
 // Exchange slot of (column tile ct, row tile rt): 32 x 32 fp32 in MFMA
 // accumulator order, element 4q + j of lane l at [(slot * 4 + q) * 64 + l] * 4 + j.
+template <bool O = false>
 __device__ __forceinline__ void xch_put(float* X, int slot, const f32x16& a) {
-  const int l = threadIdx.x & 63;
+  const int l = lane64<O>();
 #pragma unroll
   for (int q = 0; q < 4; ++q)
     *reinterpret_cast<float4*>(X + ((slot * 4 + q) * 64 + l) * 4) = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
 }
+template <bool O = false>
 __device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a) {
-  const int l = threadIdx.x & 63;
+  const int l = lane64<O>();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float4 u = *reinterpret_cast<const float4*>(X + ((slot * 4 + q) * 64 + l) * 4);
@@ -848,9 +1120,10 @@ __device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a) {
 template <int D, bool SUMMARY>
 __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlocks)) void k_walk_rs(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    float* __restrict__ out, float* __restrict__ rec, const float* __restrict__ init, int n, int cps, int nseg,
-    int normalized, float eps) {
+    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ init,
+    int n, int cps, int nseg, int normalized, float eps) {
   using G = CfgRS<D, SUMMARY>;
+  constexpr bool kO = D == 128;     // at 512 threads the hoisted LDS addresses would spill
   constexpr int C = G::C, DV = G::DV, NT = G::NT;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
@@ -861,7 +1134,6 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   uint16_t* Wl = lds + G::oB1l;
   uint16_t* Rh = lds + G::oB2h;   // R
   uint16_t* Rl = lds + G::oB2l;
-  uint16_t* Qt = lds + G::oB2h;   // summaries
   uint16_t* Th = lds + G::oTh;
   uint16_t* Tl = lds + G::oTl;
   float* XR = reinterpret_cast<float*>(lds + G::oX);     // R exchange
@@ -869,7 +1141,6 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   float* fl = reinterpret_cast<float*>(lds + ((G::n16 + 7) & ~7));
   float* eta = fl + G::f_eta;
   float* colsum = fl + G::f_cs;       // [RT][D]
-  float* den = fl + G::f_den;         // [C]
   float* denp = fl + G::f_denp;       // [RT][C]
 
   const int seg = blockIdx.x, bh = blockIdx.y;
@@ -880,59 +1151,43 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t F = state_floats(D, DV);
-  float* rc = SUMMARY ? rec + ((size_t)bh * (nseg + 1) + seg) * F : nullptr;
+  float* rc = rec + ((size_t)bh * (nseg + 1) + seg) * F;
   const rsrc_t ro = make_rsrc(SUMMARY ? nullptr : out + (size_t)bh * n * DV, SUMMARY ? 0u : (uint32_t)n * DV * 4);
 
   // ---- carry in: rows r0 .. r0 + D/2 of column tile ct ----
-  f32x16 S0[G::HT], P0[G::HT], Cs[SUMMARY ? G::HT : 1];
+  f32x16 S0[G::HT], P0[G::HT];
 #pragma unroll
   for (int i = 0; i < G::HT; ++i) {
     S0[i] = zero16();
     P0[i] = zero16();
-    if (SUMMARY) Cs[SUMMARY ? i : 0] = zero16();
   }
   for (int a = tid; a < D; a += NT) eta[a] = 0.f;
-  if constexpr (!SUMMARY) {
-    if (seg > 0 || init) {
-      constexpr int nS4 = D * D / 4 / NT;
-      static_assert(D * D % (4 * NT) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
-      float4 sa[nS4], pa[nS4];
-      float ea = 0.f;
-      const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (seg > 0 || init) {
+    // S0 = sum of the S slots of the converted initial state and the earlier
+    // segments, staged through the (still free) tile region of LDS
+    constexpr int nS4 = D * D / 4 / NT;
+    static_assert(D * D % (4 * NT) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
+    float4 sa[nS4];
 #pragma unroll
-      for (int r = 0; r < nS4; ++r) sa[r] = pa[r] = z4;
-      for (int sp = init ? -1 : 0; sp < seg; ++sp) {
-        const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
+    for (int r = 0; r < nS4; ++r) sa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sp = init ? -1 : 0; sp < seg; ++sp) {
+      const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
 #pragma unroll
-        for (int r = 0; r < nS4; ++r) {
-          const float4 u = reinterpret_cast<const float4*>(x)[tid + NT * r];
-          const float4 g = reinterpret_cast<const float4*>(x + off_G(D, DV))[tid + NT * r];
-          sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
-          pa[r].x += g.x; pa[r].y += g.y; pa[r].z += g.z; pa[r].w += g.w;
-        }
-        if (tid < D) ea += x[off_h(D, DV) + tid];
+      for (int r = 0; r < nS4; ++r) {
+        const float4 u = reinterpret_cast<const float4*>(x)[tid + NT * r];
+        sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
       }
-      float* st = reinterpret_cast<float*>(lds);
-#pragma unroll
-      for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = sa[r];
-      if (tid < D) eta[tid] = ea;
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < G::HT; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) S0[i][e] = st[(r0 + i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
-      __syncthreads();
-#pragma unroll
-      for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = pa[r];
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < G::HT; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) P0[i][e] = st[(r0 + i * 32 + acc_row(e, lg)) * DV + ct * 32 + lr];
-      __syncthreads();
     }
+    float* st = reinterpret_cast<float*>(lds);
+#pragma unroll
+    for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = sa[r];
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < G::HT; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) S0[i][e] = st[(r0 + i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+    __syncthreads();
   }
-  float m_acc = 0.f;   // SUMMARY: column sum of Q for column tid (< D)
 
   // ---- prefetch registers for the next chunk (buffer loads: the tail past n reads zero) ----
   const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
@@ -968,11 +1223,6 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       const uint16_t* kk = reinterpret_cast<const uint16_t*>(&pk[i]);
 #pragma unroll
       for (int j = 0; j < 8; ++j) Kt[(a8 + j) * G::ldKt + t] = kk[j];
-      if (SUMMARY) {
-        const uint16_t* qq = reinterpret_cast<const uint16_t*>(&pq[i]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) Qt[(a8 + j) * G::ldQt + t] = qq[j];
-      }
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
@@ -984,16 +1234,6 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     }
     __syncthreads();
     if (c + 1 < c_end) fetch(c + 1);
-    if (SUMMARY && tid < D) {
-      const uint16_t* row = Qt + tid * G::ldQt;
-#pragma unroll
-      for (int t8 = 0; t8 < C; t8 += 8) {
-        const uint4 u = *reinterpret_cast<const uint4*>(row + t8);
-        const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) m_acc += bf16_to_f(e8[j]);
-      }
-    }
 
     // ---- stage 1: W = L (.) Q K^T on tiles (key it <= query jt), stored transposed ----
     if (w < 4) {
@@ -1002,11 +1242,11 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         f32x16 acc = zero16();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
-          acc = mfma(frag(Ks, G::ldK, it * 32, s * 16), frag(Qs, G::ldQ, jt * 32, s * 16), acc);
+          acc = mfma(frag<kO>(Ks, G::ldK, it * 32, s * 16), frag<kO>(Qs, G::ldQ, jt * 32, s * 16), acc);
 #pragma unroll
         for (int e = 0; e < 16; ++e)   // keep key i <= query t
           if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
-        store_T(acc, Wh, Wl, G::ld1, it * 32, jt * 32);
+        store_T<kO>(acc, Wh, Wl, G::ld1, it * 32, jt * 32);
       }
     }
     __syncthreads();
@@ -1021,32 +1261,32 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       frag_from_acc(S0[j >> 1], j & 1, bh_, bl_);
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, r0 + j * 16);
+        const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, r0 + j * 16);
         part[rt] = mfma(aQ, bh_, part[rt]);
         part[rt] = mfma(aQ, bl_, part[rt]);
       }
     }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
+      const bf16x8 bK = frag<kO>(Kt, G::ldKt, ct * 32, s * 16);
       if (h == 0) {
         if (s < 2) {
-          part[0] = mfma(frag(Wh, G::ld1, 0, s * 16), bK, part[0]);
-          part[0] = mfma(frag(Wl, G::ld1, 0, s * 16), bK, part[0]);
+          part[0] = mfma(frag<kO>(Wh, G::ld1, 0, s * 16), bK, part[0]);
+          part[0] = mfma(frag<kO>(Wl, G::ld1, 0, s * 16), bK, part[0]);
         }
       } else {
-        part[1] = mfma(frag(Wh, G::ld1, 32, s * 16), bK, part[1]);
-        part[1] = mfma(frag(Wl, G::ld1, 32, s * 16), bK, part[1]);
+        part[1] = mfma(frag<kO>(Wh, G::ld1, 32, s * 16), bK, part[1]);
+        part[1] = mfma(frag<kO>(Wl, G::ld1, 32, s * 16), bK, part[1]);
       }
       // S0 += K^T K on this wave's rows
 #pragma unroll
-      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag(Kt, G::ldKt, r0 + i * 32, s * 16), bK, S0[i]);
+      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag<kO>(Kt, G::ldKt, r0 + i * 32, s * 16), bK, S0[i]);
     }
     __syncthreads();                      // K, K^T and W are dead: K | K^T takes the exchange
-    xch_put(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0]);
+    xch_put<kO>(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0]);
     __syncthreads();
     f32x16 racc = h == 0 ? part[0] : part[1];
-    xch_add(XR, ct * 2 + h, racc);
+    xch_add<kO>(XR, ct * 2 + h, racc);
     {
       float cs = 0.f;
 #pragma unroll
@@ -1055,9 +1295,9 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       if (lg == 0) colsum[h * D + ct * 32 + lr] = cs;
     }
     if (SUMMARY)
-      store_T(racc, Wh, Wl, G::ld1, h * 32, ct * 32);
+      store_T<kO>(racc, Wh, Wl, G::ld1, h * 32, ct * 32);
     else
-      store_TN(racc, Wh, Wl, G::ld1, Rh, Rl, G::ld2, h * 32, ct * 32);
+      store_TN<kO>(racc, Wh, Wl, G::ld1, Rh, Rl, G::ld2, h * 32, ct * 32);
     __syncthreads();
     float eta_add = 0.f;
     if (tid < D) eta_add = colsum[tid] + colsum[D + tid];
@@ -1071,9 +1311,9 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
           f32x16 acc = zero16();
 #pragma unroll
           for (int s = 0; s < D / 16; ++s) {
-            const bf16x8 b = frag(Qs, G::ldQ, jt * 32, s * 16);
-            acc = mfma(frag(Rh, G::ld2, it * 32, s * 16), b, acc);
-            acc = mfma(frag(Rl, G::ld2, it * 32, s * 16), b, acc);
+            const bf16x8 b = frag<kO>(Qs, G::ldQ, jt * 32, s * 16);
+            acc = mfma(frag<kO>(Rh, G::ld2, it * 32, s * 16), b, acc);
+            acc = mfma(frag<kO>(Rl, G::ld2, it * 32, s * 16), b, acc);
           }
 #pragma unroll
           for (int e = 0; e < 16; ++e)     // keep j <= t
@@ -1083,7 +1323,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
           for (int e = 0; e < 16; ++e) ps += acc[e];
           ps += __shfl_xor(ps, 32);
           if (lg == 0) denp[it * C + jt * 32 + lr] = ps;
-          store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);
+          store_T<kO>(acc, Th, Tl, G::ldT, it * 32, jt * 32);
         } else if (lg == 0) {
           denp[it * C + jt * 32 + lr] = 0.f;
         }
@@ -1097,83 +1337,63 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         frag_from_acc(P0[j >> 1], j & 1, bh_, bl_);
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-          const bf16x8 aQ = frag_acc_order(Qs, G::ldQ, rt * 32, r0 + j * 16);
+          const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, r0 + j * 16);
           oacc[rt] = mfma(aQ, bh_, oacc[rt]);
           oacc[rt] = mfma(aQ, bl_, oacc[rt]);
         }
       }
     }
-    // ---- stage 5: Phi0 += R^T V (and, for summaries, C += Q^T V) on this wave's rows ----
+    // ---- stage 5: Phi0 += R^T V on this wave's rows ----
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
+      const bf16x8 bV = frag<kO>(Vt, G::ldVt, ct * 32, s * 16);
 #pragma unroll
       for (int i = 0; i < G::HT; ++i) {
-        P0[i] = mfma(frag(Wh, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
-        P0[i] = mfma(frag(Wl, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
-        if (SUMMARY) Cs[SUMMARY ? i : 0] = mfma(frag(Qt, G::ldQt, r0 + i * 32, s * 16), bV, Cs[SUMMARY ? i : 0]);
+        P0[i] = mfma(frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
+        P0[i] = mfma(frag<kO>(Wl, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
       }
     }
     if (!SUMMARY) {
       __syncthreads();                    // T and denp visible; R and R^T are dead
-      xch_put(XO, ct * 2 + (1 - h), h == 0 ? oacc[1] : oacc[0]);
-      // den_t = sum_j T[t][j] + q_t . eta0 (8 or 4 threads per token, 16 dims each)
+      xch_put<kO>(XO, ct * 2 + (1 - h), h == 0 ? oacc[1] : oacc[0]);
+      // den_t = sum_j T[t][j] + q_t . eta0: the row sums here, and eta0 of this
+      // tile (before its advance) for k_fix, which adds q_t . (eta0 + eta_c)
       if (normalized) {
-        constexpr int TPR = NT / C;
-        const int t = tid / TPR, a0 = (tid % TPR) * 16;
-        const uint16_t* row = Qs + t * G::ldQ + a0;
-        float sd = 0.f;
-#pragma unroll
-        for (int a8 = 0; a8 < 16; a8 += 8) {
-          const uint4 u = *reinterpret_cast<const uint4*>(row + a8);
-          const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) sd += bf16_to_f(e8[j]) * eta[a0 + a8 + j];
-        }
-#pragma unroll
-        for (int o = 1; o < TPR; o <<= 1) sd += __shfl_xor(sd, o);
-        if (tid % TPR == 0) den[t] = 1.f / (sd + denp[t] + denp[C + t] + eps);
+        if (tid < C && t0 + tid < n) den_out[(size_t)bh * n + t0 + tid] = denp[tid] + denp[C + tid];
+        if (tid < D) den_out[(size_t)gridDim.y * n + ((size_t)bh * ((n + C - 1) / C) + c) * D + tid] = eta[tid];
       }
       __syncthreads();
       f32x16 o = h == 0 ? oacc[0] : oacc[1];
-      xch_add(XO, ct * 2 + h, o);
+      xch_add<kO>(XO, ct * 2 + h, o);
       // ---- stage 4b: O (row tile h) += T V ----
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
         if (h == 0 && s >= 2) break;      // j past row tile 0: T is zero
-        const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
-        o = mfma(frag(Th, G::ldT, h * 32, s * 16), bV, o);
-        o = mfma(frag(Tl, G::ldT, h * 32, s * 16), bV, o);
+        const bf16x8 bV = frag<kO>(Vt, G::ldVt, ct * 32, s * 16);
+        o = mfma(frag<kO>(Th, G::ldT, h * 32, s * 16), bV, o);
+        o = mfma(frag<kO>(Tl, G::ldT, h * 32, s * 16), bV, o);
       }
 #pragma unroll
       for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer and are dropped
         const int t = h * 32 + acc_row(e, lg);
-        float y = o[e];
-        if (normalized) y *= den[t];
-        buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, y);
+        buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, o[e]);
       }
     }
     __syncthreads();   // LDS tiles and den/eta are rewritten by the next chunk
     if (tid < D) eta[tid] += eta_add;
   }
 
-  if (SUMMARY) {
-    // record (S, C, m, Phi, eta): Phi in the G slot, eta in the h slot
+  // the segment's bracket: Phi0 into the G slot, eta0 into the h slot.  The
+  // opaque copy of the lane index keeps the store addresses from being
+  // computed before the walk (they would stay live through it).
+  int col = ct * 32 + lr;
+  asm volatile("" : "+v"(col));
 #pragma unroll
-    for (int i = 0; i < G::HT; ++i)
+  for (int i = 0; i < G::HT; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = r0 + i * 32 + acc_row(e, lg);
-        rc[(size_t)row * D + ct * 32 + lr] = S0[i][e];
-        rc[off_G(D, DV) + (size_t)row * DV + ct * 32 + lr] = P0[i][e];
-        rc[off_C(D, DV) + (size_t)row * DV + ct * 32 + lr] = Cs[SUMMARY ? i : 0][e];
-      }
-    __syncthreads();
-    if (tid < D) {
-      rc[off_m(D, DV) + tid] = m_acc;
-      rc[off_h(D, DV) + tid] = eta[tid];
-    }
-  }
+    for (int e = 0; e < 16; ++e)
+      rc[off_G(D, DV) + (size_t)(r0 + i * 32 + acc_row(e, lg)) * DV + col] = P0[i][e];
+  if (tid < D) rc[off_h(D, DV) + tid] = eta[tid];
 }
 
 struct Shape {
@@ -1220,59 +1440,78 @@ WalkK walk_kernel() {
 }
 
 hipError_t launch_walk(const WalkK& kk, dim3 grid, hipStream_t s, const uint16_t* q, const uint16_t* k,
-                       const uint16_t* v, float* out, float* rec, const float* init, int n, int cps, int nseg,
-                       int normalized, float eps) {
+                       const uint16_t* v, float* out, float* den_out, float* rec, const float* init, int n, int cps,
+                       int nseg, int normalized, float eps) {
   hipError_t e = hipFuncSetAttribute(kk.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kk.lds);
   if (e != hipSuccess) return e;
-  void* args[] = {&q, &k, &v, &out, &rec, &init, &n, &cps, &nseg, &normalized, &eps};
+  void* args[] = {&q, &k, &v, &out, &den_out, &rec, &init, &n, &cps, &nseg, &normalized, &eps};
   return hipLaunchKernel(kk.fn, grid, dim3(kk.threads), args, kk.lds, s);
+}
+
+size_t records_bytes(int BH, int P, int d, int dv) {
+  return (sizeof(float) * (size_t)BH * (P + 1) * state_floats(d, dv) + 255) & ~size_t(255);
 }
 
 template <int C, int D, int DV, bool RS>
 hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* ws, int P, int cps,
                      hipStream_t s) {
   const int BH = f.BH;
-  float* segs = reinterpret_cast<float*>(ws);                    // [BH][P + 1][F] segment records
+  float* segs = reinterpret_cast<float*>(ws);                                  // [BH][P + 1][F] records
+  float* den = reinterpret_cast<float*>(ws + records_bytes(BH, P, D, DV));    // [BH][n] walk denominators
   const uint16_t* q = static_cast<const uint16_t*>(f.q);
   const uint16_t* k = static_cast<const uint16_t*>(f.k);
   const uint16_t* v = static_cast<const uint16_t*>(f.v);
-  const int nsum = final_state ? P : P - 1;                      // segments whose summary is needed
-  const int ncross = nsum + (init ? 1 : 0);                      // + conversion of the initial state
+  const dim3 grid(P, BH);
   hipError_t e;
-  if (nsum > 0) {
-    prof_start("walk_summary", s);
-    e = launch_walk(walk_kernel<C, D, DV, true, RS>(), dim3(nsum, BH), s, q, k, v, nullptr, segs, nullptr, f.n,
-                    cps, P, 0, 0.f);
-    prof_stop(s);
-    if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
-  }
-  if (ncross > 0) {
+  if (init) {      // slot P <- the initial state in the (S, C, m, Phi, eta) form
     size_t lds;
     if ((e = set_cross_lds<D, DV>((const void*)k_seg_cross<D, DV>, &lds)) != hipSuccess) return e;
-    prof_start("seg_cross", s);
-    hipLaunchKernelGGL((k_seg_cross<D, DV>), dim3(ncross, BH), dim3(256), lds, s, segs, init, P, nsum);
+    prof_start("init_convert", s);
+    hipLaunchKernelGGL((k_seg_cross<D, DV>), dim3(1, BH), dim3(256), lds, s, segs, init, P, 0);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  prof_start("moments", s);
+  hipLaunchKernelGGL((k_moments<C, D, DV>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P,
+                     final_state ? 1 : 0);
+  prof_stop(s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  prof_start(f.out ? "walk" : "walk_summary", s);
+  e = f.out ? launch_walk(walk_kernel<C, D, DV, false, RS>(), grid, s, q, k, v, f.out, den, segs, init, f.n, cps, P,
+                          f.normalized, f.eps)
+            : launch_walk(walk_kernel<C, D, DV, true, RS>(), grid, s, q, k, v, nullptr, nullptr, segs, init, f.n,
+                          cps, P, 0, 0.f);
+  prof_stop(s);
+  if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
   if (final_state) {
     size_t lds;
     if ((e = set_cross_lds<D, DV>((const void*)k_total<D, DV>, &lds)) != hipSuccess) return e;
     prof_start("total", s);
-    hipLaunchKernelGGL((k_total<D, DV>), dim3(BH), dim3(256), lds, s, segs, init, final_state, P, nsum);
+    hipLaunchKernelGGL((k_total<D, DV>), dim3(BH), dim3(256), lds, s, segs, init, final_state, P, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (!f.out) return hipSuccess;
-  prof_start("walk", s);
-  e = launch_walk(walk_kernel<C, D, DV, false, RS>(), dim3(P, BH), s, q, k, v, f.out, segs, init, f.n, cps, P,
-                  f.normalized, f.eps);
-  prof_stop(s);
-  if (e != hipSuccess) return e;
-  return hipGetLastError();
+  if (f.out && (P > 1 || init || f.normalized)) {
+    float* carry = den + (((size_t)BH * f.n + (size_t)BH * ((f.n + C - 1) / C) * D + 63) & ~size_t(63));
+    prof_start("carry", s);
+    hipLaunchKernelGGL((k_carry<D, DV>), dim3((D * DV + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    constexpr size_t lds = fix_lds_bytes<C, D, DV>();
+    static_assert(lds <= 64 * 1024, "fix LDS");
+    if ((e = hipFuncSetAttribute((const void*)k_fix<C, D, DV>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
+        hipSuccess)
+      return e;
+    const int M = (f.n + C - 1) / C;
+    prof_start("fix", s);
+    hipLaunchKernelGGL((k_fix<C, D, DV>), dim3((M + kFixTiles - 1) / kFixTiles, DV / fix_cols<DV>(), BH),
+                       dim3(kThreads), lds, s, q, f.out, den, carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
-// Segments per head: enough output-walk workgroups to fill every CU
-// (HLA_FUSED_SEGMENTS overrides), each segment a whole number of tiles.
 // (64, 64, 64) and (64, 128, 128) walk in the row-split layout; the other
 // shapes in the column layout.
 bool row_split_shape(const Shape& sh) { return sh.C == 64 && sh.D == sh.DV && (sh.D == 64 || sh.D == 128); }
@@ -1305,7 +1544,9 @@ size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
   if (!sh) return 0;
   int P, cps;
   fused_plan(*sh, BH, n, &P, &cps);
-  return sizeof(float) * (size_t)BH * (P + 1) * state_floats(d, dv) + 256;
+  const size_t den = sizeof(float) * (((size_t)BH * n + (size_t)BH * ((n + sh->C - 1) / sh->C) * d + 63) & ~size_t(63));
+  const size_t carry = sizeof(float) * (size_t)BH * P * ((size_t)d * dv + d);
+  return records_bytes(BH, P, d, dv) + den + carry + 256;
 }
 
 hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, void* workspace, hipStream_t s) {
