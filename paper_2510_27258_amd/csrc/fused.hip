@@ -586,141 +586,164 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
 // sum of the converted initial state and the brackets of the segments before
 // this one (the Phi form of Eq. (semidirect)).
 //
-// k_carry: (Phi_c, eta_c) of every segment, as running sums over the records
-// (fp32, the G|h layout: Phi_c [D][DV] then eta_c [D]).  grid
-// (ceil((D*DV + D) / 256), BH); element-parallel and coalesced.
+// k_carry: (Phi_c, eta_c) of every segment, as running sums over the records.
+// Per segment, NC floats: Phi_c split into bf16 hi and lo in the B-fragment
+// order of k_fix (piece p = (ct * D/16 + s) * 64 + lane holds the 8 values
+// Phi_c[16s + 8(lane/32) + j][32ct + lane%32], j = 0..7: D*DV/8 pieces of
+// 16 bytes, all hi pieces then all lo pieces), then eta_c in fp32 [D].
+// grid (ceil((D*DV/8 + D) / 256), BH); reads and writes coalesced.
 template <int D, int DV>
 __global__ __launch_bounds__(256) void k_carry(const float* __restrict__ rec, const float* __restrict__ init,
                                                float* __restrict__ carry, int nseg) {
-  constexpr int NC = D * DV + D;
-  const int bh = blockIdx.y, e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= NC) return;
+  constexpr int NC = D * DV + D, NP = D * DV / 8, KD = D / 16;
+  const int bh = blockIdx.y, p = blockIdx.x * 256 + threadIdx.x;
+  if (p >= NP + D) return;
   const size_t F = state_floats(D, DV);
-  const float* base = rec + (size_t)bh * (nseg + 1) * F + off_G(D, DV) + e;   // G and h slots are adjacent
-  float x = init ? base[(size_t)nseg * F] : 0.f;
+  const float* base = rec + (size_t)bh * (nseg + 1) * F;
+  if (p >= NP) {                     // eta_c[a]
+    const int a = p - NP;
+    const float* src = base + off_h(D, DV) + a;
+    float x = init ? src[(size_t)nseg * F] : 0.f;
+    for (int sp = 0; sp < nseg; ++sp) {
+      carry[((size_t)bh * nseg + sp) * NC + D * DV + a] = x;
+      x += src[(size_t)sp * F];
+    }
+    return;
+  }
+  const int ct = p / (KD * 64), s = (p / 64) % KD, lane = p % 64;
+  const float* src = base + off_G(D, DV) + (size_t)(16 * s + 8 * (lane >> 5)) * DV + 32 * ct + (lane & 31);
+  float x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = init ? src[(size_t)nseg * F + j * DV] : 0.f;
   for (int sp = 0; sp < nseg; ++sp) {
-    carry[((size_t)bh * nseg + sp) * NC + e] = x;
-    x += base[(size_t)sp * F];
+    uint16_t h8[8], o8[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) split(x[j], h8[j], o8[j]);
+    uint4* dst = reinterpret_cast<uint4*>(carry + ((size_t)bh * nseg + sp) * NC);
+    dst[p] = make_uint4(pack2(h8[0], h8[1]), pack2(h8[2], h8[3]), pack2(h8[4], h8[5]), pack2(h8[6], h8[7]));
+    dst[NP + p] = make_uint4(pack2(o8[0], o8[1]), pack2(o8[2], o8[3]), pack2(o8[4], o8[5]), pack2(o8[6], o8[7]));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] += src[(size_t)sp * F + j * DV];
   }
 }
 
-// k_fix: one workgroup per (kFixTiles consecutive tiles, block of up to 64
-// value columns, head), 4 waves: out_t += q_t^T Phi_c on MFMA (q exact in
-// bf16, Phi_c split hi/lo while staged), then out_t /= (den_t + q_t . eta_c +
-// eps) when normalised.  Tiles of segment 0 have nothing to add unless there
-// is an initial state or a division.
-constexpr int kFixTiles = 4;
-
-template <int DV>
-constexpr int fix_cols() { return DV < 64 ? DV : 64; }
+// k_fix: one workgroup per (tpw consecutive tiles, head), one wave per (row
+// tile, value column tile): out_t += q_t^T Phi_c on MFMA, then out_t /= den_t
+// + eps when normalised, with den_t = (row sum of the walk) + q_t . (eta0 of
+// the tile + eta_c).  A wave keeps the B fragments of its column of Phi_c
+// (split hi/lo) in registers, reloaded when a tile starts a new segment; q is
+// exact in bf16 and goes through LDS, the next tile's q and this tile's
+// earlier outputs in flight during the products.  Tiles of segment 0 have
+// nothing to add unless there is an initial state or a division.
+template <int C, int D, int DV>
+struct FixCfg {
+  static constexpr int VT = DV / 32, RT = C / 32, NT = 64 * VT * RT, KD = D / 16, ldQ = D + kPad;
+  static constexpr int QE = C * D / 8, QV = (QE + NT - 1) / NT;       // 16-byte pieces of a q tile
+  static constexpr size_t lds = 2 * (size_t)C * ldQ + 4 * ((size_t)D + C);
+  static_assert(NT >= D && NT <= 1024, "fix workgroup");
+};
 
 template <int C, int D, int DV>
-constexpr size_t fix_lds_bytes() {
-  return 2 * ((size_t)C * (D + kPad) + 2 * (size_t)fix_cols<DV>() * (D + kPad)) + 4 * (2 * (size_t)D + C);
-}
-
-template <int C, int D, int DV>
-__global__ __launch_bounds__(kThreads) void k_fix(const uint16_t* __restrict__ q, float* __restrict__ out,
-                                                  const float* __restrict__ den_in, const float* __restrict__ carry,
-                                                  int has_init, int n, int cps, int nseg, int normalized, float eps) {
-  constexpr int XC = fix_cols<DV>(), ldQ = D + kPad, ldX = D + kPad, RT = C / 32, VT = XC / 32, KD = D / 16;
-  constexpr int NTI = RT * VT, nT = (NTI + kWaves - 1) / kWaves, NC = D * DV + D;
-  extern __shared__ __align__(16) uint16_t lds[];   // Q | Phi_c^T hi | Phi_c^T lo (XC columns), fp32 eta_c, eta, 1/den
+__global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
+    const uint16_t* __restrict__ q, float* __restrict__ out, const float* __restrict__ den_in,
+    const float* __restrict__ carry, int has_init, int n, int cps, int nseg, int normalized, float eps, int tpw) {
+  using F = FixCfg<C, D, DV>;
+  constexpr int NT = F::NT, KD = F::KD, ldQ = F::ldQ, QE = F::QE, QV = F::QV, NC = D * DV + D;
+  extern __shared__ __align__(16) uint16_t lds[];      // q tile | fp32 eta | 1/den
   uint16_t* Qs = lds;
-  uint16_t* Xh = Qs + C * ldQ;
-  uint16_t* Xl = Xh + XC * ldX;
-  float* ec = reinterpret_cast<float*>(Xl + XC * ldX);
-  float* es = ec + D;
+  float* es = reinterpret_cast<float*>(Qs + C * ldQ);
   float* inv = es + D;
-  const int bh = blockIdx.z, col0 = blockIdx.y * XC, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int bh = blockIdx.y, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), ct = w % F::VT, rt = w / F::VT;
   const int M = (n + C - 1) / C;
-  const int c0 = blockIdx.x * kFixTiles, c1 = min(M, c0 + kFixTiles);
+  int c0 = blockIdx.x * tpw;
+  const int c1 = min(M, c0 + tpw);
+  if (!has_init && !normalized) c0 = max(c0, cps);
+  if (c0 >= c1) return;
   const rsrc_t rq = make_rsrc(q + (size_t)bh * n * D, (uint32_t)n * D * 2);
   const rsrc_t ro = make_rsrc(out + (size_t)bh * n * DV, (uint32_t)n * DV * 4);
+  uint4 qp[QV];
+  auto load_q = [&](int c) {          // clamped piece index: every lane loads, only owners store
+#pragma unroll
+    for (int i = 0; i < QV; ++i) {
+      const int e = min(tid + NT * i, QE - 1), t = e / (D / 8), a8 = (e % (D / 8)) * 8;
+      qp[i] = buf_load16(rq, (((uint32_t)c * C + t) * D + a8) * 2);
+    }
+  };
+  load_q(c0);
+  bf16x8 bhi[KD], blo[KD];
   int loaded = -1;
   for (int c = c0; c < c1; ++c) {
     const int seg = c / cps;
-    if (seg == 0 && !has_init && !normalized) continue;      // uniform: nothing to do for this tile
-    const uint32_t t0 = (uint32_t)c * C;
-    if (seg != loaded) {                                      // this segment's carry columns into LDS, split
-      const float* cb = carry + ((size_t)bh * nseg + seg) * NC;
-      for (int e = tid; e < D * XC; e += kThreads) {
-        const int a = e / XC, b = e % XC;
-        uint16_t hi, lo;
-        split(cb[(size_t)a * DV + col0 + b], hi, lo);
-        Xh[b * ldX + a] = hi;
-        Xl[b * ldX + a] = lo;
+    const float* cb = carry + ((size_t)bh * nseg + seg) * NC;
+    if (seg != loaded) {              // uniform: B fragments of Phi_c, column ct * 32 + lr
+      const uint4* pc = reinterpret_cast<const uint4*>(cb) + ct * KD * 64 + l;
+#pragma unroll
+      for (int s = 0; s < KD; ++s) {
+        bhi[s] = __builtin_bit_cast(bf16x8, pc[s * 64]);
+        blo[s] = __builtin_bit_cast(bf16x8, pc[D * DV / 8 + s * 64]);
       }
-      for (int a = tid; a < D; a += kThreads) ec[a] = cb[D * DV + a];
       loaded = seg;
     }
-    for (int e = tid; e < C * D / 8; e += kThreads) {
-      const int t = e / (D / 8), a8 = (e % (D / 8)) * 8;
-      *reinterpret_cast<uint4*>(Qs + t * ldQ + a8) = buf_load16(rq, ((t0 + t) * D + a8) * 2);
-    }
-    if (normalized && tid < D)      // eta of the tile start: the walk's eta0 + eta_c
-      es[tid] = ec[tid] + den_in[(size_t)gridDim.z * n + ((size_t)bh * M + c) * D + tid];
-    // this wave's earlier output values, in flight during the products
-    float prev[nT][16];
+    const uint32_t t0 = (uint32_t)c * C;
+    __syncthreads();                  // the previous tile's readers of Qs are done
 #pragma unroll
-    for (int i = 0; i < nT; ++i) {
-      const int ti = w + kWaves * i;
-      if (ti < NTI) {
-        const int rt = ti / VT, ct = ti % VT;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer: loads read 0, stores drop
-          const int t = rt * 32 + acc_row(e, lg);
-          prev[i][e] = __uint_as_float(
-              __builtin_amdgcn_raw_buffer_load_b32(ro, (int)(((t0 + t) * DV + col0 + ct * 32 + lr) * 4), 0, 0));
-        }
-      }
+    for (int i = 0; i < QV; ++i) {
+      const int e = tid + NT * i;
+      if (e < QE) *reinterpret_cast<uint4*>(Qs + (e / (D / 8)) * ldQ + (e % (D / 8)) * 8) = qp[i];
     }
+    if (normalized && tid < D)        // eta at the tile start: the walk's eta0 + eta_c
+      es[tid] = cb[D * DV + tid] + den_in[(size_t)gridDim.y * n + ((size_t)bh * M + c) * D + tid];
     __syncthreads();
-    if (normalized) {               // den_t = rowsum_t + q_t . es, TPR lanes per row
-      constexpr int TPR = kThreads / C < D / 8 ? kThreads / C : D / 8, PER = D / TPR;
-      static_assert(PER % 8 == 0 && TPR * C <= kThreads, "den lanes");
+    // rows past n fall outside the buffer: loads read 0, stores drop
+    const uint32_t ob = ((t0 + rt * 32 + 4 * lg) * DV + ct * 32 + lr) * 4;
+    float prev[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      prev[e] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(ro, (int)(ob + (8 * (e >> 2) + (e & 3)) * DV * 4), 0, 0));
+    load_q(c + 1 < c1 ? c + 1 : c);
+    if (normalized) {                 // den_t = rowsum_t + q_t . es, TPR lanes per row
+      constexpr int TPR = NT / C < D / 8 ? NT / C : D / 8, PER = D / TPR;
+      static_assert(PER % 8 == 0 && TPR * C <= NT, "den lanes");
       const int t = tid / TPR, p0 = (tid % TPR) * PER;
       const uint16_t* row = Qs + (t < C ? t : C - 1) * ldQ + p0;
-      float s = 0.f;
+      float sd = 0.f;
 #pragma unroll
       for (int a = 0; a < PER; a += 8) {
         const uint4 x = *reinterpret_cast<const uint4*>(row + a);
         const uint32_t u[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          s += __uint_as_float(u[j] << 16) * es[p0 + a + 2 * j];
-          s += __uint_as_float(u[j] & 0xffff0000u) * es[p0 + a + 2 * j + 1];
+          sd += __uint_as_float(u[j] << 16) * es[p0 + a + 2 * j];
+          sd += __uint_as_float(u[j] & 0xffff0000u) * es[p0 + a + 2 * j + 1];
         }
       }
 #pragma unroll
-      for (int o = 1; o < TPR; o <<= 1) s += __shfl_xor(s, o);
-      if (tid % TPR == 0 && t < C) inv[t] = (t0 + t < (uint32_t)n) ? 1.f / (den_in[(size_t)bh * n + t0 + t] + s + eps) : 0.f;
+      for (int o = 1; o < TPR; o <<= 1) sd += __shfl_xor(sd, o);
+      if (tid % TPR == 0 && t < C) inv[t] = (t0 + t < (uint32_t)n) ? 1.f / (den_in[(size_t)bh * n + t0 + t] + sd + eps) : 0.f;
       __syncthreads();
     }
+    f32x16 acc = zero16();
 #pragma unroll
-    for (int i = 0; i < nT; ++i) {
-      const int ti = w + kWaves * i;
-      if (ti < NTI) {
-        const int rt = ti / VT, ct = ti % VT;
-        f32x16 acc = zero16();
-#pragma unroll
-        for (int s = 0; s < KD; ++s) {
-          const bf16x8 aQ = frag(Qs, ldQ, rt * 32, s * 16);
-          acc = mfma(aQ, frag(Xh, ldX, ct * 32, s * 16), acc);
-          acc = mfma(aQ, frag(Xl, ldX, ct * 32, s * 16), acc);
-        }
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int t = rt * 32 + acc_row(e, lg);
-          float y = prev[i][e] + acc[e];
-          if (normalized) y *= inv[t];
-          buf_store4(ro, ((t0 + t) * DV + col0 + ct * 32 + lr) * 4, y);
-        }
-      }
+    for (int s = 0; s < KD; ++s) {
+      const bf16x8 aQ = frag(Qs, ldQ, rt * 32, s * 16);
+      acc = mfma(aQ, bhi[s], acc);
+      acc = mfma(aQ, blo[s], acc);
     }
-    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      float y = prev[e] + acc[e];
+      if (normalized) y *= inv[rt * 32 + acc_row(e, lg)];
+      buf_store4(ro, ob + (8 * (e >> 2) + (e & 3)) * DV * 4, y);
+    }
   }
+}
+
+// Tiles per k_fix workgroup: about 2048 workgroups over all heads, 1 to 16 tiles each.
+inline int fix_tpw(int M, int BH) {
+  const long t = (long)M * BH / 2048;
+  return t < 1 ? 1 : (t > 16 ? 16 : (int)t);
 }
 
 // One segment walk.  grid = (segments, BH), 4 waves.  Wave w owns column tile
@@ -1494,18 +1517,18 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   if (f.out && (P > 1 || init || f.normalized)) {
     float* carry = den + (((size_t)BH * f.n + (size_t)BH * ((f.n + C - 1) / C) * D + 63) & ~size_t(63));
     prof_start("carry", s);
-    hipLaunchKernelGGL((k_carry<D, DV>), dim3((D * DV + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P);
+    hipLaunchKernelGGL((k_carry<D, DV>), dim3((D * DV / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    constexpr size_t lds = fix_lds_bytes<C, D, DV>();
-    static_assert(lds <= 64 * 1024, "fix LDS");
-    if ((e = hipFuncSetAttribute((const void*)k_fix<C, D, DV>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
-        hipSuccess)
+    using FC = FixCfg<C, D, DV>;
+    static_assert(FC::lds <= 64 * 1024, "fix LDS");
+    if ((e = hipFuncSetAttribute((const void*)k_fix<C, D, DV>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)FC::lds)) != hipSuccess)
       return e;
-    const int M = (f.n + C - 1) / C;
+    const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("fix", s);
-    hipLaunchKernelGGL((k_fix<C, D, DV>), dim3((M + kFixTiles - 1) / kFixTiles, DV / fix_cols<DV>(), BH),
-                       dim3(kThreads), lds, s, q, f.out, den, carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps);
+    hipLaunchKernelGGL((k_fix<C, D, DV>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
+                       carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps, tpw);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
