@@ -230,6 +230,218 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Row-block scan for d == dv.  One workgroup per (head, block of RPB rows),
+// one wave per 16-column tile.  The product S_c C_acc of a block is
+// S_c[rows, :] (RPB x d) times C_acc (d x d) on fp32 MFMA
+// (v_mfma_f32_16x16x4_f32: lane l = 16g + n supplies A[n][k_g] and B[k_g][n]
+// and holds D[4g + i][n], i < 4).  The contraction index of step s for lane
+// group g is k = (d/4) g + s, so a lane's A values are one contiguous piece of
+// an S row and its B values a column piece of C.
+//   * every workgroup keeps all of C_acc, as B fragments in registers (wave w:
+//     columns 16w .. 16w+15); C_c is read by each row block of the head, and
+//     the blocks of one head share an XCD so the re-reads hit its L2;
+//   * G_acc and S_acc (the block's rows, wave w's columns) stay in MFMA
+//     accumulator layout; h_acc (block rows) and m_acc (LDS) belong to wave 0;
+//   * the block's S_c rows go through LDS (double-buffered, one barrier per
+//     segment), feeding the A operand and the S_acc update;
+//   * loads run PF segments ahead in NSLOT = PF + 1 register slots, every lane
+//     loading unconditionally so the wait counts stay partial.
+// Each block writes its rows of S, G, h, a quarter of the rows of C (rows
+// (d/4) g + s with s / SB == rb), and block 0 writes m.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Buffer resource over one record; loads and stores then take a 32-bit lane
+// offset plus a uniform offset, which keeps per-load addresses out of VGPRs.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rec_rsrc(const float* p, uint32_t floats) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, (int)(floats * 4), 0x00020000);
+}
+__device__ __forceinline__ float rld(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)(vf * 4), (int)(sf * 4), 0));
+}
+__device__ __forceinline__ f32x4_t rld4(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf) {
+  return __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)(vf * 4), (int)(sf * 4), 0));
+}
+__device__ __forceinline__ void rst(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf, float x) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, (int)(vf * 4), (int)(sf * 4), 0);
+}
+
+template <int d>
+struct RbCfg {
+  static constexpr int RPB = d == 128 ? 32 : 16;       // rows per workgroup
+  static constexpr int NW = d / 16, NT = 64 * NW, RT = RPB / 16, KS = d / 4, RB = d / RPB, SB = KS / RB;
+  static constexpr int ldS = d + 4;
+  static constexpr int NM = (d + 63) / 64;               // m values per lane
+  static constexpr int NSLOT = d == 128 ? 2 : 5;
+  static constexpr int PF = NSLOT - 1;
+  static constexpr size_t lds_floats = 2 * (size_t)RPB * ldS + d;
+  static_assert(RPB * d / 4 == NT * RT && SB * RB == KS && KS % 4 == 0, "row-block geometry");
+};
+
+template <int d>
+__global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restrict__ states,
+                                                             const float* __restrict__ init,
+                                                             float* __restrict__ prefix, float* __restrict__ total,
+                                                             int BH, int M, size_t in_stride, size_t pre_stride,
+                                                             size_t tot_stride) {
+  using K = RbCfg<d>;
+  constexpr int RT = K::RT, KS = K::KS, NT = K::NT, ldS = K::ldS, NSLOT = K::NSLOT, PF = K::PF, NM = K::NM;
+  constexpr size_t F = (size_t)d * d + 2 * (size_t)d * d + 2 * d;
+  constexpr size_t oC = (size_t)d * d, om = 2 * (size_t)d * d, oG = 2 * (size_t)d * d + d,
+                   oh = 3 * (size_t)d * d + d;
+  extern __shared__ float smem[];
+  float* Sbuf = smem;                       // [2][RPB][ldS]  the block's S_c rows
+  float* macc = smem + 2 * K::RPB * ldS;    // [d]            m_acc (wave 0)
+  const int tid = threadIdx.x, l = tid & 63, g = l >> 4, n = l & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int L = blockIdx.x, group = L / (8 * K::RB), within = L % (8 * K::RB);
+  const int bh = group * 8 + within % 8;    // a head's row blocks share an XCD (and its L2)
+  const int rb = within / 8;
+  if (bh >= BH) return;
+  const int r0 = rb * K::RPB, col = 16 * w + n;
+  const float* in = states + (size_t)bh * in_stride;
+  float* pre = prefix + (size_t)bh * pre_stride;
+  const float* ini = init ? init + (size_t)bh * F : nullptr;
+
+  // carried state
+  float cacc[KS], sacc[RT][4], hacc[RT];
+  f32x4_t gacc[RT];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) cacc[s] = ini ? ini[oC + (size_t)(KS * g + s) * d + col] : 0.f;
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const size_t row = r0 + 16 * t + 4 * g + i;
+      sacc[t][i] = ini ? ini[row * d + col] : 0.f;
+      gacc[t][i] = ini ? ini[oG + row * d + col] : 0.f;
+    }
+    hacc[t] = ini ? ini[oh + r0 + 16 * t + n] : 0.f;
+  }
+  if (w == 0)
+    for (int a = l; a < d; a += 64) macc[a] = ini ? ini[om + a] : 0.f;
+
+  // segment data in register slots
+  f32x4_t sp[NSLOT][RT];
+  float cc[NSLOT][KS], gc[NSLOT][RT][4], hc[NSLOT][RT], mc[NSLOT][NM];
+  auto load = [&](int c, auto slot_tag) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_tag)::value;
+    const auto x = rec_rsrc(in + (size_t)min(c, M - 1) * F, (uint32_t)F);
+#pragma unroll
+    for (int j = 0; j < RT; ++j) {
+      const int e = tid + NT * j, row = e / (d / 4), c4 = (e % (d / 4)) * 4;
+      sp[sl][j] = rld4(x, (r0 + row) * d + c4, 0);
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s) cc[sl][s] = rld(x, KS * g * d + col, oC + s * d);
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gc[sl][t][i] = rld(x, (r0 + 4 * g) * d + col, oG + (16 * t + i) * d);
+      hc[sl][t] = rld(x, r0 + n, oh + 16 * t);
+    }
+#pragma unroll
+    for (int j = 0; j < NM; ++j) mc[sl][j] = rld(x, min(l + 64 * j, d - 1), om);
+  };
+  // the exclusive prefix held now, into record dst
+  auto put = [&](float* dst) __attribute__((always_inline)) {
+    const auto y = rec_rsrc(dst, (uint32_t)F);
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        rst(y, (r0 + 4 * g) * d + col, (16 * t + i) * d, sacc[t][i]);
+        rst(y, (r0 + 4 * g) * d + col, oG + (16 * t + i) * d, gacc[t][i]);
+      }
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      if (s / K::SB == rb) rst(y, KS * g * d + col, oC + s * d, cacc[s]);
+    if (w == 0) {
+      if (g == 0)
+#pragma unroll
+        for (int t = 0; t < RT; ++t) rst(y, r0 + n, oh + 16 * t, hacc[t]);
+      if (rb == 0)
+        for (int a = l; a < d; a += 64) rst(y, a, om, macc[a]);
+    }
+  };
+  // segment c from slot sl: write its prefix, then fold it in
+  auto step = [&](int c, auto slot_tag) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_tag)::value;
+    load(c + PF, std::integral_constant<int, (sl + PF) % NSLOT>());
+    float* Sc = Sbuf + (c & 1) * K::RPB * ldS;
+#pragma unroll
+    for (int j = 0; j < RT; ++j) {
+      const int e = tid + NT * j, row = e / (d / 4), c4 = (e % (d / 4)) * 4;
+      *reinterpret_cast<f32x4_t*>(Sc + row * ldS + c4) = sp[sl][j];
+    }
+    put(pre + (size_t)c * F);
+    __syncthreads();
+    // G_acc += G_c + S_c[rows] C_acc (old C_acc)
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+      f32x4_t acc = gacc[t];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] += gc[sl][t][i];
+      const float* arow = Sc + (16 * t + n) * ldS + KS * g;
+#pragma unroll
+      for (int s4 = 0; s4 < KS; s4 += 4) {
+        const f32x4_t a4 = *reinterpret_cast<const f32x4_t*>(arow + s4);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, cacc[s4], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, cacc[s4 + 1], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, cacc[s4 + 2], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, cacc[s4 + 3], acc, 0, 0, 0);
+      }
+      gacc[t] = acc;
+    }
+    // h_acc += h_c + S_c[rows] m_acc (old m_acc), then m_acc += m_c: wave 0
+    if (w == 0) {
+#pragma unroll
+      for (int t = 0; t < RT; ++t) {
+        const float* arow = Sc + (16 * t + n) * ldS + KS * g;
+        float e = 0.f;
+#pragma unroll
+        for (int s4 = 0; s4 < KS; s4 += 4) {
+          const f32x4_t a4 = *reinterpret_cast<const f32x4_t*>(arow + s4);
+          const f32x4_t m4 = *reinterpret_cast<const f32x4_t*>(macc + KS * g + s4);
+          e += a4.x * m4.x + a4.y * m4.y + a4.z * m4.z + a4.w * m4.w;
+        }
+        e += __shfl_xor(e, 16);
+        e += __shfl_xor(e, 32);
+        hacc[t] += hc[sl][t] + e;
+      }
+#pragma unroll
+      for (int j = 0; j < NM; ++j)
+        if (l + 64 * j < d) macc[l + 64 * j] += mc[sl][j];
+    }
+    // S_acc += S_c, C_acc += C_c
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sacc[t][i] += Sc[(16 * t + 4 * g + i) * ldS + col];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) cacc[s] += cc[sl][s];
+  };
+  if (M > 0) {
+    load(0, std::integral_constant<int, 0>());
+    if constexpr (PF > 1) load(1, std::integral_constant<int, 1>());
+    if constexpr (PF > 2) load(2, std::integral_constant<int, 2>());
+    if constexpr (PF > 3) load(3, std::integral_constant<int, 3>());
+    static_assert(PF <= 4, "initial loads");
+    for (int c = 0; c < M; c += NSLOT) {
+      step(c, std::integral_constant<int, 0>());
+      if (c + 1 < M) step(c + 1, std::integral_constant<int, 1 % NSLOT>());
+      if constexpr (NSLOT > 2)
+        if (c + 2 < M) step(c + 2, std::integral_constant<int, 2 % NSLOT>());
+      if constexpr (NSLOT > 3)
+        if (c + 3 < M) step(c + 3, std::integral_constant<int, 3 % NSLOT>());
+      if constexpr (NSLOT > 4)
+        if (c + 4 < M) step(c + 4, std::integral_constant<int, 4 % NSLOT>());
+      static_assert(NSLOT <= 5, "unrolled steps");
+    }
+  }
+  if (total) put(total + (size_t)bh * tot_stride);
+}
+
 hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
                        int BH, int M, int d, int dv, hipStream_t s) {
   const size_t F = state_floats(d, dv);
@@ -239,9 +451,30 @@ hipError_t launch_scan(const float* states, const float* init, float* prefix, fl
 hipError_t launch_scan_strided(const float* states, const float* init, float* prefix, float* total, int BH, int M,
                                int d, int dv, size_t in_stride, size_t pre_stride, size_t tot_stride,
                                hipStream_t s) {
+  const int groups = (BH + 7) / 8;
+  if (d == dv) {
+    const void* kern = nullptr;
+    size_t lds = 0;
+    int nt = 0, rbn = 0;
+#define HLA_SCAN_RB(D_)                                      \
+  if (d == D_) {                                             \
+    kern = (const void*)k_scan_rb<D_>;                       \
+    lds = RbCfg<D_>::lds_floats * sizeof(float);             \
+    nt = RbCfg<D_>::NT;                                      \
+    rbn = RbCfg<D_>::RB;                                     \
+  }
+    HLA_SCAN_RB(16) HLA_SCAN_RB(32) HLA_SCAN_RB(64) HLA_SCAN_RB(128)
+#undef HLA_SCAN_RB
+    if (!kern) return hipErrorInvalidValue;
+    hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    void* args[] = {&states, &init, &prefix, &total, &BH, &M, &in_stride, &pre_stride, &tot_stride};
+    e = hipLaunchKernel(kern, dim3(groups * 8 * rbn), dim3(nt), args, lds, s);
+    if (e != hipSuccess) return e;
+    return hipGetLastError();
+  }
   const int cb = scan_cols(d);
   const int nblk = (dv + cb - 1) / cb;
-  const int groups = (BH + 7) / 8;
   const void* kern = nullptr;
   size_t lds = 0;
 #define HLA_SCAN_CASE(D_, B_)                                 \

@@ -231,6 +231,37 @@ def test_chunk_summaries_and_scan(dist):
         assert np.abs(got - exp).max() <= 1e-5 * max(np.abs(exp).max(), 1.0)
 
 
+@pytest.mark.parametrize("d", [16, 32, 64, 128])
+@pytest.mark.parametrize("with_init", [False, True])
+def test_scan_square_states(d, with_init):
+    """The d == dv scan (row blocks on fp32 MFMA) against sequential (+) in
+    fp64 over random records: segment counts around its prefetch depth and
+    unroll, three heads (a partial group of eight), with and without an
+    initial state.  Random S is not symmetric, so S_c C_acc must use S_c's
+    rows as stored."""
+    rng = np.random.default_rng(d + 7 * with_init)
+    B, H = 1, 3
+    F = d * d + 2 * d * d + 2 * d
+    for M in (1, 2, 3, 6, 7, 12):
+        _say(f"case scan d={d} M={M} init={with_init}")
+        x = rng.standard_normal((B, H, M, F)).astype(np.float32)
+        init = rng.standard_normal((B, H, F)).astype(np.float32) if with_init else None
+        prefix, total = hla.scan(torch.from_numpy(x).cuda(), d, d,
+                                 init=torch.from_numpy(init).cuda() if with_init else None)
+        parts = [(0, d * d, (d, d)), (d * d, d * d, (d, d)), (2 * d * d, d, (d,)), (2 * d * d + d, d * d, (d, d)),
+                 (3 * d * d + d, d, (d,))]
+        split = lambda r: tuple(r[..., o:o + c].reshape(r.shape[:-1] + sh).astype(np.float64) for o, c, sh in parts)
+        acc = split(init) if with_init else tuple(np.zeros((B, H) + sh) for _, _, sh in parts)
+        got_pre, got_tot = prefix.cpu().numpy(), total.cpu().numpy()
+        for c in range(M + 1):
+            got = split(got_pre[:, :, c]) if c < M else split(got_tot)
+            for name, gv, ev in zip("SCmGh", got, acc):
+                err = np.abs(gv - ev).max() / max(np.abs(ev).max(), 1.0)
+                assert err <= 1e-5, f"M={M} segment {c} {name}: {err:.3e}"
+            if c < M:
+                acc = O.combine(acc, split(x[:, :, c]))
+
+
 # ----------------------------------------------------------------- prefill and decode
 def _state_to_np(state, d, dv):
     return tuple(x.cpu().numpy().astype(np.float64) for x in hla.split_state(state, d, dv))
