@@ -232,23 +232,28 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
 
 // ---------------------------------------------------------------------------
 // Row-block scan for d == dv.  One workgroup per (head, block of RPB rows),
-// one wave per 16-column tile.  The product S_c C_acc of a block is
-// S_c[rows, :] (RPB x d) times C_acc (d x d) on fp32 MFMA
+// one wave per 16-column tile.  The product of a block is computed transposed,
+// G_acc[rows]^T += C_acc^T S_c[rows]^T, on fp32 MFMA
 // (v_mfma_f32_16x16x4_f32: lane l = 16g + n supplies A[n][k_g] and B[k_g][n]
-// and holds D[4g + i][n], i < 4).  The contraction index of step s for lane
-// group g is k = (d/4) g + s, so a lane's A values are one contiguous piece of
-// an S row and its B values a column piece of C.
-//   * every workgroup keeps all of C_acc, as B fragments in registers (wave w:
-//     columns 16w .. 16w+15); C_c is read by each row block of the head, and
-//     the blocks of one head share an XCD so the re-reads hit its L2;
-//   * G_acc and S_acc (the block's rows, wave w's columns) stay in MFMA
-//     accumulator layout; h_acc (block rows) and m_acc (LDS) belong to wave 0;
-//   * the block's S_c rows go through LDS (double-buffered, one barrier per
-//     segment), feeding the A operand and the S_acc update;
-//   * loads run PF segments ahead in NSLOT = PF + 1 register slots, every lane
-//     loading unconditionally so the wait counts stay partial.
-// Each block writes its rows of S, G, h, a quarter of the rows of C (rows
-// (d/4) g + s with s / SB == rb), and block 0 writes m.
+// and holds D[4g + i][n], i < 4): A is wave w's column tile of C_acc, B the
+// block's S_c rows, so a lane holds G_acc[row n][4 adjacent columns].  The
+// contraction index of step s for lane group g is k = (d/4) g + s.
+//   * every workgroup keeps all of C_acc, as A fragments in registers (wave
+//     w: columns 16w .. 16w+15), and its own RPB rows of C_acc once more in
+//     row-major 16-byte pieces for the output; C_c is read by each row block
+//     of the head, and the blocks of one head share an XCD so the re-reads
+//     hit its L2;
+//   * G_acc and S_acc (the block's rows, wave w's columns) stay in that
+//     accumulator layout; every wave forms h_acc (block rows) from m_acc,
+//     which sits in LDS, double-buffered by segment parity;
+//   * the block's S_c rows and all of C_c go through LDS in 16-byte pieces
+//     (C with its 16-column tiles XOR-swizzled by row group, so the column
+//     reads of the four lane groups fall in different banks);
+//   * loads run PF segments ahead in NSLOT = PF + 1 register slots.  No load
+//     or store of the steady-state loop sits under a branch (lanes that own
+//     nothing store past the end of the record, which the buffer drops), so
+//     the compiler's wait counts stay partial and the prefetch stays deep.
+// Each block writes its rows of S, C, G, h, and block 0 writes m.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Buffer resource over one record; loads and stores then take a 32-bit lane
@@ -263,7 +268,11 @@ __device__ __forceinline__ f32x4_t rld4(__amdgpu_buffer_rsrc_t r, uint32_t vf, u
   return __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)(vf * 4), (int)(sf * 4), 0));
 }
 __device__ __forceinline__ void rst(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf, float x) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, (int)(vf * 4), (int)(sf * 4), 0);
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, (int)(vf * 4), (int)(sf * 4), 2);
+}
+__device__ __forceinline__ void rst4(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf, f32x4_t x) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) uint32_t, x), r,
+                                         (int)(vf * 4), (int)(sf * 4), 2);
 }
 
 template <int d>
@@ -271,12 +280,23 @@ struct RbCfg {
   static constexpr int RPB = d == 128 ? 32 : 16;       // rows per workgroup
   static constexpr int NW = d / 16, NT = 64 * NW, RT = RPB / 16, KS = d / 4, RB = d / RPB, SB = KS / RB;
   static constexpr int ldS = d + 4;
-  static constexpr int NM = (d + 63) / 64;               // m values per lane
+  static constexpr int NC4 = d / 16;                   // 16-byte pieces of C_c per thread
+  static constexpr int NCO = RPB * d / 4 / NT;         // 16-byte pieces of the block's C rows per thread
+  static constexpr int NM = (d + 63) / 64;             // m values per lane
+  static constexpr int CBUF = d == 128 ? 1 : 2;        // C_c buffers in LDS
   static constexpr int NSLOT = d == 128 ? 2 : 5;
   static constexpr int PF = NSLOT - 1;
-  static constexpr size_t lds_floats = 2 * (size_t)RPB * ldS + d;
-  static_assert(RPB * d / 4 == NT * RT && SB * RB == KS && KS % 4 == 0, "row-block geometry");
+  static constexpr size_t lds_floats = 2 * (size_t)RPB * ldS + (size_t)CBUF * d * d + 2 * d;
+  static_assert(RPB * d / 4 == NT * RT && SB * RB == KS && KS % 4 == 0 && NC4 * NT * 4 == d * d &&
+                    NCO * NT * 4 == RPB * d,
+                "row-block geometry");
 };
+
+// Column of C_c element (k, j) in LDS: 16-column tiles XOR-swizzled by the row group k / (d/4).
+template <int d>
+__device__ __forceinline__ int cswz(int k, int j) {
+  return j ^ ((((k / (d / 4)) % (d / 16))) << 4);
+}
 
 template <int d>
 __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restrict__ states,
@@ -285,45 +305,60 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
                                                              int BH, int M, size_t in_stride, size_t pre_stride,
                                                              size_t tot_stride) {
   using K = RbCfg<d>;
-  constexpr int RT = K::RT, KS = K::KS, NT = K::NT, ldS = K::ldS, NSLOT = K::NSLOT, PF = K::PF, NM = K::NM;
+  constexpr int RT = K::RT, KS = K::KS, NT = K::NT, ldS = K::ldS, NSLOT = K::NSLOT, PF = K::PF, NM = K::NM,
+                NC4 = K::NC4, NCO = K::NCO;
   constexpr size_t F = (size_t)d * d + 2 * (size_t)d * d + 2 * d;
-  constexpr size_t oC = (size_t)d * d, om = 2 * (size_t)d * d, oG = 2 * (size_t)d * d + d,
-                   oh = 3 * (size_t)d * d + d;
+  constexpr uint32_t oC = d * d, om = 2 * d * d, oG = 2 * d * d + d, oh = 3 * d * d + d;
   extern __shared__ float smem[];
-  float* Sbuf = smem;                       // [2][RPB][ldS]  the block's S_c rows
-  float* macc = smem + 2 * K::RPB * ldS;    // [d]            m_acc (wave 0)
+  float* Sbuf = smem;                                  // [2][RPB][ldS]  the block's S_c rows
+  float* Cbuf = smem + 2 * K::RPB * ldS;               // [CBUF][d][d]   C_c, swizzled
+  float* macc = Cbuf + K::CBUF * d * d;                // [2][d]         m_acc by segment parity
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, n = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = blockIdx.x, group = L / (8 * K::RB), within = L % (8 * K::RB);
-  const int bh = group * 8 + within % 8;    // a head's row blocks share an XCD (and its L2)
+  const int bh = group * 8 + within % 8;               // a head's row blocks share an XCD (and its L2)
   const int rb = within / 8;
   if (bh >= BH) return;
-  const int r0 = rb * K::RPB, col = 16 * w + n;
+  const int r0 = rb * K::RPB, c0 = 16 * w;
   const float* in = states + (size_t)bh * in_stride;
   float* pre = prefix + (size_t)bh * pre_stride;
-  const float* ini = init ? init + (size_t)bh * F : nullptr;
 
-  // carried state
-  float cacc[KS], sacc[RT][4], hacc[RT];
-  f32x4_t gacc[RT];
+  // carried state: C_acc column pieces (A fragments), S_acc / G_acc [row 16t + n][c0 + 4g + i], h_acc
+  // and the block's rows of C_acc: piece j of a thread is row r0 + e / d, columns e % d .. + 3, e = 4 (tid + NT j)
+  float cacc[KS], hacc[RT];
+  f32x4_t sacc[RT], gacc[RT], cown[NCO];
+  if (init) {
+    const auto x = rec_rsrc(init + (size_t)bh * F, (uint32_t)F);
 #pragma unroll
-  for (int s = 0; s < KS; ++s) cacc[s] = ini ? ini[oC + (size_t)(KS * g + s) * d + col] : 0.f;
+    for (int s = 0; s < KS; ++s) cacc[s] = rld(x, KS * g * d + c0 + n, oC + s * d);
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
+    for (int j = 0; j < NCO; ++j) cown[j] = rld4(x, 4 * (tid + NT * j), oC + r0 * d);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const size_t row = r0 + 16 * t + 4 * g + i;
-      sacc[t][i] = ini ? ini[row * d + col] : 0.f;
-      gacc[t][i] = ini ? ini[oG + row * d + col] : 0.f;
+    for (int t = 0; t < RT; ++t) {
+      sacc[t] = rld4(x, (r0 + n) * d + c0 + 4 * g, 16 * t * d);
+      gacc[t] = rld4(x, (r0 + n) * d + c0 + 4 * g, oG + 16 * t * d);
+      hacc[t] = rld(x, r0 + n, oh + 16 * t);
     }
-    hacc[t] = ini ? ini[oh + r0 + 16 * t + n] : 0.f;
+    if (w == 0)
+      for (int a = l; a < d; a += 64) macc[a] = rld(x, a, om);   // parity 0
+  } else {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) cacc[s] = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCO; ++j) cown[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+      sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      gacc[t] = sacc[t];
+      hacc[t] = 0.f;
+    }
+    if (w == 0)
+      for (int a = l; a < d; a += 64) macc[a] = 0.f;
   }
-  if (w == 0)
-    for (int a = l; a < d; a += 64) macc[a] = ini ? ini[om + a] : 0.f;
 
   // segment data in register slots
-  f32x4_t sp[NSLOT][RT];
-  float cc[NSLOT][KS], gc[NSLOT][RT][4], hc[NSLOT][RT], mc[NSLOT][NM];
+  f32x4_t sp[NSLOT][RT], cp[NSLOT][NC4], gc[NSLOT][RT];
+  float hc[NSLOT][RT], mc[NSLOT][NM];
   auto load = [&](int c, auto slot_tag) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot_tag)::value;
     const auto x = rec_rsrc(in + (size_t)min(c, M - 1) * F, (uint32_t)F);
@@ -333,35 +368,34 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
       sp[sl][j] = rld4(x, (r0 + row) * d + c4, 0);
     }
 #pragma unroll
-    for (int s = 0; s < KS; ++s) cc[sl][s] = rld(x, KS * g * d + col, oC + s * d);
+    for (int j = 0; j < NC4; ++j) cp[sl][j] = rld4(x, 4 * tid, oC + 4 * NT * j);
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) gc[sl][t][i] = rld(x, (r0 + 4 * g) * d + col, oG + (16 * t + i) * d);
+      gc[sl][t] = rld4(x, (r0 + n) * d + c0 + 4 * g, oG + 16 * t * d);
       hc[sl][t] = rld(x, r0 + n, oh + 16 * t);
     }
 #pragma unroll
     for (int j = 0; j < NM; ++j) mc[sl][j] = rld(x, min(l + 64 * j, d - 1), om);
   };
   // the exclusive prefix held now, into record dst
-  auto put = [&](float* dst) __attribute__((always_inline)) {
+  // the exclusive prefix held now (m_acc in buffer mb), into record dst
+  constexpr uint32_t kDrop = 0x10000000u;   // a lane offset (floats) past any record: the store is dropped
+  auto put = [&](float* dst, const float* mb) __attribute__((always_inline)) {
     const auto y = rec_rsrc(dst, (uint32_t)F);
 #pragma unroll
-    for (int t = 0; t < RT; ++t)
+    for (int t = 0; t < RT; ++t) {
+      rst4(y, (r0 + n) * d + c0 + 4 * g, 16 * t * d, sacc[t]);
+      rst4(y, (r0 + n) * d + c0 + 4 * g, oG + 16 * t * d, gacc[t]);
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        rst(y, (r0 + 4 * g) * d + col, (16 * t + i) * d, sacc[t][i]);
-        rst(y, (r0 + 4 * g) * d + col, oG + (16 * t + i) * d, gacc[t][i]);
-      }
+    for (int j = 0; j < NCO; ++j) rst4(y, 4 * (tid + NT * j), oC + r0 * d, cown[j]);
+    const bool hown = w == 0 && g == 0, mown = w == 0 && rb == 0;
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-      if (s / K::SB == rb) rst(y, KS * g * d + col, oC + s * d, cacc[s]);
-    if (w == 0) {
-      if (g == 0)
+    for (int t = 0; t < RT; ++t) rst(y, hown ? r0 + n : kDrop, oh + 16 * t, hacc[t]);
 #pragma unroll
-        for (int t = 0; t < RT; ++t) rst(y, r0 + n, oh + 16 * t, hacc[t]);
-      if (rb == 0)
-        for (int a = l; a < d; a += 64) rst(y, a, om, macc[a]);
+    for (int j = 0; j < NM; ++j) {
+      const int a = min(l + 64 * j, d - 1);
+      rst(y, mown && l + 64 * j < d ? a : kDrop, om, mb[a]);
     }
   };
   // segment c from slot sl: write its prefix, then fold it in
@@ -369,77 +403,97 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
     constexpr int sl = decltype(slot_tag)::value;
     load(c + PF, std::integral_constant<int, (sl + PF) % NSLOT>());
     float* Sc = Sbuf + (c & 1) * K::RPB * ldS;
+    float* Cc = Cbuf + (K::CBUF == 2 ? (c & 1) : 0) * d * d;
+    if (K::CBUF == 1) __syncthreads();   // the previous segment's readers of Cc are done
 #pragma unroll
     for (int j = 0; j < RT; ++j) {
       const int e = tid + NT * j, row = e / (d / 4), c4 = (e % (d / 4)) * 4;
       *reinterpret_cast<f32x4_t*>(Sc + row * ldS + c4) = sp[sl][j];
     }
-    put(pre + (size_t)c * F);
+#pragma unroll
+    for (int j = 0; j < NC4; ++j) {
+      const int e = 4 * (tid + NT * j), k = e / d;
+      *reinterpret_cast<f32x4_t*>(Cc + k * d + cswz<d>(k, e % d)) = cp[sl][j];
+    }
+    const float* mo = macc + (c & 1) * d;   // m_acc before segment c
+    put(pre + (size_t)c * F, mo);
     __syncthreads();
-    // G_acc += G_c + S_c[rows] C_acc (old C_acc)
+    // G_acc^T += G_c^T + C_acc^T S_c[rows]^T (old C_acc)
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      f32x4_t acc = gacc[t];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc[i] += gc[sl][t][i];
-      const float* arow = Sc + (16 * t + n) * ldS + KS * g;
+      f32x4_t acc = gacc[t] + gc[sl][t];
+      const float* brow = Sc + (16 * t + n) * ldS + KS * g;
 #pragma unroll
       for (int s4 = 0; s4 < KS; s4 += 4) {
-        const f32x4_t a4 = *reinterpret_cast<const f32x4_t*>(arow + s4);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.x, cacc[s4], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.y, cacc[s4 + 1], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.z, cacc[s4 + 2], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4.w, cacc[s4 + 3], acc, 0, 0, 0);
+        const f32x4_t b4 = *reinterpret_cast<const f32x4_t*>(brow + s4);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4], b4.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4 + 1], b4.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4 + 2], b4.z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4 + 3], b4.w, acc, 0, 0, 0);
       }
       gacc[t] = acc;
     }
-    // h_acc += h_c + S_c[rows] m_acc (old m_acc), then m_acc += m_c: wave 0
-    if (w == 0) {
+    // h_acc += h_c + S_c[rows] m_acc (old m_acc), in every wave; m_acc += m_c
+    // into the other parity buffer (its readers, segment c - 1, are past the barrier)
 #pragma unroll
-      for (int t = 0; t < RT; ++t) {
-        const float* arow = Sc + (16 * t + n) * ldS + KS * g;
-        float e = 0.f;
+    for (int t = 0; t < RT; ++t) {
+      const float* arow = Sc + (16 * t + n) * ldS + KS * g;
+      float e = 0.f;
 #pragma unroll
-        for (int s4 = 0; s4 < KS; s4 += 4) {
-          const f32x4_t a4 = *reinterpret_cast<const f32x4_t*>(arow + s4);
-          const f32x4_t m4 = *reinterpret_cast<const f32x4_t*>(macc + KS * g + s4);
-          e += a4.x * m4.x + a4.y * m4.y + a4.z * m4.z + a4.w * m4.w;
-        }
-        e += __shfl_xor(e, 16);
-        e += __shfl_xor(e, 32);
-        hacc[t] += hc[sl][t] + e;
+      for (int s4 = 0; s4 < KS; s4 += 4) {
+        const f32x4_t a4 = *reinterpret_cast<const f32x4_t*>(arow + s4);
+        const f32x4_t m4 = *reinterpret_cast<const f32x4_t*>(mo + KS * g + s4);
+        e += a4.x * m4.x + a4.y * m4.y + a4.z * m4.z + a4.w * m4.w;
       }
+      e += __shfl_xor(e, 16);
+      e += __shfl_xor(e, 32);
+      hacc[t] += hc[sl][t] + e;
+    }
+    if (w == 0) {
+      float* mn = macc + ((c + 1) & 1) * d;
 #pragma unroll
       for (int j = 0; j < NM; ++j)
-        if (l + 64 * j < d) macc[l + 64 * j] += mc[sl][j];
+        if (l + 64 * j < d) mn[l + 64 * j] = mo[l + 64 * j] + mc[sl][j];
     }
     // S_acc += S_c, C_acc += C_c
 #pragma unroll
-    for (int t = 0; t < RT; ++t)
+    for (int t = 0; t < RT; ++t) sacc[t] += *reinterpret_cast<const f32x4_t*>(Sc + (16 * t + n) * ldS + c0 + 4 * g);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sacc[t][i] += Sc[(16 * t + 4 * g + i) * ldS + col];
+    for (int s = 0; s < KS; ++s) {
+      const int k = KS * g + s;
+      cacc[s] += Cc[k * d + cswz<d>(k, c0 + n)];
+    }
 #pragma unroll
-    for (int s = 0; s < KS; ++s) cacc[s] += cc[sl][s];
+    for (int j = 0; j < NCO; ++j) {
+      const int e = 4 * (tid + NT * j), k = r0 + e / d;
+      cown[j] += *reinterpret_cast<const f32x4_t*>(Cc + k * d + cswz<d>(k, e % d));
+    }
   };
   if (M > 0) {
     load(0, std::integral_constant<int, 0>());
     if constexpr (PF > 1) load(1, std::integral_constant<int, 1>());
     if constexpr (PF > 2) load(2, std::integral_constant<int, 2>());
     if constexpr (PF > 3) load(3, std::integral_constant<int, 3>());
-    static_assert(PF <= 4, "initial loads");
-    for (int c = 0; c < M; c += NSLOT) {
+    static_assert(PF <= 4 && NSLOT <= 5, "unrolled slots");
+    int c = 0;
+    for (; c + NSLOT <= M; c += NSLOT) {     // whole groups: no branch around a step
       step(c, std::integral_constant<int, 0>());
-      if (c + 1 < M) step(c + 1, std::integral_constant<int, 1 % NSLOT>());
-      if constexpr (NSLOT > 2)
-        if (c + 2 < M) step(c + 2, std::integral_constant<int, 2 % NSLOT>());
-      if constexpr (NSLOT > 3)
-        if (c + 3 < M) step(c + 3, std::integral_constant<int, 3 % NSLOT>());
-      if constexpr (NSLOT > 4)
-        if (c + 4 < M) step(c + 4, std::integral_constant<int, 4 % NSLOT>());
-      static_assert(NSLOT <= 5, "unrolled steps");
+      step(c + 1, std::integral_constant<int, 1 % NSLOT>());
+      if constexpr (NSLOT > 2) step(c + 2, std::integral_constant<int, 2 % NSLOT>());
+      if constexpr (NSLOT > 3) step(c + 3, std::integral_constant<int, 3 % NSLOT>());
+      if constexpr (NSLOT > 4) step(c + 4, std::integral_constant<int, 4 % NSLOT>());
     }
+    if (c < M) step(c, std::integral_constant<int, 0>());
+    if (c + 1 < M) step(c + 1, std::integral_constant<int, 1 % NSLOT>());
+    if constexpr (NSLOT > 2)
+      if (c + 2 < M) step(c + 2, std::integral_constant<int, 2 % NSLOT>());
+    if constexpr (NSLOT > 3)
+      if (c + 3 < M) step(c + 3, std::integral_constant<int, 3 % NSLOT>());
   }
-  if (total) put(total + (size_t)bh * tot_stride);
+  if (total) {
+    __syncthreads();                          // m_acc of parity M is written by wave 0
+    put(total + (size_t)bh * tot_stride, macc + (M & 1) * d);
+  }
 }
 
 hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
