@@ -63,6 +63,8 @@ def kernel_costs(w, P=None):
             "moments": ("hbm", tok * d * es + BH * P * d * d * 4, tok * 2 * d * d),
             # carry fix-up: q read, out read and written (den read when normalised)
             "fix": ("hbm", tok * (d * es + 8 * dv + (4 if w["normalized"] else 0)), tok * 2 * d * dv),
+            # carry: the segments' Phi/eta brackets read, their running sums written
+            "carry": ("hbm", BH * (2 * P + 1) * (d * dv + d) * 4, BH * P * (d * dv + d)),
             "init_convert": ("hbm", BH * 2 * F * 4, BH * 2 * (d * d * dv + d * d)),
             "total": ("hbm", BH * (P + 2) * F * 4, BH * 2 * (d * d * dv + d * d)),
         })
@@ -122,7 +124,8 @@ def kernel_key(name):
     """Bench name of a library kernel from its (demangled) dispatch name."""
     if "k_walk" in name:
         return "walk_summary" if ("true" in name or "Lb1E" in name) else "walk"
-    for key in ("k_seg_cross", "k_total", "k_scan", "k_chunk_summary", "k_readout", "k_step"):
+    for key in ("k_seg_cross", "k_total", "k_moments", "k_carry", "k_fix", "k_scan", "k_chunk_summary", "k_readout",
+                "k_step"):
         if key in name:
             return key[2:]
     return None
