@@ -64,6 +64,17 @@ __device__ __forceinline__ void split(float x, uint16_t& hi, uint16_t& lo) {
 }
 __device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) { return a | (uint32_t)b << 16; }
 
+// The same for a pair: hi = (hi(x0), hi(x1)) and lo likewise, packed low
+// half first.  One packed conversion gives both high parts, so a pair costs
+// two conversions, two unpacks and two subtractions.
+__device__ __forceinline__ void split2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  hi = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){x0, x1}, b2));
+  const float h0 = __uint_as_float(hi << 16), h1 = __uint_as_float(hi & 0xffff0000u);
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){x0 - h0, x1 - h1}, b2));
+}
+
 // Buffer resource over [p, p + bytes): loads past the end return zero and
 // stores past the end are dropped, which zero-fills the ragged last chunk and
 // clips its outputs.  Offsets are 32-bit bytes from p.
@@ -128,11 +139,11 @@ __device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int 
 // lane's elements 8h .. 8h+7 are rows 16h + {4g..4g+3, 8+4g..8+4g+3} of its
 // column, matching frag_acc_order.  Split into hi and lo parts.
 __device__ __forceinline__ void frag_from_acc(const f32x16& t, int h, bf16x8& hi, bf16x8& lo) {
-  uint16_t a[8], b[8];
+  uint32_t a[4], b[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) split(t[8 * h + i], a[i], b[i]);
-  hi = __builtin_bit_cast(bf16x8, make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(a[4], a[5]), pack2(a[6], a[7])));
-  lo = __builtin_bit_cast(bf16x8, make_uint4(pack2(b[0], b[1]), pack2(b[2], b[3]), pack2(b[4], b[5]), pack2(b[6], b[7])));
+  for (int i = 0; i < 4; ++i) split2(t[8 * h + 2 * i], t[8 * h + 2 * i + 1], a[i], b[i]);
+  hi = __builtin_bit_cast(bf16x8, make_uint4(a[0], a[1], a[2], a[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(b[0], b[1], b[2], b[3]));
 }
 
 // Store an accumulator tile D[row0 + i][col0 + r] transposed as X[col0 + r][row0 + i],
@@ -144,11 +155,11 @@ __device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_
   const int base = (col0 + (l & 31)) * ld + row0 + 4 * g;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    uint16_t h[4], o[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) split(acc[4 * q + j], h[j], o[j]);
-    *reinterpret_cast<uint2*>(Xh + base + 8 * q) = make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
-    *reinterpret_cast<uint2*>(Xl + base + 8 * q) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+    uint32_t h[2], o[2];
+    split2(acc[4 * q], acc[4 * q + 1], h[0], o[0]);
+    split2(acc[4 * q + 2], acc[4 * q + 3], h[1], o[1]);
+    *reinterpret_cast<uint2*>(Xh + base + 8 * q) = make_uint2(h[0], h[1]);
+    *reinterpret_cast<uint2*>(Xl + base + 8 * q) = make_uint2(o[0], o[1]);
   }
 }
 
@@ -161,16 +172,17 @@ __device__ __forceinline__ void store_TN(const f32x16& acc, uint16_t* Th, uint16
   const int baseT = (col0 + (l & 31)) * ldT + row0 + 4 * g;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    uint16_t h[4], o[4];
+    uint32_t h[2], o[2];
+    split2(acc[4 * q], acc[4 * q + 1], h[0], o[0]);
+    split2(acc[4 * q + 2], acc[4 * q + 3], h[1], o[1]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      split(acc[4 * q + j], h[j], o[j]);
       const int offN = (row0 + 8 * q + 4 * g + j) * ldN + col0 + (l & 31);
-      Nh[offN] = h[j];
-      Nl[offN] = o[j];
+      Nh[offN] = (uint16_t)(h[j >> 1] >> (16 * (j & 1)));
+      Nl[offN] = (uint16_t)(o[j >> 1] >> (16 * (j & 1)));
     }
-    *reinterpret_cast<uint2*>(Th + baseT + 8 * q) = make_uint2(pack2(h[0], h[1]), pack2(h[2], h[3]));
-    *reinterpret_cast<uint2*>(Tl + baseT + 8 * q) = make_uint2(pack2(o[0], o[1]), pack2(o[2], o[3]));
+    *reinterpret_cast<uint2*>(Th + baseT + 8 * q) = make_uint2(h[0], h[1]);
+    *reinterpret_cast<uint2*>(Tl + baseT + 8 * q) = make_uint2(o[0], o[1]);
   }
 }
 
@@ -180,12 +192,15 @@ __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_
   const int l = lane64<O>();
   const int g = l >> 5;
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    uint16_t h, o;
-    split(acc[e], h, o);
-    const int off = (row0 + acc_row(e, g)) * ld + col0 + (l & 31);
-    Xh[off] = h;
-    Xl[off] = o;
+  for (int e = 0; e < 16; e += 2) {
+    uint32_t h, o;
+    split2(acc[e], acc[e + 1], h, o);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int off = (row0 + acc_row(e + j, g)) * ld + col0 + (l & 31);
+      Xh[off] = (uint16_t)(h >> (16 * j));
+      Xl[off] = (uint16_t)(o >> (16 * j));
+    }
   }
 }
 
