@@ -135,6 +135,27 @@ __device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int 
   return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
 }
 
+// Operand fragment read through the LDS transpose unit from a row-major bf16
+// tile Y[k][n]: lane takes Y[k0 + 8g .. 8g+7][n0 + r], the fragment frag()
+// would take from Y^T.  ds_read_b64_tr_b16 works in groups of 16 lanes:
+// element m of lane j's result is element j % 4 of the 8 bytes read by lane
+// 4m + j / 4 of its group.  So lane j of a group reads row k + j / 4 at
+// columns 4 (j % 4) .. + 3, and receives rows k .. k+3 of column j; two reads
+// give the 8 rows of a fragment.  (Layout checked on the device by an
+// in-bounds probe.)  Y and ld must keep 8-byte alignment (ld % 4 == 0).
+template <bool O = false>
+__device__ __forceinline__ bf16x8 frag_tr(const uint16_t* Y, int ld, int n0, int k0) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+  const int l = lane64<O>();
+  const int grp = l >> 4, j = l & 15;
+  const uint16_t* p = Y + (k0 + 8 * (grp >> 1) + (j >> 2)) * ld + n0 + 16 * (grp & 1) + 4 * (j & 3);
+  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
+  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p + 4 * ld));
+  const uint2 ua = __builtin_bit_cast(uint2, a), ub = __builtin_bit_cast(uint2, b);
+  return __builtin_bit_cast(bf16x8, make_uint4(ua.x, ua.y, ub.x, ub.y));
+}
+
 // B operand for k rows 16h .. 16h+15 of an accumulator tile Y (32 rows): the
 // lane's elements 8h .. 8h+7 are rows 16h + {4g..4g+3, 8+4g..8+4g+3} of its
 // column, matching frag_acc_order.  Split into hi and lo parts.
@@ -1110,22 +1131,23 @@ struct CfgRS {
   static constexpr int NCT = D / 32, NW = 2 * NCT, NT = 64 * NW;
   static constexpr int HT = NCT / 2, HALF = D / 2;             // 32-row state tiles per half
   static constexpr int RT = 2, KC = C / 16, KH = D / 32;        // k-steps over tokens / over a half
-  static constexpr int ldQ = D + kPad, ldK = D + kPad, ldKt = C + kPad, ldVt = C + kPad;
-  static constexpr int ld1 = C + kPad, ld2 = D + kPad, ldT = C + kPad, ldQt = C + kPad;
+  static constexpr int ldQ = D + kPad, ldK = D + kPad, ldKt = C + kPad, ldV = DV + kPad;
+  static constexpr int ld1 = C + kPad, ld2 = D + kPad, ldT = C + kPad;
   static constexpr int oQ = 0;
   static constexpr int oK = oQ + C * ldQ;
-  static constexpr int oKt = oK + C * ldK;
-  static constexpr int oVt = oKt + D * ldKt;
-  static constexpr int oB1h = oVt + DV * ldVt;                 // W, then R^T
+  static constexpr int oKt = oK + C * ldK;                     // (room for the R exchange and T)
+  static constexpr int oVt = oKt + D * ldKt;                   // V, row-major
+  static constexpr int oB1h = oVt + DV * (C + kPad);           // W, then R^T
   static constexpr int oB1l = oB1h + D * ld1;
-  static constexpr int oB2h = oB1l + D * ld1;                  // R (then the O exchange); absent in summaries
+  static constexpr int oB2h = oB1l + D * ld1;                  // the O exchange; absent in summaries
   static constexpr int oB2l = oB2h + C * ld2;
   static constexpr int n16 = SUMMARY ? oB2h : oB2l + C * ld2;
   static constexpr int oX = oK;                                // R exchange, then T (hi | lo)
   static constexpr int oTh = oK, oTl = oK + C * ldT;
   static constexpr int xfl = 2 * NCT * 1024;                   // exchange floats
   static_assert(2 * xfl <= oVt - oK && 2 * C * ldT <= oVt - oK, "exchange and T fit K | K^T");
-  static_assert(SUMMARY || 2 * xfl <= 2 * C * ld2, "O exchange fits the R buffer");
+  static_assert(SUMMARY || 2 * xfl <= 2 * C * ld2, "O exchange fits its buffer");
+  static_assert(C * ldV <= DV * (C + kPad), "V fits its buffer");
   static constexpr int f_eta = 0, f_cs = D, f_den = D + RT * D, f_denp = f_den + C;
   static constexpr int nf32 = f_denp + RT * C;
   static constexpr size_t bytes = (size_t)((n16 + 7) & ~7) * 2 + (size_t)nf32 * 4;
@@ -1166,12 +1188,9 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
   uint16_t* Ks = lds + G::oK;
-  uint16_t* Kt = lds + G::oKt;
-  uint16_t* Vt = lds + G::oVt;
+  uint16_t* Vs = lds + G::oVt;    // V row-major
   uint16_t* Wh = lds + G::oB1h;   // W, then R^T
   uint16_t* Wl = lds + G::oB1l;
-  uint16_t* Rh = lds + G::oB2h;   // R
-  uint16_t* Rl = lds + G::oB2l;
   uint16_t* Th = lds + G::oTh;
   uint16_t* Tl = lds + G::oTl;
   float* XR = reinterpret_cast<float*>(lds + G::oX);     // R exchange
@@ -1251,24 +1270,20 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 
   for (int c = c_begin; c < c_end; ++c) {
     const int t0 = c * C;
-    // ---- stage 0: registers -> LDS (Q, K row-major; K^T, V^T; Q^T for summaries) ----
+    // ---- stage 0: registers -> LDS (Q, K, V row-major; the transposed operands are read through the
+    // LDS transpose unit) ----
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + NT * i;
       const int t = e % C, a8 = (e / C) * 8;
       *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
       *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
-      const uint16_t* kk = reinterpret_cast<const uint16_t*>(&pk[i]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) Kt[(a8 + j) * G::ldKt + t] = kk[j];
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + NT * i;
       const int t = e % C, b8 = (e / C) * 8;
-      const uint16_t* vv = reinterpret_cast<const uint16_t*>(&pv[i]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) Vt[(b8 + j) * G::ldVt + t] = vv[j];
+      *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
     }
     __syncthreads();
     if (c + 1 < c_end) fetch(c + 1);
@@ -1306,7 +1321,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bK = frag<kO>(Kt, G::ldKt, ct * 32, s * 16);
+      const bf16x8 bK = frag_tr<kO>(Ks, G::ldK, ct * 32, s * 16);
       if (h == 0) {
         if (s < 2) {
           part[0] = mfma(frag<kO>(Wh, G::ld1, 0, s * 16), bK, part[0]);
@@ -1318,7 +1333,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       }
       // S0 += K^T K on this wave's rows
 #pragma unroll
-      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag<kO>(Kt, G::ldKt, r0 + i * 32, s * 16), bK, S0[i]);
+      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16), bK, S0[i]);
     }
     __syncthreads();                      // K, K^T and W are dead: K | K^T takes the exchange
     xch_put<kO>(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0]);
@@ -1332,10 +1347,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       cs += __shfl_xor(cs, 32);
       if (lg == 0) colsum[h * D + ct * 32 + lr] = cs;
     }
-    if (SUMMARY)
-      store_T<kO>(racc, Wh, Wl, G::ld1, h * 32, ct * 32);
-    else
-      store_TN<kO>(racc, Wh, Wl, G::ld1, Rh, Rl, G::ld2, h * 32, ct * 32);
+    store_T<kO>(racc, Wh, Wl, G::ld1, h * 32, ct * 32);     // R^T
     __syncthreads();
     float eta_add = 0.f;
     if (tid < D) eta_add = colsum[tid] + colsum[D + tid];
@@ -1350,8 +1362,8 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 #pragma unroll
           for (int s = 0; s < D / 16; ++s) {
             const bf16x8 b = frag<kO>(Qs, G::ldQ, jt * 32, s * 16);
-            acc = mfma(frag<kO>(Rh, G::ld2, it * 32, s * 16), b, acc);
-            acc = mfma(frag<kO>(Rl, G::ld2, it * 32, s * 16), b, acc);
+            acc = mfma(frag_tr<kO>(Wh, G::ld1, it * 32, s * 16), b, acc);
+            acc = mfma(frag_tr<kO>(Wl, G::ld1, it * 32, s * 16), b, acc);
           }
 #pragma unroll
           for (int e = 0; e < 16; ++e)     // keep j <= t
@@ -1384,7 +1396,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     // ---- stage 5: Phi0 += R^T V on this wave's rows ----
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bV = frag<kO>(Vt, G::ldVt, ct * 32, s * 16);
+      const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16);
 #pragma unroll
       for (int i = 0; i < G::HT; ++i) {
         P0[i] = mfma(frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
@@ -1407,7 +1419,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
         if (h == 0 && s >= 2) break;      // j past row tile 0: T is zero
-        const bf16x8 bV = frag<kO>(Vt, G::ldVt, ct * 32, s * 16);
+        const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16);
         o = mfma(frag<kO>(Th, G::ldT, h * 32, s * 16), bV, o);
         o = mfma(frag<kO>(Tl, G::ldT, h * 32, s * 16), bV, o);
       }
