@@ -184,29 +184,6 @@ __device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_
   }
 }
 
-// Both layouts from one split: transposed into (Th, Tl) and row-major into (Nh, Nl).
-template <bool O = false>
-__device__ __forceinline__ void store_TN(const f32x16& acc, uint16_t* Th, uint16_t* Tl, int ldT, uint16_t* Nh,
-                                         uint16_t* Nl, int ldN, int row0, int col0) {
-  const int l = lane64<O>();
-  const int g = l >> 5;
-  const int baseT = (col0 + (l & 31)) * ldT + row0 + 4 * g;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    uint32_t h[2], o[2];
-    split2(acc[4 * q], acc[4 * q + 1], h[0], o[0]);
-    split2(acc[4 * q + 2], acc[4 * q + 3], h[1], o[1]);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int offN = (row0 + 8 * q + 4 * g + j) * ldN + col0 + (l & 31);
-      Nh[offN] = (uint16_t)(h[j >> 1] >> (16 * (j & 1)));
-      Nl[offN] = (uint16_t)(o[j >> 1] >> (16 * (j & 1)));
-    }
-    *reinterpret_cast<uint2*>(Th + baseT + 8 * q) = make_uint2(h[0], h[1]);
-    *reinterpret_cast<uint2*>(Tl + baseT + 8 * q) = make_uint2(o[0], o[1]);
-  }
-}
-
 // Store an accumulator tile row-major as X[row0 + i][col0 + r], hi/lo.
 template <bool O = false>
 __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
@@ -227,17 +204,17 @@ __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_
 
 template <int C, int D, int DV, bool SUMMARY>
 struct Cfg {
-  // Two reused buffers: B1 holds W, then R^T (after a barrier); B2 holds R,
-  // then T (after a barrier).  SUMMARY walks use only B1.
+  // Q, K, V row-major (the transposed operands are read through the LDS
+  // transpose unit).  Two reused buffers: B1 holds W, then R^T (after a
+  // barrier); B2 holds T.  SUMMARY walks use only B1.
   static constexpr int CD = C > D ? C : D;
-  static constexpr int ldQ = D + kPad, ldK = D + kPad, ldKt = C + kPad, ldVt = C + kPad;
+  static constexpr int ldQ = D + kPad, ldK = D + kPad, ldV = DV + kPad;
   static constexpr int ld1 = C + kPad, ld2 = CD + kPad, ldQt = C + kPad;
-  static constexpr int ldW = ld1, ldRt = ld1, ldR = ld2, ldT = ld2;
+  static constexpr int ldW = ld1, ldRt = ld1, ldT = ld2;
   static constexpr int oQ = 0;
   static constexpr int oK = oQ + C * ldQ;
-  static constexpr int oKt = oK + C * ldK;
-  static constexpr int oVt = oKt + D * ldKt;
-  static constexpr int oB1h = oVt + DV * ldVt;
+  static constexpr int oVt = oK + C * ldK;                       // V
+  static constexpr int oB1h = oVt + C * ldV;
   static constexpr int oB1l = oB1h + CD * ld1;
   static constexpr int oB2h = oB1l + CD * ld1;
   static constexpr int oB2l = oB2h + (SUMMARY ? 0 : C * ld2);
@@ -800,16 +777,13 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
   uint16_t* Ks = lds + G::oK;
-  uint16_t* Kt = lds + G::oKt;
-  uint16_t* Vt = lds + G::oVt;
+  uint16_t* Vs = lds + G::oVt;    // V row-major
   uint16_t* Wh = lds + G::oB1h;   // W, then R^T
   uint16_t* Wl = lds + G::oB1l;
   uint16_t* Rth = Wh;
   uint16_t* Rtl = Wl;
-  uint16_t* Rh = lds + G::oB2h;   // R, then T
-  uint16_t* Rl = lds + G::oB2l;
-  uint16_t* Th = Rh;
-  uint16_t* Tl = Rl;
+  uint16_t* Th = lds + G::oB2h;   // T
+  uint16_t* Tl = lds + G::oB2l;
   float* fl = reinterpret_cast<float*>(lds + ((G::n16 + 7) & ~7));
   float* eta = fl + G::f_eta;
   float* colsum = fl + G::f_cs;       // [RT][D]
@@ -892,7 +866,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
 
   for (int c = c_begin; c < c_end; ++c) {
     const int t0 = c * C;
-    // ---- stage 0: registers -> LDS (Q, K row-major; K^T, V^T; Q^T for summaries) ----
+    // ---- stage 0: registers -> LDS (Q, K, V row-major) ----
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + kThreads * i;
@@ -900,9 +874,6 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         const int t = e % C, a8 = (e / C) * 8;
         *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
         *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
-        const uint16_t* kk = reinterpret_cast<const uint16_t*>(&pk[i]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) Kt[(a8 + j) * G::ldKt + t] = kk[j];
       }
     }
 #pragma unroll
@@ -910,9 +881,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
       const int e = tid + kThreads * i;
       if (e < G::segV) {
         const int t = e % C, b8 = (e / C) * 8;
-        const uint16_t* vv = reinterpret_cast<const uint16_t*>(&pv[i]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) Vt[(b8 + j) * G::ldVt + t] = vv[j];
+        *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
       }
     }
     __syncthreads();
@@ -943,7 +912,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     if (has_r) {
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
-        const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
+        const bf16x8 bK = frag_tr(Ks, G::ldK, ct * 32, s * 16);
 #pragma unroll
         for (int i = 0; i < G::RPW; ++i) {
           const int rt = rg + G::NRG * i;
@@ -969,9 +938,9 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
       }
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
-        const bf16x8 bK = frag(Kt, G::ldKt, ct * 32, s * 16);
+        const bf16x8 bK = frag_tr(Ks, G::ldK, ct * 32, s * 16);
 #pragma unroll
-        for (int i = 0; i < G::DT; ++i) S0[i] = mfma(frag(Kt, G::ldKt, i * 32, s * 16), bK, S0[i]);
+        for (int i = 0; i < G::DT; ++i) S0[i] = mfma(frag_tr(Ks, G::ldK, i * 32, s * 16), bK, S0[i]);
       }
       // eta advance: column sums of R over each row tile
 #pragma unroll
@@ -992,10 +961,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
       for (int i = 0; i < G::RPW; ++i) {
         const int rt = rg + G::NRG * i;
         if (rt < G::RT) {
-          if (SUMMARY)
-            store_T(racc[i], Rth, Rtl, G::ldRt, rt * 32, ct * 32);
-          else
-            store_TN(racc[i], Rth, Rtl, G::ldRt, Rh, Rl, G::ldR, rt * 32, ct * 32);
+          store_T(racc[i], Rth, Rtl, G::ldRt, rt * 32, ct * 32);
         }
       }
     __syncthreads();
@@ -1014,8 +980,8 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
 #pragma unroll
           for (int s = 0; s < G::KD; ++s) {
             const bf16x8 b = frag(Qs, G::ldQ, jt * 32, s * 16);
-            acc = mfma(frag(Rh, G::ldR, it * 32, s * 16), b, acc);
-            acc = mfma(frag(Rl, G::ldR, it * 32, s * 16), b, acc);
+            acc = mfma(frag_tr(Rth, G::ldRt, it * 32, s * 16), b, acc);
+            acc = mfma(frag_tr(Rtl, G::ldRt, it * 32, s * 16), b, acc);
           }
 #pragma unroll
           for (int e = 0; e < 16; ++e)     // keep j <= t
@@ -1028,8 +994,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
           ps += __shfl_xor(ps, 32);
           if (lg == 0) denp[it * C + jt * 32 + lr] = ps;
         }
-        __syncthreads();     // every wave is done reading R: B2 takes T
-        if (tile) store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);
+        if (tile) store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);   // B2: the last tile's T readers are done
       }
       __syncthreads();
       // den_t = sum_j T[t][j] + q_t . eta0: the row sums here, and eta0 of this
@@ -1051,7 +1016,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         for (int i = 0; i < G::RPW; ++i) oacc[i] = zero16();
 #pragma unroll
         for (int s = 0; s < G::KC; ++s) {
-          const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
+          const bf16x8 bV = frag_tr(Vs, G::ldV, ct * 32, s * 16);
 #pragma unroll
           for (int i = 0; i < G::RPW; ++i) {
             const int rt = rg + G::NRG * i;
@@ -1091,7 +1056,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
       // Phi0 += R^T V on column ct
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
-        const bf16x8 bV = frag(Vt, G::ldVt, ct * 32, s * 16);
+        const bf16x8 bV = frag_tr(Vs, G::ldV, ct * 32, s * 16);
 #pragma unroll
         for (int i = 0; i < G::DT; ++i) {
           P0[i] = mfma(frag(Rth, G::ldRt, i * 32, s * 16), bV, P0[i]);
