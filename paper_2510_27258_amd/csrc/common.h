@@ -23,6 +23,17 @@ __device__ __forceinline__ float ldf(const uint16_t* p, size_t i) {
   return __uint_as_float(((uint32_t)p[i]) << 16);
 }
 
+// Workgroup barrier that orders LDS only: it waits for this wave's LDS
+// operations but not for its outstanding global loads and stores, so
+// prefetches and output stores stay in flight across it (__syncthreads()
+// also drains global memory).  Use it only where no wave reads global memory
+// that another wave of the workgroup wrote before the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 }  // namespace hla
 
 // Launchers implemented in the .hip files (host code, called by the C ABI).

@@ -89,6 +89,12 @@ __device__ __forceinline__ uint4 buf_load16(rsrc_t r, uint32_t off) {
 __device__ __forceinline__ void buf_store4(rsrc_t r, uint32_t off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
 }
+__device__ __forceinline__ void buf_store16(rsrc_t r, uint32_t off, const float4& v) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                                               __float_as_uint(v.w)},
+                                         r, (int)off, 0, 0);
+}
 
 // Lane layout of v_mfma_f32_32x32x16_bf16 (l = lane, r = l % 32, g = l / 32):
 //   A: row r, k = 8g .. 8g+7;  B: column r, the same k (any k order shared by
@@ -1388,10 +1394,17 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         o = mfma(frag<kO>(Th, G::ldT, h * 32, s * 16), bV, o);
         o = mfma(frag<kO>(Tl, G::ldT, h * 32, s * 16), bV, o);
       }
+      // the output tile goes through this wave's own exchange slot (its last
+      // reader was this wave's xch_add) so that each lane stores 16 bytes:
+      // four stores per lane instead of sixteen
+      float* ob = XO + (ct * 2 + h) * 1024;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {      // rows past n fall outside the buffer and are dropped
-        const int t = h * 32 + acc_row(e, lg);
-        buf_store4(ro, (((uint32_t)t0 + t) * DV + ct * 32 + lr) * 4, o[e]);
+      for (int e = 0; e < 16; ++e) ob[acc_row(e, lg) * 32 + lr] = o[e];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {       // rows past n fall outside the buffer and are dropped
+        const int p = l + 64 * j, row = p >> 3, c4 = (p & 7) * 4;
+        buf_store16(ro, (((uint32_t)t0 + h * 32 + row) * DV + ct * 32 + c4) * 4,
+                    *reinterpret_cast<const float4*>(ob + row * 32 + c4));
       }
     }
     __syncthreads();   // LDS tiles and den/eta are rewritten by the next chunk
