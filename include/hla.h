@@ -35,7 +35,8 @@
  *   - Supported sizes: d, dv in {16, 32, 64, 128}; chunk in {16, 32, 64,
  *     128}; any n >= 1 (a short last chunk is exact); B*H <= 65535.
  *     masked, normalized in {0, 1}; eps finite and >= 0 (added to the
- *     denominator as is, den + eps).  Decay is 1 and the ridge 0.
+ *     denominator as is, den + eps).  Decay is 1 (hla2_forward_decay takes
+ *     a decay) and the ridge 0.
  *   - Every call returns an hla_status.  On failure nothing is enqueued and
  *     hla_last_error() describes the reason (a thread-local string).
  *     Results are deterministic: the same inputs give bit-identical outputs.
@@ -143,6 +144,31 @@ int hla2_step(float *state, const void *q_t, const void *k_t, const void *v_t, f
               int B, int H, int d, int dv, int masked, int normalized, float eps, int dtype,
               void *stream);
 
+
+/* ---------------------------------------------------------------------------
+ * hla2_forward_decay — second-order HLA with exponential time decay gamma
+ * (decay section; decay-aware monoid of Sec. 4).  Token moments age as
+ *   S_t = gamma S_{t-1} + k_t k_t^T,  C_t = gamma C_{t-1} + q_t v_t^T,  m_t = gamma m_{t-1} + q_t,
+ * so the pair (i, j) enters row t with weight gamma^{(t-i)+(t-j)}:
+ *   masked    o_t = sum_{j<=t} sum_{i<=j} gamma^{(t-i)+(t-j)} (q_t.k_i)(q_j.k_i) v_j
+ *   unmasked  o_t = sum_{j<=t} sum_{i<=t} gamma^{(t-i)+(t-j)} (q_t.k_i)(q_j.k_i) v_j
+ * i.e. q_t^T (S_t C_t - G_t) with G_t = gamma^2 G_{t-1} + gamma k_t k_t^T C_{t-1}
+ * (the paper prints the cross-summary and the segment concatenation in two
+ * forms that disagree; this is the reading whose masked output drops exactly
+ * the pairs j < i of the unmasked decayed output and whose concatenation,
+ * with rho^2 on G and h, is associative).  normalized divides by the same
+ * sum without v_j, plus eps.  gamma = 1 is hla2_forward's operator.
+ * Computed in fp32 on the chunked path (decayed chunk summaries, the
+ * decayed (+)-scan, decayed readout).  Arguments as hla2_forward, plus
+ * gamma, finite, 0 < gamma <= 1 (else HLA_ERR_INVALID); gamma^(2*chunk) must
+ * stay a normal fp32 number (gamma >= 0.51 at chunk 64; HLA_ERR_UNSUPPORTED
+ * otherwise).  workspace: hla2_forward_decay_workspace_bytes(...) bytes.
+ * ------------------------------------------------------------------------- */
+size_t hla2_forward_decay_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
+int hla2_forward_decay(const void *q, const void *k, const void *v, float *out,
+                       int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
+                       float eps, float gamma, int dtype, void *workspace, size_t workspace_bytes,
+                       void *stream);
 
 /* ---------------------------------------------------------------------------
  * hla3_forward — masked third-order HLA over whole sequences (Sec. 7).

@@ -38,6 +38,8 @@ _SIGS = {
     "hla_profile_begin": (_I, [_I]),
     "hla_profile_end": (_I, []),
     "hla_profile_summary": (_I, [ctypes.c_char_p, _Z]),
+    "hla2_forward_decay_workspace_bytes": (_Z, [_I] * 7),
+    "hla2_forward_decay": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _F, _I, _P, _Z, _P]),
     "hla3_workspace_bytes": (_Z, [_I] * 7),
     "hla3_forward": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
 }
@@ -128,6 +130,16 @@ def hla2_prefill(state, q, k, v, out, B, H, n, d, dv, chunk, masked, normalized,
 
 def hla2_step(state, q_t, k_t, v_t, out_t, B, H, d, dv, masked, normalized, eps, dtype, stream):
     return _call("hla2_step", state, q_t, k_t, v_t, out_t, B, H, d, dv, masked, normalized, eps, dtype, stream)
+
+
+def hla2_forward_decay_workspace_bytes(B, H, n, d, dv, chunk, dtype):
+    return lib().hla2_forward_decay_workspace_bytes(B, H, n, d, dv, chunk, dtype)
+
+
+def hla2_forward_decay(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, gamma, dtype, ws, ws_bytes,
+                       stream):
+    return _call("hla2_forward_decay", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, gamma, dtype,
+                 ws, ws_bytes, stream)
 
 
 def hla3_workspace_bytes(B, H, n, d, dv, chunk, dtype):

@@ -42,17 +42,23 @@ struct Fwd {
   const void* q; const void* k; const void* v; float* out;
   int BH, n, d, dv, chunk, masked, normalized, dtype;
   float eps;
+  float gamma = 1.f;   // decay (chunked path only); 1 = none
 };
+// gamma: decay in (0, 1]; the summaries are taken relative to each chunk's last token.
 hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, float* states,
                                   int BH, int n, int d, int dv, int chunk, int dtype,
-                                  hipStream_t s);
+                                  hipStream_t s, float gamma = 1.f);
+// rho, rho_last: attenuation gamma^length of every segment but the last, and of
+// the last (the decayed concatenation; 1 = none).
 hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
-                       int BH, int M, int d, int dv, hipStream_t s);
+                       int BH, int M, int d, int dv, hipStream_t s, float rho = 1.f, float rho_last = 1.f);
 // Strided form: head h's segment c is states[h*in_stride + c*F]; its prefix
 // goes to prefix[h*pre_stride + c*F] and its total to total[h*tot_stride].
 hipError_t launch_scan_strided(const float* states, const float* init, float* prefix, float* total, int BH, int M,
                                int d, int dv, size_t in_stride, size_t pre_stride, size_t tot_stride,
-                               hipStream_t s);
+                               hipStream_t s, float rho = 1.f, float rho_last = 1.f);
+// Chunks of at most kReadoutMaxChunk tokens (the forward paths cut larger ones).
+constexpr int kReadoutMaxChunk = 64;
 hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s);
 hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out,
                        int BH, int d, int dv, int masked, int normalized, float eps, int dtype,

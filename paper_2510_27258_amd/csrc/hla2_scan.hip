@@ -4,7 +4,11 @@
 // For each head the input is a sequence of M segment states (chunk or segment
 // summaries, record layout S|C|m|G|h); the output holds, for every segment,
 // E (+) init (+) x_0 (+) ... (+) x_{c-1} (Rem. scan-modes), and optionally the
-// inclusive total.
+// inclusive total.  With decay the concatenation of the decay-aware monoid is
+// used (rho = gamma^length of the later segment, read with rho^2 on G and h):
+//   (rho S_A + S_B, rho C_A + C_B, rho m_A + m_B, rho^2 G_A + G_B + rho S_B C_A,
+//    rho^2 h_A + h_B + rho S_B m_A);
+// every segment has attenuation rho except the last (rho_last).
 //
 // The only cross-segment product is S_c C_acc, where C_acc is an additive
 // prefix, so the work splits over column blocks of C and G.  One workgroup
@@ -47,7 +51,8 @@ template <int d, int NBLK>
 __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, const float* __restrict__ init,
                                               float* __restrict__ prefix, float* __restrict__ total,
                                               int BH, int M, int dv, int nblk, size_t in_stride,
-                                              size_t pre_stride, size_t tot_stride) {
+                                              size_t pre_stride, size_t tot_stride, float rho_full,
+                                              float rho_last) {
   using K = ScanCfg<d>;
   constexpr int CB = K::CB, NB = K::NB, ldS = K::ldS, nC4 = K::nC4;
   extern __shared__ float smem[];
@@ -153,7 +158,8 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
       if (tid < r1 - r0) dst[oh + r0 + tid] = hacc;
     }
     if (c == M) return false;
-    // stage segment c: S_c, and C_acc + C_c for the next step
+    const float rho = c == M - 1 ? rho_last : rho_full, rho2 = rho * rho;
+    // stage segment c: S_c, and rho C_acc + C_c for the next step
 #pragma unroll
     for (int r = 0; r < K::nS4; ++r) {
       const int e4 = tid + 256 * r;
@@ -168,14 +174,15 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
       const int e = tid + 256 * r;
       if (e < d * CB / 4) {
         const float4 o = ld4(Cacc + 4 * e);
-        cn[r] = make_float4(o.x + cv[sl][r].x, o.y + cv[sl][r].y, o.z + cv[sl][r].z, o.w + cv[sl][r].w);
+        cn[r] = make_float4(rho * o.x + cv[sl][r].x, rho * o.y + cv[sl][r].y, rho * o.z + cv[sl][r].z,
+                            rho * o.w + cv[sl][r].w);
         if (K::NBUF == 2) st4(Cnext + 4 * e, cn[r]);
       }
     }
 #pragma unroll
-    for (int j = 0; j < NB; ++j) gacc[j] += gv[sl][j];
+    for (int j = 0; j < NB; ++j) gacc[j] = rho2 * gacc[j] + gv[sl][j];
     const float m_c = mv[sl];
-    if (tid < r1 - r0) hacc += hv[sl];
+    if (tid < r1 - r0) hacc = rho2 * hacc + hv[sl];
     __syncthreads();
     if (c + PF < M) load(c + PF, slot_tag);
     // G_acc += S_c C_acc (segment A = accumulated prefix, B = segment c)
@@ -196,7 +203,7 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
         }
       }
 #pragma unroll
-      for (int j = 0; j < NB; ++j) gacc[j] += acc[j];
+      for (int j = 0; j < NB; ++j) gacc[j] += rho * acc[j];
     }
     // h_acc += S_c m_acc and S_acc += S_c on the owned rows
     if (tid < r1 - r0) {
@@ -204,12 +211,12 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
       float e = 0.f;
 #pragma unroll 8
       for (int ap = 0; ap < d; ++ap) e += srow[ap] * macc[ap];
-      hacc += e;
+      hacc += rho * e;
     }
 #pragma unroll
     for (int i = 0; i < nSO; ++i) {
       const int e = tid + 256 * i;
-      if (e < nown) sacc[i] += Sc[(r0 + e / d) * ldS + e % d];
+      if (e < nown) sacc[i] = rho * sacc[i] + Sc[(r0 + e / d) * ldS + e % d];
     }
     if (K::NBUF == 1) {
       __syncthreads();   // everyone is done with Sc and Cacc
@@ -220,7 +227,7 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
       }
     }
     __syncthreads();   // macc readers are done; NBUF == 2: the other buffers are free
-    if (tid < d) macc[tid] += m_c;
+    if (tid < d) macc[tid] = rho * macc[tid] + m_c;
     return true;
   };
   for (int c = 0;; c += PF) {
@@ -303,7 +310,7 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
                                                              const float* __restrict__ init,
                                                              float* __restrict__ prefix, float* __restrict__ total,
                                                              int BH, int M, size_t in_stride, size_t pre_stride,
-                                                             size_t tot_stride) {
+                                                             size_t tot_stride, float rho_full, float rho_last) {
   using K = RbCfg<d>;
   constexpr int RT = K::RT, KS = K::KS, NT = K::NT, ldS = K::ldS, NSLOT = K::NSLOT, PF = K::PF, NM = K::NM,
                 NC4 = K::NC4, NCO = K::NCO;
@@ -418,10 +425,14 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
     const float* mo = macc + (c & 1) * d;   // m_acc before segment c
     put(pre + (size_t)c * F, mo);
     __syncthreads();
-    // G_acc^T += G_c^T + C_acc^T S_c[rows]^T (old C_acc)
+    const float rho = c == M - 1 ? rho_last : rho_full, rho2 = rho * rho;
+    // C_acc <- rho C_acc first: the product below uses the attenuated old C_acc
+#pragma unroll
+    for (int s = 0; s < KS; ++s) cacc[s] *= rho;
+    // G_acc^T <- rho^2 G_acc^T + G_c^T + (rho C_acc)^T S_c[rows]^T
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      f32x4_t acc = gacc[t] + gc[sl][t];
+      f32x4_t acc = rho2 * gacc[t] + gc[sl][t];
       const float* brow = Sc + (16 * t + n) * ldS + KS * g;
 #pragma unroll
       for (int s4 = 0; s4 < KS; s4 += 4) {
@@ -447,17 +458,17 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
       }
       e += __shfl_xor(e, 16);
       e += __shfl_xor(e, 32);
-      hacc[t] += hc[sl][t] + e;
+      hacc[t] = rho2 * hacc[t] + hc[sl][t] + rho * e;
     }
     if (w == 0) {
       float* mn = macc + ((c + 1) & 1) * d;
 #pragma unroll
       for (int j = 0; j < NM; ++j)
-        if (l + 64 * j < d) mn[l + 64 * j] = mo[l + 64 * j] + mc[sl][j];
+        if (l + 64 * j < d) mn[l + 64 * j] = rho * mo[l + 64 * j] + mc[sl][j];
     }
     // S_acc += S_c, C_acc += C_c
 #pragma unroll
-    for (int t = 0; t < RT; ++t) sacc[t] += *reinterpret_cast<const f32x4_t*>(Sc + (16 * t + n) * ldS + c0 + 4 * g);
+    for (int t = 0; t < RT; ++t) sacc[t] = rho * sacc[t] + *reinterpret_cast<const f32x4_t*>(Sc + (16 * t + n) * ldS + c0 + 4 * g);
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int k = KS * g + s;
@@ -466,7 +477,7 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
 #pragma unroll
     for (int j = 0; j < NCO; ++j) {
       const int e = 4 * (tid + NT * j), k = r0 + e / d;
-      cown[j] += *reinterpret_cast<const f32x4_t*>(Cc + k * d + cswz<d>(k, e % d));
+      cown[j] = rho * cown[j] + *reinterpret_cast<const f32x4_t*>(Cc + k * d + cswz<d>(k, e % d));
     }
   };
   if (M > 0) {
@@ -497,14 +508,15 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
 }
 
 hipError_t launch_scan(const float* states, const float* init, float* prefix, float* total,
-                       int BH, int M, int d, int dv, hipStream_t s) {
+                       int BH, int M, int d, int dv, hipStream_t s, float rho, float rho_last) {
   const size_t F = state_floats(d, dv);
-  return launch_scan_strided(states, init, prefix, total, BH, M, d, dv, (size_t)M * F, (size_t)M * F, F, s);
+  return launch_scan_strided(states, init, prefix, total, BH, M, d, dv, (size_t)M * F, (size_t)M * F, F, s, rho,
+                             rho_last);
 }
 
 hipError_t launch_scan_strided(const float* states, const float* init, float* prefix, float* total, int BH, int M,
                                int d, int dv, size_t in_stride, size_t pre_stride, size_t tot_stride,
-                               hipStream_t s) {
+                               hipStream_t s, float rho, float rho_last) {
   const int groups = (BH + 7) / 8;
   if (d == dv) {
     const void* kern = nullptr;
@@ -522,7 +534,7 @@ hipError_t launch_scan_strided(const float* states, const float* init, float* pr
     if (!kern) return hipErrorInvalidValue;
     hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    void* args[] = {&states, &init, &prefix, &total, &BH, &M, &in_stride, &pre_stride, &tot_stride};
+    void* args[] = {&states, &init, &prefix, &total, &BH, &M, &in_stride, &pre_stride, &tot_stride, &rho, &rho_last};
     e = hipLaunchKernel(kern, dim3(groups * 8 * rbn), dim3(nt), args, lds, s);
     if (e != hipSuccess) return e;
     return hipGetLastError();
@@ -544,7 +556,8 @@ hipError_t launch_scan_strided(const float* states, const float* init, float* pr
   if (!kern) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  void* args[] = {&states, &init, &prefix, &total, &BH, &M, &dv, const_cast<int*>(&nblk), &in_stride, &pre_stride, &tot_stride};
+  void* args[] = {&states,    &init,       &prefix,     &total, &BH,     &M,       &dv, const_cast<int*>(&nblk),
+                  &in_stride, &pre_stride, &tot_stride, &rho,   &rho_last};
   e = hipLaunchKernel(kern, dim3(groups * 8 * nblk), dim3(256), args, lds, s);
   if (e != hipSuccess) return e;
   return hipGetLastError();

@@ -63,8 +63,12 @@ int check_ptr(const void* p, const char* name) {
   return HLA_OK;
 }
 
+// Chunk of the chunked path's summaries and readout: the caller's chunk, cut
+// to the readout's maximum (exact for any chunking, Thm. 2).
+int path_chunk(int chunk) { return chunk < hla::kReadoutMaxChunk ? chunk : hla::kReadoutMaxChunk; }
+
 size_t chunked_ws(int BH, int n, int d, int dv, int chunk) {
-  const size_t M = (size_t)(n + chunk - 1) / chunk;
+  const size_t M = (size_t)(n + path_chunk(chunk) - 1) / path_chunk(chunk);
   return 2 * align256(sizeof(float) * (size_t)BH * M * hla::state_floats(d, dv));
 }
 
@@ -131,10 +135,12 @@ int hla2_forward_ex(const void* q, const void* k, const void* v, float* out, int
   const size_t need = chunked_ws(BH, n, d, dv, chunk);
   if (!workspace || workspace_bytes < need)
     return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
-  const int M = (n + chunk - 1) / chunk;
+  f.chunk = path_chunk(chunk);
+  const int M = (n + f.chunk - 1) / f.chunk;
   float* states = static_cast<float*>(workspace);
   float* prefix = reinterpret_cast<float*>(static_cast<char*>(workspace) + need / 2);
-  hipError_t e = HLA_PROF("chunk_summary", s, hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, chunk, dtype, s));
+  hipError_t e = HLA_PROF("chunk_summary", s,
+                          hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, f.chunk, dtype, s));
   if (e != hipSuccess) return hip_fail(e, "chunk summaries");
   e = HLA_PROF("scan", s, hla::launch_scan(states, nullptr, prefix, nullptr, BH, M, d, dv, s));
   if (e != hipSuccess) return hip_fail(e, "scan");
@@ -148,6 +154,48 @@ int hla2_forward(const void* q, const void* k, const void* v, float* out, int B,
                  size_t workspace_bytes, void* stream) {
   return hla2_forward_ex(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, workspace,
                          workspace_bytes, HLA_ALGO_AUTO, stream);
+}
+
+size_t hla2_forward_decay_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  return chunked_ws(B * H, n, d, dv, chunk);
+}
+
+int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
+                       int chunk, int masked, int normalized, float eps, float gamma, int dtype, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
+  if (!std::isfinite(gamma) || gamma <= 0.f || gamma > 1.f)
+    return fail(HLA_ERR_INVALID, "gamma must be finite with 0 < gamma <= 1 (got %g)", (double)gamma);
+  // the readout scales by gamma^(2 (a + 1)), a < chunk: keep it a normal number
+  if (2.0 * chunk * std::log2((double)gamma) < -125.0)
+    return fail(HLA_ERR_UNSUPPORTED, "gamma^(2*chunk) underflows fp32 (gamma=%g chunk=%d)", (double)gamma, chunk);
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
+      (rc = check_ptr(out, "out")))
+    return rc;
+  const int BH = B * H;
+  const size_t need = chunked_ws(BH, n, d, dv, chunk);
+  if (!workspace || workspace_bytes < need)
+    return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int cc = path_chunk(chunk);
+  hla::Fwd f{q, k, v, out, BH, n, d, dv, cc, masked, normalized, dtype, eps, gamma};
+  const int M = (n + cc - 1) / cc;
+  const int last = n - (M - 1) * cc;
+  const float rho = (float)std::pow((double)gamma, (double)cc), rho_last = (float)std::pow((double)gamma, (double)last);
+  float* states = static_cast<float*>(workspace);
+  float* prefix = reinterpret_cast<float*>(static_cast<char*>(workspace) + need / 2);
+  hipError_t e = HLA_PROF("chunk_summary", s,
+                          hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, cc, dtype, s, gamma));
+  if (e != hipSuccess) return hip_fail(e, "chunk summaries");
+  e = HLA_PROF("scan", s, hla::launch_scan(states, nullptr, prefix, nullptr, BH, M, d, dv, s, rho, rho_last));
+  if (e != hipSuccess) return hip_fail(e, "scan");
+  e = HLA_PROF("readout", s, hla::launch_readout(f, prefix, s));
+  if (e != hipSuccess) return hip_fail(e, "readout");
+  return ok();
 }
 
 int hla2_chunk_summaries(const void* q, const void* k, const void* v, float* states, int B, int H, int n, int d,
@@ -202,7 +250,6 @@ int hla2_prefill(float* state, const void* q, const void* k, const void* v, floa
   if (!workspace || workspace_bytes < need)
     return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const int M = (n + chunk - 1) / chunk;
   char* base = static_cast<char*>(workspace);
   float* states = reinterpret_cast<float*>(base);
   float* prefix = reinterpret_cast<float*>(base + cws / 2);
@@ -215,12 +262,13 @@ int hla2_prefill(float* state, const void* q, const void* k, const void* v, floa
     if (e != hipSuccess) return hip_fail(e, "state copy");
     return ok();
   }
-  hipError_t e = hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, chunk, dtype, s);
+  const int cc = path_chunk(chunk), Mc = (n + cc - 1) / cc;
+  hipError_t e = hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, cc, dtype, s);
   if (e != hipSuccess) return hip_fail(e, "chunk summaries");
-  e = hla::launch_scan(states, state, prefix, total, BH, M, d, dv, s);
+  e = hla::launch_scan(states, state, prefix, total, BH, Mc, d, dv, s);
   if (e != hipSuccess) return hip_fail(e, "scan");
   if (out) {
-    hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
+    hla::Fwd f{q, k, v, out, BH, n, d, dv, cc, masked, normalized, dtype, eps};
     e = hla::launch_readout(f, prefix, s);
     if (e != hipSuccess) return hip_fail(e, "readout");
   }

@@ -67,4 +67,8 @@ WORKLOADS = {
     "hla3-masked-fp32-B1H8-n2048-d16-C32": dict(
         kind="hla3", B=1, H=8, n=2048, d=16, dv=16, chunk=32, dist="scaled",
         masked=1, normalized=0, eps=1e-6, seed=0),
+    # the B4H16 d=64 shape with decay gamma = 0.99 (the paper gives no decayed configuration)
+    "hla2-decay-bf16-B4H16-n4096-d64-C64": dict(
+        kind="decay", B=4, H=16, n=4096, d=64, dv=64, chunk=64, dist="unit",
+        masked=1, normalized=0, eps=1e-6, seed=0, gamma=0.99),
 }

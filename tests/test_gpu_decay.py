@@ -1,0 +1,108 @@
+"""GPU parity of the decayed second-order HLA forward (hla2_forward_decay)
+against the fp64 decayed oracle (C serial recurrence, itself pinned against
+brute force, the hand example and the gamma = 1 reduction).
+
+Bars as for the undecayed forward: 1e-5 (fp32 inputs) and 2e-3 (bf16 inputs)
+on the row-wise relative error; the normalised output on rows whose
+denominator is well away from zero (|den + eps| >= 0.05 D_t), num and den
+separately everywhere."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2510_27258_amd as hla
+from paper_2510_27258_amd import capi
+from paper_2510_27258_amd import inputs as I
+from oracle import hla2_decay as OD
+from oracle import native
+from tests.helpers import dev, gen, rowwise_err, tol_for
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _check(B, H, n, d, dv, chunk, dist, gamma, masked=True, normalized=False, seed=0, eps=1e-6):
+    q, k, v, code = gen(B, H, n, d, dv, dist, seed)
+    _say(f"case decay B={B} H={H} n={n} d={d} dv={dv} chunk={chunk} {dist} gamma={gamma} masked={masked} "
+         f"normalized={normalized}")
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    num_ref, den_ref, _, _ = native.hla2_decay_serial_c(q, k, v, gamma, masked=masked, threads=16,
+                                                        return_state=False)
+    tol = tol_for(code)
+    num = hla.forward_decay(qd, kd, vd, chunk, gamma, masked=masked).cpu().numpy()
+    err = rowwise_err(num, num_ref)
+    assert err <= tol, f"num row-wise error {err:.3e} > {tol}"
+    if normalized:
+        out = hla.forward_decay(qd, kd, vd, chunk, gamma, masked=masked, normalized=True, eps=eps).cpu().numpy()
+        ones = torch.ones(B, H, n, dv, dtype=vd.dtype, device="cuda")
+        den = hla.forward_decay(qd, kd, ones, chunk, gamma, masked=masked)[..., 0].cpu().numpy()
+        D = OD.hla2_decay_den_scale(q, k, gamma, masked=masked)
+        e_den = float((np.abs(den - den_ref) / D).max())
+        assert e_den <= tol, f"den error {e_den:.3e} > {tol}"
+        good = np.abs(den_ref + eps) >= 0.05 * D
+        assert good.mean() > 0.3
+        e_out = rowwise_err(out[good], (num_ref / (den_ref + eps)[..., None])[good])
+        assert e_out <= tol, f"normalised output error {e_out:.3e} > {tol}"
+    return err
+
+
+@pytest.mark.parametrize("d,dv", [(16, 16), (32, 64), (64, 32), (64, 64), (128, 128)])
+@pytest.mark.parametrize("chunk", [16, 64, 128])
+@pytest.mark.parametrize("masked", [1, 0])
+def test_decay_shapes_fp32(d, dv, chunk, masked):
+    for gamma in (0.9, 0.995):
+        _check(1, 2, 2 * chunk + 7, d, dv, chunk, "scaled", gamma, masked=bool(masked), seed=d + chunk)
+
+
+@pytest.mark.parametrize("masked", [1, 0])
+def test_decay_bf16(masked):
+    _check(2, 2, 300, 64, 64, 64, "unit", 0.98, masked=bool(masked), seed=1)
+
+
+@pytest.mark.parametrize("masked", [1, 0])
+def test_decay_normalized(masked):
+    _check(2, 2, 200, 32, 32, 32, "scaled", 0.97, masked=bool(masked), normalized=True, seed=2)
+
+
+def test_decay_short_and_single_token():
+    for n in (1, 2, 15, 17):
+        _check(1, 3, n, 32, 32, 16, "scaled", 0.8, seed=n)
+
+
+def test_gamma_one_equals_chunked_forward():
+    """gamma = 1 is the undecayed operator; every decay power is exp2(0) = 1, so
+    the decayed path equals the chunked forward bit for bit."""
+    q, k, v, code = gen(2, 2, 190, 64, 32, "scaled", 3)
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    for masked in (True, False):
+        a = hla.forward_decay(qd, kd, vd, 64, 1.0, masked=masked)
+        b = hla.forward(qd, kd, vd, 64, masked=masked, algo=capi.HLA_ALGO_CHUNKED)
+        assert torch.equal(a, b)
+
+
+def test_decay_workload_b4h16_d64():
+    """B4 H16 n4096 d=dv=64 bf16 unit, chunk 64, gamma 0.99: every head."""
+    w = I.WORKLOADS["hla2-decay-bf16-B4H16-n4096-d64-C64"]
+    err = _check(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], w["dist"], w["gamma"], seed=w["seed"])
+    _say(f"decay workload row-wise error {err:.3e}")
+
+
+def test_decay_errors():
+    q = torch.zeros(1, 1, 64, 16, device="cuda")
+    out = torch.empty_like(q)
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    base = (q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 64, 16, 16, 64, 1, 0, 1e-6)
+    for gamma, code in ((0.0, capi.HLA_ERR_INVALID), (1.5, capi.HLA_ERR_INVALID), (float("nan"), capi.HLA_ERR_INVALID),
+                        (0.3, capi.HLA_ERR_UNSUPPORTED)):
+        with pytest.raises(capi.HLAError) as ei:
+            capi.hla2_forward_decay(*base, gamma, I.HLA_FP32, ws.data_ptr(), ws.numel(), None)
+        assert ei.value.code == code, (gamma, ei.value.code)
+    with pytest.raises(capi.HLAError) as ei:
+        capi.hla2_forward_decay(*base, 0.9, I.HLA_FP32, ws.data_ptr(), 16, None)
+    assert ei.value.code == capi.HLA_ERR_WORKSPACE
