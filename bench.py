@@ -263,6 +263,57 @@ def measure_hla3(reps=20):
             "kernels_ms": {k_: v_[1] / v_[0] for k_, v_ in prof.items()}}
 
 
+def measure_decay(reps=5):
+    """hla2_forward_decay on the decayed workload (B4 H16 n4096 d=dv=64, bf16,
+    chunk 64, gamma 0.99; fp32 SIMT arithmetic on the chunked path): tokens/s
+    by HIP events, per-kernel times, and the dominant kernel against the fp32
+    vector peak with its chunk-form flop count."""
+    import torch
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
+    from paper_2510_27258_amd import inputs as I
+    name = "hla2-decay-bf16-B4H16-n4096-d64-C64"
+    w = I.WORKLOADS[name]
+    q, k, v, code = I.draw_qkv(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    out = torch.empty(w["B"], w["H"], w["n"], w["dv"], dtype=torch.float32, device=dev)
+    wsb = capi.hla2_forward_decay_workspace_bytes(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], code)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    run = lambda: hla.forward_decay(qd, kd, vd, w["chunk"], w["gamma"], out=out, workspace=ws)
+    for _ in range(2):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    capi.hla_profile_begin(8 * reps + 8)
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    prof = capi.hla_profile_summary()
+    capi.hla_profile_end()
+    kms = {k_: v_[1] / v_[0] for k_, v_ in prof.items()}
+    # chunk-form flops per launch (fp32, counted densely as written; the
+    # triangles are not halved): summary 2 C (C d + C dv + d^2 + 2 d dv) per
+    # chunk, readout 2 C (d^2 + 2 C d + d dv + C dv) per chunk
+    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], min(w["chunk"], 64)
+    chunks = B * H * (-(-n // C))
+    flops = {"chunk_summary": chunks * 2 * C * (C * d + C * dv + d * d + 2 * d * dv),
+             "readout": chunks * 2 * C * (d * d + 2 * C * d + d * dv + C * dv)}
+    dom = max((k_ for k_ in kms if k_ in flops), key=lambda k_: kms[k_])
+    achieved = flops[dom] / (kms[dom] / 1e3) / 1e12
+    tokens = B * H * n
+    return {"workload": name, "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms, "dtype": "f32",
+            "gamma": w["gamma"], "kernels_ms": kms,
+            "roofline": {"kernel": dom, "bound": "alu", "achieved": achieved, "peak": FP32_VALU_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": achieved / FP32_VALU_PEAK_TFLOPS}}
+
+
 def measure_decode(steps=None):
     """hla2_step on the decode workload: state from a prefill of the seeded
     2048-token prefix, then the seeded step tokens, one launch per step."""
@@ -312,6 +363,7 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone scan measurement")
     ap.add_argument("--no-hla3", action="store_true", help="skip the third-order measurement")
+    ap.add_argument("--no-decay", action="store_true", help="skip the decayed-forward measurement")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
     ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
@@ -417,6 +469,8 @@ def main():
         rec["scan"] = measure_scan(w, qd, kd, vd)
     if not args.no_hla3:
         rec["hla3"] = measure_hla3()
+    if not args.no_decay:
+        rec["decay"] = measure_decay()
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
     if not args.no_decode:
