@@ -13,7 +13,12 @@ Modules
   hla3      third-order HLA (Sec. 7): the triple sum over the index set of
             Thm. 3, the streaming kernel (Alg. 3), the corrected-state
             recurrence, the operator (x)_3 and the chunk-parallel scan (Alg. 4).
-  hla2_ref.c, hla3_ref.c  the serial recurrences in plain C (fp64), used to
+  hla2_decay  second-order HLA with exponential decay (decay section and the
+            decay-aware concatenation of Sec. 4).
+  ahla      asymmetric second-order HLA (Sec. 6): the double sum, the
+            streaming recurrence, (+)_AHLA and the chunked scan.
+  hla2_ref.c, hla2_decay_ref.c, hla3_ref.c, ahla_ref.c  the serial
+            recurrences in plain C (fp64), used to
             time the oracle on host cores and to check large cases quickly.
   native    ctypes loader for the compiled C oracle.
 """

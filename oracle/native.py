@@ -11,7 +11,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(_HERE, "liboracle.so")
-SOURCES = ["hla2_ref.c", "hla2_decay_ref.c", "hla3_ref.c"]
+SOURCES = ["hla2_ref.c", "hla2_decay_ref.c", "hla3_ref.c", "ahla_ref.c"]
 _handle = None
 
 
@@ -42,6 +42,10 @@ def load():
                                                   ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
                                                   P, P, P, P, P, ctypes.c_int]
             lib.hla2_decay_serial_f64.restype = ctypes.c_int
+        if hasattr(lib, "ahla_serial_f64"):
+            lib.ahla_serial_f64.argtypes = [P, P, P, P, P, ctypes.c_long, ctypes.c_long, ctypes.c_int,
+                                            ctypes.c_int, ctypes.c_int]
+            lib.ahla_serial_f64.restype = ctypes.c_int
         if hasattr(lib, "hla3_serial_f64"):
             lib.hla3_serial_f64.argtypes = [P, P, P, P, P, ctypes.c_long, ctypes.c_long,
                                             ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
@@ -137,3 +141,20 @@ def hla2_decay_serial_c(q, k, v, gamma, masked=True, state=None, threads=0, retu
                                      int(bool(masked)), float(gamma), *[_ptr(x) for x in st], int(threads))
     final = tuple(st) if st[0] is not None else None
     return num, den, final, used
+
+
+def ahla_serial_c(q, k, v, threads=0):
+    """AHLA streaming recurrence (Sec. 6) in C over heads [..., n, d].
+    Returns (num [..., n, dv], den [..., n], threads used)."""
+    lib = load()
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    batch = q.shape[:-2]
+    n, d = q.shape[-2:]
+    dv = v.shape[-1]
+    BH = int(np.prod(batch)) if batch else 1
+    num = np.empty(batch + (n, dv))
+    den = np.empty(batch + (n,))
+    used = lib.ahla_serial_f64(_ptr(q), _ptr(k), _ptr(v), _ptr(num), _ptr(den), BH, n, d, dv, int(threads))
+    return num, den, used
