@@ -193,6 +193,28 @@ int hla3_forward(const void *q, const void *k, const void *v, float *out,
                  float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * ahla_forward — asymmetric second-order HLA (AHLA, Sec. 6): the left-cascaded
+ * product ((A A) (.) L) V with A = L (.) Q K^T (diagonal kept),
+ *   o_t = sum_{j<=t} sum_{i=j..t} (q_t.k_i)(q_i.k_j) v_j     (Eq. AHLA-explicit)
+ *       = q_t^T E_t,  E_t = E_{t-1} + k_t (q_t^T P_t),  P_t = P_{t-1} + k_t v_t^T
+ * (Thm. AHLA; E_t uses P_t including token t).  With normalized = 1 the row
+ * is divided by (q_t^T n_t + eps), n_t = n_{t-1} + k_t (q_t^T m_t), m_t the
+ * key sum: the same double sum without v_j.  Decay is 1.
+ * Computed on bf16 MFMA with fp32 accumulation by a segment scan under
+ * (+)_AHLA (Eq. AHLA-semidirect): q, k, v [B, H, n, d] bf16 (dtype =
+ * HLA_BF16), out [B, H, n, d] fp32; device pointers, 16-byte aligned,
+ * caller-owned.  Supported: d = dv in {64, 128}, chunk in {64, 128} (walked
+ * in 64-token tiles; exact for any chunking), any n >= 1; everything else
+ * (fp32 inputs included) returns HLA_ERR_UNSUPPORTED.  workspace: at least
+ * ahla_workspace_bytes(...) bytes of device memory (contents on entry
+ * ignored); HLA_ERR_WORKSPACE if smaller.
+ * ------------------------------------------------------------------------- */
+size_t ahla_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
+int ahla_forward(const void *q, const void *k, const void *v, float *out,
+                 int B, int H, int n, int d, int dv, int chunk, int normalized, float eps,
+                 int dtype, void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
  * Benchmark timing.  hla_profile_begin(max_records) creates 2*max_records HIP
  * events (host objects, no device memory) and starts bracketing every kernel
  * the library launches with events recorded on that kernel's stream;

@@ -6,6 +6,7 @@
 #include <cstring>
 
 #include "../../include/hla.h"
+#include "ahla.h"
 #include "common.h"
 #include "fused.h"
 #include "hla3.h"
@@ -195,6 +196,35 @@ int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, 
   if (e != hipSuccess) return hip_fail(e, "scan");
   e = HLA_PROF("readout", s, hla::launch_readout(f, prefix, s));
   if (e != hipSuccess) return hip_fail(e, "readout");
+  return ok();
+}
+
+size_t ahla_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || !hla::ahla_supported(n, d, dv, chunk, dtype))
+    return 0;
+  return hla::ahla_workspace_bytes(B * H, n, d);
+}
+
+int ahla_forward(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
+                 int chunk, int normalized, float eps, int dtype, void* workspace, size_t workspace_bytes,
+                 void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if ((rc = check_flags(1, normalized, eps)) != HLA_OK) return rc;
+  if (!hla::ahla_supported(n, d, dv, chunk, dtype))
+    return fail(HLA_ERR_UNSUPPORTED, "AHLA covers bf16, d = dv in {64, 128}, chunk in {64, 128} "
+                "(got d=%d dv=%d chunk=%d dtype=%d)", d, dv, chunk, dtype);
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
+      (rc = check_ptr(out, "out")))
+    return rc;
+  const int BH = B * H;
+  const size_t need = hla::ahla_workspace_bytes(BH, n, d);
+  if (!workspace || workspace_bytes < need)
+    return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, 1, normalized, dtype, eps};
+  const hipError_t e = hla::launch_ahla(f, workspace, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "ahla forward");
   return ok();
 }
 

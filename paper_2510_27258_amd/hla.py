@@ -138,6 +138,22 @@ def forward_decay(q, k, v, chunk, gamma, masked=True, normalized=False, eps=1e-6
     return out
 
 
+def ahla_forward(q, k, v, chunk, normalized=False, eps=1e-6, out=None, workspace=None):
+    """AHLA (Sec. 6), ((A A) (.) L) V with A = L (.) Q K^T; q, k, v [B,H,n,d] bf16 -> out fp32."""
+    _check(q, k, v)
+    B, H, n, d = q.shape
+    dv = v.shape[-1]
+    code = _code(q)
+    if out is None:
+        out = torch.empty(B, H, n, dv, dtype=torch.float32, device=q.device)
+    wsb = capi.ahla_workspace_bytes(B, H, n, d, dv, chunk, code)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    capi.ahla_forward(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, H, n, d, dv, chunk,
+                      int(normalized), float(eps), code, workspace.data_ptr(), workspace.numel(), _stream())
+    return out
+
+
 def hla3_forward(q, k, v, chunk, masked=True, normalized=False, eps=1e-6, out=None, workspace=None):
     """Third-order masked HLA, q, k [B,H,n,d], v [B,H,n,dv] -> out fp32."""
     _check(q, k, v)

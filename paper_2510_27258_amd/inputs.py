@@ -71,4 +71,8 @@ WORKLOADS = {
     "hla2-decay-bf16-B4H16-n4096-d64-C64": dict(
         kind="decay", B=4, H=16, n=4096, d=64, dv=64, chunk=64, dist="unit",
         masked=1, normalized=0, eps=1e-6, seed=0, gamma=0.99),
+    # AHLA (Sec. 6) on the B4H16 d=64 shape of the second-order workload
+    "ahla-bf16-B4H16-n4096-d64-C64": dict(
+        kind="ahla", B=4, H=16, n=4096, d=64, dv=64, chunk=64, dist="unit",
+        masked=1, normalized=0, eps=1e-6, seed=0),
 }
