@@ -122,9 +122,11 @@ def traffic_for(kernel, workload):
 
 def kernel_key(name):
     """Bench name of a library kernel from its (demangled) dispatch name."""
+    if "k_ahla_walk" in name:
+        return "ahla_walk"
     if "k_walk" in name:
         return "walk_summary" if ("true" in name or "Lb1E" in name) else "walk"
-    for key in ("k_seg_cross", "k_total", "k_moments", "k_carry", "k_fix", "k_scan", "k_chunk_summary", "k_readout",
+    for key in ("k_init_convert", "k_total", "k_moments", "k_carry", "k_fix", "k_scan", "k_chunk_summary", "k_readout",
                 "k_step"):
         if key in name:
             return key[2:]
@@ -179,9 +181,11 @@ def source_sha():
     return h.hexdigest()[:16]
 
 
-def cpu_baseline(w, q, k, v, budget_s=20.0):
+def cpu_baseline(w, q, k, v, budget_s=20.0, min_s=10.0):
     """The C oracle (serial fp64 recurrence, heads over OpenMP threads) on the
-    host cores, on as many whole heads of the workload as fit the budget."""
+    host cores, on as many whole heads of the workload as fit the budget; the
+    sample is repeated until it has run for at least min_s seconds, so short
+    samples are timed over several passes."""
     import numpy as np
     from oracle import native
     B, H, n = w["B"], w["H"], w["n"]
@@ -195,12 +199,18 @@ def cpu_baseline(w, q, k, v, budget_s=20.0):
     qs = q.reshape(B * H, n, -1)[:heads]
     ks = k.reshape(B * H, n, -1)[:heads]
     vs = v.reshape(B * H, n, -1)[:heads]
+    passes, used = 0, 1
     t0 = time.perf_counter()
-    _, _, _, used = native.hla2_serial_c(qs, ks, vs, masked=bool(w["masked"]), threads=threads,
-                                         return_state=False)
-    dt = time.perf_counter() - t0
-    return {"value": heads * n / dt, "unit": "tokens/s", "cores": int(used), "kind": "oracle",
-            "sample": f"{heads} of {B * H} heads x {n} tokens, C fp64 serial recurrence, {dt:.2f} s"}
+    while True:
+        _, _, _, used = native.hla2_serial_c(qs, ks, vs, masked=bool(w["masked"]), threads=threads,
+                                             return_state=False)
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s or passes >= 1000:
+            break
+    return {"value": passes * heads * n / dt, "unit": "tokens/s", "cores": int(used), "kind": "oracle",
+            "sample": f"{heads} of {B * H} heads x {n} tokens, C fp64 serial recurrence, {passes} passes "
+                      f"in {dt:.2f} s"}
 
 
 def measure_scan(w, qd, kd, vd, reps=10):
@@ -314,6 +324,61 @@ def measure_decay(reps=5):
                          "unit": "TFLOP/s", "frac": achieved / FP32_VALU_PEAK_TFLOPS}}
 
 
+def ahla_flops_per_token(C, d, dv):
+    """Dense flop count per token of the AHLA chunk form with tile C (no
+    triangle discount): A = Q K^T (C d), R = A V + Q P0 (C dv + d dv),
+    O = A R + Q E0 (C dv + d dv), P0 += K^T V and E0 += K^T R (2 d dv)."""
+    return 2 * (C * d + 2 * C * dv + 4 * d * dv)
+
+
+def measure_ahla(reps=10):
+    """ahla_forward on the AHLA workload (B4 H16 n4096 d=dv=64, bf16, chunk
+    64): tokens/s by HIP events, per-kernel times, and the walk against HBM
+    (q, k, v read once, out written once) and against the bf16 MFMA peak with
+    the dense chunk-form flop count."""
+    import torch
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
+    from paper_2510_27258_amd import inputs as I
+    name = "ahla-bf16-B4H16-n4096-d64-C64"
+    w = I.WORKLOADS[name]
+    q, k, v, code = I.draw_qkv(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    out = torch.empty(w["B"], w["H"], w["n"], w["dv"], dtype=torch.float32, device=dev)
+    wsb = capi.ahla_workspace_bytes(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], code)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    run = lambda: hla.ahla_forward(qd, kd, vd, w["chunk"], out=out, workspace=ws)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    capi.hla_profile_begin(8 * reps + 8)
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    prof = capi.hla_profile_summary()
+    capi.hla_profile_end()
+    kms = {k_: v_[1] / v_[0] for k_, v_ in prof.items()}
+    B, H, n, d, dv = w["B"], w["H"], w["n"], w["d"], w["dv"]
+    tokens = B * H * n
+    nbytes = tokens * (2 * 2 * d + 2 * dv + 4 * dv)
+    flops = tokens * ahla_flops_per_token(64, d, dv)
+    s = kms["ahla_walk"] / 1e3
+    return {"workload": name, "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms, "dtype": "bf16",
+            "kernels_ms": kms,
+            "roofline": {"kernel": "ahla_walk", "bound": "hbm", "achieved": nbytes / s / 1e9, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": nbytes / s / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes,
+                         "algorithmic_flops": flops, "mfma_tflops": flops / s / 1e12,
+                         "mfma_frac": flops / s / 1e12 / BF16_MFMA_PEAK_TFLOPS}}
+
+
 def measure_decode(steps=None):
     """hla2_step on the decode workload: state from a prefill of the seeded
     2048-token prefix, then the seeded step tokens, one launch per step."""
@@ -364,6 +429,9 @@ def main():
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone scan measurement")
     ap.add_argument("--no-hla3", action="store_true", help="skip the third-order measurement")
     ap.add_argument("--no-decay", action="store_true", help="skip the decayed-forward measurement")
+    ap.add_argument("--no-ahla", action="store_true", help="skip the AHLA measurement")
+    ap.add_argument("--only", choices=["ahla", "decay", "hla3"],
+                    help="run only that measurement and print its record (for profiling one path)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
     ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
@@ -388,6 +456,11 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": args.copy_bytes, "steps": args.steps}))
+        return
+
+    if args.only:
+        rec = {"ahla": measure_ahla, "decay": measure_decay, "hla3": measure_hla3}[args.only]()
+        print(json.dumps(rec), flush=True)
         return
 
     import paper_2510_27258_amd as hla
@@ -471,6 +544,8 @@ def main():
         rec["hla3"] = measure_hla3()
     if not args.no_decay:
         rec["decay"] = measure_decay()
+    if not args.no_ahla:
+        rec["ahla"] = measure_ahla()
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
     if not args.no_decode:

@@ -362,7 +362,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
   hipError_t e;
   if (P > 1) {
     prof_start("ahla_moments", s);
-    hipLaunchKernelGGL((k_moments<C, D, D, true>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1);
+    HLA_LAUNCH((k_moments<C, D, D, true>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -370,13 +370,13 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
                                (int)G::bytes)) != hipSuccess)
     return e;
   prof_start("ahla_walk", s);
-  hipLaunchKernelGGL((k_ahla_walk<D>), grid, dim3(G::NT), G::bytes, s, q, k, v, f.out, den, segs, f.n, cps, P,
+  HLA_LAUNCH((k_ahla_walk<D>), grid, dim3(G::NT), G::bytes, s, q, k, v, f.out, den, segs, f.n, cps, P,
                      f.normalized);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (P > 1 || f.normalized) {
     prof_start("ahla_carry", s);
-    hipLaunchKernelGGL((k_carry<D, D>), dim3((D * D / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs,
+    HLA_LAUNCH((k_carry<D, D>), dim3((D * D / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs,
                        (const float*)nullptr, carry, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -386,7 +386,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
       return e;
     const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("ahla_fix", s);
-    hipLaunchKernelGGL((k_fix<C, D, D>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
+    HLA_LAUNCH((k_fix<C, D, D>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
                        carry, 0, f.n, cps, P, f.normalized, f.eps, tpw);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;

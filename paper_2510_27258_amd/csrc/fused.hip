@@ -1,18 +1,22 @@
 // Fused masked second-order HLA forward for bf16 inputs on gfx950 MFMA.
 //
-// Algorithm (Sec. 4, two-level scan, Rem. scan-modes; Thm. 1 readout):
-// the sequence of every head is cut into P segments of whole chunks.
-//   1. k_walk<SUMMARY>: each workgroup walks one segment from a zero carry and
-//      produces its summary (S, C, m, Phi, eta) with Phi = S C - G and
-//      eta = S m - h (an exact change of variables of the 5-tuple).
-//   2. k_seg_cross: the semidirect product of Eq. (semidirect) across
-//      segments in reduce-then-scan form, in the Phi variables: each
-//      segment's bracket Phi_s + S_{<s} C_s (and eta_s + S_{<s} m_s) is
-//      computed in parallel.
-//   3. k_walk<OUTPUT>: each workgroup sums the brackets before its segment
-//      into its carry (S0, Phi0, eta0), walks its chunks from that carry and
-//      writes the outputs.
-//   k_total sums all brackets into the total state when a caller needs it.
+// Algorithm (Sec. 4, two-level scan, Rem. scan-modes; Thm. 1 readout): the
+// sequence of every head is cut into P segments of whole chunks, and the
+// carries are kept as (S, Phi, eta) with Phi = S C - G and eta = S m - h (an
+// exact change of variables of the 5-tuple).  In those variables Eq.
+// (semidirect) reads Phi_{A(+)B} = Phi_A + Phi_B + S_A C_B: a segment's
+// bracket Phi_s + S_{<s} C_s depends on the earlier segments only through
+// the additive S prefix.  So
+//   1. k_moments: S = K^T K of every segment;
+//   2. k_walk_rs / k_walk<OUTPUT>: every segment walks its chunks from the
+//      true S prefix with Phi0 = eta0 = 0, writes its outputs without the Phi
+//      carry, and ends holding its bracket (Phi0, eta0), which it writes to
+//      its record;
+//   3. k_carry / k_fix: running sums of the brackets are the carries;
+//      out_t += q_t^T Phi_c (and the division when normalised).
+// With an initial state, k_init_convert converts it to the (S, C, m, Phi, eta)
+// form first; k_total sums all records into the final state when a caller
+// asks for it.  k_moments, k_carry and k_fix live in fused_tiles.h.
 //
 // Per chunk (tokens of the chunk as the rows of Q, K, V; S0, Phi0, eta0 the
 // carry of the chunk), with r_j = S_j q_j (the proof of Thm. 1 sums
@@ -87,20 +91,12 @@ struct Cfg {
   static_assert(bytes <= 160 * 1024, "LDS budget");
 };
 
-// The semidirect-product scan over segments, Eq. (semidirect), organised as
-// reduce-then-scan in the (S, C, m, Phi, eta) variables, Phi = S C - G and
-// eta = S m - h.  Substituting Eq. (semidirect) gives
-//   Phi_{A(+)B} = Phi_A + Phi_B + S_A C_B,   eta_{A(+)B} = eta_A + eta_B + S_A m_B,
-// and S, C, m add.  With A = everything before segment s (the initial state
-// included) the bracket Phi_s + S_{<s} C_s depends on A only through the
-// additive prefix S_{<s}, so every segment's bracket is formed in parallel
-// (k_seg_cross) and the carry of a segment is a plain sum of the brackets
-// before it (the output walk's prologue); the total state is the plain sum
-// of all of them, converted back to G, h once (k_total).
-//
 // Records: [BH][nseg + 1][F] in the S|C|m|G|h layout with Phi in the G slot
-// and eta in the h slot; slot nseg holds the initial state converted to this
-// form (written only when there is one).
+// and eta in the h slot.  Slot s < nseg: the segment's moments (S; C and m
+// when a final state is wanted) and, after its walk, its bracket.  Slot nseg
+// holds the initial state converted to this form (written only when there is
+// one).  Carries and the total are plain sums of these records (the Phi form
+// of Eq. (semidirect)); the total is converted back to G, h once (k_total).
 
 // out[a][b] = z * Z[a][b] + sum_a' X[a][a'] Y[a'][b] for the thread's TI x TI
 // register blocks; XT = X^T ([D][D+4]) and Y ([D][DV]) in LDS, Z and out in
@@ -173,50 +169,37 @@ __device__ __forceinline__ void add4(float4& a, const float4& b) {
   a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
 }
 
-// k_seg_cross: grid (nsum + [init != 0], BH), 256 threads.  Block s < nsum
-// replaces (Phi_s, eta_s) of record s by its bracket (Phi_s + S_{<s} C_s,
-// eta_s + S_{<s} m_s), S_{<s} = S_init + sum_{s'<s} S_s'.  Block s = nsum
-// converts the initial state into slot nseg: (S, C, m, S C - G, S m - h).
-// Blocks read S of other records and write only their own G/h slots.
+// k_init_convert: grid (1, BH), 256 threads.  Writes the initial state of
+// every head into slot nseg of its records in the (S, C, m, Phi, eta) form:
+// (S, C, m, S C - G, S m - h).
 template <int D, int DV>
-__global__ __launch_bounds__(256) void k_seg_cross(float* __restrict__ segs, const float* __restrict__ init,
-                                                   int nseg, int nsum) {
-  constexpr int nS4 = D * D / 4 / 256, nC4 = D * DV / 4 / 256, ldT = D + 4;
+__global__ __launch_bounds__(256) void k_init_convert(float* __restrict__ segs, const float* __restrict__ init,
+                                                      int nseg) {
+  constexpr int nS4 = D * D / 4 / 256, nC4 = D * DV / 4 / 256;
   static_assert(D * D % 1024 == 0 && D * DV % 1024 == 0, "thread split");
   extern __shared__ float sm[];
-  float* XT = sm;                 // [D][D+4]  X^T
-  float* Y = XT + D * ldT;        // [D][DV]
-  float* y = Y + D * DV;          // [D]
-  const int s = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  float* XT = sm;                 // [D][D+4]  S^T
+  float* Y = XT + D * (D + 4);    // [D][DV]   C
+  float* y = Y + D * DV;          // [D]       m
+  const int bh = blockIdx.y, tid = threadIdx.x;
   const size_t F = state_floats(D, DV);
-  const bool conv = s == nsum;
-  float* base = segs + (size_t)bh * (nseg + 1) * F;
-  const float* ini = init ? init + (size_t)bh * F : nullptr;
-  float* dst = base + (size_t)(conv ? nseg : s) * F;
-  const float* src = conv ? ini : dst;
+  const float* src = init + (size_t)bh * F;
+  float* dst = segs + ((size_t)bh * (nseg + 1) + nseg) * F;
   float4 xs[nS4], ys[nC4];
-  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int r = 0; r < nS4; ++r) xs[r] = ini ? reinterpret_cast<const float4*>(ini)[tid + 256 * r] : z4;
-  if (!conv)
-    for (int sp = 0; sp < s; ++sp)
-#pragma unroll
-      for (int r = 0; r < nS4; ++r) add4(xs[r], reinterpret_cast<const float4*>(base + (size_t)sp * F)[tid + 256 * r]);
+  for (int r = 0; r < nS4; ++r) xs[r] = reinterpret_cast<const float4*>(src)[tid + 256 * r];
 #pragma unroll
   for (int r = 0; r < nC4; ++r) ys[r] = reinterpret_cast<const float4*>(src + off_C(D, DV))[tid + 256 * r];
   const float yv = tid < D ? src[off_m(D, DV) + tid] : 0.f;
   stage_xy<D, DV>(XT, Y, y, xs, ys, yv);
-  if (conv) {
 #pragma unroll
-    for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(dst)[tid + 256 * r] = xs[r];
+  for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(dst)[tid + 256 * r] = xs[r];
 #pragma unroll
-    for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(dst + off_C(D, DV))[tid + 256 * r] = ys[r];
-    if (tid < D) dst[off_m(D, DV) + tid] = yv;
-  }
+  for (int r = 0; r < nC4; ++r) reinterpret_cast<float4*>(dst + off_C(D, DV))[tid + 256 * r] = ys[r];
+  if (tid < D) dst[off_m(D, DV) + tid] = yv;
   __syncthreads();
-  const float z = conv ? -1.f : 1.f;
-  xy_plus<D, DV>(XT, Y, src + off_G(D, DV), z, dst + off_G(D, DV));
-  xv_plus<D>(XT, y, src + off_h(D, DV), z, dst + off_h(D, DV));
+  xy_plus<D, DV>(XT, Y, src + off_G(D, DV), -1.f, dst + off_G(D, DV));
+  xv_plus<D>(XT, y, src + off_h(D, DV), -1.f, dst + off_h(D, DV));
 }
 
 // k_total: grid (BH), 256 threads.  The state after all nsum segments in the
@@ -400,7 +383,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
       }
     }
-    __syncthreads();
+    lds_barrier();
     if (c + 1 < c_end) fetch(c + 1);
 
     // ---- stage 1: W = L (.) Q K^T, computed as W^T = K Q^T and stored transposed ----
@@ -419,7 +402,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         store_T(acc, Wh, Wl, G::ldW, it * 32, jt * 32);
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- stage 2: R = W K + Q S0 (old S0) on column tile ct; S0 += K^T K on column ct ----
     f32x16 racc[G::RPW];
@@ -471,7 +454,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         }
       }
     }
-    __syncthreads();     // every wave is done reading W: B1 takes R^T
+    lds_barrier();     // every wave is done reading W: B1 takes R^T
     if (has_r)
 #pragma unroll
       for (int i = 0; i < G::RPW; ++i) {
@@ -480,7 +463,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
           store_T(racc[i], Rth, Rtl, G::ldRt, rt * 32, ct * 32);
         }
       }
-    __syncthreads();
+    lds_barrier();
     float eta_add = 0.f;
     if (tid < D)
 #pragma unroll
@@ -512,7 +495,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         }
         if (tile) store_T(acc, Th, Tl, G::ldT, it * 32, jt * 32);   // B2: the last tile's T readers are done
       }
-      __syncthreads();
+      lds_barrier();
       // den_t = sum_j T[t][j] + q_t . eta0: the row sums here, and eta0 of this
       // tile (before its advance) for k_fix, which adds q_t . (eta0 + eta_c)
       if (normalized) {
@@ -524,7 +507,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         }
         if (tid < D) den_out[(size_t)gridDim.y * n + ((size_t)bh * ((n + C - 1) / C) + c) * D + tid] = eta[tid];
       }
-      __syncthreads();
+      lds_barrier();
       // ---- stage 4: O = T V + Q Phi0 (old Phi0) on column tile ct; stage 5: Phi0 += R^T V ----
       if (has_o) {
         f32x16 oacc[G::RPW];
@@ -580,7 +563,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
         }
       }
     }
-    __syncthreads();   // LDS tiles and den/eta are rewritten by the next chunk
+    lds_barrier();   // LDS tiles and den/eta are rewritten by the next chunk
     if (tid < D) eta[tid] += eta_add;
   }
 
@@ -766,7 +749,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       const int t = e % C, b8 = (e / C) * 8;
       *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
     }
-    __syncthreads();
+    lds_barrier();
     if (c + 1 < c_end) fetch(c + 1);
 
     // ---- stage 1: W = L (.) Q K^T on tiles (key it <= query jt), stored transposed ----
@@ -783,7 +766,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         store_T<kO>(acc, Wh, Wl, G::ld1, it * 32, jt * 32);
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- stage 2: R partials over this wave's state rows (both row tiles), then W K on row tile h ----
     f32x16 part[2];
@@ -816,9 +799,9 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 #pragma unroll
       for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16), bK, S0[i]);
     }
-    __syncthreads();                      // K, K^T and W are dead: K | K^T takes the exchange
+    lds_barrier();                      // K, K^T and W are dead: K | K^T takes the exchange
     xch_put<kO>(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0]);
-    __syncthreads();
+    lds_barrier();
     f32x16 racc = h == 0 ? part[0] : part[1];
     xch_add<kO>(XR, ct * 2 + h, racc);
     {
@@ -829,7 +812,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       if (lg == 0) colsum[h * D + ct * 32 + lr] = cs;
     }
     store_T<kO>(racc, Wh, Wl, G::ld1, h * 32, ct * 32);     // R^T
-    __syncthreads();
+    lds_barrier();
     float eta_add = 0.f;
     if (tid < D) eta_add = colsum[tid] + colsum[D + tid];
 
@@ -885,7 +868,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       }
     }
     if (!SUMMARY) {
-      __syncthreads();                    // T and denp visible; R and R^T are dead
+      lds_barrier();                    // T and denp visible; R and R^T are dead
       xch_put<kO>(XO, ct * 2 + (1 - h), h == 0 ? oacc[1] : oacc[0]);
       // den_t = sum_j T[t][j] + q_t . eta0: the row sums here, and eta0 of this
       // tile (before its advance) for k_fix, which adds q_t . (eta0 + eta_c)
@@ -893,7 +876,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         if (tid < C && t0 + tid < n) den_out[(size_t)bh * n + t0 + tid] = denp[tid] + denp[C + tid];
         if (tid < D) den_out[(size_t)gridDim.y * n + ((size_t)bh * ((n + C - 1) / C) + c) * D + tid] = eta[tid];
       }
-      __syncthreads();
+      lds_barrier();
       f32x16 o = h == 0 ? oacc[0] : oacc[1];
       xch_add<kO>(XO, ct * 2 + h, o);
       // ---- stage 4b: O (row tile h) += T V ----
@@ -917,7 +900,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
                     *reinterpret_cast<const float4*>(ob + row * 32 + c4));
       }
     }
-    __syncthreads();   // LDS tiles and den/eta are rewritten by the next chunk
+    lds_barrier();   // LDS tiles and den/eta are rewritten by the next chunk
     if (tid < D) eta[tid] += eta_add;
   }
 
@@ -983,7 +966,7 @@ hipError_t launch_walk(const WalkK& kk, dim3 grid, hipStream_t s, const uint16_t
   hipError_t e = hipFuncSetAttribute(kk.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kk.lds);
   if (e != hipSuccess) return e;
   void* args[] = {&q, &k, &v, &out, &den_out, &rec, &init, &n, &cps, &nseg, &normalized, &eps};
-  return hipLaunchKernel(kk.fn, grid, dim3(kk.threads), args, kk.lds, s);
+  return prof_launch(kk.fn, grid, dim3(kk.threads), args, kk.lds, s);
 }
 
 size_t records_bytes(int BH, int P, int d, int dv) {
@@ -1003,14 +986,14 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   hipError_t e;
   if (init) {      // slot P <- the initial state in the (S, C, m, Phi, eta) form
     size_t lds;
-    if ((e = set_cross_lds<D, DV>((const void*)k_seg_cross<D, DV>, &lds)) != hipSuccess) return e;
+    if ((e = set_cross_lds<D, DV>((const void*)k_init_convert<D, DV>, &lds)) != hipSuccess) return e;
     prof_start("init_convert", s);
-    hipLaunchKernelGGL((k_seg_cross<D, DV>), dim3(1, BH), dim3(256), lds, s, segs, init, P, 0);
+    HLA_LAUNCH((k_init_convert<D, DV>), dim3(1, BH), dim3(256), lds, s, segs, init, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   prof_start("moments", s);
-  hipLaunchKernelGGL((k_moments<C, D, DV>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P,
+  HLA_LAUNCH((k_moments<C, D, DV>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P,
                      final_state ? 1 : 0);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1025,14 +1008,14 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     size_t lds;
     if ((e = set_cross_lds<D, DV>((const void*)k_total<D, DV>, &lds)) != hipSuccess) return e;
     prof_start("total", s);
-    hipLaunchKernelGGL((k_total<D, DV>), dim3(BH), dim3(256), lds, s, segs, init, final_state, P, P);
+    HLA_LAUNCH((k_total<D, DV>), dim3(BH), dim3(256), lds, s, segs, init, final_state, P, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (f.out && (P > 1 || init || f.normalized)) {
     float* carry = den + (((size_t)BH * f.n + (size_t)BH * ((f.n + C - 1) / C) * D + 63) & ~size_t(63));
     prof_start("carry", s);
-    hipLaunchKernelGGL((k_carry<D, DV>), dim3((D * DV / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P);
+    HLA_LAUNCH((k_carry<D, DV>), dim3((D * DV / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     using FC = FixCfg<C, D, DV>;
@@ -1042,7 +1025,7 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
       return e;
     const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("fix", s);
-    hipLaunchKernelGGL((k_fix<C, D, DV>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
+    HLA_LAUNCH((k_fix<C, D, DV>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
                        carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps, tpw);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;

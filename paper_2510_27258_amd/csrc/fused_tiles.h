@@ -232,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
           for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
         }
       }
-      __syncthreads();
+      lds_barrier();
       load(c + PF, slot_tag);
 #pragma unroll
       for (int i = 0; i < nS; ++i) {
@@ -244,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
             sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
         }
       }
-      __syncthreads();
+      lds_barrier();
     };
     if (c0 < c1) {
       load(c0, std::integral_constant<int, 0>());
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
 #pragma unroll
         for (int j = 0; j < 8; ++j) Vt[(b8 + j) * ld + t] = v8[j];
       }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int i = 0; i < nS; ++i) {
       const int ti = w + kWaves * i;
@@ -315,7 +315,7 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
   float* r = rec + ((size_t)bh * (nseg + 1) + seg) * state_floats(D, DV);
 #pragma unroll
@@ -447,7 +447,7 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
       loaded = seg;
     }
     const uint32_t t0 = (uint32_t)c * C;
-    __syncthreads();                  // the previous tile's readers of Qs are done
+    lds_barrier();                  // the previous tile's readers of Qs are done
 #pragma unroll
     for (int i = 0; i < QV; ++i) {
       const int e = tid + NT * i;
@@ -455,7 +455,7 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
     }
     if (normalized && tid < D)        // eta at the tile start: the walk's eta0 + eta_c
       es[tid] = cb[D * DV + tid] + den_in[(size_t)gridDim.y * n + ((size_t)bh * M + c) * D + tid];
-    __syncthreads();
+    lds_barrier();
     // rows past n fall outside the buffer: loads read 0, stores drop
     const uint32_t ob = ((t0 + rt * 32 + 4 * lg) * DV + ct * 32 + lr) * 4;
     float prev[16];
@@ -483,7 +483,7 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
 #pragma unroll
       for (int o = 1; o < TPR; o <<= 1) sd += __shfl_xor(sd, o);
       if (tid % TPR == 0 && t < C) inv[t] = (t0 + t < (uint32_t)n) ? 1.f / (den_in[(size_t)bh * n + t0 + t] + sd + eps) : 0.f;
-      __syncthreads();
+      lds_barrier();
     }
     f32x16 acc = zero16();
 #pragma unroll

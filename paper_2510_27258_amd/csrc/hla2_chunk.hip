@@ -17,6 +17,7 @@
 // rho^2, the cross term by rho).  gamma = 1 is the undecayed operator: every
 // power below is exp2(0) = 1 exactly.
 #include "common.h"
+#include "profile.h"
 
 namespace hla {
 
@@ -243,13 +244,13 @@ hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, f
     auto kern = k_chunk_summary<uint16_t>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, grid, block, lds, s, (const uint16_t*)q, (const uint16_t*)k,
+    HLA_LAUNCH(kern, grid, block, lds, s, (const uint16_t*)q, (const uint16_t*)k,
                        (const uint16_t*)v, states, n, d, dv, chunk, M, lg2g);
   } else {
     auto kern = k_chunk_summary<float>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, grid, block, lds, s, (const float*)q, (const float*)k, (const float*)v,
+    HLA_LAUNCH(kern, grid, block, lds, s, (const float*)q, (const float*)k, (const float*)v,
                        states, n, d, dv, chunk, M, lg2g);
   }
   return hipGetLastError();
@@ -265,14 +266,14 @@ hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s) {
     auto kern = k_readout<uint16_t>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, grid, block, lds, s, (const uint16_t*)f.q, (const uint16_t*)f.k,
+    HLA_LAUNCH(kern, grid, block, lds, s, (const uint16_t*)f.q, (const uint16_t*)f.k,
                        (const uint16_t*)f.v, prefix, f.out, f.n, f.d, f.dv, f.chunk, M, f.masked,
                        f.normalized, f.eps, lg2g);
   } else {
     auto kern = k_readout<float>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, grid, block, lds, s, (const float*)f.q, (const float*)f.k, (const float*)f.v,
+    HLA_LAUNCH(kern, grid, block, lds, s, (const float*)f.q, (const float*)f.k, (const float*)f.v,
                        prefix, f.out, f.n, f.d, f.dv, f.chunk, M, f.masked, f.normalized, f.eps, lg2g);
   }
   return hipGetLastError();

@@ -19,6 +19,7 @@
 #include <type_traits>
 
 #include "common.h"
+#include "profile.h"
 
 namespace hla {
 
@@ -535,7 +536,7 @@ hipError_t launch_scan_strided(const float* states, const float* init, float* pr
     hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     void* args[] = {&states, &init, &prefix, &total, &BH, &M, &in_stride, &pre_stride, &tot_stride, &rho, &rho_last};
-    e = hipLaunchKernel(kern, dim3(groups * 8 * rbn), dim3(nt), args, lds, s);
+    e = prof_launch(kern, dim3(groups * 8 * rbn), dim3(nt), args, lds, s);
     if (e != hipSuccess) return e;
     return hipGetLastError();
   }
@@ -558,7 +559,7 @@ hipError_t launch_scan_strided(const float* states, const float* init, float* pr
   if (e != hipSuccess) return e;
   void* args[] = {&states,    &init,       &prefix,     &total, &BH,     &M,       &dv, const_cast<int*>(&nblk),
                   &in_stride, &pre_stride, &tot_stride, &rho,   &rho_last};
-  e = hipLaunchKernel(kern, dim3(groups * 8 * nblk), dim3(256), args, lds, s);
+  e = prof_launch(kern, dim3(groups * 8 * nblk), dim3(256), args, lds, s);
   if (e != hipSuccess) return e;
   return hipGetLastError();
 }

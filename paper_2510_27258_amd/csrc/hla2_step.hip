@@ -8,6 +8,7 @@
 // once: all of S, C and G are loaded up front (16-byte vector loads, up to
 // 48 per thread), then three dependent reductions over rows run through LDS.
 #include "common.h"
+#include "profile.h"
 
 namespace hla {
 
@@ -165,10 +166,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state
 hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out, int BH, int d,
                        int dv, int masked, int normalized, float eps, int dtype, hipStream_t s) {
   if (dtype == 1)
-    hipLaunchKernelGGL(k_step<uint16_t>, dim3(BH), dim3(kStepThreads), 0, s, state, (const uint16_t*)q,
+    HLA_LAUNCH(k_step<uint16_t>, dim3(BH), dim3(kStepThreads), 0, s, state, (const uint16_t*)q,
                        (const uint16_t*)k, (const uint16_t*)v, out, d, dv, masked, normalized, eps);
   else
-    hipLaunchKernelGGL(k_step<float>, dim3(BH), dim3(kStepThreads), 0, s, state, (const float*)q,
+    HLA_LAUNCH(k_step<float>, dim3(BH), dim3(kStepThreads), 0, s, state, (const float*)q,
                        (const float*)k, (const float*)v, out, d, dv, masked, normalized, eps);
   return hipGetLastError();
 }

@@ -344,16 +344,16 @@ hipError_t run3(const Fwd& f, float* recs, float* den, int P, int cps, hipStream
   const T* v = static_cast<const T*>(f.v);
   const dim3 grid(P, f.BH);
   prof_start("hla3_moments", s);
-  hipLaunchKernelGGL((k3_moments<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, recs, f.n, cps, P);
+  HLA_LAUNCH((k3_moments<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, recs, f.n, cps, P);
   prof_stop(s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   prof_start("hla3_walk", s);
-  hipLaunchKernelGGL((k3_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, den, recs, f.n, cps, P);
+  HLA_LAUNCH((k3_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, den, recs, f.n, cps, P);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_start("hla3_fix", s);
-  hipLaunchKernelGGL((k3_fix<T, C, D, DV>), grid, dim3(kT3), 0, s, q, f.out, den, recs, f.n, cps, P, f.normalized,
+  HLA_LAUNCH((k3_fix<T, C, D, DV>), grid, dim3(kT3), 0, s, q, f.out, den, recs, f.n, cps, P, f.normalized,
                      f.eps);
   prof_stop(s);
   return hipGetLastError();

@@ -1,5 +1,9 @@
 // Optional per-kernel timing for benchmarks.  While enabled, each kernel the
-// C ABI launches is bracketed by two HIP events recorded on its own stream;
+// C ABI launches is bracketed by two HIP events: the kernel's dispatch
+// records its own start and end time into them (hipExtLaunchKernel), so the
+// figure is the kernel's execution time without the gaps of the stream.  A
+// bracket holding more than one launch (or a launch not made through
+// prof_take) falls back to events recorded on the stream around it.
 // hla_profile_summary() reads them back once the caller has synchronised.
 #include <cstdio>
 #include <cstring>
@@ -20,6 +24,7 @@ std::vector<hipEvent_t> g_ev;   // 2 per record
 std::vector<Rec> g_rec;
 int g_cap = 0;
 int g_open = -1;
+int g_launches = 0;   // launches made inside the open bracket
 }  // namespace
 
 namespace hla {
@@ -29,11 +34,24 @@ void prof_start(const char* name, hipStream_t s) {
   g_rec.push_back({name, slot});
   (void)hipEventRecord(g_ev[2 * slot], s);
   g_open = slot;
+  g_launches = 0;
 }
 void prof_stop(hipStream_t s) {
   if (!g_on || g_open < 0) return;
-  (void)hipEventRecord(g_ev[2 * g_open + 1], s);
+  if (g_launches != 1) (void)hipEventRecord(g_ev[2 * g_open + 1], s);
   g_open = -1;
+}
+bool prof_take(hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_on || g_open < 0) return false;
+  if (++g_launches != 1) return false;
+  *start = g_ev[2 * g_open];
+  *stop = g_ev[2 * g_open + 1];
+  return true;
+}
+hipError_t prof_launch(const void* fn, dim3 grid, dim3 block, void** args, size_t lds, hipStream_t s) {
+  hipEvent_t e0, e1;
+  if (prof_take(&e0, &e1)) return hipExtLaunchKernel(fn, grid, block, args, lds, s, e0, e1, 0);
+  return hipLaunchKernel(fn, grid, block, args, lds, s);
 }
 }  // namespace hla
 
