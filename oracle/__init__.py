@@ -15,6 +15,8 @@ Modules
             recurrence, the operator (x)_3 and the chunk-parallel scan (Alg. 4).
   hla2_decay  second-order HLA with exponential decay (decay section and the
             decay-aware concatenation of Sec. 4).
+  hla2_backward  gradients of the masked second-order HLA (the reverse scan
+            of Sec. 4.2 written out), pinned against torch autograd.
   ahla      asymmetric second-order HLA (Sec. 6): the double sum, the
             streaming recurrence, (+)_AHLA and the chunked scan.
   hla2_ref.c, hla2_decay_ref.c, hla3_ref.c, ahla_ref.c  the serial
