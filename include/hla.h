@@ -193,6 +193,28 @@ int hla3_forward(const void *q, const void *k, const void *v, float *out,
                  float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * hla2_backward — gradients of the masked, unnormalised second-order HLA
+ * (the reverse scan of Sec. 4.2, written out): for a loss L with upstream
+ * gradient g = dL/dout,
+ *   dq_j = Phi_j g_j + S_j u_j,   dv_j = U_j^T r_j,   dk_i = (Z_i + Z_i^T) k_i,
+ * with S_j = sum_{i<=j} k_i k_i^T, r_j = S_j q_j, Phi_j = sum_{j'<=j} r_j' v_j'^T,
+ * U_j = sum_{t>=j} q_t g_t^T, u_j = U_j v_j, Z_i = sum_{j>=i} u_j q_j^T.
+ * Computed on bf16 MFMA (fp32 operands split hi/lo, fp32 accumulation) as
+ * seven causal or anti-causal first-order chunk scans over 64-token tiles.
+ * q, k, v [B, H, n, d] bf16 (dtype = HLA_BF16); g [B, H, n, dv] fp32;
+ * dq, dk [B, H, n, d] and dv [B, H, n, dv] fp32, written (not accumulated).
+ * Device pointers, 16-byte aligned, caller-owned; outputs must not alias
+ * inputs or each other.  Supported: d = dv in {64, 128}, chunk any supported
+ * value (the tiling does not change the result beyond rounding), any n >= 1;
+ * everything else returns HLA_ERR_UNSUPPORTED.  workspace: at least
+ * hla2_backward_workspace_bytes(...) bytes (contents on entry ignored).
+ * ------------------------------------------------------------------------- */
+size_t hla2_backward_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
+int hla2_backward(const void *q, const void *k, const void *v, const float *g, float *dq, float *dk,
+                  float *dv, int B, int H, int n, int d, int dv_dim, int chunk, int dtype,
+                  void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
  * ahla_forward — asymmetric second-order HLA (AHLA, Sec. 6): the left-cascaded
  * product ((A A) (.) L) V with A = L (.) Q K^T (diagonal kept),
  *   o_t = sum_{j<=t} sum_{i=j..t} (q_t.k_i)(q_i.k_j) v_j     (Eq. AHLA-explicit)

@@ -40,6 +40,8 @@ _SIGS = {
     "hla_profile_summary": (_I, [ctypes.c_char_p, _Z]),
     "hla2_forward_decay_workspace_bytes": (_Z, [_I] * 7),
     "hla2_forward_decay": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _F, _I, _P, _Z, _P]),
+    "hla2_backward_workspace_bytes": (_Z, [_I] * 7),
+    "hla2_backward": (_I, [_P] * 7 + [_I] * 7 + [_P, _Z, _P]),
     "ahla_workspace_bytes": (_Z, [_I] * 7),
     "ahla_forward": (_I, [_P, _P, _P, _P] + [_I] * 7 + [_F, _I, _P, _Z, _P]),
     "hla3_workspace_bytes": (_Z, [_I] * 7),
@@ -142,6 +144,14 @@ def hla2_forward_decay(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, 
                        stream):
     return _call("hla2_forward_decay", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, gamma, dtype,
                  ws, ws_bytes, stream)
+
+
+def hla2_backward_workspace_bytes(B, H, n, d, dv, chunk, dtype):
+    return lib().hla2_backward_workspace_bytes(B, H, n, d, dv, chunk, dtype)
+
+
+def hla2_backward(q, k, v, g, dq, dk, dv, B, H, n, d, dv_dim, chunk, dtype, ws, ws_bytes, stream):
+    return _call("hla2_backward", q, k, v, g, dq, dk, dv, B, H, n, d, dv_dim, chunk, dtype, ws, ws_bytes, stream)
 
 
 def ahla_workspace_bytes(B, H, n, d, dv, chunk, dtype):

@@ -1,0 +1,351 @@
+// Gradients of the masked second-order HLA (the reverse scan of Sec. 4.2)
+// for bf16 inputs on gfx950 MFMA.
+//
+// With S_j = sum_{i<=j} k_i k_i^T, r_j = S_j q_j, Phi_j = sum_{j'<=j} r_j' v_j'^T
+// (the forward prefixes of Thm. 1's proof), the upstream gradient g_t and the
+// reverse prefixes U_j = sum_{t>=j} q_t g_t^T, u_j = U_j v_j and
+// Z_i = sum_{j>=i} u_j q_j^T, the vector-Jacobian product of the masked
+// operator is
+//   dq_j = Phi_j g_j + S_j u_j,   dv_j = U_j^T r_j,   dk_i = (Z_i + Z_i^T) k_i.
+// Every term is a first-order (linear) attention read causally or
+// anti-causally.  Writing LA+(x, y, z)_j = sum_{i<=j} (x_j.y_i) z_i and
+// LA-(x, y, z)_j = sum_{i>=j} (x_j.y_i) z_i:
+//   r  = LA+(q, k, k)                       u  = LA-(v, g, q)
+//   dq = LA+(g, v, r) + LA+(u, k, k)        dv = LA-(r, q, g)
+//   dk = LA-(k, q, u) + LA-(k, u, q).
+// Each pass is the first-order chunk scan: the state sum y z^T of a segment
+// does not depend on anything before it, so every segment's walk starts from
+// the exact prefix (suffix) of the segment moments and no fix-up follows.
+//
+// k_la<..., MOM = true> writes the moments M_s = sum_{i in s} y_i z_i^T of
+// every segment; k_la<..., MOM = false> walks a segment's 64-token tiles in
+// time order (causal) or in reverse (anti-causal) from
+// S0 = sum of the moments of the segments before (after) it:
+//   A = Q K^T masked (key <= query, or key >= query), O = A Z + X S0,
+//   S0 += Y^T Z,
+// and writes (or adds) O.  Operands that are exact in bf16 (q, k, v) take
+// one MFMA pass; fp32 operands (g, r, u) and every computed operand (A, S0)
+// are split into bf16 hi + lo, and a product of two split operands takes
+// three passes (hi hi, hi lo, lo hi).  Accumulation is fp32.
+#include <cstdlib>
+
+#include "backward.h"
+#include "fused_tiles.h"
+#include "profile.h"
+
+namespace hla {
+namespace {
+
+template <int D>
+struct CfgLA {
+  static constexpr int C = 64;
+  static constexpr int NCT = D / 32, NW = 2 * NCT, NT = 64 * NW;   // wave: row tile w / NCT, column tile w % NCT
+  static constexpr int ST = D / 32, KC = C / 16, KD = D / 16;
+  static constexpr int ld = D + kPad, ldA = C + kPad;
+  // row-major bf16 tiles: X, Y, Z each hi | lo, then A hi | lo
+  static constexpr int oXh = 0, oXl = oXh + C * ld, oYh = oXl + C * ld, oYl = oYh + C * ld;
+  static constexpr int oZh = oYl + C * ld, oZl = oZh + C * ld, oAh = oZl + C * ld, oAl = oAh + C * ldA;
+  static constexpr int n16 = oAl + C * ldA;
+  static constexpr size_t bytes = (size_t)n16 * 2;
+  static_assert(D * D * 2 <= n16, "state staging fits the tile region");
+  static constexpr int kBlocks = 2 * bytes <= 160 * 1024 && NW <= 4 ? 2 : 1;
+  static_assert(bytes <= 160 * 1024, "LDS budget");
+  static_assert(D == 64 || D == 128, "linear-attention pass shapes");
+};
+
+// One 64 x D operand tile, rows t0 .. t0+63 of a [n][D] array, staged into
+// LDS as bf16 (hi, and lo for fp32 inputs).  Rows past n read zero.
+template <int D, int NT, bool F32>
+struct Stage {
+  static constexpr int EP = F32 ? 4 : 8;                     // elements per 16-byte piece
+  static constexpr int NPC = 64 * D / EP;                    // pieces per tile
+  static constexpr int NV = NPC / NT;                        // pieces per thread
+  static_assert(NPC % NT == 0, "staging split");
+  uint4 p[NV];
+  __device__ __forceinline__ void fetch(rsrc_t r, int c, int tid) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int e = tid + NT * i, t = e % 64, a = (e / 64) * EP;   // consecutive lanes take consecutive tokens
+      p[i] = buf_load16(r, (((uint32_t)c * 64 + t) * D + a) * (F32 ? 4 : 2));
+    }
+  }
+  __device__ __forceinline__ void store(uint16_t* hi, uint16_t* lo, int ld, int tid) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int e = tid + NT * i, t = e % 64, a = (e / 64) * EP;
+      if constexpr (F32) {
+        uint32_t h0, l0, h1, l1;
+        split2(__uint_as_float(p[i].x), __uint_as_float(p[i].y), h0, l0);
+        split2(__uint_as_float(p[i].z), __uint_as_float(p[i].w), h1, l1);
+        *reinterpret_cast<uint2*>(hi + t * ld + a) = make_uint2(h0, h1);
+        *reinterpret_cast<uint2*>(lo + t * ld + a) = make_uint2(l0, l1);
+      } else {
+        *reinterpret_cast<uint4*>(hi + t * ld + a) = p[i];
+      }
+    }
+  }
+};
+
+// grid (nseg, BH), NT threads.  REV: anti-causal (keys at or after the
+// query; tiles walked from the last).  ACC: add to out instead of writing it.
+template <int D, bool XF, bool YF, bool ZF, bool MOM>
+__global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
+    const void* __restrict__ xp, const void* __restrict__ yp, const void* __restrict__ zp, float* __restrict__ out,
+    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out) {
+  using G = CfgLA<D>;
+  constexpr bool kO = D == 128;
+  constexpr int C = G::C, NT = G::NT, ST = G::ST, ld = G::ld, ldA = G::ldA;
+  extern __shared__ __align__(16) uint16_t lds[];
+  uint16_t* Xh = lds + G::oXh;
+  uint16_t* Xl = lds + G::oXl;
+  uint16_t* Yh = lds + G::oYh;
+  uint16_t* Yl = lds + G::oYl;
+  uint16_t* Zh = lds + G::oZh;
+  uint16_t* Zl = lds + G::oZl;
+  uint16_t* Ah = lds + G::oAh;
+  uint16_t* Al = lds + G::oAl;
+
+  const int seg = blockIdx.x, bh = blockIdx.y;
+  const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rt = w / G::NCT, ct = w % G::NCT;
+  const int M = (n + C - 1) / C;
+  const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
+  const size_t DD = (size_t)D * D;
+
+  // ---- state: zero for the moments; else the sum of the moments before (after) the segment ----
+  f32x16 S0[ST];
+#pragma unroll
+  for (int i = 0; i < ST; ++i) S0[i] = zero16();
+  if (!MOM) {
+    const int s_lo = rev ? seg + 1 : 0, s_hi = rev ? nseg : seg;
+    if (s_lo < s_hi) {
+      constexpr int nP4 = D * D / 4 / NT;
+      static_assert(D * D % (4 * NT) == 0, "state staging split");
+      float4 pa[nP4];
+#pragma unroll
+      for (int r = 0; r < nP4; ++r) pa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int sp = s_lo; sp < s_hi; ++sp) {
+        const float4* x4 = reinterpret_cast<const float4*>(rec + ((size_t)bh * nseg + sp) * DD);
+#pragma unroll
+        for (int r = 0; r < nP4; ++r) {
+          const float4 u = x4[tid + NT * r];
+          pa[r].x += u.x; pa[r].y += u.y; pa[r].z += u.z; pa[r].w += u.w;
+        }
+      }
+      float* st = reinterpret_cast<float*>(lds);
+#pragma unroll
+      for (int r = 0; r < nP4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = pa[r];
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < ST; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S0[i][e] = st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+      __syncthreads();
+    }
+  }
+
+  const size_t eX = (XF ? 4 : 2), eY = (YF ? 4 : 2), eZ = (ZF ? 4 : 2);
+  const rsrc_t rx = make_rsrc(static_cast<const char*>(xp) + (size_t)bh * n * D * eX, (uint32_t)(n * D * eX));
+  const rsrc_t ry = make_rsrc(static_cast<const char*>(yp) + (size_t)bh * n * D * eY, (uint32_t)(n * D * eY));
+  const rsrc_t rz = make_rsrc(static_cast<const char*>(zp) + (size_t)bh * n * D * eZ, (uint32_t)(n * D * eZ));
+  const rsrc_t ro = make_rsrc(MOM ? nullptr : out + (size_t)bh * n * D, MOM ? 0u : (uint32_t)n * D * 4);
+  Stage<D, NT, XF> sx;
+  Stage<D, NT, YF> sy;
+  Stage<D, NT, ZF> sz;
+  const int nt = c_end - c_begin;
+  auto tile_of = [&](int i) { return rev ? c_end - 1 - i : c_begin + i; };
+  if (nt > 0) {
+    if (!MOM) sx.fetch(rx, tile_of(0), tid);
+    sy.fetch(ry, tile_of(0), tid);
+    sz.fetch(rz, tile_of(0), tid);
+  }
+
+  for (int it = 0; it < nt; ++it) {
+    const int c = tile_of(it);
+    // ---- stage 0: operands into LDS (fp32 ones split into hi | lo) ----
+    if (!MOM) sx.store(Xh, Xl, ld, tid);
+    sy.store(Yh, Yl, ld, tid);
+    sz.store(Zh, Zl, ld, tid);
+    lds_barrier();
+    if (it + 1 < nt) {
+      if (!MOM) sx.fetch(rx, tile_of(it + 1), tid);
+      sy.fetch(ry, tile_of(it + 1), tid);
+      sz.fetch(rz, tile_of(it + 1), tid);
+    }
+
+    f32x16 o = zero16();
+    if (!MOM) {
+      // ---- stage 1: A = X Y^T masked, as A^T = Y X^T on tiles (key kt, query qt), stored row-major ----
+      if (w < 4) {
+        const int kt = w >> 1, qt = w & 1;
+        if (rev ? kt >= qt : kt <= qt) {
+          f32x16 a = zero16();
+#pragma unroll
+          for (int s = 0; s < D / 16; ++s) {
+            const bf16x8 yh = frag<kO>(Yh, ld, kt * 32, s * 16), xh = frag<kO>(Xh, ld, qt * 32, s * 16);
+            a = mfma(yh, xh, a);
+            if (XF) a = mfma(yh, frag<kO>(Xl, ld, qt * 32, s * 16), a);
+            if (YF) a = mfma(frag<kO>(Yl, ld, kt * 32, s * 16), xh, a);
+          }
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {   // keep key <= query (causal) or key >= query (anti-causal)
+            const int key = kt * 32 + acc_row(e, lg), qry = qt * 32 + lr;
+            if (rev ? key < qry : key > qry) a[e] = 0.f;
+          }
+          store_T<kO>(a, Ah, Al, ldA, kt * 32, qt * 32);
+        }
+      }
+      lds_barrier();
+      // ---- stage 2: O = X S0 (state before this tile) + A Z ----
+#pragma unroll
+      for (int j = 0; j < G::KD; ++j) {
+        bf16x8 sh, sl;
+        frag_from_acc(S0[j >> 1], j & 1, sh, sl);
+        const bf16x8 ah = frag_acc_order<kO>(Xh, ld, rt * 32, j * 16);
+        o = mfma(ah, sh, o);
+        o = mfma(ah, sl, o);
+        if (XF) o = mfma(frag_acc_order<kO>(Xl, ld, rt * 32, j * 16), sh, o);
+      }
+#pragma unroll
+      for (int s = 0; s < G::KC; ++s) {
+        // keys of this k step against the row tile's queries: causal needs s < 2 (rt + 1), anti-causal s >= 2 rt
+        if (rev ? s >= 2 * rt : s < 2 * (rt + 1)) {
+          const bf16x8 zh = frag_tr<kO>(Zh, ld, ct * 32, s * 16);
+          const bf16x8 ah = frag<kO>(Ah, ldA, rt * 32, s * 16), al = frag<kO>(Al, ldA, rt * 32, s * 16);
+          o = mfma(ah, zh, o);
+          o = mfma(al, zh, o);
+          if (ZF) o = mfma(ah, frag_tr<kO>(Zl, ld, ct * 32, s * 16), o);
+        }
+      }
+    }
+    // ---- state advance: S0 += Y^T Z (column ct, all rows) ----
+#pragma unroll
+    for (int s = 0; s < G::KC; ++s) {
+      const bf16x8 zh = frag_tr<kO>(Zh, ld, ct * 32, s * 16);
+      bf16x8 zl;
+      if (ZF) zl = frag_tr<kO>(Zl, ld, ct * 32, s * 16);
+#pragma unroll
+      for (int i = 0; i < ST; ++i) {
+        const bf16x8 yh = frag_tr<kO>(Yh, ld, i * 32, s * 16);
+        S0[i] = mfma(yh, zh, S0[i]);
+        if (ZF) S0[i] = mfma(yh, zl, S0[i]);
+        if (YF) S0[i] = mfma(frag_tr<kO>(Yl, ld, i * 32, s * 16), zh, S0[i]);
+      }
+    }
+    if (!MOM) {
+      // rows past n fall outside the buffer: loads read 0, stores drop
+      const uint32_t ob = (((uint32_t)c * C + rt * 32 + 4 * lg) * D + ct * 32 + lr) * 4;
+      float prev[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        prev[e] = acc_out ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                                ro, (int)(ob + (8 * (e >> 2) + (e & 3)) * D * 4), 0, 0))
+                          : 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) buf_store4(ro, ob + (8 * (e >> 2) + (e & 3)) * D * 4, prev[e] + o[e]);
+    }
+    lds_barrier();   // the next tile rewrites every LDS tile
+  }
+
+  if (MOM && rt == 0) {   // both row waves hold the column; row tile 0's write it
+    int col = ct * 32 + lr;
+    asm volatile("" : "+v"(col));
+    float* r = rec + ((size_t)bh * nseg + seg) * DD;
+#pragma unroll
+    for (int i = 0; i < ST; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) r[(size_t)(i * 32 + acc_row(e, lg)) * D + col] = S0[i][e];
+  }
+}
+
+void la_plan(int D, int BH, int n, int* P, int* cps) {
+  const int M = (n + 63) / 64;
+  const int blocks = D == 64 ? CfgLA<64>::kBlocks : CfgLA<128>::kBlocks;
+  int p = 256 * blocks / BH;
+  if (const char* e = getenv("HLA_FUSED_SEGMENTS")) p = atoi(e);
+  if (p < 1) p = 1;
+  if (p > M) p = M;
+  *cps = (M + p - 1) / p;
+  *P = (M + *cps - 1) / *cps;
+}
+
+// One linear-attention pass: moments of (y, z) per segment, then the walks.
+template <int D, bool XF, bool YF, bool ZF>
+hipError_t la_pass(const char* name, const void* x, const void* y, const void* z, float* out, float* rec, int BH, int n,
+                   int P, int cps, int rev, int acc, hipStream_t s) {
+  using G = CfgLA<D>;
+  const dim3 grid(P, BH);
+  hipError_t e;
+  if (P > 1) {
+    const void* km = (const void*)k_la<D, false, YF, ZF, true>;
+    if ((e = hipFuncSetAttribute(km, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess)
+      return e;
+    prof_start("bwd_moments", s);
+    HLA_LAUNCH((k_la<D, false, YF, ZF, true>), grid, dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P, rev,
+               acc);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  const void* kw = (const void*)k_la<D, XF, YF, ZF, false>;
+  if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess)
+    return e;
+  prof_start(name, s);
+  HLA_LAUNCH((k_la<D, XF, YF, ZF, false>), grid, dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P, rev, acc);
+  prof_stop(s);
+  return hipGetLastError();
+}
+
+size_t rec_bytes(int BH, int P, int d) {
+  return (sizeof(float) * (size_t)BH * P * d * d + 255) & ~size_t(255);
+}
+size_t vec_bytes(int BH, int n, int d) { return (sizeof(float) * (size_t)BH * n * d + 255) & ~size_t(255); }
+
+template <int D>
+hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
+  int P, cps;
+  la_plan(D, b.BH, b.n, &P, &cps);
+  float* rec = reinterpret_cast<float*>(ws);
+  float* r = reinterpret_cast<float*>(ws + rec_bytes(b.BH, P, D));
+  float* u = reinterpret_cast<float*>(ws + rec_bytes(b.BH, P, D) + vec_bytes(b.BH, b.n, D));
+  const int BH = b.BH, n = b.n;
+  hipError_t e;
+  // r = LA+(q, k, k),  u = LA-(v, g, q)
+  if ((e = la_pass<D, false, false, false>("bwd_r", b.q, b.k, b.k, r, rec, BH, n, P, cps, 0, 0, s)) != hipSuccess)
+    return e;
+  if ((e = la_pass<D, false, true, false>("bwd_u", b.v, b.g, b.q, u, rec, BH, n, P, cps, 1, 0, s)) != hipSuccess)
+    return e;
+  // dq = LA+(g, v, r) + LA+(u, k, k)
+  if ((e = la_pass<D, true, false, true>("bwd_dq", b.g, b.v, r, b.dq, rec, BH, n, P, cps, 0, 0, s)) != hipSuccess)
+    return e;
+  if ((e = la_pass<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, rec, BH, n, P, cps, 0, 1, s)) != hipSuccess)
+    return e;
+  // dv = LA-(r, q, g)
+  if ((e = la_pass<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, rec, BH, n, P, cps, 1, 0, s)) != hipSuccess)
+    return e;
+  // dk = LA-(k, q, u) + LA-(k, u, q)
+  if ((e = la_pass<D, false, false, true>("bwd_dk", b.k, b.q, u, b.dk, rec, BH, n, P, cps, 1, 0, s)) != hipSuccess)
+    return e;
+  return la_pass<D, false, true, false>("bwd_dk", b.k, u, b.q, b.dk, rec, BH, n, P, cps, 1, 1, s);
+}
+
+}  // namespace
+
+bool backward_supported(int n, int d, int dv, int dtype) {
+  const long long span = (long long)n * d * 4;   // per-head byte offsets stay below 2^31
+  return dtype == 1 && n >= 1 && d == dv && (d == 64 || d == 128) && span < (1LL << 31);
+}
+
+size_t backward_workspace_bytes(int BH, int n, int d) {
+  int P, cps;
+  la_plan(d, BH, n, &P, &cps);
+  return rec_bytes(BH, P, d) + 2 * vec_bytes(BH, n, d) + 256;
+}
+
+hipError_t launch_backward(const Bwd& b, void* workspace, hipStream_t s) {
+  if (!backward_supported(b.n, b.d, b.dvd, b.dtype)) return hipErrorNotSupported;
+  char* ws = static_cast<char*>(workspace);
+  return b.d == 64 ? run_backward<64>(b, ws, s) : run_backward<128>(b, ws, s);
+}
+
+}  // namespace hla

@@ -7,6 +7,7 @@
 
 #include "../../include/hla.h"
 #include "ahla.h"
+#include "backward.h"
 #include "common.h"
 #include "fused.h"
 #include "hla3.h"
@@ -196,6 +197,32 @@ int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, 
   if (e != hipSuccess) return hip_fail(e, "scan");
   e = HLA_PROF("readout", s, hla::launch_readout(f, prefix, s));
   if (e != hipSuccess) return hip_fail(e, "readout");
+  return ok();
+}
+
+size_t hla2_backward_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || !hla::backward_supported(n, d, dv, dtype)) return 0;
+  return hla::backward_workspace_bytes(B * H, n, d);
+}
+
+int hla2_backward(const void* q, const void* k, const void* v, const float* g, float* dq, float* dk, float* dv,
+                  int B, int H, int n, int d, int dv_dim, int chunk, int dtype, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv_dim, chunk, dtype, true)) != HLA_OK) return rc;
+  if (!hla::backward_supported(n, d, dv_dim, dtype))
+    return fail(HLA_ERR_UNSUPPORTED, "the backward covers bf16 q/k/v with d = dv in {64, 128} (got d=%d dv=%d dtype=%d)",
+                d, dv_dim, dtype);
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) || (rc = check_ptr(g, "g")) ||
+      (rc = check_ptr(dq, "dq")) || (rc = check_ptr(dk, "dk")) || (rc = check_ptr(dv, "dv")))
+    return rc;
+  const int BH = B * H;
+  const size_t need = hla::backward_workspace_bytes(BH, n, d);
+  if (!workspace || workspace_bytes < need)
+    return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  hla::Bwd b{q, k, v, g, dq, dk, dv, BH, n, d, dv_dim, dtype};
+  const hipError_t e = hla::launch_backward(b, workspace, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "backward");
   return ok();
 }
 

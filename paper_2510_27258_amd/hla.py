@@ -138,6 +138,48 @@ def forward_decay(q, k, v, chunk, gamma, masked=True, normalized=False, eps=1e-6
     return out
 
 
+def backward(q, k, v, g, chunk=64, workspace=None):
+    """Gradients (dq, dk, dv), fp32, of the masked unnormalised second-order HLA
+    for upstream gradient g [B,H,n,dv] fp32; q, k, v [B,H,n,d] bf16."""
+    g = g.float().contiguous()
+    _check(q, k, v, g)
+    B, H, n, d = q.shape
+    dv_dim = v.shape[-1]
+    code = _code(q)
+    dq = torch.empty(B, H, n, d, dtype=torch.float32, device=q.device)
+    dk = torch.empty_like(dq)
+    dv = torch.empty(B, H, n, dv_dim, dtype=torch.float32, device=q.device)
+    wsb = capi.hla2_backward_workspace_bytes(B, H, n, d, dv_dim, chunk, code)
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    capi.hla2_backward(q.data_ptr(), k.data_ptr(), v.data_ptr(), g.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                       dv.data_ptr(), B, H, n, d, dv_dim, chunk, code, workspace.data_ptr(), workspace.numel(),
+                       _stream())
+    return dq, dk, dv
+
+
+class HLA2(torch.autograd.Function):
+    """Masked second-order HLA as a differentiable op: forward by the library's
+    forward, backward by hla2_backward (bf16 q, k, v; fp32 output)."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, chunk):
+        ctx.save_for_backward(q, k, v)
+        ctx.chunk = chunk
+        return forward(q, k, v, chunk)
+
+    @staticmethod
+    def backward(ctx, g):
+        q, k, v = ctx.saved_tensors
+        dq, dk, dv = backward(q, k, v, g, ctx.chunk)
+        return dq.to(q.dtype), dk.to(k.dtype), dv.to(v.dtype), None
+
+
+def hla2_attention(q, k, v, chunk=64):
+    """Differentiable masked second-order HLA (see HLA2)."""
+    return HLA2.apply(q, k, v, chunk)
+
+
 def ahla_forward(q, k, v, chunk, normalized=False, eps=1e-6, out=None, workspace=None):
     """AHLA (Sec. 6), ((A A) (.) L) V with A = L (.) Q K^T; q, k, v [B,H,n,d] bf16 -> out fp32."""
     _check(q, k, v)

@@ -37,6 +37,12 @@ def draw_qkv(B, H, n, d, dv, dist, seed):
     raise ValueError(f"unknown dist {dist!r}")
 
 
+def draw_grad(B, H, n, dv, seed):
+    """Upstream gradient dL/dout for the backward: float32 standard normals
+    [B,H,n,dv] from default_rng(seed), kept float32."""
+    return np.random.default_rng(seed).standard_normal((B, H, n, dv), dtype=np.float32)
+
+
 def round_bf16(x):
     """float32 -> nearest bfloat16 (ties to even), returned as float32."""
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16).float().numpy()
