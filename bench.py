@@ -124,6 +124,8 @@ def kernel_key(name):
     """Bench name of a library kernel from its (demangled) dispatch name."""
     if "k_ahla_walk" in name:
         return "ahla_walk"
+    if "k_la<" in name or "k_laI" in name:
+        return "bwd_pass"
     if "k_walk" in name:
         return "walk_summary" if ("true" in name or "Lb1E" in name) else "walk"
     for key in ("k_init_convert", "k_total", "k_moments", "k_carry", "k_fix", "k_scan", "k_chunk_summary", "k_readout",
@@ -379,6 +381,63 @@ def measure_ahla(reps=10):
                          "mfma_frac": flops / s / 1e12 / BF16_MFMA_PEAK_TFLOPS}}
 
 
+# Per-token HBM bytes / d of each linear-attention pass of the backward: x, y, z
+# read (bf16 2 B or fp32 4 B per element), the output written (4 B), and read
+# back (4 B) when the pass adds to it.  Passes that share a name are averaged.
+BWD_PASS_BYTES = {"bwd_r": [2 + 2 + 2 + 4], "bwd_u": [2 + 4 + 2 + 4], "bwd_dq": [4 + 2 + 4 + 4, 4 + 2 + 2 + 8],
+                  "bwd_dv": [4 + 2 + 4 + 4], "bwd_dk": [2 + 2 + 4 + 4, 2 + 4 + 2 + 8]}
+
+
+def measure_backward(reps=10):
+    """hla2_backward on the B4 H16 n4096 d=dv=64 bf16 shape (upstream gradient
+    fp32): gradient tokens/s by HIP events, per-pass times, and the slowest pass
+    against HBM (its operands read once, its output written once) and against
+    the bf16 MFMA peak with the dense first-order chunk-form count
+    2 (2 C d + 2 d^2) per token."""
+    import torch
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
+    from paper_2510_27258_amd import inputs as I
+    name = "hla2-masked-bf16-B4H16-n4096-d64-C64"
+    w = I.WORKLOADS[name]
+    B, H, n, d = w["B"], w["H"], w["n"], w["d"]
+    q, k, v, code = I.draw_qkv(B, H, n, d, w["dv"], w["dist"], w["seed"])
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    g = torch.from_numpy(I.draw_grad(B, H, n, w["dv"], 1)).to(dev)
+    wsb = capi.hla2_backward_workspace_bytes(B, H, n, d, w["dv"], w["chunk"], code)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    run = lambda: hla.backward(qd, kd, vd, g, w["chunk"], workspace=ws)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    capi.hla_profile_begin(32 * reps + 8)
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    prof = capi.hla_profile_summary()
+    capi.hla_profile_end()
+    kms = {k_: v_[1] / v_[0] for k_, v_ in prof.items()}
+    tokens = B * H * n
+    dom = max((k_ for k_ in kms if k_ in BWD_PASS_BYTES), key=lambda k_: kms[k_])
+    nbytes = tokens * d * sum(BWD_PASS_BYTES[dom]) / len(BWD_PASS_BYTES[dom])
+    flops = tokens * 2 * (2 * 64 * d + 2 * d * d)
+    s = kms[dom] / 1e3
+    return {"workload": name + " backward", "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms,
+            "dtype": "bf16", "kernels_ms": kms,
+            "roofline": {"kernel": dom, "bound": "hbm", "achieved": nbytes / s / 1e9, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": nbytes / s / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes,
+                         "algorithmic_flops": flops, "mfma_tflops": flops / s / 1e12,
+                         "mfma_frac": flops / s / 1e12 / BF16_MFMA_PEAK_TFLOPS}}
+
+
 def measure_decode(steps=None):
     """hla2_step on the decode workload: state from a prefill of the seeded
     2048-token prefix, then the seeded step tokens, one launch per step."""
@@ -430,7 +489,8 @@ def main():
     ap.add_argument("--no-hla3", action="store_true", help="skip the third-order measurement")
     ap.add_argument("--no-decay", action="store_true", help="skip the decayed-forward measurement")
     ap.add_argument("--no-ahla", action="store_true", help="skip the AHLA measurement")
-    ap.add_argument("--only", choices=["ahla", "decay", "hla3"],
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
+    ap.add_argument("--only", choices=["ahla", "decay", "hla3", "backward"],
                     help="run only that measurement and print its record (for profiling one path)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
@@ -459,7 +519,8 @@ def main():
         return
 
     if args.only:
-        rec = {"ahla": measure_ahla, "decay": measure_decay, "hla3": measure_hla3}[args.only]()
+        rec = {"ahla": measure_ahla, "decay": measure_decay, "hla3": measure_hla3,
+               "backward": measure_backward}[args.only]()
         print(json.dumps(rec), flush=True)
         return
 
@@ -546,6 +607,8 @@ def main():
         rec["decay"] = measure_decay()
     if not args.no_ahla:
         rec["ahla"] = measure_ahla()
+    if not args.no_backward:
+        rec["backward"] = measure_backward()
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
     if not args.no_decode:
