@@ -73,7 +73,7 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
     float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, int n, int cps, int nseg,
     int normalized) {
   using G = CfgAH<D>;
-  constexpr bool kO = D == 128;     // opaque lane index: keeps LDS addresses from being hoisted (registers)
+  constexpr bool kO = D == 128;     // per-tile opaque lane index (registers)
   constexpr int C = G::C, DV = G::DV, NT = G::NT, ST = G::ST;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
@@ -164,6 +164,11 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
 
   for (int c = c_begin; c < c_end; ++c) {
     const int t0 = c * C;
+    // lane index for the fragment helpers, opaque once per tile at d = 128:
+    // lane offsets are formed once per tile and no address is hoisted out of
+    // the walk
+    int ln = tid & 63;
+    if constexpr (kO) asm volatile("" : "+v"(ln));
     // ---- stage 0: registers -> LDS, row-major (transposed operands go through the transpose unit) ----
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
@@ -188,7 +193,7 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
         f32x16 acc = zero16();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
-          acc = mfma(frag<kO>(Ks, G::ldK, it * 32, s * 16), frag<kO>(Qs, G::ldQ, jt * 32, s * 16), acc);
+          acc = mfma(frag<kO>(Ks, G::ldK, it * 32, s * 16, ln), frag<kO>(Qs, G::ldQ, jt * 32, s * 16, ln), acc);
 #pragma unroll
         for (int e = 0; e < 16; ++e)   // keep key i <= query t
           if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
@@ -199,7 +204,7 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
           ps += __shfl_xor(ps, 32);
           if (lg == 0) rs[it * C + jt * 32 + lr] = ps;
         }
-        store_T<kO>(acc, Wh, Wl, G::ldW, it * 32, jt * 32);
+        store_T<kO>(acc, Wh, Wl, G::ldW, it * 32, jt * 32, ln);
       } else if (normalized && lg == 0) {
         rs[it * C + jt * 32 + lr] = 0.f;
       }
@@ -230,7 +235,7 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
       bf16x8 ph, pl, eh, el;
       frag_from_acc(P0[j >> 1], j & 1, ph, pl);
       frag_from_acc(E0[j >> 1], j & 1, eh, el);
-      const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, j * 16);
+      const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, j * 16, ln);
       racc = mfma(aQ, ph, racc);
       racc = mfma(aQ, pl, racc);
       oacc = mfma(aQ, eh, oacc);
@@ -238,15 +243,15 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
     }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16);
+      const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16, ln);
       if (s < 2 * (rt + 1)) {           // keys past the row tile: A is zero
-        racc = mfma(frag<kO>(Wh, G::ldW, rt * 32, s * 16), bV, racc);
-        racc = mfma(frag<kO>(Wl, G::ldW, rt * 32, s * 16), bV, racc);
+        racc = mfma(frag<kO>(Wh, G::ldW, rt * 32, s * 16, ln), bV, racc);
+        racc = mfma(frag<kO>(Wl, G::ldW, rt * 32, s * 16, ln), bV, racc);
       }
 #pragma unroll
-      for (int i = 0; i < ST; ++i) P0[i] = mfma(frag_tr<kO>(Ks, G::ldK, i * 32, s * 16), bV, P0[i]);
+      for (int i = 0; i < ST; ++i) P0[i] = mfma(frag_tr<kO>(Ks, G::ldK, i * 32, s * 16, ln), bV, P0[i]);
     }
-    store_T<kO>(racc, Rh, Rl, G::ldR, rt * 32, ct * 32);     // R^T
+    store_T<kO>(racc, Rh, Rl, G::ldR, rt * 32, ct * 32, ln);     // R^T
     lds_barrier();                      // R^T and s visible; Q and V are dead
 
     // ---- normalised: den partial (A s)_t, the tile's n0, then m0 and n0 advance ----
@@ -285,17 +290,17 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
     // ---- stage 3: E0 += K^T R;  O += A R (A and R both split: hi hi, hi lo, lo hi) ----
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 brh = frag<kO>(Rh, G::ldR, ct * 32, s * 16);
-      const bf16x8 brl = frag<kO>(Rl, G::ldR, ct * 32, s * 16);
+      const bf16x8 brh = frag<kO>(Rh, G::ldR, ct * 32, s * 16, ln);
+      const bf16x8 brl = frag<kO>(Rl, G::ldR, ct * 32, s * 16, ln);
 #pragma unroll
       for (int i = 0; i < ST; ++i) {
-        const bf16x8 aK = frag_tr<kO>(Ks, G::ldK, i * 32, s * 16);
+        const bf16x8 aK = frag_tr<kO>(Ks, G::ldK, i * 32, s * 16, ln);
         E0[i] = mfma(aK, brh, E0[i]);
         E0[i] = mfma(aK, brl, E0[i]);
       }
       if (s < 2 * (rt + 1)) {
-        const bf16x8 awh = frag<kO>(Wh, G::ldW, rt * 32, s * 16);
-        const bf16x8 awl = frag<kO>(Wl, G::ldW, rt * 32, s * 16);
+        const bf16x8 awh = frag<kO>(Wh, G::ldW, rt * 32, s * 16, ln);
+        const bf16x8 awl = frag<kO>(Wl, G::ldW, rt * 32, s * 16, ln);
         oacc = mfma(awh, brh, oacc);
         oacc = mfma(awh, brl, oacc);
         oacc = mfma(awl, brh, oacc);

@@ -625,15 +625,13 @@ struct CfgRS {
 // Exchange slot of (column tile ct, row tile rt): 32 x 32 fp32 in MFMA
 // accumulator order, element 4q + j of lane l at [(slot * 4 + q) * 64 + l] * 4 + j.
 template <bool O = false>
-__device__ __forceinline__ void xch_put(float* X, int slot, const f32x16& a) {
-  const int l = lane64<O>();
+__device__ __forceinline__ void xch_put(float* X, int slot, const f32x16& a, int l = lane64<O>()) {
 #pragma unroll
   for (int q = 0; q < 4; ++q)
     *reinterpret_cast<float4*>(X + ((slot * 4 + q) * 64 + l) * 4) = make_float4(a[4 * q], a[4 * q + 1], a[4 * q + 2], a[4 * q + 3]);
 }
 template <bool O = false>
-__device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a) {
-  const int l = lane64<O>();
+__device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a, int l = lane64<O>()) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float4 u = *reinterpret_cast<const float4*>(X + ((slot * 4 + q) * 64 + l) * 4);
@@ -734,6 +732,12 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 
   for (int c = c_begin; c < c_end; ++c) {
     const int t0 = c * C;
+    // lane index for the fragment helpers: at d = 128 it is made opaque once
+    // per tile, so the lane-dependent offsets are computed once per tile and
+    // every access adds only a constant, while none is hoisted out of the
+    // walk (held live through it, they would spill)
+    int ln = tid & 63;
+    if constexpr (kO) asm volatile("" : "+v"(ln));
     // ---- stage 0: registers -> LDS (Q, K, V row-major; the transposed operands are read through the
     // LDS transpose unit) ----
 #pragma unroll
@@ -759,11 +763,11 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         f32x16 acc = zero16();
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
-          acc = mfma(frag<kO>(Ks, G::ldK, it * 32, s * 16), frag<kO>(Qs, G::ldQ, jt * 32, s * 16), acc);
+          acc = mfma(frag<kO>(Ks, G::ldK, it * 32, s * 16, ln), frag<kO>(Qs, G::ldQ, jt * 32, s * 16, ln), acc);
 #pragma unroll
         for (int e = 0; e < 16; ++e)   // keep key i <= query t
           if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
-        store_T<kO>(acc, Wh, Wl, G::ld1, it * 32, jt * 32);
+        store_T<kO>(acc, Wh, Wl, G::ld1, it * 32, jt * 32, ln);
       }
     }
     lds_barrier();
@@ -778,32 +782,32 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       frag_from_acc(S0[j >> 1], j & 1, bh_, bl_);
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, r0 + j * 16);
+        const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, r0 + j * 16, ln);
         part[rt] = mfma(aQ, bh_, part[rt]);
         part[rt] = mfma(aQ, bl_, part[rt]);
       }
     }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bK = frag_tr<kO>(Ks, G::ldK, ct * 32, s * 16);
+      const bf16x8 bK = frag_tr<kO>(Ks, G::ldK, ct * 32, s * 16, ln);
       if (h == 0) {
         if (s < 2) {
-          part[0] = mfma(frag<kO>(Wh, G::ld1, 0, s * 16), bK, part[0]);
-          part[0] = mfma(frag<kO>(Wl, G::ld1, 0, s * 16), bK, part[0]);
+          part[0] = mfma(frag<kO>(Wh, G::ld1, 0, s * 16, ln), bK, part[0]);
+          part[0] = mfma(frag<kO>(Wl, G::ld1, 0, s * 16, ln), bK, part[0]);
         }
       } else {
-        part[1] = mfma(frag<kO>(Wh, G::ld1, 32, s * 16), bK, part[1]);
-        part[1] = mfma(frag<kO>(Wl, G::ld1, 32, s * 16), bK, part[1]);
+        part[1] = mfma(frag<kO>(Wh, G::ld1, 32, s * 16, ln), bK, part[1]);
+        part[1] = mfma(frag<kO>(Wl, G::ld1, 32, s * 16, ln), bK, part[1]);
       }
       // S0 += K^T K on this wave's rows
 #pragma unroll
-      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16), bK, S0[i]);
+      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16, ln), bK, S0[i]);
     }
     lds_barrier();                      // K, K^T and W are dead: K | K^T takes the exchange
-    xch_put<kO>(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0]);
+    xch_put<kO>(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0], ln);
     lds_barrier();
     f32x16 racc = h == 0 ? part[0] : part[1];
-    xch_add<kO>(XR, ct * 2 + h, racc);
+    xch_add<kO>(XR, ct * 2 + h, racc, ln);
     {
       float cs = 0.f;
 #pragma unroll
@@ -811,7 +815,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       cs += __shfl_xor(cs, 32);
       if (lg == 0) colsum[h * D + ct * 32 + lr] = cs;
     }
-    store_T<kO>(racc, Wh, Wl, G::ld1, h * 32, ct * 32);     // R^T
+    store_T<kO>(racc, Wh, Wl, G::ld1, h * 32, ct * 32, ln);     // R^T
     lds_barrier();
     float eta_add = 0.f;
     if (tid < D) eta_add = colsum[tid] + colsum[D + tid];
@@ -825,9 +829,9 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
           f32x16 acc = zero16();
 #pragma unroll
           for (int s = 0; s < D / 16; ++s) {
-            const bf16x8 b = frag<kO>(Qs, G::ldQ, jt * 32, s * 16);
-            acc = mfma(frag_tr<kO>(Wh, G::ld1, it * 32, s * 16), b, acc);
-            acc = mfma(frag_tr<kO>(Wl, G::ld1, it * 32, s * 16), b, acc);
+            const bf16x8 b = frag<kO>(Qs, G::ldQ, jt * 32, s * 16, ln);
+            acc = mfma(frag_tr<kO>(Wh, G::ld1, it * 32, s * 16, ln), b, acc);
+            acc = mfma(frag_tr<kO>(Wl, G::ld1, it * 32, s * 16, ln), b, acc);
           }
 #pragma unroll
           for (int e = 0; e < 16; ++e)     // keep j <= t
@@ -837,7 +841,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
           for (int e = 0; e < 16; ++e) ps += acc[e];
           ps += __shfl_xor(ps, 32);
           if (lg == 0) denp[it * C + jt * 32 + lr] = ps;
-          store_T<kO>(acc, Th, Tl, G::ldT, it * 32, jt * 32);
+          store_T<kO>(acc, Th, Tl, G::ldT, it * 32, jt * 32, ln);
         } else if (lg == 0) {
           denp[it * C + jt * 32 + lr] = 0.f;
         }
@@ -851,7 +855,7 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         frag_from_acc(P0[j >> 1], j & 1, bh_, bl_);
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-          const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, r0 + j * 16);
+          const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, r0 + j * 16, ln);
           oacc[rt] = mfma(aQ, bh_, oacc[rt]);
           oacc[rt] = mfma(aQ, bl_, oacc[rt]);
         }
@@ -860,16 +864,16 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     // ---- stage 5: Phi0 += R^T V on this wave's rows ----
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
-      const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16);
+      const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16, ln);
 #pragma unroll
       for (int i = 0; i < G::HT; ++i) {
-        P0[i] = mfma(frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
-        P0[i] = mfma(frag<kO>(Wl, G::ld1, r0 + i * 32, s * 16), bV, P0[i]);
+        P0[i] = mfma(frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16, ln), bV, P0[i]);
+        P0[i] = mfma(frag<kO>(Wl, G::ld1, r0 + i * 32, s * 16, ln), bV, P0[i]);
       }
     }
     if (!SUMMARY) {
       lds_barrier();                    // T and denp visible; R and R^T are dead
-      xch_put<kO>(XO, ct * 2 + (1 - h), h == 0 ? oacc[1] : oacc[0]);
+      xch_put<kO>(XO, ct * 2 + (1 - h), h == 0 ? oacc[1] : oacc[0], ln);
       // den_t = sum_j T[t][j] + q_t . eta0: the row sums here, and eta0 of this
       // tile (before its advance) for k_fix, which adds q_t . (eta0 + eta_c)
       if (normalized) {
@@ -878,14 +882,14 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       }
       lds_barrier();
       f32x16 o = h == 0 ? oacc[0] : oacc[1];
-      xch_add<kO>(XO, ct * 2 + h, o);
+      xch_add<kO>(XO, ct * 2 + h, o, ln);
       // ---- stage 4b: O (row tile h) += T V ----
 #pragma unroll
       for (int s = 0; s < G::KC; ++s) {
         if (h == 0 && s >= 2) break;      // j past row tile 0: T is zero
-        const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16);
-        o = mfma(frag<kO>(Th, G::ldT, h * 32, s * 16), bV, o);
-        o = mfma(frag<kO>(Tl, G::ldT, h * 32, s * 16), bV, o);
+        const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16, ln);
+        o = mfma(frag<kO>(Th, G::ldT, h * 32, s * 16, ln), bV, o);
+        o = mfma(frag<kO>(Tl, G::ldT, h * 32, s * 16, ln), bV, o);
       }
       // the output tile goes through this wave's own exchange slot (its last
       // reader was this wave's xch_add) so that each lane stores 16 bytes:

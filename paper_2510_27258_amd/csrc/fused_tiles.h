@@ -90,8 +90,7 @@ __device__ __forceinline__ int lane64() {
 // Operand fragment from a row-major bf16 LDS tile X[row][k]: lane takes
 // X[row0 + r][k0 + 8g .. 8g+7].  A operand of X Y, or B operand of Z X^T.
 template <bool O = false>
-__device__ __forceinline__ bf16x8 frag(const uint16_t* X, int ld, int row0, int k0) {
-  const int l = lane64<O>();
+__device__ __forceinline__ bf16x8 frag(const uint16_t* X, int ld, int row0, int k0, int l = lane64<O>()) {
   const uint16_t* p = X + (row0 + (l & 31)) * ld + k0 + 8 * (l >> 5);
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 }
@@ -99,8 +98,7 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* X, int ld, int row0, int 
 // Same, in the k order of an accumulator-fed partner: lane takes
 // X[row0 + r][k0 + 4g .. 4g+3] and X[row0 + r][k0 + 8 + 4g .. 8+4g+3].
 template <bool O = false>
-__device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int row0, int k0) {
-  const int l = lane64<O>();
+__device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int row0, int k0, int l = lane64<O>()) {
   const uint16_t* p = X + (row0 + (l & 31)) * ld + k0 + 4 * (l >> 5);
   const uint2 a = *reinterpret_cast<const uint2*>(p);
   const uint2 b = *reinterpret_cast<const uint2*>(p + 8);
@@ -116,10 +114,9 @@ __device__ __forceinline__ bf16x8 frag_acc_order(const uint16_t* X, int ld, int 
 // give the 8 rows of a fragment.  (Layout checked on the device by an
 // in-bounds probe.)  Y and ld must keep 8-byte alignment (ld % 4 == 0).
 template <bool O = false>
-__device__ __forceinline__ bf16x8 frag_tr(const uint16_t* Y, int ld, int n0, int k0) {
+__device__ __forceinline__ bf16x8 frag_tr(const uint16_t* Y, int ld, int n0, int k0, int l = lane64<O>()) {
   typedef short v4i16 __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-  const int l = lane64<O>();
   const int grp = l >> 4, j = l & 15;
   const uint16_t* p = Y + (k0 + 8 * (grp >> 1) + (j >> 2)) * ld + n0 + 16 * (grp & 1) + 4 * (j & 3);
   const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
@@ -142,8 +139,7 @@ __device__ __forceinline__ void frag_from_acc(const f32x16& t, int h, bf16x8& hi
 // Store an accumulator tile D[row0 + i][col0 + r] transposed as X[col0 + r][row0 + i],
 // split into hi/lo tiles (four 8-byte stores each).
 template <bool O = false>
-__device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
-  const int l = lane64<O>();
+__device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0, int l = lane64<O>()) {
   const int g = l >> 5;
   const int base = (col0 + (l & 31)) * ld + row0 + 4 * g;
 #pragma unroll
@@ -158,8 +154,7 @@ __device__ __forceinline__ void store_T(const f32x16& acc, uint16_t* Xh, uint16_
 
 // Store an accumulator tile row-major as X[row0 + i][col0 + r], hi/lo.
 template <bool O = false>
-__device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0) {
-  const int l = lane64<O>();
+__device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_t* Xl, int ld, int row0, int col0, int l = lane64<O>()) {
   const int g = l >> 5;
 #pragma unroll
   for (int e = 0; e < 16; e += 2) {
