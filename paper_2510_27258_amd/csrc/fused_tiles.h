@@ -254,31 +254,55 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
       if (c + 3 < c1) step(c + 3, std::integral_constant<int, 3>());
     }
   }
-  for (int c = want_cm ? c0 : c1; c < c1; ++c) {
-    const uint32_t t0 = (uint32_t)c * C;
-    for (int e = tid; e < segQ; e += kThreads) {        // consecutive lanes take consecutive tokens
-      const int t = e % C, a8 = (e / C) * 8;
+  // with C (and m): the next tile's k, q, v pieces are loaded into registers
+  // while the current one is multiplied (loads unconditional: piece and tile
+  // indices are clamped, only owners store)
+  constexpr int NLK = (segQ + kThreads - 1) / kThreads, NLV = (segV + kThreads - 1) / kThreads;
+  uint4 pk_[NLK], pq_[NLK], pv_[NLV];
+  auto fetch_cm = [&](int c) {
+    const uint32_t t0 = (uint32_t)min(c, c1 - 1) * C;
+#pragma unroll
+    for (int i = 0; i < NLK; ++i) {
+      const int e = min(tid + kThreads * i, segQ - 1), t = e % C, a8 = (e / C) * 8;   // consecutive lanes take consecutive tokens
       const uint32_t off = ((t0 + t) * D + a8) * 2;
-      const uint4 kk = buf_load16(rk, off);
-      const uint16_t* k8 = reinterpret_cast<const uint16_t*>(&kk);
+      pk_[i] = buf_load16(rk, off);
+      if (!KV) pq_[i] = buf_load16(rq, off);
+    }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
-      if (want_cm && !KV) {
-        const uint4 qq = buf_load16(rq, off);
-        const uint16_t* q8 = reinterpret_cast<const uint16_t*>(&qq);
+    for (int i = 0; i < NLV; ++i) {
+      const int e = min(tid + kThreads * i, segV - 1), t = e % C, b8 = (e / C) * 8;
+      pv_[i] = buf_load16(rv, ((t0 + t) * DV + b8) * 2);
+    }
+  };
+  if (want_cm && c0 < c1) fetch_cm(c0);
+  for (int c = want_cm ? c0 : c1; c < c1; ++c) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) Qt[(a8 + j) * ld + t] = q8[j];
+    for (int i = 0; i < NLK; ++i) {
+      const int e = tid + kThreads * i;
+      if (e < segQ) {
+        const int t = e % C, a8 = (e / C) * 8;
+        const uint16_t* k8 = reinterpret_cast<const uint16_t*>(&pk_[i]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
+        if (!KV) {
+          const uint16_t* q8 = reinterpret_cast<const uint16_t*>(&pq_[i]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) Qt[(a8 + j) * ld + t] = q8[j];
+        }
       }
     }
-    if (want_cm)
-      for (int e = tid; e < segV; e += kThreads) {
+#pragma unroll
+    for (int i = 0; i < NLV; ++i) {
+      const int e = tid + kThreads * i;
+      if (e < segV) {
         const int t = e % C, b8 = (e / C) * 8;
-        const uint4 vv = buf_load16(rv, ((t0 + t) * DV + b8) * 2);
-        const uint16_t* v8 = reinterpret_cast<const uint16_t*>(&vv);
+        const uint16_t* v8 = reinterpret_cast<const uint16_t*>(&pv_[i]);
 #pragma unroll
         for (int j = 0; j < 8; ++j) Vt[(b8 + j) * ld + t] = v8[j];
       }
+    }
     lds_barrier();
+    if (c + 1 < c1) fetch_cm(c + 1);
 #pragma unroll
     for (int i = 0; i < nS; ++i) {
       const int ti = w + kWaves * i;
