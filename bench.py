@@ -275,11 +275,11 @@ def measure_hla3(reps=20):
             "kernels_ms": {k_: v_[1] / v_[0] for k_, v_ in prof.items()}}
 
 
-def measure_decay(reps=5):
+def measure_decay(reps=10):
     """hla2_forward_decay on the decayed workload (B4 H16 n4096 d=dv=64, bf16,
-    chunk 64, gamma 0.99; fp32 SIMT arithmetic on the chunked path): tokens/s
-    by HIP events, per-kernel times, and the dominant kernel against the fp32
-    vector peak with its chunk-form flop count."""
+    chunk 64, gamma 0.99): tokens/s by HIP events, per-kernel times, and the
+    fused walk against HBM (q, k, v read once, out written once) and against
+    the bf16 MFMA peak with the undecayed dense reference flop count."""
     import torch
     import paper_2510_27258_amd as hla
     from paper_2510_27258_amd import capi
@@ -293,7 +293,7 @@ def measure_decay(reps=5):
     wsb = capi.hla2_forward_decay_workspace_bytes(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], code)
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
     run = lambda: hla.forward_decay(qd, kd, vd, w["chunk"], w["gamma"], out=out, workspace=ws)
-    for _ in range(2):
+    for _ in range(3):
         run()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -310,20 +310,17 @@ def measure_decay(reps=5):
     prof = capi.hla_profile_summary()
     capi.hla_profile_end()
     kms = {k_: v_[1] / v_[0] for k_, v_ in prof.items()}
-    # chunk-form flops per launch (fp32, counted densely as written; the
-    # triangles are not halved): summary 2 C (C d + C dv + d^2 + 2 d dv) per
-    # chunk, readout 2 C (d^2 + 2 C d + d dv + C dv) per chunk
-    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], min(w["chunk"], 64)
-    chunks = B * H * (-(-n // C))
-    flops = {"chunk_summary": chunks * 2 * C * (C * d + C * dv + d * d + 2 * d * dv),
-             "readout": chunks * 2 * C * (d * d + 2 * C * d + d * dv + C * dv)}
-    dom = max((k_ for k_ in kms if k_ in flops), key=lambda k_: kms[k_])
-    achieved = flops[dom] / (kms[dom] / 1e3) / 1e12
+    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
     tokens = B * H * n
-    return {"workload": name, "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms, "dtype": "f32",
+    nbytes = tokens * (2 * (2 * d + dv) + 4 * dv)
+    flops = tokens * reference_flops_per_token(C, d, dv)
+    s = kms["walk"] / 1e3
+    return {"workload": name, "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms, "dtype": "bf16",
             "gamma": w["gamma"], "kernels_ms": kms,
-            "roofline": {"kernel": dom, "bound": "alu", "achieved": achieved, "peak": FP32_VALU_PEAK_TFLOPS,
-                         "unit": "TFLOP/s", "frac": achieved / FP32_VALU_PEAK_TFLOPS}}
+            "roofline": {"kernel": "walk", "bound": "hbm", "achieved": nbytes / s / 1e9, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": nbytes / s / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes,
+                         "algorithmic_flops": flops, "mfma_tflops": flops / s / 1e12,
+                         "mfma_frac": flops / s / 1e12 / BF16_MFMA_PEAK_TFLOPS}}
 
 
 def ahla_flops_per_token(C, d, dv):

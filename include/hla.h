@@ -158,11 +158,15 @@ int hla2_step(float *state, const void *q_t, const void *k_t, const void *v_t, f
  * the pairs j < i of the unmasked decayed output and whose concatenation,
  * with rho^2 on G and h, is associative).  normalized divides by the same
  * sum without v_j, plus eps.  gamma = 1 is hla2_forward's operator.
- * Computed in fp32 on the chunked path (decayed chunk summaries, the
- * decayed (+)-scan, decayed readout).  Arguments as hla2_forward, plus
+ * bf16 inputs, masked, d = dv in {64, 128}, chunk 64 or 128 run on the fused
+ * segment walk with decay (bf16 MFMA, every decay factor applied in fp32 before
+ * the hi/lo split); everything else on the chunked path in fp32 (decayed
+ * chunk summaries, the decayed (+)-scan, decayed readout).  Arguments as
+ * hla2_forward, plus
  * gamma, finite, 0 < gamma <= 1 (else HLA_ERR_INVALID); gamma^(2*chunk) must
  * stay a normal fp32 number (gamma >= 0.51 at chunk 64; HLA_ERR_UNSUPPORTED
- * otherwise).  workspace: hla2_forward_decay_workspace_bytes(...) bytes.
+ * otherwise).  workspace: hla2_forward_decay_workspace_bytes(...) bytes (enough
+ * for either path).
  * ------------------------------------------------------------------------- */
 size_t hla2_forward_decay_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
 int hla2_forward_decay(const void *q, const void *k, const void *v, float *out,

@@ -367,7 +367,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
   hipError_t e;
   if (P > 1) {
     prof_start("ahla_moments", s);
-    HLA_LAUNCH((k_moments<C, D, D, true>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1);
+    HLA_LAUNCH((k_moments<C, D, D, true>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1, 0.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -382,7 +382,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
   if (P > 1 || f.normalized) {
     prof_start("ahla_carry", s);
     HLA_LAUNCH((k_carry<D, D>), dim3((D * D / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs,
-                       (const float*)nullptr, carry, P);
+                       (const float*)nullptr, carry, P, 1.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     using FC = FixCfg<C, D, D>;
@@ -392,7 +392,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
     const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("ahla_fix", s);
     HLA_LAUNCH((k_fix<C, D, D>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
-                       carry, 0, f.n, cps, P, f.normalized, f.eps, tpw);
+                       carry, 0, f.n, cps, P, f.normalized, f.eps, tpw, 0.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }

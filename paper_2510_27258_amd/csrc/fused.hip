@@ -42,6 +42,8 @@
 // as the B operand straight from registers (with two row waves per column
 // both keep a copy).  Q, K, K^T, V^T, W/T, R and R^T are staged in LDS as
 // bf16.
+#include <cmath>
+
 #include "fused.h"
 #include "fused_tiles.h"
 #include "profile.h"
@@ -271,7 +273,7 @@ template <int C, int D, int DV, bool SUMMARY>
 __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k_walk(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ init,
-    int n, int cps, int nseg, int normalized, float eps) {
+    int n, int cps, int nseg, int normalized, float eps, float lg2g) {
   using G = Cfg<C, D, DV, SUMMARY>;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
@@ -613,7 +615,8 @@ struct CfgRS {
   static_assert(SUMMARY || 2 * xfl <= 2 * C * ld2, "O exchange fits its buffer");
   static_assert(C * ldV <= DV * (C + kPad), "V fits its buffer");
   static constexpr int f_eta = 0, f_cs = D, f_den = D + RT * D, f_denp = f_den + C;
-  static constexpr int nf32 = f_denp + RT * C;
+  static constexpr int f_tab = f_denp + RT * C;                // decay tables, 4 x C
+  static constexpr int nf32 = f_tab + 4 * C;
   static constexpr size_t bytes = (size_t)((n16 + 7) & ~7) * 2 + (size_t)nf32 * 4;
   static constexpr int kBlocks = 2 * bytes <= 160 * 1024 && NW <= 4 ? 2 : 1;
   static constexpr int segQ = C * D / 8, pfQ = segQ / NT, pfV = C * DV / 8 / NT;
@@ -639,11 +642,22 @@ __device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a, int
   }
 }
 
-template <int D, bool SUMMARY>
+//
+// DEC: the decayed operator (decay gamma = 2^lg2g).  With a the token's index
+// in its tile, S_j = gamma^(a_j+1) S0 + sum_{i<=j} gamma^(a_j-a_i) k_i k_i^T and
+// Phi_t = gamma^(2(a_t+1)) Phi0 + sum_{j<=t} gamma^(2(a_t-a_j)) r_j v_j^T, so
+//   R   = diag(gamma^(a+1)) Q S0 + (W (.) gamma^(a_j-a_i)) K,
+//   O   = diag(gamma^(2(a+1))) Q Phi0 + (T (.) gamma^(2(a_t-a_j))) V,
+//   S0 <- gamma^C S0 + K^T diag(gamma^(C-1-a)) K,
+//   Phi0 <- gamma^(2C) Phi0 + R^T diag(gamma^(2(C-1-a))) V  (eta0 likewise),
+// and the segment prefix of S weighs segment s' by gamma^(L (s-1-s')), L its
+// length.  The token weights of the state advances go on the B fragment in
+// registers (scaled in fp32, split hi/lo).  Every factor is at most 1.
+template <int D, bool SUMMARY, bool DEC = false>
 __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlocks)) void k_walk_rs(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ init,
-    int n, int cps, int nseg, int normalized, float eps) {
+    int n, int cps, int nseg, int normalized, float eps, float lg2g) {
   using G = CfgRS<D, SUMMARY>;
   constexpr bool kO = D == 128;     // at 512 threads the hoisted LDS addresses would spill
   constexpr int C = G::C, DV = G::DV, NT = G::NT;
@@ -661,11 +675,21 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   float* eta = fl + G::f_eta;
   float* colsum = fl + G::f_cs;       // [RT][D]
   float* denp = fl + G::f_denp;       // [RT][C]
+  float* g1 = fl + G::f_tab;          // decay tables over the tile index a: gamma^(a+1),
+  float* g2 = g1 + C;                 // gamma^(2(a+1)),
+  float* w1 = g2 + C;                 // gamma^(C-1-a),
+  float* w2 = w1 + C;                 // gamma^(2(C-1-a))
 
   const int seg = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = w / G::NCT, ct = w % G::NCT;          // state row half, column tile
+  if (DEC && tid < C) {
+    g1[tid] = exp2f(lg2g * (float)(tid + 1));
+    g2[tid] = exp2f(2.f * lg2g * (float)(tid + 1));
+    w1[tid] = exp2f(lg2g * (float)(C - 1 - tid));
+    w2[tid] = exp2f(2.f * lg2g * (float)(C - 1 - tid));
+  }
   const int r0 = h * G::HALF;                         // first state row of this wave
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
@@ -691,10 +715,16 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     for (int r = 0; r < nS4; ++r) sa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int sp = init ? -1 : 0; sp < seg; ++sp) {
       const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
+      // decayed: segment sp's moments age by gamma^(L (seg - 1 - sp)) to this segment's start
+      const float f = DEC ? exp2f(lg2g * (float)(C * cps) * (float)(seg - 1 - sp)) : 1.f;
 #pragma unroll
       for (int r = 0; r < nS4; ++r) {
         const float4 u = reinterpret_cast<const float4*>(x)[tid + NT * r];
-        sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
+        if constexpr (DEC) {
+          sa[r].x += f * u.x; sa[r].y += f * u.y; sa[r].z += f * u.z; sa[r].w += f * u.w;
+        } else {
+          sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
+        }
       }
     }
     float* st = reinterpret_cast<float*>(lds);
@@ -767,6 +797,10 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 #pragma unroll
         for (int e = 0; e < 16; ++e)   // keep key i <= query t
           if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
+        if constexpr (DEC) {           // W (.) gamma^(t - i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[e] *= exp2f(lg2g * (float)max(jt * 32 + lr - it * 32 - acc_row(e, lg), 0));
+        }
         store_T<kO>(acc, Wh, Wl, G::ld1, it * 32, jt * 32, ln);
       }
     }
@@ -787,6 +821,17 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         part[rt] = mfma(aQ, bl_, part[rt]);
       }
     }
+    if constexpr (DEC) {               // Q S0 rows age by gamma^(a+1); S0 by gamma^C before its advance
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) part[rt][e] *= g1[rt * 32 + acc_row(e, lg)];
+      const float gC = exp2f(lg2g * (float)C);
+#pragma unroll
+      for (int i = 0; i < G::HT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S0[i][e] *= gC;
+    }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
       const bf16x8 bK = frag_tr<kO>(Ks, G::ldK, ct * 32, s * 16, ln);
@@ -799,9 +844,20 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
         part[1] = mfma(frag<kO>(Wh, G::ld1, 32, s * 16, ln), bK, part[1]);
         part[1] = mfma(frag<kO>(Wl, G::ld1, 32, s * 16, ln), bK, part[1]);
       }
-      // S0 += K^T K on this wave's rows
+      // S0 += K^T K on this wave's rows (decayed: K^T diag(gamma^(C-1-a)) K)
+      if constexpr (DEC) {
+        bf16x8 kh, kl;
+        scale_split(bK, w1 + s * 16 + 8 * lg, kh, kl);
 #pragma unroll
-      for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16, ln), bK, S0[i]);
+        for (int i = 0; i < G::HT; ++i) {
+          const bf16x8 aK = frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16, ln);
+          S0[i] = mfma(aK, kh, S0[i]);
+          S0[i] = mfma(aK, kl, S0[i]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < G::HT; ++i) S0[i] = mfma(frag_tr<kO>(Ks, G::ldK, r0 + i * 32, s * 16, ln), bK, S0[i]);
+      }
     }
     lds_barrier();                      // K, K^T and W are dead: K | K^T takes the exchange
     xch_put<kO>(XR, ct * 2 + (1 - h), h == 0 ? part[1] : part[0], ln);
@@ -809,9 +865,9 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     f32x16 racc = h == 0 ? part[0] : part[1];
     xch_add<kO>(XR, ct * 2 + h, racc, ln);
     {
-      float cs = 0.f;
+      float cs = 0.f;                  // eta0 advance: R^T 1 (decayed: R^T gamma^(2(C-1-a)))
 #pragma unroll
-      for (int e = 0; e < 16; ++e) cs += racc[e];
+      for (int e = 0; e < 16; ++e) cs += DEC ? racc[e] * w2[h * 32 + acc_row(e, lg)] : racc[e];
       cs += __shfl_xor(cs, 32);
       if (lg == 0) colsum[h * D + ct * 32 + lr] = cs;
     }
@@ -836,6 +892,11 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 #pragma unroll
           for (int e = 0; e < 16; ++e)     // keep j <= t
             if (it * 32 + acc_row(e, lg) > jt * 32 + lr) acc[e] = 0.f;
+          if constexpr (DEC) {             // T (.) gamma^(2(t - j))
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              acc[e] *= exp2f(2.f * lg2g * (float)max(jt * 32 + lr - it * 32 - acc_row(e, lg), 0));
+          }
           float ps = 0.f;
 #pragma unroll
           for (int e = 0; e < 16; ++e) ps += acc[e];
@@ -860,15 +921,40 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
           oacc[rt] = mfma(aQ, bl_, oacc[rt]);
         }
       }
+      if constexpr (DEC) {             // Q Phi0 rows age by gamma^(2(a+1))
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) oacc[rt][e] *= g2[rt * 32 + acc_row(e, lg)];
+      }
     }
-    // ---- stage 5: Phi0 += R^T V on this wave's rows ----
+    // ---- stage 5: Phi0 += R^T V on this wave's rows (decayed: gamma^(2C) Phi0 + R^T diag(gamma^(2(C-1-a))) V) ----
+    if constexpr (DEC) {
+      const float g2C = exp2f(2.f * lg2g * (float)C);
+#pragma unroll
+      for (int i = 0; i < G::HT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) P0[i][e] *= g2C;
+    }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
       const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16, ln);
+      if constexpr (DEC) {
+        bf16x8 vh, vl;
+        scale_split(bV, w2 + s * 16 + 8 * lg, vh, vl);
 #pragma unroll
-      for (int i = 0; i < G::HT; ++i) {
-        P0[i] = mfma(frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16, ln), bV, P0[i]);
-        P0[i] = mfma(frag<kO>(Wl, G::ld1, r0 + i * 32, s * 16, ln), bV, P0[i]);
+        for (int i = 0; i < G::HT; ++i) {
+          const bf16x8 ah = frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16, ln);
+          P0[i] = mfma(ah, vh, P0[i]);
+          P0[i] = mfma(ah, vl, P0[i]);
+          P0[i] = mfma(frag<kO>(Wl, G::ld1, r0 + i * 32, s * 16, ln), vh, P0[i]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < G::HT; ++i) {
+          P0[i] = mfma(frag<kO>(Wh, G::ld1, r0 + i * 32, s * 16, ln), bV, P0[i]);
+          P0[i] = mfma(frag<kO>(Wl, G::ld1, r0 + i * 32, s * 16, ln), bV, P0[i]);
+        }
       }
     }
     if (!SUMMARY) {
@@ -905,7 +991,12 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
       }
     }
     lds_barrier();   // LDS tiles and den/eta are rewritten by the next chunk
-    if (tid < D) eta[tid] += eta_add;
+    if (tid < D) {
+      if constexpr (DEC)
+        eta[tid] = exp2f(2.f * lg2g * (float)C) * eta[tid] + eta_add;
+      else
+        eta[tid] += eta_add;
+    }
   }
 
   // the segment's bracket: Phi0 into the G slot, eta0 into the h slot.  The
@@ -955,10 +1046,10 @@ struct WalkK {
   size_t lds;
 };
 
-template <int C, int D, int DV, bool SUMMARY, bool RS>
+template <int C, int D, int DV, bool SUMMARY, bool RS, bool DEC = false>
 WalkK walk_kernel() {
   if constexpr (RS) {
-    return {(const void*)k_walk_rs<D, SUMMARY>, CfgRS<D, SUMMARY>::NT, CfgRS<D, SUMMARY>::bytes};
+    return {(const void*)k_walk_rs<D, SUMMARY, DEC>, CfgRS<D, SUMMARY>::NT, CfgRS<D, SUMMARY>::bytes};
   } else {
     return {(const void*)k_walk<C, D, DV, SUMMARY>, kThreads, Cfg<C, D, DV, SUMMARY>::bytes};
   }
@@ -966,10 +1057,10 @@ WalkK walk_kernel() {
 
 hipError_t launch_walk(const WalkK& kk, dim3 grid, hipStream_t s, const uint16_t* q, const uint16_t* k,
                        const uint16_t* v, float* out, float* den_out, float* rec, const float* init, int n, int cps,
-                       int nseg, int normalized, float eps) {
+                       int nseg, int normalized, float eps, float lg2g) {
   hipError_t e = hipFuncSetAttribute(kk.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kk.lds);
   if (e != hipSuccess) return e;
-  void* args[] = {&q, &k, &v, &out, &den_out, &rec, &init, &n, &cps, &nseg, &normalized, &eps};
+  void* args[] = {&q, &k, &v, &out, &den_out, &rec, &init, &n, &cps, &nseg, &normalized, &eps, &lg2g};
   return prof_launch(kk.fn, grid, dim3(kk.threads), args, kk.lds, s);
 }
 
@@ -977,9 +1068,13 @@ size_t records_bytes(int BH, int P, int d, int dv) {
   return (sizeof(float) * (size_t)BH * (P + 1) * state_floats(d, dv) + 255) & ~size_t(255);
 }
 
-template <int C, int D, int DV, bool RS>
+// DEC: the decayed operator (row-split shapes, no initial or final state).
+template <int C, int D, int DV, bool RS, bool DEC = false>
 hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* ws, int P, int cps,
                      hipStream_t s) {
+  static_assert(!DEC || RS, "the decayed walk is row-split only");
+  const float lg2g = DEC ? (float)std::log2((double)f.gamma) : 0.f;
+  const float rho2 = DEC ? (float)std::exp2(2.0 * std::log2((double)f.gamma) * (double)C * (double)cps) : 1.f;
   const int BH = f.BH;
   float* segs = reinterpret_cast<float*>(ws);                                  // [BH][P + 1][F] records
   float* den = reinterpret_cast<float*>(ws + records_bytes(BH, P, D, DV));    // [BH][n] walk denominators
@@ -997,15 +1092,15 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   prof_start("moments", s);
-  HLA_LAUNCH((k_moments<C, D, DV>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P,
-                     final_state ? 1 : 0);
+  HLA_LAUNCH((k_moments<C, D, DV, false, DEC>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P,
+             final_state ? 1 : 0, lg2g);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_start(f.out ? "walk" : "walk_summary", s);
-  e = f.out ? launch_walk(walk_kernel<C, D, DV, false, RS>(), grid, s, q, k, v, f.out, den, segs, init, f.n, cps, P,
-                          f.normalized, f.eps)
-            : launch_walk(walk_kernel<C, D, DV, true, RS>(), grid, s, q, k, v, nullptr, nullptr, segs, init, f.n,
-                          cps, P, 0, 0.f);
+  e = f.out ? launch_walk(walk_kernel<C, D, DV, false, RS, DEC>(), grid, s, q, k, v, f.out, den, segs, init, f.n,
+                          cps, P, f.normalized, f.eps, lg2g)
+            : launch_walk(walk_kernel<C, D, DV, true, RS, DEC>(), grid, s, q, k, v, nullptr, nullptr, segs, init, f.n,
+                          cps, P, 0, 0.f, lg2g);
   prof_stop(s);
   if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
   if (final_state) {
@@ -1019,18 +1114,19 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   if (f.out && (P > 1 || init || f.normalized)) {
     float* carry = den + (((size_t)BH * f.n + (size_t)BH * ((f.n + C - 1) / C) * D + 63) & ~size_t(63));
     prof_start("carry", s);
-    HLA_LAUNCH((k_carry<D, DV>), dim3((D * DV / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P);
+    HLA_LAUNCH((k_carry<D, DV>), dim3((D * DV / 8 + D + 255) / 256, BH), dim3(256), 0, s, segs, init, carry, P,
+               rho2);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     using FC = FixCfg<C, D, DV>;
     static_assert(FC::lds <= 64 * 1024, "fix LDS");
-    if ((e = hipFuncSetAttribute((const void*)k_fix<C, D, DV>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    if ((e = hipFuncSetAttribute((const void*)k_fix<C, D, DV, DEC>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                  (int)FC::lds)) != hipSuccess)
       return e;
     const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("fix", s);
-    HLA_LAUNCH((k_fix<C, D, DV>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
-                       carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps, tpw);
+    HLA_LAUNCH((k_fix<C, D, DV, DEC>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
+               carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps, tpw, lg2g);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -1064,6 +1160,11 @@ bool fused_supported(int n, int d, int dv, int chunk, int dtype, int masked) {
   return dtype == 1 && masked == 1 && n >= 1 && span < (1LL << 31) && find_shape(chunk, d, dv) != nullptr;
 }
 
+bool fused_decay_supported(int n, int d, int dv, int chunk, int dtype, int masked) {
+  const Shape* sh = find_shape(chunk, d, dv);
+  return fused_supported(n, d, dv, chunk, dtype, masked) && sh && row_split_shape(*sh);
+}
+
 size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
   const Shape* sh = find_shape(chunk, d, dv);
   if (!sh) return 0;
@@ -1080,6 +1181,11 @@ hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, voi
   int P, cps;
   fused_plan(*sh, f.BH, f.n, &P, &cps);
   char* ws = static_cast<char*>(workspace);
+  if (f.gamma != 1.f) {           // decayed: row-split shapes only, no states
+    if (!row_split_shape(*sh) || init || final_state) return hipErrorNotSupported;
+    if (sh->D == 64) return run_shape<64, 64, 64, true, true>(f, init, final_state, ws, P, cps, s);
+    return run_shape<64, 128, 128, true, true>(f, init, final_state, ws, P, cps, s);
+  }
   if (row_split_shape(*sh)) {
     if (sh->D == 64) return run_shape<64, 64, 64, true>(f, init, final_state, ws, P, cps, s);
     return run_shape<64, 128, 128, true>(f, init, final_state, ws, P, cps, s);

@@ -136,6 +136,19 @@ __device__ __forceinline__ void frag_from_acc(const f32x16& t, int h, bf16x8& hi
   lo = __builtin_bit_cast(bf16x8, make_uint4(b[0], b[1], b[2], b[3]));
 }
 
+// Decay (the decayed second-order operator): a bf16 operand fragment whose 8
+// elements are the tokens t0 .. t0+7 of one column, scaled per token by
+// w[t0 + m] (fp32, from an LDS table) and split into bf16 hi + lo.
+__device__ __forceinline__ void scale_split(const bf16x8& x, const float* w, bf16x8& hi, bf16x8& lo) {
+  const float4 w0 = *reinterpret_cast<const float4*>(w), w1 = *reinterpret_cast<const float4*>(w + 4);
+  const float wm[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+  uint32_t a[4], b[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) split2((float)x[2 * i] * wm[2 * i], (float)x[2 * i + 1] * wm[2 * i + 1], a[i], b[i]);
+  hi = __builtin_bit_cast(bf16x8, make_uint4(a[0], a[1], a[2], a[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(b[0], b[1], b[2], b[3]));
+}
+
 // Store an accumulator tile D[row0 + i][col0 + r] transposed as X[col0 + r][row0 + i],
 // split into hi/lo tiles (four 8-byte stores each).
 template <bool O = false>
@@ -178,15 +191,19 @@ __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_
 //
 // KV (the AHLA walk, Sec. 6): P = K^T V into the C slot and m^K = K^T 1 into
 // the m slot; no S, and q is not read (want_cm is ignored).
-template <int C, int D, int DV, bool KV = false>
+// DEC (decay gamma = 2^lg2g; S only): S = sum_t gamma^(e - t) k_t k_t^T with e
+// the segment's last token, the weight applied to one factor per token in
+// fp32 and split hi/lo.
+template <int C, int D, int DV, bool KV = false, bool DEC = false>
 __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v, float* __restrict__ rec, int n,
-                                                      int cps, int nseg, int want_cm) {
+                                                      int cps, int nseg, int want_cm, float lg2g) {
   constexpr int ld = C + kPad, DT = D / 32, VT = DV / 32, KC = C / 16;
   constexpr int nS = (DT * DT + kWaves - 1) / kWaves, nC = (DT * VT + kWaves - 1) / kWaves;
   constexpr int segQ = C * D / 8, segV = C * DV / 8;
   __shared__ __align__(16) uint16_t Kt[D * ld], Qs_[KV ? 8 : D * ld], Vt[DV * ld];
   uint16_t* Qt = KV ? Kt : Qs_;          // the left factor of the C slot
+  __shared__ __align__(16) float wtab[DEC ? C : 4];   // decay weights of the current tile's tokens
   if (KV) want_cm = 1;
   const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -217,6 +234,7 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
     };
     auto step = [&](int c, auto slot_tag) {
       constexpr int sl = decltype(slot_tag)::value;
+      if (DEC && tid < C) wtab[tid] = exp2f(lg2g * (float)((c0 + cps - 1 - c) * C + C - 1 - tid));
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const int e = tid + kThreads * i;
@@ -235,8 +253,17 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
         if (ti < DT * DT) {
           const int it = ti / DT, jt = ti % DT;
 #pragma unroll
-          for (int s = 0; s < KC; ++s)
-            sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
+          for (int s = 0; s < KC; ++s) {
+            if constexpr (DEC) {
+              bf16x8 bh, bl;
+              scale_split(frag(Kt, ld, jt * 32, s * 16), wtab + s * 16 + 8 * lg, bh, bl);
+              const bf16x8 a = frag(Kt, ld, it * 32, s * 16);
+              sacc[i] = mfma(a, bh, sacc[i]);
+              sacc[i] = mfma(a, bl, sacc[i]);
+            } else {
+              sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
+            }
+          }
         }
       }
       lds_barrier();
@@ -372,9 +399,11 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
 // Phi_c[16s + 8(lane/32) + j][32ct + lane%32], j = 0..7: D*DV/8 pieces of
 // 16 bytes, all hi pieces then all lo pieces), then eta_c in fp32 [D].
 // grid (ceil((D*DV/8 + D) / 256), BH); reads and writes coalesced.
+// rho2: attenuation of a carry over one segment (gamma^(2L) with decay, else 1):
+// carry_{s+1} = rho2 carry_s + bracket_s.
 template <int D, int DV>
 __global__ __launch_bounds__(256) void k_carry(const float* __restrict__ rec, const float* __restrict__ init,
-                                               float* __restrict__ carry, int nseg) {
+                                               float* __restrict__ carry, int nseg, float rho2) {
   constexpr int NC = D * DV + D, NP = D * DV / 8, KD = D / 16;
   const int bh = blockIdx.y, p = blockIdx.x * 256 + threadIdx.x;
   if (p >= NP + D) return;
@@ -386,7 +415,7 @@ __global__ __launch_bounds__(256) void k_carry(const float* __restrict__ rec, co
     float x = init ? src[(size_t)nseg * F] : 0.f;
     for (int sp = 0; sp < nseg; ++sp) {
       carry[((size_t)bh * nseg + sp) * NC + D * DV + a] = x;
-      x += src[(size_t)sp * F];
+      x = rho2 * x + src[(size_t)sp * F];
     }
     return;
   }
@@ -403,7 +432,7 @@ __global__ __launch_bounds__(256) void k_carry(const float* __restrict__ rec, co
     dst[p] = make_uint4(pack2(h8[0], h8[1]), pack2(h8[2], h8[3]), pack2(h8[4], h8[5]), pack2(h8[6], h8[7]));
     dst[NP + p] = make_uint4(pack2(o8[0], o8[1]), pack2(o8[2], o8[3]), pack2(o8[4], o8[5]), pack2(o8[6], o8[7]));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] += src[(size_t)sp * F + j * DV];
+    for (int j = 0; j < 8; ++j) x[j] = rho2 * x[j] + src[(size_t)sp * F + j * DV];
   }
 }
 
@@ -423,10 +452,14 @@ struct FixCfg {
   static_assert(NT >= D && NT <= 1024, "fix workgroup");
 };
 
-template <int C, int D, int DV>
+// DEC (decay gamma = 2^lg2g): the carry of a segment reaches token t aged by
+// gamma^(2(p+1)), p = t - (first token of the segment); the tile's eta0 by
+// gamma^(2(a+1)), a = t - (first token of the tile).
+template <int C, int D, int DV, bool DEC = false>
 __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
     const uint16_t* __restrict__ q, float* __restrict__ out, const float* __restrict__ den_in,
-    const float* __restrict__ carry, int has_init, int n, int cps, int nseg, int normalized, float eps, int tpw) {
+    const float* __restrict__ carry, int has_init, int n, int cps, int nseg, int normalized, float eps, int tpw,
+    float lg2g) {
   using F = FixCfg<C, D, DV>;
   constexpr int NT = F::NT, KD = F::KD, ldQ = F::ldQ, QE = F::QE, QV = F::QV, NC = D * DV + D;
   extern __shared__ __align__(16) uint16_t lds[];      // q tile | fp32 eta | 1/den
@@ -472,8 +505,10 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
       const int e = tid + NT * i;
       if (e < QE) *reinterpret_cast<uint4*>(Qs + (e / (D / 8)) * ldQ + (e % (D / 8)) * 8) = qp[i];
     }
-    if (normalized && tid < D)        // eta at the tile start: the walk's eta0 + eta_c
-      es[tid] = cb[D * DV + tid] + den_in[(size_t)gridDim.y * n + ((size_t)bh * M + c) * D + tid];
+    if (normalized && tid < D) {      // eta at the tile start: the walk's eta0 + eta_c
+      const float ec = DEC ? cb[D * DV + tid] * exp2f(2.f * lg2g * (float)(C * (c - seg * cps))) : cb[D * DV + tid];
+      es[tid] = ec + den_in[(size_t)gridDim.y * n + ((size_t)bh * M + c) * D + tid];
+    }
     lds_barrier();
     // rows past n fall outside the buffer: loads read 0, stores drop
     const uint32_t ob = ((t0 + rt * 32 + 4 * lg) * DV + ct * 32 + lr) * 4;
@@ -501,6 +536,7 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
       }
 #pragma unroll
       for (int o = 1; o < TPR; o <<= 1) sd += __shfl_xor(sd, o);
+      if (DEC) sd *= exp2f(2.f * lg2g * (float)(t + 1));
       if (tid % TPR == 0 && t < C) inv[t] = (t0 + t < (uint32_t)n) ? 1.f / (den_in[(size_t)bh * n + t0 + t] + sd + eps) : 0.f;
       lds_barrier();
     }
@@ -513,7 +549,8 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
     }
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      float y = prev[e] + acc[e];
+      float y = DEC ? prev[e] + acc[e] * exp2f(2.f * lg2g * (float)(C * (c - seg * cps) + rt * 32 + acc_row(e, lg) + 1))
+                    : prev[e] + acc[e];
       if (normalized) y *= inv[rt * 32 + acc_row(e, lg)];
       buf_store4(ro, ob + (8 * (e >> 2) + (e & 3)) * DV * 4, y);
     }

@@ -160,7 +160,11 @@ int hla2_forward(const void* q, const void* k, const void* v, float* out, int B,
 
 size_t hla2_forward_decay_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
   if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
-  return chunked_ws(B * H, n, d, dv, chunk);
+  // the larger of the two paths: the masked flag is not an argument here
+  const size_t fused = hla::fused_decay_supported(n, d, dv, chunk, dtype, 1)
+                           ? hla::fused_workspace_bytes(B * H, n, d, dv, chunk) : 0;
+  const size_t chunked = chunked_ws(B * H, n, d, dv, chunk);
+  return fused > chunked ? fused : chunked;
 }
 
 int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
@@ -179,10 +183,20 @@ int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, 
       (rc = check_ptr(out, "out")))
     return rc;
   const int BH = B * H;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (hla::fused_decay_supported(n, d, dv, chunk, dtype, masked)) {
+    // bf16, masked, d = dv in {64, 128}: the fused segment walk with decay
+    const size_t need = hla::fused_workspace_bytes(BH, n, d, dv, chunk);
+    if (!workspace || workspace_bytes < need)
+      return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+    hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps, gamma};
+    const hipError_t e = hla::launch_fused(f, nullptr, nullptr, workspace, s);
+    if (e != hipSuccess) return hip_fail(e, "decayed fused forward");
+    return ok();
+  }
   const size_t need = chunked_ws(BH, n, d, dv, chunk);
   if (!workspace || workspace_bytes < need)
     return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int cc = path_chunk(chunk);
   hla::Fwd f{q, k, v, out, BH, n, d, dv, cc, masked, normalized, dtype, eps, gamma};
   const int M = (n + cc - 1) / cc;

@@ -106,3 +106,54 @@ def test_decay_errors():
     with pytest.raises(capi.HLAError) as ei:
         capi.hla2_forward_decay(*base, 0.9, I.HLA_FP32, ws.data_ptr(), 16, None)
     assert ei.value.code == capi.HLA_ERR_WORKSPACE
+
+
+# ---- the fused segment walk with decay (bf16, masked, d = dv in {64, 128}) ----
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("gamma", [0.6, 0.9, 0.99, 0.9995])
+def test_decay_fused_shapes(d, gamma):
+    for n in (1, 7, 64, 65, 190, 513):
+        _check(1, 2, n, d, d, 64, "unit", gamma, seed=n + d)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("segments", [1, 2, 3, 7])
+def test_decay_fused_segment_counts(d, segments, monkeypatch):
+    """Segments of several tiles: the decayed moments prefix, the brackets and
+    the carry attenuated by gamma^(2L) per segment."""
+    monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
+    _check(2, 1, 64 * 9 + 5, d, d, 64, "unit", 0.98, seed=segments)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("segments", [1, 4, 0])
+def test_decay_fused_normalized(d, segments, monkeypatch):
+    if segments:
+        monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
+    _check(1, 2, 400, d, d, 64, "unit", 0.97, normalized=True, seed=d + segments)
+
+
+def test_decay_fused_chunk128_is_64_token_tiles():
+    q, k, v, code = gen(2, 2, 300, 64, 64, "unit", 9)
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    assert torch.equal(hla.forward_decay(qd, kd, vd, 64, 0.95), hla.forward_decay(qd, kd, vd, 128, 0.95))
+
+
+def test_decay_fused_gamma_one_equals_forward():
+    """gamma = 1 on the fused shapes is the undecayed fused forward, bit for bit."""
+    q, k, v, code = gen(2, 2, 333, 64, 64, "unit", 10)
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    assert torch.equal(hla.forward_decay(qd, kd, vd, 64, 1.0), hla.forward(qd, kd, vd, 64))
+
+
+def test_decay_fused_workload_b2h32_d128_sampled_heads():
+    """B2 H32 n16384 d=dv=128 bf16, chunk 128, gamma 0.999: every head on the GPU, heads 0-1 against the oracle."""
+    q, k, v, code = gen(2, 32, 16384, 128, 128, "unit", 0)
+    _say("case decay fused B2H32 n16384 d128 gamma 0.999 (heads 0-1 checked)")
+    out = hla.forward_decay(dev(q, code), dev(k, code), dev(v, code), 128, 0.999).cpu().numpy()
+    ref, _, _, _ = native.hla2_decay_serial_c(q[0, :2], k[0, :2], v[0, :2], 0.999, masked=True, threads=16,
+                                              return_state=False)
+    err = rowwise_err(out[0, :2], ref)
+    _say(f"decay fused d128 row-wise error {err:.3e}")
+    assert err <= tol_for(code)
