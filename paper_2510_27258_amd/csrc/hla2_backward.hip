@@ -86,12 +86,13 @@ struct Stage {
   }
 };
 
-// grid (nseg, BH), NT threads.  REV: anti-causal (keys at or after the
-// query; tiles walked from the last).  ACC: add to out instead of writing it.
+// grid (nseg, BH), NT threads.  rev: anti-causal (keys at or after the
+// query; tiles walked from the last).  acc_out: add to out instead of writing
+// it.  tr: the records hold the transposed moments (sum z y^T of another pass).
 template <int D, bool XF, bool YF, bool ZF, bool MOM>
 __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
     const void* __restrict__ xp, const void* __restrict__ yp, const void* __restrict__ zp, float* __restrict__ out,
-    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out) {
+    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr) {
   using G = CfgLA<D>;
   constexpr bool kO = D == 128;
   constexpr int C = G::C, NT = G::NT, ST = G::ST, ld = G::ld, ldA = G::ldA;
@@ -140,7 +141,8 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
 #pragma unroll
       for (int i = 0; i < ST; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) S0[i][e] = st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+        for (int e = 0; e < 16; ++e)
+          S0[i][e] = tr ? st[(ct * 32 + lr) * D + i * 32 + acc_row(e, lg)] : st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
       __syncthreads();
     }
   }
@@ -270,28 +272,32 @@ void la_plan(int D, int BH, int n, int* P, int* cps) {
   *P = (M + *cps - 1) / *cps;
 }
 
-// One linear-attention pass: moments of (y, z) per segment, then the walks.
-template <int D, bool XF, bool YF, bool ZF>
-hipError_t la_pass(const char* name, const void* x, const void* y, const void* z, float* out, float* rec, int BH, int n,
-                   int P, int cps, int rev, int acc, hipStream_t s) {
+// The moments sum y z^T of every segment (skipped with one segment: no walk reads them).
+template <int D, bool YF, bool ZF>
+hipError_t la_moments(const void* y, const void* z, float* rec, int BH, int n, int P, int cps, hipStream_t s) {
   using G = CfgLA<D>;
-  const dim3 grid(P, BH);
+  if (P == 1) return hipSuccess;
+  const void* km = (const void*)k_la<D, false, YF, ZF, true>;
   hipError_t e;
-  if (P > 1) {
-    const void* km = (const void*)k_la<D, false, YF, ZF, true>;
-    if ((e = hipFuncSetAttribute(km, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess)
-      return e;
-    prof_start("bwd_moments", s);
-    HLA_LAUNCH((k_la<D, false, YF, ZF, true>), grid, dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P, rev,
-               acc);
-    prof_stop(s);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
+  if ((e = hipFuncSetAttribute(km, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
+  prof_start("bwd_moments", s);
+  HLA_LAUNCH((k_la<D, false, YF, ZF, true>), dim3(P, BH), dim3(G::NT), G::bytes, s, y, y, z,
+             (float*)nullptr, rec, n, cps, P, 0, 0, 0);
+  prof_stop(s);
+  return hipGetLastError();
+}
+
+// One linear-attention walk over every segment from the moments in rec.
+template <int D, bool XF, bool YF, bool ZF>
+hipError_t la_walk(const char* name, const void* x, const void* y, const void* z, float* out, float* rec, int BH, int n,
+                   int P, int cps, int rev, int acc, int tr, hipStream_t s) {
+  using G = CfgLA<D>;
   const void* kw = (const void*)k_la<D, XF, YF, ZF, false>;
-  if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess)
-    return e;
+  hipError_t e;
+  if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start(name, s);
-  HLA_LAUNCH((k_la<D, XF, YF, ZF, false>), grid, dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P, rev, acc);
+  HLA_LAUNCH((k_la<D, XF, YF, ZF, false>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P, rev,
+             acc, tr);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -305,28 +311,37 @@ template <int D>
 hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
   int P, cps;
   la_plan(D, b.BH, b.n, &P, &cps);
-  float* rec = reinterpret_cast<float*>(ws);
-  float* r = reinterpret_cast<float*>(ws + rec_bytes(b.BH, P, D));
-  float* u = reinterpret_cast<float*>(ws + rec_bytes(b.BH, P, D) + vec_bytes(b.BH, b.n, D));
   const int BH = b.BH, n = b.n;
+  const size_t rb = rec_bytes(BH, P, D);
+  // four moment sets serve the seven passes: k^T k (r and the second dq
+  // term), g^T q (u; transposed for dv), v^T r (the first dq term) and
+  // q^T u (the first dk term; transposed for the second)
+  float* kk = reinterpret_cast<float*>(ws);
+  float* gq = reinterpret_cast<float*>(ws + rb);
+  float* vr = reinterpret_cast<float*>(ws + 2 * rb);
+  float* qu = reinterpret_cast<float*>(ws + 3 * rb);
+  float* r = reinterpret_cast<float*>(ws + 4 * rb);
+  float* u = reinterpret_cast<float*>(ws + 4 * rb + vec_bytes(BH, n, D));
   hipError_t e;
-  // r = LA+(q, k, k),  u = LA-(v, g, q)
-  if ((e = la_pass<D, false, false, false>("bwd_r", b.q, b.k, b.k, r, rec, BH, n, P, cps, 0, 0, s)) != hipSuccess)
-    return e;
-  if ((e = la_pass<D, false, true, false>("bwd_u", b.v, b.g, b.q, u, rec, BH, n, P, cps, 1, 0, s)) != hipSuccess)
-    return e;
+#define HLA_TRY(x) if ((e = (x)) != hipSuccess) return e
+  // r = LA+(q, k, k)
+  HLA_TRY((la_moments<D, false, false>(b.k, b.k, kk, BH, n, P, cps, s)));
+  HLA_TRY((la_walk<D, false, false, false>("bwd_r", b.q, b.k, b.k, r, kk, BH, n, P, cps, 0, 0, 0, s)));
+  // u = LA-(v, g, q)
+  HLA_TRY((la_moments<D, true, false>(b.g, b.q, gq, BH, n, P, cps, s)));
+  HLA_TRY((la_walk<D, false, true, false>("bwd_u", b.v, b.g, b.q, u, gq, BH, n, P, cps, 1, 0, 0, s)));
   // dq = LA+(g, v, r) + LA+(u, k, k)
-  if ((e = la_pass<D, true, false, true>("bwd_dq", b.g, b.v, r, b.dq, rec, BH, n, P, cps, 0, 0, s)) != hipSuccess)
-    return e;
-  if ((e = la_pass<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, rec, BH, n, P, cps, 0, 1, s)) != hipSuccess)
-    return e;
-  // dv = LA-(r, q, g)
-  if ((e = la_pass<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, rec, BH, n, P, cps, 1, 0, s)) != hipSuccess)
-    return e;
-  // dk = LA-(k, q, u) + LA-(k, u, q)
-  if ((e = la_pass<D, false, false, true>("bwd_dk", b.k, b.q, u, b.dk, rec, BH, n, P, cps, 1, 0, s)) != hipSuccess)
-    return e;
-  return la_pass<D, false, true, false>("bwd_dk", b.k, u, b.q, b.dk, rec, BH, n, P, cps, 1, 1, s);
+  HLA_TRY((la_moments<D, false, true>(b.v, r, vr, BH, n, P, cps, s)));
+  HLA_TRY((la_walk<D, true, false, true>("bwd_dq", b.g, b.v, r, b.dq, vr, BH, n, P, cps, 0, 0, 0, s)));
+  HLA_TRY((la_walk<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, kk, BH, n, P, cps, 0, 1, 0, s)));
+  // dv = LA-(r, q, g): moments q^T g = (g^T q)^T
+  HLA_TRY((la_walk<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, gq, BH, n, P, cps, 1, 0, 1, s)));
+  // dk = LA-(k, q, u) + LA-(k, u, q): moments q^T u, then (q^T u)^T
+  HLA_TRY((la_moments<D, false, true>(b.q, u, qu, BH, n, P, cps, s)));
+  HLA_TRY((la_walk<D, false, false, true>("bwd_dk", b.k, b.q, u, b.dk, qu, BH, n, P, cps, 1, 0, 0, s)));
+  HLA_TRY((la_walk<D, false, true, false>("bwd_dk", b.k, u, b.q, b.dk, qu, BH, n, P, cps, 1, 1, 1, s)));
+#undef HLA_TRY
+  return hipSuccess;
 }
 
 }  // namespace
@@ -339,7 +354,7 @@ bool backward_supported(int n, int d, int dv, int dtype) {
 size_t backward_workspace_bytes(int BH, int n, int d) {
   int P, cps;
   la_plan(d, BH, n, &P, &cps);
-  return rec_bytes(BH, P, d) + 2 * vec_bytes(BH, n, d) + 256;
+  return 4 * rec_bytes(BH, P, d) + 2 * vec_bytes(BH, n, d) + 256;
 }
 
 hipError_t launch_backward(const Bwd& b, void* workspace, hipStream_t s) {
