@@ -13,6 +13,7 @@
 //   r  = LA+(q, k, k)                       u  = LA-(v, g, q)
 //   dq = LA+(g, v, r) + LA+(u, k, k)        dv = LA-(r, q, g)
 //   dk = LA-(k, q, u) + LA-(k, u, q).
+// The two dk passes share x and swap y and z; they run as one paired walk.
 // Each pass is the first-order chunk scan: the state sum y z^T of a segment
 // does not depend on anything before it, so every segment's walk starts from
 // the exact prefix (suffix) of the segment moments and no fix-up follows.
@@ -89,11 +90,16 @@ struct Stage {
 // grid (nseg, BH), NT threads.  rev: anti-causal (keys at or after the
 // query; tiles walked from the last).  acc_out: add to out instead of writing
 // it.  tr: the records hold the transposed moments (sum z y^T of another pass).
-template <int D, bool XF, bool YF, bool ZF, bool MOM>
+// TWO: two passes that share x and swap y and z, LA(x, y, z) + LA(x, z, y),
+// in one walk: A2 = X Z^T masked adds A2 Y, and the state is
+// sum (y z^T + z y^T), staged from the moments of (y, z) plus their transpose
+// (x and y exact in bf16: A2 takes the lo regions of X and Y).
+template <int D, bool XF, bool YF, bool ZF, bool MOM, bool TWO = false>
 __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
     const void* __restrict__ xp, const void* __restrict__ yp, const void* __restrict__ zp, float* __restrict__ out,
     float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr) {
   using G = CfgLA<D>;
+  static_assert(!TWO || (!XF && !YF && !MOM), "the paired pass keeps A2 in the lo tiles of x and y");
   constexpr bool kO = D == 128;
   constexpr int C = G::C, NT = G::NT, ST = G::ST, ld = G::ld, ldA = G::ldA;
   extern __shared__ __align__(16) uint16_t lds[];
@@ -105,6 +111,8 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   uint16_t* Zl = lds + G::oZl;
   uint16_t* Ah = lds + G::oAh;
   uint16_t* Al = lds + G::oAl;
+  uint16_t* A2h = Xl;             // TWO: A2 = X Z^T masked, in the (unused) lo tiles of x and y
+  uint16_t* A2l = Yl;
 
   const int seg = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
@@ -141,8 +149,13 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
 #pragma unroll
       for (int i = 0; i < ST; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          S0[i][e] = tr ? st[(ct * 32 + lr) * D + i * 32 + acc_row(e, lg)] : st[(i * 32 + acc_row(e, lg)) * D + ct * 32 + lr];
+        for (int e = 0; e < 16; ++e) {
+          const int ra = i * 32 + acc_row(e, lg), cb = ct * 32 + lr;
+          if constexpr (TWO)
+            S0[i][e] = st[ra * D + cb] + st[cb * D + ra];
+          else
+            S0[i][e] = tr ? st[cb * D + ra] : st[ra * D + cb];
+        }
       __syncthreads();
     }
   }
@@ -196,6 +209,21 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
             if (rev ? key < qry : key > qry) a[e] = 0.f;
           }
           store_T<kO>(a, Ah, Al, ldA, kt * 32, qt * 32);
+          if constexpr (TWO) {            // A2 = X Z^T on the same tile, z split
+            f32x16 a2 = zero16();
+#pragma unroll
+            for (int s = 0; s < D / 16; ++s) {
+              const bf16x8 xh = frag<kO>(Xh, ld, qt * 32, s * 16);
+              a2 = mfma(frag<kO>(Zh, ld, kt * 32, s * 16), xh, a2);
+              a2 = mfma(frag<kO>(Zl, ld, kt * 32, s * 16), xh, a2);
+            }
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int key = kt * 32 + acc_row(e, lg), qry = qt * 32 + lr;
+              if (rev ? key < qry : key > qry) a2[e] = 0.f;
+            }
+            store_T<kO>(a2, A2h, A2l, ldA, kt * 32, qt * 32);
+          }
         }
       }
       lds_barrier();
@@ -218,6 +246,11 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
           o = mfma(ah, zh, o);
           o = mfma(al, zh, o);
           if (ZF) o = mfma(ah, frag_tr<kO>(Zl, ld, ct * 32, s * 16), o);
+          if constexpr (TWO) {            // + A2 Y
+            const bf16x8 yh = frag_tr<kO>(Yh, ld, ct * 32, s * 16);
+            o = mfma(frag<kO>(A2h, ldA, rt * 32, s * 16), yh, o);
+            o = mfma(frag<kO>(A2l, ldA, rt * 32, s * 16), yh, o);
+          }
         }
       }
     }
@@ -233,6 +266,14 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
         S0[i] = mfma(yh, zh, S0[i]);
         if (ZF) S0[i] = mfma(yh, zl, S0[i]);
         if (YF) S0[i] = mfma(frag_tr<kO>(Yl, ld, i * 32, s * 16), zh, S0[i]);
+      }
+      if constexpr (TWO) {                // + Z^T Y
+        const bf16x8 yb = frag_tr<kO>(Yh, ld, ct * 32, s * 16);
+#pragma unroll
+        for (int i = 0; i < ST; ++i) {
+          S0[i] = mfma(frag_tr<kO>(Zh, ld, i * 32, s * 16), yb, S0[i]);
+          S0[i] = mfma(frag_tr<kO>(Zl, ld, i * 32, s * 16), yb, S0[i]);
+        }
       }
     }
     if (!MOM) {
@@ -287,17 +328,18 @@ hipError_t la_moments(const void* y, const void* z, float* rec, int BH, int n, i
   return hipGetLastError();
 }
 
-// One linear-attention walk over every segment from the moments in rec.
-template <int D, bool XF, bool YF, bool ZF>
+// One linear-attention walk over every segment from the moments in rec
+// (TWO: the paired walk LA(x, y, z) + LA(x, z, y)).
+template <int D, bool XF, bool YF, bool ZF, bool TWO = false>
 hipError_t la_walk(const char* name, const void* x, const void* y, const void* z, float* out, float* rec, int BH, int n,
                    int P, int cps, int rev, int acc, int tr, hipStream_t s) {
   using G = CfgLA<D>;
-  const void* kw = (const void*)k_la<D, XF, YF, ZF, false>;
+  const void* kw = (const void*)k_la<D, XF, YF, ZF, false, TWO>;
   hipError_t e;
   if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start(name, s);
-  HLA_LAUNCH((k_la<D, XF, YF, ZF, false>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P, rev,
-             acc, tr);
+  HLA_LAUNCH((k_la<D, XF, YF, ZF, false, TWO>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P,
+             rev, acc, tr);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -336,10 +378,9 @@ hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
   HLA_TRY((la_walk<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, kk, BH, n, P, cps, 0, 1, 0, s)));
   // dv = LA-(r, q, g): moments q^T g = (g^T q)^T
   HLA_TRY((la_walk<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, gq, BH, n, P, cps, 1, 0, 1, s)));
-  // dk = LA-(k, q, u) + LA-(k, u, q): moments q^T u, then (q^T u)^T
+  // dk = LA-(k, q, u) + LA-(k, u, q) in one paired walk: state sum (q u^T + u q^T)
   HLA_TRY((la_moments<D, false, true>(b.q, u, qu, BH, n, P, cps, s)));
-  HLA_TRY((la_walk<D, false, false, true>("bwd_dk", b.k, b.q, u, b.dk, qu, BH, n, P, cps, 1, 0, 0, s)));
-  HLA_TRY((la_walk<D, false, true, false>("bwd_dk", b.k, u, b.q, b.dk, qu, BH, n, P, cps, 1, 1, 1, s)));
+  HLA_TRY((la_walk<D, false, false, true, true>("bwd_dk", b.k, b.q, u, b.dk, qu, BH, n, P, cps, 1, 0, 0, s)));
 #undef HLA_TRY
   return hipSuccess;
 }
