@@ -13,7 +13,7 @@ def _declarations():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     decls = {}
-    for m in re.finditer(r"^\s*(?:const\s+)?[a-z_]+\s*\*?\s*(hla[0-9a-z_]*)\s*\(([^)]*)\)\s*;", text, flags=re.M):
+    for m in re.finditer(r"^\s*(?:const\s+)?[a-z_]+\s*\*?\s*(a?hla[0-9a-z_]*)\s*\(([^)]*)\)\s*;", text, flags=re.M):
         name, args = m.group(1), m.group(2).strip()
         decls[name] = 0 if args in ("", "void") else len(args.split(","))
     return decls
@@ -21,7 +21,9 @@ def _declarations():
 
 def test_header_parses():
     decls = _declarations()
-    for name in ("hla2_forward", "hla2_step", "hla2_scan", "hla2_chunk_summaries", "hla2_prefill"):
+    for name in ("hla2_forward", "hla2_step", "hla2_scan", "hla2_chunk_summaries", "hla2_prefill", "hla2_forward_decay",
+                 "hla3_forward", "ahla_forward", "ahla_workspace_bytes", "hla2_backward",
+                 "hla2_backward_workspace_bytes"):
         assert name in decls
 
 
