@@ -32,6 +32,8 @@
 //      the F carry, and the segment's bracket (F, eta).
 //   3. k3_fix: out_t += q_t^T F_c, den_t += q_t . eta_c with F_c the sum of the
 //      brackets before the segment; normalises if asked.
+#include <cstdlib>
+
 #include "hla3.h"
 #include "profile.h"
 
@@ -179,18 +181,26 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
       QP[t * lV + b] = (float)s;
       QF[t * lV + b] = (float)f;
     }
-    for (int t = tid; t < C; t += kT3) {
-      double s = 0.0, w = 0.0, g = 0.0;
-      for (int a = 0; a < D; ++a) {
-        s += (double)Qs[t * lD + a] * mv[a];
-        w += (double)Qs[t * lD + a] * eta[a];
-        double y = 0.0;
-        for (int b = 0; b < D; ++b) y += (double)SQ[a * lD + b] * Ks[t * lD + b];
-        g += (double)Ks[t * lD + a] * y;
+    // per token t: q_t.m0, q_t.eta0 and k_t^T SQ0 k_t, one lane per (t, a) and
+    // the sum over a across D consecutive lanes (D divides the wave)
+    static_assert(64 % D == 0 && (C * D) % kT3 == 0, "token-row lanes");
+    for (int e = tid; e < C * D; e += kT3) {
+      const int t = e / D, a = e % D;
+      double y = 0.0;
+#pragma unroll
+      for (int b = 0; b < D; ++b) y += (double)SQ[a * lD + b] * Ks[t * lD + b];
+      double g = (double)Ks[t * lD + a] * y, sm = (double)Qs[t * lD + a] * mv[a], w = (double)Qs[t * lD + a] * eta[a];
+#pragma unroll
+      for (int o = 1; o < D; o <<= 1) {
+        g += __shfl_xor(g, o);
+        sm += __shfl_xor(sm, o);
+        w += __shfl_xor(w, o);
       }
-      pm[t] = (float)s;
-      qeta[t] = (float)w;
-      sig[t] = (float)g;
+      if (a == 0) {
+        pm[t] = (float)sm;
+        qeta[t] = (float)w;
+        sig[t] = (float)g;
+      }
     }
     __syncthreads();
     // s2: prefixes inside the tile (strictly before j)
@@ -364,7 +374,8 @@ int tile3(int chunk) { return chunk >= 32 ? 32 : chunk; }
 void plan3(int BH, int n, int chunk, int* P, int* cps) {
   const int C = tile3(chunk);
   const int M = (n + C - 1) / C;
-  int p = 512 / BH;
+  int p = 256 / BH;   // measured: one tile per segment loses to two (the prologue sums every earlier record)
+  if (const char* e = getenv("HLA_FUSED_SEGMENTS")) p = atoi(e);
   if (p < 1) p = 1;
   if (p > M) p = M;
   *cps = (M + p - 1) / p;
