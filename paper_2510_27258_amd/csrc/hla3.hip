@@ -109,12 +109,35 @@ __global__ __launch_bounds__(kT3) void k3_moments(const T* __restrict__ q, const
   for (int o = tid; o < NO; o += kT3) r[o] = acc[o];
 }
 
+// Exclusive running sums over the segments of a head, for the floats
+// [off, off + len) of every record: pre[s] = sum_{s' < s} rec[s'].  grid
+// (ceil(len / kT3), BH); each thread one float, reads and writes coalesced.
+template <int D, int DV>
+__global__ __launch_bounds__(kT3) void k3_prefix(const float* __restrict__ rec, float* __restrict__ pre, int nseg,
+                                                 int off, int len) {
+  using Rc = Rec3<D, DV>;
+  const int e = blockIdx.x * kT3 + threadIdx.x;
+  if (e >= len) return;
+  const size_t base = (size_t)blockIdx.y * nseg * Rc::floats + off + e;
+  float x = 0.f;
+  for (int s0 = 0; s0 < nseg; s0 += 32) {    // 32 records' loads in flight at a time
+    float r[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) r[j] = s0 + j < nseg ? rec[base + (size_t)(s0 + j) * Rc::floats] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      if (s0 + j < nseg) pre[base + (size_t)(s0 + j) * Rc::floats] = x;
+      x += r[j];
+    }
+  }
+}
+
 // 2. The walk of one segment from its moment carry with F = 0.  grid (nseg, BH).
 template <typename T, int C, int D, int DV>
 __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T* __restrict__ k,
                                                const T* __restrict__ v, float* __restrict__ out,
-                                               float* __restrict__ den_out, float* __restrict__ rec, int n, int cps,
-                                               int nseg) {
+                                               float* __restrict__ den_out, float* __restrict__ rec,
+                                               const float* __restrict__ pre, int n, int cps, int nseg) {
   using Rc = Rec3<D, DV>;
   constexpr int lD = D + 1, lV = DV + 1, lC = C + 1;
   __shared__ float Qs[C * lD], Ks[C * lD], Vs[C * lV];
@@ -126,26 +149,18 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
   const size_t head_tok = (size_t)bh * n;
   float* recs = rec + (size_t)bh * nseg * Rc::floats;
 
-  // moment carry: sum of the segments before this one; F = eta = 0
+  // moment carry: the sum of the segments before this one (k3_prefix); F = eta = 0
+  const float* pr = pre + ((size_t)bh * nseg + seg) * Rc::floats;
   for (int e = tid; e < D * D; e += kT3) {
-    float sk = 0.f, sq = 0.f;
-    for (int sp = 0; sp < seg; ++sp) {
-      sk += recs[(size_t)sp * Rc::floats + Rc::oSK + e];
-      sq += recs[(size_t)sp * Rc::floats + Rc::oSQ + e];
-    }
-    SK[(e / D) * lD + e % D] = sk;
-    SQ[(e / D) * lD + e % D] = sq;
+    SK[(e / D) * lD + e % D] = pr[Rc::oSK + e];
+    SQ[(e / D) * lD + e % D] = pr[Rc::oSQ + e];
   }
   for (int e = tid; e < D * DV; e += kT3) {
-    float p = 0.f;
-    for (int sp = 0; sp < seg; ++sp) p += recs[(size_t)sp * Rc::floats + Rc::oP + e];
-    Pm[(e / DV) * lV + e % DV] = p;
+    Pm[(e / DV) * lV + e % DV] = pr[Rc::oP + e];
     F[(e / DV) * lV + e % DV] = 0.f;
   }
   for (int e = tid; e < D; e += kT3) {
-    float s = 0.f;
-    for (int sp = 0; sp < seg; ++sp) s += recs[(size_t)sp * Rc::floats + Rc::om + e];
-    mv[e] = s;
+    mv[e] = pr[Rc::om + e];
     eta[e] = 0.f;
   }
 
@@ -300,7 +315,7 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
 // 3. Add the F carry of earlier segments and normalise.  grid (nseg, BH).
 template <typename T, int C, int D, int DV>
 __global__ __launch_bounds__(kT3) void k3_fix(const T* __restrict__ q, float* __restrict__ out,
-                                              const float* __restrict__ den_in, const float* __restrict__ rec, int n,
+                                              const float* __restrict__ den_in, const float* __restrict__ pre, int n,
                                               int cps, int nseg, int normalized, float eps) {
   using Rc = Rec3<D, DV>;
   __shared__ float Fc[D * (DV + 1)], ec[D], Qs[C * (D + 1)], inv[C];
@@ -308,17 +323,9 @@ __global__ __launch_bounds__(kT3) void k3_fix(const T* __restrict__ q, float* __
   if (seg == 0 && !normalized) return;          // nothing to add
   const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
   const size_t head_tok = (size_t)bh * n;
-  const float* recs = rec + (size_t)bh * nseg * Rc::floats;
-  for (int e = tid; e < D * DV; e += kT3) {
-    float s = 0.f;
-    for (int sp = 0; sp < seg; ++sp) s += recs[(size_t)sp * Rc::floats + Rc::oF + e];
-    Fc[(e / DV) * (DV + 1) + e % DV] = s;
-  }
-  for (int e = tid; e < D; e += kT3) {
-    float s = 0.f;
-    for (int sp = 0; sp < seg; ++sp) s += recs[(size_t)sp * Rc::floats + Rc::oe + e];
-    ec[e] = s;
-  }
+  const float* pr = pre + ((size_t)bh * nseg + seg) * Rc::floats;   // the brackets before this segment
+  for (int e = tid; e < D * DV; e += kT3) Fc[(e / DV) * (DV + 1) + e % DV] = pr[Rc::oF + e];
+  for (int e = tid; e < D; e += kT3) ec[e] = pr[Rc::oe + e];
   for (int c = c0; c < c1; ++c) {
     const int t0 = c * C;
     for (int e = tid; e < C * D; e += kT3) {
@@ -348,23 +355,32 @@ __global__ __launch_bounds__(kT3) void k3_fix(const T* __restrict__ q, float* __
 }
 
 template <typename T, int C, int D, int DV>
-hipError_t run3(const Fwd& f, float* recs, float* den, int P, int cps, hipStream_t s) {
+hipError_t run3(const Fwd& f, float* recs, float* pre, float* den, int P, int cps, hipStream_t s) {
+  using Rc = Rec3<D, DV>;
   const T* q = static_cast<const T*>(f.q);
   const T* k = static_cast<const T*>(f.k);
   const T* v = static_cast<const T*>(f.v);
   const dim3 grid(P, f.BH);
+  constexpr int nmom = Rc::oF, nbr = Rc::floats - Rc::oF;   // moments SK|SQ|P|m, brackets F|eta
   prof_start("hla3_moments", s);
   HLA_LAUNCH((k3_moments<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, recs, f.n, cps, P);
   prof_stop(s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  prof_start("hla3_prefix", s);
+  HLA_LAUNCH((k3_prefix<D, DV>), dim3((nmom + kT3 - 1) / kT3, f.BH), dim3(kT3), 0, s, recs, pre, P, 0, nmom);
+  prof_stop(s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_start("hla3_walk", s);
-  HLA_LAUNCH((k3_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, den, recs, f.n, cps, P);
+  HLA_LAUNCH((k3_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, den, recs, pre, f.n, cps, P);
+  prof_stop(s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  prof_start("hla3_prefix", s);
+  HLA_LAUNCH((k3_prefix<D, DV>), dim3((nbr + kT3 - 1) / kT3, f.BH), dim3(kT3), 0, s, recs, pre, P, (int)Rc::oF, nbr);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_start("hla3_fix", s);
-  HLA_LAUNCH((k3_fix<T, C, D, DV>), grid, dim3(kT3), 0, s, q, f.out, den, recs, f.n, cps, P, f.normalized,
-                     f.eps);
+  HLA_LAUNCH((k3_fix<T, C, D, DV>), grid, dim3(kT3), 0, s, q, f.out, den, pre, f.n, cps, P, f.normalized, f.eps);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -374,7 +390,7 @@ int tile3(int chunk) { return chunk >= 32 ? 32 : chunk; }
 void plan3(int BH, int n, int chunk, int* P, int* cps) {
   const int C = tile3(chunk);
   const int M = (n + C - 1) / C;
-  int p = 256 / BH;   // measured: one tile per segment loses to two (the prologue sums every earlier record)
+  int p = 512 / BH;
   if (const char* e = getenv("HLA_FUSED_SEGMENTS")) p = atoi(e);
   if (p < 1) p = 1;
   if (p > M) p = M;
@@ -394,19 +410,20 @@ size_t hla3_workspace(int BH, int n, int d, int dv, int chunk) {
   int P, cps;
   plan3(BH, n, chunk, &P, &cps);
   const size_t a = ((sizeof(float) * (size_t)BH * P * rec_floats(d, dv)) + 255) & ~size_t(255);
-  return a + sizeof(float) * (size_t)BH * n + 256;
+  return 2 * a + sizeof(float) * (size_t)BH * n + 256;
 }
 
 hipError_t launch_hla3(const Fwd& f, void* workspace, hipStream_t s) {
   int P, cps;
   plan3(f.BH, f.n, f.chunk, &P, &cps);
   char* base = static_cast<char*>(workspace);
-  float* recs = reinterpret_cast<float*>(base);
-  float* den = reinterpret_cast<float*>(base + (((sizeof(float) * (size_t)f.BH * P * rec_floats(f.d, f.dv)) + 255) &
-                                                ~size_t(255)));
+  const size_t a = ((sizeof(float) * (size_t)f.BH * P * rec_floats(f.d, f.dv)) + 255) & ~size_t(255);
+  float* recs = reinterpret_cast<float*>(base);         // [BH][P] records
+  float* pre = reinterpret_cast<float*>(base + a);      // their exclusive running sums
+  float* den = reinterpret_cast<float*>(base + 2 * a);
   const int C = tile3(f.chunk);
 #define HLA3_CASE(T_, C_, D_, DV_) \
-  if (C == C_ && f.d == D_ && f.dv == DV_) return run3<T_, C_, D_, DV_>(f, recs, den, P, cps, s);
+  if (C == C_ && f.d == D_ && f.dv == DV_) return run3<T_, C_, D_, DV_>(f, recs, pre, den, P, cps, s);
 #define HLA3_DT(T_)                                                                                       \
   HLA3_CASE(T_, 16, 16, 16) HLA3_CASE(T_, 16, 16, 32) HLA3_CASE(T_, 16, 32, 16) HLA3_CASE(T_, 16, 32, 32) \
   HLA3_CASE(T_, 32, 16, 16) HLA3_CASE(T_, 32, 16, 32) HLA3_CASE(T_, 32, 32, 16) HLA3_CASE(T_, 32, 32, 32)
