@@ -7,12 +7,23 @@
 // One workgroup per head.  Every state element is read once and written
 // once: all of S, C and G are loaded up front (16-byte vector loads, up to
 // 48 per thread), then three dependent reductions over rows run through LDS.
+// The state (all heads together larger than the last-level cache) is
+// streamed once per step, so its loads and stores are non-temporal.
 #include "common.h"
 #include "profile.h"
 
 namespace hla {
 
 constexpr int kStepThreads = 256;
+typedef float nf4 __attribute__((ext_vector_type(4)));
+// 16-byte non-temporal load and store
+__device__ __forceinline__ float4 ntld(const float4* p) {
+  const nf4 x = __builtin_nontemporal_load(reinterpret_cast<const nf4*>(p));
+  return make_float4(x[0], x[1], x[2], x[3]);
+}
+__device__ __forceinline__ void ntst(const float4& v, float4* p) {
+  __builtin_nontemporal_store(nf4{v.x, v.y, v.z, v.w}, reinterpret_cast<nf4*>(p));
+}
 constexpr int kStepMaxVec = 16;   // d*d/4/256 and d*dv/4/256 at d = dv = 128
 
 template <typename T>
@@ -36,10 +47,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state
 #pragma unroll
   for (int r = 0; r < kStepMaxVec; ++r) {
     const int f = tid + kStepThreads * r;
-    if (f < nS4) Sv[r] = reinterpret_cast<const float4*>(S)[f];
+    if (f < nS4) Sv[r] = ntld(reinterpret_cast<const float4*>(S) + f);
     if (f < nC4) {
-      Cv[r] = reinterpret_cast<const float4*>(C)[f];
-      Gv[r] = reinterpret_cast<const float4*>(G)[f];
+      Cv[r] = ntld(reinterpret_cast<const float4*>(C) + f);
+      Gv[r] = ntld(reinterpret_cast<const float4*>(G) + f);
     }
   }
   float m_old = 0.f, h_old = 0.f;
@@ -68,7 +79,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state
         s.y += ka * ks[col + 1];
         s.z += ka * ks[col + 2];
         s.w += ka * ks[col + 3];
-        reinterpret_cast<float4*>(S)[f] = s;
+        ntst(s, reinterpret_cast<float4*>(S) + f);
         up[0] += qa * s.x; up[1] += qa * s.y; up[2] += qa * s.z; up[3] += qa * s.w;
       }
     }
@@ -92,7 +103,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state
         c.z += qa * vs[col + 2];
         c.w += qa * vs[col + 3];
         Cv[r] = c;
-        reinterpret_cast<float4*>(C)[f] = c;
+        ntst(c, reinterpret_cast<float4*>(C) + f);
       }
     }
     if (tid < nC4 && tid * 4 < 1024)
@@ -138,7 +149,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state
         g.y += ka * ws[col + 1];
         g.z += ka * ws[col + 2];
         g.w += ka * ws[col + 3];
-        reinterpret_cast<float4*>(G)[f] = g;
+        ntst(g, reinterpret_cast<float4*>(G) + f);
         np[0] += ua * c.x; np[1] += ua * c.y; np[2] += ua * c.z; np[3] += ua * c.w;
         if (masked) {
           np[0] -= qa * g.x; np[1] -= qa * g.y; np[2] -= qa * g.z; np[3] -= qa * g.w;
