@@ -175,19 +175,22 @@ int hla2_forward_decay(const void *q, const void *k, const void *v, float *out,
                        void *stream);
 
 /* ---------------------------------------------------------------------------
- * hla3_forward — masked third-order HLA over whole sequences (Sec. 7).
- * out[b,h,t,:] = q_t^T F_t with F_t the corrected third-order state (Eq.
- * hla3-corrected-state, Thm. 3): the sum, over triples (i, u, j) <= t whose
- * largest index is attained at least twice, of (q_t.k_i)(k_i.q_u)(q_u.k_j) v_j.
- * With normalized = 1 the row is divided by (q_t^T eta_t + eps), eta_t the
- * same sum without v_j.  Computed in fp32 by the chunk-parallel scan of Sec.
- * 7.3 (operator (x)_3, Thm. 4).
+ * hla3_forward — third-order HLA over whole sequences (Sec. 7).
+ * masked = 1: out[b,h,t,:] = q_t^T F_t with F_t the corrected third-order
+ * state (Eq. hla3-corrected-state, Thm. 3): the sum, over triples (i, u, j)
+ * <= t whose largest index is attained at least twice, of
+ * (q_t.k_i)(k_i.q_u)(q_u.k_j) v_j.  Computed in fp32 by the chunk-parallel
+ * scan of Sec. 7.3 (operator (x)_3, Thm. 4).
+ * masked = 0: out[b,h,t,:] = q_t^T S^K_t S^Q_t P_t (Sec. 7.1), the same sum
+ * over all triples (i, u, j) <= t; the summaries only add, so each segment is
+ * walked from the running sum of the moments before it.
+ * With normalized = 1 the row is divided by (den_t + eps), den_t the same sum
+ * without v_j (q_t^T eta_t masked, q_t^T S^K_t S^Q_t m^K_t unmasked).
  * q, k: [B, H, n, d]; v: [B, H, n, dv], fp32 or bf16 (dtype); out: [B, H, n, dv]
  * fp32; all device pointers, 16-byte aligned, caller-owned.
- * Supported: masked = 1, d and dv in {16, 32}, chunk in {16, 32, 64, 128};
- * chunks above 32 are walked in 32-token tiles (exact for any chunking,
- * Thm. 4).  Other arguments return HLA_ERR_UNSUPPORTED (masked = 0: the
- * unmasked operator q_t^T S^K_t S^Q_t P_t is not built on the GPU).
+ * Supported: d and dv in {16, 32}, chunk in {16, 32, 64, 128}; chunks above
+ * 32 are walked in 32-token tiles (exact for any chunking, Thm. 4).  Other
+ * sizes return HLA_ERR_UNSUPPORTED.
  * workspace: at least hla3_workspace_bytes(...) bytes of device memory (its
  * contents on entry are ignored); HLA_ERR_WORKSPACE if smaller.
  * ------------------------------------------------------------------------- */

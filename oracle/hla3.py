@@ -212,6 +212,22 @@ def hla3_den_scale(q, k):
     return (c * np.tril(np.ones((n, n)))).sum(axis=-1)
 
 
+def hla3_den_scale_unmasked(q, k):
+    """Scale for judging the unmasked denominator (Sec. 7.1):
+    D_t = sum_{i,u,j<=t} |q_t.k_i| |k_i.q_u| |q_u.k_j|, the sum of the absolute
+    values of the terms of den_t, so |den_t| <= D_t.  Per head over leading
+    batch axes; O(n^3) per head."""
+    q, k = _f64(q), _f64(k)
+    A = np.abs(np.einsum("...ud,...jd->...uj", q, k))     # A[u, j] = |q_u . k_j|
+    n = q.shape[-2]
+    out = np.empty(q.shape[:-1])
+    for t in range(n):
+        x = A[..., : t + 1, : t + 1].sum(-1)                             # over j, per u
+        y = np.einsum("...ui,...u->...i", A[..., : t + 1, : t + 1], x)   # over u, per i
+        out[..., t] = (A[..., t, : t + 1] * y).sum(-1)                   # over i
+    return out
+
+
 # ---------------------------------------------------------------------------
 # Segment scan state and the operator (x)_3
 # ---------------------------------------------------------------------------

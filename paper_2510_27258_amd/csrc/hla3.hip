@@ -354,6 +354,151 @@ __global__ __launch_bounds__(kT3) void k3_fix(const T* __restrict__ q, float* __
   }
 }
 
+// The unmasked operator (Sec. 7.1): o_t = q_t^T S^K_t S^Q_t P_t, den_t =
+// q_t^T S^K_t S^Q_t m^K_t, every summary inclusive.  With the moment carry
+// (SK0, SQ0, P0, m0) of the tokens before the tile and W = L (.) Q K^T:
+//   R   = Q SK0 + W K                         (row t: q_t^T S^K_t)
+//   Sm  = R SQ0 + (L (.) R Q^T) Q             (row t: q_t^T S^K_t S^Q_t)
+//   O   = Sm P0 + (L (.) Sm K^T) V,   den = Sm m0 + (L (.) Sm K^T) 1.
+// The summaries only add, so a segment's walk from the moment prefix gives
+// its outputs whole: no bracket and no fix-up.  Dot products accumulate in
+// fp64; R and Sm are kept in fp64.  grid (nseg, BH).
+template <typename T, int C, int D, int DV>
+__global__ __launch_bounds__(kT3) void k3u_walk(const T* __restrict__ q, const T* __restrict__ k,
+                                                const T* __restrict__ v, float* __restrict__ out,
+                                                const float* __restrict__ pre, int n, int cps, int nseg,
+                                                int normalized, float eps) {
+  using Rc = Rec3<D, DV>;
+  constexpr int lD = D + 1, lV = DV + 1, lC = C + 1;
+  __shared__ float Qs[C * lD], Ks[C * lD], Vs[C * lV];
+  __shared__ float SK[D * lD], SQ[D * lD], Pm[D * lV], mv[D];
+  __shared__ float W[C * lC], U[C * lC], Tm[C * lC];
+  __shared__ double R[C * lD], Sm[C * lD], dn[C];
+  const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
+  const size_t head_tok = (size_t)bh * n;
+
+  const float* pr = pre + ((size_t)bh * nseg + seg) * Rc::floats;   // moments of the segments before
+  for (int e = tid; e < D * D; e += kT3) {
+    SK[(e / D) * lD + e % D] = pr[Rc::oSK + e];
+    SQ[(e / D) * lD + e % D] = pr[Rc::oSQ + e];
+  }
+  for (int e = tid; e < D * DV; e += kT3) Pm[(e / DV) * lV + e % DV] = pr[Rc::oP + e];
+  for (int e = tid; e < D; e += kT3) mv[e] = pr[Rc::om + e];
+
+  for (int c = c0; c < c1; ++c) {
+    const int t0 = c * C;
+    stage_tile<T, C, D, DV>(q, k, v, head_tok, t0, n, Qs, Ks, Vs);
+    __syncthreads();
+    // W = L (.) Q K^T;  R = Q SK0 (first part)
+    for (int e = tid; e < C * C; e += kT3) {
+      const int t = e / C, i = e % C;
+      double s = 0.0;
+      if (i <= t) {
+#pragma unroll 8
+        for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * Ks[i * lD + a];
+      }
+      W[t * lC + i] = (float)s;
+    }
+    for (int e = tid; e < C * D; e += kT3) {
+      const int t = e / D, b = e % D;
+      double s = 0.0;
+#pragma unroll 8
+      for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * SK[a * lD + b];
+      R[t * lD + b] = s;
+    }
+    __syncthreads();
+    // R += W K
+    for (int e = tid; e < C * D; e += kT3) {
+      const int t = e / D, b = e % D;
+      double s = R[t * lD + b];
+      for (int i = 0; i <= t; ++i) s += (double)W[t * lC + i] * Ks[i * lD + b];
+      R[t * lD + b] = s;
+    }
+    __syncthreads();
+    // U = L (.) R Q^T
+    for (int e = tid; e < C * C; e += kT3) {
+      const int t = e / C, u = e % C;
+      double s = 0.0;
+      if (u <= t) {
+#pragma unroll 8
+        for (int b = 0; b < D; ++b) s += R[t * lD + b] * Qs[u * lD + b];
+      }
+      U[t * lC + u] = (float)s;
+    }
+    __syncthreads();
+    // Sm = R SQ0 + U Q
+    for (int e = tid; e < C * D; e += kT3) {
+      const int t = e / D, b = e % D;
+      double s = 0.0;
+#pragma unroll 8
+      for (int a = 0; a < D; ++a) s += R[t * lD + a] * SQ[a * lD + b];
+      for (int u = 0; u <= t; ++u) s += (double)U[t * lC + u] * Qs[u * lD + b];
+      Sm[t * lD + b] = s;
+    }
+    __syncthreads();
+    // Tm = L (.) Sm K^T;  the carry part of den
+    for (int e = tid; e < C * C; e += kT3) {
+      const int t = e / C, j = e % C;
+      double s = 0.0;
+      if (j <= t) {
+#pragma unroll 8
+        for (int b = 0; b < D; ++b) s += Sm[t * lD + b] * Ks[j * lD + b];
+      }
+      Tm[t * lC + j] = (float)s;
+    }
+    for (int t = tid; t < C; t += kT3) {
+      double s = 0.0;
+      for (int a = 0; a < D; ++a) s += Sm[t * lD + a] * mv[a];
+      dn[t] = s;
+    }
+    __syncthreads();
+    if (normalized)
+      for (int t = tid; t < C; t += kT3) {
+        double s = dn[t];
+        for (int j = 0; j <= t; ++j) s += Tm[t * lC + j];
+        dn[t] = s;
+      }
+    __syncthreads();
+    // O = Sm P0 + Tm V
+    for (int e = tid; e < C * DV; e += kT3) {
+      const int t = e / DV, b = e % DV;
+      if (t0 + t >= n) continue;
+      double s = 0.0;
+#pragma unroll 8
+      for (int a = 0; a < D; ++a) s += Sm[t * lD + a] * Pm[a * lV + b];
+      for (int j = 0; j <= t; ++j) s += (double)Tm[t * lC + j] * Vs[j * lV + b];
+      float y = (float)s;
+      if (normalized) y = (float)(s / (dn[t] + (double)eps));
+      out[(head_tok + t0 + t) * DV + b] = y;
+    }
+    __syncthreads();
+    // advance the moments past this tile
+    for (int e = tid; e < D * DV; e += kT3) {
+      const int a = e / DV, b = e % DV;
+      float p = 0.f;
+      for (int j = 0; j < C; ++j) p += Ks[j * lD + a] * Vs[j * lV + b];
+      Pm[a * lV + b] += p;
+    }
+    for (int e = tid; e < D * D; e += kT3) {
+      const int a = e / D, b = e % D;
+      float sk = 0.f, sq = 0.f;
+      for (int j = 0; j < C; ++j) {
+        sk += Ks[j * lD + a] * Ks[j * lD + b];
+        sq += Qs[j * lD + a] * Qs[j * lD + b];
+      }
+      SK[a * lD + b] += sk;
+      SQ[a * lD + b] += sq;
+    }
+    for (int a = tid; a < D; a += kT3) {
+      float s = 0.f;
+      for (int j = 0; j < C; ++j) s += Ks[j * lD + a];
+      mv[a] += s;
+    }
+    __syncthreads();
+  }
+}
+
 template <typename T, int C, int D, int DV>
 hipError_t run3(const Fwd& f, float* recs, float* pre, float* den, int P, int cps, hipStream_t s) {
   using Rc = Rec3<D, DV>;
@@ -371,6 +516,13 @@ hipError_t run3(const Fwd& f, float* recs, float* pre, float* den, int P, int cp
   HLA_LAUNCH((k3_prefix<D, DV>), dim3((nmom + kT3 - 1) / kT3, f.BH), dim3(kT3), 0, s, recs, pre, P, 0, nmom);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (!f.masked) {     // the unmasked operator: outputs whole from the moment prefix
+    prof_start("hla3_walk", s);
+    HLA_LAUNCH((k3u_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, pre, f.n, cps, P, f.normalized,
+               f.eps);
+    prof_stop(s);
+    return hipGetLastError();
+  }
   prof_start("hla3_walk", s);
   HLA_LAUNCH((k3_walk<T, C, D, DV>), grid, dim3(kT3), 0, s, q, k, v, f.out, den, recs, pre, f.n, cps, P);
   prof_stop(s);
@@ -403,7 +555,8 @@ size_t rec_floats(int d, int dv) { return 2 * (size_t)d * d + 2 * (size_t)d * dv
 }  // namespace
 
 bool hla3_supported(int d, int dv, int chunk, int masked) {
-  return masked == 1 && (d == 16 || d == 32) && (dv == 16 || dv == 32) && (chunk >= 16 && chunk <= 128);
+  return (masked == 0 || masked == 1) && (d == 16 || d == 32) && (dv == 16 || dv == 32) &&
+         (chunk >= 16 && chunk <= 128);
 }
 
 size_t hla3_workspace(int BH, int n, int d, int dv, int chunk) {

@@ -379,7 +379,7 @@ int hla3_forward(const void* q, const void* k, const void* v, float* out, int B,
       (rc = check_ptr(out, "out")))
     return rc;
   if (!hla::hla3_supported(d, dv, chunk, masked))
-    return fail(HLA_ERR_UNSUPPORTED, "hla3_forward needs masked=1 and d, dv in {16, 32} (got masked=%d d=%d dv=%d)",
+    return fail(HLA_ERR_UNSUPPORTED, "hla3_forward needs d, dv in {16, 32} (got masked=%d d=%d dv=%d)",
                 masked, d, dv);
   const int BH = B * H;
   const size_t need = hla::hla3_workspace(BH, n, d, dv, chunk);

@@ -197,7 +197,7 @@ def ahla_forward(q, k, v, chunk, normalized=False, eps=1e-6, out=None, workspace
 
 
 def hla3_forward(q, k, v, chunk, masked=True, normalized=False, eps=1e-6, out=None, workspace=None):
-    """Third-order masked HLA, q, k [B,H,n,d], v [B,H,n,dv] -> out fp32."""
+    """Third-order HLA (masked or unmasked), q, k [B,H,n,d], v [B,H,n,dv] -> out fp32."""
     _check(q, k, v)
     B, H, n, d = q.shape
     dv = v.shape[-1]

@@ -1,5 +1,6 @@
-"""GPU parity of the masked third-order HLA forward (Sec. 7) against the fp64
-oracle (Alg. 3 in C, itself pinned by the brute-force triple sum and Alg. 4).
+"""GPU parity of the third-order HLA forward (Sec. 7), masked and unmasked,
+against the fp64 oracle (Alg. 3 in C, itself pinned by the brute-force triple
+sum and Alg. 4).
 
 Every call goes through the C ABI.  Bars: 1e-5 (fp32 inputs) and 2e-3 (bf16
 inputs) on the row-wise relative error; the ratio-normalised output is judged
@@ -27,24 +28,27 @@ def _say(*a):
     sys.stdout.flush()
 
 
-def _check(B, H, n, d, dv, chunk, dist, normalized=False, seed=0, eps=1e-6):
+def _check(B, H, n, d, dv, chunk, dist, normalized=False, seed=0, eps=1e-6, masked=True):
     q, k, v, code = gen(B, H, n, d, dv, dist, seed)
-    _say(f"case hla3 B={B} H={H} n={n} d={d} dv={dv} chunk={chunk} dist={dist} normalized={normalized}")
+    _say(f"case hla3 B={B} H={H} n={n} d={d} dv={dv} chunk={chunk} dist={dist} normalized={normalized} "
+         f"masked={masked}")
     qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
-    num_ref, den_ref, _ = native.hla3_serial_c(q, k, v, masked=True, threads=16)
+    num_ref, den_ref, _ = native.hla3_serial_c(q, k, v, masked=masked, threads=16)
     tol = tol_for(code)
-    num = hla.hla3_forward(qd, kd, vd, chunk).cpu().numpy()
+    num = hla.hla3_forward(qd, kd, vd, chunk, masked=masked).cpu().numpy()
     err = rowwise_err(num, num_ref)
     assert err <= tol, f"num row-wise error {err:.3e} > {tol}"
     if normalized:
-        out = hla.hla3_forward(qd, kd, vd, chunk, normalized=True, eps=eps).cpu().numpy()
+        out = hla.hla3_forward(qd, kd, vd, chunk, masked=masked, normalized=True, eps=eps).cpu().numpy()
         ones = torch.ones(B, H, n, dv, dtype=vd.dtype, device="cuda")
-        den = hla.hla3_forward(qd, kd, ones, chunk)[..., 0].cpu().numpy()
-        D = O3.hla3_den_scale(q, k)
+        den = hla.hla3_forward(qd, kd, ones, chunk, masked=masked)[..., 0].cpu().numpy()
+        D = O3.hla3_den_scale(q, k) if masked else O3.hla3_den_scale_unmasked(q, k)
         e_den = float((np.abs(den - den_ref) / D).max())
         assert e_den <= tol, f"den error {e_den:.3e} > {tol}"
         good = np.abs(den_ref + eps) >= 0.05 * D
-        assert good.mean() > 0.3
+        # the unmasked den_t sums t^3 terms whose signed sum grows only like
+        # t^2.5 on these inputs, so fewer of its rows clear the bar
+        assert good.mean() > (0.3 if masked else 0.1)
         ref = num_ref / (den_ref + eps)[..., None]
         e_out = rowwise_err(out[good], ref[good])
         assert e_out <= tol, f"normalised output error {e_out:.3e} > {tol}"
@@ -86,14 +90,45 @@ def test_hla3_workload_all_heads():
     _say(f"hla3 workload row-wise error {err:.3e}")
 
 
+@pytest.mark.parametrize("d,dv", [(16, 16), (16, 32), (32, 16), (32, 32)])
+@pytest.mark.parametrize("chunk", [16, 32, 64])
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_hla3_unmasked_shapes(d, dv, chunk, dist):
+    """The unmasked operator q_t^T S^K_t S^Q_t P_t (Sec. 7.1): several tiles
+    with a ragged tail, a one-token sequence, and a length off the tile grid."""
+    for (B, H, n) in ((1, 2, 3 * chunk + 5), (2, 1, 1), (1, 3, 100)):
+        _check(B, H, n, d, dv, chunk, dist, seed=n + d + 1, masked=False)
+
+
+@pytest.mark.parametrize("dist", ["scaled", "unit"])
+def test_hla3_unmasked_normalized(dist):
+    _check(2, 2, 150, 16, 16, 32, dist, normalized=True, seed=4, masked=False)
+
+
+def test_hla3_unmasked_first_rows_and_segments():
+    """Rows near the start (o_1 = (q_1.k_1)^3 v_1) on fp32 inputs, and head
+    counts that give one and many segments per head."""
+    for seed in range(4):
+        _check(1, 2, 200, 16, 16, 32, "scaled", seed=seed, masked=False)
+    for (B, H) in ((1, 1), (4, 16)):
+        _check(B, H, 700, 16, 16, 32, "scaled", seed=B * H, masked=False)
+
+
+def test_hla3_unmasked_workload_all_heads():
+    """B1 H8 n2048 d=dv=16 fp32, chunk 32, unmasked: every head against the oracle."""
+    w = I.WORKLOADS["hla3-masked-fp32-B1H8-n2048-d16-C32"]
+    err = _check(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], w["dist"], seed=w["seed"], masked=False)
+    _say(f"hla3 unmasked workload row-wise error {err:.3e}")
+
+
 def test_hla3_errors():
     q = torch.zeros(1, 1, 64, 16, device="cuda")
     ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
     out = torch.empty(1, 1, 64, 16, device="cuda")
     args = (q.data_ptr(), q.data_ptr(), q.data_ptr(), out.data_ptr(), 1, 1, 64, 16, 16, 32)
-    with pytest.raises(capi.HLAError) as ei:          # unmasked is not built on the GPU
-        capi.hla3_forward(*args, 0, 0, 1e-6, I.HLA_FP32, ws.data_ptr(), ws.numel(), None)
-    assert ei.value.code == capi.HLA_ERR_UNSUPPORTED
+    with pytest.raises(capi.HLAError) as ei:          # masked flag out of range
+        capi.hla3_forward(*args, 2, 0, 1e-6, I.HLA_FP32, ws.data_ptr(), ws.numel(), None)
+    assert ei.value.code == capi.HLA_ERR_INVALID
     with pytest.raises(capi.HLAError) as ei:          # workspace too small
         capi.hla3_forward(*args, 1, 0, 1e-6, I.HLA_FP32, ws.data_ptr(), 16, None)
     assert ei.value.code == capi.HLA_ERR_WORKSPACE

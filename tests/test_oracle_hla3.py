@@ -183,6 +183,22 @@ def test_den_scale_bounds_den():
     assert np.all(np.abs(den) <= D * (1 + 1e-12) + 1e-12)
 
 
+def test_unmasked_den_scale_bounds_den():
+    """|den_t| <= D_t, with equality when every term is nonnegative (q = k
+    with nonnegative entries); brute force over the triples on a tiny case."""
+    q, k, v = _rand(9, 3, 1, seed=21)
+    (_, den), _ = H.hla3_serial(q, k, v, masked=False, return_num_den=True)
+    D = H.hla3_den_scale_unmasked(q, k)
+    assert np.all(np.abs(den) <= D * (1 + 1e-12))
+    n = 5
+    brute = np.array([sum(abs(q[t] @ k[i]) * abs(k[i] @ q[u]) * abs(q[u] @ k[j])
+                          for i in range(t + 1) for u in range(t + 1) for j in range(t + 1)) for t in range(n)])
+    np.testing.assert_allclose(D[:n], brute, rtol=1e-12)
+    p = np.abs(q)
+    (_, dp), _ = H.hla3_serial(p, p, v, masked=False, return_num_den=True)
+    np.testing.assert_allclose(H.hla3_den_scale_unmasked(p, p), dp, rtol=1e-12)
+
+
 def test_c_oracle_matches_numpy():
     if not native.available():
         pytest.skip("C oracle not built")
