@@ -242,9 +242,10 @@ def measure_scan(w, qd, kd, vd, reps=10):
             "peak": HBM_PEAK_GBS, "frac": nbytes / ms / 1e6 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes}
 
 
-def measure_hla3(reps=20):
-    """hla3_forward on the masked third-order workload (B1 H8 n2048 d=dv=16,
-    fp32, chunk 32): tokens/s by HIP events, and per-kernel times."""
+def measure_hla3(reps=20, masked=True):
+    """hla3_forward on the third-order workload (B1 H8 n2048 d=dv=16, fp32,
+    chunk 32), masked or unmasked: tokens/s by HIP events, and per-kernel
+    times."""
     import torch
     import paper_2510_27258_amd as hla
     from paper_2510_27258_amd import capi
@@ -257,7 +258,7 @@ def measure_hla3(reps=20):
     out = torch.empty(w["B"], w["H"], w["n"], w["dv"], dtype=torch.float32, device=dev)
     wsb = capi.hla3_workspace_bytes(w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"], code)
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
-    run = lambda: hla.hla3_forward(qd, kd, vd, w["chunk"], out=out, workspace=ws)
+    run = lambda: hla.hla3_forward(qd, kd, vd, w["chunk"], masked=masked, out=out, workspace=ws)
     for _ in range(3):
         run()
     torch.cuda.synchronize()
@@ -275,6 +276,8 @@ def measure_hla3(reps=20):
     prof = capi.hla_profile_summary()
     capi.hla_profile_end()
     tokens = w["B"] * w["H"] * w["n"]
+    if not masked:
+        name = name.replace("masked", "unmasked")
     return {"workload": name, "value": tokens / (ms / 1e3), "unit": "tokens/s", "ms": ms, "dtype": "f32",
             "kernels_ms": {k_: v_[1] / v_[0] for k_, v_ in prof.items()}}
 
@@ -491,7 +494,7 @@ def main():
     ap.add_argument("--no-decay", action="store_true", help="skip the decayed-forward measurement")
     ap.add_argument("--no-ahla", action="store_true", help="skip the AHLA measurement")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
-    ap.add_argument("--only", choices=["ahla", "decay", "hla3", "backward"],
+    ap.add_argument("--only", choices=["ahla", "decay", "hla3", "hla3u", "backward"],
                     help="run only that measurement and print its record (for profiling one path)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
@@ -521,7 +524,7 @@ def main():
 
     if args.only:
         rec = {"ahla": measure_ahla, "decay": measure_decay, "hla3": measure_hla3,
-               "backward": measure_backward}[args.only]()
+               "hla3u": lambda: measure_hla3(masked=False), "backward": measure_backward}[args.only]()
         print(json.dumps(rec), flush=True)
         return
 
@@ -604,6 +607,7 @@ def main():
         rec["scan"] = measure_scan(w, qd, kd, vd)
     if not args.no_hla3:
         rec["hla3"] = measure_hla3()
+        rec["hla3_unmasked"] = measure_hla3(masked=False)
     if not args.no_decay:
         rec["decay"] = measure_decay()
     if not args.no_ahla:
