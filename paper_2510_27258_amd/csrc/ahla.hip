@@ -90,7 +90,8 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
   float* rs = fl + G::f_rs;   // [2][C] row sums of A per key row tile
   float* sv = fl + G::f_s;    // s_t
 
-  const int seg = blockIdx.x, bh = blockIdx.y;
+  int seg, bh;
+  seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rt = w / G::NCT, ct = w % G::NCT;

@@ -290,7 +290,8 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
   float* colsum = fl + G::f_cs;       // [RT][D]
   float* denp = fl + G::f_denp;       // [RT][C]
 
-  const int seg = blockIdx.x, bh = blockIdx.y;
+  int seg, bh;
+  seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: per-wave branches stay scalar
   const int ct = w % G::NCT, rg = G::NRG == 1 ? 0 : w / G::NCT;
@@ -680,7 +681,8 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   float* w1 = g2 + C;                 // gamma^(C-1-a),
   float* w2 = w1 + C;                 // gamma^(2(C-1-a))
 
-  const int seg = blockIdx.x, bh = blockIdx.y;
+  int seg, bh;
+  seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = w / G::NCT, ct = w % G::NCT;          // state row half, column tile

@@ -62,6 +62,23 @@ __device__ __forceinline__ void buf_store16(rsrc_t r, uint32_t off, const float4
                                          r, (int)off, 0, 0);
 }
 
+// Workgroup -> (segment, head) for the walks, grid (segments, heads): a
+// walk's prologue reads the moment records of the segments before it, so the
+// segments of one head go to one XCD and share those reads through its L2.
+// Workgroups are dealt to the 8 XCDs round-robin by linear index, so the k-th
+// workgroup on XCD x takes pair x * (total / 8) + k.
+__device__ __forceinline__ void seg_head(int& seg, int& bh) {
+  const int P = gridDim.x, total = gridDim.x * gridDim.y, L = blockIdx.x + gridDim.x * blockIdx.y;
+  if (total % 8) {
+    seg = blockIdx.x;
+    bh = blockIdx.y;
+    return;
+  }
+  const int idx = (L % 8) * (total / 8) + L / 8;
+  seg = idx % P;
+  bh = idx / P;
+}
+
 // Lane layout of v_mfma_f32_32x32x16_bf16 (l = lane, r = l % 32, g = l / 32):
 //   A: row r, k = 8g .. 8g+7;  B: column r, the same k (any k order shared by
 //   A and B gives the same product);  D: element e is D[8(e/4) + 4g + e%4][r].

@@ -114,7 +114,8 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   uint16_t* A2h = Xl;             // TWO: A2 = X Z^T masked, in the (unused) lo tiles of x and y
   uint16_t* A2l = Yl;
 
-  const int seg = blockIdx.x, bh = blockIdx.y;
+  int seg, bh;
+  seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rt = w / G::NCT, ct = w % G::NCT;
