@@ -64,7 +64,8 @@ __device__ __forceinline__ void buf_store16(rsrc_t r, uint32_t off, const float4
 
 // Workgroup -> (segment, head) for the walks, grid (segments, heads): a
 // walk's prologue reads the moment records of the segments before it, so the
-// segments of one head go to one XCD and share those reads through its L2.
+// segments of one head go to one XCD and share those reads through its L2
+// (the fix-up uses it for its tile groups, which share carry reads).
 // Workgroups are dealt to the 8 XCDs round-robin by linear index, so the k-th
 // workgroup on XCD x takes pair x * (total / 8) + k.
 __device__ __forceinline__ void seg_head(int& seg, int& bh) {
@@ -483,10 +484,14 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
   uint16_t* Qs = lds;
   float* es = reinterpret_cast<float*>(Qs + C * ldQ);
   float* inv = es + D;
-  const int bh = blockIdx.y, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
+  // d <= 64: a head's tile groups on one XCD, where they share the reads of
+  // their segments' carries (at d = 128 the spread placement measured faster)
+  int grp = blockIdx.x, bh = blockIdx.y;
+  if constexpr (D <= 64) seg_head(grp, bh);
+  const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), ct = w % F::VT, rt = w / F::VT;
   const int M = (n + C - 1) / C;
-  int c0 = blockIdx.x * tpw;
+  int c0 = grp * tpw;
   const int c1 = min(M, c0 + tpw);
   if (!has_init && !normalized) c0 = max(c0, cps);
   if (c0 >= c1) return;
