@@ -1094,8 +1094,11 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   prof_start("moments", s);
-  HLA_LAUNCH((k_moments<C, D, DV, false, DEC>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P,
-             final_state ? 1 : 0, lg2g);
+  if (final_state)
+    HLA_LAUNCH((k_moments<C, D, DV, false, DEC>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1, lg2g);
+  else
+    HLA_LAUNCH((k_moments<C, D, DV, false, DEC, false>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 0,
+               lg2g);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   prof_start(f.out ? "walk" : "walk_summary", s);

@@ -212,17 +212,23 @@ __device__ __forceinline__ void store_N(const f32x16& acc, uint16_t* Xh, uint16_
 // DEC (decay gamma = 2^lg2g; S only): S = sum_t gamma^(e - t) k_t k_t^T with e
 // the segment's last token, the weight applied to one factor per token in
 // fp32 and split hi/lo.
-template <int C, int D, int DV, bool KV = false, bool DEC = false>
+// CM = false compiles the S-only form alone (want_cm is ignored): without the
+// C and m registers and buffers it runs at a higher occupancy.
+template <int C, int D, int DV, bool KV = false, bool DEC = false, bool CM = true>
 __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v, float* __restrict__ rec, int n,
                                                       int cps, int nseg, int want_cm, float lg2g) {
   constexpr int ld = C + kPad, DT = D / 32, VT = DV / 32, KC = C / 16;
   constexpr int nS = (DT * DT + kWaves - 1) / kWaves, nC = (DT * VT + kWaves - 1) / kWaves;
   constexpr int segQ = C * D / 8, segV = C * DV / 8;
-  __shared__ __align__(16) uint16_t Kt[D * ld], Qs_[KV ? 8 : D * ld], Vt[DV * ld];
+  // Kt: K^T (C and m path) or a row-major k tile (S-only path)
+  constexpr int nKt = D * ld > C * (D + 16) ? D * ld : C * (D + 16);
+  __shared__ __align__(16) uint16_t Kt[nKt], Qs_[(KV || !CM) ? 8 : D * ld], Vt[CM ? DV * ld : 8];
   uint16_t* Qt = KV ? Kt : Qs_;          // the left factor of the C slot
   __shared__ __align__(16) float wtab[DEC ? C : 4];   // decay weights of the current tile's tokens
+  static_assert(CM || !KV, "the AHLA moments form K^T V");
   if (KV) want_cm = 1;
+  if (!CM) want_cm = 0;
   const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
@@ -238,16 +244,20 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
   if (!want_cm) {
     // S only: K tiles streamed through a ring of PF register slots (loads are
     // unconditional; the tile index is clamped to the segment), so PF tiles
-    // are in flight while one is multiplied
-    constexpr int PF = 4, NL = (segQ + kThreads - 1) / kThreads;
+    // are in flight while one is multiplied.  A tile sits row-major in LDS
+    // (16-byte stores) and the K^T fragments are read through the transpose
+    // unit; a row stride of 8 banks modulo 32 keeps the four rows of each
+    // 16-lane transposed read in different banks.
+    constexpr int PF = 4, NL = (segQ + kThreads - 1) / kThreads, ldk = D + 16;
+    uint16_t* Ks = Kt;
     uint4 kb[PF][NL];
     auto load = [&](int c, auto slot_tag) {
       constexpr int sl = decltype(slot_tag)::value;
       const uint32_t t0 = (uint32_t)min(c, c1 - 1) * C;
 #pragma unroll
-      for (int i = 0; i < NL; ++i) {
+      for (int i = 0; i < NL; ++i) {      // consecutive lanes take consecutive pieces of a token row
         const int e = min(tid + kThreads * i, segQ - 1);
-        kb[sl][i] = buf_load16(rk, ((t0 + e % C) * D + (e / C) * 8) * 2);
+        kb[sl][i] = buf_load16(rk, ((t0 + e / (D / 8)) * D + (e % (D / 8)) * 8) * 2);
       }
     };
     auto step = [&](int c, auto slot_tag) {
@@ -256,12 +266,7 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const int e = tid + kThreads * i;
-        if (e < segQ) {
-          const int t = e % C, a8 = (e / C) * 8;
-          const uint16_t* k8 = reinterpret_cast<const uint16_t*>(&kb[sl][i]);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
-        }
+        if (e < segQ) *reinterpret_cast<uint4*>(Ks + (e / (D / 8)) * ldk + (e % (D / 8)) * 8) = kb[sl][i];
       }
       lds_barrier();
       load(c + PF, slot_tag);
@@ -272,14 +277,14 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
           const int it = ti / DT, jt = ti % DT;
 #pragma unroll
           for (int s = 0; s < KC; ++s) {
+            const bf16x8 a = frag_tr(Ks, ldk, it * 32, s * 16);
             if constexpr (DEC) {
               bf16x8 bh, bl;
-              scale_split(frag(Kt, ld, jt * 32, s * 16), wtab + s * 16 + 8 * lg, bh, bl);
-              const bf16x8 a = frag(Kt, ld, it * 32, s * 16);
+              scale_split(frag_tr(Ks, ldk, jt * 32, s * 16), wtab + s * 16 + 8 * lg, bh, bl);
               sacc[i] = mfma(a, bh, sacc[i]);
               sacc[i] = mfma(a, bl, sacc[i]);
             } else {
-              sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
+              sacc[i] = mfma(a, frag_tr(Ks, ldk, jt * 32, s * 16), sacc[i]);
             }
           }
         }
