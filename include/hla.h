@@ -33,7 +33,10 @@
  *     stores the records of all heads back to back.  The all-zero record is
  *     the identity segment (Thm. 2).
  *   - Supported sizes: d, dv in {16, 32, 64, 128}; chunk in {16, 32, 64,
- *     128}; any n >= 1 (a short last chunk is exact); B*H <= 65535.
+ *     128}; any n >= 1 (a short last chunk is exact) with
+ *     n * max(d, dv) * 4 < 2^31 (one head's fp32 rows stay within 32-bit
+ *     byte offsets: n < 4 194 304 at d = dv = 128), else HLA_ERR_UNSUPPORTED;
+ *     B*H <= 65535.
  *     masked, normalized in {0, 1}; eps finite and >= 0 (added to the
  *     denominator as is, den + eps).  Decay is 1 (hla2_forward_decay takes
  *     a decay) and the ridge 0.

@@ -46,6 +46,9 @@ int check_dims(int B, int H, int n, int d, int dv, int chunk, int dtype, bool ne
   if (need_n && n < 1) return fail(HLA_ERR_INVALID, "n must be >= 1 (got %d)", n);
   if (!pow2_in(d, 16, 128) || !pow2_in(dv, 16, 128))
     return fail(HLA_ERR_UNSUPPORTED, "d and dv must be one of 16, 32, 64, 128 (got d=%d dv=%d)", d, dv);
+  // kernels address one head's rows with 32-bit byte offsets
+  if (need_n && (long long)n * (d > dv ? d : dv) * 4 >= (1LL << 31))
+    return fail(HLA_ERR_UNSUPPORTED, "n=%d is too long: n*max(d,dv)*4 must stay below 2^31 bytes", n);
   if (chunk != 0 && !pow2_in(chunk, 16, 128))
     return fail(HLA_ERR_UNSUPPORTED, "chunk must be one of 16, 32, 64, 128 (got %d)", chunk);
   if (dtype != HLA_FP32 && dtype != HLA_BF16) return fail(HLA_ERR_INVALID, "dtype must be HLA_FP32 or HLA_BF16");

@@ -74,6 +74,8 @@ def test_forward_rejects_empty_and_bad_sizes():
     for kw, code, text in ((dict(n=0), INVALID, "n must be"), (dict(n=-5), INVALID, "n must be"),
                            (dict(B=0), INVALID, "B and H"), (dict(H=-1), INVALID, "B and H"),
                            (dict(B=256, H=256), UNSUP, "exceeds"), (dict(d=24), UNSUP, "d and dv"),
+                           (dict(n=1 << 23), UNSUP, "too long"), (dict(n=2**31 - 1), UNSUP, "too long"),
+                           (dict(n=(1 << 22), d=128, dv=128), UNSUP, "too long"),
                            (dict(dv=256), UNSUP, "d and dv"), (dict(d=8), UNSUP, "d and dv"),
                            (dict(chunk=48), UNSUP, "chunk"), (dict(chunk=0), INVALID, "chunk must be set"),
                            (dict(dtype=2), INVALID, "dtype"), (dict(masked=2), INVALID, "masked"),
@@ -81,6 +83,14 @@ def test_forward_rejects_empty_and_bad_sizes():
                            (dict(eps=-1.0), INVALID, "eps")):
         assert _fwd(L, **kw) == code, kw
         assert text in capi.hla_last_error(), (kw, capi.hla_last_error())
+
+
+def test_longest_sequence_passes_the_size_checks():
+    """n = 2^22 - 1 at d = dv = 128 is the longest accepted sequence: it gets past
+    every size check to the pointer checks (NULL q)."""
+    L = capi.lib()
+    assert _fwd(L, n=(1 << 22) - 1, d=128, dv=128) == INVALID and "q is NULL" in capi.hla_last_error()
+    assert _fwd(L, n=(1 << 23) - 1, d=64, dv=64) == INVALID and "q is NULL" in capi.hla_last_error()
 
 
 def test_forward_rejects_null_and_misaligned_pointers():
