@@ -173,6 +173,13 @@ def test_fused_segment_counts(segments, monkeypatch):
     assert _check_forward(1, 2, 64 * 9 + 20, 64, 64, 64, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=11)
 
 
+def test_fused_long_single_head():
+    """One head of 262 144 tokens: 4096 tiles cut into the plan's largest
+    segment count (one head), so the longest carry chains and the largest
+    moment prefixes; every row against the oracle."""
+    assert _check_forward(1, 1, 262144, 64, 64, 64, "unit", 1, False, capi.HLA_ALGO_FUSED, seed=5)
+
+
 def test_fused_matches_chunked_closely():
     q, k, v, code = gen(2, 4, 1000, 64, 64, "unit", 21)
     qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
