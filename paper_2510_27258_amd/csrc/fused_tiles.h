@@ -218,13 +218,13 @@ template <int C, int D, int DV, bool KV = false, bool DEC = false, bool CM = tru
 __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                                                       const uint16_t* __restrict__ v, float* __restrict__ rec, int n,
                                                       int cps, int nseg, int want_cm, float lg2g) {
-  constexpr int ld = C + kPad, DT = D / 32, VT = DV / 32, KC = C / 16;
+  constexpr int DT = D / 32, VT = DV / 32, KC = C / 16;
   constexpr int nS = (DT * DT + kWaves - 1) / kWaves, nC = (DT * VT + kWaves - 1) / kWaves;
   constexpr int segQ = C * D / 8, segV = C * DV / 8;
   // Kt: K^T (C and m path) or a row-major k tile (S-only path)
-  constexpr int nKt = D * ld > C * (D + 16) ? D * ld : C * (D + 16);
-  __shared__ __align__(16) uint16_t Kt[nKt], Qs_[(KV || !CM) ? 8 : D * ld], Vt[CM ? DV * ld : 8];
-  uint16_t* Qt = KV ? Kt : Qs_;          // the left factor of the C slot
+  constexpr int nKt = C * (D + 16);                       // a row-major k tile
+  constexpr int nV = C * (DV + 16) > kWaves * D * 2 ? C * (DV + 16) : kWaves * D * 2;   // also m's partials
+  __shared__ __align__(16) uint16_t Kt[nKt], Qs_[(KV || !CM) ? 8 : C * (D + 16)], Vt[CM ? nV : 8];
   __shared__ __align__(16) float wtab[DEC ? C : 4];   // decay weights of the current tile's tokens
   static_assert(CM || !KV, "the AHLA moments form K^T V");
   if (KV) want_cm = 1;
@@ -306,22 +306,32 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
   }
   // with C (and m): the next tile's k, q, v pieces are loaded into registers
   // while the current one is multiplied (loads unconditional: piece and tile
-  // indices are clamped, only owners store)
+  // indices are clamped, only owners store).  Tiles sit row-major in LDS
+  // (16-byte stores, row stride d + 16 as in the S-only path) and every
+  // transposed operand is read through the transpose unit.  m = Q^T 1 is
+  // summed from the staged pieces: a thread's pieces always cover the same
+  // eight columns a8 .. a8+7.
   constexpr int NLK = (segQ + kThreads - 1) / kThreads, NLV = (segV + kThreads - 1) / kThreads;
+  constexpr int ldk = D + 16, ldv = DV + 16;
+  static_assert(kThreads % (D / 8) == 0 && kThreads % (DV / 8) == 0, "fixed columns per thread");
+  uint16_t* Qr = KV ? Kt : Qs_;           // row-major q (k for the K^T V form)
   uint4 pk_[NLK], pq_[NLK], pv_[NLV];
+  float m8[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) m8[j] = 0.f;
   auto fetch_cm = [&](int c) {
     const uint32_t t0 = (uint32_t)min(c, c1 - 1) * C;
 #pragma unroll
-    for (int i = 0; i < NLK; ++i) {
-      const int e = min(tid + kThreads * i, segQ - 1), t = e % C, a8 = (e / C) * 8;   // consecutive lanes take consecutive tokens
-      const uint32_t off = ((t0 + t) * D + a8) * 2;
-      pk_[i] = buf_load16(rk, off);
-      if (!KV) pq_[i] = buf_load16(rq, off);
+    for (int i = 0; i < NLK; ++i) {     // consecutive lanes take consecutive pieces of a token row
+      const int e = min(tid + kThreads * i, segQ - 1);
+      const uint32_t off = ((t0 + e / (D / 8)) * D + (e % (D / 8)) * 8) * 2;
+      if (!KV) pk_[i] = buf_load16(rk, off);
+      pq_[i] = buf_load16(KV ? rk : rq, off);
     }
 #pragma unroll
     for (int i = 0; i < NLV; ++i) {
-      const int e = min(tid + kThreads * i, segV - 1), t = e % C, b8 = (e / C) * 8;
-      pv_[i] = buf_load16(rv, ((t0 + t) * DV + b8) * 2);
+      const int e = min(tid + kThreads * i, segV - 1);
+      pv_[i] = buf_load16(rv, ((t0 + e / (DV / 8)) * DV + (e % (DV / 8)) * 8) * 2);
     }
   };
   if (want_cm && c0 < c1) fetch_cm(c0);
@@ -330,26 +340,21 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
     for (int i = 0; i < NLK; ++i) {
       const int e = tid + kThreads * i;
       if (e < segQ) {
-        const int t = e % C, a8 = (e / C) * 8;
-        const uint16_t* k8 = reinterpret_cast<const uint16_t*>(&pk_[i]);
+        const int o = (e / (D / 8)) * ldk + (e % (D / 8)) * 8;
+        if (!KV) *reinterpret_cast<uint4*>(Kt + o) = pk_[i];
+        *reinterpret_cast<uint4*>(Qr + o) = pq_[i];
+        const uint32_t u[4] = {pq_[i].x, pq_[i].y, pq_[i].z, pq_[i].w};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) Kt[(a8 + j) * ld + t] = k8[j];
-        if (!KV) {
-          const uint16_t* q8 = reinterpret_cast<const uint16_t*>(&pq_[i]);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) Qt[(a8 + j) * ld + t] = q8[j];
+        for (int j = 0; j < 4; ++j) {
+          m8[2 * j] += __uint_as_float(u[j] << 16);
+          m8[2 * j + 1] += __uint_as_float(u[j] & 0xffff0000u);
         }
       }
     }
 #pragma unroll
     for (int i = 0; i < NLV; ++i) {
       const int e = tid + kThreads * i;
-      if (e < segV) {
-        const int t = e % C, b8 = (e / C) * 8;
-        const uint16_t* v8 = reinterpret_cast<const uint16_t*>(&pv_[i]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) Vt[(b8 + j) * ld + t] = v8[j];
-      }
+      if (e < segV) *reinterpret_cast<uint4*>(Vt + (e / (DV / 8)) * ldv + (e % (DV / 8)) * 8) = pv_[i];
     }
     lds_barrier();
     if (c + 1 < c1) fetch_cm(c + 1);
@@ -359,32 +364,37 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
       if (!KV && ti < DT * DT) {
         const int it = ti / DT, jt = ti % DT;
 #pragma unroll
-        for (int s = 0; s < KC; ++s) sacc[i] = mfma(frag(Kt, ld, it * 32, s * 16), frag(Kt, ld, jt * 32, s * 16), sacc[i]);
+        for (int s = 0; s < KC; ++s)
+          sacc[i] = mfma(frag_tr(Kt, ldk, it * 32, s * 16), frag_tr(Kt, ldk, jt * 32, s * 16), sacc[i]);
       }
     }
-    if (want_cm) {
 #pragma unroll
-      for (int i = 0; i < nC; ++i) {
-        const int ti = w + kWaves * i;
-        if (ti < DT * VT) {
-          const int it = ti / VT, jt = ti % VT;
+    for (int i = 0; i < nC; ++i) {
+      const int ti = w + kWaves * i;
+      if (ti < DT * VT) {
+        const int it = ti / VT, jt = ti % VT;
 #pragma unroll
-          for (int s = 0; s < KC; ++s)
-            cacc[i] = mfma(frag(Qt, ld, it * 32, s * 16), frag(Vt, ld, jt * 32, s * 16), cacc[i]);
-        }
-      }
-      if (tid < D) {
-        const uint16_t* row = Qt + tid * ld;
-#pragma unroll
-        for (int t8 = 0; t8 < C; t8 += 8) {
-          const uint4 u = *reinterpret_cast<const uint4*>(row + t8);
-          const uint16_t* e8 = reinterpret_cast<const uint16_t*>(&u);
-#pragma unroll
-          for (int j = 0; j < 8; ++j) macc += bf16_to_f(e8[j]);
-        }
+        for (int s = 0; s < KC; ++s)
+          cacc[i] = mfma(frag_tr(Qr, ldk, it * 32, s * 16), frag_tr(Vt, ldv, jt * 32, s * 16), cacc[i]);
       }
     }
     lds_barrier();
+  }
+  if (want_cm) {      // m: sum the partial column sums over the lanes, then the waves, that share columns
+#pragma unroll
+    for (int o = D / 8; o < 64; o <<= 1)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) m8[j] += __shfl_xor(m8[j], o);
+    float* part = reinterpret_cast<float*>(Vt);          // [kWaves][D]; the tiles are dead
+    if (l < D / 8)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) part[w * D + l * 8 + j] = m8[j];
+    lds_barrier();
+    if (tid < D) {
+      macc = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < kWaves; ++ww) macc += part[ww * D + tid];
+    }
   }
   float* r = rec + ((size_t)bh * (nseg + 1) + seg) * state_floats(D, DV);
 #pragma unroll
