@@ -506,8 +506,8 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (heads or sequence segments would "
-              "shard across GPUs; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (heads, or sequence segments with "
+              "their carries exchanged, would shard across GPUs). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
