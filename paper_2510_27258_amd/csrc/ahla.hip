@@ -146,19 +146,26 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
   const rsrc_t rk = make_rsrc(k + (size_t)bh * n * D, (uint32_t)n * D * 2);
   const rsrc_t rv = make_rsrc(v + (size_t)bh * n * DV, (uint32_t)n * DV * 2);
   uint4 pq[G::pfQ], pk[G::pfQ], pv[G::pfV];
+  // 16-byte piece e of a C x W tile: token pt, first column pc.  At d = 64
+  // consecutive lanes take consecutive pieces of a token row (coalesced
+  // loads, contiguous LDS stores); at d = 128 consecutive tokens, which
+  // measured faster for this walk there.
+  constexpr bool RP = D <= 64;
+  auto pt = [](int e, int W) { return RP ? e / (W / 8) : e % C; };
+  auto pc = [](int e, int W) { return RP ? (e % (W / 8)) * 8 : (e / C) * 8; };
   auto fetch = [&](int c) {
     const uint32_t t0 = (uint32_t)c * C;
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
-      const int e = tid + NT * i;        // consecutive lanes take consecutive tokens
-      const uint32_t off = ((t0 + e % C) * D + (e / C) * 8) * 2;
+      const int e = tid + NT * i;
+      const uint32_t off = ((t0 + pt(e, D)) * D + pc(e, D)) * 2;
       pq[i] = buf_load16(rq, off);
       pk[i] = buf_load16(rk, off);
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + NT * i;
-      pv[i] = buf_load16(rv, ((t0 + e % C) * DV + (e / C) * 8) * 2);
+      pv[i] = buf_load16(rv, ((t0 + pt(e, DV)) * DV + pc(e, DV)) * 2);
     }
   };
   if (c_begin < c_end) fetch(c_begin);
@@ -174,14 +181,14 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + NT * i;
-      const int t = e % C, a8 = (e / C) * 8;
+      const int t = pt(e, D), a8 = pc(e, D);
       *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
       *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + NT * i;
-      const int t = e % C, b8 = (e / C) * 8;
+      const int t = pt(e, DV), b8 = pc(e, DV);
       *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
     }
     lds_barrier();

@@ -351,9 +351,9 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     const uint32_t t0 = (uint32_t)c * C;
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
-      const int e = tid + kThreads * i;        // consecutive lanes take consecutive tokens
+      const int e = tid + kThreads * i;        // consecutive lanes take consecutive pieces of a token row
       if (G::segQ % kThreads == 0 || e < G::segQ) {
-        const uint32_t off = ((t0 + e % C) * D + (e / C) * 8) * 2;
+        const uint32_t off = ((t0 + e / (D / 8)) * D + (e % (D / 8)) * 8) * 2;
         pq[i] = buf_load16(rq, off);
         pk[i] = buf_load16(rk, off);
       }
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + kThreads * i;
-      if (G::segV % kThreads == 0 || e < G::segV) pv[i] = buf_load16(rv, ((t0 + e % C) * DV + (e / C) * 8) * 2);
+      if (G::segV % kThreads == 0 || e < G::segV) pv[i] = buf_load16(rv, ((t0 + e / (DV / 8)) * DV + (e % (DV / 8)) * 8) * 2);
     }
   };
   if (c_begin < c_end) fetch(c_begin);
@@ -373,7 +373,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + kThreads * i;
       if (e < G::segQ) {
-        const int t = e % C, a8 = (e / C) * 8;
+        const int t = e / (D / 8), a8 = (e % (D / 8)) * 8;
         *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
         *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
       }
@@ -382,7 +382,7 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + kThreads * i;
       if (e < G::segV) {
-        const int t = e % C, b8 = (e / C) * 8;
+        const int t = e / (DV / 8), b8 = (e % (DV / 8)) * 8;
         *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
       }
     }
@@ -749,15 +749,15 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     const uint32_t t0 = (uint32_t)c * C;
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
-      const int e = tid + NT * i;        // consecutive lanes take consecutive tokens
-      const uint32_t off = ((t0 + e % C) * D + (e / C) * 8) * 2;
+      const int e = tid + NT * i;        // consecutive lanes take consecutive pieces of a token row
+      const uint32_t off = ((t0 + e / (D / 8)) * D + (e % (D / 8)) * 8) * 2;
       pq[i] = buf_load16(rq, off);
       pk[i] = buf_load16(rk, off);
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + NT * i;
-      pv[i] = buf_load16(rv, ((t0 + e % C) * DV + (e / C) * 8) * 2);
+      pv[i] = buf_load16(rv, ((t0 + e / (DV / 8)) * DV + (e % (DV / 8)) * 8) * 2);
     }
   };
   if (c_begin < c_end) fetch(c_begin);
@@ -775,14 +775,14 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
 #pragma unroll
     for (int i = 0; i < G::pfQ; ++i) {
       const int e = tid + NT * i;
-      const int t = e % C, a8 = (e / C) * 8;
+      const int t = e / (D / 8), a8 = (e % (D / 8)) * 8;
       *reinterpret_cast<uint4*>(Qs + t * G::ldQ + a8) = pq[i];
       *reinterpret_cast<uint4*>(Ks + t * G::ldK + a8) = pk[i];
     }
 #pragma unroll
     for (int i = 0; i < G::pfV; ++i) {
       const int e = tid + NT * i;
-      const int t = e % C, b8 = (e / C) * 8;
+      const int t = e / (DV / 8), b8 = (e % (DV / 8)) * 8;
       *reinterpret_cast<uint4*>(Vs + t * G::ldV + b8) = pv[i];
     }
     lds_barrier();

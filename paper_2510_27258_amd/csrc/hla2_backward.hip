@@ -66,14 +66,14 @@ struct Stage {
   __device__ __forceinline__ void fetch(rsrc_t r, int c, int tid) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int e = tid + NT * i, t = e % 64, a = (e / 64) * EP;   // consecutive lanes take consecutive tokens
+      const int e = tid + NT * i, t = e / (D / EP), a = (e % (D / EP)) * EP;   // consecutive lanes along a row
       p[i] = buf_load16(r, (((uint32_t)c * 64 + t) * D + a) * (F32 ? 4 : 2));
     }
   }
   __device__ __forceinline__ void store(uint16_t* hi, uint16_t* lo, int ld, int tid) const {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int e = tid + NT * i, t = e % 64, a = (e / 64) * EP;
+      const int e = tid + NT * i, t = e / (D / EP), a = (e % (D / EP)) * EP;
       if constexpr (F32) {
         uint32_t h0, l0, h1, l1;
         split2(__uint_as_float(p[i].x), __uint_as_float(p[i].y), h0, l0);
