@@ -43,6 +43,12 @@
  *   - Every call returns an hla_status.  On failure nothing is enqueued and
  *     hla_last_error() describes the reason (a thread-local string).
  *     Results are deterministic: the same inputs give bit-identical outputs.
+ *   - The environment variable HLA_FUSED_SEGMENTS=<p>, when set, overrides
+ *     how many segments per head the segment-walk plans (fused forward and
+ *     its decayed form, AHLA, backward, third order) cut each head into, for
+ *     testing and tuning; any p >= 1 gives the same result up to fp32
+ *     rounding order.  Workspace queries read it too: set it before the
+ *     query.  A call checks its workspace against its own plan.
  */
 #ifndef HLA_H
 #define HLA_H
