@@ -208,9 +208,14 @@ def test_den_scale_bounds_den():
         assert np.all(np.abs(den) <= Ds * (1 + 1e-12) + 1e-12)
 
 
-def test_pins_catch_g_without_cross_decay(monkeypatch):
-    """Planted mistake: the cross term added without its factor g (the printed
-    G_t = g G_{t-1} + k (k^T C_{t-1}) shape) must fail the brute-force pin."""
+def test_printed_cross_summary_is_another_operator(monkeypatch):
+    """The decay section prints the cross-summary update G_t = g G_{t-1} +
+    k (k^T C_{t-1}).  With the printed decayed moments that recurrence gives an
+    operator other than the one this build reads (pair (i, j) weighted by
+    g^((t-i)+(t-j)), whose masked output drops exactly the pairs j < i of the
+    decayed unmasked output).  This test pins the reading: it records that
+    the two differ, so the oracle's choice is visible, and that the oracle
+    follows the reading's double sum (the brute-force definition)."""
     q, k, v = _rand((), 8, 3, 2, seed=11)
     g = 0.8
     ref, _ = D.hla2_decay_definition_loops(q, k, v, g)
