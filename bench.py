@@ -22,15 +22,18 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 FP32_VALU_PEAK_TFLOPS = 157.3   # fp32 vector
 
-DEFAULT_WORKLOAD = "hla2-masked-bf16-B4H16-n4096-d64-C64"
+DEFAULT_WORKLOAD = "hla2-masked-normalized-bf16-B2H32-n16384-d128-C128"
+SUB_WORKLOAD = "hla2-masked-bf16-B4H16-n4096-d64-C64"
+FLUSH_BYTES = 512 << 20          # written between cold iterations: twice the 256 MB last-level cache
 
 
-def kernel_costs(w, P=None):
+def kernel_costs(w, P=None, tile=None):
     """Algorithmic cost of one launch of each kernel of the forward path:
     {name: (bound, bytes, flops)}.  bytes = HBM bytes the kernel must move
     (inputs read once, outputs written once); flops = useful arithmetic of
     the kernel's formulation (a dense C x C product counts C^2 per output
-    element; triangles are not halved).  P = segments per head (fused path)."""
+    element; triangles are not halved).  P = segments per head and tile = the
+    token tile of the fused path's plan (from the library)."""
     B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
     BH = B * H
     M = -(-n // C)
@@ -46,17 +49,14 @@ def kernel_costs(w, P=None):
         "scan": ("hbm", 2 * BH * M * F * 4, BH * M * 2 * (d * d * dv + d * d)),
     }
     if P:
-        Ct = fused_tile(C)
+        Ct = tile
         cps = -(-(-(-n // Ct)) // P)
         sum_tok = BH * min(n, (P - 1) * cps * Ct)
-        ncross = P - 1
         costs.update({
             # fused path: the output walk reads q/k/v once and writes out once
             # (the carry records it also reads are this design's own traffic).
-            # flops: the dense reference count of the chunk form at the
-            # workload's chunk
-            "walk": ("hbm", tok * (qkv_tok + 4 * dv),
-                     tok * reference_flops_per_token(C, d, dv)),
+            # flops: the dense count of the chunk form at the tile the walk runs
+            "walk": ("hbm", tok * (qkv_tok + 4 * dv), tok * reference_flops_per_token(Ct, d, dv)),
             "walk_summary": ("hbm", sum_tok * qkv_tok + BH * (P - 1) * F * 4,
                              sum_tok * 2 * (2 * Ct * d + 2 * d * d + 2 * d * dv + d * dv)),
             # segment moments: k read once, S = K^T K per segment written
@@ -75,23 +75,6 @@ def reference_flops_per_token(C, d, dv):
     """Dense flop count per token of the chunk form with chunk C (no triangle
     discount): 2 (C^2 + 2 C d + 2 C dv + 2 d^2 + 4 d dv)."""
     return 2 * (C * C + 2 * C * d + 2 * C * dv + 2 * d * d + 4 * d * dv)
-
-
-def fused_tile(C):
-    """Token tile of the fused walk: chunk 32 and 64 as given, chunk 128 in 64-token tiles."""
-    return 32 if C == 32 else 64
-
-
-def fused_segments(BH, n, C, d, dv):
-    """Segments per head chosen by the library for the fused path (same rule as
-    fused_plan): 256 CUs x output-walk workgroups per CU (two for d, dv <= 64,
-    one when either is 128), capped by the number of tiles."""
-    M = -(-n // fused_tile(C))
-    blocks = 1 if max(d, dv) > 64 else 2
-    p = int(os.environ.get("HLA_FUSED_SEGMENTS", 256 * blocks // BH))
-    p = max(1, min(p, M))
-    cps = -(-M // p)
-    return -(-M // cps)
 
 
 def peak_for(bound):
@@ -187,59 +170,124 @@ def source_sha():
     return h.hexdigest()[:16]
 
 
-def cpu_baseline(w, q, k, v, budget_s=20.0, min_s=10.0):
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, q, k, v, budget_s=20.0, min_s=10.0, one_thread_s=4.0):
     """The C oracle (serial fp64 recurrence, heads over OpenMP threads) on the
     host cores, on as many whole heads of the workload as fit the budget; the
     sample is repeated until it has run for at least min_s seconds, so short
-    samples are timed over several passes."""
-    import numpy as np
+    samples are timed over several passes.  Also one thread on one head, for
+    the per-core rate.  Inputs are converted to fp64 before the clock starts."""
     from oracle import native
     B, H, n = w["B"], w["H"], w["n"]
     threads = os.cpu_count() or 1
-    # probe one head to size the sample
+    qs = q.reshape(B * H, n, -1)
+    ks = k.reshape(B * H, n, -1)
+    vs = v.reshape(B * H, n, -1)
+    # one thread, one head (repeated to one_thread_s); also sizes the sample
+    import numpy as np
+    q1, k1, v1 = (np.ascontiguousarray(x[:1], dtype=np.float64) for x in (qs, ks, vs))
+    passes1 = 0
     t0 = time.perf_counter()
-    native.hla2_serial_c(q[0, :1], k[0, :1], v[0, :1], masked=bool(w["masked"]), threads=1, return_state=False)
-    per_head = max(time.perf_counter() - t0, 1e-6)
-    heads = int(min(B * H, max(1, budget_s * threads / per_head)))
+    while True:
+        native.hla2_serial_c(q1, k1, v1, masked=bool(w["masked"]), threads=1, return_state=False)
+        passes1 += 1
+        dt1 = time.perf_counter() - t0
+        if dt1 >= one_thread_s or passes1 >= 1000:
+            break
+    per_head = max(dt1 / passes1, 1e-6)
+    heads = int(min(B * H, max(1, budget_s * threads / per_head / 2)))
     heads = max(min(heads, B * H), min(threads, B * H))
-    qs = q.reshape(B * H, n, -1)[:heads]
-    ks = k.reshape(B * H, n, -1)[:heads]
-    vs = v.reshape(B * H, n, -1)[:heads]
+    import numpy as np
+    qh, kh, vh = (np.ascontiguousarray(x[:heads], dtype=np.float64) for x in (qs, ks, vs))
     passes, used = 0, 1
     t0 = time.perf_counter()
     while True:
-        _, _, _, used = native.hla2_serial_c(qs, ks, vs, masked=bool(w["masked"]), threads=threads,
-                                             return_state=False)
+        _, _, _, used = native.hla2_serial_c(qh, kh, vh, masked=bool(w["masked"]),
+                                             threads=threads, return_state=False)
         passes += 1
         dt = time.perf_counter() - t0
         if dt >= min_s or passes >= 1000:
             break
     return {"value": passes * heads * n / dt, "unit": "tokens/s", "cores": int(used), "kind": "oracle",
+            "cpu_model": cpu_model(), "nproc": threads,
+            "one_thread": {"value": passes1 * n / dt1, "unit": "tokens/s", "sample": f"1 head x {n} tokens, "
+                           f"{passes1} passes in {dt1:.2f} s"},
             "sample": f"{heads} of {B * H} heads x {n} tokens, C fp64 serial recurrence, {passes} passes "
-                      f"in {dt:.2f} s"}
+                      f"in {dt:.2f} s on {int(used)} threads"}
 
 
-def measure_scan(w, qd, kd, vd, reps=10):
+def stats_ms(xs):
+    """median, p10, p90 and mean of a list of per-iteration times (ms)."""
+    import numpy as np
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median_ms": float(np.median(a)), "p10_ms": float(np.percentile(a, 10)),
+            "p90_ms": float(np.percentile(a, 90)), "mean_ms": float(a.mean()), "iters": int(a.size)}
+
+
+def time_iters(fn, iters, cold=False):
+    """Per-iteration HIP-event times of fn() on the current stream.  cold:
+    a FLUSH_BYTES buffer is written before each iteration (outside its
+    events), so the 256 MB last-level cache holds none of fn's inputs."""
+    import torch
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda") if cold else None
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        if cold:
+            flush.fill_(1.0)
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def measure_scan(name, iters=50):
     """The semidirect-product scan kernel alone over the per-chunk summaries of
-    the workload: reads every chunk state and writes its exclusive prefix."""
+    a workload (chunk states from hla2_chunk_summaries): reads every chunk
+    state and writes its exclusive prefix and the total.  Warm (repeated on one
+    input) and cold (last-level cache flushed before each launch)."""
     import torch
     import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import inputs as I
+    w = I.WORKLOADS[name]
+    q, k, v, code = I.draw_qkv(w["B"], w["H"], w["n"], w["d"], w["dv"], w["dist"], w["seed"])
+    qd, kd, vd = (I.to_torch(x, code, "cuda") for x in (q, k, v))
+    del q, k, v
     d, dv = w["d"], w["dv"]
     states = hla.chunk_summaries(qd, kd, vd, w["chunk"])
+    del qd, kd, vd
     hla.scan(states, d, dv)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        hla.scan(states, d, dv)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    nbytes = 2 * states.numel() * 4 + states.shape[0] * states.shape[1] * states.shape[3] * 4
     B, H, M, F = states.shape
+    nbytes = 2 * states.numel() * 4 + B * H * F * 4
+    rec = {"kernel": "scan", "workload": name, "states": B * H * M, "algorithmic_bytes": nbytes, "unit": "GB/s",
+           "peak": HBM_PEAK_GBS}
+    for mode in ("warm", "cold"):
+        st = stats_ms(time_iters(lambda: hla.scan(states, d, dv), iters, cold=(mode == "cold")))
+        gbs = nbytes / st["median_ms"] / 1e6
+        rec[mode] = dict(st, achieved=gbs, frac=gbs / HBM_PEAK_GBS)
     del states
-    return {"kernel": "scan", "states": B * H * M, "ms": ms, "achieved": nbytes / ms / 1e6, "unit": "GB/s",
-            "peak": HBM_PEAK_GBS, "frac": nbytes / ms / 1e6 / HBM_PEAK_GBS, "algorithmic_bytes": nbytes}
+    torch.cuda.empty_cache()
+    return rec
 
 
 def measure_hla3(reps=20, masked=True):
@@ -453,7 +501,7 @@ def measure_decode(steps=None):
     B, H, d, dv, n = w["B"], w["H"], w["d"], w["dv"], w["n"]
     steps = steps or w["steps"]
     dev = torch.device("cuda:0")
-    state = hla.new_state(B, H, d, dv, device=dev)
+    state = hla.State(B, H, d, dv, dtype=torch.bfloat16, device=dev)
     # prefix in batch slices to bound host memory; draws follow the seeded recipe per slice
     q, k, v, code = I.draw_qkv(B, H, n, d, dv, w["dist"], w["seed"])
     qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
@@ -480,21 +528,110 @@ def measure_decode(steps=None):
             "frac": nbytes / ms / 1e6 / HBM_PEAK_GBS, "bytes_per_step": nbytes}
 
 
+def measure_forward(name, steps, warmup, algo_name="auto", cold_iters=0):
+    """Forward throughput on a named workload: `steps` back-to-back forwards
+    bracketed by synchronisations (tokens/s), per-iteration HIP-event times
+    (median, p10, p90), optionally cold iterations (last-level cache flushed
+    before each), per-kernel durations from the library's dispatch
+    timestamps, and the roofline entry of the kernel that takes the most
+    time."""
+    import torch
+    import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
+    from paper_2510_27258_amd import inputs as I
+
+    w = dict(I.WORKLOADS[name])
+    if w["kind"] != "forward":
+        raise SystemExit("bench.py times the forward workloads")
+    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
+    q, k, v, code = I.draw_qkv(B, H, n, d, dv, w["dist"], w["seed"])
+    dev = torch.device("cuda:0")
+    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
+    algo = {"auto": capi.HLA_ALGO_AUTO, "chunked": capi.HLA_ALGO_CHUNKED, "fused": capi.HLA_ALGO_FUSED}[algo_name]
+    wsb = capi.hla2_workspace_query(B, H, n, d, dv, C, code, algo)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    out = torch.empty(B, H, n, dv, dtype=torch.float32, device=dev)
+
+    def step():
+        hla.forward(qd, kd, vd, C, masked=bool(w["masked"]), normalized=bool(w["normalized"]), eps=w["eps"],
+                    algo=algo, out=out, workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    warm = stats_ms(time_iters(step, max(steps, 50)))
+    cold = stats_ms(time_iters(step, cold_iters, cold=True)) if cold_iters else None
+
+    # per-kernel durations: a second pass with the library's event bracketing
+    capi.hla_profile_begin(8 * steps + 8)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    prof = capi.hla_profile_summary()
+    capi.hla_profile_end()
+    used_algo = "fused" if "walk" in prof else "chunked"
+    P = tile = None
+    if used_algo == "fused":
+        P, tile = capi.hla2_fused_plan(B, H, n, d, dv, C)
+    costs = kernel_costs(w, P, tile)
+    dom = max(prof, key=lambda kname: prof[kname][1])
+    cnt, tot_ms = prof[dom]
+    avg_s = tot_ms / cnt / 1e3
+    bound, nbytes, nflops = costs[dom]
+    peak, unit = peak_for(bound)
+    achieved = (nbytes / avg_s / 1e9) if bound == "hbm" else (nflops / avg_s / 1e12)
+    tokens = B * H * n
+    roof = {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
+            "traffic": traffic_for(dom, name), "kernel": dom, "avg_launch_ms": avg_s * 1e3,
+            "algorithmic_bytes": nbytes, "algorithmic_flops": nflops,
+            "mfma_tflops": nflops / avg_s / 1e12, "mfma_frac": nflops / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS}
+    if dom == "walk" and tile != C:
+        # the same launch counted densely at the workload's chunk instead of the tile it walks
+        f_chunk = tokens * reference_flops_per_token(C, d, dv)
+        roof["mfma_frac_at_chunk"] = f_chunk / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS
+    rec = {
+        "value": tokens / (ms / 1e3),
+        "ms_per_step": ms,
+        "warm": warm,
+        "dtype": "bf16" if used_algo == "fused" else "f32",
+        "config": {"workload": name, "B": B, "H": H, "n": n, "d": d, "dv": dv, "chunk": C,
+                   "masked": w["masked"], "normalized": w["normalized"], "input_dtype": "bf16" if code else "fp32",
+                   "algo": used_algo, "segments_per_head": P, "tile": tile, "global_batch": B * H, "seq_len": n,
+                   "parallelism": "none"},
+        "roofline": roof,
+        "kernels_ms": {kname: v_[1] / v_[0] for kname, v_ in prof.items()},
+        "forward_mfma_frac": (tokens * reference_flops_per_token(tile or C, d, dv)) / (ms / 1e3) / 1e12
+                             / BF16_MFMA_PEAK_TFLOPS,
+    }
+    if cold is not None:
+        rec["cold"] = dict(cold, value=tokens / (cold["median_ms"] / 1e3))
+    return rec, (w, q, k, v)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--algo", default="auto", choices=["auto", "chunked", "fused"])
+    ap.add_argument("--cold-iters", type=int, default=50, help="cold (flushed) iterations of the forwards")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sub", action="store_true", help="skip the second (d = 64) forward workload")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone scan measurement")
     ap.add_argument("--no-hla3", action="store_true", help="skip the third-order measurement")
     ap.add_argument("--no-decay", action="store_true", help="skip the decayed-forward measurement")
     ap.add_argument("--no-ahla", action="store_true", help="skip the AHLA measurement")
     ap.add_argument("--no-backward", action="store_true", help="skip the backward measurement")
-    ap.add_argument("--only", choices=["ahla", "decay", "hla3", "hla3u", "backward"],
+    ap.add_argument("--only", choices=["ahla", "decay", "hla3", "hla3u", "backward", "decode", "scan"],
                     help="run only that measurement and print its record (for profiling one path)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run --steps device-to-device copies of this many bytes (counter calibration)")
@@ -510,7 +647,6 @@ def main():
               "their carries exchanged, would shard across GPUs). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     if args.copy_bytes:
@@ -524,87 +660,45 @@ def main():
 
     if args.only:
         rec = {"ahla": measure_ahla, "decay": measure_decay, "hla3": measure_hla3,
-               "hla3u": lambda: measure_hla3(masked=False), "backward": measure_backward}[args.only]()
+               "hla3u": lambda: measure_hla3(masked=False), "backward": measure_backward,
+               "decode": measure_decode, "scan": lambda: measure_scan(args.workload)}[args.only]()
         print(json.dumps(rec), flush=True)
         return
 
-    import paper_2510_27258_amd as hla
-    from paper_2510_27258_amd import capi
-    from paper_2510_27258_amd import inputs as I
-
-    w = dict(I.WORKLOADS[args.workload])
-    if w["kind"] != "forward":
-        raise SystemExit("bench.py times the forward workloads")
-    B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
-    q, k, v, code = I.draw_qkv(B, H, n, d, dv, w["dist"], w["seed"])
-    dev = torch.device("cuda:0")
-    qd, kd, vd = (I.to_torch(x, code, dev) for x in (q, k, v))
-    algo = {"auto": capi.HLA_ALGO_AUTO, "chunked": capi.HLA_ALGO_CHUNKED, "fused": capi.HLA_ALGO_FUSED}[args.algo]
-    wsb = hla.workspace_bytes(B, H, n, d, dv, C, code, algo)
-    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
-    out = torch.empty(B, H, n, dv, dtype=torch.float32, device=dev)
-
-    def step():
-        hla.forward(qd, kd, vd, C, masked=bool(w["masked"]), normalized=bool(w["normalized"]), eps=w["eps"],
-                    algo=algo, out=out, workspace=ws)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-
-    # per-kernel durations: a second pass with the library's event bracketing
-    capi.hla_profile_begin(8 * args.steps + 8)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    prof = capi.hla_profile_summary()
-    capi.hla_profile_end()
-    used_algo = "fused" if "walk" in prof else "chunked"
-    P = None
-    if used_algo == "fused":
-        P = fused_segments(B * H, n, C, d, dv)
-    costs = kernel_costs(w, P)
-    dom = max(prof, key=lambda kname: prof[kname][1])
-    cnt, tot_ms = prof[dom]
-    avg_s = tot_ms / cnt / 1e3
-    bound, nbytes, nflops = costs[dom]
-    peak, unit = peak_for(bound)
-    achieved = (nbytes / avg_s / 1e9) if bound == "hbm" else (nflops / avg_s / 1e12)
-    tr = traffic_for(dom, args.workload)
-
-    tokens = B * H * n
+    head, (w, q, k, v) = measure_forward(args.workload, args.steps, args.warmup, args.algo, args.cold_iters)
+    print(f"forward {args.workload}: {head['ms_per_step']:.4f} ms per step", file=sys.stderr, flush=True)
     rec = {
         "metric": "masked HLA-2 forward tokens/s (B*H*n) + % bf16 MFMA peak; decode step GB/s",
-        "value": tokens / (ms / 1e3),
+        "value": head["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if used_algo == "fused" else "f32",
+        "dtype": head["dtype"],
         "data": "synthetic",
-        "config": {"workload": args.workload, "B": B, "H": H, "n": n, "d": d, "dv": dv, "chunk": C,
-                   "masked": w["masked"], "normalized": w["normalized"], "input_dtype": "bf16" if code else "fp32",
-                   "algo": used_algo, "global_batch": B * H, "seq_len": n, "parallelism": "none"},
-        "roofline": {"bound": bound, "achieved": achieved, "peak": peak, "unit": unit, "frac": achieved / peak,
-                     "traffic": tr, "kernel": dom, "avg_launch_ms": avg_s * 1e3,
-                     "algorithmic_bytes": nbytes, "algorithmic_flops": nflops,
-                     "mfma_tflops": nflops / avg_s / 1e12,
-                     "mfma_frac": nflops / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS},
-        "kernels_ms": {kname: v_[1] / v_[0] for kname, v_ in prof.items()},
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "kernels_ms": head["kernels_ms"],
+        "warm": head["warm"],
+        "cold": head.get("cold"),
+        "forward_mfma_frac": head["forward_mfma_frac"],
     }
+    if not args.no_sub and args.workload != SUB_WORKLOAD:
+        sub, _ = measure_forward(SUB_WORKLOAD, args.steps, args.warmup, args.algo, args.cold_iters)
+        rec["sub_forward"] = sub
+        print(f"forward {SUB_WORKLOAD}: {sub['ms_per_step']:.4f} ms per step", file=sys.stderr, flush=True)
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
+        print("cpu baseline done", file=sys.stderr, flush=True)
+    del q, k, v
+    torch.cuda.empty_cache()
     if not args.no_scan:
-        rec["scan"] = measure_scan(w, qd, kd, vd)
+        rec["scan"] = {"d64": measure_scan(SUB_WORKLOAD), "d128": measure_scan(DEFAULT_WORKLOAD)}
+        print("scan done", file=sys.stderr, flush=True)
     if not args.no_hla3:
         rec["hla3"] = measure_hla3()
         rec["hla3_unmasked"] = measure_hla3(masked=False)
@@ -614,10 +708,8 @@ def main():
         rec["ahla"] = measure_ahla()
     if not args.no_backward:
         rec["backward"] = measure_backward()
-    if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, q, k, v)
+    print("next rows done", file=sys.stderr, flush=True)
     if not args.no_decode:
-        del q, k, v, qd, kd, vd, ws, out
         torch.cuda.empty_cache()
         rec["decode"] = measure_decode()
     print(json.dumps(rec), flush=True)

@@ -43,6 +43,10 @@
  *   - Every call returns an hla_status.  On failure nothing is enqueued and
  *     hla_last_error() describes the reason (a thread-local string).
  *     Results are deterministic: the same inputs give bit-identical outputs.
+ *   - Size queries returning size_t (*_workspace_bytes, hla2_state_bytes)
+ *     return 0 exactly when the arguments would be rejected, and then set
+ *     hla_last_error(); every accepted argument list gives a size > 0.
+ *     hla2_workspace_query returns the status itself.
  *   - The environment variable HLA_FUSED_SEGMENTS=<p>, when set, overrides
  *     how many segments per head the segment-walk plans (fused forward and
  *     its decayed form, AHLA, backward, third order) cut each head into, for
@@ -95,13 +99,28 @@ int hla2_forward(const void *q, const void *k, const void *v, float *out,
                  int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
                  float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
 
-/* As hla2_forward with an explicit algorithm (hla_algo).  HLA_ALGO_FUSED
- * returns HLA_ERR_UNSUPPORTED for shapes it does not cover. */
+/* As hla2_forward with an explicit algorithm (hla_algo) and an optional
+ * denominator output.  den: NULL, or (normalized = 1 only) fp32 [B, H, n]
+ * receiving den_t of Thm. 1 (q_t^T (S_t m_t - h_t) masked, q_t^T S_t m_t
+ * unmasked), without eps; den != NULL with normalized = 0 is HLA_ERR_INVALID.
+ * HLA_ALGO_FUSED returns HLA_ERR_UNSUPPORTED for shapes it does not cover. */
 size_t hla2_workspace_bytes_ex(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo);
-int hla2_forward_ex(const void *q, const void *k, const void *v, float *out,
+int hla2_forward_ex(const void *q, const void *k, const void *v, float *out, float *den,
                     int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
                     float eps, int dtype, void *workspace, size_t workspace_bytes, int algo,
                     void *stream);
+
+/* Workspace size of hla2_forward_ex as a status: on HLA_OK *bytes holds the
+ * size; otherwise *bytes is 0 and hla_last_error() says why.  bytes must not
+ * be NULL (HLA_ERR_INVALID). */
+int hla2_workspace_query(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo, size_t *bytes);
+
+/* The segment plan of the fused path for these arguments: *segments gets the
+ * number of segments each head is cut into (walked in parallel, composed by
+ * Eq. semidirect) and *tile the token tile the walk advances by.  Returns
+ * HLA_ERR_UNSUPPORTED when the fused path does not cover the shape (bf16
+ * inputs, masked).  Reads HLA_FUSED_SEGMENTS like the forward. */
+int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int *segments, int *tile);
 
 /* 1 if hla2_forward_ex would accept `algo` for these arguments, else 0.
  * HLA_ALGO_FUSED covers bf16 inputs, masked = 1, n * max(d, dv) * 4 < 2^31
@@ -132,27 +151,57 @@ int hla2_scan(const float *states, const float *init, float *prefix, float *tota
               int B, int H, int M, int d, int dv, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * Decode state (Sec. 3.1 online updates; Thm. 2 identity).  A descriptor
+ * fixes, for the life of the state, the operator every prefill and step on
+ * it applies (masked, normalized, eps) and the dtype of the tokens they take,
+ * so a prefill and the steps after it cannot disagree.  The state itself is
+ * caller-owned device memory holding one record of F floats per head (the
+ * layout above); S, C, m, G, h point at head 0's fields and head i's field X
+ * is X + i * head_floats.  `check` is written by hla2_state_init: a call
+ * given a descriptor whose other fields changed since then returns
+ * HLA_ERR_INVALID.  The descriptor is a host object; pass it by pointer.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int B, H, d, dv;            /* heads B*H; key and value widths            */
+  int masked, normalized;     /* operator of every prefill and step          */
+  int dtype;                  /* HLA_FP32 or HLA_BF16: the tokens' dtype     */
+  float eps;                  /* denominator offset, used when normalized    */
+  float *data;                /* [B, H, F] fp32 device memory, caller-owned  */
+  size_t head_floats;         /* F = d*d + 2*d*dv + 2*d                      */
+  float *S, *C, *m, *G, *h;   /* head 0's fields inside data                 */
+  unsigned long long check;   /* set by hla2_state_init                      */
+} hla2_state;
+
+/* Device bytes of a state of B*H heads: B*H*F*4 (0 if invalid). */
+size_t hla2_state_bytes(int B, int H, int d, int dv);
+
+/* Fill *st for the device buffer buf (at least hla2_state_bytes(B, H, d, dv)
+ * bytes, 16-byte aligned) and enqueue its zeroing on `stream`: the all-zero
+ * record is the identity segment of Thm. 2, the state before any token.
+ * Argument rules as hla2_forward (sizes, flags, eps, dtype). */
+int hla2_state_init(hla2_state *st, void *buf, size_t buf_bytes, int B, int H, int d, int dv, int masked,
+                    int normalized, float eps, int dtype, void *stream);
+
+/* ---------------------------------------------------------------------------
  * hla2_prefill — continue every head's state over n new tokens:
  *   state <- state (+) summary(tokens)          (Thm. 2)
  * and, if out != NULL, write the outputs of those tokens ([B, H, n, dv]) as
  * the serial recurrence started from the given state would (Sec. 3.1,
- * Thm. 1).  state: [B, H, F], updated in place.  workspace: at least
- * hla2_prefill_workspace_bytes(...) bytes.
+ * Thm. 1), with the state's operator.  q, k: [B, H, n, d], v: [B, H, n, dv]
+ * in the state's dtype.  workspace: at least hla2_prefill_workspace_bytes(st,
+ * n, chunk) bytes.
  * ------------------------------------------------------------------------- */
-size_t hla2_prefill_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype);
-int hla2_prefill(float *state, const void *q, const void *k, const void *v, float *out,
-                 int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
-                 float eps, int dtype, void *workspace, size_t workspace_bytes, void *stream);
+size_t hla2_prefill_workspace_bytes(const hla2_state *st, int n, int chunk);
+int hla2_prefill(hla2_state *st, const void *q, const void *k, const void *v, int n, int chunk, float *out,
+                 void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
  * hla2_step — one decode step per head: the online updates of Sec. 3.1 and
- * the readout of Thm. 1 (Sec. 5 order).  q_t, k_t: [B, H, d]; v_t: [B, H, dv];
- * out_t: [B, H, dv] fp32; state: [B, H, F], updated in place.
+ * the readout of Thm. 1 (Sec. 5 order), with the state's operator.
+ * q_t, k_t: [B, H, d]; v_t: [B, H, dv] in the state's dtype; out_t: [B, H, dv]
+ * fp32.  The state is updated in place.
  * ------------------------------------------------------------------------- */
-int hla2_step(float *state, const void *q_t, const void *k_t, const void *v_t, float *out_t,
-              int B, int H, int d, int dv, int masked, int normalized, float eps, int dtype,
-              void *stream);
-
+int hla2_step(hla2_state *st, const void *q_t, const void *k_t, const void *v_t, float *out_t, void *stream);
 
 /* ---------------------------------------------------------------------------
  * hla2_forward_decay — second-order HLA with exponential time decay gamma
@@ -172,8 +221,9 @@ int hla2_step(float *state, const void *q_t, const void *k_t, const void *v_t, f
  * the hi/lo split); everything else on the chunked path in fp32 (decayed
  * chunk summaries, the decayed (+)-scan, decayed readout).  Arguments as
  * hla2_forward, plus
- * gamma, finite, 0 < gamma <= 1 (else HLA_ERR_INVALID); gamma^(2*chunk) must
- * stay a normal fp32 number (gamma >= 0.51 at chunk 64; HLA_ERR_UNSUPPORTED
+ * gamma, finite, 0 < gamma <= 1 (else HLA_ERR_INVALID); gamma^(2*tile), with
+ * tile = min(chunk, 64) the token tile both paths walk, must stay a normal
+ * fp32 number (gamma >= 0.51 at chunk 64 and 128; HLA_ERR_UNSUPPORTED
  * otherwise).  workspace: hla2_forward_decay_workspace_bytes(...) bytes (enough
  * for either path).
  * ------------------------------------------------------------------------- */

@@ -5,6 +5,5 @@ The computation lives in libhla.so (HIP for gfx950, C ABI in include/hla.h).
 tensors (torch provides device memory and the current stream only).
 """
 from . import capi  # noqa: F401
-from .hla import (HLA2, ahla_forward, backward, chunk_summaries, forward, forward_decay,  # noqa: F401
-                  hla2_attention, hla3_forward, new_state, prefill, scan, split_state, state_floats, step,
-                  workspace_bytes)
+from .hla import (HLA2, State, ahla_forward, backward, chunk_summaries, forward, forward_decay,  # noqa: F401
+                  hla2_attention, hla3_forward, prefill, scan, split_state, state_floats, step, workspace_bytes)

@@ -22,6 +22,18 @@ _I = ctypes.c_int
 _F = ctypes.c_float
 _Z = ctypes.c_size_t
 
+
+class HLA2State(ctypes.Structure):
+    """The hla2_state descriptor of include/hla.h (a host object)."""
+    _fields_ = [("B", _I), ("H", _I), ("d", _I), ("dv", _I), ("masked", _I), ("normalized", _I), ("dtype", _I),
+                ("eps", _F), ("data", _P), ("head_floats", _Z), ("S", _P), ("C", _P), ("m", _P), ("G", _P),
+                ("h", _P), ("check", ctypes.c_ulonglong)]
+
+
+_SP = ctypes.POINTER(HLA2State)
+_ZP = ctypes.POINTER(_Z)
+_IP = ctypes.POINTER(_I)
+
 _SIGS = {
     "hla_last_error": (ctypes.c_char_p, []),
     "hla2_state_floats": (_Z, [_I, _I]),
@@ -29,12 +41,16 @@ _SIGS = {
     "hla2_workspace_bytes_ex": (_Z, [_I] * 8),
     "hla2_algo_supported": (_I, [_I] * 7),
     "hla2_forward": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
-    "hla2_forward_ex": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _I, _P]),
+    "hla2_forward_ex": (_I, [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _I, _P]),
+    "hla2_workspace_query": (_I, [_I] * 8 + [_ZP]),
+    "hla2_fused_plan": (_I, [_I] * 6 + [_IP, _IP]),
+    "hla2_state_bytes": (_Z, [_I] * 4),
+    "hla2_state_init": (_I, [_SP, _P, _Z] + [_I] * 6 + [_F, _I, _P]),
     "hla2_chunk_summaries": (_I, [_P, _P, _P, _P] + [_I] * 7 + [_P]),
     "hla2_scan": (_I, [_P, _P, _P, _P] + [_I] * 5 + [_P]),
-    "hla2_prefill_workspace_bytes": (_Z, [_I] * 7),
-    "hla2_prefill": (_I, [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
-    "hla2_step": (_I, [_P, _P, _P, _P, _P] + [_I] * 6 + [_F, _I, _P]),
+    "hla2_prefill_workspace_bytes": (_Z, [_SP, _I, _I]),
+    "hla2_prefill": (_I, [_SP, _P, _P, _P, _I, _I, _P, _P, _Z, _P]),
+    "hla2_step": (_I, [_SP, _P, _P, _P, _P, _P]),
     "hla_profile_begin": (_I, [_I]),
     "hla_profile_end": (_I, []),
     "hla_profile_summary": (_I, [ctypes.c_char_p, _Z]),
@@ -108,10 +124,33 @@ def hla2_forward(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, d
                  ws_bytes, stream)
 
 
-def hla2_forward_ex(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes, algo,
+def hla2_forward_ex(q, k, v, out, den, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes, algo,
                     stream):
-    return _call("hla2_forward_ex", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
+    return _call("hla2_forward_ex", q, k, v, out, den, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
                  ws_bytes, algo, stream)
+
+
+def hla2_workspace_query(B, H, n, d, dv, chunk, dtype, algo):
+    """Workspace bytes of hla2_forward_ex; raises HLAError for arguments it would reject."""
+    nb = _Z(0)
+    _call("hla2_workspace_query", B, H, n, d, dv, chunk, dtype, algo, ctypes.byref(nb))
+    return nb.value
+
+
+def hla2_fused_plan(B, H, n, d, dv, chunk):
+    """(segments per head, token tile) of the fused path's plan; raises HLAError if it does not cover the shape."""
+    P, tile = _I(0), _I(0)
+    _call("hla2_fused_plan", B, H, n, d, dv, chunk, ctypes.byref(P), ctypes.byref(tile))
+    return P.value, tile.value
+
+
+def hla2_state_bytes(B, H, d, dv):
+    return lib().hla2_state_bytes(B, H, d, dv)
+
+
+def hla2_state_init(st, buf, buf_bytes, B, H, d, dv, masked, normalized, eps, dtype, stream):
+    return _call("hla2_state_init", ctypes.byref(st), buf, buf_bytes, B, H, d, dv, masked, normalized, eps, dtype,
+                 stream)
 
 
 def hla2_chunk_summaries(q, k, v, states, B, H, n, d, dv, chunk, dtype, stream):
@@ -122,18 +161,16 @@ def hla2_scan(states, init, prefix, total, B, H, M, d, dv, stream):
     return _call("hla2_scan", states, init, prefix, total, B, H, M, d, dv, stream)
 
 
-def hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype):
-    return lib().hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype)
+def hla2_prefill_workspace_bytes(st, n, chunk):
+    return lib().hla2_prefill_workspace_bytes(ctypes.byref(st), n, chunk)
 
 
-def hla2_prefill(state, q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws, ws_bytes,
-                 stream):
-    return _call("hla2_prefill", state, q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
-                 ws_bytes, stream)
+def hla2_prefill(st, q, k, v, n, chunk, out, ws, ws_bytes, stream):
+    return _call("hla2_prefill", ctypes.byref(st), q, k, v, n, chunk, out, ws, ws_bytes, stream)
 
 
-def hla2_step(state, q_t, k_t, v_t, out_t, B, H, d, dv, masked, normalized, eps, dtype, stream):
-    return _call("hla2_step", state, q_t, k_t, v_t, out_t, B, H, d, dv, masked, normalized, eps, dtype, stream)
+def hla2_step(st, q_t, k_t, v_t, out_t, stream):
+    return _call("hla2_step", ctypes.byref(st), q_t, k_t, v_t, out_t, stream)
 
 
 def hla2_forward_decay_workspace_bytes(B, H, n, d, dv, chunk, dtype):

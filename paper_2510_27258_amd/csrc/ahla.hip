@@ -400,7 +400,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
     const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("ahla_fix", s);
     HLA_LAUNCH((k_fix<C, D, D>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
-                       carry, 0, f.n, cps, P, f.normalized, f.eps, tpw, 0.f);
+                       carry, (float*)nullptr, 0, f.n, cps, P, f.normalized, f.eps, tpw, 0.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }

@@ -42,7 +42,8 @@ struct Fwd {
   const void* q; const void* k; const void* v; float* out;
   int BH, n, d, dv, chunk, masked, normalized, dtype;
   float eps;
-  float gamma = 1.f;   // decay (chunked path only); 1 = none
+  float gamma = 1.f;   // decay; 1 = none
+  float* den_out = nullptr;   // [BH, n]: den_t without eps (normalized only), or null
 };
 // gamma: decay in (0, 1]; the summaries are taken relative to each chunk's last token.
 hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, float* states,
@@ -63,4 +64,6 @@ hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s);
 hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out,
                        int BH, int d, int dv, int masked, int normalized, float eps, int dtype,
                        hipStream_t s);
+// p[0 .. n4) = 0 as float4 stores (a fill kernel, so it may be captured in a graph).
+hipError_t launch_zero(float* p, size_t n4, hipStream_t s);
 }  // namespace hla

@@ -1131,7 +1131,8 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
     const int M = (f.n + C - 1) / C, tpw = fix_tpw(M, BH);
     prof_start("fix", s);
     HLA_LAUNCH((k_fix<C, D, DV, DEC>), dim3((M + tpw - 1) / tpw, BH), dim3(FC::NT), FC::lds, s, q, f.out, den,
-               carry, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps, tpw, lg2g);
+               carry, f.normalized ? f.den_out : nullptr, init ? 1 : 0, f.n, cps, P, f.normalized, f.eps, tpw,
+               lg2g);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -1158,6 +1159,15 @@ void fused_plan(const Shape& sh, int BH, int n, int* P, int* cps) {
 }
 
 }  // namespace
+
+bool fused_plan_query(int BH, int n, int d, int dv, int chunk, int* P, int* tile) {
+  const Shape* sh = find_shape(chunk, d, dv);
+  if (!sh) return false;
+  int cps;
+  fused_plan(*sh, BH, n, P, &cps);
+  *tile = sh->C;
+  return true;
+}
 
 bool fused_supported(int n, int d, int dv, int chunk, int dtype, int masked) {
   // per-head byte offsets of q/k/v and of the output stay below 2^31

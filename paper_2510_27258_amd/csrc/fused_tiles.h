@@ -491,8 +491,8 @@ struct FixCfg {
 template <int C, int D, int DV, bool DEC = false>
 __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
     const uint16_t* __restrict__ q, float* __restrict__ out, const float* __restrict__ den_in,
-    const float* __restrict__ carry, int has_init, int n, int cps, int nseg, int normalized, float eps, int tpw,
-    float lg2g) {
+    const float* __restrict__ carry, float* __restrict__ den_out, int has_init, int n, int cps, int nseg,
+    int normalized, float eps, int tpw, float lg2g) {
   using F = FixCfg<C, D, DV>;
   constexpr int NT = F::NT, KD = F::KD, ldQ = F::ldQ, QE = F::QE, QV = F::QV, NC = D * DV + D;
   extern __shared__ __align__(16) uint16_t lds[];      // q tile | fp32 eta | 1/den
@@ -574,7 +574,12 @@ __global__ __launch_bounds__((FixCfg<C, D, DV>::NT)) void k_fix(
 #pragma unroll
       for (int o = 1; o < TPR; o <<= 1) sd += __shfl_xor(sd, o);
       if (DEC) sd *= exp2f(2.f * lg2g * (float)(t + 1));
-      if (tid % TPR == 0 && t < C) inv[t] = (t0 + t < (uint32_t)n) ? 1.f / (den_in[(size_t)bh * n + t0 + t] + sd + eps) : 0.f;
+      if (tid % TPR == 0 && t < C) {
+        const bool in = t0 + t < (uint32_t)n;
+        const float den = in ? den_in[(size_t)bh * n + t0 + t] + sd : 0.f;
+        inv[t] = in ? 1.f / (den + eps) : 0.f;
+        if (den_out && in) den_out[(size_t)bh * n + t0 + t] = den;
+      }
       lds_barrier();
     }
     f32x16 acc = zero16();

@@ -120,8 +120,9 @@ __global__ __launch_bounds__(256) void k_chunk_summary(const T* __restrict__ q, 
 template <typename T>
 __global__ __launch_bounds__(256) void k_readout(const T* __restrict__ q, const T* __restrict__ k,
                                                  const T* __restrict__ v, const float* __restrict__ prefix,
-                                                 float* __restrict__ out, int n, int d, int dv, int chunk,
-                                                 int M, int masked, int normalized, float eps, float lg2g) {
+                                                 float* __restrict__ out, float* __restrict__ den_out, int n,
+                                                 int d, int dv, int chunk, int M, int masked, int normalized,
+                                                 float eps, float lg2g) {
   extern __shared__ double smemd[];
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const int t0 = c * chunk;
@@ -219,6 +220,7 @@ __global__ __launch_bounds__(256) void k_readout(const T* __restrict__ q, const 
       float s = dn[t];
       for (int j = 0; j <= t; ++j) s += W[t * L + j];
       dn[t] = s;
+      if (den_out) den_out[(size_t)bh * n + t0 + t] = s;
     }
     __syncthreads();
     for (int idx = tid; idx < L * dv; idx += blockDim.x) {
@@ -267,14 +269,14 @@ hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     HLA_LAUNCH(kern, grid, block, lds, s, (const uint16_t*)f.q, (const uint16_t*)f.k,
-                       (const uint16_t*)f.v, prefix, f.out, f.n, f.d, f.dv, f.chunk, M, f.masked,
+                       (const uint16_t*)f.v, prefix, f.out, f.den_out, f.n, f.d, f.dv, f.chunk, M, f.masked,
                        f.normalized, f.eps, lg2g);
   } else {
     auto kern = k_readout<float>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     HLA_LAUNCH(kern, grid, block, lds, s, (const float*)f.q, (const float*)f.k, (const float*)f.v,
-                       prefix, f.out, f.n, f.d, f.dv, f.chunk, M, f.masked, f.normalized, f.eps, lg2g);
+                       prefix, f.out, f.den_out, f.n, f.d, f.dv, f.chunk, M, f.masked, f.normalized, f.eps, lg2g);
   }
   return hipGetLastError();
 }

@@ -174,6 +174,18 @@ __global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state
   }
 }
 
+__global__ __launch_bounds__(256) void k_zero(float4* __restrict__ p, size_t n4) {
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) p[i] = z;
+}
+
+hipError_t launch_zero(float* p, size_t n4, hipStream_t s) {
+  if (n4 == 0) return hipSuccess;
+  const size_t blocks = (n4 + 255) / 256;
+  HLA_LAUNCH(k_zero, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s, reinterpret_cast<float4*>(p), n4);
+  return hipGetLastError();
+}
+
 hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out, int BH, int d,
                        int dv, int masked, int normalized, float eps, int dtype, hipStream_t s) {
   if (dtype == 1)

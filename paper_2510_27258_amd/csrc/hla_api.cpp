@@ -98,7 +98,13 @@ int hla2_algo_supported(int algo, int n, int d, int dv, int chunk, int dtype, in
 }
 
 size_t hla2_workspace_bytes_ex(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo) {
-  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK) return 0;
+  if (chunk == 0) { fail(HLA_ERR_INVALID, "chunk must be set"); return 0; }
+  if (algo < HLA_ALGO_AUTO || algo > HLA_ALGO_FUSED) { fail(HLA_ERR_INVALID, "unknown algo %d", algo); return 0; }
+  if (algo == HLA_ALGO_FUSED && !hla::fused_supported(n, d, dv, chunk, dtype, 1)) {
+    fail(HLA_ERR_UNSUPPORTED, "the fused path does not cover d=%d dv=%d chunk=%d dtype=%d", d, dv, chunk, dtype);
+    return 0;
+  }
   const int a = select_algo(algo, n, d, dv, chunk, dtype, 1);
   if (a == HLA_ALGO_FUSED) return hla::fused_workspace_bytes(B * H, n, d, dv, chunk);
   return chunked_ws(B * H, n, d, dv, chunk);
@@ -111,8 +117,8 @@ size_t hla2_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int d
   return a > b ? a : b;
 }
 
-int hla2_forward_ex(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
-                    int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
+int hla2_forward_ex(const void* q, const void* k, const void* v, float* out, float* den, int B, int H, int n, int d,
+                    int dv, int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
                     size_t workspace_bytes, int algo, void* stream) {
   int rc;
   if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
@@ -121,11 +127,14 @@ int hla2_forward_ex(const void* q, const void* k, const void* v, float* out, int
   if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
       (rc = check_ptr(out, "out")))
     return rc;
+  if (den && !normalized) return fail(HLA_ERR_INVALID, "den is written only with normalized = 1");
+  if (den && !aligned16(den)) return fail(HLA_ERR_INVALID, "den is not 16-byte aligned");
   if (algo < HLA_ALGO_AUTO || algo > HLA_ALGO_FUSED) return fail(HLA_ERR_INVALID, "unknown algo %d", algo);
   const int a = select_algo(algo, n, d, dv, chunk, dtype, masked);
   const int BH = B * H;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
+  f.den_out = den;
   if (a == HLA_ALGO_FUSED) {
     if (!hla::fused_supported(n, d, dv, chunk, dtype, masked))
       return fail(HLA_ERR_UNSUPPORTED, "fused path needs bf16 inputs, masked=1 and (d, dv, chunk) in its "
@@ -157,12 +166,37 @@ int hla2_forward_ex(const void* q, const void* k, const void* v, float* out, int
 int hla2_forward(const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d, int dv,
                  int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
                  size_t workspace_bytes, void* stream) {
-  return hla2_forward_ex(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, workspace,
+  return hla2_forward_ex(q, k, v, out, nullptr, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, workspace,
                          workspace_bytes, HLA_ALGO_AUTO, stream);
 }
 
+int hla2_workspace_query(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo, size_t* bytes) {
+  if (!bytes) return fail(HLA_ERR_INVALID, "bytes is NULL");
+  *bytes = 0;
+  int rc;
+  if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if (algo < HLA_ALGO_AUTO || algo > HLA_ALGO_FUSED) return fail(HLA_ERR_INVALID, "unknown algo %d", algo);
+  if (algo == HLA_ALGO_FUSED && !hla::fused_supported(n, d, dv, chunk, dtype, 1))
+    return fail(HLA_ERR_UNSUPPORTED, "the fused path does not cover d=%d dv=%d chunk=%d dtype=%d", d, dv, chunk,
+                dtype);
+  *bytes = hla2_workspace_bytes_ex(B, H, n, d, dv, chunk, dtype, algo);
+  return ok();
+}
+
+int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int* segments, int* tile) {
+  int rc;
+  if (!segments || !tile) return fail(HLA_ERR_INVALID, "segments and tile must not be NULL");
+  if ((rc = check_dims(B, H, n, d, dv, chunk, HLA_BF16, true)) != HLA_OK) return rc;
+  if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
+  if (!hla::fused_supported(n, d, dv, chunk, HLA_BF16, 1) || !hla::fused_plan_query(B * H, n, d, dv, chunk, segments, tile))
+    return fail(HLA_ERR_UNSUPPORTED, "the fused path does not cover d=%d dv=%d chunk=%d", d, dv, chunk);
+  return ok();
+}
+
 size_t hla2_forward_decay_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
-  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK) return 0;
+  if (chunk == 0) { fail(HLA_ERR_INVALID, "chunk must be set"); return 0; }
   // the larger of the two paths: the masked flag is not an argument here
   const size_t fused = hla::fused_decay_supported(n, d, dv, chunk, dtype, 1)
                            ? hla::fused_workspace_bytes(B * H, n, d, dv, chunk) : 0;
@@ -179,9 +213,11 @@ int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, 
   if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
   if (!std::isfinite(gamma) || gamma <= 0.f || gamma > 1.f)
     return fail(HLA_ERR_INVALID, "gamma must be finite with 0 < gamma <= 1 (got %g)", (double)gamma);
-  // the readout scales by gamma^(2 (a + 1)), a < chunk: keep it a normal number
-  if (2.0 * chunk * std::log2((double)gamma) < -125.0)
-    return fail(HLA_ERR_UNSUPPORTED, "gamma^(2*chunk) underflows fp32 (gamma=%g chunk=%d)", (double)gamma, chunk);
+  // both paths walk tiles of min(chunk, 64) tokens and scale by gamma^(2 (a + 1)), a < tile: keep that a
+  // normal number
+  const int tile = chunk < 64 ? chunk : 64;
+  if (2.0 * tile * std::log2((double)gamma) < -125.0)
+    return fail(HLA_ERR_UNSUPPORTED, "gamma^(2*%d) underflows fp32 (gamma=%g chunk=%d)", tile, (double)gamma, chunk);
   if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v")) ||
       (rc = check_ptr(out, "out")))
     return rc;
@@ -218,7 +254,12 @@ int hla2_forward_decay(const void* q, const void* k, const void* v, float* out, 
 }
 
 size_t hla2_backward_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
-  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || !hla::backward_supported(n, d, dv, dtype)) return 0;
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK) return 0;
+  if (!hla::backward_supported(n, d, dv, dtype)) {
+    fail(HLA_ERR_UNSUPPORTED, "the backward covers bf16 q/k/v with d = dv in {64, 128} (got d=%d dv=%d dtype=%d)", d,
+         dv, dtype);
+    return 0;
+  }
   return hla::backward_workspace_bytes(B * H, n, d);
 }
 
@@ -244,8 +285,12 @@ int hla2_backward(const void* q, const void* k, const void* v, const float* g, f
 }
 
 size_t ahla_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
-  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || !hla::ahla_supported(n, d, dv, chunk, dtype))
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK) return 0;
+  if (chunk == 0 || !hla::ahla_supported(n, d, dv, chunk, dtype)) {
+    fail(HLA_ERR_UNSUPPORTED, "AHLA covers bf16, d = dv in {64, 128}, chunk in {64, 128} (got d=%d dv=%d chunk=%d "
+         "dtype=%d)", d, dv, chunk, dtype);
     return 0;
+  }
   return hla::ahla_workspace_bytes(B * H, n, d);
 }
 
@@ -299,28 +344,96 @@ int hla2_scan(const float* states, const float* init, float* prefix, float* tota
   return ok();
 }
 
-size_t hla2_prefill_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
-  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
-  const size_t a = chunked_ws(B * H, n, d, dv, chunk);
-  const size_t b = align256(hla::fused_workspace_bytes(B * H, n, d, dv, chunk));
-  return (a > b ? a : b) + align256(sizeof(float) * (size_t)B * H * hla::state_floats(d, dv));
+// ---------------------------------------------------------------------------
+// Decode state descriptor.  The check word hashes every other field, so a
+// descriptor edited after hla2_state_init (a flag flipped between a prefill
+// and a step, say) is rejected.
+static unsigned long long state_check(const hla2_state* st) {
+  unsigned long long h = 1469598103934665603ull;
+  auto mix = [&](unsigned long long x) {
+    for (int b = 0; b < 8; ++b) {
+      h ^= (x >> (8 * b)) & 0xffu;
+      h *= 1099511628211ull;
+    }
+  };
+  uint32_t eb;
+  std::memcpy(&eb, &st->eps, 4);
+  mix((unsigned long long)st->B); mix((unsigned long long)st->H); mix((unsigned long long)st->d);
+  mix((unsigned long long)st->dv); mix((unsigned long long)st->masked); mix((unsigned long long)st->normalized);
+  mix((unsigned long long)st->dtype); mix(eb); mix((unsigned long long)(uintptr_t)st->data);
+  mix((unsigned long long)st->head_floats);
+  const float* f[5] = {st->S, st->C, st->m, st->G, st->h};
+  for (const float* p : f) mix((unsigned long long)(uintptr_t)p);
+  return h ^ 0x484c4132u;     // "HLA2"
 }
 
-int hla2_prefill(float* state, const void* q, const void* k, const void* v, float* out, int B, int H, int n, int d,
-                 int dv, int chunk, int masked, int normalized, float eps, int dtype, void* workspace,
-                 size_t workspace_bytes, void* stream) {
+static int check_state(const hla2_state* st) {
+  if (!st) return fail(HLA_ERR_INVALID, "state descriptor is NULL");
+  if (st->check != state_check(st))
+    return fail(HLA_ERR_INVALID, "state descriptor was not set by hla2_state_init or has changed since");
+  return HLA_OK;
+}
+
+size_t hla2_state_bytes(int B, int H, int d, int dv) {
+  if (check_dims(B, H, 1, d, dv, 0, HLA_FP32, false) != HLA_OK) return 0;
+  return sizeof(float) * (size_t)B * H * hla::state_floats(d, dv);
+}
+
+int hla2_state_init(hla2_state* st, void* buf, size_t buf_bytes, int B, int H, int d, int dv, int masked,
+                    int normalized, float eps, int dtype, void* stream) {
   int rc;
+  if (!st) return fail(HLA_ERR_INVALID, "state descriptor is NULL");
+  if ((rc = check_dims(B, H, 1, d, dv, 0, dtype, false)) != HLA_OK) return rc;
+  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
+  if ((rc = check_ptr(buf, "buf")) != HLA_OK) return rc;
+  const size_t need = hla2_state_bytes(B, H, d, dv);
+  if (buf_bytes < need) return fail(HLA_ERR_INVALID, "state buffer of %zu bytes needed, %zu given", need, buf_bytes);
+  hla2_state s{};
+  s.B = B; s.H = H; s.d = d; s.dv = dv;
+  s.masked = masked; s.normalized = normalized; s.dtype = dtype; s.eps = eps;
+  s.data = static_cast<float*>(buf);
+  s.head_floats = hla::state_floats(d, dv);
+  s.S = s.data;
+  s.C = s.data + hla::off_C(d, dv);
+  s.m = s.data + hla::off_m(d, dv);
+  s.G = s.data + hla::off_G(d, dv);
+  s.h = s.data + hla::off_h(d, dv);
+  s.check = state_check(&s);
+  const hipError_t e = hla::launch_zero(s.data, need / 16, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "state zeroing");
+  *st = s;
+  return ok();
+}
+
+static size_t prefill_ws(int BH, int n, int d, int dv, int chunk) {
+  const size_t a = chunked_ws(BH, n, d, dv, chunk);
+  const size_t b = align256(hla::fused_workspace_bytes(BH, n, d, dv, chunk));
+  return (a > b ? a : b) + align256(sizeof(float) * (size_t)BH * hla::state_floats(d, dv));
+}
+
+size_t hla2_prefill_workspace_bytes(const hla2_state* st, int n, int chunk) {
+  if (check_state(st) != HLA_OK) return 0;
+  if (check_dims(st->B, st->H, n, st->d, st->dv, chunk, st->dtype, true) != HLA_OK) return 0;
+  if (chunk == 0) { fail(HLA_ERR_INVALID, "chunk must be set"); return 0; }
+  return prefill_ws(st->B * st->H, n, st->d, st->dv, chunk);
+}
+
+int hla2_prefill(hla2_state* st, const void* q, const void* k, const void* v, int n, int chunk, float* out,
+                 void* workspace, size_t workspace_bytes, void* stream) {
+  int rc;
+  if ((rc = check_state(st)) != HLA_OK) return rc;
+  const int B = st->B, H = st->H, d = st->d, dv = st->dv, dtype = st->dtype;
+  const int masked = st->masked, normalized = st->normalized;
+  const float eps = st->eps;
+  float* state = st->data;
   if ((rc = check_dims(B, H, n, d, dv, chunk, dtype, true)) != HLA_OK) return rc;
   if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
-  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
-  if ((rc = check_ptr(state, "state")) || (rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) ||
-      (rc = check_ptr(v, "v")))
-    return rc;
+  if ((rc = check_ptr(q, "q")) || (rc = check_ptr(k, "k")) || (rc = check_ptr(v, "v"))) return rc;
   if (out && !aligned16(out)) return fail(HLA_ERR_INVALID, "out is not 16-byte aligned");
   const int BH = B * H;
   const size_t cws = chunked_ws(BH, n, d, dv, chunk);
   const size_t fws = align256(hla::fused_workspace_bytes(BH, n, d, dv, chunk));
-  const size_t need = hla2_prefill_workspace_bytes(B, H, n, d, dv, chunk, dtype);
+  const size_t need = prefill_ws(BH, n, d, dv, chunk);
   if (!workspace || workspace_bytes < need)
     return fail(HLA_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, workspace_bytes);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -351,23 +464,25 @@ int hla2_prefill(float* state, const void* q, const void* k, const void* v, floa
   return ok();
 }
 
-int hla2_step(float* state, const void* q_t, const void* k_t, const void* v_t, float* out_t, int B, int H, int d,
-              int dv, int masked, int normalized, float eps, int dtype, void* stream) {
+int hla2_step(hla2_state* st, const void* q_t, const void* k_t, const void* v_t, float* out_t, void* stream) {
   int rc;
-  if ((rc = check_dims(B, H, 1, d, dv, 0, dtype, false)) != HLA_OK) return rc;
-  if ((rc = check_flags(masked, normalized, eps)) != HLA_OK) return rc;
-  if ((rc = check_ptr(state, "state")) || (rc = check_ptr(q_t, "q_t")) || (rc = check_ptr(k_t, "k_t")) ||
-      (rc = check_ptr(v_t, "v_t")) || (rc = check_ptr(out_t, "out_t")))
+  if ((rc = check_state(st)) != HLA_OK) return rc;
+  if ((rc = check_ptr(q_t, "q_t")) || (rc = check_ptr(k_t, "k_t")) || (rc = check_ptr(v_t, "v_t")) ||
+      (rc = check_ptr(out_t, "out_t")))
     return rc;
-  hipError_t e = hla::launch_step(state, q_t, k_t, v_t, out_t, B * H, d, dv, masked, normalized, eps, dtype,
-                                  reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = hla::launch_step(st->data, q_t, k_t, v_t, out_t, st->B * st->H, st->d, st->dv, st->masked,
+                                  st->normalized, st->eps, st->dtype, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "step");
   return ok();
 }
 
 size_t hla3_workspace_bytes(int B, int H, int n, int d, int dv, int chunk, int dtype) {
-  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK || chunk == 0) return 0;
-  if (!hla::hla3_supported(d, dv, chunk, 1)) return 0;
+  if (check_dims(B, H, n, d, dv, chunk, dtype, true) != HLA_OK) return 0;
+  if (chunk == 0) { fail(HLA_ERR_INVALID, "chunk must be set"); return 0; }
+  if (!hla::hla3_supported(d, dv, chunk, 1)) {
+    fail(HLA_ERR_UNSUPPORTED, "hla3_forward needs d, dv in {16, 32} (got d=%d dv=%d)", d, dv);
+    return 0;
+  }
   return hla::hla3_workspace(B * H, n, d, dv, chunk);
 }
 

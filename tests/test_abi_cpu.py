@@ -1,10 +1,15 @@
 """Host-side checks of the C ABI: the library loads without a GPU, exports
 every function include/hla.h declares, and the Python binding's argument
 lists match the header.  No compute call is made."""
+import ctypes
 import os
 import re
 
+import pytest
+import torch
+
 from paper_2510_27258_amd import capi
+from paper_2510_27258_amd import hla
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "hla.h")
 
@@ -122,11 +127,15 @@ def test_other_entry_points_reject_bad_arguments():
     # scan: no segments, misaligned init
     assert L.hla2_scan(P, None, P, None, 1, 1, 0, 64, 64, None) == INVALID
     assert L.hla2_scan(P, P + 8, P, None, 1, 1, 4, 64, 64, None) == INVALID
-    # decode step and prefill: NULL state, bad flags
-    assert L.hla2_step(None, P, P, P, P, 1, 1, 64, 64, 1, 0, 1e-6, BF16, None) == INVALID
-    assert L.hla2_step(P, P, P, P, P, 1, 1, 64, 64, 1, 2, 1e-6, BF16, None) == INVALID
-    assert L.hla2_prefill(None, P, P, P, None, 1, 1, 64, 64, 64, 64, 1, 0, 1e-6, BF16, None, 0, None) == INVALID
-    assert L.hla2_prefill(P, P, P, P, P + 4, 1, 1, 64, 64, 64, 64, 1, 0, 1e-6, BF16, None, 0, None) == INVALID
+    # decode step and prefill: NULL descriptor, one not made by hla2_state_init
+    assert L.hla2_step(None, P, P, P, P, None) == INVALID
+    assert L.hla2_prefill(None, P, P, P, 64, 64, None, None, 0, None) == INVALID
+    forged = capi.HLA2State(B=1, H=1, d=64, dv=64, masked=1, normalized=0, dtype=BF16, eps=1e-6, data=P,
+                            head_floats=capi.hla2_state_floats(64, 64), check=12345)
+    assert L.hla2_step(ctypes.byref(forged), P, P, P, P, None) == INVALID
+    assert "hla2_state_init" in capi.hla_last_error()
+    assert L.hla2_prefill(ctypes.byref(forged), P, P, P, 64, 64, None, None, 0, None) == INVALID
+    assert L.hla2_prefill_workspace_bytes(ctypes.byref(forged), 64, 64) == 0
     # chunk summaries: empty input
     assert L.hla2_chunk_summaries(P, P, P, P, 1, 1, 0, 64, 64, 64, BF16, None) == INVALID
 
@@ -140,3 +149,114 @@ def test_workspace_queries_follow_the_checks():
     assert capi.hla3_workspace_bytes(1, 1, 64, 16, 16, 32, FP32) > 0
     assert capi.ahla_workspace_bytes(1, 1, 64, 64, 64, 64, BF16) > 0
     assert capi.hla2_backward_workspace_bytes(1, 1, 64, 64, 64, 64, BF16) > 0
+
+
+def test_state_queries_and_init_checks():
+    """hla2_state_bytes follows the size rules; hla2_state_init rejects bad
+    arguments before it enqueues anything (its zeroing launch needs a GPU)."""
+    L = capi.lib()
+    assert capi.hla2_state_bytes(2, 3, 64, 32) == 4 * 6 * capi.hla2_state_floats(64, 32)
+    assert capi.hla2_state_bytes(1, 1, 24, 64) == 0 and "d and dv" in capi.hla_last_error()
+    assert capi.hla2_state_bytes(0, 1, 64, 64) == 0
+    st = capi.HLA2State()
+    need = capi.hla2_state_bytes(1, 2, 64, 64)
+    assert L.hla2_state_init(None, P, need, 1, 2, 64, 64, 1, 0, 1e-6, BF16, None) == INVALID
+    assert L.hla2_state_init(ctypes.byref(st), None, need, 1, 2, 64, 64, 1, 0, 1e-6, BF16, None) == INVALID
+    assert L.hla2_state_init(ctypes.byref(st), P + 4, need, 1, 2, 64, 64, 1, 0, 1e-6, BF16, None) == INVALID
+    assert L.hla2_state_init(ctypes.byref(st), P, need - 16, 1, 2, 64, 64, 1, 0, 1e-6, BF16, None) == INVALID
+    assert "state buffer" in capi.hla_last_error()
+    assert L.hla2_state_init(ctypes.byref(st), P, need, 1, 2, 64, 64, 2, 0, 1e-6, BF16, None) == INVALID
+    assert L.hla2_state_init(ctypes.byref(st), P, need, 1, 2, 64, 64, 1, 0, -1.0, BF16, None) == INVALID
+    assert L.hla2_state_init(ctypes.byref(st), P, need, 1, 2, 64, 64, 1, 0, 1e-6, 3, None) == INVALID
+    assert L.hla2_state_init(ctypes.byref(st), P, need, 1, 2, 96, 64, 1, 0, 1e-6, BF16, None) == UNSUP
+    assert st.check == 0      # nothing was written on failure
+
+
+def test_descriptor_layout_matches_header():
+    """The ctypes mirror of hla2_state has the C layout: ints, the float eps,
+    then pointer-aligned fields."""
+    assert ctypes.sizeof(capi.HLA2State) == 96
+    assert capi.HLA2State.data.offset == 32 and capi.HLA2State.check.offset == 88
+
+
+def test_workspace_query_status():
+    nb = ctypes.c_size_t(7)
+    L = capi.lib()
+    assert L.hla2_workspace_query(1, 1, 0, 64, 64, 64, BF16, 0, ctypes.byref(nb)) == INVALID and nb.value == 0
+    assert L.hla2_workspace_query(1, 1, 64, 64, 64, 64, BF16, 0, None) == INVALID
+    assert L.hla2_workspace_query(1, 1, 64, 64, 64, 64, FP32, capi.HLA_ALGO_FUSED, ctypes.byref(nb)) == UNSUP
+    assert L.hla2_workspace_query(1, 1, 64, 64, 64, 64, BF16, 9, ctypes.byref(nb)) == INVALID
+    assert capi.hla2_workspace_query(2, 3, 500, 64, 64, 64, BF16, 0) == capi.hla2_workspace_bytes_ex(
+        2, 3, 500, 64, 64, 64, BF16, 0) > 0
+    with pytest.raises(capi.HLAError):
+        capi.hla2_workspace_query(1, 1, 64, 24, 64, 64, BF16, 0)
+
+
+def test_fused_plan_query():
+    P_, tile = capi.hla2_fused_plan(2, 32, 16384, 128, 128, 128)
+    assert tile == 64 and 1 <= P_ <= 256
+    P2, tile2 = capi.hla2_fused_plan(4, 16, 4096, 64, 64, 64)
+    assert tile2 == 64 and P2 >= 1
+    with pytest.raises(capi.HLAError) as ei:
+        capi.hla2_fused_plan(1, 1, 64, 16, 16, 16)
+    assert ei.value.code == UNSUP
+
+
+def test_forward_den_needs_normalized():
+    L = capi.lib()
+    rc = L.hla2_forward_ex(P, P, P, P, P, 1, 1, 64, 64, 64, 64, 1, 0, 1e-6, BF16, P, 1 << 30, 0, None)
+    assert rc == INVALID and "normalized" in capi.hla_last_error()
+    rc = L.hla2_forward_ex(P, P, P, P, P + 4, 1, 1, 64, 64, 64, 64, 1, 1, 1e-6, BF16, P, 1 << 30, 0, None)
+    assert rc == INVALID and "den is not 16-byte aligned" in capi.hla_last_error()
+
+
+# ----------------------------------------------------------------------------
+# The torch binding checks shapes, dtypes and devices before any launch (the C
+# ABI sees only pointers and sizes taken from q).  CPU tensors: each case must
+# fail on its own mismatch, before the device check.
+def _t(*shape, dtype=torch.bfloat16):
+    return torch.zeros(*shape, dtype=dtype)
+
+
+@pytest.mark.parametrize("case", ["k_shape", "v_rows", "k_dtype", "v_dtype", "rank"])
+def test_binding_rejects_mismatched_inputs(case):
+    q = _t(1, 2, 16, 32)
+    k, v = _t(1, 2, 16, 32), _t(1, 2, 16, 64)
+    if case == "k_shape":
+        k = _t(1, 2, 16, 16)
+    elif case == "v_rows":
+        v = _t(1, 2, 15, 64)
+    elif case == "k_dtype":
+        k = _t(1, 2, 16, 32, dtype=torch.float32)
+    elif case == "v_dtype":
+        v = _t(1, 2, 16, 64, dtype=torch.float32)
+    else:
+        q, k = _t(2, 16, 32), _t(2, 16, 32)
+    for fn in (lambda: hla.forward(q, k, v, 16), lambda: hla.forward_decay(q, k, v, 16, 0.9),
+               lambda: hla.hla3_forward(q, k, v, 16), lambda: hla.ahla_forward(q, k, v, 64),
+               lambda: hla.chunk_summaries(q, k, v, 16)):
+        with pytest.raises(ValueError) as ei:
+            fn()
+        assert "GPU" not in str(ei.value), str(ei.value)
+
+
+def test_binding_rejects_wrong_out_and_state():
+    q = _t(1, 2, 16, 32)
+    with pytest.raises(ValueError):
+        hla._fp32_out(torch.zeros(1, 2, 16, 31), (1, 2, 16, 32), q.device)
+    with pytest.raises(ValueError):
+        hla._fp32_out(torch.zeros(1, 2, 16, 32, dtype=torch.float64), (1, 2, 16, 32), q.device)
+    with pytest.raises(ValueError):
+        hla.scan(torch.zeros(1, 1, 3, 100), 32, 32)
+    with pytest.raises(ValueError):
+        hla.backward(q, q, q, torch.zeros(1, 2, 15, 32))
+
+
+def test_decay_underflow_check_uses_the_walked_tile():
+    """gamma^(2*64) must stay normal for chunk 64 and 128 alike (both walk
+    64-token tiles): 0.6 passes the check at chunk 128 and stops at the NULL
+    pointer check; 0.4 fails it."""
+    L = capi.lib()
+    assert L.hla2_forward_decay(None, P, P, P, 1, 1, 64, 64, 64, 128, 1, 0, 1e-6, 0.6, BF16, None, 0, None) == INVALID
+    assert "q is NULL" in capi.hla_last_error()
+    assert L.hla2_forward_decay(P, P, P, P, 1, 1, 64, 64, 64, 128, 1, 0, 1e-6, 0.4, BF16, None, 0, None) == UNSUP

@@ -157,3 +157,13 @@ def test_decay_fused_workload_b2h32_d128_sampled_heads():
     err = rowwise_err(out[0, :2], ref)
     _say(f"decay fused d128 row-wise error {err:.3e}")
     assert err <= tol_for(code)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_decay_chunk128_strong_gamma(d):
+    """chunk 128 runs in 64-token tiles on both paths, so the underflow check
+    applies to the tile: gamma = 0.6 (gamma^256 below the fp32 normal range,
+    gamma^128 above it) is accepted at chunk 128 and matches the oracle on the
+    fused (bf16) and chunked (fp32) paths."""
+    _check(1, 2, 3 * 128 + 21, d, d, 128, "unit", 0.6, seed=d + 3)
+    _check(1, 2, 3 * 128 + 21, d, d, 128, "scaled", 0.6, seed=d + 4)

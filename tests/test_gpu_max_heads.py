@@ -47,7 +47,7 @@ def test_decode_max_heads():
     _say(f"case max heads prefill + steps B={B} H={H} d=16")
     num_ref, _, _, _ = native.hla2_serial_c(_pick(q), _pick(k), _pick(v), masked=True, threads=16)
     qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
-    state = hla.new_state(B, H, 16, 16)
+    state = hla.State(B, H, 16, 16, dtype=qd.dtype)
     hla.prefill(state, qd[:, :, :4].contiguous(), kd[:, :, :4].contiguous(), vd[:, :, :4].contiguous(), 16,
                 want_out=False)
     got = torch.stack([hla.step(state, qd[:, :, t].contiguous(), kd[:, :, t].contiguous(), vd[:, :, t].contiguous())
