@@ -131,6 +131,25 @@ int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int *segments
 int hla2_algo_supported(int algo, int n, int d, int dv, int chunk, int dtype, int masked);
 
 /* ---------------------------------------------------------------------------
+ * hla2_forward_noalloc — hla2_forward for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, checks and results as hla2_forward
+ * (algorithm HLA_ALGO_AUTO), without the workspace arguments: the workspace
+ * is a fixed array of HLA_NOALLOC_SCRATCH_BYTES bytes in the library's own
+ * device memory, one per GPU, held until the process ends.  Sizes whose
+ * workspace (hla2_workspace_query of the algorithm HLA_ALGO_AUTO takes for
+ * the call's masked flag) exceeds it return HLA_ERR_WORKSPACE before
+ * anything is enqueued.  The call allocates nothing.  Every call on one GPU
+ * shares that GPU's array (no call needs it cleared: the workspace's
+ * contents on entry are ignored), so calls that overlap on one GPU (other
+ * streams, other threads) race and must be ordered by the caller.
+ * ------------------------------------------------------------------------- */
+#define HLA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int hla2_forward_noalloc(const void *q, const void *k, const void *v, float *out,
+                         int B, int H, int n, int d, int dv, int chunk, int masked, int normalized,
+                         float eps, int dtype, void *stream);
+
+/* ---------------------------------------------------------------------------
  * hla2_chunk_summaries — the summary of every chunk of `chunk` tokens with a
  * zero carry-in: the (+)-product of its token segments (Sec. 4.2, Rem.
  * scan-modes: chunk summary).  states: [B, H, M, F], M = ceil(n / chunk);

@@ -43,6 +43,7 @@ _SIGS = {
     "hla2_forward": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _P]),
     "hla2_forward_ex": (_I, [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _I, _P]),
     "hla2_workspace_query": (_I, [_I] * 8 + [_ZP]),
+    "hla2_forward_noalloc": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P]),
     "hla2_fused_plan": (_I, [_I] * 6 + [_IP, _IP]),
     "hla2_state_bytes": (_Z, [_I] * 4),
     "hla2_state_init": (_I, [_SP, _P, _Z] + [_I] * 6 + [_F, _I, _P]),
@@ -128,6 +129,10 @@ def hla2_forward_ex(q, k, v, out, den, B, H, n, d, dv, chunk, masked, normalized
                     stream):
     return _call("hla2_forward_ex", q, k, v, out, den, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, ws,
                  ws_bytes, algo, stream)
+
+
+def hla2_forward_noalloc(q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, stream):
+    return _call("hla2_forward_noalloc", q, k, v, out, B, H, n, d, dv, chunk, masked, normalized, eps, dtype, stream)
 
 
 def hla2_workspace_query(B, H, n, d, dv, chunk, dtype, algo):

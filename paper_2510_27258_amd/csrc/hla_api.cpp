@@ -84,6 +84,11 @@ int select_algo(int algo, int n, int d, int dv, int chunk, int dtype, int masked
 
 }  // namespace
 
+namespace hla {
+// Sets the thread's last error from another source file of the library.
+int api_fail(int code, const char* msg) { return fail(code, "%s", msg); }
+}  // namespace hla
+
 extern "C" {
 
 const char* hla_last_error(void) { return g_err; }
