@@ -53,6 +53,12 @@
  *     testing and tuning; any p >= 1 gives the same result up to fp32
  *     rounding order.  Workspace queries read it too: set it before the
  *     query.  A call checks its workspace against its own plan.
+ *   - At d = dv = 128 (chunk 64 or 128, bf16, masked, no states) the fused
+ *     forward writes every output row once: a summary walk gives each
+ *     segment's bracket, and one walk per segment starts from its true carry.
+ *     HLA_FUSED_LEGACY=1 selects instead the walk whose outputs a second
+ *     kernel corrects by the carry (the form prefill with states uses), for
+ *     testing; both give the same result up to fp32 rounding order.
  */
 #ifndef HLA_H
 #define HLA_H

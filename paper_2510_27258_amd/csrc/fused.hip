@@ -46,6 +46,7 @@
 
 #include "fused.h"
 #include "fused_tiles.h"
+#include "fused_ws.h"
 #include "profile.h"
 
 namespace hla {
@@ -1070,6 +1071,77 @@ size_t records_bytes(int BH, int P, int d, int dv) {
   return (sizeof(float) * (size_t)BH * (P + 1) * state_floats(d, dv) + 255) & ~size_t(255);
 }
 
+size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Workspace of the wave-specialised pipeline (d = dv = 128, no initial or
+// final state): records [BH][P + 1][F] | S prefixes [BH][P][d d] | Phi, eta
+// carries [BH][P][d dv + d].
+size_t ws_pipeline_bytes(int BH, int P) {
+  constexpr int D = CfgWS::D, DV = CfgWS::DV;
+  return records_bytes(BH, P, D, DV) + al256(sizeof(float) * (size_t)BH * P * D * D) +
+         al256(sizeof(float) * (size_t)BH * P * ((size_t)D * DV + D));
+}
+
+bool legacy_pipeline() {
+  const char* e = getenv("HLA_FUSED_LEGACY");
+  return e && e[0] == '1';
+}
+
+hipError_t launch_ws(bool summary, dim3 grid, hipStream_t s, const uint16_t* q, const uint16_t* k,
+                     const uint16_t* v, float* out, float* den_out, const float* spre, const float* carry,
+                     float* rec, int n, int cps, int nseg, int normalized, float eps) {
+  const void* fn = summary ? (const void*)k_walk_ws<true> : (const void*)k_walk_ws<false>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)CfgWS::bytes);
+  if (e != hipSuccess) return e;
+  void* args[] = {&q, &k, &v, &out, &den_out, &spre, &carry, &rec, &n, &cps, &nseg, &normalized, &eps};
+  return prof_launch(fn, grid, dim3(CfgWS::NT), args, CfgWS::bytes, s);
+}
+
+// The forward at d = dv = 128 (64-token tiles) without states, every output
+// row written once:
+//   1. k_moments: S of segments 0 .. P-2;  k_seg_prefix: S prefixes;
+//   2. k_walk_ws<SUMMARY> over segments 0 .. P-2: each segment's bracket
+//      (Phi, eta) from its true S prefix;  k_seg_prefix: Phi, eta carries;
+//   3. k_walk_ws over every segment from its true carry: final outputs.
+hipError_t run_ws(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
+  constexpr int C = CfgWS::C, D = CfgWS::D, DV = CfgWS::DV;
+  const int BH = f.BH;
+  const size_t F = state_floats(D, DV);
+  float* segs = reinterpret_cast<float*>(ws);
+  float* spre = reinterpret_cast<float*>(ws + records_bytes(BH, P, D, DV));
+  float* carry = reinterpret_cast<float*>(reinterpret_cast<char*>(spre) + al256(sizeof(float) * (size_t)BH * P * D * D));
+  const uint16_t* q = static_cast<const uint16_t*>(f.q);
+  const uint16_t* k = static_cast<const uint16_t*>(f.k);
+  const uint16_t* v = static_cast<const uint16_t*>(f.v);
+  hipError_t e;
+  if (P > 1) {
+    prof_start("moments", s);
+    HLA_LAUNCH((k_moments<C, D, DV, false, false, false>), dim3(P - 1, BH), dim3(kThreads), 0, s, q, k, v, segs, f.n,
+               cps, P, 0, 0.f);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    prof_start("seg_prefix", s);
+    HLA_LAUNCH(k_seg_prefix, dim3((D * D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, 0, D * D, 0, spre, P);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    prof_start("walk_summary", s);
+    e = launch_ws(true, dim3(P - 1, BH), s, q, k, v, nullptr, nullptr, spre, nullptr, segs, f.n, cps, P, 0, 0.f);
+    prof_stop(s);
+    if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
+    prof_start("seg_prefix", s);
+    HLA_LAUNCH(k_seg_prefix, dim3((D * DV + D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, (int)off_G(D, DV),
+               D * DV + D, 0, carry, P);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  prof_start("walk", s);
+  e = launch_ws(false, dim3(P, BH), s, q, k, v, f.out, f.normalized ? f.den_out : nullptr, P > 1 ? spre : nullptr,
+                P > 1 ? carry : nullptr, segs, f.n, cps, P, f.normalized, f.eps);
+  prof_stop(s);
+  if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
+  return hipSuccess;
+}
+
 // DEC: the decayed operator (row-split shapes, no initial or final state).
 template <int C, int D, int DV, bool RS, bool DEC = false>
 hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* ws, int P, int cps,
@@ -1143,6 +1215,9 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
 // shapes in the column layout.
 bool row_split_shape(const Shape& sh) { return sh.C == 64 && sh.D == sh.DV && (sh.D == 64 || sh.D == 128); }
 
+// The wave-specialised walk covers (64, 128, 128).
+bool ws_shape(const Shape& sh) { return sh.C == CfgWS::C && sh.D == CfgWS::D && sh.DV == CfgWS::DV; }
+
 int plan_blocks(const Shape& sh) {
   if (row_split_shape(sh)) return sh.D == 64 ? CfgRS<64, false>::kBlocks : CfgRS<128, false>::kBlocks;
   return sh.blocks;
@@ -1187,7 +1262,12 @@ size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
   fused_plan(*sh, BH, n, &P, &cps);
   const size_t den = sizeof(float) * (((size_t)BH * n + (size_t)BH * ((n + sh->C - 1) / sh->C) * d + 63) & ~size_t(63));
   const size_t carry = sizeof(float) * (size_t)BH * P * ((size_t)d * dv + d);
-  return records_bytes(BH, P, d, dv) + den + carry + 256;
+  const size_t legacy = records_bytes(BH, P, d, dv) + den + carry + 256;
+  if (ws_shape(*sh)) {
+    const size_t w = ws_pipeline_bytes(BH, P);
+    return w > legacy ? w : legacy;
+  }
+  return legacy;
 }
 
 hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, void* workspace, hipStream_t s) {
@@ -1196,6 +1276,8 @@ hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, voi
   int P, cps;
   fused_plan(*sh, f.BH, f.n, &P, &cps);
   char* ws = static_cast<char*>(workspace);
+  if (f.gamma == 1.f && !init && !final_state && ws_shape(*sh) && !legacy_pipeline())
+    return run_ws(f, ws, P, cps, s);
   if (f.gamma != 1.f) {           // decayed: row-split shapes only, no states
     if (!row_split_shape(*sh) || init || final_state) return hipErrorNotSupported;
     if (sh->D == 64) return run_shape<64, 64, 64, true, true>(f, init, final_state, ws, P, cps, s);

@@ -176,6 +176,34 @@ def test_fused_segment_counts(segments, monkeypatch):
     assert _check_forward(1, 2, 64 * 9 + 20, 64, 64, 64, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=11)
 
 
+@pytest.mark.parametrize("segments", [1, 2, 3, 7, 100])
+def test_fused_d128_segment_counts(segments, monkeypatch):
+    """The d = 128 pipeline (summary walk of the earlier segments, their
+    carries, then one output walk per segment from its true carry) must not
+    depend on the segment plan either; ragged tail, normalised."""
+    monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
+    assert _check_forward(2, 1, 64 * 9 + 20, 128, 128, 128, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=13)
+
+
+def test_fused_d128_pipelines_agree(monkeypatch):
+    """The d = 128 forward's two pipelines (every output row written once
+    from the true carry, and the earlier walk + carry fix-up, which prefill
+    with states still uses) agree to the bf16 bar, num and den."""
+    q, k, v, code = gen(2, 3, 64 * 11 + 5, 128, 128, "unit", 17)
+    qd, kd, vd = dev(q, code), dev(k, code), dev(v, code)
+    res = []
+    for legacy in ("0", "1"):
+        monkeypatch.setenv("HLA_FUSED_LEGACY", legacy)
+        den = torch.empty(2, 3, q.shape[2], device="cuda")
+        out = hla.forward(qd, kd, vd, 128, normalized=True, algo=capi.HLA_ALGO_FUSED, den=den)
+        num = hla.forward(qd, kd, vd, 128, algo=capi.HLA_ALGO_FUSED)
+        res.append((num.cpu().numpy(), den.cpu().numpy(), out.cpu().numpy()))
+    (n0, d0, o0), (n1, d1, o1) = res
+    assert rowwise_err(n0, n1) <= 2e-3
+    D = O.hla2_den_scale(q, k)
+    assert float((np.abs(d0 - d1) / D).max()) <= 2e-3
+
+
 def test_fused_long_single_head():
     """One head of 262 144 tokens: 4096 tiles cut into the plan's largest
     segment count (one head), so the longest carry chains and the largest
