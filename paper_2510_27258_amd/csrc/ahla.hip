@@ -18,7 +18,8 @@
 // R_B P_A is exactly what a segment's walk accumulates when it starts from
 // the true P prefix.  So
 //   1. k_moments<KV>: P = K^T V and m = K^T 1 of every segment;
-//   2. k_ahla_walk: every segment walks from P0 = the P prefix of the
+//   2. k_seg_prefix: the running sums of P and m^K over the segments;
+//      k_ahla_walk: every segment walks from P0 = the P prefix of the
 //      segments before it (m0 likewise) and E0 = n0 = 0, writes the partial
 //      outputs (and, normalised, A s plus the n0 of every tile), and leaves
 //      its bracket E0 (n0) in the G (h) slot of its record;
@@ -70,8 +71,8 @@ struct CfgAH {
 template <int D>
 __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_walk(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, int n, int cps, int nseg,
-    int normalized) {
+    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ ppre,
+    int n, int cps, int nseg, int normalized) {
   using G = CfgAH<D>;
   constexpr bool kO = D == 128;     // per-tile opaque lane index (registers)
   constexpr int C = G::C, DV = G::DV, NT = G::NT, ST = G::ST;
@@ -114,25 +115,18 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
     n0[ta] = 0.f;
   }
   if (seg > 0) {
+    // P0, m0 = the prefix of the earlier segments' moments: one record
+    // [D * DV | D] per segment (k_seg_prefix)
     constexpr int nP4 = D * DV / 4 / NT;
     static_assert(D * DV % (4 * NT) == 0, "carry staging split");
+    const float* x = ppre + ((size_t)bh * nseg + seg) * ((size_t)D * DV + D);
     float4 pa[nP4];
 #pragma unroll
-    for (int r = 0; r < nP4; ++r) pa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
-    float ma = 0.f;
-    for (int sp = 0; sp < seg; ++sp) {
-      const float* x = rec + ((size_t)bh * (nseg + 1) + sp) * F;
-#pragma unroll
-      for (int r = 0; r < nP4; ++r) {
-        const float4 u = reinterpret_cast<const float4*>(x + off_C(D, DV))[tid + NT * r];
-        pa[r].x += u.x; pa[r].y += u.y; pa[r].z += u.z; pa[r].w += u.w;
-      }
-      if (ta >= 0) ma += x[off_m(D, DV) + ta];
-    }
+    for (int r = 0; r < nP4; ++r) pa[r] = reinterpret_cast<const float4*>(x)[tid + NT * r];
     float* st = reinterpret_cast<float*>(lds);
 #pragma unroll
     for (int r = 0; r < nP4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = pa[r];
-    if (ta >= 0) m0[ta] = ma;
+    if (ta >= 0) m0[ta] = x[D * DV + ta];
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < ST; ++i)
@@ -359,6 +353,8 @@ size_t records_bytes_ah(int BH, int P, int d) {
 size_t den_bytes_ah(int BH, int n, int d) {
   return sizeof(float) * (((size_t)BH * n + (size_t)BH * ((n + 63) / 64) * d + 63) & ~size_t(63));
 }
+// carries [BH][P][d d + d] (k_carry), then the moment prefixes [BH][P][d d + d]
+size_t carry_bytes_ah(int BH, int P, int d) { return sizeof(float) * (size_t)BH * P * ((size_t)d * d + d); }
 
 template <int D>
 hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
@@ -368,6 +364,7 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
   float* segs = reinterpret_cast<float*>(ws);
   float* den = reinterpret_cast<float*>(ws + records_bytes_ah(BH, P, D));
   float* carry = reinterpret_cast<float*>(ws + records_bytes_ah(BH, P, D) + den_bytes_ah(BH, f.n, D));
+  float* ppre = reinterpret_cast<float*>(reinterpret_cast<char*>(carry) + carry_bytes_ah(BH, P, D));
   const uint16_t* q = static_cast<const uint16_t*>(f.q);
   const uint16_t* k = static_cast<const uint16_t*>(f.k);
   const uint16_t* v = static_cast<const uint16_t*>(f.v);
@@ -378,13 +375,18 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
     HLA_LAUNCH((k_moments<C, D, D, true>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1, 0.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    prof_start("ahla_prefix", s);     // the P and m^K slots are adjacent (C | m)
+    HLA_LAUNCH(k_seg_prefix, dim3((D * D + D + 1023) / 1024, BH), dim3(256), 0, s, segs, state_floats(D, D),
+               (int)off_C(D, D), D * D + D, 0, ppre, P, 1.f);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if ((e = hipFuncSetAttribute((const void*)k_ahla_walk<D>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                (int)G::bytes)) != hipSuccess)
     return e;
   prof_start("ahla_walk", s);
-  HLA_LAUNCH((k_ahla_walk<D>), grid, dim3(G::NT), G::bytes, s, q, k, v, f.out, den, segs, f.n, cps, P,
-                     f.normalized);
+  HLA_LAUNCH((k_ahla_walk<D>), grid, dim3(G::NT), G::bytes, s, q, k, v, f.out, den, segs, (const float*)ppre, f.n,
+             cps, P, f.normalized);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (P > 1 || f.normalized) {
@@ -418,8 +420,7 @@ bool ahla_supported(int n, int d, int dv, int chunk, int dtype) {
 size_t ahla_workspace_bytes(int BH, int n, int d) {
   int P, cps;
   ahla_plan(d, BH, n, &P, &cps);
-  const size_t carry = sizeof(float) * (size_t)BH * P * ((size_t)d * d + d);
-  return records_bytes_ah(BH, P, d) + den_bytes_ah(BH, n, d) + carry + 256;
+  return records_bytes_ah(BH, P, d) + den_bytes_ah(BH, n, d) + 2 * carry_bytes_ah(BH, P, d) + 256;
 }
 
 hipError_t launch_ahla(const Fwd& f, void* workspace, hipStream_t s) {

@@ -273,7 +273,7 @@ __global__ __launch_bounds__(256) void k_total(const float* __restrict__ segs, c
 template <int C, int D, int DV, bool SUMMARY>
 __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k_walk(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ init,
+    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ spre,
     int n, int cps, int nseg, int normalized, float eps, float lg2g) {
   using G = Cfg<C, D, DV, SUMMARY>;
   extern __shared__ __align__(16) uint16_t lds[];
@@ -314,23 +314,16 @@ __global__ __launch_bounds__(kThreads, (Cfg<C, D, DV, SUMMARY>::kBlocks)) void k
     P0[i] = zero16();
   }
   for (int a = tid; a < D; a += kThreads) eta[a] = 0.f;
-  if (seg > 0 || init) {
-    // S0 = sum of the S slots of the converted initial state and the earlier
-    // segments, in float4 registers, staged through the (still free) tile
-    // region of LDS; every wave picks up its columns
+  if (spre) {
+    // S0 = the S prefix of this segment (the converted initial state and the
+    // earlier segments), staged through the (still free) tile region of LDS;
+    // every wave picks up its columns
     constexpr int nS4 = D * D / 4 / kThreads;
     static_assert(D * D % (4 * kThreads) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
+    const float4* x = reinterpret_cast<const float4*>(spre + ((size_t)bh * nseg + seg) * D * D);
     float4 sa[nS4];
 #pragma unroll
-    for (int r = 0; r < nS4; ++r) sa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sp = init ? -1 : 0; sp < seg; ++sp) {
-      const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
-#pragma unroll
-      for (int r = 0; r < nS4; ++r) {
-        const float4 u = reinterpret_cast<const float4*>(x)[tid + kThreads * r];
-        sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
-      }
-    }
+    for (int r = 0; r < nS4; ++r) sa[r] = x[tid + kThreads * r];
     float* st = reinterpret_cast<float*>(lds);
 #pragma unroll
     for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + kThreads * r] = sa[r];
@@ -658,7 +651,7 @@ __device__ __forceinline__ void xch_add(const float* X, int slot, f32x16& a, int
 template <int D, bool SUMMARY, bool DEC = false>
 __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlocks)) void k_walk_rs(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ init,
+    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ spre,
     int n, int cps, int nseg, int normalized, float eps, float lg2g) {
   using G = CfgRS<D, SUMMARY>;
   constexpr bool kO = D == 128;     // at 512 threads the hoisted LDS addresses would spill
@@ -708,28 +701,16 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     P0[i] = zero16();
   }
   for (int a = tid; a < D; a += NT) eta[a] = 0.f;
-  if (seg > 0 || init) {
-    // S0 = sum of the S slots of the converted initial state and the earlier
-    // segments, staged through the (still free) tile region of LDS
+  if (spre) {
+    // S0 = the S prefix of this segment (the converted initial state and the
+    // earlier segments; decayed: each aged to this segment's start), staged
+    // through the (still free) tile region of LDS
     constexpr int nS4 = D * D / 4 / NT;
     static_assert(D * D % (4 * NT) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
+    const float4* x = reinterpret_cast<const float4*>(spre + ((size_t)bh * nseg + seg) * D * D);
     float4 sa[nS4];
 #pragma unroll
-    for (int r = 0; r < nS4; ++r) sa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sp = init ? -1 : 0; sp < seg; ++sp) {
-      const float* x = rec + ((size_t)bh * (nseg + 1) + (sp < 0 ? nseg : sp)) * F;
-      // decayed: segment sp's moments age by gamma^(L (seg - 1 - sp)) to this segment's start
-      const float f = DEC ? exp2f(lg2g * (float)(C * cps) * (float)(seg - 1 - sp)) : 1.f;
-#pragma unroll
-      for (int r = 0; r < nS4; ++r) {
-        const float4 u = reinterpret_cast<const float4*>(x)[tid + NT * r];
-        if constexpr (DEC) {
-          sa[r].x += f * u.x; sa[r].y += f * u.y; sa[r].z += f * u.z; sa[r].w += f * u.w;
-        } else {
-          sa[r].x += u.x; sa[r].y += u.y; sa[r].z += u.z; sa[r].w += u.w;
-        }
-      }
-    }
+    for (int r = 0; r < nS4; ++r) sa[r] = x[tid + NT * r];
     float* st = reinterpret_cast<float*>(lds);
 #pragma unroll
     for (int r = 0; r < nS4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = sa[r];
@@ -1059,11 +1040,11 @@ WalkK walk_kernel() {
 }
 
 hipError_t launch_walk(const WalkK& kk, dim3 grid, hipStream_t s, const uint16_t* q, const uint16_t* k,
-                       const uint16_t* v, float* out, float* den_out, float* rec, const float* init, int n, int cps,
+                       const uint16_t* v, float* out, float* den_out, float* rec, const float* spre, int n, int cps,
                        int nseg, int normalized, float eps, float lg2g) {
   hipError_t e = hipFuncSetAttribute(kk.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kk.lds);
   if (e != hipSuccess) return e;
-  void* args[] = {&q, &k, &v, &out, &den_out, &rec, &init, &n, &cps, &nseg, &normalized, &eps, &lg2g};
+  void* args[] = {&q, &k, &v, &out, &den_out, &rec, &spre, &n, &cps, &nseg, &normalized, &eps, &lg2g};
   return prof_launch(kk.fn, grid, dim3(kk.threads), args, kk.lds, s);
 }
 
@@ -1072,6 +1053,18 @@ size_t records_bytes(int BH, int P, int d, int dv) {
 }
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Workspace of the walk + carry fix-up pipeline: records [BH][P + 1][F] |
+// walk denominators [BH][n] and per-tile eta [BH][M][d] | carries
+// [BH][P][d dv + d] | S prefixes [BH][P][d d].
+size_t legacy_spre_offset(int BH, int n, int P, int C, int d, int dv) {
+  const size_t den = sizeof(float) * (((size_t)BH * n + (size_t)BH * ((n + C - 1) / C) * d + 63) & ~size_t(63));
+  const size_t carry = sizeof(float) * (size_t)BH * P * ((size_t)d * dv + d);
+  return al256(records_bytes(BH, P, d, dv) + den + carry);
+}
+size_t legacy_ws_bytes(int BH, int n, int P, int C, int d, int dv) {
+  return legacy_spre_offset(BH, n, P, C, d, dv) + sizeof(float) * (size_t)BH * P * d * d + 256;
+}
 
 // Workspace of the wave-specialised pipeline (d = dv = 128, no initial or
 // final state): records [BH][P + 1][F] | S prefixes [BH][P][d d] | Phi, eta
@@ -1121,7 +1114,7 @@ hipError_t run_ws(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     prof_start("seg_prefix", s);
-    HLA_LAUNCH(k_seg_prefix, dim3((D * D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, 0, D * D, 0, spre, P);
+    HLA_LAUNCH(k_seg_prefix, dim3((D * D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, 0, D * D, 0, spre, P, 1.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     prof_start("walk_summary", s);
@@ -1130,7 +1123,7 @@ hipError_t run_ws(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
     if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
     prof_start("seg_prefix", s);
     HLA_LAUNCH(k_seg_prefix, dim3((D * DV + D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, (int)off_G(D, DV),
-               D * DV + D, 0, carry, P);
+               D * DV + D, 0, carry, P, 1.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
@@ -1173,10 +1166,22 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
                lg2g);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  // S prefix of every segment (the walks each read one): init + the earlier
+  // segments' moments, each aged to the segment's start when decayed
+  float* spre = nullptr;
+  if (P > 1 || init) {
+    spre = reinterpret_cast<float*>(ws + legacy_spre_offset(BH, f.n, P, C, D, DV));
+    const float rhoS = DEC ? (float)std::exp2((double)lg2g * (double)C * (double)cps) : 1.f;
+    prof_start("seg_prefix", s);
+    HLA_LAUNCH(k_seg_prefix, dim3((D * D + 1023) / 1024, BH), dim3(256), 0, s, segs, state_floats(D, DV), 0, D * D,
+               init ? 1 : 0, spre, P, rhoS);
+    prof_stop(s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   prof_start(f.out ? "walk" : "walk_summary", s);
-  e = f.out ? launch_walk(walk_kernel<C, D, DV, false, RS, DEC>(), grid, s, q, k, v, f.out, den, segs, init, f.n,
+  e = f.out ? launch_walk(walk_kernel<C, D, DV, false, RS, DEC>(), grid, s, q, k, v, f.out, den, segs, spre, f.n,
                           cps, P, f.normalized, f.eps, lg2g)
-            : launch_walk(walk_kernel<C, D, DV, true, RS, DEC>(), grid, s, q, k, v, nullptr, nullptr, segs, init, f.n,
+            : launch_walk(walk_kernel<C, D, DV, true, RS, DEC>(), grid, s, q, k, v, nullptr, nullptr, segs, spre, f.n,
                           cps, P, 0, 0.f, lg2g);
   prof_stop(s);
   if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
@@ -1260,9 +1265,7 @@ size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
   if (!sh) return 0;
   int P, cps;
   fused_plan(*sh, BH, n, &P, &cps);
-  const size_t den = sizeof(float) * (((size_t)BH * n + (size_t)BH * ((n + sh->C - 1) / sh->C) * d + 63) & ~size_t(63));
-  const size_t carry = sizeof(float) * (size_t)BH * P * ((size_t)d * dv + d);
-  const size_t legacy = records_bytes(BH, P, d, dv) + den + carry + 256;
+  const size_t legacy = legacy_ws_bytes(BH, n, P, sh->C, d, dv);
   if (ws_shape(*sh)) {
     const size_t w = ws_pipeline_bytes(BH, P);
     return w > legacy ? w : legacy;

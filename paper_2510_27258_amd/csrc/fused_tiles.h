@@ -421,6 +421,25 @@ __global__ __launch_bounds__(kThreads) void k_moments(const uint16_t* __restrict
   }
 }
 
+// dst[bh][s][0 .. len): the exclusive running sums over a head's segments of
+// one part of the records rec[bh][0 .. nseg] (F floats each, from float `off`
+// on): x_0 = (use_init ? slot nseg : 0), x_{s+1} = rho x_s + slot s (rho: the
+// decay of one segment's moments over the next, 1 without decay).  Each walk
+// then reads its segment's prefix as one record.  grid (ceil(len / 1024), BH).
+__global__ __launch_bounds__(256) void k_seg_prefix(const float* __restrict__ rec, size_t F, int off, int len,
+                                                    int use_init, float* __restrict__ dst, int nseg, float rho) {
+  const int bh = blockIdx.y, p = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (p >= len) return;
+  const float* base = rec + (size_t)bh * (nseg + 1) * F + off + p;
+  float4 x = use_init ? *reinterpret_cast<const float4*>(base + (size_t)nseg * F) : make_float4(0.f, 0.f, 0.f, 0.f);
+  float* out = dst + (size_t)bh * nseg * len + p;
+  for (int s = 0; s < nseg; ++s) {
+    *reinterpret_cast<float4*>(out + (size_t)s * len) = x;
+    const float4 u = *reinterpret_cast<const float4*>(base + (size_t)s * F);
+    x.x = rho * x.x + u.x; x.y = rho * x.y + u.y; x.z = rho * x.z + u.z; x.w = rho * x.w + u.w;
+  }
+}
+
 // The carry fix-up.  The walks run every segment with Phi0 = eta0 = 0, so
 // their outputs miss q_t^T Phi_c and q_t . eta_c, where (Phi_c, eta_c) is the
 // sum of the converted initial state and the brackets of the segments before

@@ -56,24 +56,6 @@ struct CfgWS {
   static_assert(4 * C * 32 * 4 <= (oRh - oWh) * 2, "output staging fits the W | T region");
 };
 
-// dst[bh][s][0 .. len) = (use_init ? slot nseg : 0) + sum_{s' < s} slot s' of
-// the records rec[bh][0 .. nseg] (F floats each) from float `off` on: the
-// exclusive running sums over a head's segments of one part of the records
-// (the S moments, or the Phi / eta brackets).  grid (ceil(len / 1024), BH).
-__global__ __launch_bounds__(256) void k_seg_prefix(const float* __restrict__ rec, size_t F, int off, int len,
-                                                    int use_init, float* __restrict__ dst, int nseg) {
-  const int bh = blockIdx.y, p = (blockIdx.x * 256 + threadIdx.x) * 4;
-  if (p >= len) return;
-  const float* base = rec + (size_t)bh * (nseg + 1) * F + off + p;
-  float4 x = use_init ? *reinterpret_cast<const float4*>(base + (size_t)nseg * F) : make_float4(0.f, 0.f, 0.f, 0.f);
-  float* out = dst + (size_t)bh * nseg * len + p;
-  for (int s = 0; s < nseg; ++s) {
-    *reinterpret_cast<float4*>(out + (size_t)s * len) = x;
-    const float4 u = *reinterpret_cast<const float4*>(base + (size_t)s * F);
-    x.x += u.x; x.y += u.y; x.z += u.z; x.w += u.w;
-  }
-}
-
 // grid (segments walked, BH), 512 threads.  spre: [BH][nseg][D*D] S prefixes
 // (null: zero); carry: [BH][nseg][D*DV + D] Phi, eta carries (null: zero;
 // unused by SUMMARY); rec: [BH][nseg + 1][F] records (SUMMARY writes the
