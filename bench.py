@@ -65,6 +65,8 @@ def kernel_costs(w, P=None, tile=None):
             "fix": ("hbm", tok * (d * es + 8 * dv + (4 if w["normalized"] else 0)), tok * 2 * d * dv),
             # carry: the segments' Phi/eta brackets read, their running sums written
             "carry": ("hbm", BH * (2 * P + 1) * (d * dv + d) * 4, BH * P * (d * dv + d)),
+            # running sums of the per-segment records (S, or the Phi/eta brackets): read once, written once
+            "seg_prefix": ("hbm", BH * 2 * P * (d * d + d * dv + d) * 4, BH * P * (d * d + d * dv + d)),
             "init_convert": ("hbm", BH * 2 * F * 4, BH * 2 * (d * d * dv + d * d)),
             "total": ("hbm", BH * (P + 2) * F * 4, BH * 2 * (d * d * dv + d * d)),
         })
@@ -112,7 +114,7 @@ def kernel_key(name):
     if "k_walk" in name:
         return "walk_summary" if ("true" in name or "Lb1E" in name) else "walk"
     for key in ("k_init_convert", "k_total", "k_moments", "k_carry", "k_fix", "k_scan", "k_chunk_summary", "k_readout",
-                "k_step"):
+                "k_step", "k_seg_prefix"):
         if key in name:
             return key[2:]
     return None
@@ -159,7 +161,7 @@ def ingest_counters(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_c
 
 # Sources the fused forward's kernels (moments, walk, carry, fix-up) are built
 # from: the HBM counter summary is used only while these hash as recorded.
-FORWARD_SOURCES = ("fused.hip", "fused_tiles.h", "fused.h", "common.h", "profile.h")
+FORWARD_SOURCES = ("fused.hip", "fused_ws.h", "fused_tiles.h", "fused.h", "common.h", "profile.h")
 
 
 def source_sha():
