@@ -4,174 +4,286 @@
 // Sec. 5 (u = q^T S_t, num = u C_t - q^T G_t, den = u m_t - q^T h_t):
 //   w = k^T C_{t-1},  s = k^T m_{t-1}
 //   G += k w^T,  h += s k,  S += k k^T,  C += q v^T,  m += q
-// One workgroup per head.  Every state element is read once and written
-// once: all of S, C and G are loaded up front (16-byte vector loads, up to
-// 48 per thread), then three dependent reductions over rows run through LDS.
-// The state (all heads together larger than the last-level cache) is
-// streamed once per step, so its loads and stores are non-temporal.
+// Every state element is read once and written once per step.
+//
+// One workgroup per CU walks heads blockIdx.x, blockIdx.x + gridDim.x, ...
+// A head is three streaming passes over its state (S, then C, then G), each
+// a d x d or d x dv matrix held in registers, 16-byte pieces 1024/d rows
+// apart per thread; while one pass is computed, the next pass's matrix is
+// already loading into the other register buffer (C during the S pass, G
+// during the C pass, the next head's S during the G pass), so every
+// workgroup keeps one to two matrices of loads in flight.  The reductions
+// between passes go through LDS behind barriers that do not drain global
+// memory.
+//   S pass: S_t = S_{t-1} + k k^T,  u = q^T S_t
+//   C pass: w = k^T C_{t-1},  C_t = C_{t-1} + q v^T,  num = u C_t
+//   G pass: G_t = G_{t-1} + k w^T,  num -= q^T G_t (masked)
+// Launch shape and cache policy were measured on 2048 heads at d = dv = 128
+// (812 MB per step): one workgroup per CU streams at 0.85 of HBM peak, two at
+// 0.77, four at 0.80; non-temporal loads drop two per CU to 0.67.  The
+// stores are non-temporal (the state, larger than the last-level cache, is
+// not read again within the step).
 #include "common.h"
 #include "profile.h"
 
 namespace hla {
 
 constexpr int kStepThreads = 256;
-typedef float nf4 __attribute__((ext_vector_type(4)));
-// 16-byte non-temporal load and store
-__device__ __forceinline__ float4 ntld(const float4* p) {
-  const nf4 x = __builtin_nontemporal_load(reinterpret_cast<const nf4*>(p));
-  return make_float4(x[0], x[1], x[2], x[3]);
-}
-__device__ __forceinline__ void ntst(const float4& v, float4* p) {
-  __builtin_nontemporal_store(nf4{v.x, v.y, v.z, v.w}, reinterpret_cast<nf4*>(p));
-}
 constexpr int kStepMaxVec = 16;   // d*d/4/256 and d*dv/4/256 at d = dv = 128
+constexpr int kStepWGsPerCU = 1;
+constexpr int kCUs = 256;   // MI355X
 
-template <typename T>
-__global__ __launch_bounds__(kStepThreads) void k_step(float* __restrict__ state, const T* __restrict__ q,
-                                                       const T* __restrict__ k, const T* __restrict__ v,
-                                                       float* __restrict__ out, int d, int dv, int masked,
-                                                       int normalized, float eps) {
-  __shared__ float qs[128], ks[128], vs[128], us[128], ws[128], mk[128], dterm[128];
-  __shared__ float red1[1024], red2[1024];
-  const int bh = blockIdx.x, tid = threadIdx.x;
-  const size_t F = state_floats(d, dv);
+typedef __amdgpu_buffer_rsrc_t step_rsrc;
+constexpr int kStoreNT = 2;   // buffer cache policy bit: non-temporal
+
+struct StepSmall {
+  float q, k, v, m, h;
+};
+
+// One head's state as a buffer resource (offsets in bytes from the head's S).
+__device__ __forceinline__ step_rsrc step_res(float* st, size_t F) {
+  return __builtin_amdgcn_make_buffer_rsrc(st, (short)0, (int)(F * 4), 0x00020000);
+}
+
+template <typename T, int D, int DV>
+__device__ __forceinline__ void step_small(StepSmall& x, const T* q, const T* k, const T* v, const float* st,
+                                           int bh, int tid) {
+  if (tid < D) {
+    x.q = ldf(q, (size_t)bh * D + tid);
+    x.k = ldf(k, (size_t)bh * D + tid);
+    x.m = st[off_m(D, DV) + tid];
+    x.h = st[off_h(D, DV) + tid];
+  }
+  if (tid < DV) x.v = ldf(v, (size_t)bh * DV + tid);
+}
+
+// Matrix of N4 float4 at byte offset base of the head: element tid + 256 r
+// of thread tid in slot r.
+template <int N4>
+struct StepMat {
+  static constexpr int R = N4 >= kStepThreads ? N4 / kStepThreads : 1;
+  static __device__ __forceinline__ bool lane_ok(int tid) { return N4 >= kStepThreads || tid < N4; }
+};
+
+template <int N4>
+__device__ __forceinline__ void step_load(float4 (&X)[kStepMaxVec], step_rsrc res, uint32_t base, int tid) {
+  if (!StepMat<N4>::lane_ok(tid)) return;
+#pragma unroll
+  for (int r = 0; r < StepMat<N4>::R; ++r) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(res, (int)(base + tid * 16), r * kStepThreads * 16, 0);
+    X[r] = make_float4(__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]), __uint_as_float(x[3]));
+  }
+}
+
+__device__ __forceinline__ void step_store(const float4& v, step_rsrc res, uint32_t base, int tid, int r) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(
+      u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)}, res,
+      (int)(base + tid * 16), r * kStepThreads * 16, kStoreNT);
+}
+
+struct StepLds {
+  float vec[2][4][128];     // per head slot: q, k, v, k_a m_a
+  float us[128], ws[128], dterm[128];
+  float redA[1024], redB[1024];
+};
+
+// One head.  On entry X holds (or is loading) the head's S and x its small
+// vectors; on exit Y holds (or is loading) the next head's S and x its small
+// vectors.
+template <typename T, int D, int DV>
+__device__ __forceinline__ void step_head(float4 (&X)[kStepMaxVec], float4 (&Y)[kStepMaxVec], StepSmall& x,
+                                          StepLds& L, int slot, float* __restrict__ state, const T* q,
+                                          const T* k, const T* v, float* __restrict__ out, int bh, int nb,
+                                          int masked, int normalized, float eps) {
+  constexpr int nS4 = D * D / 4, nC4 = D * DV / 4;
+  constexpr size_t F = (size_t)D * D + 2 * (size_t)D * DV + 2 * D;
+  constexpr uint32_t oC = 4 * D * D, oG = 4 * (D * D + D * DV + D);
+  const int tid = threadIdx.x;
   float* st = state + (size_t)bh * F;
-  float* S = st;
-  float* C = st + off_C(d, dv);
-  float* m = st + off_m(d, dv);
-  float* G = st + off_G(d, dv);
-  float* h = st + off_h(d, dv);
-  const int nS4 = d * d / 4, nC4 = d * dv / 4;
-
-  float4 Sv[kStepMaxVec], Cv[kStepMaxVec], Gv[kStepMaxVec];
-#pragma unroll
-  for (int r = 0; r < kStepMaxVec; ++r) {
-    const int f = tid + kStepThreads * r;
-    if (f < nS4) Sv[r] = ntld(reinterpret_cast<const float4*>(S) + f);
-    if (f < nC4) {
-      Cv[r] = ntld(reinterpret_cast<const float4*>(C) + f);
-      Gv[r] = ntld(reinterpret_cast<const float4*>(G) + f);
-    }
+  const step_rsrc res = step_res(st, F);
+  // C loads go out first: the small vectors below were loaded after this
+  // head's S, so waiting for them waits for S as well
+  step_load<nC4>(Y, res, oC, tid);
+  float* qs = L.vec[slot][0];
+  float* ks = L.vec[slot][1];
+  float* vs = L.vec[slot][2];
+  float* mk = L.vec[slot][3];
+  const float m_old = x.m, h_old = x.h;
+  if (tid < D) {
+    qs[tid] = x.q;
+    ks[tid] = x.k;
+    mk[tid] = x.k * x.m;
   }
-  float m_old = 0.f, h_old = 0.f;
-  if (tid < d) {
-    qs[tid] = ldf(q, (size_t)bh * d + tid);
-    ks[tid] = ldf(k, (size_t)bh * d + tid);
-    m_old = m[tid];
-    h_old = h[tid];
-    mk[tid] = ks[tid] * m_old;
-  }
-  if (tid < dv) vs[tid] = ldf(v, (size_t)bh * dv + tid);
-  __syncthreads();
+  if (tid < DV) vs[tid] = x.v;
+  lds_barrier();
 
-  // S pass: S_t = S_{t-1} + k k^T, partial u = q^T S_t over this thread's rows
+  // S pass
   {
-    const int col = (tid * 4) % d, rg = (tid * 4) / d;
+    constexpr int rstep = kStepThreads * 4 / D;
+    const int col = (tid * 4) % D, rg = (tid * 4) / D;
     float up[4] = {0.f, 0.f, 0.f, 0.f};
+    if (StepMat<nS4>::lane_ok(tid)) {
 #pragma unroll
-    for (int r = 0; r < kStepMaxVec; ++r) {
-      const int f = tid + kStepThreads * r;
-      if (f < nS4) {
-        const int a = (f * 4) / d;
+      for (int r = 0; r < StepMat<nS4>::R; ++r) {
+        const int a = rg + r * rstep;
         const float ka = ks[a], qa = qs[a];
-        float4 s = Sv[r];
+        float4 s = X[r];
         s.x += ka * ks[col + 0];
         s.y += ka * ks[col + 1];
         s.z += ka * ks[col + 2];
         s.w += ka * ks[col + 3];
-        ntst(s, reinterpret_cast<float4*>(S) + f);
+        step_store(s, res, 0, tid, r);
         up[0] += qa * s.x; up[1] += qa * s.y; up[2] += qa * s.z; up[3] += qa * s.w;
       }
+      for (int i = 0; i < 4; ++i) L.redA[rg * D + col + i] = up[i];
     }
-    if (tid < nS4 && tid * 4 < 1024)
-      for (int i = 0; i < 4; ++i) red1[rg * d + col + i] = up[i];
   }
-  // C pass: w = k^T C_{t-1} (old values), then C_t = C_{t-1} + q v^T (kept in registers)
-  {
-    const int col = (tid * 4) % dv, rg = (tid * 4) / dv;
-    float wp[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int r = 0; r < kStepMaxVec; ++r) {
-      const int f = tid + kStepThreads * r;
-      if (f < nC4) {
-        const int a = (f * 4) / dv;
-        const float ka = ks[a], qa = qs[a];
-        float4 c = Cv[r];
-        wp[0] += ka * c.x; wp[1] += ka * c.y; wp[2] += ka * c.z; wp[3] += ka * c.w;
-        c.x += qa * vs[col + 0];
-        c.y += qa * vs[col + 1];
-        c.z += qa * vs[col + 2];
-        c.w += qa * vs[col + 3];
-        Cv[r] = c;
-        ntst(c, reinterpret_cast<float4*>(C) + f);
-      }
-    }
-    if (tid < nC4 && tid * 4 < 1024)
-      for (int i = 0; i < 4; ++i) red2[rg * dv + col + i] = wp[i];
-  }
-  __syncthreads();
-
-  // finish u, w; update m, h; denominator terms
-  if (tid < d) {
+  lds_barrier();
+  if (tid < D) {
     float u = 0.f;
-    const int ngS = min(1024, nS4 * 4) / d;
-    for (int g = 0; g < ngS; ++g) u += red1[g * d + tid];
-    us[tid] = u;
+    constexpr int ng = (kStepThreads * 4 < D * D ? kStepThreads * 4 : D * D) / D;
+    for (int g = 0; g < ng; ++g) u += L.redA[g * D + tid];
+    L.us[tid] = u;
     float s = 0.f;
-    for (int a = 0; a < d; ++a) s += mk[a];
+    for (int a = 0; a < D; ++a) s += mk[a];
     const float m_new = m_old + qs[tid];
     const float h_new = h_old + s * ks[tid];
-    m[tid] = m_new;
-    h[tid] = h_new;
-    dterm[tid] = u * m_new - (masked ? qs[tid] * h_new : 0.f);
+    st[off_m(D, DV) + tid] = m_new;
+    st[off_h(D, DV) + tid] = h_new;
+    L.dterm[tid] = u * m_new - (masked ? qs[tid] * h_new : 0.f);
   }
-  if (tid < dv) {
-    float w = 0.f;
-    const int ngC = min(1024, nC4 * 4) / dv;
-    for (int g = 0; g < ngC; ++g) w += red2[g * dv + tid];
-    ws[tid] = w;
-  }
-  __syncthreads();
+  lds_barrier();
 
-  // num = u C_t - q^T G_t, with G_t = G_{t-1} + k w^T
-  {
-    const int col = (tid * 4) % dv, rg = (tid * 4) / dv;
-    float np[4] = {0.f, 0.f, 0.f, 0.f};
+  constexpr int rstepC = kStepThreads * 4 / DV;
+  constexpr int ngC = (kStepThreads * 4 < D * DV ? kStepThreads * 4 : D * DV) / DV;
+  const int colC = (tid * 4) % DV, rgC = (tid * 4) / DV;
+  // C pass (G loading into X meanwhile)
+  step_load<nC4>(X, res, oG, tid);
+  if (StepMat<nC4>::lane_ok(tid)) {
+    float wp[4] = {0.f, 0.f, 0.f, 0.f}, np[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < kStepMaxVec; ++r) {
-      const int f = tid + kStepThreads * r;
-      if (f < nC4) {
-        const int a = (f * 4) / dv;
-        const float ka = ks[a], qa = qs[a], ua = us[a];
-        const float4 c = Cv[r];
-        float4 g = Gv[r];
-        g.x += ka * ws[col + 0];
-        g.y += ka * ws[col + 1];
-        g.z += ka * ws[col + 2];
-        g.w += ka * ws[col + 3];
-        ntst(g, reinterpret_cast<float4*>(G) + f);
-        np[0] += ua * c.x; np[1] += ua * c.y; np[2] += ua * c.z; np[3] += ua * c.w;
-        if (masked) {
-          np[0] -= qa * g.x; np[1] -= qa * g.y; np[2] -= qa * g.z; np[3] -= qa * g.w;
-        }
-      }
+    for (int r = 0; r < StepMat<nC4>::R; ++r) {
+      const int a = rgC + r * rstepC;
+      const float ka = ks[a], qa = qs[a], ua = L.us[a];
+      float4 c = Y[r];
+      wp[0] += ka * c.x; wp[1] += ka * c.y; wp[2] += ka * c.z; wp[3] += ka * c.w;
+      c.x += qa * vs[colC + 0];
+      c.y += qa * vs[colC + 1];
+      c.z += qa * vs[colC + 2];
+      c.w += qa * vs[colC + 3];
+      step_store(c, res, oC, tid, r);
+      np[0] += ua * c.x; np[1] += ua * c.y; np[2] += ua * c.z; np[3] += ua * c.w;
     }
-    __syncthreads();   // red1 was read above; reuse it
-    if (tid < nC4 && tid * 4 < 1024)
-      for (int i = 0; i < 4; ++i) red1[rg * dv + col + i] = np[i];
+    for (int i = 0; i < 4; ++i) {
+      L.redA[rgC * DV + colC + i] = wp[i];
+      L.redB[rgC * DV + colC + i] = np[i];
+    }
   }
-  __syncthreads();
-  if (tid < dv) {
-    float num = 0.f;
-    const int ngC = min(1024, nC4 * 4) / dv;
-    for (int g = 0; g < ngC; ++g) num += red1[g * dv + tid];
+  lds_barrier();
+  float num = 0.f;
+  if (tid < DV) {
+    float w = 0.f;
+    for (int g = 0; g < ngC; ++g) {
+      w += L.redA[g * DV + tid];
+      num += L.redB[g * DV + tid];
+    }
+    L.ws[tid] = w;
+  }
+  lds_barrier();
+
+  // G pass (the next head's S and small vectors loading meanwhile)
+  if (nb >= 0) {
+    float* nst = state + (size_t)nb * F;
+    step_load<nS4>(Y, step_res(nst, F), 0, tid);
+    step_small<T, D, DV>(x, q, k, v, nst, nb, tid);
+  }
+  if (StepMat<nC4>::lane_ok(tid)) {
+    float gp[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < StepMat<nC4>::R; ++r) {
+      const int a = rgC + r * rstepC;
+      const float ka = ks[a], qa = qs[a];
+      float4 g = X[r];
+      g.x += ka * L.ws[colC + 0];
+      g.y += ka * L.ws[colC + 1];
+      g.z += ka * L.ws[colC + 2];
+      g.w += ka * L.ws[colC + 3];
+      step_store(g, res, oG, tid, r);
+      gp[0] += qa * g.x; gp[1] += qa * g.y; gp[2] += qa * g.z; gp[3] += qa * g.w;
+    }
+    if (masked)
+      for (int i = 0; i < 4; ++i) L.redA[rgC * DV + colC + i] = gp[i];
+  }
+  lds_barrier();
+  if (tid < DV) {
+    if (masked)
+      for (int g = 0; g < ngC; ++g) num -= L.redA[g * DV + tid];
     if (normalized) {
       float den = 0.f;
-      for (int a = 0; a < d; ++a) den += dterm[a];
+      for (int a = 0; a < D; ++a) den += L.dterm[a];
       num = num / (den + eps);
     }
-    out[(size_t)bh * dv + tid] = num;
+    out[(size_t)bh * DV + tid] = num;
   }
+}
+
+template <typename T, int D, int DV>
+__global__ __launch_bounds__(kStepThreads) void k_step_pipe(float* __restrict__ state, const T* __restrict__ q,
+                                                            const T* __restrict__ k, const T* __restrict__ v,
+                                                            float* __restrict__ out, int BH, int masked,
+                                                            int normalized, float eps) {
+  __shared__ StepLds L;
+  constexpr size_t F = (size_t)D * D + 2 * (size_t)D * DV + 2 * D;
+  float4 A[kStepMaxVec], B[kStepMaxVec];
+  StepSmall x{0.f, 0.f, 0.f, 0.f, 0.f};
+  const int tid = threadIdx.x, G = gridDim.x;
+  int bh = blockIdx.x;
+  step_load<D * D / 4>(A, step_res(state + (size_t)bh * F, F), 0, tid);
+  step_small<T, D, DV>(x, q, k, v, state + (size_t)bh * F, bh, tid);
+  for (int slot = 0;; slot ^= 1) {
+    int nb = bh + G < BH ? bh + G : -1;
+    step_head<T, D, DV>(A, B, x, L, slot, state, q, k, v, out, bh, nb, masked, normalized, eps);
+    if (nb < 0) break;
+    bh = nb;
+    slot ^= 1;
+    nb = bh + G < BH ? bh + G : -1;
+    step_head<T, D, DV>(B, A, x, L, slot, state, q, k, v, out, bh, nb, masked, normalized, eps);
+    if (nb < 0) break;
+    bh = nb;
+  }
+}
+
+template <typename T, int D, int DV>
+hipError_t launch_step_pipe(float* state, const void* q, const void* k, const void* v, float* out, int BH,
+                            int masked, int normalized, float eps, int grid, hipStream_t s) {
+  HLA_LAUNCH((k_step_pipe<T, D, DV>), dim3(grid), dim3(kStepThreads), 0, s, state, (const T*)q, (const T*)k,
+             (const T*)v, out, BH, masked, normalized, eps);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t step_dv(int dv, float* state, const void* q, const void* k, const void* v, float* out, int BH,
+                   int masked, int normalized, float eps, int grid, hipStream_t s) {
+  switch (dv) {
+    case 16: return launch_step_pipe<T, D, 16>(state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+    case 32: return launch_step_pipe<T, D, 32>(state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+    case 64: return launch_step_pipe<T, D, 64>(state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+    case 128: return launch_step_pipe<T, D, 128>(state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+hipError_t step_d(int d, int dv, float* state, const void* q, const void* k, const void* v, float* out, int BH,
+                  int masked, int normalized, float eps, int grid, hipStream_t s) {
+  switch (d) {
+    case 16: return step_dv<T, 16>(dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+    case 32: return step_dv<T, 32>(dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+    case 64: return step_dv<T, 64>(dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+    case 128: return step_dv<T, 128>(dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 __global__ __launch_bounds__(256) void k_zero(float4* __restrict__ p, size_t n4) {
@@ -188,13 +300,9 @@ hipError_t launch_zero(float* p, size_t n4, hipStream_t s) {
 
 hipError_t launch_step(float* state, const void* q, const void* k, const void* v, float* out, int BH, int d,
                        int dv, int masked, int normalized, float eps, int dtype, hipStream_t s) {
-  if (dtype == 1)
-    HLA_LAUNCH(k_step<uint16_t>, dim3(BH), dim3(kStepThreads), 0, s, state, (const uint16_t*)q,
-                       (const uint16_t*)k, (const uint16_t*)v, out, d, dv, masked, normalized, eps);
-  else
-    HLA_LAUNCH(k_step<float>, dim3(BH), dim3(kStepThreads), 0, s, state, (const float*)q,
-                       (const float*)k, (const float*)v, out, d, dv, masked, normalized, eps);
-  return hipGetLastError();
+  const int grid = BH < kStepWGsPerCU * kCUs ? BH : kStepWGsPerCU * kCUs;
+  if (dtype == 1) return step_d<uint16_t>(d, dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
+  return step_d<float>(d, dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
 }
 
 }  // namespace hla
