@@ -15,7 +15,9 @@
 // owns (head, column block) and streams the head's segments in order; the
 // blocks also share out the rows of S and h, and block 0 carries m.  The
 // column blocks of one head are placed on the same XCD so the segment's S
-// tile, read by each of them, is served from that XCD's L2.
+// tile, read by each of them, is served from that XCD's L2.  Waves share
+// only LDS, so the barriers order LDS alone: the next segment's loads and
+// this segment's prefix stores stay in flight across them.
 #include <type_traits>
 
 #include "common.h"
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
   if (M > 0) load(0, std::integral_constant<int, 0>());
   if constexpr (PF > 1)
     if (M > 1) load(1, std::integral_constant<int, 1>());
-  __syncthreads();
+  lds_barrier();
 
   // one step: write the prefix of segment c, then consume slot sl and refill it with segment c + PF
   auto step = [&](int c, auto slot_tag) -> bool {
@@ -184,7 +186,7 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
     for (int j = 0; j < NB; ++j) gacc[j] = rho2 * gacc[j] + gv[sl][j];
     const float m_c = mv[sl];
     if (tid < r1 - r0) hacc = rho2 * hacc + hv[sl];
-    __syncthreads();
+    lds_barrier();
     if (c + PF < M) load(c + PF, slot_tag);
     // G_acc += S_c C_acc (segment A = accumulated prefix, B = segment c)
     {
@@ -220,14 +222,14 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
       if (e < nown) sacc[i] = rho * sacc[i] + Sc[(r0 + e / d) * ldS + e % d];
     }
     if (K::NBUF == 1) {
-      __syncthreads();   // everyone is done with Sc and Cacc
+      lds_barrier();   // everyone is done with Sc and Cacc
 #pragma unroll
       for (int r = 0; r < nC4; ++r) {
         const int e = tid + 256 * r;
         if (e < d * CB / 4) st4(Cacc + 4 * e, cn[r]);
       }
     }
-    __syncthreads();   // macc readers are done; NBUF == 2: the other buffers are free
+    lds_barrier();   // macc readers are done; NBUF == 2: the other buffers are free
     if (tid < d) macc[tid] = rho * macc[tid] + m_c;
     return true;
   };
@@ -247,18 +249,22 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
 // block's S_c rows, so a lane holds G_acc[row n][4 adjacent columns].  The
 // contraction index of step s for lane group g is k = (d/4) g + s.
 //   * every workgroup keeps all of C_acc, as A fragments in registers (wave
-//     w: columns 16w .. 16w+15), and its own RPB rows of C_acc once more in
-//     row-major 16-byte pieces for the output; C_c is read by each row block
-//     of the head, and the blocks of one head share an XCD so the re-reads
-//     hit its L2;
-//   * G_acc and S_acc (the block's rows, wave w's columns) stay in that
-//     accumulator layout; every wave forms h_acc (block rows) from m_acc,
-//     which sits in LDS, double-buffered by segment parity;
+//     w: columns 16w .. 16w+15), and its own RPB rows of C_acc and S_acc in
+//     row-major 16-byte pieces; C_c is read by each row block of the head,
+//     and the blocks of one head share an XCD so the re-reads hit its L2;
+//   * G_acc (the block's rows, wave w's columns) stays in the accumulator
+//     layout and is staged through LDS for the prefix stores, so that every
+//     store of the block's rows (S, C, G) is a contiguous row-major piece
+//     (the accumulator layout would write 64-byte halves of 128-byte lines);
+//   * every wave forms h_acc (block rows) from m_acc, which sits in LDS,
+//     double-buffered by segment parity;
 //   * the block's S_c rows and all of C_c go through LDS in 16-byte pieces
 //     (C with its 16-column tiles XOR-swizzled by row group, so the column
 //     reads of the four lane groups fall in different banks);
-//   * loads run PF segments ahead in NSLOT = PF + 1 register slots.  No load
-//     or store of the steady-state loop sits under a branch (lanes that own
+//   * loads run ahead in register slots, one slot per segment ahead, each
+//     slot refilled as soon as its segment is consumed: the block's own rows
+//     (S_c, G_c, h_c) and m_c PF segments ahead, C_c PFC ahead.  No load or
+//     store of the steady-state loop sits under a branch (lanes that own
 //     nothing store past the end of the record, which the buffer drops), so
 //     the compiler's wait counts stay partial and the prefetch stays deep.
 // Each block writes its rows of S, C, G, h, and block 0 writes m.
@@ -278,25 +284,41 @@ __device__ __forceinline__ f32x4_t rld4(__amdgpu_buffer_rsrc_t r, uint32_t vf, u
 __device__ __forceinline__ void rst(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf, float x) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, (int)(vf * 4), (int)(sf * 4), 2);
 }
+// The 16-byte store takes its uniform offset in the lane offset, with a zero
+// soffset: with an SGPR soffset the compiler may place a VALU write of the
+// store's data registers right after the store, and on gfx950 such a write
+// was seen to reach memory in place of the data.
 __device__ __forceinline__ void rst4(__amdgpu_buffer_rsrc_t r, uint32_t vf, uint32_t sf, f32x4_t x) {
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) uint32_t, x), r,
-                                         (int)(vf * 4), (int)(sf * 4), 2);
+                                         (int)((vf + sf) * 4), 0, 2);
 }
 
 template <int d>
 struct RbCfg {
   static constexpr int RPB = d == 128 ? 32 : 16;       // rows per workgroup
-  static constexpr int NW = d / 16, NT = 64 * NW, RT = RPB / 16, KS = d / 4, RB = d / RPB, SB = KS / RB;
+  // 16-column tiles per wave (two, at four waves of up to 512 registers,
+  // measured slower at d = 128 than one at eight waves)
+  static constexpr int CT = 1;
+  static constexpr int NW = d / 16 / CT, NT = 64 * NW, RT = RPB / 16, KS = d / 4, RB = d / RPB;
   static constexpr int ldS = d + 4;
-  static constexpr int NC4 = d / 16;                   // 16-byte pieces of C_c per thread
+  static constexpr int NSP = RPB * d / 4 / NT;         // 16-byte pieces of the block's S rows per thread
+  static constexpr int NC4 = d * d / 4 / NT;           // 16-byte pieces of C_c per thread
   static constexpr int NCO = RPB * d / 4 / NT;         // 16-byte pieces of the block's C rows per thread
   static constexpr int NM = (d + 63) / 64;             // m values per lane
   static constexpr int CBUF = d == 128 ? 1 : 2;        // C_c buffers in LDS
-  static constexpr int NSLOT = d == 128 ? 2 : 5;
-  static constexpr int PF = NSLOT - 1;
-  static constexpr size_t lds_floats = 2 * (size_t)RPB * ldS + (size_t)CBUF * d * d + 2 * d;
-  static_assert(RPB * d / 4 == NT * RT && SB * RB == KS && KS % 4 == 0 && NC4 * NT * 4 == d * d &&
-                    NCO * NT * 4 == RPB * d,
+  // segments loaded ahead, one register slot each (a slot is refilled as
+  // soon as its segment's data is consumed): the block's S, G, h rows and m
+  // (read by this workgroup only) PF ahead; C_c (read by each row block of
+  // the head, the later ones from L2) PFC ahead
+  static constexpr int PF = d == 128 ? 2 : 4;
+  static constexpr int PFC = d == 128 ? 1 : 4;
+  static constexpr int GRP = PF == PFC ? PF : PF * PFC;   // steps per unrolled group
+  // LDS: the block's S_c rows and the G_acc rows staged for row-major
+  // prefix stores (two each, by segment parity), C_c (CBUF) and m_acc (two)
+  static constexpr size_t lds_floats = 4 * (size_t)RPB * ldS + (size_t)CBUF * d * d + 2 * d;
+  static_assert(GRP <= 4 && PF <= 4 && PFC <= 4 && GRP % PF == 0 && GRP % PFC == 0, "unrolled slots");
+  static_assert(NSP * NT * 4 == RPB * d && KS % 4 == 0 && NC4 * NT * 4 == d * d && NCO * NT * 4 == RPB * d &&
+                    NW * CT * 16 == d,
                 "row-block geometry");
 };
 
@@ -307,19 +329,18 @@ __device__ __forceinline__ int cswz(int k, int j) {
 }
 
 template <int d>
-__global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restrict__ states,
-                                                             const float* __restrict__ init,
-                                                             float* __restrict__ prefix, float* __restrict__ total,
-                                                             int BH, int M, size_t in_stride, size_t pre_stride,
-                                                             size_t tot_stride, float rho_full, float rho_last) {
+__global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restrict__ states, const float* __restrict__ init, float* __restrict__ prefix,
+               float* __restrict__ total, int BH, int M, size_t in_stride, size_t pre_stride, size_t tot_stride,
+               float rho_full, float rho_last) {
   using K = RbCfg<d>;
-  constexpr int RT = K::RT, KS = K::KS, NT = K::NT, ldS = K::ldS, NSLOT = K::NSLOT, PF = K::PF, NM = K::NM,
-                NC4 = K::NC4, NCO = K::NCO;
+  constexpr int RT = K::RT, KS = K::KS, NT = K::NT, ldS = K::ldS, PF = K::PF, PFC = K::PFC, GRP = K::GRP, NM = K::NM, NC4 = K::NC4, NCO = K::NCO, NSP = K::NSP, CT = K::CT;
+  using std::integral_constant;
   constexpr size_t F = (size_t)d * d + 2 * (size_t)d * d + 2 * d;
   constexpr uint32_t oC = d * d, om = 2 * d * d, oG = 2 * d * d + d, oh = 3 * d * d + d;
   extern __shared__ float smem[];
   float* Sbuf = smem;                                  // [2][RPB][ldS]  the block's S_c rows
-  float* Cbuf = smem + 2 * K::RPB * ldS;               // [CBUF][d][d]   C_c, swizzled
+  float* Gst = Sbuf + 2 * K::RPB * ldS;                // [2][RPB][ldS]  G_acc rows for the prefix stores
+  float* Cbuf = Gst + 2 * K::RPB * ldS;                // [CBUF][d][d]   C_c, swizzled
   float* macc = Cbuf + K::CBUF * d * d;                // [2][d]         m_acc by segment parity
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, n = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -327,37 +348,48 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
   const int bh = group * 8 + within % 8;               // a head's row blocks share an XCD (and its L2)
   const int rb = within / 8;
   if (bh >= BH) return;
-  const int r0 = rb * K::RPB, c0 = 16 * w;
+  const int r0 = rb * K::RPB, cw = 16 * CT * w;        // the wave's first column
   const float* in = states + (size_t)bh * in_stride;
   float* pre = prefix + (size_t)bh * pre_stride;
 
-  // carried state: C_acc column pieces (A fragments), S_acc / G_acc [row 16t + n][c0 + 4g + i], h_acc
-  // and the block's rows of C_acc: piece j of a thread is row r0 + e / d, columns e % d .. + 3, e = 4 (tid + NT j)
-  float cacc[KS], hacc[RT];
-  f32x4_t sacc[RT], gacc[RT], cown[NCO];
+  // carried state: C_acc column pieces (A fragments; tile ct = columns cw + 16 ct ..), G_acc
+  // [row 16t + n][cw + 16 ct + 4g + i], h_acc, and the block's rows of S_acc and C_acc row-major:
+  // piece j of a thread is row r0 + e / d, columns e % d .. + 3, e = 4 (tid + NT j)
+  float cacc[CT][KS], hacc[RT];
+  f32x4_t gacc[CT][RT], sown[NCO], cown[NCO];
   if (init) {
     const auto x = rec_rsrc(init + (size_t)bh * F, (uint32_t)F);
 #pragma unroll
-    for (int s = 0; s < KS; ++s) cacc[s] = rld(x, KS * g * d + c0 + n, oC + s * d);
+    for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int j = 0; j < NCO; ++j) cown[j] = rld4(x, 4 * (tid + NT * j), oC + r0 * d);
+      for (int s = 0; s < KS; ++s) cacc[ct][s] = rld(x, KS * g * d + cw + 16 * ct + n, oC + s * d);
+#pragma unroll
+    for (int j = 0; j < NCO; ++j) {
+      cown[j] = rld4(x, 4 * (tid + NT * j), oC + r0 * d);
+      sown[j] = rld4(x, 4 * (tid + NT * j), r0 * d);
+    }
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      sacc[t] = rld4(x, (r0 + n) * d + c0 + 4 * g, 16 * t * d);
-      gacc[t] = rld4(x, (r0 + n) * d + c0 + 4 * g, oG + 16 * t * d);
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) gacc[ct][t] = rld4(x, (r0 + n) * d + cw + 16 * ct + 4 * g, oG + 16 * t * d);
       hacc[t] = rld(x, r0 + n, oh + 16 * t);
     }
     if (w == 0)
       for (int a = l; a < d; a += 64) macc[a] = rld(x, a, om);   // parity 0
   } else {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) cacc[s] = 0.f;
+    for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-    for (int j = 0; j < NCO; ++j) cown[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < KS; ++s) cacc[ct][s] = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCO; ++j) {
+      cown[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      sown[j] = cown[j];
+    }
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      sacc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      gacc[t] = sacc[t];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) gacc[ct][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       hacc[t] = 0.f;
     }
     if (w == 0)
@@ -365,38 +397,59 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
   }
 
   // segment data in register slots
-  f32x4_t sp[NSLOT][RT], cp[NSLOT][NC4], gc[NSLOT][RT];
-  float hc[NSLOT][RT], mc[NSLOT][NM];
-  auto load = [&](int c, auto slot_tag) __attribute__((always_inline)) {
+  f32x4_t sp[PF][NSP], cp[PFC][NC4], gc[PF][CT][RT];
+  float hc[PF][RT], mc[PF][NM];
+  auto load_c = [&](int c, auto slot_tag) __attribute__((always_inline)) {
     constexpr int sl = decltype(slot_tag)::value;
     const auto x = rec_rsrc(in + (size_t)min(c, M - 1) * F, (uint32_t)F);
 #pragma unroll
-    for (int j = 0; j < RT; ++j) {
+    for (int j = 0; j < NC4; ++j) cp[sl][j] = rld4(x, 4 * tid, oC + 4 * NT * j);
+  };
+  auto load_s = [&](int c, auto slot_tag) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_tag)::value;
+    const auto x = rec_rsrc(in + (size_t)min(c, M - 1) * F, (uint32_t)F);
+#pragma unroll
+    for (int j = 0; j < NSP; ++j) {
       const int e = tid + NT * j, row = e / (d / 4), c4 = (e % (d / 4)) * 4;
       sp[sl][j] = rld4(x, (r0 + row) * d + c4, 0);
     }
-#pragma unroll
-    for (int j = 0; j < NC4; ++j) cp[sl][j] = rld4(x, 4 * tid, oC + 4 * NT * j);
+  };
+  auto load_g = [&](int c, auto slot_tag) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_tag)::value;
+    const auto x = rec_rsrc(in + (size_t)min(c, M - 1) * F, (uint32_t)F);
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      gc[sl][t] = rld4(x, (r0 + n) * d + c0 + 4 * g, oG + 16 * t * d);
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) gc[sl][ct][t] = rld4(x, (r0 + n) * d + cw + 16 * ct + 4 * g, oG + 16 * t * d);
       hc[sl][t] = rld(x, r0 + n, oh + 16 * t);
     }
 #pragma unroll
     for (int j = 0; j < NM; ++j) mc[sl][j] = rld(x, min(l + 64 * j, d - 1), om);
   };
-  // the exclusive prefix held now, into record dst
-  // the exclusive prefix held now (m_acc in buffer mb), into record dst
+  // the exclusive prefix held now (m_acc in buffer mb), into record dst.  G_acc
+  // goes through LDS (Gst, buffer par) so that every store of the block's
+  // rows is a contiguous row-major piece; the caller has a barrier between
+  // gst_write and put, and the two buffers alternate by segment parity, so a
+  // buffer is rewritten only after a later barrier.
   constexpr uint32_t kDrop = 0x10000000u;   // a lane offset (floats) past any record: the store is dropped
-  auto put = [&](float* dst, const float* mb) __attribute__((always_inline)) {
+  auto gst_write = [&](int par) __attribute__((always_inline)) {
+    float* gs = Gst + par * K::RPB * ldS;
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+        *reinterpret_cast<f32x4_t*>(gs + (16 * t + n) * ldS + cw + 16 * ct + 4 * g) = gacc[ct][t];
+  };
+  auto put = [&](float* dst, const float* mb, int par) __attribute__((always_inline)) {
     const auto y = rec_rsrc(dst, (uint32_t)F);
+    const float* gs = Gst + par * K::RPB * ldS;
 #pragma unroll
-    for (int t = 0; t < RT; ++t) {
-      rst4(y, (r0 + n) * d + c0 + 4 * g, 16 * t * d, sacc[t]);
-      rst4(y, (r0 + n) * d + c0 + 4 * g, oG + 16 * t * d, gacc[t]);
+    for (int j = 0; j < NCO; ++j) {
+      const int e = 4 * (tid + NT * j);
+      rst4(y, e, r0 * d, sown[j]);
+      rst4(y, e, oC + r0 * d, cown[j]);
+      rst4(y, e, oG + r0 * d, *reinterpret_cast<const f32x4_t*>(gs + (e / d) * ldS + e % d));
     }
-#pragma unroll
-    for (int j = 0; j < NCO; ++j) rst4(y, 4 * (tid + NT * j), oC + r0 * d, cown[j]);
     const bool hown = w == 0 && g == 0, mown = w == 0 && rb == 0;
 #pragma unroll
     for (int t = 0; t < RT; ++t) rst(y, hown ? r0 + n : kDrop, oh + 16 * t, hacc[t]);
@@ -406,44 +459,54 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
       rst(y, mown && l + 64 * j < d ? a : kDrop, om, mb[a]);
     }
   };
-  // segment c from slot sl: write its prefix, then fold it in
-  auto step = [&](int c, auto slot_tag) __attribute__((always_inline)) {
-    constexpr int sl = decltype(slot_tag)::value;
-    load(c + PF, std::integral_constant<int, (sl + PF) % NSLOT>());
+  // segment c from slots sl (rows, m) and slc (C_c): write its prefix, then fold it in
+  auto step = [&](int c, auto slot_tag, auto cslot_tag) __attribute__((always_inline)) {
+    constexpr int sl = decltype(slot_tag)::value, slc = decltype(cslot_tag)::value;
     float* Sc = Sbuf + (c & 1) * K::RPB * ldS;
     float* Cc = Cbuf + (K::CBUF == 2 ? (c & 1) : 0) * d * d;
-    if (K::CBUF == 1) __syncthreads();   // the previous segment's readers of Cc are done
+    if (K::CBUF == 1) lds_barrier();   // the previous segment's readers of Cc are done
 #pragma unroll
-    for (int j = 0; j < RT; ++j) {
+    for (int j = 0; j < NSP; ++j) {
       const int e = tid + NT * j, row = e / (d / 4), c4 = (e % (d / 4)) * 4;
       *reinterpret_cast<f32x4_t*>(Sc + row * ldS + c4) = sp[sl][j];
     }
 #pragma unroll
     for (int j = 0; j < NC4; ++j) {
       const int e = 4 * (tid + NT * j), k = e / d;
-      *reinterpret_cast<f32x4_t*>(Cc + k * d + cswz<d>(k, e % d)) = cp[sl][j];
+      *reinterpret_cast<f32x4_t*>(Cc + k * d + cswz<d>(k, e % d)) = cp[slc][j];
     }
+    load_s(c + PF, slot_tag);     // the slots just emptied
+    load_c(c + PFC, cslot_tag);
     const float* mo = macc + (c & 1) * d;   // m_acc before segment c
-    put(pre + (size_t)c * F, mo);
-    __syncthreads();
+    gst_write(c & 1);
+    lds_barrier();
+    put(pre + (size_t)c * F, mo, c & 1);
     const float rho = c == M - 1 ? rho_last : rho_full, rho2 = rho * rho;
     // C_acc <- rho C_acc first: the product below uses the attenuated old C_acc
 #pragma unroll
-    for (int s = 0; s < KS; ++s) cacc[s] *= rho;
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) cacc[ct][s] *= rho;
     // G_acc^T <- rho^2 G_acc^T + G_c^T + (rho C_acc)^T S_c[rows]^T
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
-      f32x4_t acc = rho2 * gacc[t] + gc[sl][t];
+      f32x4_t acc[CT];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) acc[ct] = rho2 * gacc[ct][t] + gc[sl][ct][t];
       const float* brow = Sc + (16 * t + n) * ldS + KS * g;
 #pragma unroll
       for (int s4 = 0; s4 < KS; s4 += 4) {
         const f32x4_t b4 = *reinterpret_cast<const f32x4_t*>(brow + s4);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4], b4.x, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4 + 1], b4.y, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4 + 2], b4.z, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[s4 + 3], b4.w, acc, 0, 0, 0);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[ct][s4], b4.x, acc[ct], 0, 0, 0);
+          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[ct][s4 + 1], b4.y, acc[ct], 0, 0, 0);
+          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[ct][s4 + 2], b4.z, acc[ct], 0, 0, 0);
+          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(cacc[ct][s4 + 3], b4.w, acc[ct], 0, 0, 0);
+        }
       }
-      gacc[t] = acc;
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) gacc[ct][t] = acc[ct];
     }
     // h_acc += h_c + S_c[rows] m_acc (old m_acc), in every wave; m_acc += m_c
     // into the other parity buffer (its readers, segment c - 1, are past the barrier)
@@ -467,14 +530,20 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
       for (int j = 0; j < NM; ++j)
         if (l + 64 * j < d) mn[l + 64 * j] = rho * mo[l + 64 * j] + mc[sl][j];
     }
+    load_g(c + PF, slot_tag);
     // S_acc += S_c, C_acc += C_c
 #pragma unroll
-    for (int t = 0; t < RT; ++t) sacc[t] = rho * sacc[t] + *reinterpret_cast<const f32x4_t*>(Sc + (16 * t + n) * ldS + c0 + 4 * g);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int k = KS * g + s;
-      cacc[s] += Cc[k * d + cswz<d>(k, c0 + n)];
+    for (int j = 0; j < NCO; ++j) {
+      const int e = 4 * (tid + NT * j);
+      sown[j] = rho * sown[j] + *reinterpret_cast<const f32x4_t*>(Sc + (e / d) * ldS + e % d);
     }
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const int k = KS * g + s;
+        cacc[ct][s] += Cc[k * d + cswz<d>(k, cw + 16 * ct + n)];
+      }
 #pragma unroll
     for (int j = 0; j < NCO; ++j) {
       const int e = 4 * (tid + NT * j), k = r0 + e / d;
@@ -482,29 +551,33 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
     }
   };
   if (M > 0) {
-    load(0, std::integral_constant<int, 0>());
-    if constexpr (PF > 1) load(1, std::integral_constant<int, 1>());
-    if constexpr (PF > 2) load(2, std::integral_constant<int, 2>());
-    if constexpr (PF > 3) load(3, std::integral_constant<int, 3>());
-    static_assert(PF <= 4 && NSLOT <= 5, "unrolled slots");
+#define HLA_RB_LOAD(J) load_s(J, integral_constant<int, J>()), load_g(J, integral_constant<int, J>())
+    HLA_RB_LOAD(0);
+    if constexpr (PF > 1) HLA_RB_LOAD(1);
+    if constexpr (PF > 2) HLA_RB_LOAD(2);
+    if constexpr (PF > 3) HLA_RB_LOAD(3);
+#undef HLA_RB_LOAD
+    load_c(0, integral_constant<int, 0>());
+    if constexpr (PFC > 1) load_c(1, integral_constant<int, 1>());
+    if constexpr (PFC > 2) load_c(2, integral_constant<int, 2>());
+    if constexpr (PFC > 3) load_c(3, integral_constant<int, 3>());
+#define HLA_RB_STEP(J) step(c + J, integral_constant<int, J % PF>(), integral_constant<int, J % PFC>())
     int c = 0;
-    for (; c + NSLOT <= M; c += NSLOT) {     // whole groups: no branch around a step
-      step(c, std::integral_constant<int, 0>());
-      step(c + 1, std::integral_constant<int, 1 % NSLOT>());
-      if constexpr (NSLOT > 2) step(c + 2, std::integral_constant<int, 2 % NSLOT>());
-      if constexpr (NSLOT > 3) step(c + 3, std::integral_constant<int, 3 % NSLOT>());
-      if constexpr (NSLOT > 4) step(c + 4, std::integral_constant<int, 4 % NSLOT>());
+    for (; c + GRP <= M; c += GRP) {     // whole groups: no branch around a step
+      HLA_RB_STEP(0);
+      if constexpr (GRP > 1) HLA_RB_STEP(1);
+      if constexpr (GRP > 2) HLA_RB_STEP(2);
+      if constexpr (GRP > 3) HLA_RB_STEP(3);
     }
-    if (c < M) step(c, std::integral_constant<int, 0>());
-    if (c + 1 < M) step(c + 1, std::integral_constant<int, 1 % NSLOT>());
-    if constexpr (NSLOT > 2)
-      if (c + 2 < M) step(c + 2, std::integral_constant<int, 2 % NSLOT>());
-    if constexpr (NSLOT > 3)
-      if (c + 3 < M) step(c + 3, std::integral_constant<int, 3 % NSLOT>());
+    if (c < M) HLA_RB_STEP(0);
+    if constexpr (GRP > 1) if (c + 1 < M) HLA_RB_STEP(1);
+    if constexpr (GRP > 2) if (c + 2 < M) HLA_RB_STEP(2);
+#undef HLA_RB_STEP
   }
   if (total) {
-    __syncthreads();                          // m_acc of parity M is written by wave 0
-    put(total + (size_t)bh * tot_stride, macc + (M & 1) * d);
+    gst_write(M & 1);                       // the last put read the other buffer
+    lds_barrier();                          // and m_acc of parity M is written by wave 0
+    put(total + (size_t)bh * tot_stride, macc + (M & 1) * d, M & 1);
   }
 }
 

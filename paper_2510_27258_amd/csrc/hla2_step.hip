@@ -75,11 +75,15 @@ __device__ __forceinline__ void step_load(float4 (&X)[kStepMaxVec], step_rsrc re
   }
 }
 
+// Whole offset in the lane offset and a zero soffset: with an SGPR soffset
+// the compiler may place a VALU write of a 16-byte store's data registers
+// right after the store, and on gfx950 such a write was seen to reach memory
+// in place of the data.
 __device__ __forceinline__ void step_store(const float4& v, step_rsrc res, uint32_t base, int tid, int r) {
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   __builtin_amdgcn_raw_buffer_store_b128(
       u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)}, res,
-      (int)(base + tid * 16), r * kStepThreads * 16, kStoreNT);
+      (int)(base + tid * 16 + r * kStepThreads * 16), 0, kStoreNT);
 }
 
 struct StepLds {
