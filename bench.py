@@ -498,6 +498,7 @@ def measure_decode(steps=None):
     import numpy as np
     import torch
     import paper_2510_27258_amd as hla
+    from paper_2510_27258_amd import capi
     from paper_2510_27258_amd import inputs as I
     w = I.WORKLOADS["hla2-decode-bf16-B64H32-d128-prefix2048-steps1024"]
     B, H, d, dv, n = w["B"], w["H"], w["d"], w["dv"], w["n"]
@@ -522,8 +523,8 @@ def measure_decode(steps=None):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
-    F = d * d + 2 * d * dv + 2 * d
-    per_head = 2 * F * 4 + (2 * d + dv) * 2 + dv * 4
+    # the state is read and written once (S packed symmetric), tokens read, output written
+    per_head = 2 * capi.hla2_state_bytes(1, 1, d, dv) + (2 * d + dv) * 2 + dv * 4
     nbytes = B * H * per_head
     return {"workload": "hla2-decode-bf16-B64H32-d128-prefix2048-steps1024", "steps": steps, "ms_per_step": ms,
             "achieved": nbytes / ms / 1e6, "unit": "GB/s", "peak": HBM_PEAK_GBS,

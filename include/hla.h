@@ -180,9 +180,16 @@ int hla2_scan(const float *states, const float *init, float *prefix, float *tota
  * fixes, for the life of the state, the operator every prefill and step on
  * it applies (masked, normalized, eps) and the dtype of the tokens they take,
  * so a prefill and the steps after it cannot disagree.  The state itself is
- * caller-owned device memory holding one record of F floats per head (the
- * layout above); S, C, m, G, h point at head 0's fields and head i's field X
- * is X + i * head_floats.  `check` is written by hla2_state_init: a call
+ * caller-owned device memory holding one record of FP floats per head: the
+ * fields of the record above with S packed symmetric (Sec. 5: only its upper
+ * triangle is stored), FP = d(d+1)/2 + 2*d*dv + 2*d:
+ *   S [d(d+1)/2] | C [d][dv] | m [d] | G [d][dv] | h [d].
+ * S is stored as d/2 folded row pairs of d+1 floats: pair p holds row p of S
+ * from column p (d-p values), then row d-1-p from column d-1-p (p+1 values);
+ * element (a, j), a <= j, is at p*(d+1) + c with p = a, c = j-a when a < d/2,
+ * else p = d-1-a, c = j+1.  hla2_state_export writes the full records.
+ * S, C, m, G, h point at head 0's fields and head i's field X is
+ * X + i * head_floats.  `check` is written by hla2_state_init: a call
  * given a descriptor whose other fields changed since then returns
  * HLA_ERR_INVALID.  The descriptor is a host object; pass it by pointer.
  * ------------------------------------------------------------------------- */
@@ -191,13 +198,13 @@ typedef struct {
   int masked, normalized;     /* operator of every prefill and step          */
   int dtype;                  /* HLA_FP32 or HLA_BF16: the tokens' dtype     */
   float eps;                  /* denominator offset, used when normalized    */
-  float *data;                /* [B, H, F] fp32 device memory, caller-owned  */
-  size_t head_floats;         /* F = d*d + 2*d*dv + 2*d                      */
+  float *data;                /* [B, H, FP] fp32 device memory, caller-owned */
+  size_t head_floats;         /* FP = d*(d+1)/2 + 2*d*dv + 2*d               */
   float *S, *C, *m, *G, *h;   /* head 0's fields inside data                 */
   unsigned long long check;   /* set by hla2_state_init                      */
 } hla2_state;
 
-/* Device bytes of a state of B*H heads: B*H*F*4 (0 if invalid). */
+/* Device bytes of a state of B*H heads: B*H*FP*4 (0 if invalid). */
 size_t hla2_state_bytes(int B, int H, int d, int dv);
 
 /* Fill *st for the device buffer buf (at least hla2_state_bytes(B, H, d, dv)
@@ -227,6 +234,14 @@ int hla2_prefill(hla2_state *st, const void *q, const void *k, const void *v, in
  * fp32.  The state is updated in place.
  * ------------------------------------------------------------------------- */
 int hla2_step(hla2_state *st, const void *q_t, const void *k_t, const void *v_t, float *out_t, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * hla2_state_export — the state as full records (the paper's 5-tuple with S
+ * as a d x d matrix): full is [B, H, F] fp32 device memory, F =
+ * hla2_state_floats(d, dv), caller-owned, 16-byte aligned, not aliasing the
+ * state.  Enqueued on `stream`; the state is not changed.
+ * ------------------------------------------------------------------------- */
+int hla2_state_export(const hla2_state *st, float *full, void *stream);
 
 /* ---------------------------------------------------------------------------
  * hla2_forward_decay — second-order HLA with exponential time decay gamma

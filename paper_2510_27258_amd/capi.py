@@ -52,6 +52,7 @@ _SIGS = {
     "hla2_prefill_workspace_bytes": (_Z, [_SP, _I, _I]),
     "hla2_prefill": (_I, [_SP, _P, _P, _P, _I, _I, _P, _P, _Z, _P]),
     "hla2_step": (_I, [_SP, _P, _P, _P, _P, _P]),
+    "hla2_state_export": (_I, [_SP, _P, _P]),
     "hla_profile_begin": (_I, [_I]),
     "hla_profile_end": (_I, []),
     "hla_profile_summary": (_I, [ctypes.c_char_p, _Z]),
@@ -176,6 +177,10 @@ def hla2_prefill(st, q, k, v, n, chunk, out, ws, ws_bytes, stream):
 
 def hla2_step(st, q_t, k_t, v_t, out_t, stream):
     return _call("hla2_step", ctypes.byref(st), q_t, k_t, v_t, out_t, stream)
+
+
+def hla2_state_export(st, full, stream):
+    return _call("hla2_state_export", ctypes.byref(st), full, stream)
 
 
 def hla2_forward_decay_workspace_bytes(B, H, n, d, dv, chunk, dtype):

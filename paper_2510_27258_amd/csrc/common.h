@@ -16,6 +16,24 @@ __host__ __device__ inline size_t off_m(int d, int dv) { return (size_t)d * d + 
 __host__ __device__ inline size_t off_G(int d, int dv) { return (size_t)d * d + (size_t)d * dv + d; }
 __host__ __device__ inline size_t off_h(int d, int dv) { return (size_t)d * d + 2 * (size_t)d * dv + d; }
 
+// Record of one head of a decode state (hla2_state): the same fields with S
+// packed symmetric (Sec. 5: only the upper triangle is stored), d(d+1)/2
+// floats in d/2 folded row pairs: pair p holds row p of S from column p
+// (d - p values), then row d-1-p from column d-1-p (p + 1 values); then
+// C | m | G | h as above.  Element (a, j), a <= j, sits at p (d+1) + c with
+// p = a, c = j - a when a < d/2, else p = d-1-a, c = j + 1.
+__host__ __device__ inline size_t packed_s_floats(int d) { return (size_t)d * (d + 1) / 2; }
+__host__ __device__ inline size_t dstate_floats(int d, int dv) {
+  return packed_s_floats(d) + 2 * (size_t)d * dv + 2 * (size_t)d;
+}
+// (a, j), a <= j, of packed S element e
+__host__ __device__ inline void packed_s_index(int e, int d, int& a, int& j) {
+  const int p = e / (d + 1), c = e - p * (d + 1);
+  const bool first = c < d - p;
+  a = first ? p : d - 1 - p;
+  j = first ? p + c : c - 1;
+}
+
 // Element loads converting the storage type to fp32.  bf16 is held as its
 // 16-bit pattern; widening is exact.
 __device__ __forceinline__ float ldf(const float* p, size_t i) { return p[i]; }
@@ -66,4 +84,7 @@ hipError_t launch_step(float* state, const void* q, const void* k, const void* v
                        hipStream_t s);
 // p[0 .. n4) = 0 as float4 stores (a fill kernel, so it may be captured in a graph).
 hipError_t launch_zero(float* p, size_t n4, hipStream_t s);
+// Decode states: full records [BH][state_floats] <-> packed [BH][dstate_floats].
+hipError_t launch_state_pack(const float* full, float* packed, int BH, int d, int dv, hipStream_t s);
+hipError_t launch_state_unpack(const float* packed, float* full, int BH, int d, int dv, hipStream_t s);
 }  // namespace hla

@@ -4,23 +4,27 @@
 // Sec. 5 (u = q^T S_t, num = u C_t - q^T G_t, den = u m_t - q^T h_t):
 //   w = k^T C_{t-1},  s = k^T m_{t-1}
 //   G += k w^T,  h += s k,  S += k k^T,  C += q v^T,  m += q
-// Every state element is read once and written once per step.
+// Every state element is read once and written once per step.  The state is
+// the paper's 5-tuple with S packed symmetric (Sec. 5: its upper triangle,
+// d(d+1)/2 floats in folded row pairs; layout in common.h), which cuts a
+// head's bytes from 2 (d^2 + 2 d dv + 2d) 4 to 2 (d(d+1)/2 + 2 d dv + 2d) 4.
 //
 // One workgroup per CU walks heads blockIdx.x, blockIdx.x + gridDim.x, ...
 // A head is three streaming passes over its state (S, then C, then G), each
-// a d x d or d x dv matrix held in registers, 16-byte pieces 1024/d rows
-// apart per thread; while one pass is computed, the next pass's matrix is
-// already loading into the other register buffer (C during the S pass, G
-// during the C pass, the next head's S during the G pass), so every
-// workgroup keeps one to two matrices of loads in flight.  The reductions
-// between passes go through LDS behind barriers that do not drain global
-// memory.
-//   S pass: S_t = S_{t-1} + k k^T,  u = q^T S_t
+// held in registers (16-byte pieces, 1024/d rows apart per thread for C and
+// G); while one pass is computed, the next pass's matrix is already loading
+// into the other register buffer (C during the S pass, G during the C pass,
+// the next head's S during the G pass), so every workgroup keeps one to two
+// matrices of loads in flight.  The reductions between passes go through
+// LDS behind barriers that do not drain global memory.
+//   S pass: S_t = S_{t-1} + k k^T on the triangle, mirrored into LDS in
+//           full; u = q^T S_t from the LDS copy (a fixed summation order)
 //   C pass: w = k^T C_{t-1},  C_t = C_{t-1} + q v^T,  num = u C_t
 //   G pass: G_t = G_{t-1} + k w^T,  num -= q^T G_t (masked)
 // Launch shape and cache policy were measured on 2048 heads at d = dv = 128
-// (812 MB per step): one workgroup per CU streams at 0.85 of HBM peak, two at
-// 0.77, four at 0.80; non-temporal loads drop two per CU to 0.67.  The
+// with the full S (812 MB per step): one workgroup per CU streamed at 0.85 of
+// HBM peak, two at 0.77, four at 0.80; non-temporal loads dropped two per CU
+// to 0.67.  The
 // stores are non-temporal (the state, larger than the last-level cache, is
 // not read again within the step).
 #include "common.h"
@@ -45,14 +49,23 @@ __device__ __forceinline__ step_rsrc step_res(float* st, size_t F) {
   return __builtin_amdgcn_make_buffer_rsrc(st, (short)0, (int)(F * 4), 0x00020000);
 }
 
+// Offsets (floats) of the packed decode record's fields.
+template <int D, int DV>
+struct StepRec {
+  static constexpr size_t nS = (size_t)D * (D + 1) / 2;
+  static constexpr size_t oC = nS, om = nS + (size_t)D * DV, oG = om + D, oh = oG + (size_t)D * DV;
+  static constexpr size_t F = oh + D;
+  static_assert(nS % 4 == 0, "C, m, G, h stay 16-byte aligned");
+};
+
 template <typename T, int D, int DV>
 __device__ __forceinline__ void step_small(StepSmall& x, const T* q, const T* k, const T* v, const float* st,
                                            int bh, int tid) {
   if (tid < D) {
     x.q = ldf(q, (size_t)bh * D + tid);
     x.k = ldf(k, (size_t)bh * D + tid);
-    x.m = st[off_m(D, DV) + tid];
-    x.h = st[off_h(D, DV) + tid];
+    x.m = st[StepRec<D, DV>::om + tid];
+    x.h = st[StepRec<D, DV>::oh + tid];
   }
   if (tid < DV) x.v = ldf(v, (size_t)bh * DV + tid);
 }
@@ -79,6 +92,18 @@ __device__ __forceinline__ void step_load(float4 (&X)[kStepMaxVec], step_rsrc re
 // the compiler may place a VALU write of a 16-byte store's data registers
 // right after the store, and on gfx950 such a write was seen to reach memory
 // in place of the data.
+// The packed S of a head: element tid + 256 r in slot r, the last slot partial.
+template <int N4>
+__device__ __forceinline__ void step_load_s(float4 (&X)[kStepMaxVec], step_rsrc res, int tid) {
+  static_assert((N4 + kStepThreads - 1) / kStepThreads <= kStepMaxVec, "packed S fits the slots");
+#pragma unroll
+  for (int r = 0; r < (N4 + kStepThreads - 1) / kStepThreads; ++r)
+    if (tid + kStepThreads * r < N4) {
+      const auto x = __builtin_amdgcn_raw_buffer_load_b128(res, (int)((tid + kStepThreads * r) * 16), 0, 0);
+      X[r] = make_float4(__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]), __uint_as_float(x[3]));
+    }
+}
+
 __device__ __forceinline__ void step_store(const float4& v, step_rsrc res, uint32_t base, int tid, int r) {
   typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
   __builtin_amdgcn_raw_buffer_store_b128(
@@ -90,19 +115,22 @@ struct StepLds {
   float vec[2][4][128];     // per head slot: q, k, v, k_a m_a
   float us[128], ws[128], dterm[128];
   float redA[1024], redB[1024];
+  float Sm[128 * 129];      // S_t in full (row stride d + 1), mirrored from the packed triangle
 };
 
-// One head.  On entry X holds (or is loading) the head's S and x its small
-// vectors; on exit Y holds (or is loading) the next head's S and x its small
-// vectors.
+// One head.  On entry X holds (or is loading) the head's packed S and x its
+// small vectors; on exit Y holds (or is loading) the next head's S and x its
+// small vectors.  The head's C goes to Y, then its G to X once the S pass has
+// read X, and the next head's S to Y once the C pass has read Y.
 template <typename T, int D, int DV>
 __device__ __forceinline__ void step_head(float4 (&X)[kStepMaxVec], float4 (&Y)[kStepMaxVec], StepSmall& x,
                                           StepLds& L, int slot, float* __restrict__ state, const T* q,
                                           const T* k, const T* v, float* __restrict__ out, int bh, int nb,
                                           int masked, int normalized, float eps) {
-  constexpr int nS4 = D * D / 4, nC4 = D * DV / 4;
-  constexpr size_t F = (size_t)D * D + 2 * (size_t)D * DV + 2 * D;
-  constexpr uint32_t oC = 4 * D * D, oG = 4 * (D * D + D * DV + D);
+  using Rec = StepRec<D, DV>;
+  constexpr int nSp4 = (int)(Rec::nS / 4), nC4 = D * DV / 4;
+  constexpr size_t F = Rec::F;
+  constexpr uint32_t oC = 4 * Rec::oC, oG = 4 * Rec::oG;
   const int tid = threadIdx.x;
   float* st = state + (size_t)bh * F;
   const step_rsrc res = step_res(st, F);
@@ -122,39 +150,48 @@ __device__ __forceinline__ void step_head(float4 (&X)[kStepMaxVec], float4 (&Y)[
   if (tid < DV) vs[tid] = x.v;
   lds_barrier();
 
-  // S pass
+  // S pass: S_t = S_{t-1} + k k^T on the stored triangle, each updated value
+  // mirrored into the full matrix in LDS; then u = q^T S_t by columns
   {
-    constexpr int rstep = kStepThreads * 4 / D;
-    const int col = (tid * 4) % D, rg = (tid * 4) / D;
-    float up[4] = {0.f, 0.f, 0.f, 0.f};
-    if (StepMat<nS4>::lane_ok(tid)) {
+    constexpr int RS = (nSp4 + kStepThreads - 1) / kStepThreads;
 #pragma unroll
-      for (int r = 0; r < StepMat<nS4>::R; ++r) {
-        const int a = rg + r * rstep;
-        const float ka = ks[a], qa = qs[a];
-        float4 s = X[r];
-        s.x += ka * ks[col + 0];
-        s.y += ka * ks[col + 1];
-        s.z += ka * ks[col + 2];
-        s.w += ka * ks[col + 3];
-        step_store(s, res, 0, tid, r);
-        up[0] += qa * s.x; up[1] += qa * s.y; up[2] += qa * s.z; up[3] += qa * s.w;
+    for (int r = 0; r < RS; ++r) {
+      const int f = tid + kStepThreads * r;
+      if (f < nSp4) {
+        float x4[4] = {X[r].x, X[r].y, X[r].z, X[r].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          int a, j;
+          packed_s_index(4 * f + i, D, a, j);
+          x4[i] += ks[a] * ks[j];
+          L.Sm[a * (D + 1) + j] = x4[i];
+          L.Sm[j * (D + 1) + a] = x4[i];
+        }
+        step_store(make_float4(x4[0], x4[1], x4[2], x4[3]), res, 0, tid, r);
       }
-      for (int i = 0; i < 4; ++i) L.redA[rg * D + col + i] = up[i];
     }
+  }
+  step_load<nC4>(X, res, oG, tid);   // X is free: this head's G
+  lds_barrier();
+  {
+    constexpr int NG = kStepThreads / D, RPG = D / NG;   // row groups, rows per group
+    const int j = tid % D, g = tid / D;
+    float up = 0.f;
+#pragma unroll 8
+    for (int a = g * RPG; a < (g + 1) * RPG; ++a) up += qs[a] * L.Sm[a * (D + 1) + j];
+    L.redA[g * D + j] = up;
   }
   lds_barrier();
   if (tid < D) {
     float u = 0.f;
-    constexpr int ng = (kStepThreads * 4 < D * D ? kStepThreads * 4 : D * D) / D;
-    for (int g = 0; g < ng; ++g) u += L.redA[g * D + tid];
+    for (int g = 0; g < kStepThreads / D; ++g) u += L.redA[g * D + tid];
     L.us[tid] = u;
     float s = 0.f;
     for (int a = 0; a < D; ++a) s += mk[a];
     const float m_new = m_old + qs[tid];
     const float h_new = h_old + s * ks[tid];
-    st[off_m(D, DV) + tid] = m_new;
-    st[off_h(D, DV) + tid] = h_new;
+    st[Rec::om + tid] = m_new;
+    st[Rec::oh + tid] = h_new;
     L.dterm[tid] = u * m_new - (masked ? qs[tid] * h_new : 0.f);
   }
   lds_barrier();
@@ -162,8 +199,7 @@ __device__ __forceinline__ void step_head(float4 (&X)[kStepMaxVec], float4 (&Y)[
   constexpr int rstepC = kStepThreads * 4 / DV;
   constexpr int ngC = (kStepThreads * 4 < D * DV ? kStepThreads * 4 : D * DV) / DV;
   const int colC = (tid * 4) % DV, rgC = (tid * 4) / DV;
-  // C pass (G loading into X meanwhile)
-  step_load<nC4>(X, res, oG, tid);
+  // C pass
   if (StepMat<nC4>::lane_ok(tid)) {
     float wp[4] = {0.f, 0.f, 0.f, 0.f}, np[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -184,6 +220,11 @@ __device__ __forceinline__ void step_head(float4 (&X)[kStepMaxVec], float4 (&Y)[
       L.redB[rgC * DV + colC + i] = np[i];
     }
   }
+  if (nb >= 0) {                 // Y is free: the next head's S and small vectors
+    float* nst = state + (size_t)nb * F;
+    step_load_s<nSp4>(Y, step_res(nst, F), tid);
+    step_small<T, D, DV>(x, q, k, v, nst, nb, tid);
+  }
   lds_barrier();
   float num = 0.f;
   if (tid < DV) {
@@ -196,12 +237,7 @@ __device__ __forceinline__ void step_head(float4 (&X)[kStepMaxVec], float4 (&Y)[
   }
   lds_barrier();
 
-  // G pass (the next head's S and small vectors loading meanwhile)
-  if (nb >= 0) {
-    float* nst = state + (size_t)nb * F;
-    step_load<nS4>(Y, step_res(nst, F), 0, tid);
-    step_small<T, D, DV>(x, q, k, v, nst, nb, tid);
-  }
+  // G pass
   if (StepMat<nC4>::lane_ok(tid)) {
     float gp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -238,12 +274,12 @@ __global__ __launch_bounds__(kStepThreads) void k_step_pipe(float* __restrict__ 
                                                             float* __restrict__ out, int BH, int masked,
                                                             int normalized, float eps) {
   __shared__ StepLds L;
-  constexpr size_t F = (size_t)D * D + 2 * (size_t)D * DV + 2 * D;
+  constexpr size_t F = StepRec<D, DV>::F;
   float4 A[kStepMaxVec], B[kStepMaxVec];
   StepSmall x{0.f, 0.f, 0.f, 0.f, 0.f};
   const int tid = threadIdx.x, G = gridDim.x;
   int bh = blockIdx.x;
-  step_load<D * D / 4>(A, step_res(state + (size_t)bh * F, F), 0, tid);
+  step_load_s<(int)(StepRec<D, DV>::nS / 4)>(A, step_res(state + (size_t)bh * F, F), tid);
   step_small<T, D, DV>(x, q, k, v, state + (size_t)bh * F, bh, tid);
   for (int slot = 0;; slot ^= 1) {
     int nb = bh + G < BH ? bh + G : -1;
@@ -288,6 +324,48 @@ hipError_t step_d(int d, int dv, float* state, const void* q, const void* k, con
     case 128: return step_dv<T, 128>(dv, state, q, k, v, out, BH, masked, normalized, eps, grid, s);
   }
   return hipErrorInvalidValue;
+}
+
+// Full decode records [BH][state_floats] <-> packed [BH][dstate_floats]
+// (S's upper triangle in folded row pairs, then C | m | G | h).  grid
+// (blocks, BH); S is symmetric, so packing takes the upper triangle and
+// unpacking writes both (a, j) and (j, a).
+template <bool PACK>
+__global__ __launch_bounds__(256) void k_state_pack(const float* __restrict__ src, float* __restrict__ dst, int d,
+                                                    int dv) {
+  const int bh = blockIdx.y;
+  const size_t F = state_floats(d, dv), FP = dstate_floats(d, dv), nS = packed_s_floats(d);
+  const float* in = src + (size_t)bh * (PACK ? F : FP);
+  float* out = dst + (size_t)bh * (PACK ? FP : F);
+  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < FP; e += (size_t)gridDim.x * 256) {
+    if (e < nS) {
+      int a, j;
+      packed_s_index((int)e, d, a, j);
+      if (PACK) {
+        out[e] = in[(size_t)a * d + j];
+      } else {
+        const float x = in[e];
+        out[(size_t)a * d + j] = x;
+        out[(size_t)j * d + a] = x;
+      }
+    } else {
+      const size_t r = e - nS, dd = (size_t)d * d;
+      if (PACK) out[e] = in[dd + r];
+      else out[dd + r] = in[e];
+    }
+  }
+}
+
+hipError_t launch_state_pack(const float* full, float* packed, int BH, int d, int dv, hipStream_t s) {
+  const size_t blocks = (dstate_floats(d, dv) + 255) / 256;
+  HLA_LAUNCH(k_state_pack<true>, dim3((unsigned)(blocks < 64 ? blocks : 64), BH), dim3(256), 0, s, full, packed, d, dv);
+  return hipGetLastError();
+}
+
+hipError_t launch_state_unpack(const float* packed, float* full, int BH, int d, int dv, hipStream_t s) {
+  const size_t blocks = (dstate_floats(d, dv) + 255) / 256;
+  HLA_LAUNCH(k_state_pack<false>, dim3((unsigned)(blocks < 64 ? blocks : 64), BH), dim3(256), 0, s, packed, full, d, dv);
+  return hipGetLastError();
 }
 
 __global__ __launch_bounds__(256) void k_zero(float4* __restrict__ p, size_t n4) {

@@ -381,7 +381,7 @@ static int check_state(const hla2_state* st) {
 
 size_t hla2_state_bytes(int B, int H, int d, int dv) {
   if (check_dims(B, H, 1, d, dv, 0, HLA_FP32, false) != HLA_OK) return 0;
-  return sizeof(float) * (size_t)B * H * hla::state_floats(d, dv);
+  return sizeof(float) * (size_t)B * H * hla::dstate_floats(d, dv);
 }
 
 int hla2_state_init(hla2_state* st, void* buf, size_t buf_bytes, int B, int H, int d, int dv, int masked,
@@ -397,12 +397,12 @@ int hla2_state_init(hla2_state* st, void* buf, size_t buf_bytes, int B, int H, i
   s.B = B; s.H = H; s.d = d; s.dv = dv;
   s.masked = masked; s.normalized = normalized; s.dtype = dtype; s.eps = eps;
   s.data = static_cast<float*>(buf);
-  s.head_floats = hla::state_floats(d, dv);
+  s.head_floats = hla::dstate_floats(d, dv);
   s.S = s.data;
-  s.C = s.data + hla::off_C(d, dv);
-  s.m = s.data + hla::off_m(d, dv);
-  s.G = s.data + hla::off_G(d, dv);
-  s.h = s.data + hla::off_h(d, dv);
+  s.C = s.S + hla::packed_s_floats(d);
+  s.m = s.C + (size_t)d * dv;
+  s.G = s.m + d;
+  s.h = s.G + (size_t)d * dv;
   s.check = state_check(&s);
   const hipError_t e = hla::launch_zero(s.data, need / 16, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "state zeroing");
@@ -413,7 +413,7 @@ int hla2_state_init(hla2_state* st, void* buf, size_t buf_bytes, int B, int H, i
 static size_t prefill_ws(int BH, int n, int d, int dv, int chunk) {
   const size_t a = chunked_ws(BH, n, d, dv, chunk);
   const size_t b = align256(hla::fused_workspace_bytes(BH, n, d, dv, chunk));
-  return (a > b ? a : b) + align256(sizeof(float) * (size_t)BH * hla::state_floats(d, dv));
+  return (a > b ? a : b) + 2 * align256(sizeof(float) * (size_t)BH * hla::state_floats(d, dv));
 }
 
 size_t hla2_prefill_workspace_bytes(const hla2_state* st, int n, int chunk) {
@@ -445,27 +445,41 @@ int hla2_prefill(hla2_state* st, const void* q, const void* k, const void* v, in
   char* base = static_cast<char*>(workspace);
   float* states = reinterpret_cast<float*>(base);
   float* prefix = reinterpret_cast<float*>(base + cws / 2);
-  float* total = reinterpret_cast<float*>(base + (cws > fws ? cws : fws));
+  char* tail = base + (cws > fws ? cws : fws);
+  float* total = reinterpret_cast<float*>(tail);
+  float* init = reinterpret_cast<float*>(tail + align256(sizeof(float) * (size_t)BH * hla::state_floats(d, dv)));
+  // the state's packed records to full ones, the forward from them, the new
+  // total packed back into the state
+  hipError_t e = hla::launch_state_unpack(state, init, BH, d, dv, s);
+  if (e != hipSuccess) return hip_fail(e, "state unpack");
   if (hla::fused_supported(n, d, dv, chunk, dtype, out ? masked : 1)) {
     hla::Fwd f{q, k, v, out, BH, n, d, dv, chunk, masked, normalized, dtype, eps};
-    hipError_t e = hla::launch_fused(f, state, total, workspace, s);
+    e = hla::launch_fused(f, init, total, workspace, s);
     if (e != hipSuccess) return hip_fail(e, "fused prefill");
-    e = hipMemcpyAsync(state, total, sizeof(float) * (size_t)BH * hla::state_floats(d, dv), hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) return hip_fail(e, "state copy");
-    return ok();
+  } else {
+    const int cc = path_chunk(chunk), Mc = (n + cc - 1) / cc;
+    e = hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, cc, dtype, s);
+    if (e != hipSuccess) return hip_fail(e, "chunk summaries");
+    e = hla::launch_scan(states, init, prefix, total, BH, Mc, d, dv, s);
+    if (e != hipSuccess) return hip_fail(e, "scan");
+    if (out) {
+      hla::Fwd f{q, k, v, out, BH, n, d, dv, cc, masked, normalized, dtype, eps};
+      e = hla::launch_readout(f, prefix, s);
+      if (e != hipSuccess) return hip_fail(e, "readout");
+    }
   }
-  const int cc = path_chunk(chunk), Mc = (n + cc - 1) / cc;
-  hipError_t e = hla::launch_chunk_summaries(q, k, v, states, BH, n, d, dv, cc, dtype, s);
-  if (e != hipSuccess) return hip_fail(e, "chunk summaries");
-  e = hla::launch_scan(states, state, prefix, total, BH, Mc, d, dv, s);
-  if (e != hipSuccess) return hip_fail(e, "scan");
-  if (out) {
-    hla::Fwd f{q, k, v, out, BH, n, d, dv, cc, masked, normalized, dtype, eps};
-    e = hla::launch_readout(f, prefix, s);
-    if (e != hipSuccess) return hip_fail(e, "readout");
-  }
-  e = hipMemcpyAsync(state, total, sizeof(float) * (size_t)BH * hla::state_floats(d, dv), hipMemcpyDeviceToDevice, s);
-  if (e != hipSuccess) return hip_fail(e, "state copy");
+  e = hla::launch_state_pack(total, state, BH, d, dv, s);
+  if (e != hipSuccess) return hip_fail(e, "state pack");
+  return ok();
+}
+
+int hla2_state_export(const hla2_state* st, float* full, void* stream) {
+  int rc;
+  if ((rc = check_state(st)) != HLA_OK) return rc;
+  if ((rc = check_ptr(full, "full")) != HLA_OK) return rc;
+  const hipError_t e = hla::launch_state_unpack(st->data, full, st->B * st->H, st->d, st->dv,
+                                                reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "state export");
   return ok();
 }
 

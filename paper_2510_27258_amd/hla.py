@@ -88,9 +88,10 @@ def split_state(state, d, dv):
 
 class State:
     """A decode state (the hla2_state descriptor of the C ABI): per-head
-    records `data` [B, H, F] fp32 in device memory, zeroed at creation (the
-    identity segment), and the operator (masked, normalized, eps) and token
-    dtype that every prefill and step on it uses."""
+    records `data` [B, H, FP] fp32 in device memory (S packed symmetric, see
+    include/hla.h), zeroed at creation (the identity segment), and the
+    operator (masked, normalized, eps) and token dtype that every prefill and
+    step on it uses.  `export()` returns the full records [B, H, F]."""
 
     def __init__(self, B, H, d, dv, masked=True, normalized=False, eps=1e-6, dtype=torch.bfloat16,
                  device="cuda"):
@@ -100,10 +101,17 @@ class State:
             raise capi.HLAError(capi.HLA_ERR_INVALID, capi.hla_last_error())
         self.B, self.H, self.d, self.dv = B, H, d, dv
         self.dtype = dtype
-        self.data = torch.empty(B, H, state_floats(d, dv), dtype=torch.float32, device=device)
+        self.data = torch.empty(B, H, nbytes // (4 * B * H), dtype=torch.float32, device=device)
         self.desc = capi.HLA2State()
         capi.hla2_state_init(self.desc, self.data.data_ptr(), nbytes, B, H, d, dv, int(masked), int(normalized),
                              float(eps), code, _stream())
+
+    def export(self):
+        """The state as full records [B, H, F] (S as a d x d matrix), made by hla2_state_export."""
+        full = torch.empty(self.B, self.H, state_floats(self.d, self.dv), dtype=torch.float32,
+                           device=self.data.device)
+        capi.hla2_state_export(self.desc, full.data_ptr(), _stream())
+        return full
 
     def _tokens(self, q, k, v, rank):
         _qkv(q, k, v, rank)

@@ -136,6 +136,8 @@ def test_other_entry_points_reject_bad_arguments():
     assert "hla2_state_init" in capi.hla_last_error()
     assert L.hla2_prefill(ctypes.byref(forged), P, P, P, 64, 64, None, None, 0, None) == INVALID
     assert L.hla2_prefill_workspace_bytes(ctypes.byref(forged), 64, 64) == 0
+    assert L.hla2_state_export(ctypes.byref(forged), P, None) == INVALID
+    assert L.hla2_state_export(None, P, None) == INVALID
     # chunk summaries: empty input
     assert L.hla2_chunk_summaries(P, P, P, P, 1, 1, 0, 64, 64, 64, BF16, None) == INVALID
 
@@ -155,7 +157,9 @@ def test_state_queries_and_init_checks():
     """hla2_state_bytes follows the size rules; hla2_state_init rejects bad
     arguments before it enqueues anything (its zeroing launch needs a GPU)."""
     L = capi.lib()
-    assert capi.hla2_state_bytes(2, 3, 64, 32) == 4 * 6 * capi.hla2_state_floats(64, 32)
+    # S packed symmetric: d(d+1)/2 floats, then C, m, G, h
+    assert capi.hla2_state_bytes(2, 3, 64, 32) == 4 * 6 * (64 * 65 // 2 + 2 * 64 * 32 + 2 * 64)
+    assert capi.hla2_state_bytes(64, 32, 128, 128) == 4 * 2048 * (128 * 129 // 2 + 2 * 128 * 128 + 2 * 128)
     assert capi.hla2_state_bytes(1, 1, 24, 64) == 0 and "d and dv" in capi.hla_last_error()
     assert capi.hla2_state_bytes(0, 1, 64, 64) == 0
     st = capi.HLA2State()

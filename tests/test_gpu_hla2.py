@@ -302,7 +302,7 @@ def test_scan_square_states(d, with_init):
 
 # ----------------------------------------------------------------- prefill and decode
 def _state_to_np(state, d, dv):
-    return tuple(x.cpu().numpy().astype(np.float64) for x in hla.split_state(state.data, d, dv))
+    return tuple(x.cpu().numpy().astype(np.float64) for x in hla.split_state(state.export(), d, dv))
 
 
 def _tdtype(code):
@@ -434,6 +434,43 @@ def test_deterministic():
         a = hla.forward(qd, kd, vd, 64, algo=algo)
         b = hla.forward(qd, kd, vd, 64, algo=algo)
         assert torch.equal(a, b)
+
+
+def _packed_s_from_full(S):
+    """The decode state's packed S as include/hla.h describes it, from a full
+    [..., d, d] S: for p < d/2, row p from column p, then row d-1-p from
+    column d-1-p."""
+    d = S.shape[-1]
+    parts = []
+    for p in range(d // 2):
+        parts += [S[..., p, p:], S[..., d - 1 - p, d - 1 - p:]]
+    return np.concatenate(parts, axis=-1)
+
+
+@pytest.mark.parametrize("d,dv", [(16, 32), (64, 64), (128, 128)])
+def test_state_packed_layout(d, dv):
+    """The state buffer holds S's upper triangle in the documented folded
+    order (d(d+1)/2 floats), then C, m, G, h; hla2_state_export gives the full
+    records with S symmetric, equal to the oracle's state after the same
+    tokens (prefill, then steps)."""
+    B, H, n = 1, 3, 40
+    q, k, v, code = gen(B, H, n + 2, d, dv, "unit", 43 + d)
+    _say(f"case packed state layout d={d} dv={dv}")
+    st = hla.State(B, H, d, dv, dtype=torch.bfloat16)
+    hla.prefill(st, dev(q[:, :, :n], code), dev(k[:, :, :n], code), dev(v[:, :, :n], code), 32, want_out=False)
+    for t in (n, n + 1):
+        hla.step(st, dev(q[:, :, t], code), dev(k[:, :, t], code), dev(v[:, :, t], code))
+    full = st.export().cpu().numpy()
+    raw = st.data.cpu().numpy()
+    nS = d * (d + 1) // 2
+    assert raw.shape[-1] == nS + 2 * d * dv + 2 * d
+    S = full[..., :d * d].reshape(B, H, d, d)
+    assert np.array_equal(S, np.swapaxes(S, -1, -2))
+    assert np.array_equal(raw[..., :nS], _packed_s_from_full(S))
+    assert np.array_equal(raw[..., nS:], full[..., d * d:])
+    _, _, fin_ref = _oracle(q, k, v, True)
+    for g, e in zip(_state_to_np(st, d, dv), fin_ref):
+        assert np.abs(g - e).max() / max(np.abs(e).max(), 1.0) <= 2e-3
 
 
 def test_state_descriptor_fixes_the_operator():
