@@ -26,9 +26,12 @@
 //   3. k_carry / k_fix: running sums of the brackets are the E and n carries
 //      of the segments; out_t += q_t^T E_c, den_t += q_t . (n0 + n_c).
 //
-// Layout: wave w owns output tile (row tile w / NCT, column tile ct = w % NCT)
-// and keeps column ct of P0 and E0 (all d rows) in MFMA accumulators; the two
-// row waves of a column both keep it, so no partial sums are exchanged.
+// Layout: wave w owns column tile ct = w % NCT of the output for RPW row
+// tiles (from row tile (w / NCT) RPW), and keeps column ct of P0 and E0 (all
+// d rows) in MFMA accumulators.  At d = 64 (RPW = 1) the two row waves of a
+// column both keep it, so no partial sums are exchanged; at d = 128 (RPW = 2)
+// four waves, one per SIMD, each keep one column (the state once, with up to
+// 512 registers a wave: two row waves per column spilled 152 bytes a lane).
 // Numerics as in the second-order walk: q, k, v exact in bf16; every computed
 // operand (A, R, P0, E0) split into bf16 hi + lo, fp32 accumulation.
 #include <cstdlib>
@@ -43,7 +46,7 @@ namespace {
 template <int D>
 struct CfgAH {
   static constexpr int C = 64, DV = D;
-  static constexpr int NCT = D / 32, NW = 2 * NCT, NT = 64 * NW;
+  static constexpr int NCT = D / 32, RPW = D == 128 ? 2 : 1, NW = 2 * NCT / RPW, NT = 64 * NW;
   static constexpr int ST = D / 32, KC = C / 16, KD = D / 16;
   static constexpr int ldQ = D + kPad, ldK = D + kPad, ldV = DV + kPad, ldW = C + kPad, ldR = C + kPad;
   static constexpr int oQ = 0;
@@ -55,7 +58,7 @@ struct CfgAH {
   static constexpr int oRl = oRh + DV * ldR;
   static constexpr int n16 = oRl + DV * ldR;
   static constexpr int oX = oQ;                // output staging, over Q | V once both are dead
-  static_assert(NW * 1024 * 2 <= oK - oQ, "output staging fits Q | V");
+  static_assert(NW * RPW * 1024 * 2 <= oK - oQ, "output staging fits Q | V");
   static_assert(D * DV * 2 <= n16, "carry staging fits the tile region");
   static constexpr int f_m = 0, f_n = D, f_rs = 2 * D, f_s = 2 * D + 2 * C;
   static constexpr int nf32 = f_s + C;
@@ -69,13 +72,14 @@ struct CfgAH {
 };
 
 template <int D>
-__global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_walk(
+__global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks))
+__attribute__((amdgpu_waves_per_eu(CfgAH<D>::RPW == 2 ? 1 : 2))) void k_ahla_walk(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, const float* __restrict__ ppre,
     int n, int cps, int nseg, int normalized) {
   using G = CfgAH<D>;
   constexpr bool kO = D == 128;     // per-tile opaque lane index (registers)
-  constexpr int C = G::C, DV = G::DV, NT = G::NT, ST = G::ST;
+  constexpr int C = G::C, DV = G::DV, NT = G::NT, ST = G::ST, RPW = G::RPW;
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* Qs = lds + G::oQ;
   uint16_t* Vs = lds + G::oV;
@@ -95,7 +99,7 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
   seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int rt = w / G::NCT, ct = w % G::NCT;
+  const int rtb = (w / G::NCT) * RPW, ct = w % G::NCT;   // row tiles rtb .. rtb + RPW - 1
   const int M = (n + C - 1) / C;
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t F = state_floats(D, DV);
@@ -231,29 +235,40 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
     }
 
     // ---- stage 2: R = Q P0 + A V and the O partial Q E0 (old carries); P0 += K^T V ----
-    f32x16 racc = zero16(), oacc = zero16();
+    f32x16 racc[RPW], oacc[RPW];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      racc[r] = zero16();
+      oacc[r] = zero16();
+    }
 #pragma unroll
     for (int j = 0; j < G::KD; ++j) {
       bf16x8 ph, pl, eh, el;
       frag_from_acc(P0[j >> 1], j & 1, ph, pl);
       frag_from_acc(E0[j >> 1], j & 1, eh, el);
-      const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, rt * 32, j * 16, ln);
-      racc = mfma(aQ, ph, racc);
-      racc = mfma(aQ, pl, racc);
-      oacc = mfma(aQ, eh, oacc);
-      oacc = mfma(aQ, el, oacc);
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        const bf16x8 aQ = frag_acc_order<kO>(Qs, G::ldQ, (rtb + r) * 32, j * 16, ln);
+        racc[r] = mfma(aQ, ph, racc[r]);
+        racc[r] = mfma(aQ, pl, racc[r]);
+        oacc[r] = mfma(aQ, eh, oacc[r]);
+        oacc[r] = mfma(aQ, el, oacc[r]);
+      }
     }
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
       const bf16x8 bV = frag_tr<kO>(Vs, G::ldV, ct * 32, s * 16, ln);
-      if (s < 2 * (rt + 1)) {           // keys past the row tile: A is zero
-        racc = mfma(frag<kO>(Wh, G::ldW, rt * 32, s * 16, ln), bV, racc);
-        racc = mfma(frag<kO>(Wl, G::ldW, rt * 32, s * 16, ln), bV, racc);
-      }
+#pragma unroll
+      for (int r = 0; r < RPW; ++r)
+        if (s < 2 * (rtb + r + 1)) {    // keys past the row tile: A is zero
+          racc[r] = mfma(frag<kO>(Wh, G::ldW, (rtb + r) * 32, s * 16, ln), bV, racc[r]);
+          racc[r] = mfma(frag<kO>(Wl, G::ldW, (rtb + r) * 32, s * 16, ln), bV, racc[r]);
+        }
 #pragma unroll
       for (int i = 0; i < ST; ++i) P0[i] = mfma(frag_tr<kO>(Ks, G::ldK, i * 32, s * 16, ln), bV, P0[i]);
     }
-    store_T<kO>(racc, Rh, Rl, G::ldR, rt * 32, ct * 32, ln);     // R^T
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) store_T<kO>(racc[r], Rh, Rl, G::ldR, (rtb + r) * 32, ct * 32, ln);   // R^T
     lds_barrier();                      // R^T and s visible; Q and V are dead
 
     // ---- normalised: den partial (A s)_t, the tile's n0, then m0 and n0 advance ----
@@ -300,33 +315,38 @@ __global__ __launch_bounds__((CfgAH<D>::NT), (CfgAH<D>::kBlocks)) void k_ahla_wa
         E0[i] = mfma(aK, brh, E0[i]);
         E0[i] = mfma(aK, brl, E0[i]);
       }
-      if (s < 2 * (rt + 1)) {
-        const bf16x8 awh = frag<kO>(Wh, G::ldW, rt * 32, s * 16, ln);
-        const bf16x8 awl = frag<kO>(Wl, G::ldW, rt * 32, s * 16, ln);
-        oacc = mfma(awh, brh, oacc);
-        oacc = mfma(awh, brl, oacc);
-        oacc = mfma(awl, brh, oacc);
-      }
+#pragma unroll
+      for (int r = 0; r < RPW; ++r)
+        if (s < 2 * (rtb + r + 1)) {
+          const bf16x8 awh = frag<kO>(Wh, G::ldW, (rtb + r) * 32, s * 16, ln);
+          const bf16x8 awl = frag<kO>(Wl, G::ldW, (rtb + r) * 32, s * 16, ln);
+          oacc[r] = mfma(awh, brh, oacc[r]);
+          oacc[r] = mfma(awh, brl, oacc[r]);
+          oacc[r] = mfma(awl, brh, oacc[r]);
+        }
     }
-    // the output tile goes through this wave's staging slot so that each lane
+    // the output tiles go through this wave's staging slots so that each lane
     // stores 16 bytes; rows past n fall outside the buffer and are dropped
-    float* ob = XO + w * 1024;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) ob[acc_row(e, lg) * 32 + lr] = oacc[e];
+    for (int r = 0; r < RPW; ++r) {
+      float* ob = XO + (w * RPW + r) * 1024;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int p = l + 64 * j, row = p >> 3, c4 = (p & 7) * 4;
-      buf_store16(ro, (((uint32_t)t0 + rt * 32 + row) * DV + ct * 32 + c4) * 4,
-                  *reinterpret_cast<const float4*>(ob + row * 32 + c4));
+      for (int e = 0; e < 16; ++e) ob[acc_row(e, lg) * 32 + lr] = oacc[r][e];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int p = l + 64 * j, row = p >> 3, c4 = (p & 7) * 4;
+        buf_store16(ro, (((uint32_t)t0 + (rtb + r) * 32 + row) * DV + ct * 32 + c4) * 4,
+                    *reinterpret_cast<const float4*>(ob + row * 32 + c4));
+      }
     }
     lds_barrier();   // every LDS tile is rewritten by the next chunk
   }
 
-  // the segment's bracket: E0 into the G slot (row tile 0's waves; the other
-  // row waves hold the same columns), n0 into the h slot
+  // the segment's bracket: E0 into the G slot (the waves of row tile 0; any
+  // other row waves hold the same columns), n0 into the h slot
   int col = ct * 32 + lr;
   asm volatile("" : "+v"(col));
-  if (rt == 0) {
+  if (rtb == 0) {
 #pragma unroll
     for (int i = 0; i < ST; ++i)
 #pragma unroll
