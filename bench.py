@@ -27,13 +27,15 @@ SUB_WORKLOAD = "hla2-masked-bf16-B4H16-n4096-d64-C64"
 FLUSH_BYTES = 512 << 20          # written between cold iterations: twice the 256 MB last-level cache
 
 
-def kernel_costs(w, P=None, tile=None):
+def kernel_costs(w, P=None, tile=None, first=None, per=None, two_pass=False):
     """Algorithmic cost of one launch of each kernel of the forward path:
     {name: (bound, bytes, flops)}.  bytes = HBM bytes the kernel must move
     (inputs read once, outputs written once); flops = useful arithmetic of
     the kernel's formulation (a dense C x C product counts C^2 per output
-    element; triangles are not halved).  P = segments per head and tile = the
-    token tile of the fused path's plan (from the library)."""
+    element; triangles are not halved).  P = segments per head, tile = the
+    token tile, first / per = the tiles of segment 0 / of each later segment
+    of the fused path's plan (from the library); two_pass: the plan that walks
+    segment 0 beside the summary walks and then the other segments' output."""
     B, H, n, d, dv, C = w["B"], w["H"], w["n"], w["d"], w["dv"], w["chunk"]
     BH = B * H
     M = -(-n // C)
@@ -50,7 +52,7 @@ def kernel_costs(w, P=None, tile=None):
     }
     if P:
         Ct = tile
-        cps = -(-(-(-n // Ct)) // P)
+        cps = per or -(-(-(-n // Ct)) // P)
         sum_tok = BH * min(n, (P - 1) * cps * Ct)
         costs.update({
             # fused path: the output walk reads q/k/v once and writes out once
@@ -70,6 +72,22 @@ def kernel_costs(w, P=None, tile=None):
             "init_convert": ("hbm", BH * 2 * F * 4, BH * 2 * (d * d * dv + d * d)),
             "total": ("hbm", BH * (P + 2) * F * 4, BH * 2 * (d * d * dv + d * d)),
         })
+        if two_pass and P > 1:
+            # launch 1: segment 0's output walk and the summary walks of
+            # segments 1 .. P-2 (which also form C = Q^T V); launch 2: the
+            # output walks of segments 1 .. P-1
+            seg0 = BH * min(n, first * Ct)
+            summ = BH * min(n, (first + (P - 2) * cps) * Ct) - seg0
+            out_tok = tok - seg0
+            ref = reference_flops_per_token(Ct, d, dv)
+            costs.update({
+                "walk": ("hbm", out_tok * (qkv_tok + 4 * dv), out_tok * ref),
+                "walk_first": ("hbm", seg0 * (qkv_tok + 4 * dv) + summ * qkv_tok + BH * (P - 1) * F * 4,
+                               seg0 * ref + summ * 2 * (2 * Ct * d + 2 * d * d + 2 * d * dv)),
+                # the brackets: S prefix, C, m and (Phi, eta) read, (Phi, eta) written
+                "bracket": ("hbm", BH * (P - 2) * (d * d + d * dv + d + 2 * (d * dv + d)) * 4,
+                            BH * (P - 2) * 2 * (d * d * dv + d * d)),
+            })
     return costs
 
 
@@ -111,6 +129,10 @@ def kernel_key(name):
         return "ahla_walk"
     if "k_la<" in name or "k_laI" in name:
         return "bwd_pass"
+    if "k_walk_ws_first" in name:
+        return "walk_first"
+    if "k_ws_bracket" in name:
+        return "bracket"
     if "k_walk" in name:
         return "walk_summary" if ("true" in name or "Lb1E" in name) else "walk"
     for key in ("k_init_convert", "k_total", "k_moments", "k_carry", "k_fix", "k_scan", "k_chunk_summary", "k_readout",
@@ -580,10 +602,10 @@ def measure_forward(name, steps, warmup, algo_name="auto", cold_iters=0):
     prof = capi.hla_profile_summary()
     capi.hla_profile_end()
     used_algo = "fused" if "walk" in prof else "chunked"
-    P = tile = None
+    P = tile = first = per = None
     if used_algo == "fused":
-        P, tile = capi.hla2_fused_plan(B, H, n, d, dv, C)
-    costs = kernel_costs(w, P, tile)
+        P, tile, first, per = capi.hla2_fused_plan(B, H, n, d, dv, C, tiles=True)
+    costs = kernel_costs(w, P, tile, first, per, two_pass="walk_first" in prof)
     dom = max(prof, key=lambda kname: prof[kname][1])
     cnt, tot_ms = prof[dom]
     avg_s = tot_ms / cnt / 1e3
@@ -597,7 +619,7 @@ def measure_forward(name, steps, warmup, algo_name="auto", cold_iters=0):
             "mfma_tflops": nflops / avg_s / 1e12, "mfma_frac": nflops / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS}
     if dom == "walk" and tile != C:
         # the same launch counted densely at the workload's chunk instead of the tile it walks
-        f_chunk = tokens * reference_flops_per_token(C, d, dv)
+        f_chunk = nflops * reference_flops_per_token(C, d, dv) / reference_flops_per_token(tile, d, dv)
         roof["mfma_frac_at_chunk"] = f_chunk / avg_s / 1e12 / BF16_MFMA_PEAK_TFLOPS
     rec = {
         "value": tokens / (ms / 1e3),
@@ -606,7 +628,8 @@ def measure_forward(name, steps, warmup, algo_name="auto", cold_iters=0):
         "dtype": "bf16" if used_algo == "fused" else "f32",
         "config": {"workload": name, "B": B, "H": H, "n": n, "d": d, "dv": dv, "chunk": C,
                    "masked": w["masked"], "normalized": w["normalized"], "input_dtype": "bf16" if code else "fp32",
-                   "algo": used_algo, "segments_per_head": P, "tile": tile, "global_batch": B * H, "seq_len": n,
+                   "algo": used_algo, "segments_per_head": P, "tile": tile, "segment_tiles": [first, per],
+                   "global_batch": B * H, "seq_len": n,
                    "parallelism": "none"},
         "roofline": roof,
         "kernels_ms": {kname: v_[1] / v_[0] for kname, v_ in prof.items()},

@@ -121,12 +121,16 @@ int hla2_forward_ex(const void *q, const void *k, const void *v, float *out, flo
  * be NULL (HLA_ERR_INVALID). */
 int hla2_workspace_query(int B, int H, int n, int d, int dv, int chunk, int dtype, int algo, size_t *bytes);
 
-/* The segment plan of the fused path for these arguments: *segments gets the
- * number of segments each head is cut into (walked in parallel, composed by
- * Eq. semidirect) and *tile the token tile the walk advances by.  Returns
- * HLA_ERR_UNSUPPORTED when the fused path does not cover the shape (bf16
- * inputs, masked).  Reads HLA_FUSED_SEGMENTS like the forward. */
-int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int *segments, int *tile);
+/* The segment plan of the fused path for these arguments, as the forward
+ * without initial or final state uses it: *segments gets the number of
+ * segments each head is cut into (walked in parallel, composed by
+ * Eq. semidirect), *tile the token tile the walk advances by, and, unless the
+ * pointers are NULL, *first_tiles the tiles of segment 0 and
+ * *tiles_per_segment those of every later segment (the last holds the rest).
+ * Returns HLA_ERR_UNSUPPORTED when the fused path does not cover the shape
+ * (bf16 inputs, masked).  Reads HLA_FUSED_SEGMENTS like the forward. */
+int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int *segments, int *tile, int *first_tiles,
+                    int *tiles_per_segment);
 
 /* 1 if hla2_forward_ex would accept `algo` for these arguments, else 0.
  * HLA_ALGO_FUSED covers bf16 inputs, masked = 1, n * max(d, dv) * 4 < 2^31

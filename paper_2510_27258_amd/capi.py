@@ -44,7 +44,7 @@ _SIGS = {
     "hla2_forward_ex": (_I, [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P, _Z, _I, _P]),
     "hla2_workspace_query": (_I, [_I] * 8 + [_ZP]),
     "hla2_forward_noalloc": (_I, [_P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P]),
-    "hla2_fused_plan": (_I, [_I] * 6 + [_IP, _IP]),
+    "hla2_fused_plan": (_I, [_I] * 6 + [_IP, _IP, _IP, _IP]),
     "hla2_state_bytes": (_Z, [_I] * 4),
     "hla2_state_init": (_I, [_SP, _P, _Z] + [_I] * 6 + [_F, _I, _P]),
     "hla2_chunk_summaries": (_I, [_P, _P, _P, _P] + [_I] * 7 + [_P]),
@@ -143,10 +143,15 @@ def hla2_workspace_query(B, H, n, d, dv, chunk, dtype, algo):
     return nb.value
 
 
-def hla2_fused_plan(B, H, n, d, dv, chunk):
-    """(segments per head, token tile) of the fused path's plan; raises HLAError if it does not cover the shape."""
-    P, tile = _I(0), _I(0)
-    _call("hla2_fused_plan", B, H, n, d, dv, chunk, ctypes.byref(P), ctypes.byref(tile))
+def hla2_fused_plan(B, H, n, d, dv, chunk, tiles=False):
+    """(segments per head, token tile) of the fused path's plan, and with
+    tiles=True also (tiles of segment 0, tiles of each later segment);
+    raises HLAError if it does not cover the shape."""
+    P, tile, first, per = _I(0), _I(0), _I(0), _I(0)
+    _call("hla2_fused_plan", B, H, n, d, dv, chunk, ctypes.byref(P), ctypes.byref(tile), ctypes.byref(first),
+          ctypes.byref(per))
+    if tiles:
+        return P.value, tile.value, first.value, per.value
     return P.value, tile.value
 
 

@@ -1066,9 +1066,9 @@ size_t legacy_ws_bytes(int BH, int n, int P, int C, int d, int dv) {
   return legacy_spre_offset(BH, n, P, C, d, dv) + sizeof(float) * (size_t)BH * P * d * d + 256;
 }
 
-// Workspace of the wave-specialised pipeline (d = dv = 128, no initial or
-// final state): records [BH][P + 1][F] | S prefixes [BH][P][d d] | Phi, eta
-// carries [BH][P][d dv + d].
+// Workspace of the two-pass pipeline (d = dv = 128, no initial or final
+// state): records [BH][P + 1][F] | S prefixes [BH][P][d d] | Phi, eta carries
+// [BH][P][d dv + d].
 size_t ws_pipeline_bytes(int BH, int P) {
   constexpr int D = CfgWS::D, DV = CfgWS::DV;
   return records_bytes(BH, P, D, DV) + al256(sizeof(float) * (size_t)BH * P * D * D) +
@@ -1080,25 +1080,61 @@ bool legacy_pipeline() {
   return e && e[0] == '1';
 }
 
-hipError_t launch_ws(bool summary, dim3 grid, hipStream_t s, const uint16_t* q, const uint16_t* k,
-                     const uint16_t* v, float* out, float* den_out, const float* spre, const float* carry,
-                     float* rec, int n, int cps, int nseg, int normalized, float eps) {
-  const void* fn = summary ? (const void*)k_walk_ws<true> : (const void*)k_walk_ws<false>;
+// Per-tile time of the summary walk over that of the output walk (both at
+// one workgroup per CU, d = dv = 128: about 3.9 and 6.6 us per tile).
+constexpr double kWsSummaryRatio = 0.6;
+
+// Segments of the two-pass plan: with Q = 256 / BH walks per head in each
+// launch (one workgroup per CU), segments 1 .. P-1 get x tiles each (the
+// last the rest) and segment 0 about r x, r the ratio above, so that segment
+// 0's output walk and the summary walks beside it end together.  With fewer
+// than two later segments the plan is a single output walk per head.
+void ws_plan(int BH, int n, int* P, int* cps, int* c0) {
+  const int M = (n + CfgWS::C - 1) / CfgWS::C;
+  int Q = 256 / BH;
+  if (const char* e = getenv("HLA_FUSED_SEGMENTS")) Q = atoi(e) - 1;
+  double r = kWsSummaryRatio;
+  if (const char* e = getenv("HLA_WS_RATIO")) r = atof(e);
+  if (Q >= 2 && M >= 3 && r > 0.0) {
+    int x = (int)ceil(M / (Q + r));
+    const int l0 = std::max(1, (int)lround(r * x));
+    if (l0 < M) {
+      const int rest = M - l0;
+      if ((rest + x - 1) / x > Q) x = (rest + Q - 1) / Q;
+      const int p1 = (rest + x - 1) / x;
+      if (p1 >= 2) {
+        *P = 1 + p1;
+        *cps = x;
+        *c0 = l0;
+        return;
+      }
+    }
+  }
+  *P = 1;
+  *cps = M;
+  *c0 = M;
+}
+
+hipError_t launch_ws(const void* fn, dim3 grid, hipStream_t s, void** args) {
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)CfgWS::bytes);
   if (e != hipSuccess) return e;
-  void* args[] = {&q, &k, &v, &out, &den_out, &spre, &carry, &rec, &n, &cps, &nseg, &normalized, &eps};
   return prof_launch(fn, grid, dim3(CfgWS::NT), args, CfgWS::bytes, s);
 }
 
 // The forward at d = dv = 128 (64-token tiles) without states, every output
-// row written once:
-//   1. k_moments: S of segments 0 .. P-2;  k_seg_prefix: S prefixes;
-//   2. k_walk_ws<SUMMARY> over segments 0 .. P-2: each segment's bracket
-//      (Phi, eta) from its true S prefix;  k_seg_prefix: Phi, eta carries;
-//   3. k_walk_ws over every segment from its true carry: final outputs.
-hipError_t run_ws(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
-  constexpr int C = CfgWS::C, D = CfgWS::D, DV = CfgWS::DV;
+// row written once (plan in ws_plan):
+//   1. k_walk_ws_first: segment 0's output walk, and the summary walks of
+//      segments 1 .. P-2 from a zero state (S, C, m, Phi, eta records);
+//   2. k_seg_prefix: the S prefixes;  k_ws_bracket: each record's bracket
+//      (Phi_s + S_{<s} C_s, eta_s + S_{<s} m_s) in place;  k_seg_prefix: the
+//      running sums of the brackets, the Phi, eta carries;
+//   3. k_walk_ws_out over segments 1 .. P-1 from their true carries.
+// With P = 1, step 3 alone over whole heads.
+hipError_t run_ws(const Fwd& f, char* ws, hipStream_t s) {
+  constexpr int D = CfgWS::D, DV = CfgWS::DV;
   const int BH = f.BH;
+  int P, cps, c0;
+  ws_plan(BH, f.n, &P, &cps, &c0);
   const size_t F = state_floats(D, DV);
   float* segs = reinterpret_cast<float*>(ws);
   float* spre = reinterpret_cast<float*>(ws + records_bytes(BH, P, D, DV));
@@ -1106,30 +1142,40 @@ hipError_t run_ws(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
   const uint16_t* q = static_cast<const uint16_t*>(f.q);
   const uint16_t* k = static_cast<const uint16_t*>(f.k);
   const uint16_t* v = static_cast<const uint16_t*>(f.v);
+  float* out = f.out;
+  float* den = f.normalized ? f.den_out : nullptr;
+  int n = f.n, normalized = f.normalized;
+  float eps = f.eps;
   hipError_t e;
   if (P > 1) {
-    prof_start("moments", s);
-    HLA_LAUNCH((k_moments<C, D, DV, false, false, false>), dim3(P - 1, BH), dim3(kThreads), 0, s, q, k, v, segs, f.n,
-               cps, P, 0, 0.f);
+    prof_start("walk_first", s);
+    void* a1[] = {&q, &k, &v, &out, &den, &segs, &n, &c0, &cps, &P, &normalized, &eps};
+    e = launch_ws((const void*)k_walk_ws_first, dim3(P - 1, BH), s, a1);
     prof_stop(s);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
+    // (no walk writes record P - 1: the sums that include it are never stored)
     prof_start("seg_prefix", s);
     HLA_LAUNCH(k_seg_prefix, dim3((D * D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, 0, D * D, 0, spre, P, 1.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    prof_start("walk_summary", s);
-    e = launch_ws(true, dim3(P - 1, BH), s, q, k, v, nullptr, nullptr, spre, nullptr, segs, f.n, cps, P, 0, 0.f);
-    prof_stop(s);
-    if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
+    if (P > 2) {
+      prof_start("bracket", s);
+      HLA_LAUNCH((k_ws_bracket<D, DV>), dim3(P - 2, BH), dim3(1024), 0, s, segs, spre, P);
+      prof_stop(s);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     prof_start("seg_prefix", s);
     HLA_LAUNCH(k_seg_prefix, dim3((D * DV + D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, (int)off_G(D, DV),
                D * DV + D, 0, carry, P, 1.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  const float* sp = P > 1 ? spre : nullptr;
+  const float* cp = P > 1 ? carry : nullptr;
+  int seg0 = P > 1 ? 1 : 0;
   prof_start("walk", s);
-  e = launch_ws(false, dim3(P, BH), s, q, k, v, f.out, f.normalized ? f.den_out : nullptr, P > 1 ? spre : nullptr,
-                P > 1 ? carry : nullptr, segs, f.n, cps, P, f.normalized, f.eps);
+  void* a2[] = {&q, &k, &v, &out, &den, &sp, &cp, &n, &c0, &cps, &P, &seg0, &normalized, &eps};
+  e = launch_ws((const void*)k_walk_ws_out, dim3(P > 1 ? P - 1 : 1, BH), s, a2);
   prof_stop(s);
   if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
   return hipSuccess;
@@ -1240,12 +1286,19 @@ void fused_plan(const Shape& sh, int BH, int n, int* P, int* cps) {
 
 }  // namespace
 
-bool fused_plan_query(int BH, int n, int d, int dv, int chunk, int* P, int* tile) {
+bool fused_plan_query(int BH, int n, int d, int dv, int chunk, int* P, int* tile, int* first, int* per) {
   const Shape* sh = find_shape(chunk, d, dv);
   if (!sh) return false;
-  int cps;
-  fused_plan(*sh, BH, n, P, &cps);
+  int cps, c0;
+  if (ws_shape(*sh) && !legacy_pipeline()) {
+    ws_plan(BH, n, P, &cps, &c0);   // the plan of the forward without states
+  } else {
+    fused_plan(*sh, BH, n, P, &cps);
+    c0 = cps;
+  }
   *tile = sh->C;
+  if (first) *first = c0;
+  if (per) *per = cps;
   return true;
 }
 
@@ -1267,7 +1320,9 @@ size_t fused_workspace_bytes(int BH, int n, int d, int dv, int chunk) {
   fused_plan(*sh, BH, n, &P, &cps);
   const size_t legacy = legacy_ws_bytes(BH, n, P, sh->C, d, dv);
   if (ws_shape(*sh)) {
-    const size_t w = ws_pipeline_bytes(BH, P);
+    int Pw, cw, c0;
+    ws_plan(BH, n, &Pw, &cw, &c0);
+    const size_t w = ws_pipeline_bytes(BH, Pw);
     return w > legacy ? w : legacy;
   }
   return legacy;
@@ -1279,8 +1334,7 @@ hipError_t launch_fused(const Fwd& f, const float* init, float* final_state, voi
   int P, cps;
   fused_plan(*sh, f.BH, f.n, &P, &cps);
   char* ws = static_cast<char*>(workspace);
-  if (f.gamma == 1.f && !init && !final_state && ws_shape(*sh) && !legacy_pipeline())
-    return run_ws(f, ws, P, cps, s);
+  if (f.gamma == 1.f && !init && !final_state && ws_shape(*sh) && !legacy_pipeline()) return run_ws(f, ws, s);
   if (f.gamma != 1.f) {           // decayed: row-split shapes only, no states
     if (!row_split_shape(*sh) || init || final_state) return hipErrorNotSupported;
     if (sh->D == 64) return run_shape<64, 64, 64, true, true>(f, init, final_state, ws, P, cps, s);

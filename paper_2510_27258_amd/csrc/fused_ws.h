@@ -21,11 +21,18 @@
 // computed operand is split into bf16 hi + lo, q/k/v are exact, fp32
 // accumulation.
 //
-// The walk starts from the true carry of its segment: S0 = S prefix, and
-// (output walk) Phi0, eta0 = the running sums of the earlier segments'
-// brackets, so every output row is final when written (division included).
-// The SUMMARY form starts from Phi0 = eta0 = 0, skips T and O, and writes its
-// ending (Phi0, eta0), the segment's bracket, into its record.
+// Two-pass plan (no initial or final state).  Segment 0 holds c0 tiles and
+// every later segment cps tiles (the last the rest); the first launch runs,
+// side by side, the output walk of segment 0 (its carry is zero) and the
+// summary walks of segments 1 .. P-2 from a zero state, the latter also
+// forming C = Q^T V and m = Q^T 1 of their tiles; the S prefixes, the
+// brackets (Eq. semidirect in the Phi form: the bracket of segment s is
+// Phi_s + S_{<s} C_s, k_ws_bracket) and their running sums turn these
+// records into the true carries; the second launch runs the output
+// walks of segments 1 .. P-1 from their carries, so every output row is
+// final when written (division included).  Segment 0 is shorter than the
+// others by about the ratio of the two walks' per-tile times, so that both
+// launches fill every CU for the same time.
 #pragma once
 #include "fused_tiles.h"
 
@@ -56,19 +63,28 @@ struct CfgWS {
   static_assert(4 * C * 32 * 4 <= (oRh - oWh) * 2, "output staging fits the W | T region");
 };
 
-// grid (segments walked, BH), 512 threads.  spre: [BH][nseg][D*D] S prefixes
-// (null: zero); carry: [BH][nseg][D*DV + D] Phi, eta carries (null: zero;
-// unused by SUMMARY); rec: [BH][nseg + 1][F] records (SUMMARY writes the
-// bracket into the G and h slots of its segment).
+// Tile range of segment seg: segment 0 holds tiles [0, c0), segment s >= 1
+// tiles [c0 + (s - 1) cps, c0 + s cps), cut at M.
+__device__ __forceinline__ void ws_range(int seg, int c0, int cps, int M, int& c_begin, int& nt) {
+  c_begin = seg == 0 ? 0 : c0 + (seg - 1) * cps;
+  nt = min(M, seg == 0 ? c0 : c_begin + cps) - c_begin;
+}
+
+// One segment's walk over tiles [c_begin, c_begin + nt) of head bh.
+// s_in: S0 at the start (D x D, row-major; null: zero); c_in: Phi0 (D x DV)
+// then eta0 (D) at the start (null: zero; unused by SUMMARY); rec: this
+// segment's record (null: none), which receives the ending S0, Phi0 and eta0
+// in its S, G and h slots, and with SUMMARY also the segment's C = Q^T V and
+// m = Q^T 1 in its C and m slots.
 template <bool SUMMARY>
-__global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws(
+__device__ __forceinline__ void walk_ws(uint16_t* lds,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-    float* __restrict__ out, float* __restrict__ den_out, const float* __restrict__ spre,
-    const float* __restrict__ carry, float* __restrict__ rec, int n, int cps, int nseg, int normalized,
+    float* __restrict__ out, float* __restrict__ den_out, const float* __restrict__ s_in,
+    const float* __restrict__ c_in, float* __restrict__ rec, int bh, int n, int c_begin, int nt, int normalized,
     float eps) {
   using G = CfgWS;
   constexpr int C = G::C, D = G::D, DV = G::DV, NT = G::NT;
-  extern __shared__ __align__(16) uint16_t lds[];
+  static_assert(D == DV, "S0 and Phi0 share the column-tile layout");
   uint16_t* Ks = lds + G::oK;
   uint16_t* Vs = lds + G::oV;
   uint16_t* Wh = lds + G::oWh;
@@ -84,21 +100,15 @@ __global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws(
   float* qeta = fl + G::f_qeta;    // [C]: q_t . eta0
   float* inv = fl + G::f_inv;      // [C]: 1 / (den_t + eps)
 
-  int seg, bh;
-  seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool keyside = w < 4;        // waves 0-3: S0 and R; waves 4-7: Phi0, T and O
   const int cw = w & 3;              // this wave's state column tile
-  const int M = (n + C - 1) / C;
-  const int c_begin = seg * cps, nt = min(M, c_begin + cps) - c_begin;
-  const size_t F = state_floats(D, DV);
 
   // ---- carry in: column tile cw of S0 (key side) or Phi0 (value side), all rows ----
   f32x16 st[4];      // rows 32i .. 32i + 31
   {
-    const float* src = keyside ? (spre ? spre + ((size_t)bh * nseg + seg) * D * D : nullptr)
-                               : ((!SUMMARY && carry) ? carry + ((size_t)bh * nseg + seg) * (D * DV + D) : nullptr);
+    const float* src = keyside ? s_in : (SUMMARY ? nullptr : c_in);
     if (src) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -109,8 +119,16 @@ __global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws(
       for (int i = 0; i < 4; ++i) st[i] = zero16();
     }
   }
+  f32x16 cacc[4];    // SUMMARY, value side: column tile cw of C = Q^T V
+  float macc[8];     // SUMMARY, value side: partial column sums of Q
+  if (SUMMARY) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cacc[i] = zero16();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) macc[j] = 0.f;
+  }
   if (tid < D) {
-    eta[tid] = (!SUMMARY && carry) ? carry[((size_t)bh * nseg + seg) * (D * DV + D) + D * DV + tid] : 0.f;
+    eta[tid] = (!SUMMARY && c_in) ? c_in[D * DV + tid] : 0.f;
     inc[tid] = 0.f;
   }
   if (tid < C) denp[C + tid] = 0.f;  // key tile 1 adds nothing to query rows 0 .. 31
@@ -256,6 +274,25 @@ __global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws(
       asm volatile("" : "+v"(ln));
       const int lr = ln & 31, lg = ln >> 5, u = ln + 64 * (w - 4);
       f32x16 acc[2];
+      // phase 1 (SUMMARY): C += Q^T V on column tile cw, and this thread's
+      // share of m: columns 8 (u % 16) .. + 7 over tokens 4 (u / 16) .. + 3
+      // (rows past n were loaded as zeros)
+      if (SUMMARY && hasY) {
+#pragma unroll
+        for (int s = 0; s < C / 16; ++s) {
+          const bf16x8 bV = frag_tr<true>(Vs, G::ldV, cw * 32, s * 16, ln);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) cacc[i] = mfma(frag_tr<true>(Qy, G::ldQ, i * 32, s * 16, ln), bV, cacc[i]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint4 x = *reinterpret_cast<const uint4*>(Qy + (4 * (u >> 4) + r) * G::ldQ + (u & 15) * 8);
+          macc[0] += __uint_as_float(x.x << 16); macc[1] += __uint_as_float(x.x & 0xffff0000u);
+          macc[2] += __uint_as_float(x.y << 16); macc[3] += __uint_as_float(x.y & 0xffff0000u);
+          macc[4] += __uint_as_float(x.z << 16); macc[5] += __uint_as_float(x.z & 0xffff0000u);
+          macc[6] += __uint_as_float(x.w << 16); macc[7] += __uint_as_float(x.w & 0xffff0000u);
+        }
+      }
       // phase 1: T^T tile (keys it, queries jt) = R Q^T, it <= jt; O = Q Phi0; q . eta0
       if (!SUMMARY && hasY) {
         if (cw < 3) {
@@ -371,17 +408,150 @@ __global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws(
       }
       lds_barrier();
     }
-    if (SUMMARY) {                   // the bracket: Phi0 into the G slot, eta0 into the h slot
-      const int u = tid - 256;
-      float* rc = rec + ((size_t)bh * (nseg + 1) + seg) * F;
-      int col = cw * 32 + lr;
-      asm volatile("" : "+v"(col));
+  }
+  // ending state into the record: S0 (key side), Phi0 and eta0 (value side),
+  // and with SUMMARY the segment's C and m
+  if (rec) {
+    int col = cw * 32 + lr;
+    asm volatile("" : "+v"(col));
+    float* dst = rec + (keyside ? 0 : off_G(D, DV));
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) rc[off_G(D, DV) + (size_t)(32 * i + acc_row(e, lg)) * DV + col] = st[i][e];
-      if (u < D) rc[off_h(D, DV) + u] = eta[u];
+      for (int e = 0; e < 16; ++e) dst[(size_t)(32 * i + acc_row(e, lg)) * D + col] = st[i][e];
+    const int u = tid - 256;
+    float* red = reinterpret_cast<float*>(lds + G::oWh);   // [16][D] partial sums of m (dead W | T region)
+    if (!keyside) {
+      if (u < D) rec[off_h(D, DV) + u] = eta[u];
+      if (SUMMARY) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) rec[off_C(D, DV) + (size_t)(32 * i + acc_row(e, lg)) * DV + col] = cacc[i][e];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) red[(u >> 4) * D + (u & 15) * 8 + j] = macc[j];
+      }
     }
+    if (SUMMARY) {
+      lds_barrier();
+      if (!keyside && u < D) {
+        float m = 0.f;
+#pragma unroll
+        for (int g = 0; g < 16; ++g) m += red[g * D + u];
+        rec[off_m(D, DV) + u] = m;
+      }
+    }
+  }
+}
+
+// First launch of the two-pass plan, grid (P - 1, BH): segment 0's output
+// walk (zero carry) and the summary walks of segments 1 .. P-2 (zero state),
+// each writing its record rec[bh][seg].
+__global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws_first(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    float* __restrict__ out, float* __restrict__ den_out, float* __restrict__ rec, int n, int c0, int cps,
+    int nseg, int normalized, float eps) {
+  extern __shared__ __align__(16) uint16_t lds[];
+  int seg, bh;
+  seg_head(seg, bh);
+  int cb, nt;
+  ws_range(seg, c0, cps, (n + CfgWS::C - 1) / CfgWS::C, cb, nt);
+  float* r = rec + ((size_t)bh * (nseg + 1) + seg) * state_floats(CfgWS::D, CfgWS::DV);
+  if (seg == 0)
+    walk_ws<false>(lds, q, k, v, out, den_out, nullptr, nullptr, r, bh, n, cb, nt, normalized, eps);
+  else
+    walk_ws<true>(lds, q, k, v, nullptr, nullptr, nullptr, nullptr, r, bh, n, cb, nt, 0, 0.f);
+}
+
+// Output walks from the true carries, grid (walks, BH): grid column x walks
+// segment seg0 + x.  spre: [BH][nseg][D*D] S prefixes and carry:
+// [BH][nseg][D*DV + D] Phi, eta carries (both null for a single segment: zero).
+__global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws_out(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    float* __restrict__ out, float* __restrict__ den_out, const float* __restrict__ spre,
+    const float* __restrict__ carry, int n, int c0, int cps, int nseg, int seg0, int normalized, float eps) {
+  constexpr int D = CfgWS::D, DV = CfgWS::DV;
+  extern __shared__ __align__(16) uint16_t lds[];
+  int seg, bh;
+  seg_head(seg, bh);
+  seg += seg0;
+  int cb, nt;
+  ws_range(seg, c0, cps, (n + CfgWS::C - 1) / CfgWS::C, cb, nt);
+  const float* si = spre ? spre + ((size_t)bh * nseg + seg) * D * D : nullptr;
+  const float* ci = carry ? carry + ((size_t)bh * nseg + seg) * (D * DV + D) : nullptr;
+  walk_ws<false>(lds, q, k, v, out, den_out, si, ci, nullptr, bh, n, cb, nt, normalized, eps);
+}
+
+// The brackets of the two-pass plan (Eq. semidirect in the Phi form): for
+// segment s = 1 .. nseg-2, whose record holds its S, C, m, Phi, eta from a
+// zero start, b_s = (Phi_s + S_{<s} C_s, eta_s + S_{<s} m_s), written in
+// place of (Phi_s, eta_s); S_{<s} = spre[s].  Record 0 (the ending state of
+// segment 0's output walk) already holds b_0.  grid (nseg - 2, BH), 1024
+// threads, one workgroup per (segment, head), a head's workgroups on one
+// XCD.  S_{<s} and C_s are split into bf16 hi + lo in LDS, as every computed
+// operand of the walks, and wave w forms the 32 x 32 tile (w / 4, w % 4) of
+// S_{<s} C_s in three passes (hi hi, hi lo, lo hi) with fp32 accumulation.
+template <int D, int DV>
+__global__ __launch_bounds__(1024) void k_ws_bracket(float* __restrict__ rec, const float* __restrict__ spre,
+                                                     int nseg) {
+  constexpr int ldS = D + kPad, ldC = DV + 16, NT = 1024;   // ldC: C is read through the transpose unit
+  static_assert(D == 128 && DV == 128, "16 waves of 32 x 32 output tiles");
+  __shared__ __align__(16) uint16_t Sh[D * ldS], Sl[D * ldS], Ch[D * ldC], Cl[D * ldC];
+  __shared__ float mv[D], ep[8 * D];
+  int s, bh;
+  seg_head(s, bh);
+  s += 1;
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 31, lg = l >> 5;
+  const int r0 = 32 * (w >> 2), c0 = 32 * (w & 3);
+  float* r = rec + ((size_t)bh * (nseg + 1) + s) * state_floats(D, DV);
+  const float* sp = spre + ((size_t)bh * nseg + s) * D * D;
+#pragma unroll
+  for (int i = 0; i < D * D / 4 / NT; ++i) {
+    const int e = tid + NT * i, row = e / (D / 4), c4 = e % (D / 4);
+    const float4 x = *reinterpret_cast<const float4*>(sp + 4 * (size_t)e);
+    const float4 y = *reinterpret_cast<const float4*>(r + off_C(D, DV) + (size_t)row * DV + 4 * c4);
+    uint32_t h0, h1, l0, l1;
+    split2(x.x, x.y, h0, l0);
+    split2(x.z, x.w, h1, l1);
+    *reinterpret_cast<uint2*>(Sh + row * ldS + 4 * c4) = make_uint2(h0, h1);
+    *reinterpret_cast<uint2*>(Sl + row * ldS + 4 * c4) = make_uint2(l0, l1);
+    split2(y.x, y.y, h0, l0);
+    split2(y.z, y.w, h1, l1);
+    *reinterpret_cast<uint2*>(Ch + row * ldC + 4 * c4) = make_uint2(h0, h1);
+    *reinterpret_cast<uint2*>(Cl + row * ldC + 4 * c4) = make_uint2(l0, l1);
+  }
+  if (tid < D) mv[tid] = r[off_m(D, DV) + tid];
+  f32x16 acc;        // b_s: element e is row r0 + acc_row(e, lg), column c0 + lr
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = r[off_G(D, DV) + (size_t)(r0 + acc_row(e, lg)) * DV + c0 + lr];
+  const float eta = tid < D ? r[off_h(D, DV) + tid] : 0.f;
+  __syncthreads();
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const bf16x8 ah = frag(Sh, ldS, r0, 16 * ks), al = frag(Sl, ldS, r0, 16 * ks);
+    const bf16x8 bh_ = frag_tr(Ch, ldC, c0, 16 * ks), bl_ = frag_tr(Cl, ldC, c0, 16 * ks);
+    acc = mfma(ah, bh_, acc);
+    acc = mfma(ah, bl_, acc);
+    acc = mfma(al, bh_, acc);
+  }
+  {  // S_{<s} m_s: eight partial sums of 16 k per row, then their total
+    const int row = tid % D, part = tid / D;
+    float x = 0.f;
+#pragma unroll
+    for (int j = 0; j < D / 8; ++j) {
+      const int kk = part * (D / 8) + j;
+      x += (bf16_to_f(Sh[row * ldS + kk]) + bf16_to_f(Sl[row * ldS + kk])) * mv[kk];
+    }
+    ep[part * D + row] = x;
+  }
+#pragma unroll
+  for (int e = 0; e < 16; ++e) r[off_G(D, DV) + (size_t)(r0 + acc_row(e, lg)) * DV + c0 + lr] = acc[e];
+  __syncthreads();
+  if (tid < D) {
+    float e = eta;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) e += ep[p * D + tid];
+    r[off_h(D, DV) + tid] = e;
   }
 }
 

@@ -189,12 +189,13 @@ int hla2_workspace_query(int B, int H, int n, int d, int dv, int chunk, int dtyp
   return ok();
 }
 
-int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int* segments, int* tile) {
+int hla2_fused_plan(int B, int H, int n, int d, int dv, int chunk, int* segments, int* tile, int* first_tiles,
+                    int* tiles_per_segment) {
   int rc;
   if (!segments || !tile) return fail(HLA_ERR_INVALID, "segments and tile must not be NULL");
   if ((rc = check_dims(B, H, n, d, dv, chunk, HLA_BF16, true)) != HLA_OK) return rc;
   if (chunk == 0) return fail(HLA_ERR_INVALID, "chunk must be set");
-  if (!hla::fused_supported(n, d, dv, chunk, HLA_BF16, 1) || !hla::fused_plan_query(B * H, n, d, dv, chunk, segments, tile))
+  if (!hla::fused_supported(n, d, dv, chunk, HLA_BF16, 1) || !hla::fused_plan_query(B * H, n, d, dv, chunk, segments, tile, first_tiles, tiles_per_segment))
     return fail(HLA_ERR_UNSUPPORTED, "the fused path does not cover d=%d dv=%d chunk=%d", d, dv, chunk);
   return ok();
 }

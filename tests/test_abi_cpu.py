@@ -204,6 +204,34 @@ def test_fused_plan_query():
     with pytest.raises(capi.HLAError) as ei:
         capi.hla2_fused_plan(1, 1, 64, 16, 16, 16)
     assert ei.value.code == UNSUP
+    L = capi.lib()
+    seg, tl = ctypes.c_int(0), ctypes.c_int(0)
+    assert L.hla2_fused_plan(2, 32, 16384, 128, 128, 128, ctypes.byref(seg), ctypes.byref(tl), None, None) == 0
+    assert (seg.value, tl.value) == (P_, tile)
+
+
+def _segment_tiles(P, first, per, M):
+    """Tile counts of the segments: segment 0 holds `first`, the others `per`, the last the rest."""
+    if P == 1:
+        return [M]
+    return [first] + [per] * (P - 2) + [M - first - per * (P - 2)]
+
+
+@pytest.mark.parametrize("B,H", [(2, 32), (1, 1), (1, 2), (4, 16), (8, 32), (1, 100), (3, 5)])
+@pytest.mark.parametrize("n", [1, 64, 130, 596, 4096, 16384])
+def test_fused_plan_d128_segments(B, H, n):
+    """The d = 128 plan (two launches of one walk per CU each, segment 0
+    shorter than the others) covers every tile once with non-empty segments,
+    and walks at most 256 workgroups per launch."""
+    P, tile, first, per = capi.hla2_fused_plan(B, H, n, 128, 128, 128, tiles=True)
+    M = -(-n // tile)
+    sizes = _segment_tiles(P, first, per, M)
+    assert sum(sizes) == M and min(sizes) >= 1 and len(sizes) == P
+    if P > 1:
+        assert P >= 3 and (P - 1) * B * H <= 256
+        assert first <= per and max(sizes[1:]) == per
+    if (B, H, n) == (2, 32, 16384):
+        assert (P, first, per) == (5, 34, 56)
 
 
 def test_forward_den_needs_normalized():

@@ -178,11 +178,21 @@ def test_fused_segment_counts(segments, monkeypatch):
 
 @pytest.mark.parametrize("segments", [1, 2, 3, 7, 100])
 def test_fused_d128_segment_counts(segments, monkeypatch):
-    """The d = 128 pipeline (summary walk of the earlier segments, their
-    carries, then one output walk per segment from its true carry) must not
+    """The d = 128 pipeline (segment 0's output walk beside the summary walks
+    of the later segments from a zero state, their brackets and carries, then
+    the other segments' output walks from their true carries) must not
     depend on the segment plan either; ragged tail, normalised."""
     monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
     assert _check_forward(2, 1, 64 * 9 + 20, 128, 128, 128, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=13)
+
+
+@pytest.mark.parametrize("ratio", ["0.2", "1.0", "2.5"])
+def test_fused_d128_first_segment_length(ratio, monkeypatch):
+    """Nor on the length of segment 0 against the others (HLA_WS_RATIO), at
+    the plan of a 64-head launch; ragged tail, normalised."""
+    monkeypatch.setenv("HLA_WS_RATIO", ratio)
+    monkeypatch.setenv("HLA_FUSED_SEGMENTS", "5")
+    assert _check_forward(1, 2, 64 * 23 + 9, 128, 128, 128, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=19)
 
 
 def test_fused_d128_pipelines_agree(monkeypatch):
@@ -209,6 +219,16 @@ def test_fused_long_single_head():
     segment count (one head), so the longest carry chains and the largest
     moment prefixes; every row against the oracle."""
     assert _check_forward(1, 1, 262144, 64, 64, 64, "unit", 1, False, capi.HLA_ALGO_FUSED, seed=5)
+
+
+def test_fused_long_single_head_d128():
+    """One d = 128 head of 65 536 tokens: 1024 tiles cut into 257 segments of
+    the two-pass plan (segment 0 of 2 tiles, 256 of 4), so the longest
+    bracket and carry chains of that plan; every row against the oracle.
+    (Unnormalised: at this length too few rows' denominators stand clear of
+    their cancellation scale for the ratio test.)"""
+    assert capi.hla2_fused_plan(1, 1, 65536, 128, 128, 128, tiles=True) == (257, 64, 2, 4)
+    assert _check_forward(1, 1, 65536, 128, 128, 128, "unit", 1, False, capi.HLA_ALGO_FUSED, seed=23)
 
 
 def test_fused_matches_chunked_closely():
