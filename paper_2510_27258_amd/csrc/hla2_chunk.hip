@@ -1,4 +1,4 @@
-// Chunk-parallel second-order HLA, general path (fp32 SIMT arithmetic).
+// Chunk-parallel second-order HLA, general path (fp32 and fp64 arithmetic).
 //
 // Two kernels, one workgroup per (head, chunk):
 //   k_chunk_summary  the chunk's masked summary (S, C, m, G, h) with zero
@@ -31,51 +31,25 @@ namespace hla {
 // The chunk is walked in blocks of TB = min(chunk, 32) tokens staged in LDS
 // (fp32, zero rows past n), so any chunk up to 128 fits:
 //   1. Y = A_s [V | 1] block row by block row: Y_ib = sum_{jb <= ib} A_s(ib, jb) [V_jb | 1];
-//   2. S, C, m, G, h summed over the token blocks, S, C and G in 4 x 4
-//      register tiles that each thread keeps for the whole chunk.
-// fp32 arithmetic throughout.  LDS: K, Q [TB][d+1], V [TB][dv+1],
-// A [TB][TB+1], Y [chunk][dv+1].
+//   2. S, C, m, G, h summed over the token blocks.
+// Every product runs on fp32 MFMA (v_mfma_f32_16x16x4_f32: lane l = 16 g + n
+// supplies A[n][k_g] and B[k_g][n] and holds D[4 g + i][n], i < 4): fp32
+// products and sums, one 16 x 16 output tile per wave at a time; a wave keeps
+// its tiles of Y (over the blocks jb) and of S, C, G (over the chunk) in its
+// accumulators.  LDS rows are padded to 17 floats modulo 32, so that the
+// reads along rows (k over tokens) and along columns (A_s = K Q^T, k over the
+// dimensions) of a half-wave fall in distinct banks but one.
+// LDS: K, Q [TB][ld], V [TB][ldv], A [TB][lda], Y [chunk][ldv], w [TB].
 // ----------------------------------------------------------------------------
-constexpr int kSumThreads = 512;
-constexpr int kSumTiles = 2;    // 4 x 4 tiles of a d x d or d x dv product per thread (d, dv <= 128)
+constexpr int kSumThreads = 512, kSumWaves = kSumThreads / 64;
+constexpr int kSumTiles = 8;   // 16 x 16 tiles of S, C or G per wave: (128 / 16)^2 over 8 waves
 
-// acc[r] += the thread's r-th 4 x 4 tile of A B (M x N, K terms), tiles dealt
-// round-robin over the workgroup; A(m, k) = al(m, k), B(k, n) = bl(k, n).
-template <typename AL, typename BL>
-__device__ __forceinline__ void tile_acc(float (&acc)[kSumTiles][16], int M, int N, int K, AL al, BL bl) {
-  const int tn = N / 4, tiles = (M / 4) * tn;
-#pragma unroll
-  for (int r = 0; r < kSumTiles; ++r) {
-    const int ti = threadIdx.x + kSumThreads * r;
-    if (ti >= tiles) continue;
-    const int m0 = (ti / tn) * 4, n0 = (ti % tn) * 4;
-    for (int kk = 0; kk < K; ++kk) {
-      float av[4], bv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = al(m0 + i, kk);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bv[j] = bl(kk, n0 + j);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[r][i * 4 + j] += av[i] * bv[j];
-    }
-  }
-}
+typedef float f32x4c __attribute__((ext_vector_type(4)));
 
-template <typename F>
-__device__ __forceinline__ void tile_put(const float (&acc)[kSumTiles][16], int M, int N, F put) {
-  const int tn = N / 4, tiles = (M / 4) * tn;
-#pragma unroll
-  for (int r = 0; r < kSumTiles; ++r) {
-    const int ti = threadIdx.x + kSumThreads * r;
-    if (ti >= tiles) continue;
-    const int m0 = (ti / tn) * 4, n0 = (ti % tn) * 4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) put(m0 + i, n0 + j, acc[r][i * 4 + j]);
-  }
+__host__ __device__ constexpr int sum_ld(int x) { return (x + 31) / 32 * 32 + 17; }
+
+__device__ __forceinline__ f32x4c mfma4(float a, float b, const f32x4c& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
 template <typename T>
@@ -84,10 +58,11 @@ __global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restri
                                                                int n, int d, int dv, int chunk, int M, float lg2g) {
   extern __shared__ float smem[];
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, nn = tid & 15, g = (tid >> 4) & 3;
   const int t0 = c * chunk;
   const int L = min(chunk, n - t0);
   const int TB = chunk < 32 ? chunk : 32, nb = chunk / TB;
-  const int ld = d + 1, ldv = dv + 1, lda = TB + 1;
+  const int ld = sum_ld(d), ldv = sum_ld(dv), lda = sum_ld(TB);
   const size_t qk_base = ((size_t)bh * n + t0) * d;
   const size_t v_base = ((size_t)bh * n + t0) * dv;
   float* Kb = smem;                          // [TB][ld]
@@ -95,8 +70,9 @@ __global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restri
   float* Vb = Qb + TB * ld;                  // [TB][ldv]
   float* Ab = Vb + TB * ldv;                 // [TB][lda]
   float* Y = Ab + TB * lda;                  // [chunk][ldv]: A_s V | A_s 1
+  float* wv = Y + chunk * ldv;               // [TB]: the block's token weights
   float* st = states + ((size_t)bh * M + c) * state_floats(d, dv);
-  auto w = [&](int t) { return exp2f(lg2g * (float)(L - 1 - t)); };   // gamma^(L-1-t)
+  auto wt = [&](int t) { return exp2f(lg2g * (float)(L - 1 - t)); };   // gamma^(L-1-t)
   auto stage_qk = [&](float* dst, const T* src, int tb) {
     for (int idx = tid; idx < TB * d; idx += kSumThreads) {
       const int t = idx / d, a = idx % d, tt = tb * TB + t;
@@ -109,63 +85,112 @@ __global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restri
       Vb[t * ldv + b] = tt < L ? ldf(v, v_base + (size_t)tt * dv + b) : 0.f;
     }
   };
+  const f32x4c zero = {0.f, 0.f, 0.f, 0.f};
 
   // 1. Y rows of block ib from the blocks jb <= ib
+  const int at = TB / 16, ytn = dv / 16, ytiles = at * ytn;   // ytiles <= 16: two per wave
   for (int ib = 0; ib < nb; ++ib) {
-    float accy[kSumTiles][16] = {};
+    f32x4c ya[2] = {zero, zero};
     float ysum = 0.f;
     for (int jb = 0; jb <= ib; ++jb) {
       if (jb == 0) stage_qk(Kb, k, ib);
       stage_qk(Qb, q, jb);
       stage_v(jb);
       __syncthreads();
-      // A_s(ib, jb): [j < i] gamma^(2L-2-i-j) k_i . q_j
-      for (int idx = tid; idx < TB * TB; idx += kSumThreads) {
-        const int i = idx / TB, j = idx % TB, gi = ib * TB + i, gj = jb * TB + j;
-        float x = 0.f;
-        if (gj < gi) {
-          for (int a = 0; a < d; ++a) x += Kb[i * ld + a] * Qb[j * ld + a];
-          x *= exp2f(lg2g * (float)(2 * L - 2 - gi - gj));
+      // A_s(ib, jb) = [j < i] gamma^(2L-2-i-j) k_i . q_j, one 16 x 16 tile per wave
+      if (w < at * at) {
+        const int i0 = (w / at) * 16, j0 = (w % at) * 16;
+        f32x4c x = zero;
+        if (jb < ib || j0 <= i0)
+          for (int k0 = 0; k0 < d; k0 += 4) x = mfma4(Kb[(i0 + nn) * ld + k0 + g], Qb[(j0 + nn) * ld + k0 + g], x);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = i0 + 4 * g + e, j = j0 + nn, gi = ib * TB + i, gj = jb * TB + j;
+          Ab[i * lda + j] = gj < gi ? x[e] * exp2f(lg2g * (float)(2 * L - 2 - gi - gj)) : 0.f;
         }
-        Ab[i * lda + j] = x;
       }
       __syncthreads();
-      tile_acc(accy, TB, dv, TB, [&](int i, int j) { return Ab[i * lda + j]; },
-               [&](int j, int b) { return Vb[j * ldv + b]; });
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int tile = w + kSumWaves * r;
+        if (tile < ytiles) {
+          const int i0 = (tile / ytn) * 16, b0 = (tile % ytn) * 16;
+          for (int k0 = 0; k0 < TB; k0 += 4)
+            ya[r] = mfma4(Ab[(i0 + nn) * lda + k0 + g], Vb[(k0 + g) * ldv + b0 + nn], ya[r]);
+        }
+      }
       if (tid < TB)
         for (int j = 0; j < TB; ++j) ysum += Ab[tid * lda + j];
       __syncthreads();             // Q, V and A are restaged for the next block
     }
-    tile_put(accy, TB, dv, [&](int i, int b, float x) { Y[(ib * TB + i) * ldv + b] = x; });
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int tile = w + kSumWaves * r;
+      if (tile < ytiles) {
+        const int i0 = (tile / ytn) * 16, b0 = (tile % ytn) * 16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Y[(ib * TB + i0 + 4 * g + e) * ldv + b0 + nn] = ya[r][e];
+      }
+    }
     if (tid < TB) Y[(ib * TB + tid) * ldv + dv] = ysum;
   }
 
   // 2. S = K^T diag(w) K, C = Q^T diag(w) V, m = Q^T w, G = K^T Y, h = K^T (A_s 1)
-  float accs[kSumTiles][16] = {}, accc[kSumTiles][16] = {}, accg[kSumTiles][16] = {};
+  const int stn = d / 16, sti = stn * stn, ctn = dv / 16, cti = stn * ctn;
+  f32x4c as[kSumTiles], ac[kSumTiles], ag[kSumTiles];
+#pragma unroll
+  for (int r = 0; r < kSumTiles; ++r) as[r] = ac[r] = ag[r] = zero;
   float am = 0.f, ah = 0.f;
   for (int tb = 0; tb < nb; ++tb) {
     stage_qk(Kb, k, tb);
     stage_qk(Qb, q, tb);
     stage_v(tb);
-    if (tid < TB) Ab[tid] = tb * TB + tid < L ? w(tb * TB + tid) : 0.f;   // the block's token weights
+    if (tid < TB) wv[tid] = tb * TB + tid < L ? wt(tb * TB + tid) : 0.f;
     __syncthreads();               // also orders the Y writes of step 1 before their reads
     const float* Yb = Y + tb * TB * ldv;
-    tile_acc(accs, d, d, TB, [&](int a, int t) { return Kb[t * ld + a]; },
-             [&](int t, int b) { return Ab[t] * Kb[t * ld + b]; });
-    tile_acc(accc, d, dv, TB, [&](int a, int t) { return Qb[t * ld + a]; },
-             [&](int t, int b) { return Ab[t] * Vb[t * ldv + b]; });
-    tile_acc(accg, d, dv, TB, [&](int a, int t) { return Kb[t * ld + a]; },
-             [&](int t, int b) { return Yb[t * ldv + b]; });
+#pragma unroll
+    for (int r = 0; r < kSumTiles; ++r) {
+      const int tile = w + kSumWaves * r;
+      if (tile < sti) {
+        const int a0 = (tile / stn) * 16, b0 = (tile % stn) * 16;
+        for (int k0 = 0; k0 < TB; k0 += 4) {
+          const int t = k0 + g;
+          as[r] = mfma4(Kb[t * ld + a0 + nn], wv[t] * Kb[t * ld + b0 + nn], as[r]);
+        }
+      }
+      if (tile < cti) {
+        const int a0 = (tile / ctn) * 16, b0 = (tile % ctn) * 16;
+        for (int k0 = 0; k0 < TB; k0 += 4) {
+          const int t = k0 + g;
+          ac[r] = mfma4(Qb[t * ld + a0 + nn], wv[t] * Vb[t * ldv + b0 + nn], ac[r]);
+          ag[r] = mfma4(Kb[t * ld + a0 + nn], Yb[t * ldv + b0 + nn], ag[r]);
+        }
+      }
+    }
     if (tid < d)
       for (int t = 0; t < TB; ++t) {
-        am += Ab[t] * Qb[t * ld + tid];
+        am += wv[t] * Qb[t * ld + tid];
         ah += Kb[t * ld + tid] * Yb[t * ldv + dv];
       }
     __syncthreads();
   }
-  tile_put(accs, d, d, [&](int a, int b, float x) { st[(size_t)a * d + b] = x; });
-  tile_put(accc, d, dv, [&](int a, int b, float x) { st[off_C(d, dv) + (size_t)a * dv + b] = x; });
-  tile_put(accg, d, dv, [&](int a, int b, float x) { st[off_G(d, dv) + (size_t)a * dv + b] = x; });
+#pragma unroll
+  for (int r = 0; r < kSumTiles; ++r) {
+    const int tile = w + kSumWaves * r;
+    if (tile < sti) {
+      const int a0 = (tile / stn) * 16, b0 = (tile % stn) * 16;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) st[(size_t)(a0 + 4 * g + e) * d + b0 + nn] = as[r][e];
+    }
+    if (tile < cti) {
+      const int a0 = (tile / ctn) * 16, b0 = (tile % ctn) * 16;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        st[off_C(d, dv) + (size_t)(a0 + 4 * g + e) * dv + b0 + nn] = ac[r][e];
+        st[off_G(d, dv) + (size_t)(a0 + 4 * g + e) * dv + b0 + nn] = ag[r][e];
+      }
+    }
+  }
   if (tid < d) {
     st[off_m(d, dv) + tid] = am;
     st[off_h(d, dv) + tid] = ah;
@@ -194,45 +219,57 @@ __global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restri
 // r_j and q_t . r_j are not rounded to fp32 on the way.  Chunks of up to 64
 // tokens (the forward paths cut larger chunks, exact by Thm. 2).
 //
-// The chunk's q and k are staged in LDS (fp32, zero rows past n), and every
-// product runs as register tiles: a thread owns 4 x 4 outputs at a time
-// (512 threads, so two waves share each SIMD).
-// LDS: R [chunk][d+1] fp64, Q and K [chunk][d+1] fp32, W/T [chunk][chunk+1]
-// fp32, den [chunk] fp32 (149 KB at chunk 64, d 128).
+// Every product runs on MFMA, one 16 x 16 output tile per wave at a time
+// (lane l = 16 g + n supplies A[n][k_g] and B[k_g][n] and holds
+// D[4 g + i][n]): the fp64 ones (Q S0, Q K^T, the carry term, W K, the T
+// products) on v_mfma_f64_16x16x4_f64 with fp32 operands widened exactly,
+// T V on v_mfma_f32_16x16x4_f32.  Triangular products stop at the
+// diagonal tile.  A wave keeps the carry part of its output tiles in its
+// accumulators until T V is added.
+// LDS: R [chunk][d+1] fp64 (V [chunk][dv+1] fp32 in its place once R is
+// dead), Q and K [chunk][d+1] fp32, W/T [chunk][chunk+1] fp32, den [chunk]
+// fp32 (149 KB at chunk 64, d = dv = 128).
+typedef double f64x4c __attribute__((ext_vector_type(4)));
 
-// Out(m, n) = sum_k A(m, k) B(k, n) for m < M, n < N (multiples of 4), k < K,
-// 4 x 4 outputs per thread and tile.  A(m, k) = a[m sam + k sak] (LDS);
-// B(k, n) = bl(k, n).  lower: tiles wholly above the diagonal (n > m) are not
-// computed; epi(m, n, 0) is called for their outputs.
-template <typename Acc, typename TA, typename BL, typename EPI>
-__device__ __forceinline__ void tgemm(int M, int N, int K, const TA* a, int sam, int sak, BL bl, EPI epi,
-                                      bool lower) {
-  const int tn = N / 4, tiles = (M / 4) * tn;
-  for (int ti = threadIdx.x; ti < tiles; ti += blockDim.x) {
-    const int m0 = (ti / tn) * 4, n0 = (ti % tn) * 4;
-    Acc acc[4][4];
+__device__ __forceinline__ f64x4c mfma4(double a, double b, const f64x4c& c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// acc += sum_{k < K} A(k) B(k) for this lane's operands, K a multiple of 16,
+// af(k) = A[m0 + n][k], bf(k) = B[k][n0 + n]; both from LDS, four k steps'
+// loads issued ahead of their products.
+template <typename E, typename V, typename AF, typename BF>
+__device__ __forceinline__ void mma_lds(V& acc, int K, int g, AF af, BF bf) {
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    E x[4], y[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = Acc(0);
-    if (!lower || n0 <= m0 + 3) {
-      for (int kk = 0; kk < K; ++kk) {
-        Acc av[4], bv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) av[i] = (Acc)a[(m0 + i) * sam + kk * sak];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) bv[j] = (Acc)bl(kk, n0 + j);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] += av[i] * bv[j];
-      }
+    for (int u = 0; u < 4; ++u) {
+      x[u] = af(k0 + 4 * u + g);
+      y[u] = bf(k0 + 4 * u + g);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) epi(m0 + i, n0 + j, acc[i][j]);
+    for (int u = 0; u < 4; ++u) acc = mfma4(x[u], y[u], acc);
   }
+}
+
+// The same with B from global memory (K <= 128): all of the lane's B loads
+// are issued before the first product.
+template <typename E, typename V, typename AF, typename BF>
+__device__ __forceinline__ void mma_glb(V& acc, int K, int g, AF af, BF bf) {
+  float y[32];
+#pragma unroll
+  for (int s = 0; s < 32; ++s)
+    if (4 * s < K) y[s] = bf(4 * s + g);
+#pragma unroll
+  for (int s = 0; s < 32; ++s)
+    if (4 * s < K) acc = mfma4(af(4 * s + g), (E)y[s], acc);
+}
+
+__device__ __forceinline__ float4 ld4f(const float* p, size_t i) { return *reinterpret_cast<const float4*>(p + i); }
+__device__ __forceinline__ float4 ld4f(const uint16_t* p, size_t i) {
+  const uint2 x = *reinterpret_cast<const uint2*>(p + i);
+  return make_float4(__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xffff0000u), __uint_as_float(x.y << 16),
+                     __uint_as_float(x.y & 0xffff0000u));
 }
 
 template <typename T>
@@ -243,12 +280,19 @@ __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const 
                                                  float eps, float lg2g) {
   extern __shared__ double smemd[];
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, nn = tid & 15, g = (tid >> 4) & 3;
+  // The fp64 MFMA holds D[4 i + g][n] in element i (the fp32 one D[4 g + i][n]):
+  // lane n supplies A row pr = 4 (n % 4) + n / 4 instead of row n, so that the
+  // fp64 results arrive in the fp32 layout.
+  const int pr = 4 * (nn & 3) + (nn >> 2);
   const int t0 = c * chunk;
-  const int L = min(chunk, n - t0), Lp = chunk, ld = d + 1, ldw = chunk + 1;
+  const int L = min(chunk, n - t0), Lp = chunk, ld = d + 1, ldw = chunk + 1, ldv = dv + 1;
   const size_t qk_base = ((size_t)bh * n + t0) * d;
   const size_t v_base = ((size_t)bh * n + t0) * dv;
   double* R = smemd;                                           // [Lp][ld]
-  float* Qs = reinterpret_cast<float*>(R + (size_t)Lp * ld);   // [Lp][ld]
+  float* Vs = reinterpret_cast<float*>(smemd);                 // [Lp][ldv], once R is dead
+  const size_t rv = (size_t)Lp * ld * 2 > (size_t)Lp * ldv ? (size_t)Lp * ld * 2 : (size_t)Lp * ldv;
+  float* Qs = reinterpret_cast<float*>(smemd) + ((rv + 3) & ~size_t(3));   // [Lp][ld]
   float* Ks = Qs + (size_t)Lp * ld;                            // [Lp][ld]
   float* W = Ks + (size_t)Lp * ld;                             // [Lp][ldw]
   float* dn = W + (size_t)Lp * ldw;                            // [Lp]
@@ -259,113 +303,181 @@ __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const 
   const float* G0 = st + off_G(d, dv);
   const float* h0 = st + off_h(d, dv);
   float* o = out + v_base;
-  auto g = [&](int e) { return exp2f(lg2g * (float)e); };      // gamma^e
+  auto gp = [&](int e) { return exp2f(lg2g * (float)e); };     // gamma^e
+  const int mt = Lp / 16, rn = d / 16, rtiles = mt * rn, on = dv / 16, otiles = mt * on;
+  const int wtiles = mt * (mt + 1) / 2;                        // tiles on or below the diagonal
+  auto lower_tile = [&](int tile, int& m0_, int& n0_) {
+    int mi = 0;
+    while ((mi + 1) * (mi + 2) / 2 <= tile) ++mi;
+    m0_ = 16 * mi;
+    n0_ = 16 * (tile - mi * (mi + 1) / 2);
+  };
+  const f64x4c zd = {0.0, 0.0, 0.0, 0.0};
+  const f32x4c zf = {0.f, 0.f, 0.f, 0.f};
 
-  for (int idx = tid; idx < Lp * d; idx += blockDim.x) {
-    const int t = idx / d, a = idx % d;
-    Qs[t * ld + a] = t < L ? ldf(q, qk_base + (size_t)t * d + a) : 0.f;
-    Ks[t * ld + a] = t < L ? ldf(k, qk_base + (size_t)t * d + a) : 0.f;
+  for (int idx = tid; idx < Lp * d / 4; idx += blockDim.x) {
+    const int t = idx / (d / 4), a = (idx % (d / 4)) * 4;
+    const float4 xq = t < L ? ld4f(q, qk_base + (size_t)t * d + a) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4 xk = t < L ? ld4f(k, qk_base + (size_t)t * d + a) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float* pq = Qs + t * ld + a;
+    float* pk = Ks + t * ld + a;
+    pq[0] = xq.x; pq[1] = xq.y; pq[2] = xq.z; pq[3] = xq.w;
+    pk[0] = xk.x; pk[1] = xk.y; pk[2] = xk.z; pk[3] = xk.w;
   }
   __syncthreads();
 
   // P = Q S0 into R;  W[t][i] = [i <= t] g^(t-i) q_t . k_i
-  tgemm<double>(Lp, d, d, Qs, ld, 1, [&](int kk, int nn) { return S0[(size_t)kk * d + nn]; },
-                [&](int m, int nn, double x) { R[m * ld + nn] = x; }, false);
-  tgemm<double>(Lp, Lp, d, Qs, ld, 1, [&](int kk, int nn) { return Ks[nn * ld + kk]; },
-                [&](int t, int i, double x) { W[t * ldw + i] = i <= t ? (float)(x * (double)g(t - i)) : 0.f; },
-                true);
+  for (int tile = w; tile < rtiles; tile += kSumWaves) {
+    const int mm = (tile / rn) * 16, n0 = (tile % rn) * 16;
+    f64x4c acc = zd;
+    mma_glb<double>(acc, d, g, [&](int kk) { return (double)Qs[(mm + pr) * ld + kk]; },
+                    [&](int kk) { return S0[(size_t)kk * d + n0 + nn]; });
+#pragma unroll
+    for (int i = 0; i < 4; ++i) R[(mm + 4 * g + i) * ld + n0 + nn] = acc[i];
+  }
+  for (int tile = w; tile < wtiles; tile += kSumWaves) {
+    int mm, n0;
+    lower_tile(tile, mm, n0);
+    f64x4c acc = zd;
+    mma_lds<double>(acc, d, g, [&](int kk) { return (double)Qs[(mm + pr) * ld + kk]; },
+                    [&](int kk) { return (double)Ks[(n0 + nn) * ld + kk]; });
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = mm + 4 * g + i, j = n0 + nn;
+      W[t * ldw + j] = j <= t ? (float)(acc[i] * (double)gp(t - j)) : 0.f;
+    }
+  }
   __syncthreads();
+  // eight lanes per token row: x(t) summed over the d dimensions, in fp64
+  auto rowdot = [&](auto term) {
+    const int t = tid >> 3, p = tid & 7;
+    double s = 0.0;
+    if (t < Lp)
+      for (int a = p; a < d; a += 8) s += term(t, a);
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    return s;
+  };
+  f32x4c oc[4];      // carry part of this wave's output tiles w + 8 r
+#pragma unroll
+  for (int r = 0; r < 4; ++r) oc[r] = zf;
   if (masked) {
     // carry term g^(2(a+1)) (q_t^T S0 C0 - q_t^T G0) (and its denominator)
-    const int tn = dv / 4, tiles = (Lp / 4) * tn;
-    for (int ti = tid; ti < tiles; ti += blockDim.x) {
-      const int mm = (ti / tn) * 4, n0 = (ti % tn) * 4;
-      double acc[4][4] = {};
-      for (int a = 0; a < d; ++a) {
-        double rc[4], qc[4], cb[4], gb[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          rc[i] = R[(mm + i) * ld + a];
-          qc[i] = Qs[(mm + i) * ld + a];
-        }
+    for (int r = 0; r < 4; ++r) {
+      const int tile = w + kSumWaves * r;
+      if (tile < otiles) {
+        const int mm = (tile / on) * 16, n0 = (tile % on) * 16;
+        f64x4c acc = zd;
+        mma_glb<double>(acc, d, g, [&](int kk) { return R[(mm + pr) * ld + kk]; },
+                        [&](int kk) { return C0[(size_t)kk * dv + n0 + nn]; });
+        mma_glb<double>(acc, d, g, [&](int kk) { return -(double)Qs[(mm + pr) * ld + kk]; },
+                        [&](int kk) { return G0[(size_t)kk * dv + n0 + nn]; });
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          cb[j] = C0[(size_t)a * dv + n0 + j];
-          gb[j] = G0[(size_t)a * dv + n0 + j];
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] += rc[i] * cb[j] - qc[i] * gb[j];
+        for (int i = 0; i < 4; ++i) oc[r][i] = (float)acc[i] * gp(2 * (mm + 4 * g + i) + 2);
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (mm + i < L)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) o[(size_t)(mm + i) * dv + n0 + j] = (float)acc[i][j] * g(2 * (mm + i) + 2);
     }
-    for (int t = tid; t < L; t += blockDim.x) {
-      double s = 0.0;
-      for (int a = 0; a < d; ++a) s += R[t * ld + a] * (double)m0[a] - (double)Qs[t * ld + a] * (double)h0[a];
-      dn[t] = (float)s * g(2 * t + 2);
-    }
+    const double s = rowdot([&](int t, int a) { return R[t * ld + a] * (double)m0[a] - (double)Qs[t * ld + a] * (double)h0[a]; });
+    if ((tid & 7) == 0 && (tid >> 3) < Lp) dn[tid >> 3] = (float)s * gp(2 * (tid >> 3) + 2);
   }
   __syncthreads();
-  // the carry part of r_t decays by g^(a+1); then R += W K  (r_j = S_j q_j)
-  tgemm<double>(Lp, d, Lp, W, ldw, 1, [&](int kk, int nn) { return Ks[kk * ld + nn]; },
-                [&](int j, int a, double x) { R[j * ld + a] = R[j * ld + a] * (double)g(j + 1) + x; }, false);
+  // the carry part of r_t decays by g^(a+1); then R += W K  (r_j = S_j q_j; W is zero past the diagonal)
+  for (int tile = w; tile < rtiles; tile += kSumWaves) {
+    const int mm = (tile / rn) * 16, n0 = (tile % rn) * 16;
+    f64x4c acc = zd;
+    mma_lds<double>(acc, mm + 16, g, [&](int kk) { return (double)W[(mm + pr) * ldw + kk]; },
+                    [&](int kk) { return (double)Ks[kk * ld + n0 + nn]; });
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = mm + 4 * g + i;
+      R[j * ld + n0 + nn] = R[j * ld + n0 + nn] * (double)gp(j + 1) + acc[i];
+    }
+  }
   __syncthreads();
   // T[t][j] = [j <= t] g^(2(t-j)) (q_t . r_j)  (masked)  or  g^(t-j) (r_t . q_j)  (unmasked)
-  if (masked)
-    tgemm<double>(Lp, Lp, d, Qs, ld, 1, [&](int kk, int nn) { return R[nn * ld + kk]; },
-                  [&](int t, int j, double x) { W[t * ldw + j] = j <= t ? (float)(x * (double)g(2 * (t - j))) : 0.f; },
-                  true);
-  else
-    tgemm<double>(Lp, Lp, d, R, ld, 1, [&](int kk, int nn) { return (double)Qs[nn * ld + kk]; },
-                  [&](int t, int j, double x) { W[t * ldw + j] = j <= t ? (float)(x * (double)g(t - j)) : 0.f; },
-                  true);
+  for (int tile = w; tile < wtiles; tile += kSumWaves) {
+    int mm, n0;
+    lower_tile(tile, mm, n0);
+    f64x4c acc = zd;
+    if (masked)
+      mma_lds<double>(acc, d, g, [&](int kk) { return (double)Qs[(mm + pr) * ld + kk]; },
+                      [&](int kk) { return R[(n0 + nn) * ld + kk]; });
+    else
+      mma_lds<double>(acc, d, g, [&](int kk) { return R[(mm + pr) * ld + kk]; },
+                      [&](int kk) { return (double)Qs[(n0 + nn) * ld + kk]; });
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = mm + 4 * g + i, j = n0 + nn;
+      W[t * ldw + j] = j <= t ? (float)(acc[i] * (double)gp(masked ? 2 * (t - j) : t - j)) : 0.f;
+    }
+  }
   if (!masked) {
-    tgemm<double>(Lp, dv, d, R, ld, 1, [&](int kk, int nn) { return C0[(size_t)kk * dv + nn]; },
-                  [&](int t, int b, double x) {
-                    if (t < L) o[(size_t)t * dv + b] = (float)x * g(t + 1);
-                  },
-                  false);
-    for (int t = tid; t < L; t += blockDim.x) {
-      double s = 0.0;
-      for (int a = 0; a < d; ++a) s += R[t * ld + a] * (double)m0[a];
-      dn[t] = (float)s * g(t + 1);
+    // carry term g^(a+1) r_t^T C0 (and its denominator)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int tile = w + kSumWaves * r;
+      if (tile < otiles) {
+        const int mm = (tile / on) * 16, n0 = (tile % on) * 16;
+        f64x4c acc = zd;
+        mma_glb<double>(acc, d, g, [&](int kk) { return R[(mm + pr) * ld + kk]; },
+                        [&](int kk) { return C0[(size_t)kk * dv + n0 + nn]; });
+#pragma unroll
+        for (int i = 0; i < 4; ++i) oc[r][i] = (float)acc[i] * gp(mm + 4 * g + i + 1);
+      }
+    }
+    const double s = rowdot([&](int t, int a) { return R[t * ld + a] * (double)m0[a]; });
+    if ((tid & 7) == 0 && (tid >> 3) < Lp) dn[tid >> 3] = (float)s * gp((tid >> 3) + 1);
+  }
+  __syncthreads();
+  // V into the space of R (rows past the chunk's tokens zero); the rows' denominators
+  for (int idx = tid; idx < Lp * dv / 4; idx += blockDim.x) {
+    const int t = idx / (dv / 4), b = (idx % (dv / 4)) * 4;
+    const float4 x = t < L ? ld4f(v, v_base + (size_t)t * dv + b) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float* pv = Vs + t * ldv + b;
+    pv[0] = x.x; pv[1] = x.y; pv[2] = x.z; pv[3] = x.w;
+  }
+  if (normalized) {
+    const int t = tid >> 3, p = tid & 7;
+    float s = 0.f;
+    if (t < Lp)
+      for (int j = p; j <= t; j += 8) s += W[t * ldw + j];
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    if (p == 0 && t < Lp) {
+      s += dn[t];
+      dn[t] = s;
+      if (den_out && t < L) den_out[(size_t)bh * n + t0 + t] = s;
     }
   }
   __syncthreads();
-  if (normalized) {
-    for (int t = tid; t < L; t += blockDim.x) {
-      float s = dn[t];
-      for (int j = 0; j <= t; ++j) s += W[t * ldw + j];
-      dn[t] = s;
-      if (den_out) den_out[(size_t)bh * n + t0 + t] = s;
+  // o_t = carry + sum_{j <= t} T[t][j] v_j
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int tile = w + kSumWaves * r;
+    if (tile < otiles) {
+      const int mm = (tile / on) * 16, n0 = (tile % on) * 16;
+      f32x4c acc = oc[r];
+      mma_lds<float>(acc, mm + 16, g, [&](int kk) { return W[(mm + nn) * ldw + kk]; },
+                     [&](int kk) { return Vs[kk * ldv + n0 + nn]; });
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = mm + 4 * g + i;
+        if (t < L) o[(size_t)t * dv + n0 + nn] = normalized ? acc[i] / (dn[t] + eps) : acc[i];
+      }
     }
-    __syncthreads();
   }
-  // o_t += sum_{j <= t} T[t][j] v_j (rows past the chunk's tokens read as zero)
-  tgemm<float>(Lp, dv, Lp, W, ldw, 1,
-               [&](int kk, int nn) { return kk < L ? ldf(v, v_base + (size_t)kk * dv + nn) : 0.f; },
-               [&](int t, int b, float x) {
-                 if (t < L) {
-                   const float y = o[(size_t)t * dv + b] + x;
-                   o[(size_t)t * dv + b] = normalized ? y / (dn[t] + eps) : y;
-                 }
-               },
-               false);
 }
 
 // ----------------------------------------------------------------------------
 static size_t summary_lds(int chunk, int d, int dv) {
   const size_t tb = chunk < 32 ? chunk : 32;
-  return sizeof(float) * (2 * tb * (d + 1) + tb * (dv + 1) + tb * (tb + 1) + (size_t)chunk * (dv + 1));
+  return sizeof(float) * (2 * tb * sum_ld(d) + tb * sum_ld(dv) + tb * sum_ld((int)tb) + (size_t)chunk * sum_ld(dv) + tb);
 }
-static size_t readout_lds(int chunk, int d) {
-  return sizeof(double) * (size_t)chunk * (d + 1) +
-         sizeof(float) * (2 * (size_t)chunk * (d + 1) + (size_t)chunk * (chunk + 1) + chunk);
+static size_t readout_lds(int chunk, int d, int dv) {
+  const size_t r = 2 * (size_t)chunk * (d + 1), v = (size_t)chunk * (dv + 1);   // floats of R, or of V after it
+  return sizeof(float) * (((r > v ? r : v) + 3) / 4 * 4 + 2 * (size_t)chunk * (d + 1) + (size_t)chunk * (chunk + 1) + chunk);
 }
 
 hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, float* states,
@@ -394,7 +506,7 @@ hipError_t launch_readout(const Fwd& f, const float* prefix, hipStream_t s) {
   if (f.chunk > kReadoutMaxChunk) return hipErrorInvalidValue;
   const float lg2g = log2f(f.gamma);
   const int M = (f.n + f.chunk - 1) / f.chunk;
-  const size_t lds = readout_lds(f.chunk, f.d);
+  const size_t lds = readout_lds(f.chunk, f.d, f.dv);
   dim3 grid(M, f.BH), block(512);
   if (f.dtype == 1) {
     auto kern = k_readout<uint16_t>;
