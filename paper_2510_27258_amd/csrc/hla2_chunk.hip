@@ -52,8 +52,51 @@ __device__ __forceinline__ f32x4c mfma4(float a, float b, const f32x4c& c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+typedef double f64x4c __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f64x4c mfma4(double a, double b, const f64x4c& c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// acc += sum_{k < K} A(k) B(k) for this lane's operands, K a multiple of 16,
+// af(k) = A[m0 + n][k], bf(k) = B[k][n0 + n]; both from LDS, four k steps'
+// loads issued ahead of their products.
+template <typename E, typename V, typename AF, typename BF>
+__device__ __forceinline__ void mma_lds(V& acc, int K, int g, AF af, BF bf) {
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    E x[4], y[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      x[u] = af(k0 + 4 * u + g);
+      y[u] = bf(k0 + 4 * u + g);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc = mfma4(x[u], y[u], acc);
+  }
+}
+
+// The same with B from global memory (K <= 128): all of the lane's B loads
+// are issued before the first product.
+template <typename E, typename V, typename AF, typename BF>
+__device__ __forceinline__ void mma_glb(V& acc, int K, int g, AF af, BF bf) {
+  float y[32];
+#pragma unroll
+  for (int s = 0; s < 32; ++s)
+    if (4 * s < K) y[s] = bf(4 * s + g);
+#pragma unroll
+  for (int s = 0; s < 32; ++s)
+    if (4 * s < K) acc = mfma4(af(4 * s + g), (E)y[s], acc);
+}
+
+__device__ __forceinline__ float4 ld4f(const float* p, size_t i) { return *reinterpret_cast<const float4*>(p + i); }
+__device__ __forceinline__ float4 ld4f(const uint16_t* p, size_t i) {
+  const uint2 x = *reinterpret_cast<const uint2*>(p + i);
+  return make_float4(__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xffff0000u), __uint_as_float(x.y << 16),
+                     __uint_as_float(x.y & 0xffff0000u));
+}
+
 template <typename T>
-__global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restrict__ q, const T* __restrict__ k,
+__global__ __launch_bounds__(kSumThreads) void k_chunk_summary_blocks(const T* __restrict__ q, const T* __restrict__ k,
                                                                const T* __restrict__ v, float* __restrict__ states,
                                                                int n, int d, int dv, int chunk, int M, float lg2g) {
   extern __shared__ float smem[];
@@ -197,6 +240,172 @@ __global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restri
   }
 }
 
+// One pass over the blocks when the chunk's Q and V fit in LDS (the forward
+// paths' chunks of up to 64 tokens): block tb is staged once (its Q and V
+// kept for the later blocks, its K for this step only), with the next
+// block's loads in flight meanwhile, and
+//   A_row = A_s(tb, 0 .. tb),  Y_tb = A_row [V_{0..tb} | 1],
+//   S += K_tb^T diag(w) K_tb,  C += Q_tb^T diag(w) V_tb,  G += K_tb^T Y_tb,
+//   m += Q_tb^T w,  h += K_tb^T (A_row 1).
+// LDS: Q, V [chunk][ld, ldv], K [TB][ld], A_row [TB][sum_ld(chunk)],
+// Y [TB][ldv], w [TB]; the column sums of m and h are reduced through A_row.
+template <typename T>
+__global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restrict__ q, const T* __restrict__ k,
+                                                               const T* __restrict__ v, float* __restrict__ states,
+                                                               int n, int d, int dv, int chunk, int M, float lg2g) {
+  extern __shared__ float smem[];
+  const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, nn = tid & 15, g = (tid >> 4) & 3;
+  const int t0 = c * chunk;
+  const int L = min(chunk, n - t0);
+  const int TB = chunk < 32 ? chunk : 32, nb = chunk / TB;
+  const int ld = sum_ld(d), ldv = sum_ld(dv), lar = sum_ld(chunk);
+  const size_t qk_base = ((size_t)bh * n + t0) * d;
+  const size_t v_base = ((size_t)bh * n + t0) * dv;
+  float* Qa = smem;                          // [chunk][ld]
+  float* Va = Qa + chunk * ld;               // [chunk][ldv]
+  float* Kb = Va + chunk * ldv;              // [TB][ld]
+  float* Ar = Kb + TB * ld;                  // [TB][lar]
+  float* Yb = Ar + TB * lar;                 // [TB][ldv]: A_row V | A_row 1
+  float* wv = Yb + TB * ldv;                 // [TB]
+  float* st = states + ((size_t)bh * M + c) * state_floats(d, dv);
+  const f32x4c zero = {0.f, 0.f, 0.f, 0.f};
+  // staging: piece e = tid + 512 i of a block is row e / (width / 4), columns 4 (e % (width / 4)) ..
+  const int nqk = TB * d / 4, nv = TB * dv / 4;
+  float4 pk[2], pq[2], pv[2];
+  auto fetch = [&](int tb) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int e = tid + kSumThreads * i;
+      const int tq = tb * TB + e / (d / 4), tv = tb * TB + e / (dv / 4);
+      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+      const bool okq = e < nqk && tq < L, okv = e < nv && tv < L;
+      pk[i] = okq ? ld4f(k, qk_base + (size_t)tq * d + (e % (d / 4)) * 4) : z;
+      pq[i] = okq ? ld4f(q, qk_base + (size_t)tq * d + (e % (d / 4)) * 4) : z;
+      pv[i] = okv ? ld4f(v, v_base + (size_t)tv * dv + (e % (dv / 4)) * 4) : z;
+    }
+  };
+  auto put4 = [&](float* dst, const float4& x) { dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w; };
+  const int at = TB / 16, stn = d / 16, sti = stn * stn, ctn = dv / 16, cti = stn * ctn, ytiles = at * ctn;
+  f32x4c as[kSumTiles], ac[kSumTiles], ag[kSumTiles];
+#pragma unroll
+  for (int r = 0; r < kSumTiles; ++r) as[r] = ac[r] = ag[r] = zero;
+  // m and h: thread (column a, part p) sums the block rows p, p + P, ...
+  const int P = kSumThreads / d, ma = tid % d, mp = tid / d;
+  float am = 0.f, ah = 0.f;
+  fetch(0);
+  for (int tb = 0; tb < nb; ++tb) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int e = tid + kSumThreads * i;
+      if (e < nqk) {
+        const int t = e / (d / 4), a = (e % (d / 4)) * 4;
+        put4(Kb + t * ld + a, pk[i]);
+        put4(Qa + (tb * TB + t) * ld + a, pq[i]);
+      }
+      if (e < nv) put4(Va + (tb * TB + e / (dv / 4)) * ldv + (e % (dv / 4)) * 4, pv[i]);
+    }
+    if (tid < TB) wv[tid] = tb * TB + tid < L ? exp2f(lg2g * (float)(L - 1 - tb * TB - tid)) : 0.f;
+    if (tb + 1 < nb) fetch(tb + 1);
+    __syncthreads();
+    // A_row[i][j] = [j < tb TB + i] gamma^(2L-2-gi-j) k_i . q_j for the keys j of blocks 0 .. tb
+    const int jn = (tb + 1) * TB / 16, atiles = at * jn;
+    for (int tile = w; tile < atiles; tile += kSumWaves) {
+      const int i0 = (tile / jn) * 16, j0 = (tile % jn) * 16;
+      f32x4c x = zero;
+      if (j0 < tb * TB + i0 + 15)
+        mma_lds<float>(x, d, g, [&](int kk) { return Kb[(i0 + nn) * ld + kk]; },
+                       [&](int kk) { return Qa[(j0 + nn) * ld + kk]; });
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = i0 + 4 * g + e, j = j0 + nn, gi = tb * TB + i;
+        Ar[i * lar + j] = j < gi ? x[e] * exp2f(lg2g * (float)(2 * L - 2 - gi - j)) : 0.f;
+      }
+    }
+    __syncthreads();
+    // Y_tb = A_row V (the keys up to the row tile's last query) and A_row 1
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int tile = w + kSumWaves * r;
+      if (tile < ytiles) {
+        const int i0 = (tile / ctn) * 16, b0 = (tile % ctn) * 16;
+        f32x4c y = zero;
+        mma_lds<float>(y, tb * TB + i0 + 16, g, [&](int kk) { return Ar[(i0 + nn) * lar + kk]; },
+                       [&](int kk) { return Va[kk * ldv + b0 + nn]; });
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Yb[(i0 + 4 * g + e) * ldv + b0 + nn] = y[e];
+      }
+    }
+    {
+      const int row = tid >> 4, p = tid & 15;
+      float x = 0.f;
+      if (row < TB)
+        for (int j = p; j < (tb + 1) * TB; j += 16) x += Ar[row * lar + j];
+      x += __shfl_xor(x, 1);
+      x += __shfl_xor(x, 2);
+      x += __shfl_xor(x, 4);
+      x += __shfl_xor(x, 8);
+      if (p == 0 && row < TB) Yb[row * ldv + dv] = x;
+    }
+    __syncthreads();
+    const float* Qt = Qa + tb * TB * ld;
+    const float* Vt = Va + tb * TB * ldv;
+// (a rolled loop: unrolled, the three products' operands of all eight tiles
+    // would be scheduled together and spill)
+#pragma unroll 1
+    for (int r = 0; r < kSumTiles; ++r) {
+      const int tile = w + kSumWaves * r;
+      if (tile < sti) {
+        const int a0 = (tile / stn) * 16, b0 = (tile % stn) * 16;
+        mma_lds<float>(as[r], TB, g, [&](int t) { return Kb[t * ld + a0 + nn]; },
+                       [&](int t) { return wv[t] * Kb[t * ld + b0 + nn]; });
+      }
+      if (tile < cti) {
+        const int a0 = (tile / ctn) * 16, b0 = (tile % ctn) * 16;
+        mma_lds<float>(ac[r], TB, g, [&](int t) { return Qt[t * ld + a0 + nn]; },
+                       [&](int t) { return wv[t] * Vt[t * ldv + b0 + nn]; });
+        mma_lds<float>(ag[r], TB, g, [&](int t) { return Kb[t * ld + a0 + nn]; },
+                       [&](int t) { return Yb[t * ldv + b0 + nn]; });
+      }
+    }
+    for (int t = mp; t < TB; t += P) {
+      am += wv[t] * Qt[t * ld + ma];
+      ah += Kb[t * ld + ma] * Yb[t * ldv + dv];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < kSumTiles; ++r) {
+    const int tile = w + kSumWaves * r;
+    if (tile < sti) {
+      const int a0 = (tile / stn) * 16, b0 = (tile % stn) * 16;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) st[(size_t)(a0 + 4 * g + e) * d + b0 + nn] = as[r][e];
+    }
+    if (tile < cti) {
+      const int a0 = (tile / ctn) * 16, b0 = (tile % ctn) * 16;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        st[off_C(d, dv) + (size_t)(a0 + 4 * g + e) * dv + b0 + nn] = ac[r][e];
+        st[off_G(d, dv) + (size_t)(a0 + 4 * g + e) * dv + b0 + nn] = ag[r][e];
+      }
+    }
+  }
+  // m and h: the P partial sums of each column, through the A_row space
+  Ar[tid] = am;
+  Ar[kSumThreads + tid] = ah;
+  __syncthreads();
+  if (tid < d) {
+    float xm = 0.f, xh = 0.f;
+    for (int p = 0; p < P; ++p) {
+      xm += Ar[p * d + tid];
+      xh += Ar[kSumThreads + p * d + tid];
+    }
+    st[off_m(d, dv) + tid] = xm;
+    st[off_h(d, dv) + tid] = xh;
+  }
+}
+
 // ----------------------------------------------------------------------------
 // Readout of one chunk from its carry-in (S0, C0, m0, G0, h0).
 // With p_t = S0 q_t and r_j = S_j q_j = p_j + sum_{i<=j, i in chunk} (k_i.q_j) k_i:
@@ -229,49 +438,6 @@ __global__ __launch_bounds__(kSumThreads) void k_chunk_summary(const T* __restri
 // LDS: R [chunk][d+1] fp64 (V [chunk][dv+1] fp32 in its place once R is
 // dead), Q and K [chunk][d+1] fp32, W/T [chunk][chunk+1] fp32, den [chunk]
 // fp32 (149 KB at chunk 64, d = dv = 128).
-typedef double f64x4c __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f64x4c mfma4(double a, double b, const f64x4c& c) {
-  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
-}
-
-// acc += sum_{k < K} A(k) B(k) for this lane's operands, K a multiple of 16,
-// af(k) = A[m0 + n][k], bf(k) = B[k][n0 + n]; both from LDS, four k steps'
-// loads issued ahead of their products.
-template <typename E, typename V, typename AF, typename BF>
-__device__ __forceinline__ void mma_lds(V& acc, int K, int g, AF af, BF bf) {
-  for (int k0 = 0; k0 < K; k0 += 16) {
-    E x[4], y[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      x[u] = af(k0 + 4 * u + g);
-      y[u] = bf(k0 + 4 * u + g);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) acc = mfma4(x[u], y[u], acc);
-  }
-}
-
-// The same with B from global memory (K <= 128): all of the lane's B loads
-// are issued before the first product.
-template <typename E, typename V, typename AF, typename BF>
-__device__ __forceinline__ void mma_glb(V& acc, int K, int g, AF af, BF bf) {
-  float y[32];
-#pragma unroll
-  for (int s = 0; s < 32; ++s)
-    if (4 * s < K) y[s] = bf(4 * s + g);
-#pragma unroll
-  for (int s = 0; s < 32; ++s)
-    if (4 * s < K) acc = mfma4(af(4 * s + g), (E)y[s], acc);
-}
-
-__device__ __forceinline__ float4 ld4f(const float* p, size_t i) { return *reinterpret_cast<const float4*>(p + i); }
-__device__ __forceinline__ float4 ld4f(const uint16_t* p, size_t i) {
-  const uint2 x = *reinterpret_cast<const uint2*>(p + i);
-  return make_float4(__uint_as_float(x.x << 16), __uint_as_float(x.x & 0xffff0000u), __uint_as_float(x.y << 16),
-                     __uint_as_float(x.y & 0xffff0000u));
-}
-
 template <typename T>
 __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const T* __restrict__ k,
                                                  const T* __restrict__ v, const float* __restrict__ prefix,
@@ -471,6 +637,10 @@ __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const 
 }
 
 // ----------------------------------------------------------------------------
+static size_t summary1_lds(int chunk, int d, int dv) {
+  const size_t tb = chunk < 32 ? chunk : 32;
+  return sizeof(float) * ((size_t)chunk * (sum_ld(d) + sum_ld(dv)) + tb * (sum_ld(d) + sum_ld(chunk) + sum_ld(dv)) + tb);
+}
 static size_t summary_lds(int chunk, int d, int dv) {
   const size_t tb = chunk < 32 ? chunk : 32;
   return sizeof(float) * (2 * tb * sum_ld(d) + tb * sum_ld(dv) + tb * sum_ld((int)tb) + (size_t)chunk * sum_ld(dv) + tb);
@@ -484,16 +654,19 @@ hipError_t launch_chunk_summaries(const void* q, const void* k, const void* v, f
                                   int BH, int n, int d, int dv, int chunk, int dtype, hipStream_t s, float gamma) {
   const float lg2g = log2f(gamma);
   const int M = (n + chunk - 1) / chunk;
-  const size_t lds = summary_lds(chunk, d, dv);
+  // the one-pass kernel when the chunk's Q and V fit (and the m, h partials fit in A_row), else the block kernel
+  const size_t l1 = summary1_lds(chunk, d, dv);
+  const bool one = l1 <= 160 * 1024 && (size_t)(chunk < 32 ? chunk : 32) * sum_ld(chunk) >= 2 * kSumThreads;
+  const size_t lds = one ? l1 : summary_lds(chunk, d, dv);
   dim3 grid(M, BH), block(kSumThreads);
   if (dtype == 1) {
-    auto kern = k_chunk_summary<uint16_t>;
+    auto kern = one ? k_chunk_summary<uint16_t> : k_chunk_summary_blocks<uint16_t>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     HLA_LAUNCH(kern, grid, block, lds, s, (const uint16_t*)q, (const uint16_t*)k,
                        (const uint16_t*)v, states, n, d, dv, chunk, M, lg2g);
   } else {
-    auto kern = k_chunk_summary<float>;
+    auto kern = one ? k_chunk_summary<float> : k_chunk_summary_blocks<float>;
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     HLA_LAUNCH(kern, grid, block, lds, s, (const float*)q, (const float*)k, (const float*)v,
