@@ -289,6 +289,25 @@ def test_chunk_summaries_and_scan(dist):
         assert np.abs(got - exp).max() <= 1e-5 * max(np.abs(exp).max(), 1.0)
 
 
+@pytest.mark.parametrize("d,dv,chunk", [
+    (128, 128, 128),   # Q and V of the chunk exceed LDS: the block-restaging kernel
+    (128, 64, 128),
+    (64, 64, 128),     # one pass over four 32-token blocks
+    (16, 128, 16),     # a single 16-token block (block-restaging kernel)
+    (32, 16, 64),
+])
+def test_chunk_summaries_shapes(d, dv, chunk):
+    """Per-chunk summaries (S, C, m, G, h) of both summary kernels against
+    the oracle, ragged last chunk."""
+    B, H, n = 1, 2, 2 * chunk + 37
+    q, k, v, code = gen(B, H, n, d, dv, "scaled", 31)
+    _say(f"case summaries d={d} dv={dv} chunk={chunk}")
+    st = hla.chunk_summaries(dev(q, code), dev(k, code), dev(v, code), chunk)
+    ref = O.chunk_summaries(q, k, v, chunk)
+    for got, exp in zip((x.cpu().numpy() for x in hla.split_state(st, d, dv)), ref):
+        assert np.abs(got - exp).max() <= 1e-5 * np.abs(exp).max()
+
+
 @pytest.mark.parametrize("d", [16, 32, 64, 128])
 @pytest.mark.parametrize("with_init", [False, True])
 def test_scan_square_states(d, with_init):
