@@ -984,15 +984,15 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
   }
 
   // the segment's bracket: Phi0 into the G slot, eta0 into the h slot.  The
-  // opaque copy of the lane index keeps the store addresses from being
+  // opaque copies of the lane coordinates keep the store addresses from being
   // computed before the walk (they would stay live through it).
-  int col = ct * 32 + lr;
-  asm volatile("" : "+v"(col));
+  int col = ct * 32 + lr, lgo = lg;
+  asm volatile("" : "+v"(col), "+v"(lgo));
 #pragma unroll
   for (int i = 0; i < G::HT; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      rc[off_G(D, DV) + (size_t)(r0 + i * 32 + acc_row(e, lg)) * DV + col] = P0[i][e];
+      rc[off_G(D, DV) + (size_t)(r0 + i * 32 + acc_row(e, lgo)) * DV + col] = P0[i][e];
   if (tid < D) rc[off_h(D, DV) + tid] = eta[tid];
 }
 
