@@ -17,6 +17,7 @@
 // rho^2, the cross term by rho).  gamma = 1 is the undecayed operator: every
 // power below is exp2(0) = 1 exactly.
 #include "common.h"
+#include "mfma16.h"
 #include "profile.h"
 
 namespace hla {
@@ -44,49 +45,8 @@ namespace hla {
 constexpr int kSumThreads = 512, kSumWaves = kSumThreads / 64;
 constexpr int kSumTiles = 8;   // 16 x 16 tiles of S, C or G per wave: (128 / 16)^2 over 8 waves
 
-typedef float f32x4c __attribute__((ext_vector_type(4)));
-
 __host__ __device__ constexpr int sum_ld(int x) { return (x + 31) / 32 * 32 + 17; }
 
-__device__ __forceinline__ f32x4c mfma4(float a, float b, const f32x4c& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-typedef double f64x4c __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f64x4c mfma4(double a, double b, const f64x4c& c) {
-  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
-}
-
-// acc += sum_{k < K} A(k) B(k) for this lane's operands, K a multiple of 16,
-// af(k) = A[m0 + n][k], bf(k) = B[k][n0 + n]; both from LDS, four k steps'
-// loads issued ahead of their products.
-template <typename E, typename V, typename AF, typename BF>
-__device__ __forceinline__ void mma_lds(V& acc, int K, int g, AF af, BF bf) {
-  for (int k0 = 0; k0 < K; k0 += 16) {
-    E x[4], y[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      x[u] = af(k0 + 4 * u + g);
-      y[u] = bf(k0 + 4 * u + g);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) acc = mfma4(x[u], y[u], acc);
-  }
-}
-
-// The same with B from global memory (K <= 128): all of the lane's B loads
-// are issued before the first product.
-template <typename E, typename V, typename AF, typename BF>
-__device__ __forceinline__ void mma_glb(V& acc, int K, int g, AF af, BF bf) {
-  float y[32];
-#pragma unroll
-  for (int s = 0; s < 32; ++s)
-    if (4 * s < K) y[s] = bf(4 * s + g);
-#pragma unroll
-  for (int s = 0; s < 32; ++s)
-    if (4 * s < K) acc = mfma4(af(4 * s + g), (E)y[s], acc);
-}
 
 __device__ __forceinline__ float4 ld4f(const float* p, size_t i) { return *reinterpret_cast<const float4*>(p + i); }
 __device__ __forceinline__ float4 ld4f(const uint16_t* p, size_t i) {
@@ -447,10 +407,7 @@ __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const 
   extern __shared__ double smemd[];
   const int c = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
   const int w = tid >> 6, nn = tid & 15, g = (tid >> 4) & 3;
-  // The fp64 MFMA holds D[4 i + g][n] in element i (the fp32 one D[4 g + i][n]):
-  // lane n supplies A row pr = 4 (n % 4) + n / 4 instead of row n, so that the
-  // fp64 results arrive in the fp32 layout.
-  const int pr = 4 * (nn & 3) + (nn >> 2);
+  const int pr = mfma_pr(nn);        // fp64 A rows in the order that returns the fp32 layout
   const int t0 = c * chunk;
   const int L = min(chunk, n - t0), Lp = chunk, ld = d + 1, ldw = chunk + 1, ldv = dv + 1;
   const size_t qk_base = ((size_t)bh * n + t0) * d;

@@ -1,6 +1,6 @@
 // Masked third-order HLA forward (Sec. 7), fp32 arithmetic (dot products over
-// d accumulated in fp64) on fp32 or bf16 inputs, by the chunk-parallel scan of
-// Sec. 7.3 in a walk form.
+// d in fp64) on fp32 or bf16 inputs, by the chunk-parallel scan of Sec. 7.3 in
+// a walk form; the walks' products run on 16 x 16 MFMA tiles.
 //
 // The corrected state F_t = S^K S^Q P - G1 - G2 - G3 (Eq. hla3-corrected-state)
 // advances per token by (Eq. hla3-corrected-recurrence, with primes for the
@@ -35,6 +35,7 @@
 #include <cstdlib>
 
 #include "hla3.h"
+#include "mfma16.h"
 #include "profile.h"
 
 namespace hla {
@@ -133,34 +134,44 @@ __global__ __launch_bounds__(kT3) void k3_prefix(const float* __restrict__ rec, 
 }
 
 // 2. The walk of one segment from its moment carry with F = 0.  grid (nseg, BH).
+// Every product of a tile runs on 16 x 16 MFMA tiles, one per wave at a time:
+// the dot products over d (Q K^T, Q SK0, Q P0, Q F0, Q R^T) in fp64
+// (v_mfma_f64_16x16x4_f64, fp32 operands widened exactly), the products over
+// the tile's tokens (the prefixes R and Pq, the outputs, the moment and F
+// advances) in fp32 (v_mfma_f32_16x16x4_f32), as the arithmetic of the
+// recurrence asks; products with a causal mask stop at the diagonal tile.
 template <typename T, int C, int D, int DV>
 __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T* __restrict__ k,
                                                const T* __restrict__ v, float* __restrict__ out,
                                                float* __restrict__ den_out, float* __restrict__ rec,
                                                const float* __restrict__ pre, int n, int cps, int nseg) {
   using Rc = Rec3<D, DV>;
-  constexpr int lD = D + 1, lV = DV + 1, lC = C + 1;
+  constexpr int lD = D + 1, lV = DV + 1, lC = C + 1, NW = kT3 / 64;
+  constexpr int ct = C / 16, dt = D / 16, vt = DV / 16;
   __shared__ float Qs[C * lD], Ks[C * lD], Vs[C * lV];
   __shared__ float SK[D * lD], SQ[D * lD], Pm[D * lV], mv[D], F[D * lV], eta[D];
   __shared__ float A[C * lC], R[C * lD], Tm[C * lC], QSK[C * lD], QP[C * lV], QF[C * lV], Pq[C * lV], X[C * lV];
   __shared__ float sig[C], dl[C], pm[C], xv[C], qeta[C];
   const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, nn = tid & 15, g = (tid >> 4) & 3, pr = mfma_pr(nn);
   const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
   const size_t head_tok = (size_t)bh * n;
   float* recs = rec + (size_t)bh * nseg * Rc::floats;
+  const f32x4c zf = {0.f, 0.f, 0.f, 0.f};
+  const f64x4c zd = {0.0, 0.0, 0.0, 0.0};
 
   // moment carry: the sum of the segments before this one (k3_prefix); F = eta = 0
-  const float* pr = pre + ((size_t)bh * nseg + seg) * Rc::floats;
+  const float* prc = pre + ((size_t)bh * nseg + seg) * Rc::floats;
   for (int e = tid; e < D * D; e += kT3) {
-    SK[(e / D) * lD + e % D] = pr[Rc::oSK + e];
-    SQ[(e / D) * lD + e % D] = pr[Rc::oSQ + e];
+    SK[(e / D) * lD + e % D] = prc[Rc::oSK + e];
+    SQ[(e / D) * lD + e % D] = prc[Rc::oSQ + e];
   }
   for (int e = tid; e < D * DV; e += kT3) {
-    Pm[(e / DV) * lV + e % DV] = pr[Rc::oP + e];
+    Pm[(e / DV) * lV + e % DV] = prc[Rc::oP + e];
     F[(e / DV) * lV + e % DV] = 0.f;
   }
   for (int e = tid; e < D; e += kT3) {
-    mv[e] = pr[Rc::om + e];
+    mv[e] = prc[Rc::om + e];
     eta[e] = 0.f;
   }
 
@@ -168,33 +179,32 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
     const int t0 = c * C;
     stage_tile<T, C, D, DV>(q, k, v, head_tok, t0, n, Qs, Ks, Vs);
     __syncthreads();
-    // s1: A = Q K^T, Q SK0, Q P0, Q F0, q.m0, q.eta0, k^T SQ0 k.  Dot products
-    // over d accumulate in fp64 (products of fp32 values are exact there): a
-    // row such as o_1 = (q_1.k_1)^3 v_1 amplifies the cancellation of q.k.
-    for (int e = tid; e < C * C; e += kT3) {
-      const int t = e / C, i = e % C;
-      double s = 0.0;
-#pragma unroll 8
-      for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * Ks[i * lD + a];
-      A[t * lC + i] = (float)s;
-    }
-    for (int e = tid; e < C * D; e += kT3) {
-      const int t = e / D, b = e % D;
-      double s = 0.0;
-#pragma unroll 8
-      for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * SK[a * lD + b];
-      QSK[t * lD + b] = (float)s;
-    }
-    for (int e = tid; e < C * DV; e += kT3) {
-      const int t = e / DV, b = e % DV;
-      double s = 0.0, f = 0.0;
-#pragma unroll 8
-      for (int a = 0; a < D; ++a) {
-        s += (double)Qs[t * lD + a] * Pm[a * lV + b];
-        f += (double)Qs[t * lD + a] * F[a * lV + b];
+    // s1: A = Q K^T (every tile: its upper part feeds sigma), Q SK0, Q P0, Q F0
+    // in fp64 (a row such as o_1 = (q_1.k_1)^3 v_1 amplifies the cancellation
+    // of q.k); q.m0, q.eta0 and k^T SQ0 k per token
+    {
+      constexpr int nA = ct * ct, nS = ct * dt, nP = ct * vt;
+      for (int tile = w; tile < nA + nS + 2 * nP; tile += NW) {
+        f64x4c acc = zd;
+        float* dst;
+        int ldd, mm, n0;
+        auto aq = [&](int kk) { return (double)Qs[(mm + pr) * lD + kk]; };
+        if (tile < nA) {
+          mm = 16 * (tile / ct), n0 = 16 * (tile % ct), dst = A, ldd = lC;
+          mma_lds<double>(acc, D, g, aq, [&](int kk) { return (double)Ks[(n0 + nn) * lD + kk]; });
+        } else if (tile < nA + nS) {
+          const int u = tile - nA;
+          mm = 16 * (u / dt), n0 = 16 * (u % dt), dst = QSK, ldd = lD;
+          mma_lds<double>(acc, D, g, aq, [&](int kk) { return (double)SK[kk * lD + n0 + nn]; });
+        } else {
+          const int u = tile - nA - nS, uu = u % nP;
+          const float* B = u < nP ? Pm : F;
+          mm = 16 * (uu / vt), n0 = 16 * (uu % vt), dst = u < nP ? QP : QF, ldd = lV;
+          mma_lds<double>(acc, D, g, aq, [&](int kk) { return (double)B[kk * lV + n0 + nn]; });
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[(mm + 4 * g + i) * ldd + n0 + nn] = (float)acc[i];
       }
-      QP[t * lV + b] = (float)s;
-      QF[t * lV + b] = (float)f;
     }
     // per token t: q_t.m0, q_t.eta0 and k_t^T SQ0 k_t, one lane per (t, a) and
     // the sum over a across D consecutive lanes (D divides the wave)
@@ -204,54 +214,76 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
       double y = 0.0;
 #pragma unroll
       for (int b = 0; b < D; ++b) y += (double)SQ[a * lD + b] * Ks[t * lD + b];
-      double g = (double)Ks[t * lD + a] * y, sm = (double)Qs[t * lD + a] * mv[a], w = (double)Qs[t * lD + a] * eta[a];
+      double gq = (double)Ks[t * lD + a] * y, sm = (double)Qs[t * lD + a] * mv[a], wq = (double)Qs[t * lD + a] * eta[a];
 #pragma unroll
       for (int o = 1; o < D; o <<= 1) {
-        g += __shfl_xor(g, o);
+        gq += __shfl_xor(gq, o);
         sm += __shfl_xor(sm, o);
-        w += __shfl_xor(w, o);
+        wq += __shfl_xor(wq, o);
       }
       if (a == 0) {
         pm[t] = (float)sm;
-        qeta[t] = (float)w;
-        sig[t] = (float)g;
+        qeta[t] = (float)wq;
+        sig[t] = (float)gq;
       }
     }
     __syncthreads();
-    // s2: prefixes inside the tile (strictly before j)
-    for (int e = tid; e < C * D; e += kT3) {
-      const int j = e / D, b = e % D;
-      float s = QSK[j * lD + b];
-      for (int i = 0; i < j; ++i) s += A[j * lC + i] * Ks[i * lD + b];
-      R[j * lD + b] = s;
-    }
-    for (int e = tid; e < C * DV; e += kT3) {
-      const int j = e / DV, b = e % DV;
-      float s = QP[j * lV + b];
-      for (int i = 0; i < j; ++i) s += A[j * lC + i] * Vs[i * lV + b];
-      Pq[j * lV + b] = s;
-    }
-    for (int j = tid; j < C; j += kT3) {
-      float s = sig[j], p = pm[j];
-      for (int u = 0; u < j; ++u) {
-        const float a = A[u * lC + j];
-        s += a * a;
-        p += A[j * lC + u];
+    // s2: prefixes inside the tile (strictly before j), in fp32:
+    //   R = Q SK0 + (A (.) Ls) K,  Pq = Q P0 + (A (.) Ls) V,
+    //   sigma_j += sum_{u<j} A_uj^2,  pm_j += sum_{u<j} A_ju,  delta_j = A_jj
+    {
+      constexpr int nS = ct * dt, nP = ct * vt;
+      for (int tile = w; tile < nS + nP; tile += NW) {
+        const bool isR = tile < nS;
+        const int u = isR ? tile : tile - nS, cn = isR ? dt : vt, mm = 16 * (u / cn), n0 = 16 * (u % cn);
+        const float* init = isR ? QSK : QP;
+        const float* B = isR ? Ks : Vs;
+        const int li = isR ? lD : lV;
+        f32x4c acc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = init[(mm + 4 * g + i) * li + n0 + nn];
+        mma_lds<float>(acc, mm + 16, g, [&](int kk) { return kk < mm + nn ? A[(mm + nn) * lC + kk] : 0.f; },
+                       [&](int kk) { return B[kk * li + n0 + nn]; });
+        float* dst = isR ? R : Pq;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[(mm + 4 * g + i) * li + n0 + nn] = acc[i];
       }
-      sig[j] = s;
-      pm[j] = p;
-      dl[j] = A[j * lC + j];
+      const int j = tid >> 3, p = tid & 7;
+      float s2 = 0.f, p2 = 0.f;
+      if (j < C)
+        for (int uu = p; uu < j; uu += 8) {
+          const float a = A[uu * lC + j];
+          s2 += a * a;
+          p2 += A[j * lC + uu];
+        }
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) {
+        s2 += __shfl_xor(s2, o);
+        p2 += __shfl_xor(p2, o);
+      }
+      if (p == 0 && j < C) {
+        sig[j] += s2;
+        pm[j] += p2;
+        dl[j] = A[j * lC + j];
+      }
     }
     __syncthreads();
-    // s3: T = (Q R^T) (.) L, X, x
-    for (int e = tid; e < C * C; e += kT3) {
-      const int t = e / C, j = e % C;
-      double s = 0.0;
-      if (j <= t) {
-#pragma unroll 8
-        for (int b = 0; b < D; ++b) s += (double)Qs[t * lD + b] * R[j * lD + b];
+    // s3: T = (Q R^T) (.) L in fp64 (tiles on or below the diagonal), X, x
+    {
+      constexpr int nT = ct * (ct + 1) / 2;
+      for (int tile = w; tile < nT; tile += NW) {
+        int mi = 0;
+        while ((mi + 1) * (mi + 2) / 2 <= tile) ++mi;
+        const int mm = 16 * mi, n0 = 16 * (tile - mi * (mi + 1) / 2);
+        f64x4c acc = zd;
+        mma_lds<double>(acc, D, g, [&](int kk) { return (double)Qs[(mm + pr) * lD + kk]; },
+                        [&](int kk) { return (double)R[(n0 + nn) * lD + kk]; });
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = mm + 4 * g + i, j = n0 + nn;
+          Tm[t * lC + j] = j <= t ? (float)acc[i] : 0.f;
+        }
       }
-      Tm[t * lC + j] = (float)s;
     }
     for (int e = tid; e < C * DV; e += kT3) {
       const int j = e / DV, b = e % DV;
@@ -263,46 +295,78 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
       xv[j] = sig[j] + d0 * d0 + d0 * pm[j];
     }
     __syncthreads();
-    // s4: outputs without the F carry of earlier segments, then the advance
-    for (int e = tid; e < C * DV; e += kT3) {
-      const int t = e / DV, b = e % DV;
-      float s = QF[t * lV + b];
-      for (int j = 0; j <= t; ++j) s += Tm[t * lC + j] * dl[j] * Vs[j * lV + b] + A[t * lC + j] * X[j * lV + b];
-      if (t0 + t < n) out[(head_tok + t0 + t) * DV + b] = s;
-    }
-    for (int t = tid; t < C; t += kT3) {
-      float s = qeta[t];
-      for (int j = 0; j <= t; ++j) s += Tm[t * lC + j] * dl[j] + A[t * lC + j] * xv[j];
-      if (t0 + t < n) den_out[head_tok + t0 + t] = s;
-    }
-    for (int e = tid; e < D * DV; e += kT3) {
-      const int a = e / DV, b = e % DV;
-      float f = 0.f, p = 0.f;
-      for (int j = 0; j < C; ++j) {
-        f += R[j * lD + a] * dl[j] * Vs[j * lV + b] + Ks[j * lD + a] * X[j * lV + b];
-        p += Ks[j * lD + a] * Vs[j * lV + b];
+    // s4: outputs without the F carry of earlier segments, then the advances,
+    // all in fp32: num = Q F0 + (T diag(delta)) V + (A (.) L) X, and
+    // F0 += R^T (delta (.) V) + K^T X, P0 += K^T V, SK0 += K^T K, SQ0 += Q^T Q
+    {
+      constexpr int nO = ct * vt, nF = dt * vt, nQ = dt * dt;
+      for (int tile = w; tile < nO + 2 * nF + 2 * nQ; tile += NW) {
+        f32x4c acc;
+        if (tile < nO) {
+          const int mm = 16 * (tile / vt), n0 = 16 * (tile % vt);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = QF[(mm + 4 * g + i) * lV + n0 + nn];
+          mma_lds<float>(acc, mm + 16, g, [&](int kk) { return Tm[(mm + nn) * lC + kk] * dl[kk]; },
+                         [&](int kk) { return Vs[kk * lV + n0 + nn]; });
+          mma_lds<float>(acc, mm + 16, g, [&](int kk) { return kk <= mm + nn ? A[(mm + nn) * lC + kk] : 0.f; },
+                         [&](int kk) { return X[kk * lV + n0 + nn]; });
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int t = mm + 4 * g + i;
+            if (t0 + t < n) out[(head_tok + t0 + t) * DV + n0 + nn] = acc[i];
+          }
+        } else if (tile < nO + 2 * nF) {
+          const bool isF = tile < nO + nF;
+          const int u = isF ? tile - nO : tile - nO - nF, a0 = 16 * (u / vt), b0 = 16 * (u % vt);
+          float* S = isF ? F : Pm;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = S[(a0 + 4 * g + i) * lV + b0 + nn];
+          if (isF) {
+            mma_lds<float>(acc, C, g, [&](int kk) { return R[kk * lD + a0 + nn]; },
+                           [&](int kk) { return dl[kk] * Vs[kk * lV + b0 + nn]; });
+            mma_lds<float>(acc, C, g, [&](int kk) { return Ks[kk * lD + a0 + nn]; },
+                           [&](int kk) { return X[kk * lV + b0 + nn]; });
+          } else {
+            mma_lds<float>(acc, C, g, [&](int kk) { return Ks[kk * lD + a0 + nn]; },
+                           [&](int kk) { return Vs[kk * lV + b0 + nn]; });
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) S[(a0 + 4 * g + i) * lV + b0 + nn] = acc[i];
+        } else {
+          const bool isK = tile < nO + 2 * nF + nQ;
+          const int u = isK ? tile - nO - 2 * nF : tile - nO - 2 * nF - nQ, a0 = 16 * (u / dt), b0 = 16 * (u % dt);
+          float* S = isK ? SK : SQ;
+          const float* Y = isK ? Ks : Qs;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = S[(a0 + 4 * g + i) * lD + b0 + nn];
+          mma_lds<float>(acc, C, g, [&](int kk) { return Y[kk * lD + a0 + nn]; },
+                         [&](int kk) { return Y[kk * lD + b0 + nn]; });
+#pragma unroll
+          for (int i = 0; i < 4; ++i) S[(a0 + 4 * g + i) * lD + b0 + nn] = acc[i];
+        }
       }
-      F[a * lV + b] += f;
-      Pm[a * lV + b] += p;
     }
-    for (int e = tid; e < D * D; e += kT3) {
-      const int a = e / D, b = e % D;
-      float sk = 0.f, sq = 0.f;
-      for (int j = 0; j < C; ++j) {
-        sk += Ks[j * lD + a] * Ks[j * lD + b];
-        sq += Qs[j * lD + a] * Qs[j * lD + b];
+    {  // den (eight lanes per token) and the eta0, m0 advances (eight lanes per dimension)
+      const int r = tid >> 3, p = tid & 7;
+      float sd = 0.f, e2 = 0.f, sm = 0.f;
+      if (r < C)
+        for (int j = p; j <= r; j += 8) sd += Tm[r * lC + j] * dl[j] + A[r * lC + j] * xv[j];
+      if (r < D)
+        for (int j = p; j < C; j += 8) {
+          e2 += R[j * lD + r] * dl[j] + Ks[j * lD + r] * xv[j];
+          sm += Ks[j * lD + r];
+        }
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) {
+        sd += __shfl_xor(sd, o);
+        e2 += __shfl_xor(e2, o);
+        sm += __shfl_xor(sm, o);
       }
-      SK[a * lD + b] += sk;
-      SQ[a * lD + b] += sq;
-    }
-    for (int a = tid; a < D; a += kT3) {
-      float e2 = 0.f, s = 0.f;
-      for (int j = 0; j < C; ++j) {
-        e2 += R[j * lD + a] * dl[j] + Ks[j * lD + a] * xv[j];
-        s += Ks[j * lD + a];
+      if (p == 0 && r < C && t0 + r < n) den_out[head_tok + t0 + r] = qeta[r] + sd;
+      if (p == 0 && r < D) {
+        eta[r] += e2;
+        mv[r] += sm;
       }
-      eta[a] += e2;
-      mv[a] += s;
     }
     __syncthreads();
   }
@@ -361,139 +425,189 @@ __global__ __launch_bounds__(kT3) void k3_fix(const T* __restrict__ q, float* __
 //   Sm  = R SQ0 + (L (.) R Q^T) Q             (row t: q_t^T S^K_t S^Q_t)
 //   O   = Sm P0 + (L (.) Sm K^T) V,   den = Sm m0 + (L (.) Sm K^T) 1.
 // The summaries only add, so a segment's walk from the moment prefix gives
-// its outputs whole: no bracket and no fix-up.  Dot products accumulate in
-// fp64; R and Sm are kept in fp64.  grid (nseg, BH).
+// its outputs whole: no bracket and no fix-up.  The products of R, U, Sm,
+// Tm and O run on fp64 MFMA tiles (fp32 operands widened exactly) and R, Sm
+// are kept in fp64; the moment advances on fp32 MFMA.  grid (nseg, BH).
 template <typename T, int C, int D, int DV>
 __global__ __launch_bounds__(kT3) void k3u_walk(const T* __restrict__ q, const T* __restrict__ k,
                                                 const T* __restrict__ v, float* __restrict__ out,
                                                 const float* __restrict__ pre, int n, int cps, int nseg,
                                                 int normalized, float eps) {
   using Rc = Rec3<D, DV>;
-  constexpr int lD = D + 1, lV = DV + 1, lC = C + 1;
+  constexpr int lD = D + 1, lV = DV + 1, lC = C + 1, NW = kT3 / 64;
+  constexpr int ct = C / 16, dt = D / 16, vt = DV / 16, nW = ct * (ct + 1) / 2, nR = ct * dt, nO = ct * vt;
   __shared__ float Qs[C * lD], Ks[C * lD], Vs[C * lV];
   __shared__ float SK[D * lD], SQ[D * lD], Pm[D * lV], mv[D];
   __shared__ float W[C * lC], U[C * lC], Tm[C * lC];
   __shared__ double R[C * lD], Sm[C * lD], dn[C];
   const int seg = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int w = tid >> 6, nn = tid & 15, g = (tid >> 4) & 3, pr = mfma_pr(nn);
   const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
   const size_t head_tok = (size_t)bh * n;
+  const f64x4c zd = {0.0, 0.0, 0.0, 0.0};
+  // tile `tile` of the lower triangle of C x C tiles: rows mm, columns n0
+  auto lower = [&](int tile, int& mm, int& n0) {
+    int mi = 0;
+    while ((mi + 1) * (mi + 2) / 2 <= tile) ++mi;
+    mm = 16 * mi;
+    n0 = 16 * (tile - mi * (mi + 1) / 2);
+  };
 
-  const float* pr = pre + ((size_t)bh * nseg + seg) * Rc::floats;   // moments of the segments before
+  const float* prc = pre + ((size_t)bh * nseg + seg) * Rc::floats;   // moments of the segments before
   for (int e = tid; e < D * D; e += kT3) {
-    SK[(e / D) * lD + e % D] = pr[Rc::oSK + e];
-    SQ[(e / D) * lD + e % D] = pr[Rc::oSQ + e];
+    SK[(e / D) * lD + e % D] = prc[Rc::oSK + e];
+    SQ[(e / D) * lD + e % D] = prc[Rc::oSQ + e];
   }
-  for (int e = tid; e < D * DV; e += kT3) Pm[(e / DV) * lV + e % DV] = pr[Rc::oP + e];
-  for (int e = tid; e < D; e += kT3) mv[e] = pr[Rc::om + e];
+  for (int e = tid; e < D * DV; e += kT3) Pm[(e / DV) * lV + e % DV] = prc[Rc::oP + e];
+  for (int e = tid; e < D; e += kT3) mv[e] = prc[Rc::om + e];
 
   for (int c = c0; c < c1; ++c) {
     const int t0 = c * C;
     stage_tile<T, C, D, DV>(q, k, v, head_tok, t0, n, Qs, Ks, Vs);
     __syncthreads();
     // W = L (.) Q K^T;  R = Q SK0 (first part)
-    for (int e = tid; e < C * C; e += kT3) {
-      const int t = e / C, i = e % C;
-      double s = 0.0;
-      if (i <= t) {
-#pragma unroll 8
-        for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * Ks[i * lD + a];
+    for (int tile = w; tile < nW + nR; tile += NW) {
+      f64x4c acc = zd;
+      int mm, n0;
+      if (tile < nW) {
+        lower(tile, mm, n0);
+        mma_lds<double>(acc, D, g, [&](int kk) { return (double)Qs[(mm + pr) * lD + kk]; },
+                        [&](int kk) { return (double)Ks[(n0 + nn) * lD + kk]; });
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = mm + 4 * g + i, j = n0 + nn;
+          W[t * lC + j] = j <= t ? (float)acc[i] : 0.f;
+        }
+      } else {
+        const int u = tile - nW;
+        mm = 16 * (u / dt), n0 = 16 * (u % dt);
+        mma_lds<double>(acc, D, g, [&](int kk) { return (double)Qs[(mm + pr) * lD + kk]; },
+                        [&](int kk) { return (double)SK[kk * lD + n0 + nn]; });
+#pragma unroll
+        for (int i = 0; i < 4; ++i) R[(mm + 4 * g + i) * lD + n0 + nn] = acc[i];
       }
-      W[t * lC + i] = (float)s;
-    }
-    for (int e = tid; e < C * D; e += kT3) {
-      const int t = e / D, b = e % D;
-      double s = 0.0;
-#pragma unroll 8
-      for (int a = 0; a < D; ++a) s += (double)Qs[t * lD + a] * SK[a * lD + b];
-      R[t * lD + b] = s;
     }
     __syncthreads();
     // R += W K
-    for (int e = tid; e < C * D; e += kT3) {
-      const int t = e / D, b = e % D;
-      double s = R[t * lD + b];
-      for (int i = 0; i <= t; ++i) s += (double)W[t * lC + i] * Ks[i * lD + b];
-      R[t * lD + b] = s;
+    for (int tile = w; tile < nR; tile += NW) {
+      const int mm = 16 * (tile / dt), n0 = 16 * (tile % dt);
+      f64x4c acc;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] = R[(mm + 4 * g + i) * lD + n0 + nn];
+      mma_lds<double>(acc, mm + 16, g, [&](int kk) { return (double)W[(mm + pr) * lC + kk]; },
+                      [&](int kk) { return (double)Ks[kk * lD + n0 + nn]; });
+#pragma unroll
+      for (int i = 0; i < 4; ++i) R[(mm + 4 * g + i) * lD + n0 + nn] = acc[i];
     }
     __syncthreads();
     // U = L (.) R Q^T
-    for (int e = tid; e < C * C; e += kT3) {
-      const int t = e / C, u = e % C;
-      double s = 0.0;
-      if (u <= t) {
-#pragma unroll 8
-        for (int b = 0; b < D; ++b) s += R[t * lD + b] * Qs[u * lD + b];
+    for (int tile = w; tile < nW; tile += NW) {
+      int mm, n0;
+      lower(tile, mm, n0);
+      f64x4c acc = zd;
+      mma_lds<double>(acc, D, g, [&](int kk) { return R[(mm + pr) * lD + kk]; },
+                      [&](int kk) { return (double)Qs[(n0 + nn) * lD + kk]; });
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = mm + 4 * g + i, u = n0 + nn;
+        U[t * lC + u] = u <= t ? (float)acc[i] : 0.f;
       }
-      U[t * lC + u] = (float)s;
     }
     __syncthreads();
     // Sm = R SQ0 + U Q
-    for (int e = tid; e < C * D; e += kT3) {
-      const int t = e / D, b = e % D;
-      double s = 0.0;
-#pragma unroll 8
-      for (int a = 0; a < D; ++a) s += R[t * lD + a] * SQ[a * lD + b];
-      for (int u = 0; u <= t; ++u) s += (double)U[t * lC + u] * Qs[u * lD + b];
-      Sm[t * lD + b] = s;
+    for (int tile = w; tile < nR; tile += NW) {
+      const int mm = 16 * (tile / dt), n0 = 16 * (tile % dt);
+      f64x4c acc = zd;
+      mma_lds<double>(acc, D, g, [&](int kk) { return R[(mm + pr) * lD + kk]; },
+                      [&](int kk) { return (double)SQ[kk * lD + n0 + nn]; });
+      mma_lds<double>(acc, mm + 16, g, [&](int kk) { return (double)U[(mm + pr) * lC + kk]; },
+                      [&](int kk) { return (double)Qs[kk * lD + n0 + nn]; });
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Sm[(mm + 4 * g + i) * lD + n0 + nn] = acc[i];
     }
     __syncthreads();
-    // Tm = L (.) Sm K^T;  the carry part of den
-    for (int e = tid; e < C * C; e += kT3) {
-      const int t = e / C, j = e % C;
-      double s = 0.0;
-      if (j <= t) {
-#pragma unroll 8
-        for (int b = 0; b < D; ++b) s += Sm[t * lD + b] * Ks[j * lD + b];
+    // Tm = L (.) Sm K^T;  the carry part of den (eight lanes per token)
+    for (int tile = w; tile < nW; tile += NW) {
+      int mm, n0;
+      lower(tile, mm, n0);
+      f64x4c acc = zd;
+      mma_lds<double>(acc, D, g, [&](int kk) { return Sm[(mm + pr) * lD + kk]; },
+                      [&](int kk) { return (double)Ks[(n0 + nn) * lD + kk]; });
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = mm + 4 * g + i, j = n0 + nn;
+        Tm[t * lC + j] = j <= t ? (float)acc[i] : 0.f;
       }
-      Tm[t * lC + j] = (float)s;
     }
-    for (int t = tid; t < C; t += kT3) {
+    {
+      const int t = tid >> 3, p = tid & 7;
       double s = 0.0;
-      for (int a = 0; a < D; ++a) s += Sm[t * lD + a] * mv[a];
-      dn[t] = s;
+      if (t < C)
+        for (int a = p; a < D; a += 8) s += Sm[t * lD + a] * mv[a];
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) s += __shfl_xor(s, o);
+      if (p == 0 && t < C) dn[t] = s;
     }
     __syncthreads();
-    if (normalized)
-      for (int t = tid; t < C; t += kT3) {
-        double s = dn[t];
-        for (int j = 0; j <= t; ++j) s += Tm[t * lC + j];
-        dn[t] = s;
-      }
-    __syncthreads();
+    if (normalized) {
+      const int t = tid >> 3, p = tid & 7;
+      double s = 0.0;
+      if (t < C)
+        for (int j = p; j <= t; j += 8) s += Tm[t * lC + j];
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) s += __shfl_xor(s, o);
+      if (p == 0 && t < C) dn[t] += s;
+      __syncthreads();
+    }
     // O = Sm P0 + Tm V
-    for (int e = tid; e < C * DV; e += kT3) {
-      const int t = e / DV, b = e % DV;
-      if (t0 + t >= n) continue;
-      double s = 0.0;
-#pragma unroll 8
-      for (int a = 0; a < D; ++a) s += Sm[t * lD + a] * Pm[a * lV + b];
-      for (int j = 0; j <= t; ++j) s += (double)Tm[t * lC + j] * Vs[j * lV + b];
-      float y = (float)s;
-      if (normalized) y = (float)(s / (dn[t] + (double)eps));
-      out[(head_tok + t0 + t) * DV + b] = y;
+    for (int tile = w; tile < nO; tile += NW) {
+      const int mm = 16 * (tile / vt), n0 = 16 * (tile % vt);
+      f64x4c acc = zd;
+      mma_lds<double>(acc, D, g, [&](int kk) { return Sm[(mm + pr) * lD + kk]; },
+                      [&](int kk) { return (double)Pm[kk * lV + n0 + nn]; });
+      mma_lds<double>(acc, mm + 16, g, [&](int kk) { return (double)Tm[(mm + pr) * lC + kk]; },
+                      [&](int kk) { return (double)Vs[kk * lV + n0 + nn]; });
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = mm + 4 * g + i;
+        if (t0 + t < n)
+          out[(head_tok + t0 + t) * DV + n0 + nn] = normalized ? (float)(acc[i] / (dn[t] + (double)eps)) : (float)acc[i];
+      }
     }
     __syncthreads();
-    // advance the moments past this tile
-    for (int e = tid; e < D * DV; e += kT3) {
-      const int a = e / DV, b = e % DV;
-      float p = 0.f;
-      for (int j = 0; j < C; ++j) p += Ks[j * lD + a] * Vs[j * lV + b];
-      Pm[a * lV + b] += p;
-    }
-    for (int e = tid; e < D * D; e += kT3) {
-      const int a = e / D, b = e % D;
-      float sk = 0.f, sq = 0.f;
-      for (int j = 0; j < C; ++j) {
-        sk += Ks[j * lD + a] * Ks[j * lD + b];
-        sq += Qs[j * lD + a] * Qs[j * lD + b];
+    // advance the moments past this tile: P0 += K^T V, SK0 += K^T K, SQ0 += Q^T Q (fp32), m0 += K^T 1
+    {
+      constexpr int nF = dt * vt, nQ = dt * dt;
+      for (int tile = w; tile < nF + 2 * nQ; tile += NW) {
+        f32x4c acc;
+        if (tile < nF) {
+          const int a0 = 16 * (tile / vt), b0 = 16 * (tile % vt);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = Pm[(a0 + 4 * g + i) * lV + b0 + nn];
+          mma_lds<float>(acc, C, g, [&](int kk) { return Ks[kk * lD + a0 + nn]; },
+                         [&](int kk) { return Vs[kk * lV + b0 + nn]; });
+#pragma unroll
+          for (int i = 0; i < 4; ++i) Pm[(a0 + 4 * g + i) * lV + b0 + nn] = acc[i];
+        } else {
+          const bool isK = tile < nF + nQ;
+          const int u = isK ? tile - nF : tile - nF - nQ, a0 = 16 * (u / dt), b0 = 16 * (u % dt);
+          float* S = isK ? SK : SQ;
+          const float* Y = isK ? Ks : Qs;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[i] = S[(a0 + 4 * g + i) * lD + b0 + nn];
+          mma_lds<float>(acc, C, g, [&](int kk) { return Y[kk * lD + a0 + nn]; },
+                         [&](int kk) { return Y[kk * lD + b0 + nn]; });
+#pragma unroll
+          for (int i = 0; i < 4; ++i) S[(a0 + 4 * g + i) * lD + b0 + nn] = acc[i];
+        }
       }
-      SK[a * lD + b] += sk;
-      SQ[a * lD + b] += sq;
-    }
-    for (int a = tid; a < D; a += kT3) {
-      float s = 0.f;
-      for (int j = 0; j < C; ++j) s += Ks[j * lD + a];
-      mv[a] += s;
+      const int a = tid >> 3, p = tid & 7;
+      float sm = 0.f;
+      if (a < D)
+        for (int j = p; j < C; j += 8) sm += Ks[j * lD + a];
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) sm += __shfl_xor(sm, o);
+      if (p == 0 && a < D) mv[a] += sm;
     }
     __syncthreads();
   }
