@@ -186,6 +186,22 @@ def test_fused_d128_segment_counts(segments, monkeypatch):
     assert _check_forward(2, 1, 64 * 9 + 20, 128, 128, 128, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=13)
 
 
+@pytest.mark.parametrize("B,H,n", [
+    (1, 1, 64),        # one tile: a single output walk
+    (1, 3, 130),       # three one-tile segments
+    (2, 5, 777),       # 13 segments of one tile
+    (1, 100, 200),     # two walks per head: segments of 1, 2 and 1 tiles
+    (3, 50, 300),      # more than 128 heads: a single walk per head
+    (1, 40, 2000),     # seven segments, segment 0 shorter than the others
+    (4, 16, 640),      # four segments of 2, 3, 3 and 2 tiles
+])
+def test_fused_d128_plan_sweep(B, H, n):
+    """The d = 128 two-pass plan over head counts and lengths that give
+    every plan shape (the plan query reports each); normalised, num and den
+    against the oracle on every head."""
+    assert _check_forward(B, H, n, 128, 128, 128, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=29)
+
+
 @pytest.mark.parametrize("ratio", ["0.2", "1.0", "2.5"])
 def test_fused_d128_first_segment_length(ratio, monkeypatch):
     """Nor on the length of segment 0 against the others (HLA_WS_RATIO), at
