@@ -438,6 +438,13 @@ __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const 
   const f64x4c zd = {0.0, 0.0, 0.0, 0.0};
   const f32x4c zf = {0.f, 0.f, 0.f, 0.f};
 
+  // V's loads go out first; V is written to LDS only once R is dead
+  float4 pvr[4];     // Lp dv / 4 <= 2048 pieces over 512 threads
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int idx = tid + 512 * i, t = idx / (dv / 4), b = (idx % (dv / 4)) * 4;
+    pvr[i] = idx < Lp * dv / 4 && t < L ? ld4f(v, v_base + (size_t)t * dv + b) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   for (int idx = tid; idx < Lp * d / 4; idx += blockDim.x) {
     const int t = idx / (d / 4), a = (idx % (d / 4)) * 4;
     const float4 xq = t < L ? ld4f(q, qk_base + (size_t)t * d + a) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -554,11 +561,13 @@ __global__ __launch_bounds__(512) void k_readout(const T* __restrict__ q, const 
   }
   __syncthreads();
   // V into the space of R (rows past the chunk's tokens zero); the rows' denominators
-  for (int idx = tid; idx < Lp * dv / 4; idx += blockDim.x) {
-    const int t = idx / (dv / 4), b = (idx % (dv / 4)) * 4;
-    const float4 x = t < L ? ld4f(v, v_base + (size_t)t * dv + b) : make_float4(0.f, 0.f, 0.f, 0.f);
-    float* pv = Vs + t * ldv + b;
-    pv[0] = x.x; pv[1] = x.y; pv[2] = x.z; pv[3] = x.w;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int idx = tid + 512 * i;
+    if (idx < Lp * dv / 4) {
+      float* pv = Vs + (idx / (dv / 4)) * ldv + (idx % (dv / 4)) * 4;
+      pv[0] = pvr[i].x; pv[1] = pvr[i].y; pv[2] = pvr[i].z; pv[3] = pvr[i].w;
+    }
   }
   if (normalized) {
     const int t = tid >> 3, p = tid & 7;
