@@ -17,6 +17,10 @@
 // With an initial state, k_init_convert converts it to the (S, C, m, Phi, eta)
 // form first; k_total sums all records into the final state when a caller
 // asks for it.  k_moments, k_carry and k_fix live in fused_tiles.h.
+// At d = dv = 128 without states the forward takes the two-pass plan of
+// fused_ws.h instead (run_ws): segment 0's output walk beside the summary
+// walks of the later segments, the brackets, then the other segments' output
+// walks from their true carries, so that every output row is written once.
 //
 // Per chunk (tokens of the chunk as the rows of Q, K, V; S0, Phi0, eta0 the
 // carry of the chunk), with r_j = S_j q_j (the proof of Thm. 1 sums
