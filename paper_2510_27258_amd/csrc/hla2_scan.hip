@@ -247,7 +247,10 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
 // (v_mfma_f32_16x16x4_f32: lane l = 16g + n supplies A[n][k_g] and B[k_g][n]
 // and holds D[4g + i][n], i < 4): A is wave w's column tile of C_acc, B the
 // block's S_c rows, so a lane holds G_acc[row n][4 adjacent columns].  The
-// contraction index of step s for lane group g is k = (d/4) g + s.
+// contraction index of step s for lane group g is k = (d/4) g + s.  At
+// d = 128 the same product runs on bf16 MFMA (v_mfma_f32_16x16x32_bf16, the
+// same output layout; lane group g supplies 8 consecutive k of its range)
+// over exact three-piece splits of both operands.
 //   * every workgroup keeps all of C_acc, as A fragments in registers (wave
 //     w: columns 16w .. 16w+15), and its own RPB rows of C_acc and S_acc in
 //     row-major 16-byte pieces; C_c is read by each row block of the head,
@@ -256,8 +259,8 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
 //     layout and is staged through LDS for the prefix stores, so that every
 //     store of the block's rows (S, C, G) is a contiguous row-major piece
 //     (the accumulator layout would write 64-byte halves of 128-byte lines);
-//   * every wave forms h_acc (block rows) from m_acc, which sits in LDS,
-//     double-buffered by segment parity;
+//   * wave t forms h_acc of row tile t (rows 16t .. 16t+15 of the block)
+//     from m_acc, which sits in LDS, double-buffered by segment parity;
 //   * the block's S_c rows and all of C_c go through LDS in 16-byte pieces
 //     (C with its 16-column tiles XOR-swizzled by row group, so the column
 //     reads of the four lane groups fall in different banks);
@@ -269,6 +272,25 @@ __global__ __launch_bounds__(256) void k_scan(const float* __restrict__ states, 
 //     the compiler's wait counts stay partial and the prefetch stays deep.
 // Each block writes its rows of S, C, G, h, and block 0 writes m.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+
+// Exact three-piece bf16 split of fp32 values: hi keeps the top 8 significand
+// bits (truncation), mid the next 8 bits of the remainder, lo the rest, which
+// then spans at most 8 bit positions; so x = hi + mid + lo exactly for every
+// normal x whose pieces stay normal.  Products of two such splits keep the six
+// cross terms down to 2^-24 relative (the three dropped terms are below it),
+// the rounding level of an fp32 product.  Pieces are returned packed, two
+// bf16 per word, in the order of the inputs.
+__device__ __forceinline__ uint32_t bf16_hi_pair(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
+__device__ __forceinline__ void split3_pair(float x0, float x1, uint32_t& h, uint32_t& m, uint32_t& l) {
+  const uint32_t u0 = __float_as_uint(x0), u1 = __float_as_uint(x1);
+  const float r0 = x0 - __uint_as_float(u0 & 0xffff0000u), r1 = x1 - __uint_as_float(u1 & 0xffff0000u);
+  const uint32_t v0 = __float_as_uint(r0), v1 = __float_as_uint(r1);
+  const float s0 = r0 - __uint_as_float(v0 & 0xffff0000u), s1 = r1 - __uint_as_float(v1 & 0xffff0000u);
+  h = bf16_hi_pair(u0, u1);
+  m = bf16_hi_pair(v0, v1);
+  l = bf16_hi_pair(__float_as_uint(s0), __float_as_uint(s1));
+}
 
 // Buffer resource over one record; loads and stores then take a 32-bit lane
 // offset plus a uniform offset, which keeps per-load addresses out of VGPRs.
@@ -316,9 +338,21 @@ struct RbCfg {
   // LDS: the block's S_c rows and the G_acc rows staged for row-major
   // prefix stores (two each, by segment parity), C_c (CBUF) and m_acc (two)
   static constexpr size_t lds_floats = 4 * (size_t)RPB * ldS + (size_t)CBUF * d * d + 2 * d;
+  // d = 128: the product runs on bf16 MFMA (16x16x32) over exact three-piece
+  // splits of both operands (six cross products), 2.7x the fp32 MFMA rate.
+  // The block's S_c rows are split once, when staged, into three bf16 planes
+  // (one per piece; by segment parity where C_c is double-buffered, else one
+  // set, which the step's first barrier protects); each wave splits its own
+  // column tile of C_acc.
+  static constexpr bool SPL = d == 128;
+  static constexpr int ldB = d + 8;                    // plane row stride (bf16): 16-byte reads of rows n, n+1 in different banks
+  static constexpr int NPB = CBUF == 1 ? 1 : 2;
+  static constexpr size_t plane = (size_t)RPB * ldB;   // bf16 per plane
+  static constexpr size_t lds_bytes = lds_floats * 4 + (SPL ? (size_t)NPB * 3 * plane * 2 : 0);
+  static_assert(lds_floats % 4 == 0 && ldB % 8 == 0 && lds_bytes <= 160 * 1024, "LDS layout");
   static_assert(GRP <= 4 && PF <= 4 && PFC <= 4 && GRP % PF == 0 && GRP % PFC == 0, "unrolled slots");
   static_assert(NSP * NT * 4 == RPB * d && KS % 4 == 0 && NC4 * NT * 4 == d * d && NCO * NT * 4 == RPB * d &&
-                    NW * CT * 16 == d,
+                    NW * CT * 16 == d && NW >= RT,
                 "row-block geometry");
 };
 
@@ -342,6 +376,7 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
   float* Gst = Sbuf + 2 * K::RPB * ldS;                // [2][RPB][ldS]  G_acc rows for the prefix stores
   float* Cbuf = Gst + 2 * K::RPB * ldS;                // [CBUF][d][d]   C_c, swizzled
   float* macc = Cbuf + K::CBUF * d * d;                // [2][d]         m_acc by segment parity
+  uint16_t* Bpl = reinterpret_cast<uint16_t*>(smem + K::lds_floats);   // [NPB][3][RPB][ldB] S_c row pieces
   const int tid = threadIdx.x, l = tid & 63, g = l >> 4, n = l & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = blockIdx.x, group = L / (8 * K::RB), within = L % (8 * K::RB);
@@ -450,9 +485,9 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
       rst4(y, e, oC + r0 * d, cown[j]);
       rst4(y, e, oG + r0 * d, *reinterpret_cast<const f32x4_t*>(gs + (e / d) * ldS + e % d));
     }
-    const bool hown = w == 0 && g == 0, mown = w == 0 && rb == 0;
+    const bool mown = w == 0 && rb == 0;
 #pragma unroll
-    for (int t = 0; t < RT; ++t) rst(y, hown ? r0 + n : kDrop, oh + 16 * t, hacc[t]);
+    for (int t = 0; t < RT; ++t) rst(y, w == t && g == 0 ? r0 + n : kDrop, oh + 16 * t, hacc[t]);
 #pragma unroll
     for (int j = 0; j < NM; ++j) {
       const int a = min(l + 64 * j, d - 1);
@@ -469,6 +504,15 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
     for (int j = 0; j < NSP; ++j) {
       const int e = tid + NT * j, row = e / (d / 4), c4 = (e % (d / 4)) * 4;
       *reinterpret_cast<f32x4_t*>(Sc + row * ldS + c4) = sp[sl][j];
+      if constexpr (K::SPL) {
+        uint2 ph, pm, pl;
+        split3_pair(sp[sl][j].x, sp[sl][j].y, ph.x, pm.x, pl.x);
+        split3_pair(sp[sl][j].z, sp[sl][j].w, ph.y, pm.y, pl.y);
+        uint16_t* pb = Bpl + (K::NPB == 2 ? (c & 1) : 0) * 3 * K::plane + row * K::ldB + c4;
+        *reinterpret_cast<uint2*>(pb) = ph;
+        *reinterpret_cast<uint2*>(pb + K::plane) = pm;
+        *reinterpret_cast<uint2*>(pb + 2 * K::plane) = pl;
+      }
     }
 #pragma unroll
     for (int j = 0; j < NC4; ++j) {
@@ -482,17 +526,53 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
     lds_barrier();
     put(pre + (size_t)c * F, mo, c & 1);
     const float rho = c == M - 1 ? rho_last : rho_full, rho2 = rho * rho;
-    // C_acc <- rho C_acc first: the product below uses the attenuated old C_acc
+    // G_acc^T <- rho^2 G_acc^T + G_c^T + rho (C_acc^T S_c[rows]^T): the
+    // product takes the old C_acc, and rho is applied to its result
+    if constexpr (K::SPL) {
+      // MFMA step s, lane group g, element j: contraction index KS g + 8 s + j
+      const uint16_t* pb = Bpl + (K::NPB == 2 ? (c & 1) : 0) * 3 * K::plane + n * K::ldB + KS * g;
+      f32x4_t acc[RT][CT];
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
+      for (int t = 0; t < RT; ++t)
 #pragma unroll
-      for (int s = 0; s < KS; ++s) cacc[ct][s] *= rho;
-    // G_acc^T <- rho^2 G_acc^T + G_c^T + (rho C_acc)^T S_c[rows]^T
+        for (int ct = 0; ct < CT; ++ct) acc[t][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS / 8; ++s) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          uint4 ah, am, al;
+          split3_pair(cacc[ct][8 * s + 0], cacc[ct][8 * s + 1], ah.x, am.x, al.x);
+          split3_pair(cacc[ct][8 * s + 2], cacc[ct][8 * s + 3], ah.y, am.y, al.y);
+          split3_pair(cacc[ct][8 * s + 4], cacc[ct][8 * s + 5], ah.z, am.z, al.z);
+          split3_pair(cacc[ct][8 * s + 6], cacc[ct][8 * s + 7], ah.w, am.w, al.w);
+          const bf16x8_t a1 = __builtin_bit_cast(bf16x8_t, ah), a2 = __builtin_bit_cast(bf16x8_t, am),
+                         a3 = __builtin_bit_cast(bf16x8_t, al);
+#pragma unroll
+          for (int t = 0; t < RT; ++t) {
+            const uint16_t* bp = pb + 16 * t * K::ldB + 8 * s;
+            const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(bp);
+            const bf16x8_t b2 = *reinterpret_cast<const bf16x8_t*>(bp + K::plane);
+            const bf16x8_t b3 = *reinterpret_cast<const bf16x8_t*>(bp + 2 * K::plane);
+            f32x4_t x = acc[t][ct];
+            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b1, x, 0, 0, 0);
+            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b2, x, 0, 0, 0);
+            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b3, x, 0, 0, 0);
+            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b1, x, 0, 0, 0);
+            x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b2, x, 0, 0, 0);
+            acc[t][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, x, 0, 0, 0);
+          }
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) gacc[ct][t] = rho2 * gacc[ct][t] + gc[sl][ct][t] + rho * acc[t][ct];
+    } else
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
       f32x4_t acc[CT];
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) acc[ct] = rho2 * gacc[ct][t] + gc[sl][ct][t];
+      for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       const float* brow = Sc + (16 * t + n) * ldS + KS * g;
 #pragma unroll
       for (int s4 = 0; s4 < KS; s4 += 4) {
@@ -506,12 +586,14 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
         }
       }
 #pragma unroll
-      for (int ct = 0; ct < CT; ++ct) gacc[ct][t] = acc[ct];
+      for (int ct = 0; ct < CT; ++ct) gacc[ct][t] = rho2 * gacc[ct][t] + gc[sl][ct][t] + rho * acc[ct];
     }
-    // h_acc += h_c + S_c[rows] m_acc (old m_acc), in every wave; m_acc += m_c
-    // into the other parity buffer (its readers, segment c - 1, are past the barrier)
+    // h_acc += h_c + S_c[rows] m_acc (old m_acc) of row tile t in wave t
+    // alone (the wave that stores it); m_acc += m_c into the other parity
+    // buffer (its readers, segment c - 1, are past the barrier)
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
+      if (w != t) continue;
       const float* arow = Sc + (16 * t + n) * ldS + KS * g;
       float e = 0.f;
 #pragma unroll
@@ -531,7 +613,7 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
         if (l + 64 * j < d) mn[l + 64 * j] = rho * mo[l + 64 * j] + mc[sl][j];
     }
     load_g(c + PF, slot_tag);
-    // S_acc += S_c, C_acc += C_c
+    // S_acc <- rho S_acc + S_c, C_acc <- rho C_acc + C_c
 #pragma unroll
     for (int j = 0; j < NCO; ++j) {
       const int e = 4 * (tid + NT * j);
@@ -542,7 +624,7 @@ __global__ __launch_bounds__((RbCfg<d>::NT)) void k_scan_rb(const float* __restr
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         const int k = KS * g + s;
-        cacc[ct][s] += Cc[k * d + cswz<d>(k, cw + 16 * ct + n)];
+        cacc[ct][s] = rho * cacc[ct][s] + Cc[k * d + cswz<d>(k, cw + 16 * ct + n)];
       }
 #pragma unroll
     for (int j = 0; j < NCO; ++j) {
@@ -599,7 +681,7 @@ hipError_t launch_scan_strided(const float* states, const float* init, float* pr
 #define HLA_SCAN_RB(D_)                                      \
   if (d == D_) {                                             \
     kern = (const void*)k_scan_rb<D_>;                       \
-    lds = RbCfg<D_>::lds_floats * sizeof(float);             \
+    lds = RbCfg<D_>::lds_bytes;                              \
     nt = RbCfg<D_>::NT;                                      \
     rbn = RbCfg<D_>::RB;                                     \
   }
