@@ -601,6 +601,7 @@ def measure_forward(name, steps, warmup, algo_name="auto", cold_iters=0):
     ms = e0.elapsed_time(e1) / steps
     warm = stats_ms(time_iters(step, max(steps, 50)))
     cold = stats_ms(time_iters(step, cold_iters, cold=True)) if cold_iters else None
+    cold_clean = stats_ms(time_iters(step, cold_iters, cold=True, clean=True)) if cold_iters else None
 
     # per-kernel durations: a second pass with the library's event bracketing
     capi.hla_profile_begin(8 * steps + 8)
@@ -646,6 +647,7 @@ def measure_forward(name, steps, warmup, algo_name="auto", cold_iters=0):
     }
     if cold is not None:
         rec["cold"] = dict(cold, value=tokens / (cold["median_ms"] / 1e3))
+        rec["cold_clean"] = dict(cold_clean, value=tokens / (cold_clean["median_ms"] / 1e3))
     return rec, (w, q, k, v)
 
 
@@ -719,6 +721,7 @@ def main():
         "kernels_ms": head["kernels_ms"],
         "warm": head["warm"],
         "cold": head.get("cold"),
+        "cold_clean": head.get("cold_clean"),
         "forward_mfma_frac": head["forward_mfma_frac"],
     }
     if not args.no_sub and args.workload != SUB_WORKLOAD:
