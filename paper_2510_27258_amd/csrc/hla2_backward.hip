@@ -19,9 +19,10 @@
 // the exact prefix (suffix) of the segment moments and no fix-up follows.
 //
 // k_la<..., MOM = true> writes the moments M_s = sum_{i in s} y_i z_i^T of
-// every segment; k_la<..., MOM = false> walks a segment's 64-token tiles in
+// every segment; k_la_scan replaces them in place by their exclusive prefix
+// (suffix) sums; k_la<..., MOM = false> walks a segment's 64-token tiles in
 // time order (causal) or in reverse (anti-causal) from
-// S0 = sum of the moments of the segments before (after) it:
+// S0 = sum of the moments of the segments before (after) it, one record:
 //   A = Q K^T masked (key <= query, or key >= query), O = A Z + X S0,
 //   S0 += Y^T Z,
 // and writes (or adds) O.  Operands that are exact in bf16 (q, k, v) take
@@ -97,7 +98,7 @@ struct Stage {
 template <int D, bool XF, bool YF, bool ZF, bool MOM, bool TWO = false>
 __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
     const void* __restrict__ xp, const void* __restrict__ yp, const void* __restrict__ zp, float* __restrict__ out,
-    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr) {
+    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr, int scanned) {
   using G = CfgLA<D>;
   static_assert(!TWO || (!XF && !YF && !MOM), "the paired pass keeps A2 in the lo tiles of x and y");
   constexpr bool kO = D == 128;
@@ -123,44 +124,12 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   const int c_begin = seg * cps, c_end = min(M, c_begin + cps);
   const size_t DD = (size_t)D * D;
 
-  // ---- state: zero for the moments; else the sum of the moments before (after) the segment ----
+  // ---- state: zero for the moments; else the moments of the segments
+  // before (after) this one, which k_la_scan has summed into this segment's
+  // record ----
   f32x16 S0[ST];
 #pragma unroll
   for (int i = 0; i < ST; ++i) S0[i] = zero16();
-  if (!MOM) {
-    const int s_lo = rev ? seg + 1 : 0, s_hi = rev ? nseg : seg;
-    if (s_lo < s_hi) {
-      constexpr int nP4 = D * D / 4 / NT;
-      static_assert(D * D % (4 * NT) == 0, "state staging split");
-      float4 pa[nP4];
-#pragma unroll
-      for (int r = 0; r < nP4; ++r) pa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int sp = s_lo; sp < s_hi; ++sp) {
-        const float4* x4 = reinterpret_cast<const float4*>(rec + ((size_t)bh * nseg + sp) * DD);
-#pragma unroll
-        for (int r = 0; r < nP4; ++r) {
-          const float4 u = x4[tid + NT * r];
-          pa[r].x += u.x; pa[r].y += u.y; pa[r].z += u.z; pa[r].w += u.w;
-        }
-      }
-      float* st = reinterpret_cast<float*>(lds);
-#pragma unroll
-      for (int r = 0; r < nP4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = pa[r];
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < ST; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int ra = i * 32 + acc_row(e, lg), cb = ct * 32 + lr;
-          if constexpr (TWO)
-            S0[i][e] = st[ra * D + cb] + st[cb * D + ra];
-          else
-            S0[i][e] = tr ? st[cb * D + ra] : st[ra * D + cb];
-        }
-      __syncthreads();
-    }
-  }
-
   const size_t eX = (XF ? 4 : 2), eY = (YF ? 4 : 2), eZ = (ZF ? 4 : 2);
   const rsrc_t rx = make_rsrc(static_cast<const char*>(xp) + (size_t)bh * n * D * eX, (uint32_t)(n * D * eX));
   const rsrc_t ry = make_rsrc(static_cast<const char*>(yp) + (size_t)bh * n * D * eY, (uint32_t)(n * D * eY));
@@ -171,10 +140,63 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   Stage<D, NT, ZF> sz;
   const int nt = c_end - c_begin;
   auto tile_of = [&](int i) { return rev ? c_end - 1 - i : c_begin + i; };
+  // the first tile's loads go out before the state record's, so the two wait together
   if (nt > 0) {
     if (!MOM) sx.fetch(rx, tile_of(0), tid);
     sy.fetch(ry, tile_of(0), tid);
     sz.fetch(rz, tile_of(0), tid);
+  }
+  if (!MOM && nseg > 1) {
+    // the records to sum: this segment's alone once k_la_scan has run
+    // (scanned), else those of every segment before (after) it
+    const int s_lo = scanned ? seg : rev ? seg + 1 : 0, s_hi = scanned ? seg + 1 : rev ? nseg : seg;
+    if (s_lo < s_hi) {
+      constexpr int nP4 = D * D / 4 / NT, RB = D == 64 ? 8 : 4, lds_ = D + 1;
+      static_assert(D * D % (4 * NT) == 0 && D * lds_ * 4 <= 2 * G::n16, "state staging split");
+      float4 pa[nP4];
+#pragma unroll
+      for (int r = 0; r < nP4; ++r) pa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+      // RB records at a time, all their loads issued before the sums
+      for (int sp = s_lo; sp < s_hi; sp += RB) {
+        float4 u[RB][nP4];
+#pragma unroll
+        for (int j = 0; j < RB; ++j)
+#pragma unroll
+          for (int r = 0; r < nP4; ++r)
+            u[j][r] = sp + j < s_hi
+                          ? reinterpret_cast<const float4*>(rec + ((size_t)bh * nseg + sp + j) * DD)[tid + NT * r]
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int j = 0; j < RB; ++j)
+#pragma unroll
+          for (int r = 0; r < nP4; ++r) {
+            pa[r].x += u[j][r].x; pa[r].y += u[j][r].y; pa[r].z += u[j][r].z; pa[r].w += u[j][r].w;
+          }
+      }
+      // staged row-major with an odd row stride, so the transposed reads
+      // (tr, TWO) fall in different banks
+      float* st = reinterpret_cast<float*>(lds);
+#pragma unroll
+      for (int r = 0; r < nP4; ++r) {
+        const int e = 4 * (tid + NT * r), row = e / D, col = e % D;
+        st[row * lds_ + col] = pa[r].x;
+        st[row * lds_ + col + 1] = pa[r].y;
+        st[row * lds_ + col + 2] = pa[r].z;
+        st[row * lds_ + col + 3] = pa[r].w;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < ST; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int ra = i * 32 + acc_row(e, lg), cb = ct * 32 + lr;
+          if constexpr (TWO)
+            S0[i][e] = st[ra * lds_ + cb] + st[cb * lds_ + ra];
+          else
+            S0[i][e] = tr ? st[cb * lds_ + ra] : st[ra * lds_ + cb];
+        }
+      __syncthreads();
+    }
   }
 
   for (int it = 0; it < nt; ++it) {
@@ -303,6 +325,47 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   }
 }
 
+// The segment moments of one set turned in place into their exclusive
+// prefix (rev = 0: the sum over the segments before each one, for causal
+// walks) or suffix (rev = 1: over the segments after it, for anti-causal
+// walks), so that a walk reads one record.  grid (D*D/256, BH), 64 * NPG
+// threads (NPG <= 16): a block owns 64 consecutive float4 of the records of
+// one head, and thread group g of it the g-th run of ceil(P / NPG)
+// consecutive segments.  The groups sum their runs, take the exclusive sum
+// of the groups before them from LDS, then rewrite their runs.
+__global__ __launch_bounds__(1024) void k_la_scan(float* __restrict__ rec, int rev, int P, int DD) {
+  __shared__ float4 part[16][64];
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6, npg = blockDim.x >> 6;
+  const int per = (P + npg - 1) / npg, p0 = min(P, grp * per), p1 = min(P, p0 + per);
+  float4* base = reinterpret_cast<float4*>(rec + (size_t)blockIdx.y * P * DD) + blockIdx.x * 64 + lane;
+  const size_t stride = DD / 4;
+  auto at = [&](int p) { return base + (size_t)(rev ? P - 1 - p : p) * stride; };
+  float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int p = p0; p < p1; ++p) {
+    const float4 u = *at(p);
+    sum.x += u.x; sum.y += u.y; sum.z += u.z; sum.w += u.w;
+  }
+  part[grp][lane] = sum;
+  __syncthreads();
+  float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int g = 0; g < grp; ++g) {
+    const float4 u = part[g][lane];
+    x.x += u.x; x.y += u.y; x.z += u.z; x.w += u.w;
+  }
+#pragma unroll 4
+  for (int p = p0; p < p1; ++p) {
+    float4* a = at(p);
+    const float4 u = *a;
+    *a = x;
+    x.x += u.x; x.y += u.y; x.z += u.z; x.w += u.w;
+  }
+}
+
+// Segments per head above which the moments are scanned first: a walk sums
+// at most this many records itself (in one or two batches of loads).
+constexpr int kScanAbove = 8;
+
 void la_plan(int D, int BH, int n, int* P, int* cps) {
   const int M = (n + 63) / 64;
   const int blocks = D == 64 ? CfgLA<64>::kBlocks : CfgLA<128>::kBlocks;
@@ -324,7 +387,18 @@ hipError_t la_moments(const void* y, const void* z, float* rec, int BH, int n, i
   if ((e = hipFuncSetAttribute(km, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start("bwd_moments", s);
   HLA_LAUNCH((k_la<D, false, YF, ZF, true>), dim3(P, BH), dim3(G::NT), G::bytes, s, y, y, z,
-             (float*)nullptr, rec, n, cps, P, 0, 0, 0);
+             (float*)nullptr, rec, n, cps, P, 0, 0, 0, 0);
+  prof_stop(s);
+  return hipGetLastError();
+}
+
+// Prefix (rev: suffix) sums of one moment set, in place, when P > kScanAbove.
+hipError_t la_scan(float* rec, int rev, int BH, int P, int D, hipStream_t s) {
+  if (P <= kScanAbove) return hipSuccess;
+  int npg = 1;
+  while (npg < 16 && npg < P) npg *= 2;
+  prof_start("bwd_scan", s);
+  HLA_LAUNCH(k_la_scan, dim3(D * D / 256, BH), dim3(64 * npg), 0, s, rec, rev, P, D * D);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -339,8 +413,9 @@ hipError_t la_walk(const char* name, const void* x, const void* y, const void* z
   hipError_t e;
   if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start(name, s);
+  const int scanned = P > kScanAbove;
   HLA_LAUNCH((k_la<D, XF, YF, ZF, false, TWO>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P,
-             rev, acc, tr);
+             rev, acc, tr, scanned);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -367,20 +442,28 @@ hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
   float* u = reinterpret_cast<float*>(ws + 4 * rb + vec_bytes(BH, n, D));
   hipError_t e;
 #define HLA_TRY(x) if ((e = (x)) != hipSuccess) return e
+  // Each moment set serves walks of one direction only, so with many
+  // segments the scan turns it in place into the prefixes (k^T k, v^T r:
+  // causal) or suffixes (g^T q, q^T u: anti-causal) the walks start from.
+  // Each moments launch directly precedes the walk that reads the same inputs.
   // r = LA+(q, k, k)
   HLA_TRY((la_moments<D, false, false>(b.k, b.k, kk, BH, n, P, cps, s)));
+  HLA_TRY(la_scan(kk, 0, BH, P, D, s));
   HLA_TRY((la_walk<D, false, false, false>("bwd_r", b.q, b.k, b.k, r, kk, BH, n, P, cps, 0, 0, 0, s)));
   // u = LA-(v, g, q)
   HLA_TRY((la_moments<D, true, false>(b.g, b.q, gq, BH, n, P, cps, s)));
+  HLA_TRY(la_scan(gq, 1, BH, P, D, s));
   HLA_TRY((la_walk<D, false, true, false>("bwd_u", b.v, b.g, b.q, u, gq, BH, n, P, cps, 1, 0, 0, s)));
   // dq = LA+(g, v, r) + LA+(u, k, k)
   HLA_TRY((la_moments<D, false, true>(b.v, r, vr, BH, n, P, cps, s)));
+  HLA_TRY(la_scan(vr, 0, BH, P, D, s));
   HLA_TRY((la_walk<D, true, false, true>("bwd_dq", b.g, b.v, r, b.dq, vr, BH, n, P, cps, 0, 0, 0, s)));
   HLA_TRY((la_walk<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, kk, BH, n, P, cps, 0, 1, 0, s)));
   // dv = LA-(r, q, g): moments q^T g = (g^T q)^T
   HLA_TRY((la_walk<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, gq, BH, n, P, cps, 1, 0, 1, s)));
   // dk = LA-(k, q, u) + LA-(k, u, q) in one paired walk: state sum (q u^T + u q^T)
   HLA_TRY((la_moments<D, false, true>(b.q, u, qu, BH, n, P, cps, s)));
+  HLA_TRY(la_scan(qu, 1, BH, P, D, s));
   HLA_TRY((la_walk<D, false, false, true, true>("bwd_dk", b.k, b.q, u, b.dk, qu, BH, n, P, cps, 1, 0, 0, s)));
 #undef HLA_TRY
   return hipSuccess;

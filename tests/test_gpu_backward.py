@@ -53,6 +53,26 @@ def test_backward_segment_counts(d, segments, monkeypatch):
     _check(2, 1, 64 * 9 + 5, d, seed=segments)
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("segments", [17, 34])
+def test_backward_many_segments(d, segments, monkeypatch):
+    """More segments than the moment scan's sixteen thread groups: runs of
+    two or three segments, the last ones partial or empty."""
+    monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
+    n = 64 * 33 + 17
+    P, _ = _plan(n, segments)
+    assert P == segments
+    _check(1, 1, n, d, seed=segments + d)
+
+
+def _plan(n, p):
+    """Segments and tiles per segment of the walks for a requested count p."""
+    M = (n + 63) // 64
+    p = max(1, min(p, M))
+    cps = (M + p - 1) // p
+    return (M + cps - 1) // cps, cps
+
+
 def test_backward_matches_autograd_of_definition_small():
     q, k, v, code = gen(1, 1, 70, 64, 64, "unit", 3)
     g = I.draw_grad(1, 1, 70, 64, 4)
