@@ -95,12 +95,18 @@ struct Stage {
 // in one walk: A2 = X Z^T masked adds A2 Y, and the state is
 // sum (y z^T + z y^T), staged from the moments of (y, z) plus their transpose
 // (x and y exact in bf16: A2 takes the lo regions of X and Y).
-template <int D, bool XF, bool YF, bool ZF, bool MOM, bool TWO = false>
+template <int D, bool XF, bool YF, bool ZF, bool MOM, bool TWO = false, int MO = 0>
 __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
     const void* __restrict__ xp, const void* __restrict__ yp, const void* __restrict__ zp, float* __restrict__ out,
-    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr, int scanned) {
+    float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr, int scanned,
+    const void* __restrict__ wp, float* __restrict__ rec2) {
   using G = CfgLA<D>;
   static_assert(!TWO || (!XF && !YF && !MOM), "the paired pass keeps A2 in the lo tiles of x and y");
+  // MO: the walk also forms its segment's moments sum w o^T of its own output
+  // o with w (MO = 1: a further bf16 input wp, staged in the lo tile of z;
+  // MO = 2: w = z), into rec2; o goes through the lo tiles of x and y (MO = 1)
+  // or x and z (MO = 2), which exact bf16 operands leave free
+  static_assert(MO == 0 || (!MOM && !TWO && !XF && !ZF && (MO == 2 || !YF)), "free lo tiles for o and w");
   constexpr bool kO = D == 128;
   constexpr int C = G::C, NT = G::NT, ST = G::ST, ld = G::ld, ldA = G::ldA;
   extern __shared__ __align__(16) uint16_t lds[];
@@ -138,6 +144,9 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   Stage<D, NT, XF> sx;
   Stage<D, NT, YF> sy;
   Stage<D, NT, ZF> sz;
+  Stage<D, NT, false> sw;
+  const rsrc_t rw = make_rsrc(MO == 1 ? static_cast<const char*>(wp) + (size_t)bh * n * D * 2 : nullptr,
+                              MO == 1 ? (uint32_t)(n * D * 2) : 0u);
   const int nt = c_end - c_begin;
   auto tile_of = [&](int i) { return rev ? c_end - 1 - i : c_begin + i; };
   // the first tile's loads go out before the state record's, so the two wait together
@@ -145,7 +154,14 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
     if (!MOM) sx.fetch(rx, tile_of(0), tid);
     sy.fetch(ry, tile_of(0), tid);
     sz.fetch(rz, tile_of(0), tid);
+    if (MO == 1) sw.fetch(rw, tile_of(0), tid);
   }
+  // MO: column ct of w o^T, all rows, over this wave's row tile of tokens
+  // (the two waves of a column tile add their halves at the end)
+  constexpr int SH = MO ? ST : 1;
+  f32x16 M2[SH];
+#pragma unroll
+  for (int i = 0; i < SH; ++i) M2[i] = zero16();
   if (!MOM && nseg > 1) {
     // the records to sum: this segment's alone once k_la_scan has run
     // (scanned), else those of every segment before (after) it
@@ -205,11 +221,13 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
     if (!MOM) sx.store(Xh, Xl, ld, tid);
     sy.store(Yh, Yl, ld, tid);
     sz.store(Zh, Zl, ld, tid);
+    if (MO == 1) sw.store(Zl, nullptr, ld, tid);
     lds_barrier();
     if (it + 1 < nt) {
       if (!MOM) sx.fetch(rx, tile_of(it + 1), tid);
       sy.fetch(ry, tile_of(it + 1), tid);
       sz.fetch(rz, tile_of(it + 1), tid);
+      if (MO == 1) sw.fetch(rw, tile_of(it + 1), tid);
     }
 
     f32x16 o = zero16();
@@ -277,6 +295,9 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
         }
       }
     }
+    uint16_t* Oh = Xl;                       // MO: this tile's o, hi | lo
+    uint16_t* Ol = MO == 1 ? Yl : Zl;
+    if constexpr (MO != 0) store_N<kO>(o, Oh, Ol, ld, rt * 32, ct * 32);
     // ---- state advance: S0 += Y^T Z (column ct, all rows) ----
 #pragma unroll
     for (int s = 0; s < G::KC; ++s) {
@@ -311,9 +332,49 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
 #pragma unroll
       for (int e = 0; e < 16; ++e) buf_store4(ro, ob + (8 * (e >> 2) + (e & 3)) * D * 4, prev[e] + o[e]);
     }
+    if constexpr (MO != 0) {
+      // M2 += w^T o over this wave's 32 tokens: the o piece read back is the
+      // one this wave stored (a wave's LDS accesses complete in order), and w
+      // was staged before the first barrier of the tile
+      const uint16_t* Wt = MO == 1 ? Zl : Zh;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int k0 = rt * 32 + s * 16;
+        const bf16x8 oh = frag_tr<kO>(Oh, ld, ct * 32, k0), ol = frag_tr<kO>(Ol, ld, ct * 32, k0);
+#pragma unroll
+        for (int i = 0; i < SH; ++i) {
+          const bf16x8 a = frag_tr<kO>(Wt, ld, i * 32, k0);
+          M2[i] = mfma(a, oh, M2[i]);
+          M2[i] = mfma(a, ol, M2[i]);
+        }
+      }
+    }
     lds_barrier();   // the next tile rewrites every LDS tile
   }
 
+  if (MO != 0 && nseg > 1) {   // this segment's w o^T (no walk reads it with one segment)
+    // the second token half's sums through LDS ([ct][row][32], free after the
+    // loop's last barrier), added by the first half's waves, which write
+    float* part = reinterpret_cast<float*>(lds) + ct * (D * 32);
+    if (rt == 1)
+#pragma unroll
+      for (int i = 0; i < SH; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) part[(i * 32 + acc_row(e, lg)) * 32 + lr] = M2[i][e];
+    lds_barrier();
+    if (rt == 0) {
+      int col = ct * 32 + lr;
+      asm volatile("" : "+v"(col));
+      float* r2 = rec2 + ((size_t)bh * nseg + seg) * DD;
+#pragma unroll
+      for (int i = 0; i < SH; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = i * 32 + acc_row(e, lg);
+          r2[(size_t)row * D + col] = M2[i][e] + part[row * 32 + lr];
+        }
+    }
+  }
   if (MOM && rt == 0) {   // both row waves hold the column; row tile 0's write it
     int col = ct * 32 + lr;
     asm volatile("" : "+v"(col));
@@ -387,7 +448,7 @@ hipError_t la_moments(const void* y, const void* z, float* rec, int BH, int n, i
   if ((e = hipFuncSetAttribute(km, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start("bwd_moments", s);
   HLA_LAUNCH((k_la<D, false, YF, ZF, true>), dim3(P, BH), dim3(G::NT), G::bytes, s, y, y, z,
-             (float*)nullptr, rec, n, cps, P, 0, 0, 0, 0);
+             (float*)nullptr, rec, n, cps, P, 0, 0, 0, 0, (const void*)nullptr, (float*)nullptr);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -404,18 +465,20 @@ hipError_t la_scan(float* rec, int rev, int BH, int P, int D, hipStream_t s) {
 }
 
 // One linear-attention walk over every segment from the moments in rec
-// (TWO: the paired walk LA(x, y, z) + LA(x, z, y)).
-template <int D, bool XF, bool YF, bool ZF, bool TWO = false>
+// (TWO: the paired walk LA(x, y, z) + LA(x, z, y); MO: also the moments
+// w o^T of its output into rec2, with w = wp (MO = 1) or z (MO = 2)).
+template <int D, bool XF, bool YF, bool ZF, bool TWO = false, int MO = 0>
 hipError_t la_walk(const char* name, const void* x, const void* y, const void* z, float* out, float* rec, int BH, int n,
-                   int P, int cps, int rev, int acc, int tr, hipStream_t s) {
+                   int P, int cps, int rev, int acc, int tr, hipStream_t s, const void* wp = nullptr,
+                   float* rec2 = nullptr) {
   using G = CfgLA<D>;
-  const void* kw = (const void*)k_la<D, XF, YF, ZF, false, TWO>;
+  const void* kw = (const void*)k_la<D, XF, YF, ZF, false, TWO, MO>;
   hipError_t e;
   if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start(name, s);
   const int scanned = P > kScanAbove;
-  HLA_LAUNCH((k_la<D, XF, YF, ZF, false, TWO>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps, P,
-             rev, acc, tr, scanned);
+  HLA_LAUNCH((k_la<D, XF, YF, ZF, false, TWO, MO>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps,
+             P, rev, acc, tr, scanned, wp, rec2);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -446,23 +509,23 @@ hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
   // segments the scan turns it in place into the prefixes (k^T k, v^T r:
   // causal) or suffixes (g^T q, q^T u: anti-causal) the walks start from.
   // Each moments launch directly precedes the walk that reads the same inputs.
-  // r = LA+(q, k, k)
+  // r = LA+(q, k, k), which also forms the v^T r moments
   HLA_TRY((la_moments<D, false, false>(b.k, b.k, kk, BH, n, P, cps, s)));
   HLA_TRY(la_scan(kk, 0, BH, P, D, s));
-  HLA_TRY((la_walk<D, false, false, false>("bwd_r", b.q, b.k, b.k, r, kk, BH, n, P, cps, 0, 0, 0, s)));
-  // u = LA-(v, g, q)
+  HLA_TRY((la_walk<D, false, false, false, false, 1>("bwd_r", b.q, b.k, b.k, r, kk, BH, n, P, cps, 0, 0, 0, s, b.v,
+                                                     vr)));
+  // u = LA-(v, g, q), which also forms the q^T u moments
   HLA_TRY((la_moments<D, true, false>(b.g, b.q, gq, BH, n, P, cps, s)));
   HLA_TRY(la_scan(gq, 1, BH, P, D, s));
-  HLA_TRY((la_walk<D, false, true, false>("bwd_u", b.v, b.g, b.q, u, gq, BH, n, P, cps, 1, 0, 0, s)));
+  HLA_TRY((la_walk<D, false, true, false, false, 2>("bwd_u", b.v, b.g, b.q, u, gq, BH, n, P, cps, 1, 0, 0, s, nullptr,
+                                                    qu)));
   // dq = LA+(g, v, r) + LA+(u, k, k)
-  HLA_TRY((la_moments<D, false, true>(b.v, r, vr, BH, n, P, cps, s)));
   HLA_TRY(la_scan(vr, 0, BH, P, D, s));
   HLA_TRY((la_walk<D, true, false, true>("bwd_dq", b.g, b.v, r, b.dq, vr, BH, n, P, cps, 0, 0, 0, s)));
   HLA_TRY((la_walk<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, kk, BH, n, P, cps, 0, 1, 0, s)));
   // dv = LA-(r, q, g): moments q^T g = (g^T q)^T
   HLA_TRY((la_walk<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, gq, BH, n, P, cps, 1, 0, 1, s)));
   // dk = LA-(k, q, u) + LA-(k, u, q) in one paired walk: state sum (q u^T + u q^T)
-  HLA_TRY((la_moments<D, false, true>(b.q, u, qu, BH, n, P, cps, s)));
   HLA_TRY(la_scan(qu, 1, BH, P, D, s));
   HLA_TRY((la_walk<D, false, false, true, true>("bwd_dk", b.k, b.q, u, b.dk, qu, BH, n, P, cps, 1, 0, 0, s)));
 #undef HLA_TRY
