@@ -466,8 +466,9 @@ def measure_ahla(reps=10):
 
 
 # Per-token HBM bytes / d of each linear-attention pass of the backward: x, y, z
-# read (bf16 2 B or fp32 4 B per element), the output written (4 B), and read
-# back (4 B) when the pass adds to it.  Passes that share a name are averaged.
+# read (bf16 2 B or fp32 4 B per element; the r pass also reads v, for the
+# v^T r moments of its output), the output written (4 B), and read back (4 B)
+# when the pass adds to it.  Passes that share a name are averaged.
 BWD_PASS_BYTES = {"bwd_r": [2 + 2 + 2 + 2 + 4], "bwd_u": [2 + 4 + 2 + 4], "bwd_dq": [4 + 2 + 4 + 4, 4 + 2 + 2 + 8],
                   "bwd_dv": [4 + 2 + 4 + 4], "bwd_dk": [2 + 2 + 4 + 4, 2 + 4 + 2 + 8]}
 
