@@ -120,17 +120,48 @@ __attribute__((amdgpu_waves_per_eu(CfgAH<D>::RPW == 2 ? 1 : 2))) void k_ahla_wal
   }
   if (seg > 0) {
     // P0, m0 = the prefix of the earlier segments' moments: one record
-    // [D * DV | D] per segment (k_seg_prefix)
-    constexpr int nP4 = D * DV / 4 / NT;
+    // [D * DV | D] per segment (k_seg_prefix), or without ppre (few
+    // segments) the sum of the earlier records' C | m slots, which the
+    // moments launch wrote (walks write only G and h), four records' loads
+    // in flight at a time
+    constexpr int nP4 = D * DV / 4 / NT, SB = 4;
     static_assert(D * DV % (4 * NT) == 0, "carry staging split");
-    const float* x = ppre + ((size_t)bh * nseg + seg) * ((size_t)D * DV + D);
     float4 pa[nP4];
+    float ma = 0.f;
+    if (ppre) {
+      const float* x = ppre + ((size_t)bh * nseg + seg) * ((size_t)D * DV + D);
 #pragma unroll
-    for (int r = 0; r < nP4; ++r) pa[r] = reinterpret_cast<const float4*>(x)[tid + NT * r];
+      for (int r = 0; r < nP4; ++r) pa[r] = reinterpret_cast<const float4*>(x)[tid + NT * r];
+      if (ta >= 0) ma = x[D * DV + ta];
+    } else {
+      const float* base = rec + (size_t)bh * (nseg + 1) * F + off_C(D, DV);
+#pragma unroll
+      for (int r = 0; r < nP4; ++r) pa[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int sp = 0; sp < seg; sp += SB) {
+        float4 u[SB][nP4];
+        float um[SB];
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+          const float* x = base + (size_t)(sp + j) * F;
+#pragma unroll
+          for (int r = 0; r < nP4; ++r)
+            u[j][r] = sp + j < seg ? reinterpret_cast<const float4*>(x)[tid + NT * r] : make_float4(0.f, 0.f, 0.f, 0.f);
+          um[j] = sp + j < seg && ta >= 0 ? x[D * DV + ta] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < SB; ++j) {
+#pragma unroll
+          for (int r = 0; r < nP4; ++r) {
+            pa[r].x += u[j][r].x; pa[r].y += u[j][r].y; pa[r].z += u[j][r].z; pa[r].w += u[j][r].w;
+          }
+          ma += um[j];
+        }
+      }
+    }
     float* st = reinterpret_cast<float*>(lds);
 #pragma unroll
     for (int r = 0; r < nP4; ++r) reinterpret_cast<float4*>(st)[tid + NT * r] = pa[r];
-    if (ta >= 0) m0[ta] = x[D * DV + ta];
+    if (ta >= 0) m0[ta] = ma;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < ST; ++i)
@@ -376,6 +407,10 @@ size_t den_bytes_ah(int BH, int n, int d) {
 // carries [BH][P][d d + d] (k_carry), then the moment prefixes [BH][P][d d + d]
 size_t carry_bytes_ah(int BH, int P, int d) { return sizeof(float) * (size_t)BH * P * ((size_t)d * d + d); }
 
+// Segments per head up to which an AHLA walk sums its P and m^K prefixes
+// from the moment records itself instead of reading them from a prefix launch.
+constexpr int kAhlaWalkSumMax = 8;
+
 template <int D>
 hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
   constexpr int C = 64;
@@ -395,17 +430,21 @@ hipError_t run_ahla(const Fwd& f, char* ws, int P, int cps, hipStream_t s) {
     HLA_LAUNCH((k_moments<C, D, D, true>), grid, dim3(kThreads), 0, s, q, k, v, segs, f.n, cps, P, 1, 0.f);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    prof_start("ahla_prefix", s);     // the P and m^K slots are adjacent (C | m)
-    HLA_LAUNCH(k_seg_prefix, dim3((D * D + D + 1023) / 1024, BH), dim3(256), 0, s, segs, state_floats(D, D),
-               (int)off_C(D, D), D * D + D, 0, ppre, P, 1.f);
-    prof_stop(s);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (P > kAhlaWalkSumMax) {
+      prof_start("ahla_prefix", s);     // the P and m^K slots are adjacent (C | m)
+      HLA_LAUNCH(k_seg_prefix, dim3((D * D + D + 1023) / 1024, BH), dim3(256), 0, s, segs, state_floats(D, D),
+                 (int)off_C(D, D), D * D + D, 0, ppre, P, 1.f);
+      prof_stop(s);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
   }
+  // up to kAhlaWalkSumMax segments per head each walk sums the earlier moments itself
+  const float* ppre_walk = P > kAhlaWalkSumMax ? ppre : nullptr;
   if ((e = hipFuncSetAttribute((const void*)k_ahla_walk<D>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                (int)G::bytes)) != hipSuccess)
     return e;
   prof_start("ahla_walk", s);
-  HLA_LAUNCH((k_ahla_walk<D>), grid, dim3(G::NT), G::bytes, s, q, k, v, f.out, den, segs, (const float*)ppre, f.n,
+  HLA_LAUNCH((k_ahla_walk<D>), grid, dim3(G::NT), G::bytes, s, q, k, v, f.out, den, segs, ppre_walk, f.n,
              cps, P, f.normalized);
   prof_stop(s);
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -58,9 +58,10 @@ def test_ahla_shapes(d, chunk):
 
 
 @pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("segments", [1, 2, 3, 7])
+@pytest.mark.parametrize("segments", [1, 2, 3, 7, 10])
 def test_ahla_segment_counts(d, segments, monkeypatch):
-    """Segments of several tiles: the P prefix, the brackets and the fix-up."""
+    """Segments of several tiles: the P prefix (summed by the walks up to 8
+    segments, a prefix launch above), the brackets and the fix-up."""
     monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
     _check(2, 1, 64 * 9 + 5, d, 64, seed=segments)
 
