@@ -705,13 +705,14 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
     P0[i] = zero16();
   }
   for (int a = tid; a < D; a += NT) eta[a] = 0.f;
-  if (spre || (!DEC && nseg > 1)) {
+  if (spre || nseg > 1) {
     // S0 = the S prefix of this segment (the converted initial state and the
     // earlier segments; decayed: each aged to this segment's start), staged
     // through the (still free) tile region of LDS.  Without spre (no initial
-    // state, no decay, few segments) it is summed here from the S slots of
-    // the earlier segments' records, which the moments launch wrote (walks
-    // write only G and h), four records' loads in flight at a time.
+    // state, few segments) it is summed here from the S slots of the earlier
+    // segments' records, which the moments launch wrote (walks write only G
+    // and h), four records' loads in flight at a time; decayed, segment sp
+    // is aged by gamma^(C cps (seg - 1 - sp)), as the prefix launch ages it.
     constexpr int nS4 = D * D / 4 / NT, SB = 4;
     static_assert(D * D % (4 * NT) == 0 && D * D * 4 <= G::n16 * 2, "carry staging");
     float4 sa[nS4];
@@ -732,11 +733,15 @@ __global__ __launch_bounds__((CfgRS<D, SUMMARY>::NT), (CfgRS<D, SUMMARY>::kBlock
                           ? reinterpret_cast<const float4*>(rec + ((size_t)bh * (nseg + 1) + sp + j) * F)[tid + NT * r]
                           : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int j = 0; j < SB; ++j)
+        for (int j = 0; j < SB; ++j) {
+          // (entries past the last record hold zeros; their would-be age is
+          // negative, so they take weight 0, not an overflowing power)
+          const float a = !DEC ? 1.f : sp + j < seg ? exp2f(lg2g * (float)(C * cps) * (float)(seg - 1 - sp - j)) : 0.f;
 #pragma unroll
           for (int r = 0; r < nS4; ++r) {
-            sa[r].x += u[j][r].x; sa[r].y += u[j][r].y; sa[r].z += u[j][r].z; sa[r].w += u[j][r].w;
+            sa[r].x += a * u[j][r].x; sa[r].y += a * u[j][r].y; sa[r].z += a * u[j][r].z; sa[r].w += a * u[j][r].w;
           }
+        }
       }
     }
     float* st = reinterpret_cast<float*>(lds);
@@ -1112,9 +1117,9 @@ bool legacy_pipeline() {
 // one workgroup per CU, d = dv = 128: about 3.9 and 6.6 us per tile).
 constexpr double kWsSummaryRatio = 0.6;
 
-// Segments per head up to which the row-split walk (no decay, no initial
-// state) sums its S prefix from the moments itself instead of reading it from
-// a prefix launch.
+// Segments per head up to which the row-split walk (no initial state) sums
+// its S prefix from the moments itself instead of reading it from a prefix
+// launch.
 constexpr int kWalkSumMax = 8;
 
 // Segments of the two-pass plan: with Q = 256 / BH walks per head in each
@@ -1247,10 +1252,10 @@ hipError_t run_shape(const Fwd& f, const float* init, float* final_state, char* 
   if ((e = hipGetLastError()) != hipSuccess) return e;
   // S prefix of every segment (the walks each read one): init + the earlier
   // segments' moments, each aged to the segment's start when decayed.  The
-  // row-split walk without decay or initial state sums up to kWalkSumMax - 1
+  // row-split walk without an initial state sums up to kWalkSumMax - 1
   // earlier moments itself, which saves this launch.
   float* spre = nullptr;
-  const bool walk_sums = RS && !DEC && !init && P <= kWalkSumMax;
+  const bool walk_sums = RS && !init && P <= kWalkSumMax;
   if ((P > 1 || init) && !walk_sums) {
     spre = reinterpret_cast<float*>(ws + legacy_spre_offset(BH, f.n, P, C, D, DV));
     const float rhoS = DEC ? (float)std::exp2((double)lg2g * (double)C * (double)cps) : 1.f;
