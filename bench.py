@@ -465,12 +465,14 @@ def measure_ahla(reps=10):
                          "mfma_frac": flops / s / 1e12 / BF16_MFMA_PEAK_TFLOPS}}
 
 
-# Per-token HBM bytes / d of each linear-attention pass of the backward: x, y, z
-# read (bf16 2 B or fp32 4 B per element; the r pass also reads v, for the
-# v^T r moments of its output), the output written (4 B), and read back (4 B)
-# when the pass adds to it.  Passes that share a name are averaged.
-BWD_PASS_BYTES = {"bwd_r": [2 + 2 + 2 + 2 + 4], "bwd_u": [2 + 4 + 2 + 4], "bwd_dq": [4 + 2 + 4 + 4, 4 + 2 + 2 + 8],
-                  "bwd_dv": [4 + 2 + 4 + 4], "bwd_dk": [2 + 2 + 4 + 4, 2 + 4 + 2 + 8]}
+# Per-token HBM bytes / d of each launch of the backward: x, y, z read (bf16
+# 2 B or fp32 4 B per element; the r pass also reads v, for the v^T r moments
+# of its output), the output written (4 B), and read back (4 B) when the pass
+# adds to it; a launch of two passes side by side counts both.  Launches that
+# share a name are averaged.
+BWD_PASS_BYTES = {"bwd_ru": [(2 + 2 + 2 + 2 + 4) + (2 + 4 + 2 + 4)],
+                  "bwd_dq": [4 + 2 + 4 + 4, 4 + 2 + 2 + 8],
+                  "bwd_dvdk": [(4 + 2 + 4 + 4) + (2 + 2 + 4 + 4)]}
 
 
 def measure_backward(reps=10):

@@ -30,6 +30,7 @@
 // are split into bf16 hi + lo, and a product of two split operands takes
 // three passes (hi hi, hi lo, lo hi).  Accumulation is fp32.
 #include <cstdlib>
+#include <type_traits>
 
 #include "backward.h"
 #include "fused_tiles.h"
@@ -96,10 +97,10 @@ struct Stage {
 // sum (y z^T + z y^T), staged from the moments of (y, z) plus their transpose
 // (x and y exact in bf16: A2 takes the lo regions of X and Y).
 template <int D, bool XF, bool YF, bool ZF, bool MOM, bool TWO = false, int MO = 0>
-__global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
+__device__ __forceinline__ void la_pass(
     const void* __restrict__ xp, const void* __restrict__ yp, const void* __restrict__ zp, float* __restrict__ out,
     float* __restrict__ rec, int n, int cps, int nseg, int rev, int acc_out, int tr, int scanned,
-    const void* __restrict__ wp, float* __restrict__ rec2) {
+    const void* __restrict__ wp, float* __restrict__ rec2, int seg, int bh) {
   using G = CfgLA<D>;
   static_assert(!TWO || (!XF && !YF && !MOM), "the paired pass keeps A2 in the lo tiles of x and y");
   // MO: the walk also forms its segment's moments sum w o^T of its own output
@@ -121,8 +122,6 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   uint16_t* A2h = Xl;             // TWO: A2 = X Z^T masked, in the (unused) lo tiles of x and y
   uint16_t* A2l = Yl;
 
-  int seg, bh;
-  seg_head(seg, bh);
   const int tid = threadIdx.x, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rt = w / G::NCT, ct = w % G::NCT;
@@ -386,6 +385,41 @@ __global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(
   }
 }
 
+// The arguments of one pass, and a pass as a type (its template arguments).
+struct LaArgs {
+  const void* xp;
+  const void* yp;
+  const void* zp;
+  float* out;
+  float* rec;
+  int n, cps, nseg, rev, acc_out, tr, scanned;
+  const void* wp;
+  float* rec2;
+};
+template <int D, bool XF, bool YF, bool ZF, bool MOM, bool TWO = false, int MO = 0>
+struct LaPass {
+  static __device__ __forceinline__ void run(const LaArgs& a, int seg, int bh) {
+    la_pass<D, XF, YF, ZF, MOM, TWO, MO>(a.xp, a.yp, a.zp, a.out, a.rec, a.n, a.cps, a.nseg, a.rev, a.acc_out, a.tr,
+                                         a.scanned, a.wp, a.rec2, seg, bh);
+  }
+};
+
+// grid (segments, heads, 1 or 2): pass A, or two independent passes of the
+// same shape in one launch, A on blockIdx.z = 0 and B on 1.
+template <int D, class A, class B = A>
+__global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(LaArgs a0, LaArgs a1) {
+  int seg, bh;
+  seg_head(seg, bh);
+  if constexpr (std::is_same<A, B>::value) {
+    A::run(a0, seg, bh);
+  } else {
+    if (blockIdx.z == 0)
+      A::run(a0, seg, bh);
+    else
+      B::run(a1, seg, bh);
+  }
+}
+
 // The segment moments of one set turned in place into their exclusive
 // prefix (rev = 0: the sum over the segments before each one, for causal
 // walks) or suffix (rev = 1: over the segments after it, for anti-causal
@@ -438,21 +472,6 @@ void la_plan(int D, int BH, int n, int* P, int* cps) {
   *P = (M + *cps - 1) / *cps;
 }
 
-// The moments sum y z^T of every segment (skipped with one segment: no walk reads them).
-template <int D, bool YF, bool ZF>
-hipError_t la_moments(const void* y, const void* z, float* rec, int BH, int n, int P, int cps, hipStream_t s) {
-  using G = CfgLA<D>;
-  if (P == 1) return hipSuccess;
-  const void* km = (const void*)k_la<D, false, YF, ZF, true>;
-  hipError_t e;
-  if ((e = hipFuncSetAttribute(km, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
-  prof_start("bwd_moments", s);
-  HLA_LAUNCH((k_la<D, false, YF, ZF, true>), dim3(P, BH), dim3(G::NT), G::bytes, s, y, y, z,
-             (float*)nullptr, rec, n, cps, P, 0, 0, 0, 0, (const void*)nullptr, (float*)nullptr);
-  prof_stop(s);
-  return hipGetLastError();
-}
-
 // Prefix (rev: suffix) sums of one moment set, in place, when P > kScanAbove.
 hipError_t la_scan(float* rec, int rev, int BH, int P, int D, hipStream_t s) {
   if (P <= kScanAbove) return hipSuccess;
@@ -464,23 +483,28 @@ hipError_t la_scan(float* rec, int rev, int BH, int P, int D, hipStream_t s) {
   return hipGetLastError();
 }
 
-// One linear-attention walk over every segment from the moments in rec
-// (TWO: the paired walk LA(x, y, z) + LA(x, z, y); MO: also the moments
-// w o^T of its output into rec2, with w = wp (MO = 1) or z (MO = 2)).
-template <int D, bool XF, bool YF, bool ZF, bool TWO = false, int MO = 0>
-hipError_t la_walk(const char* name, const void* x, const void* y, const void* z, float* out, float* rec, int BH, int n,
-                   int P, int cps, int rev, int acc, int tr, hipStream_t s, const void* wp = nullptr,
-                   float* rec2 = nullptr) {
+// One launch of pass A, or of passes A and B side by side (grid z = 2), over
+// every (segment, head).  A pass's moments (MOM) are the sums y z^T of each
+// segment; a walk (TWO: the paired walk LA(x, y, z) + LA(x, z, y); MO: also
+// the moments w o^T of its output into rec2, with w = wp (MO = 1) or z
+// (MO = 2)) starts every segment from the moments of the others on its side.
+template <int D, class A, class B = A>
+hipError_t la_launch(const char* name, const LaArgs& a0, const LaArgs& a1, int BH, int P, hipStream_t s) {
   using G = CfgLA<D>;
-  const void* kw = (const void*)k_la<D, XF, YF, ZF, false, TWO, MO>;
+  const void* kf = (const void*)k_la<D, A, B>;
   hipError_t e;
-  if ((e = hipFuncSetAttribute(kw, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
+  if ((e = hipFuncSetAttribute(kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start(name, s);
-  const int scanned = P > kScanAbove;
-  HLA_LAUNCH((k_la<D, XF, YF, ZF, false, TWO, MO>), dim3(P, BH), dim3(G::NT), G::bytes, s, x, y, z, out, rec, n, cps,
-             P, rev, acc, tr, scanned, wp, rec2);
+  HLA_LAUNCH((k_la<D, A, B>), dim3(P, BH, std::is_same<A, B>::value ? 1 : 2), dim3(G::NT), G::bytes, s, a0, a1);
   prof_stop(s);
   return hipGetLastError();
+}
+
+// The arguments of a pass LA(x, y, z) (rev: anti-causal; acc: add to out;
+// tr: the records hold the transposed moments).
+LaArgs la_args(const void* x, const void* y, const void* z, float* out, float* rec, int n, int cps, int P, int rev,
+               int acc, int tr, const void* wp = nullptr, float* rec2 = nullptr) {
+  return LaArgs{x, y, z, out, rec, n, cps, P, rev, acc, tr, P > kScanAbove ? 1 : 0, wp, rec2};
 }
 
 size_t rec_bytes(int BH, int P, int d) {
@@ -508,26 +532,33 @@ hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
   // Each moment set serves walks of one direction only, so with many
   // segments the scan turns it in place into the prefixes (k^T k, v^T r:
   // causal) or suffixes (g^T q, q^T u: anti-causal) the walks start from.
-  // Each moments launch directly precedes the walk that reads the same inputs.
-  // r = LA+(q, k, k), which also forms the v^T r moments
-  HLA_TRY((la_moments<D, false, false>(b.k, b.k, kk, BH, n, P, cps, s)));
+  // Passes that do not depend on each other share a launch.
+  using MomKK = LaPass<D, false, false, false, true>;
+  using MomGQ = LaPass<D, false, true, false, true>;
+  using WalkR = LaPass<D, false, false, false, false, false, 1>;    // also v^T r
+  using WalkU = LaPass<D, false, true, false, false, false, 2>;     // also q^T u
+  using WalkG = LaPass<D, true, false, true, false>;                       // x, z fp32: dq (first term), dv
+  using WalkU2 = LaPass<D, true, false, false, false>;                     // x fp32: dq (second term)
+  using WalkK = LaPass<D, false, false, true, false, true>;          // paired dk
+  // the moments k^T k (r, the second dq term) and g^T q (u; transposed for dv)
+  if (P > 1)
+    HLA_TRY((la_launch<D, MomKK, MomGQ>("bwd_moments", la_args(b.k, b.k, b.k, nullptr, kk, n, cps, P, 0, 0, 0),
+                                        la_args(b.g, b.g, b.q, nullptr, gq, n, cps, P, 0, 0, 0), BH, P, s)));
   HLA_TRY(la_scan(kk, 0, BH, P, D, s));
-  HLA_TRY((la_walk<D, false, false, false, false, 1>("bwd_r", b.q, b.k, b.k, r, kk, BH, n, P, cps, 0, 0, 0, s, b.v,
-                                                     vr)));
-  // u = LA-(v, g, q), which also forms the q^T u moments
-  HLA_TRY((la_moments<D, true, false>(b.g, b.q, gq, BH, n, P, cps, s)));
   HLA_TRY(la_scan(gq, 1, BH, P, D, s));
-  HLA_TRY((la_walk<D, false, true, false, false, 2>("bwd_u", b.v, b.g, b.q, u, gq, BH, n, P, cps, 1, 0, 0, s, nullptr,
-                                                    qu)));
-  // dq = LA+(g, v, r) + LA+(u, k, k)
+  // r = LA+(q, k, k) with the v^T r moments, beside u = LA-(v, g, q) with the q^T u moments
+  HLA_TRY((la_launch<D, WalkR, WalkU>("bwd_ru", la_args(b.q, b.k, b.k, r, kk, n, cps, P, 0, 0, 0, b.v, vr),
+                                      la_args(b.v, b.g, b.q, u, gq, n, cps, P, 1, 0, 0, nullptr, qu), BH, P, s)));
   HLA_TRY(la_scan(vr, 0, BH, P, D, s));
-  HLA_TRY((la_walk<D, true, false, true>("bwd_dq", b.g, b.v, r, b.dq, vr, BH, n, P, cps, 0, 0, 0, s)));
-  HLA_TRY((la_walk<D, true, false, false>("bwd_dq", u, b.k, b.k, b.dq, kk, BH, n, P, cps, 0, 1, 0, s)));
-  // dv = LA-(r, q, g): moments q^T g = (g^T q)^T
-  HLA_TRY((la_walk<D, true, false, true>("bwd_dv", r, b.q, b.g, b.dv, gq, BH, n, P, cps, 1, 0, 1, s)));
-  // dk = LA-(k, q, u) + LA-(k, u, q) in one paired walk: state sum (q u^T + u q^T)
   HLA_TRY(la_scan(qu, 1, BH, P, D, s));
-  HLA_TRY((la_walk<D, false, false, true, true>("bwd_dk", b.k, b.q, u, b.dk, qu, BH, n, P, cps, 1, 0, 0, s)));
+  // dq = LA+(g, v, r) + LA+(u, k, k)
+  const LaArgs none{};
+  HLA_TRY((la_launch<D, WalkG>("bwd_dq", la_args(b.g, b.v, r, b.dq, vr, n, cps, P, 0, 0, 0), none, BH, P, s)));
+  HLA_TRY((la_launch<D, WalkU2>("bwd_dq", la_args(u, b.k, b.k, b.dq, kk, n, cps, P, 0, 1, 0), none, BH, P, s)));
+  // dv = LA-(r, q, g) (moments q^T g = (g^T q)^T) beside dk = LA-(k, q, u) + LA-(k, u, q)
+  // in one paired walk (state sum q u^T + u q^T)
+  HLA_TRY((la_launch<D, WalkG, WalkK>("bwd_dvdk", la_args(r, b.q, b.g, b.dv, gq, n, cps, P, 1, 0, 1),
+                                      la_args(b.k, b.q, u, b.dk, qu, n, cps, P, 1, 0, 0), BH, P, s)));
 #undef HLA_TRY
   return hipSuccess;
 }
