@@ -18,9 +18,10 @@
 // does not depend on anything before it, so every segment's walk starts from
 // the exact prefix (suffix) of the segment moments and no fix-up follows.
 //
-// k_la<..., MOM = true> writes the moments M_s = sum_{i in s} y_i z_i^T of
-// every segment; k_la_scan replaces them in place by their exclusive prefix
-// (suffix) sums; k_la<..., MOM = false> walks a segment's 64-token tiles in
+// A moments pass (la_pass<..., MOM = true>) writes the moments
+// M_s = sum_{i in s} y_i z_i^T of every segment; k_la_scan replaces them in
+// place by their exclusive prefix (suffix) sums; a walk pass (MOM = false;
+// k_la runs one pass or two side by side) walks a segment's 64-token tiles in
 // time order (causal) or in reverse (anti-causal) from
 // S0 = sum of the moments of the segments before (after) it, one record:
 //   A = Q K^T masked (key <= query, or key >= query), O = A Z + X S0,
