@@ -230,6 +230,18 @@ def test_fused_d128_pipelines_agree(monkeypatch):
     assert float((np.abs(d0 - d1) / D).max()) <= 2e-3
 
 
+@pytest.mark.parametrize("segments", [3, 14])
+def test_fused_d128_legacy_segments(segments, monkeypatch):
+    """The d = 128 walk + carry fix-up pipeline at a few segments per head,
+    where each walk sums its S prefix from the moment records itself, and at
+    more, where a prefix launch forms it; normalised, against the oracle."""
+    monkeypatch.setenv("HLA_FUSED_LEGACY", "1")
+    monkeypatch.setenv("HLA_FUSED_SEGMENTS", str(segments))
+    n = 64 * 13 + 9
+    assert capi.hla2_fused_plan(1, 2, n, 128, 128, 128)[0] == segments
+    assert _check_forward(1, 2, n, 128, 128, 128, "unit", 1, True, capi.HLA_ALGO_FUSED, seed=23)
+
+
 def test_fused_long_single_head():
     """One head of 262 144 tokens: 4096 tiles cut into the plan's largest
     segment count (one head), so the longest carry chains and the largest
