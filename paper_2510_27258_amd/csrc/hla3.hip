@@ -157,7 +157,6 @@ __global__ __launch_bounds__(kT3) void k3_walk(const T* __restrict__ q, const T*
   const int M = (n + C - 1) / C, c0 = seg * cps, c1 = min(M, c0 + cps);
   const size_t head_tok = (size_t)bh * n;
   float* recs = rec + (size_t)bh * nseg * Rc::floats;
-  const f32x4c zf = {0.f, 0.f, 0.f, 0.f};
   const f64x4c zd = {0.0, 0.0, 0.0, 0.0};
 
   // moment carry: the sum of the segments before this one (k3_prefix); F = eta = 0
