@@ -468,11 +468,10 @@ def measure_ahla(reps=10):
 # Per-token HBM bytes / d of each launch of the backward: x, y, z read (bf16
 # 2 B or fp32 4 B per element; the r pass also reads v, for the v^T r moments
 # of its output), the output written (4 B), and read back (4 B) when the pass
-# adds to it; a launch of two passes side by side counts both.  Launches that
-# share a name are averaged.
+# adds to it; a launch of several passes side by side counts them all.
 BWD_PASS_BYTES = {"bwd_ru": [(2 + 2 + 2 + 2 + 4) + (2 + 4 + 2 + 4)],
-                  "bwd_dq": [4 + 2 + 4 + 4, 4 + 2 + 2 + 8],
-                  "bwd_dvdk": [(4 + 2 + 4 + 4) + (2 + 2 + 4 + 4)]}
+                  "bwd_dq_dv_dk": [(4 + 2 + 4 + 4) + (4 + 2 + 4 + 4) + (2 + 2 + 4 + 4)],
+                  "bwd_dq": [4 + 2 + 2 + 8]}
 
 
 def measure_backward(reps=10):

@@ -21,7 +21,7 @@
 // A moments pass (la_pass<..., MOM = true>) writes the moments
 // M_s = sum_{i in s} y_i z_i^T of every segment; k_la_scan replaces them in
 // place by their exclusive prefix (suffix) sums; a walk pass (MOM = false;
-// k_la runs one pass or two side by side) walks a segment's 64-token tiles in
+// k_la runs one pass or up to three side by side) walks a segment's 64-token tiles in
 // time order (causal) or in reverse (anti-causal) from
 // S0 = sum of the moments of the segments before (after) it, one record:
 //   A = Q K^T masked (key <= query, or key >= query), O = A Z + X S0,
@@ -405,19 +405,26 @@ struct LaPass {
   }
 };
 
-// grid (segments, heads, 1 or 2): pass A, or two independent passes of the
-// same shape in one launch, A on blockIdx.z = 0 and B on 1.
-template <int D, class A, class B = A>
-__global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(LaArgs a0, LaArgs a1) {
+// grid (segments, heads, passes): pass A, or up to three independent passes
+// of the same shape in one launch, pass z on blockIdx.z (NP passes).
+template <int D, int NP, class A, class B = A, class C = A>
+__global__ __launch_bounds__((CfgLA<D>::NT), (CfgLA<D>::kBlocks)) void k_la(LaArgs a0, LaArgs a1, LaArgs a2) {
   int seg, bh;
   seg_head(seg, bh);
-  if constexpr (std::is_same<A, B>::value) {
+  if constexpr (NP == 1) {
     A::run(a0, seg, bh);
-  } else {
+  } else if constexpr (NP == 2) {
     if (blockIdx.z == 0)
       A::run(a0, seg, bh);
     else
       B::run(a1, seg, bh);
+  } else {
+    if (blockIdx.z == 0)
+      A::run(a0, seg, bh);
+    else if (blockIdx.z == 1)
+      B::run(a1, seg, bh);
+    else
+      C::run(a2, seg, bh);
   }
 }
 
@@ -489,14 +496,15 @@ hipError_t la_scan(float* rec, int rev, int BH, int P, int D, hipStream_t s) {
 // segment; a walk (TWO: the paired walk LA(x, y, z) + LA(x, z, y); MO: also
 // the moments w o^T of its output into rec2, with w = wp (MO = 1) or z
 // (MO = 2)) starts every segment from the moments of the others on its side.
-template <int D, class A, class B = A>
-hipError_t la_launch(const char* name, const LaArgs& a0, const LaArgs& a1, int BH, int P, hipStream_t s) {
+template <int D, int NP, class A, class B = A, class C = A>
+hipError_t la_launch(const char* name, const LaArgs& a0, const LaArgs& a1, const LaArgs& a2, int BH, int P,
+                     hipStream_t s) {
   using G = CfgLA<D>;
-  const void* kf = (const void*)k_la<D, A, B>;
+  const void* kf = (const void*)k_la<D, NP, A, B, C>;
   hipError_t e;
   if ((e = hipFuncSetAttribute(kf, hipFuncAttributeMaxDynamicSharedMemorySize, (int)G::bytes)) != hipSuccess) return e;
   prof_start(name, s);
-  HLA_LAUNCH((k_la<D, A, B>), dim3(P, BH, std::is_same<A, B>::value ? 1 : 2), dim3(G::NT), G::bytes, s, a0, a1);
+  HLA_LAUNCH((k_la<D, NP, A, B, C>), dim3(P, BH, NP), dim3(G::NT), G::bytes, s, a0, a1, a2);
   prof_stop(s);
   return hipGetLastError();
 }
@@ -541,25 +549,28 @@ hipError_t run_backward(const Bwd& b, char* ws, hipStream_t s) {
   using WalkG = LaPass<D, true, false, true, false>;                       // x, z fp32: dq (first term), dv
   using WalkU2 = LaPass<D, true, false, false, false>;                     // x fp32: dq (second term)
   using WalkK = LaPass<D, false, false, true, false, true>;          // paired dk
+  const LaArgs none{};
   // the moments k^T k (r, the second dq term) and g^T q (u; transposed for dv)
   if (P > 1)
-    HLA_TRY((la_launch<D, MomKK, MomGQ>("bwd_moments", la_args(b.k, b.k, b.k, nullptr, kk, n, cps, P, 0, 0, 0),
-                                        la_args(b.g, b.g, b.q, nullptr, gq, n, cps, P, 0, 0, 0), BH, P, s)));
+    HLA_TRY((la_launch<D, 2, MomKK, MomGQ>("bwd_moments", la_args(b.k, b.k, b.k, nullptr, kk, n, cps, P, 0, 0, 0),
+                                           la_args(b.g, b.g, b.q, nullptr, gq, n, cps, P, 0, 0, 0), none, BH, P,
+                                           s)));
   HLA_TRY(la_scan(kk, 0, BH, P, D, s));
   HLA_TRY(la_scan(gq, 1, BH, P, D, s));
   // r = LA+(q, k, k) with the v^T r moments, beside u = LA-(v, g, q) with the q^T u moments
-  HLA_TRY((la_launch<D, WalkR, WalkU>("bwd_ru", la_args(b.q, b.k, b.k, r, kk, n, cps, P, 0, 0, 0, b.v, vr),
-                                      la_args(b.v, b.g, b.q, u, gq, n, cps, P, 1, 0, 0, nullptr, qu), BH, P, s)));
+  HLA_TRY((la_launch<D, 2, WalkR, WalkU>("bwd_ru", la_args(b.q, b.k, b.k, r, kk, n, cps, P, 0, 0, 0, b.v, vr),
+                                         la_args(b.v, b.g, b.q, u, gq, n, cps, P, 1, 0, 0, nullptr, qu), none, BH,
+                                         P, s)));
   HLA_TRY(la_scan(vr, 0, BH, P, D, s));
   HLA_TRY(la_scan(qu, 1, BH, P, D, s));
-  // dq = LA+(g, v, r) + LA+(u, k, k)
-  const LaArgs none{};
-  HLA_TRY((la_launch<D, WalkG>("bwd_dq", la_args(b.g, b.v, r, b.dq, vr, n, cps, P, 0, 0, 0), none, BH, P, s)));
-  HLA_TRY((la_launch<D, WalkU2>("bwd_dq", la_args(u, b.k, b.k, b.dq, kk, n, cps, P, 0, 1, 0), none, BH, P, s)));
-  // dv = LA-(r, q, g) (moments q^T g = (g^T q)^T) beside dk = LA-(k, q, u) + LA-(k, u, q)
-  // in one paired walk (state sum q u^T + u q^T)
-  HLA_TRY((la_launch<D, WalkG, WalkK>("bwd_dvdk", la_args(r, b.q, b.g, b.dv, gq, n, cps, P, 1, 0, 1),
-                                      la_args(b.k, b.q, u, b.dk, qu, n, cps, P, 1, 0, 0), BH, P, s)));
+  // the first dq term LA+(g, v, r), beside dv = LA-(r, q, g) (moments q^T g =
+  // (g^T q)^T) and dk = LA-(k, q, u) + LA-(k, u, q) in one paired walk (state
+  // sum q u^T + u q^T); then the second dq term LA+(u, k, k), added
+  HLA_TRY((la_launch<D, 3, WalkG, WalkG, WalkK>("bwd_dq_dv_dk", la_args(b.g, b.v, r, b.dq, vr, n, cps, P, 0, 0, 0),
+                                                la_args(r, b.q, b.g, b.dv, gq, n, cps, P, 1, 0, 1),
+                                                la_args(b.k, b.q, u, b.dk, qu, n, cps, P, 1, 0, 0), BH, P, s)));
+  HLA_TRY((la_launch<D, 1, WalkU2>("bwd_dq", la_args(u, b.k, b.k, b.dq, kk, n, cps, P, 0, 1, 0), none, none, BH, P,
+                                   s)));
 #undef HLA_TRY
   return hipSuccess;
 }
