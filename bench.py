@@ -84,9 +84,13 @@ def kernel_costs(w, P=None, tile=None, first=None, per=None, two_pass=False):
                 "walk": ("hbm", out_tok * (qkv_tok + 4 * dv), out_tok * ref),
                 "walk_first": ("hbm", seg0 * (qkv_tok + 4 * dv) + summ * qkv_tok + BH * (P - 1) * F * 4,
                                seg0 * ref + summ * 2 * (2 * Ct * d + 2 * d * d + 2 * d * dv)),
-                # the brackets: S prefix, C, m and (Phi, eta) read, (Phi, eta) written
-                "bracket": ("hbm", BH * (P - 2) * (d * d + d * dv + d + 2 * (d * dv + d)) * 4,
+                # the S prefixes of segments 1 .. P-1 (the S of records 0 .. P-2 read,
+                # the prefixes written) and the brackets: C, m and (Phi, eta) read,
+                # (Phi, eta) written
+                "bracket": ("hbm", BH * (2 * (P - 1) * d * d + (P - 2) * (d * dv + d + 2 * (d * dv + d))) * 4,
                             BH * (P - 2) * 2 * (d * d * dv + d * d)),
+                # one prefix launch: the running sums of the (Phi, eta) brackets
+                "seg_prefix": ("hbm", BH * 2 * P * (d * dv + d) * 4, BH * P * (d * dv + d)),
             })
     return costs
 

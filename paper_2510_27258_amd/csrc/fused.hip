@@ -1163,9 +1163,9 @@ hipError_t launch_ws(const void* fn, dim3 grid, hipStream_t s, void** args) {
 // row written once (plan in ws_plan):
 //   1. k_walk_ws_first: segment 0's output walk, and the summary walks of
 //      segments 1 .. P-2 from a zero state (S, C, m, Phi, eta records);
-//   2. k_seg_prefix: the S prefixes;  k_ws_bracket: each record's bracket
-//      (Phi_s + S_{<s} C_s, eta_s + S_{<s} m_s) in place;  k_seg_prefix: the
-//      running sums of the brackets, the Phi, eta carries;
+//   2. k_ws_bracket: the S prefixes, summed from the records, and each
+//      record's bracket (Phi_s + S_{<s} C_s, eta_s + S_{<s} m_s) in place;
+//      k_seg_prefix: the running sums of the brackets, the Phi, eta carries;
 //   3. k_walk_ws_out over segments 1 .. P-1 from their true carries.
 // With P = 1, step 3 alone over whole heads.
 hipError_t run_ws(const Fwd& f, char* ws, hipStream_t s) {
@@ -1191,17 +1191,12 @@ hipError_t run_ws(const Fwd& f, char* ws, hipStream_t s) {
     e = launch_ws((const void*)k_walk_ws_first, dim3(P - 1, BH), s, a1);
     prof_stop(s);
     if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
-    // (no walk writes record P - 1: the sums that include it are never stored)
-    prof_start("seg_prefix", s);
-    HLA_LAUNCH(k_seg_prefix, dim3((D * D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, 0, D * D, 0, spre, P, 1.f);
+    // the S prefixes of segments 1 .. P-1 and the brackets of 1 .. P-2 (no
+    // walk writes record P - 1: the sums that include it are never stored)
+    prof_start("bracket", s);
+    HLA_LAUNCH((k_ws_bracket<D, DV>), dim3(P - 1, BH), dim3(1024), 0, s, segs, spre, P);
     prof_stop(s);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (P > 2) {
-      prof_start("bracket", s);
-      HLA_LAUNCH((k_ws_bracket<D, DV>), dim3(P - 2, BH), dim3(1024), 0, s, segs, spre, P);
-      prof_stop(s);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
     prof_start("seg_prefix", s);
     HLA_LAUNCH(k_seg_prefix, dim3((D * DV + D + 1023) / 1024, BH), dim3(256), 0, s, segs, F, (int)off_G(D, DV),
                D * DV + D, 0, carry, P, 1.f);

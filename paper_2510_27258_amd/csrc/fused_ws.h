@@ -482,18 +482,20 @@ __global__ __launch_bounds__(CfgWS::NT, 1) void k_walk_ws_out(
   walk_ws<false>(lds, q, k, v, out, den_out, si, ci, nullptr, bh, n, cb, nt, normalized, eps);
 }
 
-// The brackets of the two-pass plan (Eq. semidirect in the Phi form): for
-// segment s = 1 .. nseg-2, whose record holds its S, C, m, Phi, eta from a
-// zero start, b_s = (Phi_s + S_{<s} C_s, eta_s + S_{<s} m_s), written in
-// place of (Phi_s, eta_s); S_{<s} = spre[s].  Record 0 (the ending state of
-// segment 0's output walk) already holds b_0.  grid (nseg - 2, BH), 1024
-// threads, one workgroup per (segment, head), a head's workgroups on one
-// XCD.  S_{<s} and C_s are split into bf16 hi + lo in LDS, as every computed
-// operand of the walks, and wave w forms the 32 x 32 tile (w / 4, w % 4) of
-// S_{<s} C_s in three passes (hi hi, hi lo, lo hi) with fp32 accumulation.
+// The S prefixes and the brackets of the two-pass plan (Eq. semidirect in
+// the Phi form).  For segment s = 1 .. nseg-1: S_{<s}, the sum of the S
+// slots of records 0 .. s-1 (record 0 holds the ending state of segment 0's
+// output walk, records 1 .. nseg-2 the summaries), into spre[s] for the
+// output walks.  For s <= nseg-2, whose record holds its S, C, m, Phi, eta
+// from a zero start, also b_s = (Phi_s + S_{<s} C_s, eta_s + S_{<s} m_s),
+// written in place of (Phi_s, eta_s); record 0 already holds b_0.
+// grid (nseg - 1, BH), 1024 threads, one workgroup per (segment, head), a
+// head's workgroups on one XCD.  S_{<s} and C_s are split into bf16 hi + lo
+// in LDS, as every computed operand of the walks, and wave w forms the
+// 32 x 32 tile (w / 4, w % 4) of S_{<s} C_s in three passes (hi hi, hi lo,
+// lo hi) with fp32 accumulation.
 template <int D, int DV>
-__global__ __launch_bounds__(1024) void k_ws_bracket(float* __restrict__ rec, const float* __restrict__ spre,
-                                                     int nseg) {
+__global__ __launch_bounds__(1024) void k_ws_bracket(float* __restrict__ rec, float* __restrict__ spre, int nseg) {
   constexpr int ldS = D + kPad, ldC = DV + 16, NT = 1024;   // ldC: C is read through the transpose unit
   static_assert(D == 128 && DV == 128, "16 waves of 32 x 32 output tiles");
   __shared__ __align__(16) uint16_t Sh[D * ldS], Sl[D * ldS], Ch[D * ldC], Cl[D * ldC];
@@ -503,12 +505,37 @@ __global__ __launch_bounds__(1024) void k_ws_bracket(float* __restrict__ rec, co
   s += 1;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 31, lg = l >> 5;
   const int r0 = 32 * (w >> 2), c0 = 32 * (w & 3);
-  float* r = rec + ((size_t)bh * (nseg + 1) + s) * state_floats(D, DV);
-  const float* sp = spre + ((size_t)bh * nseg + s) * D * D;
+  const size_t F = state_floats(D, DV);
+  float* r = rec + ((size_t)bh * (nseg + 1) + s) * F;
+  constexpr int NS4 = D * D / 4 / NT;
+  // S_{<s}: the earlier records' S slots, two records' loads in flight at a time
+  float4 sx[NS4];
 #pragma unroll
-  for (int i = 0; i < D * D / 4 / NT; ++i) {
+  for (int i = 0; i < NS4; ++i) sx[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float* r0s = rec + (size_t)bh * (nseg + 1) * F;
+  for (int sp = 0; sp < s; sp += 2) {
+    float4 u[2][NS4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < NS4; ++i)
+        u[j][i] = sp + j < s ? reinterpret_cast<const float4*>(r0s + (size_t)(sp + j) * F)[tid + NT * i]
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < NS4; ++i) {
+        sx[i].x += u[j][i].x; sx[i].y += u[j][i].y; sx[i].z += u[j][i].z; sx[i].w += u[j][i].w;
+      }
+  }
+  float4* spw = reinterpret_cast<float4*>(spre + ((size_t)bh * nseg + s) * D * D);
+#pragma unroll
+  for (int i = 0; i < NS4; ++i) spw[tid + NT * i] = sx[i];
+  if (s == nseg - 1) return;   // the last segment has no summary, so no bracket
+#pragma unroll
+  for (int i = 0; i < NS4; ++i) {
     const int e = tid + NT * i, row = e / (D / 4), c4 = e % (D / 4);
-    const float4 x = *reinterpret_cast<const float4*>(sp + 4 * (size_t)e);
+    const float4 x = sx[i];
     const float4 y = *reinterpret_cast<const float4*>(r + off_C(D, DV) + (size_t)row * DV + 4 * c4);
     uint32_t h0, h1, l0, l1;
     split2(x.x, x.y, h0, l0);
