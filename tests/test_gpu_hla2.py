@@ -367,6 +367,37 @@ def test_scan_square_states(d, with_init):
                 acc = O.combine(acc, split(x[:, :, c]))
 
 
+@pytest.mark.parametrize("d,B,H,M", [(128, 2, 32, 128), (64, 4, 16, 64)])
+def test_scan_full_size_sampled_heads(d, B, H, M):
+    """The scan at the benchmark's full sizes and launch configuration (8192
+    records at d = 128 for B2 H32, 4096 at d = 64 for B4 H16) over seeded
+    random records: the prefixes and the total of three heads against a
+    sequential (+) in fp64."""
+    F = 3 * d * d + 2 * d
+    rng = np.random.default_rng(100 + d)
+    x = rng.standard_normal((B, H, M, F), dtype=np.float32)
+    _say(f"case scan full size d={d} B={B} H={H} M={M}")
+    prefix, total = hla.scan(torch.from_numpy(x).cuda(), d, d)
+    heads = [0, (B * H) // 2 + 1, B * H - 1]
+    idx = torch.tensor(heads, device="cuda")
+    got_pre = prefix.reshape(B * H, M, F).index_select(0, idx).cpu().numpy()
+    got_tot = total.reshape(B * H, F).index_select(0, idx).cpu().numpy()
+    del prefix, total
+    parts = [(0, d * d, (d, d)), (d * d, d * d, (d, d)), (2 * d * d, d, (d,)), (2 * d * d + d, d * d, (d, d)),
+             (3 * d * d + d, d, (d,))]
+    split = lambda r: tuple(r[..., o:o + c].reshape(r.shape[:-1] + sh).astype(np.float64) for o, c, sh in parts)
+    for j, hd in enumerate(heads):
+        b, h = divmod(hd, H)
+        acc = tuple(np.zeros(sh) for _, _, sh in parts)
+        for c in range(M + 1):
+            got = split(got_pre[j, c]) if c < M else split(got_tot[j])
+            for name, gv, ev in zip("SCmGh", got, acc):
+                err = np.abs(gv - ev).max() / max(np.abs(ev).max(), 1.0)
+                assert err <= 1e-5, f"head {hd} segment {c} {name}: {err:.3e}"
+            if c < M:
+                acc = O.combine(acc, split(x[b, h, c]))
+
+
 # ----------------------------------------------------------------- prefill and decode
 def _state_to_np(state, d, dv):
     return tuple(x.cpu().numpy().astype(np.float64) for x in hla.split_state(state.export(), d, dv))
