@@ -1115,7 +1115,7 @@ bool legacy_pipeline() {
 
 // Per-tile time of the summary walk over that of the output walk (both at
 // one workgroup per CU, d = dv = 128: about 3.9 and 6.6 us per tile).
-constexpr double kWsSummaryRatio = 0.6;
+constexpr double kWsSummaryRatio = 0.65;
 
 // Segments per head up to which the row-split walk (no initial state) sums
 // its S prefix from the moments itself instead of reading it from a prefix

@@ -70,12 +70,29 @@ __device__ __forceinline__ void ws_range(int seg, int c0, int cps, int M, int& c
   nt = min(M, seg == 0 ? c0 : c_begin + cps) - c_begin;
 }
 
+// Instruction order for one block of LDS-fed products: PRE LDS reads first,
+// then the NM MFMAs with the remaining NR - PRE reads spread evenly between
+// them, so each wave keeps several fragment reads in flight instead of
+// waiting on the read that feeds the very next MFMA (mask 0x100: LDS reads,
+// 0x008: MFMAs).  It only orders; data dependences still hold.
+template <int PRE, int NM, int NR, int I = 0>
+__device__ __forceinline__ void read_ahead() {
+  if constexpr (I == 0) __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);
+  if constexpr (I < NM) {
+    constexpr int c = ((I + 1) * (NR - PRE)) / NM - (I * (NR - PRE)) / NM;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (c > 0) __builtin_amdgcn_sched_group_barrier(0x100, c, 0);
+    read_ahead<PRE, NM, NR, I + 1>();
+  }
+}
+
 // One segment's walk over tiles [c_begin, c_begin + nt) of head bh.
 // s_in: S0 at the start (D x D, row-major; null: zero); c_in: Phi0 (D x DV)
 // then eta0 (D) at the start (null: zero; unused by SUMMARY); rec: this
 // segment's record (null: none), which receives the ending S0, Phi0 and eta0
 // in its S, G and h slots, and with SUMMARY also the segment's C = Q^T V and
-// m = Q^T 1 in its C and m slots.
+// m = Q^T 1 in its C and m slots.  Each block of products is ordered with
+// read_ahead.
 template <bool SUMMARY>
 __device__ __forceinline__ void walk_ws(uint16_t* lds,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
@@ -225,6 +242,7 @@ __device__ __forceinline__ void walk_ws(uint16_t* lds,
             acc[rt] = mfma(aQ, bl_, acc[rt]);
           }
         }
+        read_ahead<6, 32, 16>();     // Q S0: 32 MFMAs, 16 reads
       }
       prefetch(t);
       lds_barrier();
@@ -245,6 +263,7 @@ __device__ __forceinline__ void walk_ws(uint16_t* lds,
         for (int s = 0; s < C / 16; ++s)
 #pragma unroll
           for (int i = 0; i < 4; ++i) st[i] = mfma(frag_tr<true>(Ks, G::ldK, i * 32, s * 16, ln), bK[s], st[i]);
+        read_ahead<16, 28, 52>();    // W K, S0 advance: 28 MFMAs, 52 reads
       }
       lds_barrier();
       // phase 3: R^T of tile t + 1 for the value side, and its column sums
@@ -328,6 +347,7 @@ __device__ __forceinline__ void walk_ws(uint16_t* lds,
             acc[rt] = mfma(aQ, bl_, acc[rt]);
           }
         }
+        read_ahead<6, 32, 16>();     // Q Phi0
         if (normalized) {            // four lanes per token, 32 dimensions each
           const int tok = u >> 2, p0 = (u & 3) * 32;
           const uint16_t* row = Qy + tok * G::ldQ + p0;
@@ -368,6 +388,8 @@ __device__ __forceinline__ void walk_ws(uint16_t* lds,
             st[i] = mfma(frag<true>(Rl, G::ldR, i * 32, s * 16, ln), bV, st[i]);
           }
         }
+        if constexpr (SUMMARY) read_ahead<12, 32, 40>();   // Phi0 advance: 32 MFMAs, 40 reads
+        else read_ahead<12, 44, 52>();                    // T V, Phi0 advance: 44 MFMAs, 52 reads
         if (u < D) eta[u] += inc[u];
         if (!SUMMARY && normalized && u < C) {
           const float den = denp[u] + denp[C + u] + qeta[u];

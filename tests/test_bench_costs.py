@@ -13,14 +13,14 @@ def test_dense_chunk_form_flops_per_token():
 
 
 def test_headline_output_walk_costs():
-    # B2 H32 n16384, d = dv = 128, five segments per head with segment 0 of 34
+    # B2 H32 n16384, d = dv = 128, five segments per head with segment 0 of 36
     # 64-token tiles: the output walk covers every token but segment 0's,
     # reading q, k, v in bf16 (3 x 256 B) and writing an fp32 row (512 B),
     # counted densely at the 64-token tile it walks
     w = I.WORKLOADS["hla2-masked-normalized-bf16-B2H32-n16384-d128-C128"]
-    c = bench.kernel_costs(w, 5, 64, 34, 56, two_pass=True)
-    tok = 2 * 32 * 16384 - 2 * 32 * 34 * 64
-    assert tok == 909312
+    c = bench.kernel_costs(w, 5, 64, 36, 56, two_pass=True)
+    tok = 2 * 32 * 16384 - 2 * 32 * 36 * 64
+    assert tok == 901120
     assert c["walk"] == ("hbm", tok * 1280, tok * 270336)
     assert bench.reference_flops_per_token(64, 128, 128) == 270336
 

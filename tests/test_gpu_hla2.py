@@ -251,11 +251,12 @@ def test_fused_long_single_head():
 
 def test_fused_long_single_head_d128():
     """One d = 128 head of 65 536 tokens: 1024 tiles cut into 257 segments of
-    the two-pass plan (segment 0 of 2 tiles, 256 of 4), so the longest
-    bracket and carry chains of that plan; every row against the oracle.
+    the two-pass plan (segment 0 of 3 tiles, 255 of 4 and the last of 1), so
+    the longest bracket and carry chains of that plan; every row against the
+    oracle.
     (Unnormalised: at this length too few rows' denominators stand clear of
     their cancellation scale for the ratio test.)"""
-    assert capi.hla2_fused_plan(1, 1, 65536, 128, 128, 128, tiles=True) == (257, 64, 2, 4)
+    assert capi.hla2_fused_plan(1, 1, 65536, 128, 128, 128, tiles=True) == (257, 64, 3, 4)
     assert _check_forward(1, 1, 65536, 128, 128, 128, "unit", 1, False, capi.HLA_ALGO_FUSED, seed=23)
 
 
