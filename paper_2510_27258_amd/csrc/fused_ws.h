@@ -222,6 +222,7 @@ __device__ __forceinline__ void walk_ws(uint16_t* lds,
 #pragma unroll
         for (int s = 0; s < D / 16; ++s)
           a = mfma(frag<true>(Ks, G::ldK, it * 32, s * 16, ln), frag<true>(Qx, G::ldQ, jt * 32, s * 16, ln), a);
+        read_ahead<6, 8, 16>();      // W: 8 MFMAs, 16 reads
         if (it == jt)
 #pragma unroll
           for (int e = 0; e < 16; ++e)   // keep key <= query
@@ -323,6 +324,7 @@ __device__ __forceinline__ void walk_ws(uint16_t* lds,
             a = mfma(frag_tr<true>(Rh, G::ldR, it * 32, s * 16, ln), b, a);
             a = mfma(frag_tr<true>(Rl, G::ldR, it * 32, s * 16, ln), b, a);
           }
+          read_ahead<10, 16, 40>();    // T: 16 MFMAs, 40 reads
           if (it == jt)
 #pragma unroll
             for (int e = 0; e < 16; ++e)
